@@ -1,0 +1,233 @@
+"""fp64 CPU oracle for clustered / improved-clustered attention.
+
+TEST INFRASTRUCTURE ONLY.  Only the test-suite, ``__graft_entry__.smoke()`` and
+the CPU-baseline leg of ``bench.py`` may import this package.  The GPU library
+never calls it and shares no code with it.
+
+The arithmetic lives in ``oracle.c`` (plain C, fp64); this module compiles it
+with gcc when needed and wraps it with numpy through ctypes.  Every input is
+widened to float64 exactly (fp32 and bf16 values are representable in fp64).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_HDR = os.path.join(_HERE, "oracle.h")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile liboracle.so with gcc (fp64, OpenMP over (batch, head) units)."""
+    if not force and os.path.exists(_LIB) and os.path.getmtime(_LIB) >= max(
+        os.path.getmtime(_SRC), os.path.getmtime(_HDR)
+    ):
+        return _LIB
+    tmp = _LIB + ".tmp%d" % os.getpid()
+    cmd = ["gcc", "-O2", "-std=c11", "-fno-fast-math", "-fopenmp", "-fPIC",
+           "-shared", _SRC, "-o", tmp, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    build(force=False)
+    lib = ctypes.CDLL(_LIB)
+    dp = ctypes.POINTER(ctypes.c_double)
+    u64p = ctypes.POINTER(ctypes.c_uint64)
+    i32p = ctypes.POINTER(ctypes.c_int32)
+    i64p = ctypes.POINTER(ctypes.c_int64)
+    i64, i32 = ctypes.c_int64, ctypes.c_int
+    lib.orc_full_attention.argtypes = [dp, dp, dp, i64, i32, dp]
+    lib.orc_hash.argtypes = [dp, i64, i32, dp, i32, u64p]
+    lib.orc_projections.argtypes = [dp, i64, i32, dp, i32, dp]
+    lib.orc_kmeans.argtypes = [u64p, i64, i32, i32, i32p, u64p, i64p]
+    lib.orc_centroids.argtypes = [dp, i64, i32, i32p, i32, dp, i64p]
+    lib.orc_centroid_row.argtypes = [dp, dp, i64, i32, dp, dp]
+    lib.orc_topk.argtypes = [dp, i64, i32, i32p]
+    lib.orc_topk.restype = i32
+    lib.orc_clustered_from_assign.argtypes = [dp, dp, dp, i64, i32, i32p, i32, dp, dp, dp]
+    lib.orc_iclustered_from_assign.argtypes = [dp, dp, dp, i64, i32, i32p, i32, i32,
+                                               i32p, dp, i32p, dp, dp]
+    lib.orc_dense_rows.argtypes = [dp, dp, i64, i32, i32p, i32, i32, dp, dp]
+    lib.orc_forward.argtypes = [dp, dp, dp, i32p, i32, i32, i64, i32, dp, i32, i32,
+                                i32, i32, i32, dp, u64p, i32p, i32p, dp, i32p, dp, dp]
+    lib.orc_forward.restype = i32
+    _lib = lib
+    return lib
+
+
+def _f64(x):
+    return np.ascontiguousarray(np.asarray(x, dtype=np.float64))
+
+
+def _ptr(a, ctype):
+    if a is None:
+        return None
+    return a.ctypes.data_as(ctypes.POINTER(ctype))
+
+
+def full_attention(q, k, v):
+    """Exact softmax attention of one (batch, head): q, k, v are [n, d]."""
+    q, k, v = _f64(q), _f64(k), _f64(v)
+    n, d = q.shape
+    out = np.zeros((n, d), np.float64)
+    _load().orc_full_attention(_ptr(q, ctypes.c_double), _ptr(k, ctypes.c_double),
+                               _ptr(v, ctypes.c_double), n, d, _ptr(out, ctypes.c_double))
+    return out
+
+
+def hash_codes(q, planes):
+    """Sign-of-random-projection codes of [n, d] queries with [n_bits, d] planes."""
+    q, planes = _f64(q), _f64(planes)
+    n, d = q.shape
+    codes = np.zeros(n, np.uint64)
+    _load().orc_hash(_ptr(q, ctypes.c_double), n, d, _ptr(planes, ctypes.c_double),
+                     planes.shape[0], _ptr(codes, ctypes.c_uint64))
+    return codes
+
+
+def projections(q, planes):
+    q, planes = _f64(q), _f64(planes)
+    n, d = q.shape
+    out = np.zeros((n, planes.shape[0]), np.float64)
+    _load().orc_projections(_ptr(q, ctypes.c_double), n, d, _ptr(planes, ctypes.c_double),
+                            planes.shape[0], _ptr(out, ctypes.c_double))
+    return out
+
+
+def kmeans(codes, C, L):
+    """Hamming K-means on uint64 codes.  Returns (assign, centroids, objective)."""
+    codes = np.ascontiguousarray(codes, dtype=np.uint64)
+    n = codes.shape[0]
+    assign = np.full(n, -1, np.int32)
+    cent = np.zeros(C, np.uint64)
+    obj = np.zeros(2 * L, np.int64)
+    _load().orc_kmeans(_ptr(codes, ctypes.c_uint64), n, C, L, _ptr(assign, ctypes.c_int32),
+                       _ptr(cent, ctypes.c_uint64), _ptr(obj, ctypes.c_int64))
+    return assign, cent, obj
+
+
+def centroids(q, assign, C):
+    q = _f64(q)
+    assign = np.ascontiguousarray(assign, dtype=np.int32)
+    n, d = q.shape
+    qc = np.zeros((C, d), np.float64)
+    sizes = np.zeros(C, np.int64)
+    _load().orc_centroids(_ptr(q, ctypes.c_double), n, d, _ptr(assign, ctypes.c_int32), C,
+                          _ptr(qc, ctypes.c_double), _ptr(sizes, ctypes.c_int64))
+    return qc, sizes
+
+
+def centroid_row(qcj, k):
+    qcj, k = _f64(qcj), _f64(k)
+    n, d = k.shape
+    s = np.zeros(n, np.float64)
+    a = np.zeros(n, np.float64)
+    _load().orc_centroid_row(_ptr(qcj, ctypes.c_double), _ptr(k, ctypes.c_double), n, d,
+                             _ptr(s, ctypes.c_double), _ptr(a, ctypes.c_double))
+    return s, a
+
+
+def topk(s, k):
+    s = _f64(s)
+    n = s.shape[0]
+    top = np.full(max(min(k, n), 1), -1, np.int32)
+    ke = _load().orc_topk(_ptr(s, ctypes.c_double), n, k, _ptr(top, ctypes.c_int32))
+    return top[:ke]
+
+
+def clustered_from_assign(q, k, v, assign, C):
+    """Clustered attention of one (batch, head) for a given partition."""
+    q, k, v = _f64(q), _f64(k), _f64(v)
+    assign = np.ascontiguousarray(assign, dtype=np.int32)
+    n, d = q.shape
+    out = np.zeros((n, d), np.float64)
+    qc = np.zeros((C, d), np.float64)
+    vc = np.zeros((C, d), np.float64)
+    _load().orc_clustered_from_assign(
+        _ptr(q, ctypes.c_double), _ptr(k, ctypes.c_double), _ptr(v, ctypes.c_double), n, d,
+        _ptr(assign, ctypes.c_int32), C, _ptr(out, ctypes.c_double),
+        _ptr(qc, ctypes.c_double), _ptr(vc, ctypes.c_double))
+    return out, qc, vc
+
+
+def iclustered_from_assign(q, k, v, assign, C, topk_, topk_in=None):
+    """Improved clustered attention of one (batch, head) for a given partition.
+
+    Returns (out, T, mass, Vb) with T as [C, topk] ascending, -1 padded."""
+    q, k, v = _f64(q), _f64(k), _f64(v)
+    assign = np.ascontiguousarray(assign, dtype=np.int32)
+    n, d = q.shape
+    out = np.zeros((n, d), np.float64)
+    tk = np.full((C, topk_), -1, np.int32)
+    mass = np.zeros(C, np.float64)
+    vb = np.zeros((C, d), np.float64)
+    tin = None if topk_in is None else np.ascontiguousarray(topk_in, dtype=np.int32)
+    _load().orc_iclustered_from_assign(
+        _ptr(q, ctypes.c_double), _ptr(k, ctypes.c_double), _ptr(v, ctypes.c_double), n, d,
+        _ptr(assign, ctypes.c_int32), C, topk_, _ptr(tin, ctypes.c_int32),
+        _ptr(out, ctypes.c_double), _ptr(tk, ctypes.c_int32), _ptr(mass, ctypes.c_double),
+        _ptr(vb, ctypes.c_double))
+    return out, tk, mass, vb
+
+
+def dense_rows(q, k, assign, C, topk_):
+    """Dense [n, n] matrices (A^c row of each query's cluster, A^t of Eq. 11)."""
+    q, k = _f64(q), _f64(k)
+    assign = np.ascontiguousarray(assign, dtype=np.int32)
+    n, d = q.shape
+    ac = np.zeros((n, n), np.float64)
+    at = np.zeros((n, n), np.float64)
+    _load().orc_dense_rows(_ptr(q, ctypes.c_double), _ptr(k, ctypes.c_double), n, d,
+                           _ptr(assign, ctypes.c_int32), C, topk_,
+                           _ptr(ac, ctypes.c_double), _ptr(at, ctypes.c_double))
+    return ac, at
+
+
+def forward(q, k, v, lengths, planes, C, n_bits, L, topk_=0, num_threads=None,
+            exports=True):
+    """Whole forward pass over [B, H, N, d] inputs.
+
+    topk_ <= 0 runs clustered attention, topk_ >= 1 improved clustered attention.
+    Returns a dict with 'out' and, if exports, the intermediate results."""
+    q, k, v = _f64(q), _f64(k), _f64(v)
+    B, H, N, d = q.shape
+    planes = _f64(planes)
+    assert planes.shape == (H, n_bits, d)
+    lens = None if lengths is None else np.ascontiguousarray(lengths, dtype=np.int32)
+    out = np.zeros((B, H, N, d), np.float64)
+    res = {"out": out}
+    if exports:
+        res["codes"] = np.zeros((B, H, N), np.uint64)
+        res["assign"] = np.zeros((B, H, N), np.int32)
+        res["sizes"] = np.zeros((B, H, C), np.int32)
+        res["qc"] = np.zeros((B, H, C, d), np.float64)
+        res["topk"] = np.zeros((B, H, C, max(topk_, 1)), np.int32)
+        res["mass"] = np.zeros((B, H, C), np.float64)
+        res["vcb"] = np.zeros((B, H, C, d), np.float64)
+    g = res.get
+    if num_threads is None:
+        num_threads = os.cpu_count() or 1
+    rc = _load().orc_forward(
+        _ptr(q, ctypes.c_double), _ptr(k, ctypes.c_double), _ptr(v, ctypes.c_double),
+        _ptr(lens, ctypes.c_int32), B, H, N, d, _ptr(planes, ctypes.c_double), n_bits, C, L,
+        topk_, int(num_threads), _ptr(out, ctypes.c_double),
+        _ptr(g("codes"), ctypes.c_uint64), _ptr(g("assign"), ctypes.c_int32),
+        _ptr(g("sizes"), ctypes.c_int32), _ptr(g("qc"), ctypes.c_double),
+        _ptr(g("topk"), ctypes.c_int32) if topk_ > 0 else None,
+        _ptr(g("mass"), ctypes.c_double), _ptr(g("vcb"), ctypes.c_double))
+    if rc != 0:
+        raise ValueError("oracle rejected the arguments")
+    return res

@@ -1,0 +1,38 @@
+/* Declarations of the fp64 CPU oracle (test infrastructure only; see oracle.c). */
+#ifndef CLUSTERED_ATTN_ORACLE_H
+#define CLUSTERED_ATTN_ORACLE_H
+#include <stdint.h>
+
+void orc_full_attention(const double* q, const double* k, const double* v,
+                        int64_t n, int d, double* out);
+void orc_hash(const double* q, int64_t n, int d, const double* planes,
+              int n_bits, uint64_t* codes);
+void orc_projections(const double* q, int64_t n, int d, const double* planes,
+                     int n_bits, double* proj);
+void orc_kmeans(const uint64_t* h, int64_t n, int C, int L, int32_t* assign,
+                uint64_t* centroids, int64_t* objective);
+void orc_centroids(const double* q, int64_t n, int d, const int32_t* assign,
+                   int C, double* qc, int64_t* sizes);
+void orc_centroid_row(const double* qcj, const double* k, int64_t n, int d,
+                      double* s, double* a);
+int orc_topk(const double* s, int64_t n, int k, int32_t* top);
+void orc_clustered_from_assign(const double* q, const double* k,
+                               const double* v, int64_t n, int d,
+                               const int32_t* assign, int C, double* out,
+                               double* qc_out, double* vc_out);
+void orc_iclustered_from_assign(const double* q, const double* k,
+                                const double* v, int64_t n, int d,
+                                const int32_t* assign, int C, int topk,
+                                const int32_t* topk_in, double* out,
+                                int32_t* topk_out, double* mass_out,
+                                double* vb_out);
+void orc_dense_rows(const double* q, const double* k, int64_t n, int d,
+                    const int32_t* assign, int C, int topk, double* ac,
+                    double* at);
+int orc_forward(const double* q, const double* k, const double* v,
+                const int32_t* lengths, int batch, int heads, int64_t N, int d,
+                const double* planes, int n_bits, int C, int L, int topk,
+                int num_threads, double* out, uint64_t* codes_out,
+                int32_t* assign_out, int32_t* sizes_out, double* qc_out,
+                int32_t* topk_out, double* mass_out, double* vcb_out);
+#endif
