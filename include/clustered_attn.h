@@ -1,0 +1,166 @@
+/*
+ * clustered_attn.h -- C ABI of the gfx950 (MI355X) library for the forward
+ * pass of clustered and improved-clustered attention
+ * (Vyas, Katharopoulos, Fleuret, "Fast Transformers with Clustered Attention").
+ *
+ * Conventions shared by every entry point
+ * ----------------------------------------
+ * - q, k, v and out are DEVICE pointers to contiguous row-major tensors of
+ *   shape [batch][heads][n][d] with element type `dtype` (CA_F32 or CA_BF16,
+ *   the same for all four).  A (batch, head) pair is a "unit"; units are
+ *   independent (Section 3.2: each head clusters its own queries).
+ * - lengths is NULL (every row valid) or a DEVICE pointer to int32[batch]:
+ *   only rows 0..lengths[b]-1 of sample b are queries/keys.  Values are
+ *   clamped to [0, n] on the device.  Keys past the length get no attention,
+ *   queries past it are not hashed or clustered, and their output rows are
+ *   written as 0.
+ * - planes is a DEVICE pointer to fp32[heads][n_bits][d]: the random
+ *   hyperplanes of the sign-random-projection hash (Section 3.2.2), drawn by
+ *   the caller (the library draws no random numbers).  Any fp32 values work;
+ *   the projections are evaluated in fp64, where each product is exact.
+ * - C = n_clusters, B = n_bits, L = lloyd_iters, k = topk are the method's
+ *   hyper-parameters (Sections 3.2.2 and 3.3).  Per unit the library uses
+ *   C_eff = min(C, length) clusters and k_eff = min(k, length) keys.
+ * - workspace is a DEVICE buffer of at least ca_workspace_bytes(...) bytes,
+ *   owned by the caller and 256-byte aligned; its contents on entry do not
+ *   matter and on exit are unspecified.  The library allocates no device
+ *   memory in a forward call.
+ * - stream is a hipStream_t (NULL = the null stream).  All work is enqueued
+ *   on it and the call returns without synchronising.  Arguments are
+ *   validated on the host before anything is enqueued: on an error nothing
+ *   is launched.  A fault inside a kernel surfaces at the caller's next
+ *   synchronisation.
+ * - Results are deterministic: identical inputs give bitwise identical
+ *   outputs (no floating-point atomics are used).
+ * - Return value: CA_OK, or a negative CA_ERR_* code; ca_last_error() then
+ *   returns a message for the calling thread.  No C++ exception crosses this
+ *   interface.
+ *
+ * Supported sizes: d in {32, 64}; 1 <= n_bits <= 63; 1 <= C <= 256;
+ * 1 <= L <= 1000; 1 <= k <= 128; 1 <= n <= 1048576; 1 <= batch*heads <= 65535
+ * and batch*heads*n < 2^31.
+ */
+#ifndef CLUSTERED_ATTN_H
+#define CLUSTERED_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define CA_OK 0
+#define CA_ERR_INVALID_ARG (-1) /* null required pointer, non-positive size, bad enum */
+#define CA_ERR_UNSUPPORTED (-2) /* size outside the supported ranges above          */
+#define CA_ERR_WORKSPACE (-3)   /* workspace NULL or smaller than required          */
+#define CA_ERR_HIP (-4)         /* a HIP runtime call failed                        */
+
+#define CA_F32 0
+#define CA_BF16 1
+
+/*
+ * Optional stage inputs and outputs (all DEVICE pointers, each may be NULL).
+ * An "_in" pointer replaces the stage that would compute it, which is how the
+ * stages are tested one at a time; an "_out" pointer receives a copy of an
+ * intermediate result.  Shapes use U = batch*heads and the unit order of q.
+ *
+ *   codes_in    uint64[U][n]  hash codes; skips hashing.  Bits at positions
+ *                             >= n_bits are ignored.
+ *   assign_in   int32[U][n]   cluster of each valid query, in
+ *                             [0, C_eff); skips hashing and K-means.
+ *   topk_in     int32[U][C][k] top-k key set of each cluster, ascending and
+ *                             -1 padded, each entry < length; skips the
+ *                             top-k selection (improved variant only).
+ *   codes_out   uint64[U][n]  hash codes (Section 3.2.2); 0 on padded rows.
+ *   assign_out  int32[U][n]   final cluster of each query (the assignment of
+ *                             the L-th Lloyd round); -1 on padded rows.
+ *   sizes_out   int32[U][C]   members per cluster.
+ *   centroids_out float[U][C][d] query centroids Q^c (Eq. 3); 0 when empty.
+ *   topk_out    int32[U][C][k] top-k set T_j (Section 3.3), ascending, -1
+ *                             padded and all -1 for empty clusters.
+ *   mass_out    float[U][C]   clustered attention mass on T_j (Section 3.3).
+ *   values_out  float[U][C][d] V^c = A^c V (Eq. 5) for the clustered variant;
+ *                             for the improved variant the part of A^c V
+ *                             over the keys outside T_j (supplementary
+ *                             decomposition of the improved values).
+ */
+typedef struct ca_aux {
+  const uint64_t* codes_in;
+  const int32_t* assign_in;
+  const int32_t* topk_in;
+  uint64_t* codes_out;
+  int32_t* assign_out;
+  int32_t* sizes_out;
+  float* centroids_out;
+  int32_t* topk_out;
+  float* mass_out;
+  float* values_out;
+} ca_aux;
+
+/*
+ * Bytes of workspace that clustered_attention_fwd (topk = 0) or
+ * iclustered_attention_fwd (topk >= 1) needs for these sizes.  Returns 0 if
+ * the sizes are invalid or unsupported.
+ */
+size_t ca_workspace_bytes(int batch, int heads, int n, int d, int dtype,
+                          int n_clusters, int n_bits, int topk);
+
+/*
+ * Clustered attention (Section 3.2, Eqs. 3-6), one call for all units:
+ *   1. hash each valid query to an n_bits code by the signs of its
+ *      projections on the planes (Section 3.2.2);
+ *   2. run L rounds of K-means in Hamming space on the codes (assign to the
+ *      nearest binary centroid, ties to the smaller index; replace each
+ *      non-empty centroid by the per-bit majority of its members, ties to 0;
+ *      initial centroids: the codes of queries floor(j*length/C_eff));
+ *   3. Q^c_j = mean of the member queries (Eq. 3);
+ *   4. A^c = softmax(Q^c K^T / sqrt(d)) over the valid keys (Eq. 4),
+ *      V^c = A^c V (Eq. 5);
+ *   5. out_i = V^c of the cluster of query i (Eq. 6).
+ */
+int clustered_attention_fwd(const void* q, const void* k, const void* v,
+                            const int32_t* lengths, const float* planes,
+                            int batch, int heads, int n, int d, int dtype,
+                            int n_clusters, int n_bits, int lloyd_iters,
+                            void* out, void* workspace, size_t workspace_bytes,
+                            const ca_aux* aux, void* stream);
+
+/*
+ * Improved clustered attention (Section 3.3, Eq. 11), steps 1-4 as above and
+ * then, per cluster j:
+ *   5. T_j = the k_eff keys with the largest centroid logit (ties to the
+ *      smaller key index), m_j = sum of A^c_jl over l in T_j;
+ *   6. for each member query i:
+ *        out_i = m_j * sum_{l in T_j} softmax_{T_j}(Q_i K_l / sqrt(d)) V_l
+ *              + sum_{l not in T_j} A^c_jl V_l
+ *      (the decomposition of A^t V given in the supplementary material).
+ */
+int iclustered_attention_fwd(const void* q, const void* k, const void* v,
+                             const int32_t* lengths, const float* planes,
+                             int batch, int heads, int n, int d, int dtype,
+                             int n_clusters, int n_bits, int lloyd_iters,
+                             int topk, void* out, void* workspace,
+                             size_t workspace_bytes, const ca_aux* aux,
+                             void* stream);
+
+/* Message describing the last non-zero status returned on this thread. */
+const char* ca_last_error(void);
+
+/* Library version, major*10000 + minor*100 + patch. */
+int ca_version(void);
+
+/*
+ * Chooses the K-means driver for later calls in this process: 0 automatic
+ * (default), 1 one workgroup per unit (used only when n <= 4096), 2 one
+ * kernel pair per Lloyd round.  Both give identical results; the switch
+ * exists so that tests cover both and benchmarks can compare them.
+ * Returns CA_OK or CA_ERR_INVALID_ARG.
+ */
+int ca_set_kmeans_path(int path);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CLUSTERED_ATTN_H */

@@ -1,0 +1,208 @@
+"""Clustered and improved-clustered attention forward pass on MI355X (gfx950).
+
+A thin ctypes binding over the C ABI declared in ``include/clustered_attn.h``
+(``libclustered_attn.so`` in this directory).  It only marshals arguments:
+torch tensors supply device memory and the current HIP stream; every step of
+the method runs in the library's HIP kernels.  There is no CPU fallback: if
+the library is missing or no GPU is present, the calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+__all__ = [
+    "CA_OK", "CA_ERR_INVALID_ARG", "CA_ERR_UNSUPPORTED", "CA_ERR_WORKSPACE", "CA_ERR_HIP",
+    "CA_F32", "CA_BF16", "Aux", "ClusteredAttnError", "library", "lib_path",
+    "workspace_bytes", "clustered_attention_fwd", "iclustered_attention_fwd",
+    "clustered_attention", "iclustered_attention", "set_kmeans_path", "EXPORTED_SYMBOLS",
+]
+
+CA_OK = 0
+CA_ERR_INVALID_ARG = -1
+CA_ERR_UNSUPPORTED = -2
+CA_ERR_WORKSPACE = -3
+CA_ERR_HIP = -4
+CA_F32 = 0
+CA_BF16 = 1
+
+EXPORTED_SYMBOLS = ("ca_workspace_bytes", "clustered_attention_fwd", "iclustered_attention_fwd",
+                    "ca_last_error", "ca_version", "ca_set_kmeans_path")
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+lib_path = os.path.join(_HERE, "libclustered_attn.so")
+_lib = None
+
+
+class ClusteredAttnError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__("clustered_attn error %d: %s" % (code, msg))
+        self.code = code
+
+
+class Aux(ctypes.Structure):
+    """Mirror of ``ca_aux`` (all device pointers, 0 = unused)."""
+    _fields_ = [(name, ctypes.c_void_p) for name in (
+        "codes_in", "assign_in", "topk_in", "codes_out", "assign_out", "sizes_out",
+        "centroids_out", "topk_out", "mass_out", "values_out")]
+
+
+def library():
+    """Loads the HIP library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(lib_path):
+        raise RuntimeError("libclustered_attn.so is not built; run "
+                           "`python -c 'import __graft_entry__ as g; g.build()'`")
+    lib = ctypes.CDLL(lib_path)
+    vp, i32, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
+    lib.ca_workspace_bytes.argtypes = [i32] * 8
+    lib.ca_workspace_bytes.restype = sz
+    common = [vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, i32]
+    lib.clustered_attention_fwd.argtypes = common + [vp, vp, sz, ctypes.POINTER(Aux), vp]
+    lib.clustered_attention_fwd.restype = i32
+    lib.iclustered_attention_fwd.argtypes = common + [i32, vp, vp, sz, ctypes.POINTER(Aux), vp]
+    lib.iclustered_attention_fwd.restype = i32
+    lib.ca_last_error.argtypes = []
+    lib.ca_last_error.restype = ctypes.c_char_p
+    lib.ca_version.restype = i32
+    lib.ca_set_kmeans_path.argtypes = [i32]
+    lib.ca_set_kmeans_path.restype = i32
+    _lib = lib
+    return lib
+
+
+def _check(rc: int):
+    if rc != CA_OK:
+        raise ClusteredAttnError(rc, library().ca_last_error().decode())
+
+
+def workspace_bytes(batch, heads, n, d, dtype, n_clusters, n_bits, topk=0) -> int:
+    return int(library().ca_workspace_bytes(batch, heads, n, d, dtype, n_clusters, n_bits, topk))
+
+
+def set_kmeans_path(path: int):
+    """0 automatic, 1 one workgroup per unit, 2 one kernel pair per Lloyd round."""
+    _check(library().ca_set_kmeans_path(int(path)))
+
+
+def clustered_attention_fwd(q, k, v, lengths, planes, batch, heads, n, d, dtype, n_clusters,
+                            n_bits, lloyd_iters, out, workspace, workspace_nbytes, aux=None,
+                            stream=None):
+    """Raw call with integer device addresses; returns the status code."""
+    return library().clustered_attention_fwd(
+        q, k, v, lengths, planes, batch, heads, n, d, dtype, n_clusters, n_bits, lloyd_iters,
+        out, workspace, workspace_nbytes, ctypes.byref(aux) if aux is not None else None, stream)
+
+
+def iclustered_attention_fwd(q, k, v, lengths, planes, batch, heads, n, d, dtype, n_clusters,
+                             n_bits, lloyd_iters, topk, out, workspace, workspace_nbytes,
+                             aux=None, stream=None):
+    """Raw call with integer device addresses; returns the status code."""
+    return library().iclustered_attention_fwd(
+        q, k, v, lengths, planes, batch, heads, n, d, dtype, n_clusters, n_bits, lloyd_iters,
+        topk, out, workspace, workspace_nbytes, ctypes.byref(aux) if aux is not None else None,
+        stream)
+
+
+# ---------------------------------------------------------------------------
+# torch convenience layer (device memory and stream plumbing only)
+# ---------------------------------------------------------------------------
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dtype_code(t):
+    torch = _torch()
+    if t.dtype == torch.float32:
+        return CA_F32
+    if t.dtype == torch.bfloat16:
+        return CA_BF16
+    raise TypeError("q, k, v must be float32 or bfloat16, got %s" % t.dtype)
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def make_aux(**tensors) -> Aux:
+    """Builds an Aux from keyword tensors (e.g. codes_out=t); others stay 0."""
+    aux = Aux()
+    for name, t in tensors.items():
+        if t is not None:
+            setattr(aux, name, t.data_ptr())
+    return aux
+
+
+def _prepare(q, k, v, planes, lengths):
+    torch = _torch()
+    if not (q.is_cuda and k.is_cuda and v.is_cuda):
+        raise ValueError("q, k, v must be device tensors")
+    if q.dim() != 4 or k.shape != q.shape or v.shape != q.shape:
+        raise ValueError("q, k, v must share the shape [batch, heads, n, d]")
+    if not (q.dtype == k.dtype == v.dtype):
+        raise ValueError("q, k, v must share a dtype")
+    for t in (q, k, v):
+        if not t.is_contiguous():
+            raise ValueError("q, k, v must be contiguous")
+    if planes is not None and (planes.dtype != torch.float32 or not planes.is_cuda
+                               or not planes.is_contiguous()):
+        raise ValueError("planes must be a contiguous float32 device tensor [heads, n_bits, d]")
+    if lengths is not None and (lengths.dtype != torch.int32 or not lengths.is_cuda):
+        raise ValueError("lengths must be an int32 device tensor [batch]")
+    return q.shape
+
+
+def _workspace(nbytes, device, workspace):
+    torch = _torch()
+    if workspace is not None:
+        if workspace.numel() * workspace.element_size() < nbytes:
+            raise ValueError("workspace too small: need %d bytes" % nbytes)
+        return workspace
+    return torch.empty(max(nbytes, 1), dtype=torch.uint8, device=device)
+
+
+def clustered_attention(q, k, v, planes, n_clusters=100, n_bits=63, lloyd_iters=10,
+                        lengths=None, out=None, workspace=None, aux: Optional[Aux] = None):
+    """Clustered attention forward (Section 3.2) on torch device tensors."""
+    torch = _torch()
+    B, H, N, D = _prepare(q, k, v, planes, lengths)
+    dt = _dtype_code(q)
+    need = workspace_bytes(B, H, N, D, dt, n_clusters, n_bits, 0)
+    if need == 0:
+        _check(library().clustered_attention_fwd(None, None, None, None, None, B, H, N, D, dt,
+                                                 n_clusters, n_bits, lloyd_iters, None, None, 0,
+                                                 None, None))
+    ws = _workspace(need, q.device, workspace)
+    if out is None:
+        out = torch.empty_like(q)
+    stream = torch.cuda.current_stream(q.device).cuda_stream
+    _check(clustered_attention_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), _ptr(lengths),
+                                   _ptr(planes), B, H, N, D, dt, n_clusters, n_bits, lloyd_iters,
+                                   out.data_ptr(), ws.data_ptr(), need, aux, stream))
+    return out
+
+
+def iclustered_attention(q, k, v, planes, n_clusters=100, n_bits=63, lloyd_iters=10, topk=32,
+                         lengths=None, out=None, workspace=None, aux: Optional[Aux] = None):
+    """Improved clustered attention forward (Section 3.3) on torch device tensors."""
+    torch = _torch()
+    B, H, N, D = _prepare(q, k, v, planes, lengths)
+    dt = _dtype_code(q)
+    need = workspace_bytes(B, H, N, D, dt, n_clusters, n_bits, topk)
+    if need == 0:
+        _check(library().iclustered_attention_fwd(None, None, None, None, None, B, H, N, D, dt,
+                                                  n_clusters, n_bits, lloyd_iters, topk, None,
+                                                  None, 0, None, None))
+    ws = _workspace(need, q.device, workspace)
+    if out is None:
+        out = torch.empty_like(q)
+    stream = torch.cuda.current_stream(q.device).cuda_stream
+    _check(iclustered_attention_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), _ptr(lengths),
+                                    _ptr(planes), B, H, N, D, dt, n_clusters, n_bits, lloyd_iters,
+                                    topk, out.data_ptr(), ws.data_ptr(), need, aux, stream))
+    return out

@@ -1,0 +1,241 @@
+// C ABI of the library: argument validation, workspace carving and the
+// launch sequence of the forward pass on the caller's stream.
+#include <stdarg.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <string>
+
+#include "../../include/clustered_attn.h"
+#include "kernels.h"
+
+namespace ca {
+
+static thread_local std::string g_last_error;
+
+static int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+static int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return code;
+}
+
+static size_t align_up(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+
+size_t carve_workspace(const Problem& p, void* base, Workspace* ws) {
+  const size_t U = static_cast<size_t>(p.units());
+  const size_t N = static_cast<size_t>(p.n);
+  const size_t C = static_cast<size_t>(p.C);
+  const size_t D = static_cast<size_t>(p.d);
+  const size_t K = static_cast<size_t>(p.topk > 0 ? p.topk : 1);
+  Workspace w;
+  w.nblk = (p.n + kKmBlockQ - 1) / kKmBlockQ;
+  w.ncsr = (p.n + kCsrBlockQ - 1) / kCsrBlockQ;
+  w.nchunk = (p.n + kChunk - 1) / kChunk;
+  size_t off = 0;
+  auto take = [&](size_t bytes) -> void* {
+    void* ptr = base ? static_cast<void*>(static_cast<char*>(base) + off) : nullptr;
+    off += align_up(bytes);
+    return ptr;
+  };
+  w.codes = static_cast<uint64_t*>(take(U * N * 8));
+  w.assign = static_cast<int32_t*>(take(U * N * 4));
+  w.members = static_cast<int32_t*>(take(U * N * 4));
+  w.offsets = static_cast<int32_t*>(take(U * (C + 1) * 4));
+  w.sizes = static_cast<int32_t*>(take(U * C * 4));
+  w.cent = static_cast<uint64_t*>(take(2 * U * C * 8));
+  w.part = static_cast<uint32_t*>(take(U * w.nblk * C * 32 * 4));
+  w.part_sizes = static_cast<int32_t*>(take(U * w.nblk * C * 4));
+  w.csr_cnt = static_cast<int32_t*>(take(U * w.ncsr * C * 4));
+  w.qc = static_cast<float*>(take(U * C * D * 4));
+  w.pm = static_cast<float*>(take(U * C * w.nchunk * 4));
+  w.pz = static_cast<float*>(take(U * C * w.nchunk * 4));
+  w.pacc = static_cast<float*>(take(U * C * w.nchunk * D * 4));
+  w.cand_idx = static_cast<int32_t*>(take(p.topk > 0 ? U * C * w.nchunk * K * 4 : 0));
+  w.cand_val = static_cast<float*>(take(p.topk > 0 ? U * C * w.nchunk * K * 4 : 0));
+  w.topk = static_cast<int32_t*>(take(p.topk > 0 ? U * C * K * 4 : 0));
+  w.mass = static_cast<float*>(take(p.topk > 0 ? U * C * 4 : 0));
+  w.vcb = static_cast<float*>(take(U * C * D * 4));
+  if (ws) *ws = w;
+  return off;
+}
+
+// Returns CA_OK or an error code (message recorded) for the given sizes.
+static int check_sizes(int batch, int heads, int n, int d, int dtype, int C, int n_bits, int L,
+                       int topk, bool improved) {
+  if (batch < 1 || heads < 1 || n < 1 || d < 1)
+    return fail(CA_ERR_INVALID_ARG, "batch, heads, n and d must be >= 1 (got %d, %d, %d, %d)",
+                batch, heads, n, d);
+  if (dtype != CA_F32 && dtype != CA_BF16)
+    return fail(CA_ERR_INVALID_ARG, "dtype must be CA_F32 or CA_BF16 (got %d)", dtype);
+  if (n_bits < 1) return fail(CA_ERR_INVALID_ARG, "n_bits must be >= 1 (got %d)", n_bits);
+  if (C < 1) return fail(CA_ERR_INVALID_ARG, "n_clusters must be >= 1 (got %d)", C);
+  if (L < 1) return fail(CA_ERR_INVALID_ARG, "lloyd_iters must be >= 1 (got %d)", L);
+  if (improved && topk < 1) return fail(CA_ERR_INVALID_ARG, "topk must be >= 1 (got %d)", topk);
+  if (d != 32 && d != 64) return fail(CA_ERR_UNSUPPORTED, "d must be 32 or 64 (got %d)", d);
+  if (n_bits > 63) return fail(CA_ERR_UNSUPPORTED, "n_bits must be <= 63 (got %d)", n_bits);
+  if (C > 256) return fail(CA_ERR_UNSUPPORTED, "n_clusters must be <= 256 (got %d)", C);
+  if (L > 1000) return fail(CA_ERR_UNSUPPORTED, "lloyd_iters must be <= 1000 (got %d)", L);
+  if (improved && topk > 128) return fail(CA_ERR_UNSUPPORTED, "topk must be <= 128 (got %d)", topk);
+  if (n > (1 << 20)) return fail(CA_ERR_UNSUPPORTED, "n must be <= 1048576 (got %d)", n);
+  const long long rows = static_cast<long long>(batch) * heads * n;
+  if (rows >= (1ll << 31)) return fail(CA_ERR_UNSUPPORTED, "batch*heads*n must be < 2^31");
+  if (static_cast<long long>(batch) * heads > 65535)
+    return fail(CA_ERR_UNSUPPORTED, "batch*heads must be <= 65535");
+  return CA_OK;
+}
+
+static int run_forward(const void* q, const void* k, const void* v, const int32_t* lengths,
+                       const float* planes, int batch, int heads, int n, int d, int dtype, int C,
+                       int n_bits, int L, int topk, void* out, void* workspace,
+                       size_t workspace_bytes, const ca_aux* aux, void* stream) {
+  const bool improved = topk > 0;
+  int rc = check_sizes(batch, heads, n, d, dtype, C, n_bits, L, topk, improved);
+  if (rc != CA_OK) return rc;
+  const bool assign_given = aux && aux->assign_in;
+  if (!q || !k || !v || !out)
+    return fail(CA_ERR_INVALID_ARG, "q, k, v and out must not be NULL");
+  if (!planes && !assign_given && !(aux && aux->codes_in))
+    return fail(CA_ERR_INVALID_ARG, "planes must not be NULL");
+  Problem p;
+  p.batch = batch;
+  p.heads = heads;
+  p.n = n;
+  p.d = d;
+  p.dtype = dtype;
+  p.C = C;
+  p.n_bits = n_bits;
+  p.L = L;
+  p.topk = improved ? topk : 0;
+  p.q = q;
+  p.k = k;
+  p.v = v;
+  p.lengths = lengths;
+  p.planes = planes;
+  p.out = out;
+  const size_t need = carve_workspace(p, nullptr, nullptr);
+  if (!workspace) return fail(CA_ERR_WORKSPACE, "workspace must not be NULL (%zu bytes needed)", need);
+  if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0)
+    return fail(CA_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if (workspace_bytes < need)
+    return fail(CA_ERR_WORKSPACE, "workspace too small: %zu bytes given, %zu needed", workspace_bytes, need);
+  Workspace ws;
+  carve_workspace(p, workspace, &ws);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+
+  hipError_t e = hipSuccess;
+#define CA_TRY(call)                                                                  \
+  do {                                                                                \
+    e = (call);                                                                       \
+    if (e != hipSuccess)                                                              \
+      return fail(CA_ERR_HIP, "%s failed: %s", #call, hipGetErrorString(e));          \
+  } while (0)
+
+  bool csr_done = false;
+  if (assign_given) {
+    CA_TRY(launch_load_assign(p, aux->assign_in, ws, s));
+    CA_TRY(launch_csr(p, ws.assign, ws, s));
+  } else {
+    if (aux && aux->codes_in)
+      CA_TRY(launch_load_codes(p, aux->codes_in, ws, s));
+    else
+      CA_TRY(launch_hash(p, ws, s));
+    CA_TRY(launch_kmeans(p, ws, s, &csr_done));
+    if (!csr_done) CA_TRY(launch_csr(p, ws.assign, ws, s));
+  }
+  CA_TRY(launch_centroids(p, ws, s));
+  CA_TRY(launch_centroid_attention(p, ws, improved && aux ? aux->topk_in : nullptr, s));
+  if (improved) {
+    CA_TRY(launch_sparse(p, ws, s));
+    if (lengths) CA_TRY(launch_pad_zero(p, s));
+  } else {
+    CA_TRY(launch_broadcast(p, ws.assign, ws, s));
+  }
+  if (aux) {
+    const size_t U = static_cast<size_t>(batch) * heads;
+    auto copy = [&](void* dst, const void* src, size_t bytes) -> hipError_t {
+      if (!dst) return hipSuccess;
+      return hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDevice, s);
+    };
+    if (!assign_given) CA_TRY(copy(aux->codes_out, ws.codes, U * n * 8));
+    CA_TRY(copy(aux->assign_out, ws.assign, U * n * 4));
+    CA_TRY(copy(aux->sizes_out, ws.sizes, U * C * 4));
+    CA_TRY(copy(aux->centroids_out, ws.qc, U * C * d * 4));
+    CA_TRY(copy(aux->values_out, ws.vcb, U * C * d * 4));
+    if (improved) {
+      CA_TRY(copy(aux->topk_out, ws.topk, U * C * topk * 4));
+      CA_TRY(copy(aux->mass_out, ws.mass, U * C * 4));
+    }
+  }
+#undef CA_TRY
+  return CA_OK;
+}
+
+}  // namespace ca
+
+extern "C" {
+
+size_t ca_workspace_bytes(int batch, int heads, int n, int d, int dtype, int n_clusters,
+                          int n_bits, int topk) {
+  const bool improved = topk > 0;
+  if (ca::check_sizes(batch, heads, n, d, dtype, n_clusters, n_bits, 1, topk, improved) != CA_OK)
+    return 0;
+  ca::Problem p;
+  memset(&p, 0, sizeof(p));
+  p.batch = batch;
+  p.heads = heads;
+  p.n = n;
+  p.d = d;
+  p.dtype = dtype;
+  p.C = n_clusters;
+  p.n_bits = n_bits;
+  p.L = 1;
+  p.topk = improved ? topk : 0;
+  return ca::carve_workspace(p, nullptr, nullptr);
+}
+
+int clustered_attention_fwd(const void* q, const void* k, const void* v, const int32_t* lengths,
+                            const float* planes, int batch, int heads, int n, int d, int dtype,
+                            int n_clusters, int n_bits, int lloyd_iters, void* out,
+                            void* workspace, size_t workspace_bytes, const ca_aux* aux,
+                            void* stream) {
+  try {
+    return ca::run_forward(q, k, v, lengths, planes, batch, heads, n, d, dtype, n_clusters,
+                           n_bits, lloyd_iters, 0, out, workspace, workspace_bytes, aux, stream);
+  } catch (...) {
+    return ca::fail(CA_ERR_HIP, "unexpected C++ exception");
+  }
+}
+
+int iclustered_attention_fwd(const void* q, const void* k, const void* v, const int32_t* lengths,
+                             const float* planes, int batch, int heads, int n, int d, int dtype,
+                             int n_clusters, int n_bits, int lloyd_iters, int topk, void* out,
+                             void* workspace, size_t workspace_bytes, const ca_aux* aux,
+                             void* stream) {
+  try {
+    if (topk < 1) return ca::fail(CA_ERR_INVALID_ARG, "topk must be >= 1 (got %d)", topk);
+    return ca::run_forward(q, k, v, lengths, planes, batch, heads, n, d, dtype, n_clusters,
+                           n_bits, lloyd_iters, topk, out, workspace, workspace_bytes, aux, stream);
+  } catch (...) {
+    return ca::fail(CA_ERR_HIP, "unexpected C++ exception");
+  }
+}
+
+const char* ca_last_error(void) { return ca::g_last_error.c_str(); }
+
+int ca_version(void) { return 100; }
+
+// Selects the K-means driver (0 automatic, 1 one workgroup per unit, 2 one
+// launch pair per round).  Exposed for tests that cover both drivers.
+int ca_set_kmeans_path(int path) {
+  if (path < 0 || path > 2) return ca::fail(CA_ERR_INVALID_ARG, "path must be 0, 1 or 2");
+  ca::set_kmeans_path(path);
+  return CA_OK;
+}
+
+}  // extern "C"

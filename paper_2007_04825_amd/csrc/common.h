@@ -1,0 +1,138 @@
+// Device helpers shared by the gfx950 kernels of the clustered-attention library.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ca {
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+constexpr int kWave = 64;
+
+// ---------------------------------------------------------------------------
+// Element types.  bf16 is carried as raw uint16_t storage.
+// ---------------------------------------------------------------------------
+struct bf16_t {
+  uint16_t x;
+};
+
+__device__ __forceinline__ float to_f32(float x) { return x; }
+__device__ __forceinline__ float to_f32(bf16_t x) {
+  return __uint_as_float(static_cast<uint32_t>(x.x) << 16);
+}
+
+// fp32 -> bf16, round to nearest even; NaN stays NaN.
+__device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
+
+// Loads CNT consecutive elements starting at p (aligned to CNT elements) as fp32.
+template <int CNT>
+__device__ __forceinline__ void load_row(const float* __restrict__ p, float* dst) {
+  static_assert(CNT % 4 == 0, "vector width");
+#pragma unroll
+  for (int i = 0; i < CNT; i += 4) {
+    const float4 t = *reinterpret_cast<const float4*>(p + i);
+    dst[i] = t.x;
+    dst[i + 1] = t.y;
+    dst[i + 2] = t.z;
+    dst[i + 3] = t.w;
+  }
+}
+template <int CNT>
+__device__ __forceinline__ void load_row(const bf16_t* __restrict__ p, float* dst) {
+  static_assert(CNT % 4 == 0, "vector width");
+#pragma unroll
+  for (int i = 0; i < CNT; i += 4) {
+    const uint2 t = *reinterpret_cast<const uint2*>(p + i);
+    dst[i] = __uint_as_float(t.x << 16);
+    dst[i + 1] = __uint_as_float(t.x & 0xffff0000u);
+    dst[i + 2] = __uint_as_float(t.y << 16);
+    dst[i + 3] = __uint_as_float(t.y & 0xffff0000u);
+  }
+}
+
+// Stores 4 consecutive fp32 values (aligned) as the output element type.
+__device__ __forceinline__ void store4(float* p, float a, float b, float c, float d) {
+  *reinterpret_cast<float4*>(p) = make_float4(a, b, c, d);
+}
+__device__ __forceinline__ void store4(bf16_t* p, float a, float b, float c, float d) {
+  uint2 t;
+  t.x = static_cast<uint32_t>(f32_to_bf16_bits(a)) | (static_cast<uint32_t>(f32_to_bf16_bits(b)) << 16);
+  t.y = static_cast<uint32_t>(f32_to_bf16_bits(c)) | (static_cast<uint32_t>(f32_to_bf16_bits(d)) << 16);
+  *reinterpret_cast<uint2*>(p) = t;
+}
+
+// ---------------------------------------------------------------------------
+// Lengths: lengths[b] clamped to [0, N]; NULL means every row is valid.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int unit_length(const int32_t* __restrict__ lengths, int b, int N) {
+  if (lengths == nullptr) return N;
+  int n = lengths[b];
+  return n < 0 ? 0 : (n > N ? N : n);
+}
+
+// ---------------------------------------------------------------------------
+// Wave utilities (wave64).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int lane_id() { return static_cast<int>(threadIdx.x) & (kWave - 1); }
+
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x = fmaxf(x, __shfl_xor(x, o));
+  return x;
+}
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o);
+  return x;
+}
+__device__ __forceinline__ int wave_sum_i(int x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o);
+  return x;
+}
+// Inclusive prefix sum over the 64 lanes.
+__device__ __forceinline__ int wave_incl_scan(int x) {
+  const int l = lane_id();
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int y = __shfl_up(x, o);
+    if (l >= o) x += y;
+  }
+  return x;
+}
+__device__ __forceinline__ uint64_t lanemask_lt() {
+  const int l = lane_id();
+  return l == 0 ? 0ull : (~0ull >> (64 - l));
+}
+
+// ---------------------------------------------------------------------------
+// MFMA wrappers (gfx950).  For the 16x16 shapes used here:
+//   A operand: lane l holds row (l % 16) and k-group (l / 16);
+//   B operand: lane l holds column (l % 16) and k-group (l / 16);
+//   result   : lane l, register r holds element [4 * (l / 16) + r][l % 16].
+// A and B pair their k values by (k-group, position in the register), so any
+// permutation of the reduction index applied to both operands is allowed.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ v4f mfma_f32_16x16x4(float a, float b, v4f c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ v4i mfma_i8_16x16x64(v4i a, v4i b, v4i c) {
+  return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
+}
+
+// ---------------------------------------------------------------------------
+// Order-preserving map from fp32 to uint32: a < b  <=>  key(a) < key(b).
+// -0 is folded onto +0 so that equal values get equal keys.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t order_key(float f) {
+  uint32_t u = __float_as_uint(f == 0.0f ? 0.0f : f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+}  // namespace ca

@@ -1,0 +1,80 @@
+// Host-side launchers of the gfx950 kernels (internal to the library).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace ca {
+
+// Problem description shared by the launchers.
+struct Problem {
+  int batch, heads, n, d, dtype;   // n = padded length N
+  int C, n_bits, L, topk;          // topk = 0 for the clustered variant
+  const void* q;
+  const void* k;
+  const void* v;
+  const int32_t* lengths;          // device, may be null
+  const float* planes;             // device [heads][n_bits][d]
+  void* out;
+  int units() const { return batch * heads; }
+};
+
+// Keys per chunk of the centroid-attention kernel.
+constexpr int kChunk = 1024;
+// Largest n handled by the one-workgroup-per-unit K-means.
+constexpr int kKmLdsMaxN = 4096;
+// Queries per workgroup of the multi-workgroup K-means.
+constexpr int kKmBlockQ = 1024;
+// Queries per workgroup of the CSR build.
+constexpr int kCsrBlockQ = 256;
+
+// Device buffers carved from the caller's workspace.
+struct Workspace {
+  uint64_t* codes;      // [U][N]
+  int32_t* assign;      // [U][N]
+  int32_t* members;     // [U][N]   CSR member lists, ascending query index per cluster
+  int32_t* offsets;     // [U][C+1]
+  int32_t* sizes;       // [U][C]
+  uint64_t* cent;       // [2][U][C] centroid codes (multi-workgroup K-means)
+  uint32_t* part;       // [U][nblk][C][32] packed 16-bit bit-pair counts
+  int32_t* part_sizes;  // [U][nblk][C]
+  int32_t* csr_cnt;     // [U][ncsr][C] per-block counts, then per-block bases
+  float* qc;            // [U][C][d]
+  float* pm;            // [U][C][nchunk]
+  float* pz;            // [U][C][nchunk]
+  float* pacc;          // [U][C][nchunk][d]
+  int32_t* cand_idx;    // [U][C][nchunk][k]
+  float* cand_val;      // [U][C][nchunk][k]
+  int32_t* topk;        // [U][C][k]
+  float* mass;          // [U][C]
+  float* vcb;           // [U][C][d]
+  int nblk;             // ceil(N / kKmBlockQ)
+  int ncsr;             // ceil(N / kCsrBlockQ)
+  int nchunk;           // ceil(N / kChunk)
+};
+
+// Carves the workspace; returns the bytes needed (ws may be null to only size it).
+size_t carve_workspace(const Problem& p, void* base, Workspace* ws);
+
+hipError_t launch_hash(const Problem& p, const Workspace& ws, hipStream_t s);
+hipError_t launch_load_codes(const Problem& p, const uint64_t* codes_in, const Workspace& ws,
+                             hipStream_t s);
+// K-means; also builds sizes/offsets/members when the one-workgroup path runs.
+// *csr_done tells whether the CSR lists were produced.
+hipError_t launch_kmeans(const Problem& p, const Workspace& ws, hipStream_t s, bool* csr_done);
+hipError_t launch_load_assign(const Problem& p, const int32_t* assign_in, const Workspace& ws,
+                              hipStream_t s);
+hipError_t launch_csr(const Problem& p, const int32_t* assign, const Workspace& ws, hipStream_t s);
+hipError_t launch_centroids(const Problem& p, const Workspace& ws, hipStream_t s);
+hipError_t launch_centroid_attention(const Problem& p, const Workspace& ws, const int32_t* topk_in,
+                                     hipStream_t s);
+hipError_t launch_broadcast(const Problem& p, const int32_t* assign, const Workspace& ws,
+                            hipStream_t s);
+hipError_t launch_sparse(const Problem& p, const Workspace& ws, hipStream_t s);
+hipError_t launch_pad_zero(const Problem& p, hipStream_t s);
+
+// Which K-means path runs: 0 automatic, 1 one workgroup per unit, 2 multi-workgroup.
+void set_kmeans_path(int path);
+int kmeans_uses_lds(const Problem& p);
+
+}  // namespace ca

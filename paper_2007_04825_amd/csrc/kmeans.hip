@@ -1,0 +1,580 @@
+// K-means in Hamming space on the hash codes (Section 3.2.2), and the
+// cluster-sorted member lists (CSR) that the later stages read.
+//
+// Assign step on the int8 matrix cores.  A code h is expanded to a 64-entry
+// int8 vector: bit b (b < n_bits) becomes +64 / -64 for a query and +2 / -2
+// for a centroid, positions n_bits..62 are 0, and position 63 (never a hash
+// bit, n_bits <= 63) carries 1 for a query and 127 - j for centroid j.  One
+// v_mfma_i32_16x16x64_i8 then yields, for 16 centroids x 16 queries,
+//     key = 128 * (n_bits - 2 * ham(h, c_j)) + 127 - j,
+// so the largest key is the nearest centroid with ties resolved to the
+// smallest index, exactly; the argmin costs one integer max per distance.
+// Centroid slots past C_eff in the last 16-wide tile repeat centroid 0 with
+// tie byte -128 (index 255), so they can never win against centroid 0.
+//
+// Update step.  Member bit counts live in LDS as 16-bit pairs (dword w holds
+// the counts of bits 2w and 2w+1); a lane adds its query's 32 pairs with LDS
+// atomics, starting at pair (lane mod 32) so that the 64 lanes of a wave hit
+// distinct dwords.  The new centroid is the per-bit majority (tie -> 0) taken
+// with one wave ballot per cluster; an empty cluster keeps its code.  Integer
+// arithmetic only, so the result is independent of the order of the atomics.
+//
+// Two drivers:
+//  * kmeans_lds_kernel: one 1024-thread workgroup per (batch, head) unit for
+//    n <= 4096; codes, assignments and counts stay in LDS for all L rounds,
+//    only queries whose cluster changed update the counts, and the stable
+//    member lists are written at the end.
+//  * kmeans_assign_kernel + kmeans_reduce_kernel: one launch pair per round
+//    for long sequences; each 1024-query workgroup writes its partial counts
+//    and a reduction kernel forms the next centroids.
+#include <limits.h>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace ca {
+
+constexpr int kCmax = 256;
+constexpr int kCntStride = 33;  // dwords per cluster row of the count table (32 + 1 pad)
+constexpr int kMaxQt = 16;      // query tiles of 16 per wave in both drivers
+
+// ---------------------------------------------------------------------------
+// int8 operand construction.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t spread4(uint32_t nib) {
+  return (nib & 1u) | ((nib & 2u) << 7) | ((nib & 4u) << 14) | ((nib & 8u) << 21);
+}
+
+// keep[q]: byte p is 0xff when bit 16g + 4q + p is a hash bit (< n_bits).
+struct OpMasks {
+  uint32_t keep[4];
+};
+__device__ __forceinline__ OpMasks op_masks(int g, int n_bits) {
+  OpMasks m;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    uint32_t k = 0;
+#pragma unroll
+    for (int p = 0; p < 4; ++p)
+      if (16 * g + 4 * q + p < n_bits) k |= 0xffu << (8 * p);
+    m.keep[q] = k;
+  }
+  return m;
+}
+
+// Bits 16g..16g+15 of a query code as 16 int8: +64 / -64, 0 past n_bits, 1 at slot 63.
+__device__ __forceinline__ v4i query_operand(uint64_t code, int g, const OpMasks& m) {
+  const uint32_t x = static_cast<uint32_t>(code >> (16 * g)) & 0xffffu;
+  v4i r;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const uint32_t s = spread4((x >> (4 * q)) & 0xfu);
+    r[q] = static_cast<int>((0xc0c0c0c0u ^ (s << 7)) & m.keep[q]);
+  }
+  if (g == 3) r[3] |= 0x01000000;
+  return r;
+}
+
+// Bits 16g..16g+15 of centroid j as 16 int8: +2 / -2, 0 past n_bits, 127 - j at slot 63.
+__device__ __forceinline__ v4i centroid_operand(uint64_t code, int g, const OpMasks& m, int j) {
+  const uint32_t x = static_cast<uint32_t>(code >> (16 * g)) & 0xffffu;
+  v4i r;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const uint32_t s = spread4((x >> (4 * q)) & 0xfu);
+    r[q] = static_cast<int>((0xfefefefeu ^ (s * 0xfcu)) & m.keep[q]);
+  }
+  if (g == 3) r[3] |= static_cast<int>(static_cast<uint32_t>(static_cast<uint8_t>(127 - j)) << 24);
+  return r;
+}
+
+// Same as query_operand, from a table mapping 8 code bits to 8 int8 entries.
+__device__ __forceinline__ v4i query_operand_lut(uint64_t code, int g, const OpMasks& m,
+                                                 const uint2* lut) {
+  const uint32_t x = static_cast<uint32_t>(code >> (16 * g)) & 0xffffu;
+  const uint2 lo = lut[x & 0xffu], hi = lut[x >> 8];
+  v4i r;
+  r[0] = static_cast<int>(lo.x & m.keep[0]);
+  r[1] = static_cast<int>(lo.y & m.keep[1]);
+  r[2] = static_cast<int>(hi.x & m.keep[2]);
+  r[3] = static_cast<int>(hi.y & m.keep[3]);
+  if (g == 3) r[3] |= 0x01000000;
+  return r;
+}
+
+// Cluster index from the best key.
+__device__ __forceinline__ int decode_cluster(int best, int n_bits) {
+  return (128 * n_bits + 127 - best) & 255;
+}
+
+// Bit-pair w of a code as two 16-bit counters.
+__device__ __forceinline__ uint32_t pair_val(uint64_t code, int w) {
+  const uint32_t x = static_cast<uint32_t>(code >> (2 * w));
+  return (x & 1u) | ((x & 2u) << 15);
+}
+
+// Best key over the centroid tiles for one 16-query tile (B operand bq).
+// cop[ct * 64 + lane] holds the A operand of centroid tile ct.
+__device__ __forceinline__ int best_key(const v4i* cop, int nct, v4i bq, int lane) {
+  int best = INT_MIN;
+  const v4i zero = {0, 0, 0, 0};
+  for (int ct = 0; ct < nct; ++ct) {
+    const v4i d = mfma_i8_16x16x64(cop[ct * 64 + lane], bq, zero);
+    best = max(best, max(max(d[0], d[1]), max(d[2], d[3])));
+  }
+  best = max(best, __shfl_xor(best, 16));
+  best = max(best, __shfl_xor(best, 32));
+  return best;
+}
+
+// Fills the centroid operands of nct tiles (entries e = ct * 64 + lane).
+__device__ __forceinline__ void build_centroid_operands(v4i* cop, const uint64_t* cent, int ce,
+                                                        int nct, int n_bits, int tid, int nthreads) {
+  for (int e = tid; e < nct * 64; e += nthreads) {
+    const int ct = e >> 6, ln = e & 63;
+    const int j = ct * 16 + (ln & 15), g = ln >> 4;
+    const OpMasks m = op_masks(g, n_bits);
+    cop[e] = j < ce ? centroid_operand(cent[j], g, m, j) : centroid_operand(cent[0], g, m, 255);
+  }
+}
+
+// ===========================================================================
+// One workgroup per unit.
+// ===========================================================================
+constexpr int kKmThreads = 1024;
+constexpr int kKmWaves = kKmThreads / 64;
+static_assert(kKmLdsMaxN == kMaxQt * 16 * kKmWaves, "tile budget");
+
+struct KmShared {
+  uint64_t codes[kKmLdsMaxN];
+  int32_t assign[kKmLdsMaxN];
+  int32_t scratch[kKmLdsMaxN];  // change list; later per-wave cluster counts
+  uint32_t cnt[kCmax * kCntStride];
+  int32_t size[kCmax];
+  uint64_t cent[kCmax];
+  v4i cop[kCmax / 16 * 64];
+  int32_t offs[kCmax + 1];
+  int32_t run[kCmax];
+  uint2 qlut[256];
+  int nchange;
+};
+
+__global__ __launch_bounds__(kKmThreads) void kmeans_lds_kernel(
+    const uint64_t* __restrict__ codes_g, const int32_t* __restrict__ lengths, int heads, int N,
+    int C, int n_bits, int L, int32_t* __restrict__ assign_g, int32_t* __restrict__ sizes_g,
+    int32_t* __restrict__ offsets_g, int32_t* __restrict__ members_g) {
+  __shared__ KmShared sh;
+  const int u = blockIdx.x;
+  const int n = unit_length(lengths, u / heads, N);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int32_t* asg = assign_g + static_cast<size_t>(u) * N;
+  int32_t* mem = members_g + static_cast<size_t>(u) * N;
+  for (int i = n + tid; i < N; i += kKmThreads) asg[i] = -1;
+  if (n == 0) {
+    for (int j = tid; j < C; j += kKmThreads) sizes_g[static_cast<size_t>(u) * C + j] = 0;
+    for (int j = tid; j <= C; j += kKmThreads) offsets_g[static_cast<size_t>(u) * (C + 1) + j] = 0;
+    return;
+  }
+  const int ce = C < n ? C : n;
+  const int nct = (ce + 15) / 16;
+  const int nqt = (n + 15) / 16;
+  for (int i = tid; i < n; i += kKmThreads) {
+    sh.codes[i] = codes_g[static_cast<size_t>(u) * N + i];
+    sh.assign[i] = -1;
+  }
+  for (int x = tid; x < kCmax * kCntStride; x += kKmThreads) sh.cnt[x] = 0;
+  for (int j = tid; j < kCmax; j += kKmThreads) sh.size[j] = 0;
+  __syncthreads();
+  for (int j = tid; j < ce; j += kKmThreads)
+    sh.cent[j] = sh.codes[(static_cast<int64_t>(j) * n) / ce];
+
+  // byte pattern -> 8 int8 of +64 / -64, for rebuilding query operands cheaply
+  for (int b = tid; b < 256; b += kKmThreads) {
+    const uint32_t lo = 0xc0c0c0c0u ^ (spread4(b & 0xf) << 7);
+    const uint32_t hi = 0xc0c0c0c0u ^ (spread4(b >> 4) << 7);
+    sh.qlut[b] = make_uint2(lo, hi);
+  }
+  const int g = lane >> 4, c = lane & 15;
+  const OpMasks qm = op_masks(g, n_bits);
+  __syncthreads();
+
+  for (int t = 0; t < L; ++t) {
+    build_centroid_operands(sh.cop, sh.cent, ce, nct, n_bits, tid, kKmThreads);
+    if (tid == 0) sh.nchange = 0;
+    __syncthreads();
+    // assign
+    for (int s = 0; s < kMaxQt; ++s) {
+      const int qt = wave + s * kKmWaves;
+      if (qt < nqt) {
+        const int qb = qt * 16 + c;
+        const v4i bq = query_operand_lut(qb < n ? sh.codes[qb] : 0ull, g, qm, sh.qlut);
+        const int best = best_key(sh.cop, nct, bq, lane);
+        const int qi = qt * 16 + lane;
+        if (lane < 16 && qi < n) {
+          const int j = decode_cluster(best, n_bits);
+          const int old = sh.assign[qi];
+          if (j != old) {
+            sh.assign[qi] = j;
+            const int pos = atomicAdd(&sh.nchange, 1);
+            sh.scratch[pos] = (qi << 9) | (old + 1);
+          }
+        }
+      }
+    }
+    __syncthreads();
+    // counts of the queries whose cluster changed
+    const int nc = sh.nchange;
+    for (int e = tid; e < nc; e += kKmThreads) {
+      const int x = sh.scratch[e];
+      const int qi = x >> 9, old = (x & 511) - 1;
+      const int nw = sh.assign[qi];
+      const uint64_t code = sh.codes[qi];
+      if (old >= 0) {
+        atomicSub(&sh.size[old], 1);
+#pragma unroll 4
+        for (int s = 0; s < 32; ++s) {
+          const int w = (s + lane) & 31;
+          atomicSub(&sh.cnt[old * kCntStride + w], pair_val(code, w));
+        }
+      }
+      atomicAdd(&sh.size[nw], 1);
+#pragma unroll 4
+      for (int s = 0; s < 32; ++s) {
+        const int w = (s + lane) & 31;
+        atomicAdd(&sh.cnt[nw * kCntStride + w], pair_val(code, w));
+      }
+    }
+    __syncthreads();
+    if (t == L - 1) break;
+    // majority update
+    for (int j = wave; j < ce; j += kKmWaves) {
+      const int sz = sh.size[j];
+      const uint32_t dw = sh.cnt[j * kCntStride + (lane >> 1)];
+      const int field = static_cast<int>((dw >> ((lane & 1) * 16)) & 0xffffu);
+      const uint64_t bits = __ballot(2 * field > sz);
+      if (lane == 0 && sz > 0) sh.cent[j] = bits;
+    }
+    __syncthreads();
+  }
+
+  // sizes and offsets (exclusive scan over clusters)
+  if (wave == 0) {
+    int running = 0;
+    for (int j0 = 0; j0 < C; j0 += 64) {
+      const int j = j0 + lane;
+      const int v = (j < ce) ? sh.size[j] : 0;
+      const int incl = wave_incl_scan(v);
+      if (j < C) sh.offs[j] = running + incl - v;
+      running += __shfl(incl, 63);
+    }
+    if (lane == 0) sh.offs[C] = running;
+  }
+  for (int i = tid; i < n; i += kKmThreads) asg[i] = sh.assign[i];
+  for (int j = tid; j < ce; j += kKmThreads) sh.run[j] = 0;
+  __syncthreads();
+  for (int j = tid; j < C; j += kKmThreads) sizes_g[static_cast<size_t>(u) * C + j] = j < ce ? sh.size[j] : 0;
+  for (int j = tid; j <= C; j += kKmThreads) offsets_g[static_cast<size_t>(u) * (C + 1) + j] = sh.offs[j];
+  for (int j = tid; j < ce; j += kKmThreads) sh.run[j] = sh.offs[j];
+
+  // stable member lists, 1024 queries per round
+  for (int r0 = 0; r0 < n; r0 += kKmThreads) {
+    for (int x = tid; x < kKmWaves * ce; x += kKmThreads) sh.scratch[x] = 0;
+    __syncthreads();
+    const int i = r0 + tid;
+    const int a = i < n ? sh.assign[i] : -1;
+    uint64_t active = __ballot(a >= 0);
+    int rank = 0;
+    while (active) {
+      const int leader = __ffsll(static_cast<unsigned long long>(active)) - 1;
+      const int aj = __shfl(a, leader);
+      const uint64_t mm = __ballot(a == aj) & active;
+      if (a == aj) rank = __popcll(mm & lanemask_lt());
+      if (lane == leader) sh.scratch[wave * ce + aj] = __popcll(mm);
+      active &= ~mm;
+    }
+    __syncthreads();
+    if (a >= 0) {
+      int base = sh.run[a];
+      for (int w = 0; w < wave; ++w) base += sh.scratch[w * ce + a];
+      mem[base + rank] = i;
+    }
+    __syncthreads();
+    for (int j = tid; j < ce; j += kKmThreads) {
+      int tot = 0;
+      for (int w = 0; w < kKmWaves; ++w) tot += sh.scratch[w * ce + j];
+      sh.run[j] += tot;
+    }
+    __syncthreads();
+  }
+}
+
+// ===========================================================================
+// Multi-workgroup path: one launch pair per Lloyd round.
+// ===========================================================================
+constexpr int kKbThreads = 256;
+constexpr int kKbWaves = kKbThreads / 64;
+static_assert(kKmBlockQ == kMaxQt * 16 * kKbWaves, "tile budget");
+
+__global__ __launch_bounds__(kKbThreads) void kmeans_assign_kernel(
+    const uint64_t* __restrict__ codes_g, const int32_t* __restrict__ lengths, int heads, int N,
+    int C, int n_bits, int t, uint64_t* __restrict__ cent_cur, int32_t* __restrict__ assign_g,
+    uint32_t* __restrict__ part, int32_t* __restrict__ part_sizes, int nblk) {
+  __shared__ uint64_t cent[kCmax];
+  __shared__ v4i cop[kCmax / 16 * 64];
+  __shared__ uint32_t cnt[kCmax * kCntStride];
+  __shared__ int32_t size[kCmax];
+  __shared__ int32_t la[kKmBlockQ];
+  __shared__ uint64_t lcodes[kKmBlockQ];
+  const int u = blockIdx.y, blk = blockIdx.x;
+  const int n = unit_length(lengths, u / heads, N);
+  const int q0 = blk * kKmBlockQ;
+  if (q0 >= n) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int nq = min(kKmBlockQ, n - q0);
+  const int ce = C < n ? C : n;
+  const int nct = (ce + 15) / 16;
+  const uint64_t* cu = codes_g + static_cast<size_t>(u) * N;
+  for (int j = tid; j < ce; j += kKbThreads) {
+    const uint64_t cj = t == 0 ? cu[(static_cast<int64_t>(j) * n) / ce]
+                               : cent_cur[static_cast<size_t>(u) * C + j];
+    cent[j] = cj;
+    if (t == 0 && blk == 0) cent_cur[static_cast<size_t>(u) * C + j] = cj;
+  }
+  for (int x = tid; x < nq; x += kKbThreads) lcodes[x] = cu[q0 + x];
+  for (int x = tid; x < kCmax * kCntStride; x += kKbThreads) cnt[x] = 0;
+  for (int j = tid; j < kCmax; j += kKbThreads) size[j] = 0;
+  __syncthreads();
+  build_centroid_operands(cop, cent, ce, nct, n_bits, tid, kKbThreads);
+  __syncthreads();
+  const int g = lane >> 4, c = lane & 15;
+  const OpMasks qm = op_masks(g, n_bits);
+  const int nqt = (nq + 15) / 16;
+#pragma unroll 4
+  for (int s = 0; s < kMaxQt; ++s) {
+    const int qt = wave + s * kKbWaves;
+    if (qt < nqt) {
+      const int qi = qt * 16 + c;
+      const v4i bq = query_operand(qi < nq ? lcodes[qi] : 0ull, g, qm);
+      const int best = best_key(cop, nct, bq, lane);
+      const int qo = qt * 16 + lane;
+      if (lane < 16 && qo < nq) {
+        const int j = decode_cluster(best, n_bits);
+        la[qo] = j;
+        assign_g[static_cast<size_t>(u) * N + q0 + qo] = j;
+      }
+    }
+  }
+  __syncthreads();
+  for (int x = tid; x < nq; x += kKbThreads) {
+    const int a = la[x];
+    const uint64_t code = lcodes[x];
+    atomicAdd(&size[a], 1);
+#pragma unroll 4
+    for (int s = 0; s < 32; ++s) {
+      const int w = (s + lane) & 31;
+      atomicAdd(&cnt[a * kCntStride + w], pair_val(code, w));
+    }
+  }
+  __syncthreads();
+  const size_t base = (static_cast<size_t>(u) * nblk + blk) * C;
+  for (int x = tid; x < ce * 32; x += kKbThreads) {
+    const int j = x >> 5, w = x & 31;
+    part[(base + j) * 32 + w] = cnt[j * kCntStride + w];
+  }
+  for (int j = tid; j < ce; j += kKbThreads) part_sizes[base + j] = size[j];
+}
+
+// One wave per cluster: sums the partial counts and forms the next centroid.
+__global__ __launch_bounds__(256) void kmeans_reduce_kernel(
+    const uint32_t* __restrict__ part, const int32_t* __restrict__ part_sizes,
+    const int32_t* __restrict__ lengths, int heads, int N, int C, int nblk,
+    const uint64_t* __restrict__ cent_cur, uint64_t* __restrict__ cent_next) {
+  const int u = blockIdx.y;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int j = blockIdx.x * 4 + wave;
+  const int n = unit_length(lengths, u / heads, N);
+  const int ce = C < n ? C : n;
+  if (j >= ce) return;
+  const int nb = (n + kKmBlockQ - 1) / kKmBlockQ;
+  int cnt = 0, sz = 0;
+  for (int blk = 0; blk < nb; ++blk) {
+    const size_t base = (static_cast<size_t>(u) * nblk + blk) * C + j;
+    const uint32_t dw = part[base * 32 + (lane >> 1)];
+    cnt += static_cast<int>((dw >> ((lane & 1) * 16)) & 0xffffu);
+    sz += part_sizes[base];
+  }
+  const uint64_t bits = __ballot(2 * cnt > sz);
+  if (lane == 0)
+    cent_next[static_cast<size_t>(u) * C + j] = sz > 0 ? bits : cent_cur[static_cast<size_t>(u) * C + j];
+}
+
+// ===========================================================================
+// CSR build from an assignment array (multi-workgroup path and injected
+// assignments): per-block counts, prefix over blocks and clusters, stable
+// scatter.  Assignments outside [0, C_eff) are clamped into it.
+// ===========================================================================
+__device__ __forceinline__ int clamp_cluster(int a, int ce) {
+  return a < 0 ? 0 : (a >= ce ? ce - 1 : a);
+}
+
+__global__ __launch_bounds__(kCsrBlockQ) void csr_count_kernel(
+    const int32_t* __restrict__ assign, const int32_t* __restrict__ lengths, int heads, int N,
+    int C, int ncsr, int32_t* __restrict__ csr_cnt, int32_t* __restrict__ assign_pad) {
+  __shared__ int32_t cnt[kCmax];
+  const int u = blockIdx.y, blk = blockIdx.x, tid = threadIdx.x;
+  const int n = unit_length(lengths, u / heads, N);
+  const int ce = C < n ? C : n;
+  const int i = blk * kCsrBlockQ + tid;
+  if (assign_pad != nullptr && i >= n && i < N) assign_pad[static_cast<size_t>(u) * N + i] = -1;
+  if (blk * kCsrBlockQ >= n) return;
+  for (int j = tid; j < C; j += kCsrBlockQ) cnt[j] = 0;
+  __syncthreads();
+  if (i < n) atomicAdd(&cnt[clamp_cluster(assign[static_cast<size_t>(u) * N + i], ce)], 1);
+  __syncthreads();
+  for (int j = tid; j < C; j += kCsrBlockQ) csr_cnt[(static_cast<size_t>(u) * ncsr + blk) * C + j] = cnt[j];
+}
+
+__global__ __launch_bounds__(256) void csr_scan_kernel(int32_t* __restrict__ csr_cnt,
+                                                       const int32_t* __restrict__ lengths, int heads,
+                                                       int N, int C, int ncsr,
+                                                       int32_t* __restrict__ sizes,
+                                                       int32_t* __restrict__ offsets) {
+  __shared__ int32_t wtot[4];
+  const int u = blockIdx.x, j = threadIdx.x, lane = j & 63, wave = j >> 6;
+  const int n = unit_length(lengths, u / heads, N);
+  const int nb = (n + kCsrBlockQ - 1) / kCsrBlockQ;
+  int run = 0;
+  if (j < C)
+    for (int blk = 0; blk < nb; ++blk) {
+      int32_t* x = &csr_cnt[(static_cast<size_t>(u) * ncsr + blk) * C + j];
+      const int v = *x;
+      *x = run;
+      run += v;
+    }
+  const int incl = wave_incl_scan(run);
+  if (lane == 63) wtot[wave] = incl;
+  __syncthreads();
+  int excl = incl - run;
+  for (int w = 0; w < wave; ++w) excl += wtot[w];
+  if (j < C) {
+    sizes[static_cast<size_t>(u) * C + j] = run;
+    offsets[static_cast<size_t>(u) * (C + 1) + j] = excl;
+    if (j == C - 1) offsets[static_cast<size_t>(u) * (C + 1) + C] = excl + run;
+    for (int blk = 0; blk < nb; ++blk) csr_cnt[(static_cast<size_t>(u) * ncsr + blk) * C + j] += excl;
+  }
+}
+
+__global__ __launch_bounds__(kCsrBlockQ) void csr_scatter_kernel(
+    const int32_t* __restrict__ assign, const int32_t* __restrict__ lengths, int heads, int N,
+    int C, int ncsr, const int32_t* __restrict__ csr_base, int32_t* __restrict__ members) {
+  __shared__ int32_t wcnt[kCsrBlockQ / 64][kCmax];
+  const int u = blockIdx.y, blk = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n = unit_length(lengths, u / heads, N);
+  if (blk * kCsrBlockQ >= n) return;
+  const int ce = C < n ? C : n;
+  const int i = blk * kCsrBlockQ + tid;
+  const int a = i < n ? clamp_cluster(assign[static_cast<size_t>(u) * N + i], ce) : -1;
+  for (int x = tid; x < (kCsrBlockQ / 64) * kCmax; x += kCsrBlockQ) (&wcnt[0][0])[x] = 0;
+  __syncthreads();
+  uint64_t active = __ballot(a >= 0);
+  int rank = 0;
+  while (active) {
+    const int leader = __ffsll(static_cast<unsigned long long>(active)) - 1;
+    const int aj = __shfl(a, leader);
+    const uint64_t mm = __ballot(a == aj) & active;
+    if (a == aj) rank = __popcll(mm & lanemask_lt());
+    if (lane == leader) wcnt[wave][aj] = __popcll(mm);
+    active &= ~mm;
+  }
+  __syncthreads();
+  if (a >= 0) {
+    int base = csr_base[(static_cast<size_t>(u) * ncsr + blk) * C + a];
+    for (int w = 0; w < wave; ++w) base += wcnt[w][a];
+    members[static_cast<size_t>(u) * N + base + rank] = i;
+  }
+}
+
+// Copies caller-supplied assignments, clamped into [0, C_eff), -1 on padded rows.
+__global__ __launch_bounds__(256) void load_assign_kernel(const int32_t* __restrict__ in,
+                                                          const int32_t* __restrict__ lengths,
+                                                          int heads, int N, int C,
+                                                          int32_t* __restrict__ assign) {
+  const int u = blockIdx.y;
+  const int n = unit_length(lengths, u / heads, N);
+  const int ce = C < n ? C : n;
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= N) return;
+  const size_t x = static_cast<size_t>(u) * N + i;
+  assign[x] = i < n ? clamp_cluster(in[x], ce) : -1;
+}
+
+// ===========================================================================
+// Host launchers.
+// ===========================================================================
+static int g_kmeans_path = 0;
+void set_kmeans_path(int path) { g_kmeans_path = path; }
+
+int kmeans_uses_lds(const Problem& p) {
+  if (p.n > kKmLdsMaxN) return 0;
+  if (g_kmeans_path == 1) return 1;
+  if (g_kmeans_path == 2) return 0;
+  // One workgroup per unit when there are enough units to occupy the chip
+  // or the sequences are short; otherwise spread each unit over workgroups.
+  return (p.units() >= 128 || p.n <= 1024) ? 1 : 0;
+}
+
+hipError_t launch_load_assign(const Problem& p, const int32_t* assign_in, const Workspace& ws,
+                              hipStream_t s) {
+  hipLaunchKernelGGL(load_assign_kernel, dim3((p.n + 255) / 256, p.units()), dim3(256), 0, s,
+                     assign_in, p.lengths, p.heads, p.n, p.C, ws.assign);
+  return hipGetLastError();
+}
+
+hipError_t launch_csr(const Problem& p, const int32_t* assign, const Workspace& ws, hipStream_t s) {
+  const int U = p.units();
+  dim3 grid(ws.ncsr, U);
+  int32_t* pad = (assign == ws.assign) ? ws.assign : nullptr;
+  hipLaunchKernelGGL(csr_count_kernel, grid, dim3(kCsrBlockQ), 0, s, assign, p.lengths, p.heads,
+                     p.n, p.C, ws.ncsr, ws.csr_cnt, pad);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(csr_scan_kernel, dim3(U), dim3(256), 0, s, ws.csr_cnt, p.lengths, p.heads,
+                     p.n, p.C, ws.ncsr, ws.sizes, ws.offsets);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(csr_scatter_kernel, grid, dim3(kCsrBlockQ), 0, s, assign, p.lengths, p.heads,
+                     p.n, p.C, ws.ncsr, ws.csr_cnt, ws.members);
+  return hipGetLastError();
+}
+
+hipError_t launch_kmeans(const Problem& p, const Workspace& ws, hipStream_t s, bool* csr_done) {
+  const int U = p.units();
+  if (kmeans_uses_lds(p)) {
+    hipLaunchKernelGGL(kmeans_lds_kernel, dim3(U), dim3(kKmThreads), 0, s, ws.codes, p.lengths,
+                       p.heads, p.n, p.C, p.n_bits, p.L, ws.assign, ws.sizes, ws.offsets,
+                       ws.members);
+    *csr_done = true;
+    return hipGetLastError();
+  }
+  *csr_done = false;
+  uint64_t* cent0 = ws.cent;
+  uint64_t* cent1 = ws.cent + static_cast<size_t>(U) * p.C;
+  for (int t = 0; t < p.L; ++t) {
+    uint64_t* cur = (t & 1) ? cent1 : cent0;
+    uint64_t* nxt = (t & 1) ? cent0 : cent1;
+    hipLaunchKernelGGL(kmeans_assign_kernel, dim3(ws.nblk, U), dim3(kKbThreads), 0, s, ws.codes,
+                       p.lengths, p.heads, p.n, p.C, p.n_bits, t, cur, ws.assign, ws.part,
+                       ws.part_sizes, ws.nblk);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (t + 1 < p.L) {
+      hipLaunchKernelGGL(kmeans_reduce_kernel, dim3((p.C + 3) / 4, U), dim3(256), 0, s, ws.part,
+                         ws.part_sizes, p.lengths, p.heads, p.n, p.C, ws.nblk, cur, nxt);
+      e = hipGetLastError();
+      if (e != hipSuccess) return e;
+    }
+  }
+  return hipSuccess;
+}
+
+}  // namespace ca
