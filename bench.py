@@ -1,0 +1,269 @@
+"""Benchmark of the clustered / improved-clustered attention forward pass.
+
+One step = one clustered forward and one improved-clustered forward over the
+whole batch of the speech-encoder-shaped workload (32 sequences x 6 heads,
+padded length 800 with lengths uniform in [400, 800], d = 32, fp32, C = 100,
+63-bit hashes, 10 Lloyd rounds, top-32 keys), i.e. every stage of both
+variants.  Inputs are seeded synthetic data already resident in HBM.
+
+Prints one JSON line.  value = queries answered per second, counting each
+valid (sequence, head, position) once per variant.  The roofline entry times
+the dominant stage with HIP events recorded by the library around its kernels
+on the call's stream; the cpu_baseline entry times the fp64 oracle on the
+host's cores on the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAKS = {  # MI355X published peaks
+    "hbm_GBps": 8000.0,
+    "fp32_mfma_TFLOPs": 157.3,
+    "bf16_mfma_TFLOPs": 2500.0,
+    "int8_mfma_TOPs": 5000.0,
+    "fp64_TFLOPs": 78.6,
+}
+
+
+class Hip:
+    """Minimal HIP event API through ctypes (events on an explicit stream)."""
+
+    def __init__(self):
+        self.lib = ctypes.CDLL("libamdhip64.so")
+        self.lib.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.lib.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        self.lib.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+        self.lib.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                 ctypes.c_void_p]
+        self.lib.hipEventDestroy.argtypes = [ctypes.c_void_p]
+
+    def event(self):
+        ev = ctypes.c_void_p()
+        assert self.lib.hipEventCreate(ctypes.byref(ev)) == 0
+        return ev
+
+    def record(self, ev, stream):
+        assert self.lib.hipEventRecord(ev, ctypes.c_void_p(stream)) == 0
+
+    def elapsed_ms(self, a, b):
+        assert self.lib.hipEventSynchronize(b) == 0
+        ms = ctypes.c_float()
+        assert self.lib.hipEventElapsedTime(ctypes.byref(ms), a, b) == 0
+        return float(ms.value)
+
+    def destroy(self, ev):
+        self.lib.hipEventDestroy(ev)
+
+
+def stage_work(w, stage, variant_topk):
+    """Algorithmic work of one launch of a stage over the whole batch:
+    returns (amount, unit, bound, peak) for the roofline entry."""
+    H = w.q.shape[1]
+    D = w.q.shape[3]
+    nsum = int(w.lengths.astype(np.int64).sum()) * H        # valid queries = valid keys
+    s = 4 if w.dtype == "f32" else 2
+    if stage == "centroid_attn":
+        # Q^c K^T and A^c V: 2 * C * n * d flops each, per (sequence, head)
+        flops = 4.0 * w.C * nsum * D
+        return flops, "TFLOP/s", "mfma", PEAKS["fp32_mfma_TFLOPs"]
+    if stage == "kmeans":
+        # L rounds x n x C Hamming distances, each a 64-entry int8 dot product
+        ops = 2.0 * 64 * w.L * nsum * w.C
+        return ops, "TOP/s", "mfma", PEAKS["int8_mfma_TOPs"]
+    if stage == "hash":
+        byts = nsum * D * s + nsum * 8                          # read Q, write codes
+        return byts, "GB/s", "hbm", PEAKS["hbm_GBps"]
+    if stage == "output":
+        if variant_topk:
+            byts = 2 * nsum * D * s                             # gather Q, scatter out
+        else:
+            byts = nsum * D * s + nsum * 4                      # write out, read assign
+        return byts, "GB/s", "hbm", PEAKS["hbm_GBps"]
+    if stage == "centroids":
+        byts = nsum * D * s + nsum * 4
+        return byts, "GB/s", "hbm", PEAKS["hbm_GBps"]
+    raise ValueError(stage)
+
+
+def cpu_baseline(w, min_seconds=10.0, max_passes=40):
+    """Times the fp64 oracle (both variants) on the same workload."""
+    import oracle
+    threads = os.cpu_count() or 1
+    q = np.nan_to_num(w.q, nan=0.0)
+    oracle.forward(q[:1], w.k[:1], w.v[:1], w.lengths[:1], w.planes, w.C, w.n_bits, w.L, w.topk,
+                   num_threads=threads, exports=False)  # load / warm
+    passes, t0 = 0, time.perf_counter()
+    while True:
+        for topk in (0, w.topk):
+            oracle.forward(q, w.k, w.v, w.lengths, w.planes, w.C, w.n_bits, w.L, topk,
+                           num_threads=threads, exports=False)
+        passes += 1
+        el = time.perf_counter() - t0
+        if el >= min_seconds or passes >= max_passes:
+            break
+    queries = 2 * w.queries() * passes
+    return {"value": queries / el, "unit": "queries/s", "cores": threads, "kind": "oracle",
+            "sample": "%d passes of the full workload, both variants (%.1f s)" % (passes, el)}
+
+
+def copy_calibration(nbytes):
+    """A plain device-to-device copy of known size, for scaling HBM counters."""
+    import torch
+    a = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(5):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": nbytes}))
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--stage", default="auto",
+                    choices=["auto", "hash", "kmeans", "centroids", "centroid_attn", "output"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: the forward pass of each (sequence, head) is "
+              "independent and this build has no multi-GPU path (--gpus %d refused)" % args.gpus,
+              file=sys.stderr)
+        sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
+
+    import torch
+
+    import gen
+    import paper_2007_04825_amd as ca
+
+    w = gen.make_config(2)
+    B, H, N, D = w.q.shape
+    dev = torch.device("cuda:0")
+    q, k, v = (torch.from_numpy(x).to(dev) for x in (w.q, w.k, w.v))
+    planes = torch.from_numpy(w.planes).to(dev)
+    lengths = torch.from_numpy(w.lengths).to(dev)
+    ws = torch.empty(max(ca.workspace_bytes(B, H, N, D, 0, w.C, w.n_bits, w.topk),
+                         ca.workspace_bytes(B, H, N, D, 0, w.C, w.n_bits, 0)),
+                     dtype=torch.uint8, device=dev)
+    out_c = torch.empty_like(q)
+    out_i = torch.empty_like(q)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    hip = Hip()
+
+    def step():
+        ca.clustered_attention(q, k, v, planes, w.C, w.n_bits, w.L, lengths=lengths, out=out_c,
+                               workspace=ws)
+        ca.iclustered_attention(q, k, v, planes, w.C, w.n_bits, w.L, w.topk, lengths=lengths,
+                                out=out_i, workspace=ws)
+
+    # per-stage times (one event pair per stage and variant) to find the dominant stage
+    def stage_times(reps=5):
+        tot = {}
+        for name, sid in ca.STAGES.items():
+            for topk in (0, w.topk):
+                acc = 0.0
+                for _ in range(reps):
+                    e0, e1 = hip.event(), hip.event()
+                    lib = ca.library()
+                    assert lib.ca_time_next_stage(sid, e0, e1) == 0
+                    if topk:
+                        ca.iclustered_attention(q, k, v, planes, w.C, w.n_bits, w.L, topk,
+                                                lengths=lengths, out=out_i, workspace=ws)
+                    else:
+                        ca.clustered_attention(q, k, v, planes, w.C, w.n_bits, w.L,
+                                               lengths=lengths, out=out_c, workspace=ws)
+                    acc += hip.elapsed_ms(e0, e1)
+                    hip.destroy(e0)
+                    hip.destroy(e1)
+                tot[(name, topk)] = acc / reps
+        return tot
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    st = stage_times()
+    if args.stage == "auto":
+        name, var_topk = max(st, key=st.get)
+    else:
+        name = args.stage
+        var_topk = w.topk if st[(name, w.topk)] >= st[(name, 0)] else 0
+
+    # timed region: K steps; the dominant stage of the chosen variant is timed
+    # in every step with its own event pair
+    sid = ca.STAGES[name]
+    evs = [(hip.event(), hip.event()) for _ in range(args.steps)]
+    t_start, t_stop = hip.event(), hip.event()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    hip.record(t_start, stream)
+    lib = ca.library()
+    for i in range(args.steps):
+        if var_topk == 0:
+            assert lib.ca_time_next_stage(sid, evs[i][0], evs[i][1]) == 0
+        ca.clustered_attention(q, k, v, planes, w.C, w.n_bits, w.L, lengths=lengths, out=out_c,
+                               workspace=ws)
+        if var_topk:
+            assert lib.ca_time_next_stage(sid, evs[i][0], evs[i][1]) == 0
+        ca.iclustered_attention(q, k, v, planes, w.C, w.n_bits, w.L, w.topk, lengths=lengths,
+                                out=out_i, workspace=ws)
+    hip.record(t_stop, stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    total_ms = hip.elapsed_ms(t_start, t_stop)
+    stage_ms = sum(hip.elapsed_ms(a, b) for a, b in evs) / args.steps
+    ms_per_step = total_ms / args.steps
+    queries_per_step = 2 * w.queries()
+    value = queries_per_step / (ms_per_step * 1e-3)
+
+    amount, unit, bound, peak = stage_work(w, name, var_topk)
+    achieved = amount / (stage_ms * 1e-3) / (1e12 if unit != "GB/s" else 1e9)
+    roof = {"bound": bound, "achieved": round(achieved, 3), "peak": peak, "unit": unit,
+            "frac": round(achieved / peak, 5), "traffic": None,
+            "kernel": "%s (%s)" % (name, "iclustered" if var_topk else "clustered"),
+            "avg_launch_us": round(stage_ms * 1e3, 3)}
+    stages_us = {"%s_%s" % (n, "ic" if t else "c"): round(v * 1e3, 2) for (n, t), v in st.items()}
+    cpu = None if args.no_cpu_baseline else cpu_baseline(w)
+    rec = {
+        "metric": "queries/sec/GPU of clustered & i-clustered attn fwd",
+        "value": round(value, 1),
+        "unit": "queries/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "wall_ms_per_step": round(wall / args.steps * 1e3, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "speech-encoder layer: batch 32, heads 6, N 800 (lengths 400-800), "
+                               "d 32, fp32, C 100, B 63, L 10, k 32; clustered + i-clustered",
+                   "global_batch": B, "seq_len": N, "parallelism": "none"},
+        "per_variant_ms": {"stage_sum_clustered": round(sum(v for (n, t), v in st.items() if t == 0), 4),
+                           "stage_sum_iclustered": round(sum(v for (n, t), v in st.items() if t), 4)},
+        "stages_us": stages_us,
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(rec))
+
+
+if __name__ == "__main__":
+    main()

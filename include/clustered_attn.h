@@ -151,6 +151,30 @@ const char* ca_last_error(void);
 int ca_version(void);
 
 /*
+ * Stages of a forward call, for ca_time_next_stage.
+ *   CA_KERNEL_HASH           hashing of the queries (Section 3.2.2)
+ *   CA_KERNEL_KMEANS         the L Lloyd rounds of Hamming K-means
+ *   CA_KERNEL_CENTROIDS      query centroids (Eq. 3)
+ *   CA_KERNEL_CENTROID_ATTN  centroid attention, top-k and mass (Eqs. 4-5, Section 3.3)
+ *   CA_KERNEL_OUTPUT         broadcast (Eq. 6) or the improved per-query part
+ */
+#define CA_KERNEL_HASH 1
+#define CA_KERNEL_KMEANS 2
+#define CA_KERNEL_CENTROIDS 3
+#define CA_KERNEL_CENTROID_ATTN 4
+#define CA_KERNEL_OUTPUT 5
+
+/*
+ * Profiling hook for callers that time one stage with HIP events: in the
+ * next forward call made by this thread, hipEventRecord(start_event) is
+ * enqueued on the call's stream just before the stage's kernels and
+ * hipEventRecord(stop_event) just after them; the hook is then disarmed.
+ * start_event and stop_event are hipEvent_t owned by the caller.  stage 0
+ * disarms it.  Returns CA_OK or CA_ERR_INVALID_ARG.
+ */
+int ca_time_next_stage(int stage, void* start_event, void* stop_event);
+
+/*
  * Chooses the K-means driver for later calls in this process: 0 automatic
  * (default), 1 one workgroup per unit (used only when n <= 4096), 2 one
  * kernel pair per Lloyd round.  Both give identical results; the switch

@@ -28,7 +28,10 @@ CA_F32 = 0
 CA_BF16 = 1
 
 EXPORTED_SYMBOLS = ("ca_workspace_bytes", "clustered_attention_fwd", "iclustered_attention_fwd",
-                    "ca_last_error", "ca_version", "ca_set_kmeans_path")
+                    "ca_last_error", "ca_version", "ca_set_kmeans_path", "ca_time_next_stage")
+CA_KERNEL_HASH, CA_KERNEL_KMEANS, CA_KERNEL_CENTROIDS, CA_KERNEL_CENTROID_ATTN, CA_KERNEL_OUTPUT = \
+    1, 2, 3, 4, 5
+STAGES = {"hash": 1, "kmeans": 2, "centroids": 3, "centroid_attn": 4, "output": 5}
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 lib_path = os.path.join(_HERE, "libclustered_attn.so")
@@ -70,6 +73,8 @@ def library():
     lib.ca_version.restype = i32
     lib.ca_set_kmeans_path.argtypes = [i32]
     lib.ca_set_kmeans_path.restype = i32
+    lib.ca_time_next_stage.argtypes = [i32, vp, vp]
+    lib.ca_time_next_stage.restype = i32
     _lib = lib
     return lib
 
@@ -81,6 +86,12 @@ def _check(rc: int):
 
 def workspace_bytes(batch, heads, n, d, dtype, n_clusters, n_bits, topk=0) -> int:
     return int(library().ca_workspace_bytes(batch, heads, n, d, dtype, n_clusters, n_bits, topk))
+
+
+def time_next_stage(stage: int, start_event, stop_event):
+    """Arms the one-shot event pair (torch.cuda.Event objects) around a stage
+    of the next forward call on this thread."""
+    _check(library().ca_time_next_stage(int(stage), start_event.cuda_event, stop_event.cuda_event))
 
 
 def set_kmeans_path(path: int):

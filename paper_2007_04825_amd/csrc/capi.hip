@@ -25,6 +25,15 @@ static int fail(int code, const char* fmt, ...) {
   return code;
 }
 
+// One-shot event pair around one kernel of the next forward call on this thread.
+static thread_local int g_ev_kernel = 0;
+static thread_local hipEvent_t g_ev_start = nullptr, g_ev_stop = nullptr;
+
+static hipError_t mark(int kernel_id, bool start, hipStream_t s) {
+  if (g_ev_kernel != kernel_id) return hipSuccess;
+  return hipEventRecord(start ? g_ev_start : g_ev_stop, s);
+}
+
 static size_t align_up(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
 size_t carve_workspace(const Problem& p, void* base, Workspace* ws) {
@@ -141,21 +150,33 @@ static int run_forward(const void* q, const void* k, const void* v, const int32_
     CA_TRY(launch_load_assign(p, aux->assign_in, ws, s));
     CA_TRY(launch_csr(p, ws.assign, ws, s));
   } else {
-    if (aux && aux->codes_in)
+    if (aux && aux->codes_in) {
       CA_TRY(launch_load_codes(p, aux->codes_in, ws, s));
-    else
+    } else {
+      CA_TRY(mark(CA_KERNEL_HASH, true, s));
       CA_TRY(launch_hash(p, ws, s));
+      CA_TRY(mark(CA_KERNEL_HASH, false, s));
+    }
+    CA_TRY(mark(CA_KERNEL_KMEANS, true, s));
     CA_TRY(launch_kmeans(p, ws, s, &csr_done));
+    CA_TRY(mark(CA_KERNEL_KMEANS, false, s));
     if (!csr_done) CA_TRY(launch_csr(p, ws.assign, ws, s));
   }
+  CA_TRY(mark(CA_KERNEL_CENTROIDS, true, s));
   CA_TRY(launch_centroids(p, ws, s));
+  CA_TRY(mark(CA_KERNEL_CENTROIDS, false, s));
+  CA_TRY(mark(CA_KERNEL_CENTROID_ATTN, true, s));
   CA_TRY(launch_centroid_attention(p, ws, improved && aux ? aux->topk_in : nullptr, s));
+  CA_TRY(mark(CA_KERNEL_CENTROID_ATTN, false, s));
+  CA_TRY(mark(CA_KERNEL_OUTPUT, true, s));
   if (improved) {
     CA_TRY(launch_sparse(p, ws, s));
     if (lengths) CA_TRY(launch_pad_zero(p, s));
   } else {
     CA_TRY(launch_broadcast(p, ws.assign, ws, s));
   }
+  CA_TRY(mark(CA_KERNEL_OUTPUT, false, s));
+  g_ev_kernel = 0;
   if (aux) {
     const size_t U = static_cast<size_t>(batch) * heads;
     auto copy = [&](void* dst, const void* src, size_t bytes) -> hipError_t {
@@ -229,6 +250,15 @@ int iclustered_attention_fwd(const void* q, const void* k, const void* v, const 
 const char* ca_last_error(void) { return ca::g_last_error.c_str(); }
 
 int ca_version(void) { return 100; }
+
+int ca_time_next_stage(int stage, void* start_event, void* stop_event) {
+  if (stage < 0 || stage > CA_KERNEL_OUTPUT || (stage != 0 && (!start_event || !stop_event)))
+    return ca::fail(CA_ERR_INVALID_ARG, "invalid stage %d or null event", stage);
+  ca::g_ev_kernel = stage;
+  ca::g_ev_start = static_cast<hipEvent_t>(start_event);
+  ca::g_ev_stop = static_cast<hipEvent_t>(stop_event);
+  return CA_OK;
+}
 
 // Selects the K-means driver (0 automatic, 1 one workgroup per unit, 2 one
 // launch pair per round).  Exposed for tests that cover both drivers.
