@@ -145,10 +145,9 @@ static int run_forward(const void* q, const void* k, const void* v, const int32_
       return fail(CA_ERR_HIP, "%s failed: %s", #call, hipGetErrorString(e));          \
   } while (0)
 
-  bool csr_done = false;
+  bool lds_path = false;
   if (assign_given) {
     CA_TRY(launch_load_assign(p, aux->assign_in, ws, s));
-    CA_TRY(launch_csr(p, ws.assign, ws, s));
   } else {
     if (aux && aux->codes_in) {
       CA_TRY(launch_load_codes(p, aux->codes_in, ws, s));
@@ -158,22 +157,24 @@ static int run_forward(const void* q, const void* k, const void* v, const int32_
       CA_TRY(mark(CA_KERNEL_HASH, false, s));
     }
     CA_TRY(mark(CA_KERNEL_KMEANS, true, s));
-    CA_TRY(launch_kmeans(p, ws, s, &csr_done));
+    CA_TRY(launch_kmeans(p, ws, s, &lds_path));
     CA_TRY(mark(CA_KERNEL_KMEANS, false, s));
-    if (!csr_done) CA_TRY(launch_csr(p, ws.assign, ws, s));
   }
+  // A single key chunk lets the centroid-attention kernel build the member
+  // lists and centroids of its clusters itself; it then only needs the sizes.
+  const bool single_chunk = ws.nchunk == 1;
   CA_TRY(mark(CA_KERNEL_CENTROIDS, true, s));
-  CA_TRY(launch_centroids(p, ws, s));
+  if (!lds_path || !single_chunk) CA_TRY(launch_csr(p, ws.assign, ws, s));
+  if (!single_chunk) CA_TRY(launch_centroids(p, ws, s));
   CA_TRY(mark(CA_KERNEL_CENTROIDS, false, s));
   CA_TRY(mark(CA_KERNEL_CENTROID_ATTN, true, s));
   CA_TRY(launch_centroid_attention(p, ws, improved && aux ? aux->topk_in : nullptr, s));
   CA_TRY(mark(CA_KERNEL_CENTROID_ATTN, false, s));
   CA_TRY(mark(CA_KERNEL_OUTPUT, true, s));
-  if (improved) {
-    CA_TRY(launch_sparse(p, ws, s));
-    if (lengths) CA_TRY(launch_pad_zero(p, s));
-  } else {
-    CA_TRY(launch_broadcast(p, ws.assign, ws, s));
+  if (!improved && ws.nchunk > 1) {
+    CA_TRY(launch_broadcast(p, ws.assign, ws, s));  // also zeroes the padded rows
+  } else if (lengths && (assign_given || (aux && aux->codes_in))) {
+    CA_TRY(launch_pad_zero(p, s));  // otherwise the hashing kernel zeroed them
   }
   CA_TRY(mark(CA_KERNEL_OUTPUT, false, s));
   g_ev_kernel = 0;

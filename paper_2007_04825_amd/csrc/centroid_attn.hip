@@ -1,24 +1,29 @@
-// Centroids (Eq. 3), centroid attention (Eqs. 4-5) and the top-k keys of
-// each cluster with their attention mass (Section 3.3).
+// Centroids (Eq. 3), centroid attention (Eqs. 4-5), the top-k keys of each
+// cluster with their attention mass (Section 3.3) and, when a sequence fits
+// in one key chunk, the per-query outputs (Eq. 6 or the improved values).
 //
 // centroid_kernel: one wave per cluster sums the member rows of Q in fp64
 //   (members in ascending query order) and divides by the cluster size.
 //
-// centroid_attn_partial_kernel: one workgroup per (unit, 16 centroids,
-//   1024-key chunk).  Logits S^T = K Q^c^T come from v_mfma_f32_16x16x4f32
-//   with keys as rows and centroids as columns; they are scaled by 1/sqrt(d),
-//   masked past the valid length and kept in LDS, so A^c is never written to
-//   HBM.  Per centroid the chunk's row maximum m, sum z = sum exp(s - m), and
-//   (improved variant) the chunk's top-k candidates are taken from LDS; then
-//   V^T P^T accumulates the unnormalised chunk values on the matrix cores.
-//   The result layout of the first product is exactly the B-operand layout of
-//   the second (key 4*g + i of a 16-key tile sits in lane group g, register
-//   i), so P never leaves registers between the two products.
-//
-// centroid_attn_merge_kernel: one wave per cluster merges the chunks with the
-//   log-sum-exp rule, giving V^c = A^c V; for the improved variant it selects
-//   T_j among the chunk candidates, computes m_j = sum_{T_j} A^c and the rest
-//   part V^b_j = V^c_j - sum_{T_j} A^c_jl V_l.
+// attn_tile_kernel: one workgroup per (unit, 16 centroids, 1024-key chunk).
+//   Logits S^T = K Q^c^T come from v_mfma_f32_16x16x4f32 with keys as rows
+//   and centroids as columns, scaled by 1/sqrt(d), masked past the valid
+//   length and kept in LDS (A^c is never written to memory).  K rows are
+//   fetched four tiles at a time so that their latencies overlap.  One wave
+//   per centroid row then finds the row maximum m, z = sum exp(s - m) and,
+//   for the improved variant, the top-k set.  V^T P^T accumulates the values
+//   on the matrix cores: the result registers of the first product are in the
+//   B-operand layout of the second (key 4g+i of a tile sits in lane group g,
+//   register i), so P never leaves registers.
+//   * single chunk (n <= 1024): the workgroup finishes the clusters itself.
+//     For the improved variant the top-k keys are masked out of P, so the
+//     product yields the rest part V^b = sum_{l not in T} A^c_l V_l directly,
+//     and m_j = sum_{l in T} A^c_l.  It then writes every member row: V^c for
+//     the clustered variant, m_j * softmax_T(q K_T^T / sqrt d) V_T + V^b for
+//     the improved one (sparse_cluster below).
+//   * several chunks: it writes (m, z, unnormalised values, top-k candidates)
+//     of its chunk; attn_merge_kernel combines the chunks (log-sum-exp rule),
+//     selects T among the candidates and forms m_j and V^b = V^c - sum_T A^c V.
 #include <math.h>
 
 #include "common.h"
@@ -50,179 +55,578 @@ __global__ __launch_bounds__(256) void centroid_kernel(const T* __restrict__ q,
   const int32_t* mem = members + static_cast<size_t>(u) * N + offsets[static_cast<size_t>(u) * (C + 1) + j];
   const T* qu = q + static_cast<size_t>(u) * N * D;
   double acc = 0.0;
-#pragma unroll 4
-  for (int m = r; m < sz; m += RPS) acc += static_cast<double>(to_f32(qu[static_cast<size_t>(mem[m]) * D + t]));
-  if (RPS == 2) acc += __shfl_xor(acc, 32);
+  int m = r;
+  for (; m + 7 * RPS < sz; m += 8 * RPS) {  // eight rows in flight
+    float x[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x[e] = to_f32(qu[static_cast<size_t>(mem[m + e * RPS]) * D + t]);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc += static_cast<double>(x[e]);
+  }
+  for (; m < sz; m += RPS) acc += static_cast<double>(to_f32(qu[static_cast<size_t>(mem[m]) * D + t]));
+  if (RPS == 2) acc += lane_xor32(acc);
   if (lane < D) dst[t] = static_cast<float>(acc / static_cast<double>(sz));
 }
 
 // ---------------------------------------------------------------------------
-// Eqs. (4)-(5) per chunk of keys.
+// Small vector helpers for the DT-wide value loads.
 // ---------------------------------------------------------------------------
-constexpr int kLStride = kChunk + 4;  // floats per LDS logit row
+template <int W>
+__device__ __forceinline__ void load_vec(const float* p, float* d) {
+  if constexpr (W == 4) {
+    const float4 t = *reinterpret_cast<const float4*>(p);
+    d[0] = t.x; d[1] = t.y; d[2] = t.z; d[3] = t.w;
+  } else {
+    const float2 t = *reinterpret_cast<const float2*>(p);
+    d[0] = t.x; d[1] = t.y;
+  }
+}
+template <int W>
+__device__ __forceinline__ void load_vec(const bf16_t* p, float* d) {
+  if constexpr (W == 4) {
+    const uint2 t = *reinterpret_cast<const uint2*>(p);
+    d[0] = __uint_as_float(t.x << 16); d[1] = __uint_as_float(t.x & 0xffff0000u);
+    d[2] = __uint_as_float(t.y << 16); d[3] = __uint_as_float(t.y & 0xffff0000u);
+  } else {
+    const uint32_t t = *reinterpret_cast<const uint32_t*>(p);
+    d[0] = __uint_as_float(t << 16); d[1] = __uint_as_float(t & 0xffff0000u);
+  }
+}
+// Stores W consecutive fp32 values as the output type.
+template <int W>
+__device__ __forceinline__ void store_vec(float* p, const float* s) {
+#pragma unroll
+  for (int i = 0; i < W; i += 4) store4(p + i, s[i], s[i + 1], s[i + 2], s[i + 3]);
+}
+template <int W>
+__device__ __forceinline__ void store_vec(bf16_t* p, const float* s) {
+#pragma unroll
+  for (int i = 0; i < W; i += 4) store4(p + i, s[i], s[i + 1], s[i + 2], s[i + 3]);
+}
 
-template <int D, typename T, bool TOPK>
-__global__ __launch_bounds__(256) void centroid_attn_partial_kernel(
-    const float* __restrict__ qc, const int32_t* __restrict__ sizes, const T* __restrict__ kmat,
-    const T* __restrict__ vmat, const int32_t* __restrict__ lengths, int heads, int N, int C,
-    int nchunk, int topk, float scale, float* __restrict__ pm, float* __restrict__ pz,
-    float* __restrict__ pacc, int32_t* __restrict__ cand_idx, float* __restrict__ cand_val) {
-  __shared__ float logits[16 * kLStride];
-  __shared__ float rowm[16], rowz[16];
-  __shared__ int hist[4][256];
-  __shared__ int selpos[4][128];
-  __shared__ int any_nonempty;
-  const int chunk = blockIdx.x, tile = blockIdx.y, u = blockIdx.z;
-  const int n = unit_length(lengths, u / heads, N);
-  const int k0 = chunk * kChunk;
-  if (k0 >= n) return;
-  const int kn = min(kChunk, n - k0);
-  const int j0 = tile * 16;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  if (tid == 0) any_nonempty = 0;
-  __syncthreads();
-  if (tid < 16 && j0 + tid < C && sizes[static_cast<size_t>(u) * C + j0 + tid] > 0) any_nonempty = 1;
-  __syncthreads();
-  if (!any_nonempty) return;
-
-  const int c = lane & 15, g = lane >> 4;
-  constexpr int KS = D / 4;  // reduction steps of the 16x16x4 product
-  // B operand: centroid c, dimensions g*KS .. g*KS+KS-1.
+// ---------------------------------------------------------------------------
+// Improved values of one cluster (one wave), Section 3.3 / supplementary
+// decomposition: for each member i,
+//   out_i = mh * sum_{l in T} softmax_T(Q_i K_l / sqrt d)_l V_l + vb.
+// tpos[0..kk) are the key indices of T (LDS or global).  The K_T and V_T
+// operand fragments stay in registers for all member tiles.
+//   S^T = K_T Q^T : A = K_T rows (key kt*16 + lane%16, dims g*KS..), B = Q^T
+//   O^T = V_T^T P^T: A = V_T^T (dims DT*(lane%16)+dt, key kt*16+4g+i),
+//                     B = P^T straight from the S^T result registers.
+// Lane (query c, group g) ends with dims DT*4g .. DT*4g + 4*DT - 1 of its row.
+// ---------------------------------------------------------------------------
+template <int D, typename T, int NKT>
+__device__ void sparse_cluster(const int* tpos, int kk, float mh, const float* vb,
+                               const int32_t* mem, int sz, const T* __restrict__ qu,
+                               const T* __restrict__ ku, const T* __restrict__ vu,
+                               T* __restrict__ ou, float scale) {
+  constexpr int KS = D / 4, DT = D / 16;
+  const int lane = lane_id(), c = lane & 15, g = lane >> 4;
+  const int nkt = (kk + 15) >> 4;
+  // Q rows of the first member tile are requested before the K_T / V_T gathers
   float bq[KS];
-  if (j0 + c < C) {
-    load_row<KS>(qc + (static_cast<size_t>(u) * C + j0 + c) * D + g * KS, bq);
+  int row = c < sz ? mem[c] : -1;
+  if (row >= 0) {
+    load_row<KS>(qu + static_cast<size_t>(row) * D + g * KS, bq);
   } else {
 #pragma unroll
     for (int s = 0; s < KS; ++s) bq[s] = 0.0f;
   }
-  const T* ku = kmat + (static_cast<size_t>(u) * N + k0) * D;
-  const T* vu = vmat + (static_cast<size_t>(u) * N + k0) * D;
-  const int nkt = (kn + 15) / 16;
-
-  // logits of this chunk
-  for (int kt = wave; kt < nkt; kt += 4) {
-    const int key = kt * 16 + c;  // A operand row
-    float a[KS];
-    if (key < kn) {
-      load_row<KS>(ku + static_cast<size_t>(key) * D + g * KS, a);
+  float kf[NKT][KS];
+  float vf[NKT][4][DT];
+#pragma unroll
+  for (int kt = 0; kt < NKT; ++kt) {
+    const int slot = kt * 16 + c;
+    const int key = (kt < nkt && slot < kk) ? tpos[slot] : -1;
+    if (key >= 0) {
+      load_row<KS>(ku + static_cast<size_t>(key) * D + g * KS, kf[kt]);
     } else {
 #pragma unroll
-      for (int s = 0; s < KS; ++s) a[s] = 0.0f;
+      for (int s = 0; s < KS; ++s) kf[kt][s] = 0.0f;
     }
-    v4f acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int s = 0; s < KS; ++s) acc = mfma_f32_16x16x4(a[s], bq[s], acc);
-    float o[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) o[i] = (kt * 16 + 4 * g + i < kn) ? acc[i] * scale : -INFINITY;
-    *reinterpret_cast<float4*>(&logits[c * kLStride + kt * 16 + 4 * g]) = make_float4(o[0], o[1], o[2], o[3]);
-  }
-  __syncthreads();
-
-  // per-row maximum, sum and top-k candidates (wave w owns rows 4w..4w+3)
-  const int kk = min(topk, kn);
-  for (int rr = 0; rr < 4; ++rr) {
-    const int r = wave * 4 + rr;
-    const float* row = &logits[r * kLStride];
-    float mx = -INFINITY;
-    for (int x = lane; x < kn; x += 64) mx = fmaxf(mx, row[x]);
-    mx = wave_max(mx);
-    float z = 0.0f;
-    for (int x = lane; x < kn; x += 64) z += __expf(row[x] - mx);
-    z = wave_sum(z);
-    if (lane == 0) {
-      rowm[r] = mx;
-      rowz[r] = z;
-    }
-    if (TOPK && j0 + r < C) {
-      const int got = wave_select_topk([&](int pos) { return order_key(row[pos]); }, kn, kk,
-                                       hist[wave], selpos[wave]);
-      wave_lds_sync();
-      const size_t cb = ((static_cast<size_t>(u) * C + j0 + r) * nchunk + chunk) * topk;
-      for (int x = lane; x < topk; x += 64) {
-        const bool ok = x < got;
-        const int pos = ok ? selpos[wave][x] : 0;
-        cand_idx[cb + x] = ok ? k0 + pos : -1;
-        cand_val[cb + x] = ok ? row[pos] : -INFINITY;
-      }
-      wave_lds_sync();
-    }
-  }
-  __syncthreads();
-
-  // unnormalised chunk values: O^T = V^T P^T, P = exp(S - m)
-  constexpr int DT = D / 16;
-  v4f oacc[DT];
-#pragma unroll
-  for (int dt = 0; dt < DT; ++dt) oacc[dt] = v4f{0.f, 0.f, 0.f, 0.f};
-  const float mc = rowm[c];
-  for (int kt = wave; kt < nkt; kt += 4) {
-    const float4 s4 = *reinterpret_cast<const float4*>(&logits[c * kLStride + kt * 16 + 4 * g]);
-    const float p[4] = {__expf(s4.x - mc), __expf(s4.y - mc), __expf(s4.z - mc), __expf(s4.w - mc)};
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int key = kt * 16 + 4 * g + i;
-      const bool ok = key < kn;
+      const int sl = kt * 16 + 4 * g + i;
+      const int kv = (kt < nkt && sl < kk) ? tpos[sl] : -1;
+      if (kv >= 0) {
+        load_vec<DT>(vu + static_cast<size_t>(kv) * D + DT * c, vf[kt][i]);
+      } else {
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        const float a = ok ? to_f32(vu[static_cast<size_t>(key) * D + 16 * dt + c]) : 0.0f;
-        oacc[dt] = mfma_f32_16x16x4(a, p[i], oacc[dt]);
+        for (int dt = 0; dt < DT; ++dt) vf[kt][i][dt] = 0.0f;
       }
     }
   }
-  __syncthreads();  // logits no longer needed: reuse them for the cross-wave sum
-  float* red = logits;  // [4 waves][16 centroids][D]
+  float vbf[4 * DT];
 #pragma unroll
-  for (int dt = 0; dt < DT; ++dt)
-    *reinterpret_cast<float4*>(&red[(wave * 16 + c) * D + 16 * dt + 4 * g]) =
-        make_float4(oacc[dt][0], oacc[dt][1], oacc[dt][2], oacc[dt][3]);
-  __syncthreads();
-  for (int x = tid; x < 16 * D; x += 256) {
-    const int cc = x / D, dim = x % D;
-    if (j0 + cc >= C) continue;
-    const float sum = ((red[(0 * 16 + cc) * D + dim] + red[(1 * 16 + cc) * D + dim]) +
-                       red[(2 * 16 + cc) * D + dim]) + red[(3 * 16 + cc) * D + dim];
-    const size_t pj = (static_cast<size_t>(u) * C + j0 + cc) * nchunk + chunk;
-    pacc[pj * D + dim] = sum;
-    if (dim == 0) {
-      pm[pj] = rowm[cc];
-      pz[pj] = rowz[cc];
+  for (int x = 0; x < 4 * DT; ++x) vbf[x] = vb[DT * 4 * g + x];
+
+  for (int mt = 0; mt < sz; mt += 16) {
+    if (mt > 0) {
+      const int mi = mt + c;
+      row = mi < sz ? mem[mi] : -1;
+      if (row >= 0) {
+        load_row<KS>(qu + static_cast<size_t>(row) * D + g * KS, bq);
+      } else {
+#pragma unroll
+        for (int s = 0; s < KS; ++s) bq[s] = 0.0f;
+      }
+    }
+    v4f sacc[NKT];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt) {
+      sacc[kt] = v4f{0.f, 0.f, 0.f, 0.f};
+      if (kt < nkt) {
+#pragma unroll
+        for (int s = 0; s < KS; ++s) sacc[kt] = mfma_f32_16x16x4(kf[kt][s], bq[s], sacc[kt]);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float sv = (kt < nkt && kt * 16 + 4 * g + i < kk) ? sacc[kt][i] * scale : -INFINITY;
+        sacc[kt][i] = sv;
+        mx = fmaxf(mx, sv);
+      }
+    }
+    mx = cross_rows_max(mx);
+    float z = 0.0f;
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float e = __expf(sacc[kt][i] - mx);
+        sacc[kt][i] = e;
+        z += e;
+      }
+    z = cross_rows_sum(z);
+    const float f = mh / z;
+    v4f oacc[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) oacc[dt] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt) {
+      if (kt < nkt) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float pv = sacc[kt][i] * f;
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) oacc[dt] = mfma_f32_16x16x4(vf[kt][i][dt], pv, oacc[dt]);
+        }
+      }
+    }
+    if (row >= 0) {
+      float o[4 * DT];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) o[i * DT + dt] = oacc[dt][i] + vbf[i * DT + dt];
+      store_vec<4 * DT>(ou + static_cast<size_t>(row) * D + DT * 4 * g, o);
     }
   }
 }
 
 // ---------------------------------------------------------------------------
-// Merge of the chunks, top-k set, mass and rest part.
+// Centroid attention tile kernel.
 // ---------------------------------------------------------------------------
-template <int D, typename T, bool TOPK>
-__global__ __launch_bounds__(256) void centroid_attn_merge_kernel(
-    const float* __restrict__ qc, const int32_t* __restrict__ sizes, const T* __restrict__ kmat,
-    const T* __restrict__ vmat, const int32_t* __restrict__ lengths, int heads, int N, int C,
-    int nchunk, int topk, float scale, const float* __restrict__ pm, const float* __restrict__ pz,
-    const float* __restrict__ pacc, const int32_t* __restrict__ cand_idx,
-    const float* __restrict__ cand_val, const int32_t* __restrict__ topk_in,
-    int32_t* __restrict__ topk_out, float* __restrict__ mass, float* __restrict__ vcb) {
-  __shared__ int hist[4][256];
-  __shared__ int selpos[4][128];
+constexpr int kLStride = kChunk + 4;  // floats per LDS logit row
+constexpr int kCandCap = 128;
+
+struct AttnArgs {
+  const int32_t* assign;
+  float* qc;
+  const int32_t* sizes;
+  const int32_t* offsets;
+  const int32_t* members;
+  const void* q;
+  const void* k;
+  const void* v;
+  const int32_t* lengths;
+  int heads, N, C, nchunk, topk;
+  float scale;
+  const int32_t* topk_in;
+  float* pm;
+  float* pz;
+  float* pacc;
+  int32_t* cand_idx;
+  float* cand_val;
+  int32_t* topk_out;
+  float* mass;
+  float* vcb;
+  void* out;
+};
+
+// MODE: 0 clustered single chunk, 1 improved single chunk, 2 clustered
+// partial, 3 improved partial.
+template <int D, typename T, int MODE, int NKT>
+__global__ __launch_bounds__(256) void attn_tile_kernel(AttnArgs a) {
+  constexpr bool IMPROVED = (MODE & 1) != 0;
+  constexpr bool FUSED = MODE < 2;
+  constexpr int KS = D / 4, DT = D / 16;
+  constexpr int BT = 4;  // key tiles per batch of loads
+  __shared__ __align__(16) float logits[16 * kLStride];
+  __shared__ float rowm[16], rowz[16], rowmass[16];
+  __shared__ int tcnt[16];
+  __shared__ uint16_t tpos16[IMPROVED && FUSED ? 16 : 1][128];
+  __shared__ int cscr[4][2 * kCandCap];  // per-wave top-k scratch
+  __shared__ int selout[4][128];
+  __shared__ int mlist[FUSED ? kChunk : 1];  // member lists of the 16 clusters
+  __shared__ int moff[17];
+  __shared__ int any_nonempty;
+
+  const int chunk = blockIdx.x, tile = blockIdx.y, u = blockIdx.z;
+  const int n = unit_length(a.lengths, u / a.heads, a.N);
+  const int k0 = chunk * kChunk;
+  if (k0 >= n) return;
+  const int kn = min(kChunk, n - k0);
+  const int C = a.C;
+  const int j0 = tile * 16;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (tid == 0) any_nonempty = 0;
+  __syncthreads();
+  if (tid < 16 && j0 + tid < C && a.sizes[static_cast<size_t>(u) * C + j0 + tid] > 0) any_nonempty = 1;
+  __syncthreads();
+  if (!any_nonempty) {
+    if constexpr (FUSED)
+      for (int x = tid; x < 16 * D; x += 256)
+        if (j0 + x / D < C) a.qc[(static_cast<size_t>(u) * C + j0) * D + x] = 0.0f;
+    return;
+  }
+
+  const int c = lane & 15, g = lane >> 4;
+  const T* ku = static_cast<const T*>(a.k) + (static_cast<size_t>(u) * a.N + k0) * D;
+  const T* vu = static_cast<const T*>(a.v) + (static_cast<size_t>(u) * a.N + k0) * D;
+  const int nkt = (kn + 15) / 16;
+
+  if constexpr (FUSED) {
+    // ---- member lists (ascending query order) and centroids, Eq. (3) --------
+    int* asg = reinterpret_cast<int*>(logits);  // the logit rows are free until the QK product
+    float* qct = logits + kChunk;               // [16][D]
+    for (int x = tid; x < kn; x += 256) asg[x] = a.assign[static_cast<size_t>(u) * a.N + x];
+    if (tid < 16) moff[tid + 1] = j0 + tid < C ? a.sizes[static_cast<size_t>(u) * C + j0 + tid] : 0;
+    __syncthreads();
+    if (tid == 0) {  // sizes -> offsets
+      int run = 0;
+      for (int r = 0; r < 16; ++r) {
+        const int sz = moff[r + 1];
+        moff[r] = run;
+        run += sz;
+      }
+      moff[16] = run;
+    }
+    __syncthreads();
+    int cnt[4] = {0, 0, 0, 0};
+    for (int base = 0; base < kn; base += 64) {
+      const int i = base + lane;
+      const int ai = i < kn ? asg[i] : -1;
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) {
+        const int r = wave * 4 + rr;
+        const uint64_t m = __ballot(ai == j0 + r);
+        if (ai == j0 + r) mlist[moff[r] + cnt[rr] + __popcll(m & lanemask_lt())] = i;
+        cnt[rr] += __popcll(m);
+      }
+    }
+    wave_lds_sync();
+    // fp64 sums in member order; the first 16 members of all four clusters of
+    // the wave are fetched in one batch
+    constexpr int RPS = 64 / D;
+    constexpr int BATCH = 16 / RPS;  // rows per lane per batch
+    const int t = lane % D, rsub = lane / D;
+    const T* qu = static_cast<const T*>(a.q) + static_cast<size_t>(u) * a.N * D;
+    float x[4][BATCH];
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) {
+      const int r = wave * 4 + rr;
+      const int sz = moff[r + 1] - moff[r];
+#pragma unroll
+      for (int e = 0; e < BATCH; ++e) {
+        const int m = rsub + e * RPS;
+        x[rr][e] = m < sz ? to_f32(qu[static_cast<size_t>(mlist[moff[r] + m]) * D + t]) : 0.0f;
+      }
+    }
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) {
+      const int r = wave * 4 + rr;
+      const int sz = moff[r + 1] - moff[r];
+      const int* ml = mlist + moff[r];
+      double acc = 0.0;
+#pragma unroll
+      for (int e = 0; e < BATCH; ++e) acc += static_cast<double>(x[rr][e]);
+      for (int m0 = 16 + rsub; m0 < sz; m0 += 8 * RPS) {  // larger clusters: eight rows in flight
+        float y[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int m = m0 + e * RPS;
+          y[e] = m < sz ? to_f32(qu[static_cast<size_t>(ml[m]) * D + t]) : 0.0f;
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc += static_cast<double>(y[e]);
+      }
+      if (RPS == 2) acc += lane_xor32(acc);
+      const float val = sz > 0 ? static_cast<float>(acc / static_cast<double>(sz)) : 0.0f;
+      if (lane < D) {
+        qct[r * D + t] = val;
+        if (j0 + r < C) a.qc[(static_cast<size_t>(u) * C + j0 + r) * D + t] = val;
+      }
+    }
+    __syncthreads();
+  }
+
+  // ---- logits of this chunk -------------------------------------------------
+  {
+    float bq[KS];
+    if constexpr (FUSED) {
+      const float* qr = logits + kChunk + c * D + g * KS;
+#pragma unroll
+      for (int s = 0; s < KS; ++s) bq[s] = qr[s];
+      __syncthreads();  // every wave holds its centroid operand before the rows are overwritten
+    } else if (j0 + c < C) {
+      load_row<KS>(a.qc + (static_cast<size_t>(u) * C + j0 + c) * D + g * KS, bq);
+    } else {
+#pragma unroll
+      for (int s = 0; s < KS; ++s) bq[s] = 0.0f;
+    }
+    for (int kt0 = wave; kt0 < nkt; kt0 += 4 * BT) {
+      float ka[BT][KS];
+#pragma unroll
+      for (int b = 0; b < BT; ++b) {
+        const int key = (kt0 + 4 * b) * 16 + c;
+        if (key < kn) {
+          load_row<KS>(ku + static_cast<size_t>(key) * D + g * KS, ka[b]);
+        } else {
+#pragma unroll
+          for (int s = 0; s < KS; ++s) ka[b][s] = 0.0f;
+        }
+      }
+#pragma unroll
+      for (int b = 0; b < BT; ++b) {
+        const int kt = kt0 + 4 * b;
+        if (kt < nkt) {
+          v4f acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int s = 0; s < KS; ++s) acc = mfma_f32_16x16x4(ka[b][s], bq[s], acc);
+          float o[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) o[i] = (kt * 16 + 4 * g + i < kn) ? acc[i] * a.scale : -INFINITY;
+          *reinterpret_cast<float4*>(&logits[c * kLStride + kt * 16 + 4 * g]) = make_float4(o[0], o[1], o[2], o[3]);
+        }
+      }
+    }
+  }
+  __syncthreads();
+
+  // ---- per-row maximum, normaliser and top-k (wave w owns rows 4w..4w+3) ------
+  const int kk = min(a.topk, kn);
+  for (int rr = 0; rr < 4; ++rr) {
+    const int r = wave * 4 + rr;
+    const int j = j0 + r;
+    float* row = &logits[r * kLStride];
+    float mx, z;
+    const int jsize = !(IMPROVED && j < C) ? 0
+                      : FUSED ? moff[r + 1] - moff[r] : a.sizes[static_cast<size_t>(u) * C + j];
+    if (IMPROVED && j < C && jsize == 0) {
+      // empty cluster: no top-k set, no mass
+      const size_t uj = static_cast<size_t>(u) * C + j;
+      if constexpr (FUSED) {
+        for (int x = lane; x < a.topk; x += 64) a.topk_out[uj * a.topk + x] = -1;
+        if (lane == 0) {
+          a.mass[uj] = 0.0f;
+          tcnt[r] = 0;
+          rowmass[r] = 0.0f;
+        }
+      } else {
+        const size_t cb = (uj * a.nchunk + chunk) * a.topk;
+        for (int x = lane; x < a.topk; x += 64) {
+          a.cand_idx[cb + x] = -1;
+          a.cand_val[cb + x] = -INFINITY;
+        }
+      }
+      mx = 0.0f;
+      z = 1.0f;
+    } else if (IMPROVED && j < C) {
+      const size_t uj = static_cast<size_t>(u) * C + j;
+      int* sel = selout[wave];
+      int cnt;
+      if (FUSED && a.topk_in != nullptr) {
+        // caller-supplied set: entries until the first negative or out-of-range one
+        const int32_t* tin = a.topk_in + uj * a.topk;
+        float m1 = -INFINITY;
+        for (int x = lane; x < kn; x += 64) m1 = fmaxf(m1, row[x]);
+        mx = wave_max(m1);
+        float zz = 0.0f;
+        for (int x = lane; x < kn; x += 64) zz += __expf(row[x] - mx);
+        z = wave_sum(zz);
+        cnt = 0;
+        while (cnt < a.topk && tin[cnt] >= 0 && tin[cnt] < kn) ++cnt;
+        for (int x = lane; x < cnt; x += 64) sel[x] = tin[x];
+        wave_lds_sync();
+      } else {
+        cnt = wave_topk_row<kCandCap>(row, kn, kk, cscr[wave], sel, &mx, &z);
+      }
+      if constexpr (FUSED) {
+        // mass of T, then mask T out of the row so that P V gives the rest part
+        float msum = 0.0f;
+        for (int x = lane; x < cnt; x += 64) msum += __expf(row[sel[x]] - mx);
+        msum = wave_sum(msum) / z;
+        wave_lds_sync();
+        for (int x = lane; x < cnt; x += 64) {
+          tpos16[r][x] = static_cast<uint16_t>(sel[x]);
+          row[sel[x]] = -INFINITY;
+        }
+        for (int x = lane; x < a.topk; x += 64) a.topk_out[uj * a.topk + x] = x < cnt ? sel[x] : -1;
+        if (lane == 0) {
+          rowmass[r] = msum;
+          tcnt[r] = cnt;
+          a.mass[uj] = msum;
+        }
+      } else {
+        const size_t cb = (uj * a.nchunk + chunk) * a.topk;
+        for (int x = lane; x < a.topk; x += 64) {
+          const bool ok = x < cnt;
+          const int pos = ok ? sel[x] : 0;
+          a.cand_idx[cb + x] = ok ? k0 + pos : -1;
+          a.cand_val[cb + x] = ok ? row[pos] : -INFINITY;
+        }
+      }
+      wave_lds_sync();
+    } else {
+      float m1 = -INFINITY;
+      for (int x = lane; x < kn; x += 64) m1 = fmaxf(m1, row[x]);
+      mx = wave_max(m1);
+      float zz = 0.0f;
+      for (int x = lane; x < kn; x += 64) zz += __expf(row[x] - mx);
+      z = wave_sum(zz);
+    }
+    if (lane == 0) {
+      rowm[r] = mx;
+      rowz[r] = z;
+    }
+  }
+  __syncthreads();
+
+  // ---- values: O^T = V^T P^T (P = exp(S - m), T masked in the fused improved case)
+  v4f oacc[DT];
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt) oacc[dt] = v4f{0.f, 0.f, 0.f, 0.f};
+  {
+    const float mc = rowm[c];
+    for (int kt0 = wave; kt0 < nkt; kt0 += 4 * BT) {
+      float va[BT][4][DT];
+#pragma unroll
+      for (int b = 0; b < BT; ++b)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int key = (kt0 + 4 * b) * 16 + 4 * g + i;
+          if (key < kn) {
+            load_vec<DT>(vu + static_cast<size_t>(key) * D + DT * c, va[b][i]);
+          } else {
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) va[b][i][dt] = 0.0f;
+          }
+        }
+#pragma unroll
+      for (int b = 0; b < BT; ++b) {
+        const int kt = kt0 + 4 * b;
+        if (kt < nkt) {
+          const float4 s4 = *reinterpret_cast<const float4*>(&logits[c * kLStride + kt * 16 + 4 * g]);
+          const float p[4] = {__expf(s4.x - mc), __expf(s4.y - mc), __expf(s4.z - mc), __expf(s4.w - mc)};
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) oacc[dt] = mfma_f32_16x16x4(va[b][i][dt], p[i], oacc[dt]);
+        }
+      }
+    }
+  }
+  __syncthreads();  // logits are dead from here on: reuse them
+  float* red = logits;                 // [4 waves][16 centroids][D]
+  float* vhat = logits + 4 * 16 * D;   // [16][D]
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) red[(wave * 16 + c) * D + DT * (4 * g + i) + dt] = oacc[dt][i];
+  __syncthreads();
+  for (int x = tid; x < 16 * D; x += 256) {
+    const int cc = x / D, dim = x % D;
+    const float sum = ((red[(0 * 16 + cc) * D + dim] + red[(1 * 16 + cc) * D + dim]) +
+                       red[(2 * 16 + cc) * D + dim]) + red[(3 * 16 + cc) * D + dim];
+    if (j0 + cc >= C) continue;
+    const size_t ujc = static_cast<size_t>(u) * C + j0 + cc;
+    if (FUSED) {
+      const float val = moff[cc + 1] > moff[cc] ? sum / rowz[cc] : 0.0f;
+      vhat[cc * D + dim] = val;
+      a.vcb[ujc * D + dim] = val;
+    } else {
+      const size_t pj = ujc * a.nchunk + chunk;
+      a.pacc[pj * D + dim] = sum;
+      if (dim == 0) {
+        a.pm[pj] = rowm[cc];
+        a.pz[pj] = rowz[cc];
+      }
+    }
+  }
+  if constexpr (FUSED) {
+    __syncthreads();
+
+    // ---- fused outputs: every member row of the 16 clusters ---------------------
+    const T* qu = static_cast<const T*>(a.q) + static_cast<size_t>(u) * a.N * D;
+    T* ou = static_cast<T*>(a.out) + static_cast<size_t>(u) * a.N * D;
+    for (int rr = 0; rr < 4; ++rr) {
+      const int r = wave * 4 + rr;
+      const int j = j0 + r;
+      if (j >= C) break;
+      const int sz = moff[r + 1] - moff[r];
+      if (sz == 0) continue;
+      const int* mem = mlist + moff[r];
+      if constexpr (!IMPROVED) {
+        // Eq. (6): each member row receives V^c_j; a lane writes 4 dims of a row
+        constexpr int LPR = D / 4, RPS = 64 / LPR;
+        const int part = lane % LPR, sub = lane / LPR;
+        const float4 val = *reinterpret_cast<const float4*>(&vhat[r * D + part * 4]);
+        for (int m0 = sub; m0 < sz; m0 += RPS) {
+          const int qrow = mem[m0];
+          store4(ou + static_cast<size_t>(qrow) * D + part * 4, val.x, val.y, val.z, val.w);
+        }
+      } else {
+        // T of this cluster as int positions for the sparse routine (reuse selout)
+        int* tposi = selout[wave];
+        const int cnt = tcnt[r];
+        for (int x = lane; x < cnt; x += 64) tposi[x] = tpos16[r][x];
+        wave_lds_sync();
+        sparse_cluster<D, T, NKT>(tposi, cnt, rowmass[r], &vhat[r * D], mem, sz, qu, ku, vu, ou,
+                                  a.scale);
+        wave_lds_sync();
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Merge of the chunks (several chunks only).
+// ---------------------------------------------------------------------------
+template <int D, typename T, bool IMPROVED>
+__global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
+  __shared__ int cscr[4][2 * kCandCap];  // per-wave top-k scratch
+  __shared__ int selout[4][128];
   __shared__ float selval[4][128];
   __shared__ float vcs[4][D];
   const int u = blockIdx.y, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int C = a.C;
   const int j = blockIdx.x * 4 + wave;
   if (j >= C) return;
   const size_t uj = static_cast<size_t>(u) * C + j;
-  const int sz = sizes[uj];
+  const int sz = a.sizes[uj];
   if (sz == 0) {
-    for (int x = lane; x < D; x += 64) vcb[uj * D + x] = 0.0f;
-    if (TOPK) {
-      for (int x = lane; x < topk; x += 64) topk_out[uj * topk + x] = -1;
-      if (lane == 0) mass[uj] = 0.0f;
+    for (int x = lane; x < D; x += 64) a.vcb[uj * D + x] = 0.0f;
+    if (IMPROVED) {
+      for (int x = lane; x < a.topk; x += 64) a.topk_out[uj * a.topk + x] = -1;
+      if (lane == 0) a.mass[uj] = 0.0f;
     }
     return;
   }
-  const int n = unit_length(lengths, u / heads, N);
+  const int n = unit_length(a.lengths, u / a.heads, a.N);
   const int nch = (n + kChunk - 1) / kChunk;
-  const float* pmj = pm + uj * nchunk;
-  const float* pzj = pz + uj * nchunk;
+  const float* pmj = a.pm + uj * a.nchunk;
+  const float* pzj = a.pz + uj * a.nchunk;
   float M = -INFINITY;
   for (int x = lane; x < nch; x += 64) M = fmaxf(M, pmj[x]);
   M = wave_max(M);
@@ -233,66 +637,93 @@ __global__ __launch_bounds__(256) void centroid_attn_merge_kernel(
   constexpr int RPS = 64 / D;
   const int t = lane % D, r = lane / D;
   float acc = 0.0f;
-  for (int x = r; x < nch; x += RPS) acc += __expf(pmj[x] - M) * pacc[(uj * nchunk + x) * D + t];
-  if (RPS == 2) acc += __shfl_xor(acc, 32);
+  for (int x = r; x < nch; x += RPS) acc += __expf(pmj[x] - M) * a.pacc[(uj * a.nchunk + x) * D + t];
+  if (RPS == 2) acc += lane_xor32(acc);
   const float vc = acc / Z;
-  if (!TOPK) {
-    if (lane < D) vcb[uj * D + t] = vc;
+  if (!IMPROVED) {
+    if (lane < D) a.vcb[uj * D + t] = vc;
     return;
   }
   if (lane < D) vcs[wave][t] = vc;
-  const int kk = min(topk, n);
+  const int kk = min(a.topk, n);
+  const T* ku = static_cast<const T*>(a.k) + static_cast<size_t>(u) * a.N * D;
+  const T* vu = static_cast<const T*>(a.v) + static_cast<size_t>(u) * a.N * D;
   int cnt;
-  if (topk_in != nullptr) {
-    // caller-supplied set: entries until the first negative one; logits recomputed
-    const int32_t* tin = topk_in + uj * topk;
-    const float* qj = qc + uj * D;
-    const T* ku = kmat + static_cast<size_t>(u) * N * D;
+  if (a.topk_in != nullptr) {
+    // caller-supplied set: entries until the first negative or out-of-range one;
+    // their logits are recomputed
+    const int32_t* tin = a.topk_in + uj * a.topk;
+    const float* qj = a.qc + uj * D;
     cnt = 0;
-    while (cnt < topk && tin[cnt] >= 0 && tin[cnt] < n) ++cnt;
+    while (cnt < a.topk && tin[cnt] >= 0 && tin[cnt] < n) ++cnt;
     for (int x = lane; x < cnt; x += 64) {
       const int key = tin[x];
       float dot = 0.0f;
       for (int d = 0; d < D; ++d) dot = fmaf(qj[d], to_f32(ku[static_cast<size_t>(key) * D + d]), dot);
-      selpos[wave][x] = key;
-      selval[wave][x] = dot * scale;
-    }
-  } else if (nch == 1) {
-    cnt = kk;
-    const size_t cb = uj * nchunk * topk;
-    for (int x = lane; x < kk; x += 64) {
-      selpos[wave][x] = cand_idx[cb + x];
-      selval[wave][x] = cand_val[cb + x];
+      selout[wave][x] = key;
+      selval[wave][x] = dot * a.scale;
     }
   } else {
-    const int32_t* ci = cand_idx + uj * nchunk * topk;
-    const float* cv = cand_val + uj * nchunk * topk;
-    const int m = nch * topk;
-    cnt = wave_select_topk([&](int pos) { return ci[pos] >= 0 ? order_key(cv[pos]) : 0u; }, m, kk,
-                           hist[wave], selpos[wave]);
+    const int32_t* ci = a.cand_idx + uj * a.nchunk * a.topk;
+    const float* cv = a.cand_val + uj * a.nchunk * a.topk;
+    float mdummy, zdummy;
+    cnt = wave_topk_row<kCandCap>(cv, nch * a.topk, kk, cscr[wave], selout[wave], &mdummy,
+                                  &zdummy);
     wave_lds_sync();
     for (int x = lane; x < cnt; x += 64) {
-      const int pos = selpos[wave][x];
+      const int pos = selout[wave][x];
       selval[wave][x] = cv[pos];
+      selout[wave][x] = ci[pos];
     }
-    wave_lds_sync();
-    for (int x = lane; x < cnt; x += 64) selpos[wave][x] = ci[selpos[wave][x]];
   }
   wave_lds_sync();
-  // m_j and the top-k part of A^c V
+  // m_j and the top-k part of A^c V (eight value rows in flight per lane group)
   float msum = 0.0f;
   for (int x = lane; x < cnt; x += 64) msum += __expf(selval[wave][x] - M) / Z;
   msum = wave_sum(msum);
-  const T* vu = vmat + static_cast<size_t>(u) * N * D;
   float top = 0.0f;
-  for (int x = r; x < cnt; x += RPS) {
-    const float w = __expf(selval[wave][x] - M) / Z;
-    top += w * to_f32(vu[static_cast<size_t>(selpos[wave][x]) * D + t]);
+  int x = r;
+  for (; x + 7 * RPS < cnt; x += 8 * RPS) {
+    float wv[8], vv[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      wv[e] = __expf(selval[wave][x + e * RPS] - M) / Z;
+      vv[e] = to_f32(vu[static_cast<size_t>(selout[wave][x + e * RPS]) * D + t]);
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) top += wv[e] * vv[e];
   }
-  if (RPS == 2) top += __shfl_xor(top, 32);
-  if (lane < D) vcb[uj * D + t] = vcs[wave][t] - top;
-  for (int x = lane; x < topk; x += 64) topk_out[uj * topk + x] = x < cnt ? selpos[wave][x] : -1;
-  if (lane == 0) mass[uj] = msum;
+  for (; x < cnt; x += RPS)
+    top += (__expf(selval[wave][x] - M) / Z) * to_f32(vu[static_cast<size_t>(selout[wave][x]) * D + t]);
+  if (RPS == 2) top += lane_xor32(top);
+  if (lane < D) a.vcb[uj * D + t] = vcs[wave][t] - top;
+  for (int y = lane; y < a.topk; y += 64) a.topk_out[uj * a.topk + y] = y < cnt ? selout[wave][y] : -1;
+  if (lane == 0) a.mass[uj] = msum;
+}
+
+// ---------------------------------------------------------------------------
+// Improved values for the several-chunk case: one wave per cluster.
+// ---------------------------------------------------------------------------
+template <int D, typename T, int NKT>
+__global__ __launch_bounds__(256) void sparse_kernel(AttnArgs a) {
+  __shared__ int tp[4][128];
+  const int u = blockIdx.y, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int C = a.C;
+  const int j = blockIdx.x * 4 + wave;
+  if (j >= C) return;
+  const size_t uj = static_cast<size_t>(u) * C + j;
+  const int sz = a.sizes[uj];
+  if (sz == 0) return;
+  const int n = unit_length(a.lengths, u / a.heads, a.N);
+  const int kk = min(a.topk, n);
+  for (int x = lane; x < kk; x += 64) tp[wave][x] = a.topk_out[uj * a.topk + x];
+  wave_lds_sync();
+  const int32_t* mem = a.members + static_cast<size_t>(u) * a.N + a.offsets[static_cast<size_t>(u) * (C + 1) + j];
+  const size_t base = static_cast<size_t>(u) * a.N * D;
+  sparse_cluster<D, T, NKT>(tp[wave], kk, a.mass[uj], a.vcb + uj * D, mem, sz,
+                            static_cast<const T*>(a.q) + base, static_cast<const T*>(a.k) + base,
+                            static_cast<const T*>(a.v) + base, static_cast<T*>(a.out) + base,
+                            a.scale);
 }
 
 // ---------------------------------------------------------------------------
@@ -310,37 +741,82 @@ hipError_t launch_centroids(const Problem& p, const Workspace& ws, hipStream_t s
   return p.dtype == 0 ? launch_centroids_t<64, float>(p, ws, s) : launch_centroids_t<64, bf16_t>(p, ws, s);
 }
 
-template <int D, typename T, bool TOPK>
-static hipError_t launch_cattn_t(const Problem& p, const Workspace& ws, const int32_t* topk_in,
-                                 hipStream_t s) {
-  const float scale = 1.0f / sqrtf(static_cast<float>(D));
-  const int tk = TOPK ? p.topk : 1;
+static AttnArgs make_args(const Problem& p, const Workspace& ws, const int32_t* topk_in) {
+  AttnArgs a;
+  a.assign = ws.assign;
+  a.qc = ws.qc;
+  a.sizes = ws.sizes;
+  a.offsets = ws.offsets;
+  a.members = ws.members;
+  a.q = p.q;
+  a.k = p.k;
+  a.v = p.v;
+  a.lengths = p.lengths;
+  a.heads = p.heads;
+  a.N = p.n;
+  a.C = p.C;
+  a.nchunk = ws.nchunk;
+  a.topk = p.topk > 0 ? p.topk : 1;
+  a.scale = 1.0f / sqrtf(static_cast<float>(p.d));
+  a.topk_in = topk_in;
+  a.pm = ws.pm;
+  a.pz = ws.pz;
+  a.pacc = ws.pacc;
+  a.cand_idx = ws.cand_idx;
+  a.cand_val = ws.cand_val;
+  a.topk_out = ws.topk;
+  a.mass = ws.mass;
+  a.vcb = ws.vcb;
+  a.out = p.out;
+  return a;
+}
+
+// Key tiles of the register-resident sparse routine (k <= 16 * NKT).
+static int sparse_tiles(int topk) { return topk <= 16 ? 1 : topk <= 32 ? 2 : topk <= 64 ? 4 : 8; }
+
+template <int D, typename T, int NKT>
+static hipError_t launch_attn_nkt(const Problem& p, const Workspace& ws, const int32_t* topk_in,
+                                  hipStream_t s) {
+  const AttnArgs a = make_args(p, ws, topk_in);
+  const bool improved = p.topk > 0;
   dim3 g1(ws.nchunk, (p.C + 15) / 16, p.units());
-  hipLaunchKernelGGL((centroid_attn_partial_kernel<D, T, TOPK>), g1, dim3(256), 0, s, ws.qc,
-                     ws.sizes, static_cast<const T*>(p.k), static_cast<const T*>(p.v), p.lengths,
-                     p.heads, p.n, p.C, ws.nchunk, tk, scale, ws.pm, ws.pz, ws.pacc, ws.cand_idx,
-                     ws.cand_val);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  if (ws.nchunk == 1) {
+    if (improved)
+      hipLaunchKernelGGL((attn_tile_kernel<D, T, 1, NKT>), g1, dim3(256), 0, s, a);
+    else
+      hipLaunchKernelGGL((attn_tile_kernel<D, T, 0, NKT>), g1, dim3(256), 0, s, a);
+    return hipGetLastError();
+  }
   dim3 g2((p.C + 3) / 4, p.units());
-  hipLaunchKernelGGL((centroid_attn_merge_kernel<D, T, TOPK>), g2, dim3(256), 0, s, ws.qc, ws.sizes,
-                     static_cast<const T*>(p.k), static_cast<const T*>(p.v), p.lengths, p.heads,
-                     p.n, p.C, ws.nchunk, tk, scale, ws.pm, ws.pz, ws.pacc, ws.cand_idx,
-                     ws.cand_val, topk_in, ws.topk, ws.mass, ws.vcb);
+  if (improved) {
+    hipLaunchKernelGGL((attn_tile_kernel<D, T, 3, NKT>), g1, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((attn_merge_kernel<D, T, true>), g2, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((sparse_kernel<D, T, NKT>), g2, dim3(256), 0, s, a);
+  } else {
+    hipLaunchKernelGGL((attn_tile_kernel<D, T, 2, NKT>), g1, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((attn_merge_kernel<D, T, false>), g2, dim3(256), 0, s, a);
+  }
   return hipGetLastError();
 }
 
 template <int D, typename T>
-static hipError_t launch_cattn_d(const Problem& p, const Workspace& ws, const int32_t* topk_in,
+static hipError_t launch_attn_dt(const Problem& p, const Workspace& ws, const int32_t* topk_in,
                                  hipStream_t s) {
-  return p.topk > 0 ? launch_cattn_t<D, T, true>(p, ws, topk_in, s)
-                    : launch_cattn_t<D, T, false>(p, ws, topk_in, s);
+  if (p.topk <= 0) return launch_attn_nkt<D, T, 1>(p, ws, topk_in, s);
+  switch (sparse_tiles(p.topk)) {
+    case 1: return launch_attn_nkt<D, T, 1>(p, ws, topk_in, s);
+    case 2: return launch_attn_nkt<D, T, 2>(p, ws, topk_in, s);
+    case 4: return launch_attn_nkt<D, T, 4>(p, ws, topk_in, s);
+    default: return launch_attn_nkt<D, T, 8>(p, ws, topk_in, s);
+  }
 }
 
+// Centroid attention and everything after it: clustered -> out via Eq. (6),
+// improved -> top-k, mass, rest part and the improved values.
 hipError_t launch_centroid_attention(const Problem& p, const Workspace& ws, const int32_t* topk_in,
                                      hipStream_t s) {
-  if (p.d == 32) return p.dtype == 0 ? launch_cattn_d<32, float>(p, ws, topk_in, s) : launch_cattn_d<32, bf16_t>(p, ws, topk_in, s);
-  return p.dtype == 0 ? launch_cattn_d<64, float>(p, ws, topk_in, s) : launch_cattn_d<64, bf16_t>(p, ws, topk_in, s);
+  if (p.d == 32) return p.dtype == 0 ? launch_attn_dt<32, float>(p, ws, topk_in, s) : launch_attn_dt<32, bf16_t>(p, ws, topk_in, s);
+  return p.dtype == 0 ? launch_attn_dt<64, float>(p, ws, topk_in, s) : launch_attn_dt<64, bf16_t>(p, ws, topk_in, s);
 }
 
 }  // namespace ca

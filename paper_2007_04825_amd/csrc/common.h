@@ -7,6 +7,7 @@ namespace ca {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef float v4f __attribute__((ext_vector_type(4)));
+typedef double v4d __attribute__((ext_vector_type(4)));
 
 constexpr int kWave = 64;
 
@@ -81,16 +82,76 @@ __device__ __forceinline__ int unit_length(const int32_t* __restrict__ lengths, 
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ int lane_id() { return static_cast<int>(threadIdx.x) & (kWave - 1); }
 
-__device__ __forceinline__ float wave_max(float x) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) x = fmaxf(x, __shfl_xor(x, o));
-  return x;
+// Cross-lane moves without the LDS: DPP within 16-lane rows, and the gfx950
+// permlane swaps between rows.  The swaps need two distinct registers, so the
+// source is first copied explicitly.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xf, 0xf, false));
 }
-__device__ __forceinline__ float wave_sum(float x) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o);
-  return x;
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int x) {
+  return __builtin_amdgcn_update_dpp(0, x, CTRL, 0xf, 0xf, false);
 }
+__device__ __forceinline__ unsigned vreg_copy(unsigned x) {
+  unsigned y;
+  asm volatile("v_mov_b32 %0, %1" : "=v"(y) : "v"(x));
+  return y;
+}
+// value of lane (l ^ 32) / (l ^ 16)
+__device__ __forceinline__ unsigned lane_xor32_u(unsigned u) {
+  const auto p = __builtin_amdgcn_permlane32_swap(u, vreg_copy(u), false, false);
+  return (threadIdx.x & 32) ? p[0] : p[1];
+}
+__device__ __forceinline__ unsigned lane_xor16_u(unsigned u) {
+  const auto p = __builtin_amdgcn_permlane16_swap(u, vreg_copy(u), false, false);
+  return (threadIdx.x & 16) ? p[0] : p[1];
+}
+__device__ __forceinline__ float lane_xor32(float x) {
+  return __builtin_bit_cast(float, lane_xor32_u(__builtin_bit_cast(unsigned, x)));
+}
+__device__ __forceinline__ float lane_xor16(float x) {
+  return __builtin_bit_cast(float, lane_xor16_u(__builtin_bit_cast(unsigned, x)));
+}
+__device__ __forceinline__ int lane_xor32(int x) { return static_cast<int>(lane_xor32_u(static_cast<unsigned>(x))); }
+__device__ __forceinline__ double lane_xor32(double x) {
+  const uint64_t u = __builtin_bit_cast(uint64_t, x);
+  const uint64_t lo = lane_xor32_u(static_cast<unsigned>(u));
+  const uint64_t hi = lane_xor32_u(static_cast<unsigned>(u >> 32));
+  return __builtin_bit_cast(double, lo | (hi << 32));
+}
+__device__ __forceinline__ int lane_xor16(int x) { return static_cast<int>(lane_xor16_u(static_cast<unsigned>(x))); }
+
+// Reductions over the 16 lanes of a row (quad swaps, half-row mirror, row
+// mirror); every lane of the row ends with the same value.
+__device__ __forceinline__ float row16_max(float x) {
+  x = fmaxf(x, dpp_f<0xB1>(x));
+  x = fmaxf(x, dpp_f<0x4E>(x));
+  x = fmaxf(x, dpp_f<0x141>(x));
+  return fmaxf(x, dpp_f<0x140>(x));
+}
+__device__ __forceinline__ float row16_sum(float x) {
+  x += dpp_f<0xB1>(x);
+  x += dpp_f<0x4E>(x);
+  x += dpp_f<0x141>(x);
+  return x + dpp_f<0x140>(x);
+}
+// Reductions over lanes c, c+16, c+32, c+48 (one column of an MFMA result).
+__device__ __forceinline__ float cross_rows_max(float x) {
+  x = fmaxf(x, lane_xor16(x));
+  return fmaxf(x, lane_xor32(x));
+}
+__device__ __forceinline__ float cross_rows_sum(float x) {
+  x += lane_xor16(x);
+  return x + lane_xor32(x);
+}
+__device__ __forceinline__ int cross_rows_max(int x) {
+  x = max(x, lane_xor16(x));
+  return max(x, lane_xor32(x));
+}
+// Whole-wave reductions; every lane gets the (bitwise identical) result.
+__device__ __forceinline__ float wave_max(float x) { return cross_rows_max(row16_max(x)); }
+__device__ __forceinline__ float wave_sum(float x) { return cross_rows_sum(row16_sum(x)); }
 __device__ __forceinline__ int wave_sum_i(int x) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o);
@@ -121,6 +182,11 @@ __device__ __forceinline__ uint64_t lanemask_lt() {
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ v4f mfma_f32_16x16x4(float a, float b, v4f c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+// fp64 16x16x4: A and B pair as above, but the result of lane l, register r
+// is element [l / 16 + 4 * r][l % 16].
+__device__ __forceinline__ v4d mfma_f64_16x16x4(double a, double b, v4d c) {
+  return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
 }
 __device__ __forceinline__ v4i mfma_i8_16x16x64(v4i a, v4i b, v4i c) {
   return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);

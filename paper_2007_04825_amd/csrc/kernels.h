@@ -56,21 +56,24 @@ struct Workspace {
 // Carves the workspace; returns the bytes needed (ws may be null to only size it).
 size_t carve_workspace(const Problem& p, void* base, Workspace* ws);
 
+// Hashing; also writes 0 to the output rows past each sequence's length.
 hipError_t launch_hash(const Problem& p, const Workspace& ws, hipStream_t s);
 hipError_t launch_load_codes(const Problem& p, const uint64_t* codes_in, const Workspace& ws,
                              hipStream_t s);
-// K-means; also builds sizes/offsets/members when the one-workgroup path runs.
-// *csr_done tells whether the CSR lists were produced.
-hipError_t launch_kmeans(const Problem& p, const Workspace& ws, hipStream_t s, bool* csr_done);
+// K-means: writes the assignments (and, on the one-workgroup path, the
+// cluster sizes); *lds_path tells whether the one-workgroup path ran.
+hipError_t launch_kmeans(const Problem& p, const Workspace& ws, hipStream_t s, bool* lds_path);
 hipError_t launch_load_assign(const Problem& p, const int32_t* assign_in, const Workspace& ws,
                               hipStream_t s);
 hipError_t launch_csr(const Problem& p, const int32_t* assign, const Workspace& ws, hipStream_t s);
 hipError_t launch_centroids(const Problem& p, const Workspace& ws, hipStream_t s);
+// Centroid attention and, when every sequence fits in one key chunk, the
+// output rows; for longer sequences the improved output rows as well (the
+// clustered ones then come from launch_broadcast).
 hipError_t launch_centroid_attention(const Problem& p, const Workspace& ws, const int32_t* topk_in,
                                      hipStream_t s);
 hipError_t launch_broadcast(const Problem& p, const int32_t* assign, const Workspace& ws,
                             hipStream_t s);
-hipError_t launch_sparse(const Problem& p, const Workspace& ws, hipStream_t s);
 hipError_t launch_pad_zero(const Problem& p, hipStream_t s);
 
 // Which K-means path runs: 0 automatic, 1 one workgroup per unit, 2 multi-workgroup.

@@ -22,8 +22,8 @@
 // Two drivers:
 //  * kmeans_lds_kernel: one 1024-thread workgroup per (batch, head) unit for
 //    n <= 4096; codes, assignments and counts stay in LDS for all L rounds,
-//    only queries whose cluster changed update the counts, and the stable
-//    member lists are written at the end.
+//    only queries whose cluster changed update the counts; it writes the
+//    assignments and the cluster sizes.
 //  * kmeans_assign_kernel + kmeans_reduce_kernel: one launch pair per round
 //    for long sequences; each 1024-query workgroup writes its partial counts
 //    and a reduction kernel forms the next centroids.
@@ -75,9 +75,9 @@ __device__ __forceinline__ v4i query_operand(uint64_t code, int g, const OpMasks
   return r;
 }
 
-// Bits 16g..16g+15 of centroid j as 16 int8: +2 / -2, 0 past n_bits, 127 - j at slot 63.
-__device__ __forceinline__ v4i centroid_operand(uint64_t code, int g, const OpMasks& m, int j) {
-  const uint32_t x = static_cast<uint32_t>(code >> (16 * g)) & 0xffffu;
+// 16 code bits x (bits 16g..16g+15 of centroid j) as 16 int8: +2 / -2, 0 past
+// n_bits, 127 - j at slot 63.
+__device__ __forceinline__ v4i centroid_operand16(uint32_t x, int g, const OpMasks& m, int j) {
   v4i r;
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
@@ -86,6 +86,9 @@ __device__ __forceinline__ v4i centroid_operand(uint64_t code, int g, const OpMa
   }
   if (g == 3) r[3] |= static_cast<int>(static_cast<uint32_t>(static_cast<uint8_t>(127 - j)) << 24);
   return r;
+}
+__device__ __forceinline__ v4i centroid_operand(uint64_t code, int g, const OpMasks& m, int j) {
+  return centroid_operand16(static_cast<uint32_t>(code >> (16 * g)) & 0xffffu, g, m, j);
 }
 
 // Same as query_operand, from a table mapping 8 code bits to 8 int8 entries.
@@ -122,9 +125,38 @@ __device__ __forceinline__ int best_key(const v4i* cop, int nct, v4i bq, int lan
     const v4i d = mfma_i8_16x16x64(cop[ct * 64 + lane], bq, zero);
     best = max(best, max(max(d[0], d[1]), max(d[2], d[3])));
   }
-  best = max(best, __shfl_xor(best, 16));
-  best = max(best, __shfl_xor(best, 32));
+  best = cross_rows_max(best);
   return best;
+}
+
+// Best keys of NG 16-query tiles at once: one centroid-operand load feeds NG
+// independent MFMAs, and the next operand is fetched before they issue.
+template <int NG>
+__device__ __forceinline__ void best_keys(const v4i* cop, int nct, const v4i* bq, int* best, int lane) {
+  const v4i zero = {0, 0, 0, 0};
+  v4i a = cop[lane];
+  for (int ct = 0; ct < nct; ++ct) {
+    const v4i an = cop[(ct + 1 < nct ? ct + 1 : ct) * 64 + lane];
+    v4i d[NG];
+#pragma unroll
+    for (int e = 0; e < NG; ++e) d[e] = mfma_i8_16x16x64(a, bq[e], zero);
+#pragma unroll
+    for (int e = 0; e < NG; ++e) best[e] = max(best[e], max(max(d[e][0], d[e][1]), max(d[e][2], d[e][3])));
+    a = an;
+  }
+#pragma unroll
+  for (int e = 0; e < NG; ++e) {
+    best[e] = cross_rows_max(best[e]);
+  }
+}
+__device__ __forceinline__ void best_keys_n(int ng, const v4i* cop, int nct, const v4i* bq,
+                                            int* best, int lane) {
+  switch (ng) {
+    case 1: best_keys<1>(cop, nct, bq, best, lane); break;
+    case 2: best_keys<2>(cop, nct, bq, best, lane); break;
+    case 3: best_keys<3>(cop, nct, bq, best, lane); break;
+    default: best_keys<4>(cop, nct, bq, best, lane); break;
+  }
 }
 
 // Fills the centroid operands of nct tiles (entries e = ct * 64 + lane).
@@ -153,26 +185,21 @@ struct KmShared {
   int32_t size[kCmax];
   uint64_t cent[kCmax];
   v4i cop[kCmax / 16 * 64];
-  int32_t offs[kCmax + 1];
-  int32_t run[kCmax];
   uint2 qlut[256];
   int nchange;
 };
 
 __global__ __launch_bounds__(kKmThreads) void kmeans_lds_kernel(
     const uint64_t* __restrict__ codes_g, const int32_t* __restrict__ lengths, int heads, int N,
-    int C, int n_bits, int L, int32_t* __restrict__ assign_g, int32_t* __restrict__ sizes_g,
-    int32_t* __restrict__ offsets_g, int32_t* __restrict__ members_g) {
+    int C, int n_bits, int L, int32_t* __restrict__ assign_g, int32_t* __restrict__ sizes_g) {
   __shared__ KmShared sh;
   const int u = blockIdx.x;
   const int n = unit_length(lengths, u / heads, N);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   int32_t* asg = assign_g + static_cast<size_t>(u) * N;
-  int32_t* mem = members_g + static_cast<size_t>(u) * N;
   for (int i = n + tid; i < N; i += kKmThreads) asg[i] = -1;
   if (n == 0) {
     for (int j = tid; j < C; j += kKmThreads) sizes_g[static_cast<size_t>(u) * C + j] = 0;
-    for (int j = tid; j <= C; j += kKmThreads) offsets_g[static_cast<size_t>(u) * (C + 1) + j] = 0;
     return;
   }
   const int ce = C < n ? C : n;
@@ -198,20 +225,28 @@ __global__ __launch_bounds__(kKmThreads) void kmeans_lds_kernel(
   const OpMasks qm = op_masks(g, n_bits);
   __syncthreads();
 
+  build_centroid_operands(sh.cop, sh.cent, ce, nct, n_bits, tid, kKmThreads);
   for (int t = 0; t < L; ++t) {
-    build_centroid_operands(sh.cop, sh.cent, ce, nct, n_bits, tid, kKmThreads);
     if (tid == 0) sh.nchange = 0;
     __syncthreads();
-    // assign
-    for (int s = 0; s < kMaxQt; ++s) {
-      const int qt = wave + s * kKmWaves;
-      if (qt < nqt) {
-        const int qb = qt * 16 + c;
-        const v4i bq = query_operand_lut(qb < n ? sh.codes[qb] : 0ull, g, qm, sh.qlut);
-        const int best = best_key(sh.cop, nct, bq, lane);
-        const int qi = qt * 16 + lane;
+    // assign: up to four query tiles share every centroid-operand load
+    for (int s0 = 0; s0 < kMaxQt; s0 += 4) {
+      const int left = (nqt - wave + kKmWaves - 1) / kKmWaves - s0;  // tiles of this wave not yet done
+      if (left <= 0) break;
+      v4i bq[4];
+      int best[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int qb = (wave + (s0 + e) * kKmWaves) * 16 + c;
+        bq[e] = query_operand_lut(qb < n ? sh.codes[qb] : 0ull, g, qm, sh.qlut);
+        best[e] = INT_MIN;
+      }
+      best_keys_n(left < 4 ? left : 4, sh.cop, nct, bq, best, lane);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int qi = (wave + (s0 + e) * kKmWaves) * 16 + lane;
         if (lane < 16 && qi < n) {
-          const int j = decode_cluster(best, n_bits);
+          const int j = decode_cluster(best[e], n_bits);
           const int old = sh.assign[qi];
           if (j != old) {
             sh.assign[qi] = j;
@@ -246,66 +281,29 @@ __global__ __launch_bounds__(kKmThreads) void kmeans_lds_kernel(
     }
     __syncthreads();
     if (t == L - 1) break;
-    // majority update
-    for (int j = wave; j < ce; j += kKmWaves) {
-      const int sz = sh.size[j];
-      const uint32_t dw = sh.cnt[j * kCntStride + (lane >> 1)];
-      const int field = static_cast<int>((dw >> ((lane & 1) * 16)) & 0xffffu);
-      const uint64_t bits = __ballot(2 * field > sz);
-      if (lane == 0 && sz > 0) sh.cent[j] = bits;
+    // majority update fused with the operand rebuild: thread (tile, lane)
+    // forms the 16 bits of k-group g of centroid j (slots past C_eff copy
+    // centroid 0 with tie byte 255); an empty cluster keeps its operands
+    for (int e = tid; e < nct * 64; e += kKmThreads) {
+      const int j = (e >> 6) * 16 + c;  // e & 63 == lane because the stride is a multiple of 64
+      const int src = j < ce ? j : 0;
+      const int sz = sh.size[src];
+      if (sz == 0) continue;
+      const uint32_t* row = &sh.cnt[src * kCntStride + 8 * g];
+      uint32_t bits16 = 0;
+#pragma unroll
+      for (int w = 0; w < 8; ++w) {
+        const uint32_t dw = row[w];
+        bits16 |= static_cast<uint32_t>(2 * static_cast<int>(dw & 0xffffu) > sz) << (2 * w);
+        bits16 |= static_cast<uint32_t>(2 * static_cast<int>(dw >> 16) > sz) << (2 * w + 1);
+      }
+      sh.cop[e] = centroid_operand16(bits16, g, qm, j < ce ? j : 255);
     }
     __syncthreads();
   }
 
-  // sizes and offsets (exclusive scan over clusters)
-  if (wave == 0) {
-    int running = 0;
-    for (int j0 = 0; j0 < C; j0 += 64) {
-      const int j = j0 + lane;
-      const int v = (j < ce) ? sh.size[j] : 0;
-      const int incl = wave_incl_scan(v);
-      if (j < C) sh.offs[j] = running + incl - v;
-      running += __shfl(incl, 63);
-    }
-    if (lane == 0) sh.offs[C] = running;
-  }
   for (int i = tid; i < n; i += kKmThreads) asg[i] = sh.assign[i];
-  for (int j = tid; j < ce; j += kKmThreads) sh.run[j] = 0;
-  __syncthreads();
   for (int j = tid; j < C; j += kKmThreads) sizes_g[static_cast<size_t>(u) * C + j] = j < ce ? sh.size[j] : 0;
-  for (int j = tid; j <= C; j += kKmThreads) offsets_g[static_cast<size_t>(u) * (C + 1) + j] = sh.offs[j];
-  for (int j = tid; j < ce; j += kKmThreads) sh.run[j] = sh.offs[j];
-
-  // stable member lists, 1024 queries per round
-  for (int r0 = 0; r0 < n; r0 += kKmThreads) {
-    for (int x = tid; x < kKmWaves * ce; x += kKmThreads) sh.scratch[x] = 0;
-    __syncthreads();
-    const int i = r0 + tid;
-    const int a = i < n ? sh.assign[i] : -1;
-    uint64_t active = __ballot(a >= 0);
-    int rank = 0;
-    while (active) {
-      const int leader = __ffsll(static_cast<unsigned long long>(active)) - 1;
-      const int aj = __shfl(a, leader);
-      const uint64_t mm = __ballot(a == aj) & active;
-      if (a == aj) rank = __popcll(mm & lanemask_lt());
-      if (lane == leader) sh.scratch[wave * ce + aj] = __popcll(mm);
-      active &= ~mm;
-    }
-    __syncthreads();
-    if (a >= 0) {
-      int base = sh.run[a];
-      for (int w = 0; w < wave; ++w) base += sh.scratch[w * ce + a];
-      mem[base + rank] = i;
-    }
-    __syncthreads();
-    for (int j = tid; j < ce; j += kKmThreads) {
-      int tot = 0;
-      for (int w = 0; w < kKmWaves; ++w) tot += sh.scratch[w * ce + j];
-      sh.run[j] += tot;
-    }
-    __syncthreads();
-  }
 }
 
 // ===========================================================================
@@ -349,16 +347,23 @@ __global__ __launch_bounds__(kKbThreads) void kmeans_assign_kernel(
   const int g = lane >> 4, c = lane & 15;
   const OpMasks qm = op_masks(g, n_bits);
   const int nqt = (nq + 15) / 16;
-#pragma unroll 4
-  for (int s = 0; s < kMaxQt; ++s) {
-    const int qt = wave + s * kKbWaves;
-    if (qt < nqt) {
-      const int qi = qt * 16 + c;
-      const v4i bq = query_operand(qi < nq ? lcodes[qi] : 0ull, g, qm);
-      const int best = best_key(cop, nct, bq, lane);
-      const int qo = qt * 16 + lane;
+  for (int s0 = 0; s0 < kMaxQt; s0 += 4) {
+    const int left = (nqt - wave + kKbWaves - 1) / kKbWaves - s0;
+    if (left <= 0) break;
+    v4i bq[4];
+    int best[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int qi = (wave + (s0 + e) * kKbWaves) * 16 + c;
+      bq[e] = query_operand(qi < nq ? lcodes[qi] : 0ull, g, qm);
+      best[e] = INT_MIN;
+    }
+    best_keys_n(left < 4 ? left : 4, cop, nct, bq, best, lane);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int qo = (wave + (s0 + e) * kKbWaves) * 16 + lane;
       if (lane < 16 && qo < nq) {
-        const int j = decode_cluster(best, n_bits);
+        const int j = decode_cluster(best[e], n_bits);
         la[qo] = j;
         assign_g[static_cast<size_t>(u) * N + q0 + qo] = j;
       }
@@ -480,7 +485,7 @@ __global__ __launch_bounds__(kCsrBlockQ) void csr_scatter_kernel(
   int rank = 0;
   while (active) {
     const int leader = __ffsll(static_cast<unsigned long long>(active)) - 1;
-    const int aj = __shfl(a, leader);
+    const int aj = __builtin_amdgcn_readlane(a, leader);
     const uint64_t mm = __ballot(a == aj) & active;
     if (a == aj) rank = __popcll(mm & lanemask_lt());
     if (lane == leader) wcnt[wave][aj] = __popcll(mm);
@@ -547,16 +552,15 @@ hipError_t launch_csr(const Problem& p, const int32_t* assign, const Workspace& 
   return hipGetLastError();
 }
 
-hipError_t launch_kmeans(const Problem& p, const Workspace& ws, hipStream_t s, bool* csr_done) {
+hipError_t launch_kmeans(const Problem& p, const Workspace& ws, hipStream_t s, bool* lds_path) {
   const int U = p.units();
   if (kmeans_uses_lds(p)) {
     hipLaunchKernelGGL(kmeans_lds_kernel, dim3(U), dim3(kKmThreads), 0, s, ws.codes, p.lengths,
-                       p.heads, p.n, p.C, p.n_bits, p.L, ws.assign, ws.sizes, ws.offsets,
-                       ws.members);
-    *csr_done = true;
+                       p.heads, p.n, p.C, p.n_bits, p.L, ws.assign, ws.sizes);
+    *lds_path = true;
     return hipGetLastError();
   }
-  *csr_done = false;
+  *lds_path = false;
   uint64_t* cent0 = ws.cent;
   uint64_t* cent1 = ws.cent + static_cast<size_t>(U) * p.C;
   for (int t = 0; t < p.L; ++t) {

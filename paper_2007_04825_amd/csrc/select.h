@@ -63,8 +63,8 @@ __device__ int wave_select_topk(KeyFn key, int m, int kk, int* hist, int* out) {
         above += c[e];
       }
     }
-    bin = __shfl(bin, leader);
-    above = __shfl(above, leader);
+    bin = __builtin_amdgcn_readlane(bin, leader);
+    above = __builtin_amdgcn_readlane(above, leader);
     prefix |= static_cast<uint32_t>(bin) << shift;
     pmask |= 0xffu << shift;
     need -= above;
@@ -86,6 +86,100 @@ __device__ int wave_select_topk(KeyFn key, int m, int kk, int* hist, int* out) {
     written += __popcll(selmask);
     eq_seen += __popcll(eqmask);
   }
+  return written;
+}
+
+// The kk-th largest of the keys held by the wave (k1 in every lane, plus k2
+// when two is set; key 0 stands for "no value"): the largest T with at least
+// kk keys >= T, built one bit at a time from the most significant down with
+// wave ballots (no LDS traffic).  Requires kk <= number of nonzero keys.
+__device__ __forceinline__ uint32_t wave_kth_key(uint32_t k1, uint32_t k2, bool two, int kk) {
+  uint32_t t = 0;
+  for (int bit = 31; bit >= 0; --bit) {
+    const uint32_t cand = t | (1u << bit);
+    int cnt = __popcll(__ballot(k1 >= cand));
+    if (two) cnt += __popcll(__ballot(k2 >= cand));
+    if (cnt >= kk) t = cand;
+  }
+  return t;
+}
+
+// Top-kk (1 <= kk <= 128, kk <= m) of row[0..m) by value, ties to the smaller
+// position, for one wave.  row may live in LDS or global memory.  Writes the
+// chosen positions in ascending order to out[] and returns their number (kk);
+// also returns the row maximum and z = sum_pos exp(row[pos] - max).
+//
+// Each lane keeps the largest (and, for kk > 64, the second largest) value of
+// its strided slice.  The kk-th largest of those values is a threshold tau
+// that at least kk entries reach, so every entry of the top-kk set is >= tau.
+// One more sweep collects the entries >= tau in position order (usually
+// little more than kk of them); the exact kk-th value among them is found by
+// the same bitwise search, and the entries above it plus the first ones equal
+// to it (smallest positions) are kept.  If more than CAP entries reach tau
+// (many ties) the radix selection above runs instead.
+// scratch: 2*CAP ints of LDS private to the wave (candidate values, then
+// candidate positions; the whole area is the radix histogram of the fallback).
+template <int CAP>
+__device__ int wave_topk_row(const float* row, int m, int kk, int* scratch, int* out,
+                             float* mx_out, float* z_out) {
+  static_assert(2 * CAP >= 256 && CAP <= 128, "scratch layout");
+  float* cval = reinterpret_cast<float*>(scratch);
+  int* cpos = scratch + CAP;
+  const int lane = lane_id();
+  float a1 = -INFINITY, a2 = -INFINITY;
+  int have = 0;
+  for (int pos = lane; pos < m; pos += 64) {
+    const float x = row[pos];
+    a2 = fmaxf(a2, fminf(a1, x));
+    a1 = fmaxf(a1, x);
+    ++have;
+  }
+  const float mx = wave_max(a1);
+  const bool two = kk > 64;
+  const uint32_t tau = wave_kth_key(have > 0 ? order_key(a1) : 0u, have > 1 ? order_key(a2) : 0u,
+                                    two, kk);
+  float z = 0.0f;
+  int c = 0;
+  for (int base = 0; base < m; base += 64) {
+    const int pos = base + lane;
+    const bool ok = pos < m;
+    const float x = ok ? row[pos] : -INFINITY;
+    z += ok ? __expf(x - mx) : 0.0f;
+    const bool sel = ok && order_key(x) >= tau;
+    const uint64_t bal = __ballot(sel);
+    const int idx = c + __popcll(bal & lanemask_lt());
+    if (sel && idx < CAP) {
+      cval[idx] = x;
+      cpos[idx] = pos;
+    }
+    c += __popcll(bal);
+  }
+  z = wave_sum(z);
+  *mx_out = mx;
+  *z_out = z;
+  wave_lds_sync();
+  if (c > CAP) {
+    return wave_select_topk([&](int pos) { return order_key(row[pos]); }, m, kk, scratch, out);
+  }
+  const uint32_t kc1 = lane < c ? order_key(cval[lane]) : 0u;
+  const uint32_t kc2 = lane + 64 < c ? order_key(cval[lane + 64]) : 0u;
+  const uint32_t kth = wave_kth_key(kc1, kc2, c > 64, kk);
+  const int need = kk - __popcll(__ballot(kc1 > kth)) - __popcll(__ballot(kc2 > kth));
+  int written = 0, eq_seen = 0;
+#pragma unroll
+  for (int r = 0; r < 2; ++r) {
+    const int i = lane + 64 * r;
+    const uint32_t key = r ? kc2 : kc1;
+    const bool valid = i < c;
+    const bool eq = valid && key == kth;
+    const uint64_t eqmask = __ballot(eq);
+    const bool sel = (valid && key > kth) || (eq && eq_seen + __popcll(eqmask & lanemask_lt()) < need);
+    const uint64_t selmask = __ballot(sel);
+    if (sel) out[written + __popcll(selmask & lanemask_lt())] = cpos[i];
+    written += __popcll(selmask);
+    eq_seen += __popcll(eqmask);
+  }
+  wave_lds_sync();
   return written;
 }
 
