@@ -31,10 +31,12 @@ def rng(config: int, stream: int, extra: int = 0) -> np.random.Generator:
 
 def round_bf16(x: np.ndarray) -> np.ndarray:
     """Round fp32 values to the nearest bf16 value (ties to even); fp32 storage."""
-    x = np.ascontiguousarray(x, dtype=np.float32)
-    u = x.view(np.uint32).astype(np.uint64)
-    r = ((u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000).astype(np.uint32)
-    return r.view(np.float32)
+    u = np.array(x, dtype=np.float32).view(np.uint32)  # a copy
+    lsb = (u >> 16) & np.uint32(1)
+    u += np.uint32(0x7FFF)  # wraps modulo 2^32, like the 64-bit form truncated
+    u += lsb
+    u &= np.uint32(0xFFFF0000)
+    return u.view(np.float32)
 
 
 def hyperplanes(config: int, heads: int, n_bits: int, d: int, extra: int = 0) -> np.ndarray:
@@ -72,7 +74,7 @@ def _mixture(config, B, H, N, d, n_comp, sigma, stream_means=3, stream_labels=4,
     means = rng(config, stream_means, extra).standard_normal((B, H, n_comp, d))
     labels = rng(config, stream_labels, extra).integers(0, n_comp, size=(B, H, N))
     noise = rng(config, stream_noise, extra).standard_normal((B, H, N, d))
-    x = scale * np.take_along_axis(means, labels[..., None].repeat(d, -1), axis=2)
+    x = scale * np.take_along_axis(means, labels[..., None], axis=2)
     return x + sigma * noise
 
 

@@ -1,0 +1,50 @@
+"""GPU parity at the full sizes of the sequence-length sweep (batch 1, 8 heads,
+d 64, N = 2^10 .. 2^15, fp32 and bf16, C 100, L 10, k 32, both variants) and of
+the long-context case (batch 1, 8 heads, N 65536, d 64, bf16, C 200, L 15,
+k 64, improved variant).  These sizes take the several-chunk attention path
+(partial tiles, merge, sparse kernel) and the several-workgroup K-means path.
+
+The oracle computes every output of these workloads (a few seconds each on
+the host cores), so the comparison is element by element, to the same bars as
+the smaller cases: codes, assignments and sizes exact, top-k sets up to near
+ties, outputs within 2e-5 (fp32) or 2e-2 (bf16).
+"""
+import pytest
+
+import gen
+import gpu_util
+from gpu_util import check_end_to_end
+
+pytestmark = pytest.mark.gpu
+
+_W = {}
+
+
+def workload(key):
+    if key not in _W:
+        _W.clear()  # one full-size workload (and its oracle results) resident at a time
+        gpu_util.clear_oracle_cache()
+        if key[0] == "long":
+            _W[key] = gen.make_config(5)
+        else:
+            _W[key] = gen.make_config(3, N=key[1], dtype=key[2])
+    return _W[key]
+
+
+@pytest.fixture(autouse=True)
+def _announce(request):
+    print("\n[gpu test] %s" % request.node.name, flush=True)
+    yield
+
+
+@pytest.mark.parametrize("variant", ["clustered", "iclustered"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("log2n", [10, 11, 12, 13, 14, 15])
+def test_sweep_full_size(log2n, dtype, variant):
+    w = workload(("sweep", 1 << log2n, dtype))
+    check_end_to_end(w, w.topk if variant == "iclustered" else 0)
+
+
+def test_long_context_full_size():
+    w = workload(("long",))
+    check_end_to_end(w, w.topk)

@@ -19,7 +19,7 @@ import pytest
 
 import gen
 import oracle
-from gpu_util import run_gpu, run_oracle, topk_mismatches
+from gpu_util import check_end_to_end, run_gpu, run_oracle, tol, topk_mismatches, valid_mask
 
 pytestmark = pytest.mark.gpu
 
@@ -39,27 +39,6 @@ def workload(name):
     return _W[name]
 
 
-def tol(w):
-    return 2e-5 if w.dtype == "f32" else 2e-2
-
-
-def valid_mask(w):
-    B, H, N, _ = w.q.shape
-    return np.broadcast_to(np.arange(N)[None, None, :] < w.lengths[:, None, None], (B, H, N))
-
-
-def band_bits(w):
-    """Number of (query, plane) projections within 1e-6 of zero."""
-    cnt = 0
-    B, H, N, _ = w.q.shape
-    for b in range(B):
-        n = int(w.lengths[b])
-        for h in range(H):
-            p = w.q[b, h, :n].astype(np.float64) @ w.planes[h].astype(np.float64).T
-            cnt += int(np.sum(np.abs(p) < 1e-6))
-    return cnt
-
-
 @pytest.fixture(autouse=True)
 def _announce(request):
     print("\n[gpu test] %s" % request.node.name, flush=True)
@@ -70,32 +49,7 @@ def _announce(request):
 @pytest.mark.parametrize("variant", ["clustered", "iclustered"])
 def test_end_to_end_parity(name, variant):
     w = workload(name)
-    topk = w.topk if variant == "iclustered" else 0
-    ref = run_oracle(w, topk)
-    got = run_gpu(w, topk)
-    vm = valid_mask(w)
-    nband = band_bits(w)
-    print("band bits: %d" % nband)
-    if nband == 0:
-        assert np.array_equal(got["codes"], ref["codes"]), "hash codes differ"
-    else:
-        assert np.array_equal(got["codes"][vm], ref["codes"][vm]) or nband > 0
-    assert np.array_equal(got["assign"], ref["assign"]), "assignments differ"
-    assert np.array_equal(got["sizes"], ref["sizes"]), "cluster sizes differ"
-    np.testing.assert_allclose(got["centroids"], ref["qc"], rtol=0, atol=2e-6)
-    skip_rows = np.zeros(vm.shape, bool)
-    if topk:
-        diff, bad = topk_mismatches(w, ref, got, topk)
-        print("top-k near-tie differences: %d clusters" % len(diff))
-        assert not bad, "top-k sets differ beyond near ties: %s" % bad[:5]
-        for (b, h, j) in diff:
-            skip_rows[b, h] |= ref["assign"][b, h] == j
-        np.testing.assert_allclose(got["mass"], ref["mass"], rtol=0, atol=1e-5)
-    cmp = vm & ~skip_rows
-    err = np.abs(got["out"] - ref["out"])[cmp].max()
-    print("max abs error: %.3g (tolerance %.0e)" % (err, tol(w)))
-    assert err <= tol(w)
-    assert np.all(got["out"][~vm] == 0), "padded rows must be 0"
+    check_end_to_end(w, w.topk if variant == "iclustered" else 0)
 
 
 @pytest.mark.parametrize("name", ["speech", "encoder", "sweep4096_bf16"])
