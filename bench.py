@@ -57,9 +57,13 @@ class Hip:
         assert self.lib.hipEventRecord(ev, ctypes.c_void_p(stream)) == 0
 
     def elapsed_ms(self, a, b):
+        """Milliseconds between two recorded events; None if they were never
+        recorded (a stage that the call's path does not contain)."""
         assert self.lib.hipEventSynchronize(b) == 0
         ms = ctypes.c_float()
-        assert self.lib.hipEventElapsedTime(ctypes.byref(ms), a, b) == 0
+        if self.lib.hipEventElapsedTime(ctypes.byref(ms), a, b) != 0:
+            self.lib.hipGetLastError()  # clear the error state of the failed query
+            return None
         return float(ms.value)
 
     def destroy(self, ev):
@@ -74,8 +78,12 @@ def stage_work(w, stage, variant_topk):
     nsum = int(w.lengths.astype(np.int64).sum()) * H        # valid queries = valid keys
     s = 4 if w.dtype == "f32" else 2
     if stage == "centroid_attn":
-        # Q^c K^T and A^c V: 2 * C * n * d flops each, per (sequence, head)
+        # Q^c K^T and A^c V: 2 * C * n * d flops each, per (sequence, head); the
+        # improved variant's kernel also does the sparse part, Q_i K_T^T and
+        # A^t V_T: 2 * n * k * d flops each
         flops = 4.0 * w.C * nsum * D
+        if variant_topk:
+            flops += 4.0 * nsum * variant_topk * D
         return flops, "TFLOP/s", "mfma", PEAKS["fp32_mfma_TFLOPs"]
     if stage == "kmeans":
         # L rounds x n x C Hamming distances, each a 64-entry int8 dot product
@@ -96,10 +104,21 @@ def stage_work(w, stage, variant_topk):
     raise ValueError(stage)
 
 
-def cpu_baseline(w, min_seconds=10.0, max_passes=40):
-    """Times the fp64 oracle (both variants) on the same workload."""
+def cpu_threads():
+    """Host threads for the oracle: the CPU share of this process (its affinity
+    mask, capped by OMP_NUM_THREADS when set)."""
+    n = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
+    omp = os.environ.get("OMP_NUM_THREADS", "")
+    if omp.isdigit() and int(omp) > 0:
+        n = min(n, int(omp))
+    return max(n, 1)
+
+
+def cpu_baseline(w, min_seconds=10.0, max_passes=1000):
+    """Times the fp64 oracle (both variants) on the same workload for at
+    least min_seconds."""
     import oracle
-    threads = os.cpu_count() or 1
+    threads = cpu_threads()
     q = np.nan_to_num(w.q, nan=0.0)
     oracle.forward(q[:1], w.k[:1], w.v[:1], w.lengths[:1], w.planes, w.C, w.n_bits, w.L, w.topk,
                    num_threads=threads, exports=False)  # load / warm
@@ -178,6 +197,7 @@ def main():
         for name, sid in ca.STAGES.items():
             for topk in (0, w.topk):
                 acc = 0.0
+                present = True
                 for _ in range(reps):
                     e0, e1 = hip.event(), hip.event()
                     lib = ca.library()
@@ -188,10 +208,15 @@ def main():
                     else:
                         ca.clustered_attention(q, k, v, planes, w.C, w.n_bits, w.L,
                                                lengths=lengths, out=out_c, workspace=ws)
-                    acc += hip.elapsed_ms(e0, e1)
+                    ms = hip.elapsed_ms(e0, e1)
                     hip.destroy(e0)
                     hip.destroy(e1)
-                tot[(name, topk)] = acc / reps
+                    if ms is None:
+                        present = False
+                        break
+                    acc += ms
+                if present:
+                    tot[(name, topk)] = acc / reps
         return tot
 
     for _ in range(args.warmup):

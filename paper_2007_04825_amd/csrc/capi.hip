@@ -136,6 +136,9 @@ static int run_forward(const void* q, const void* k, const void* v, const int32_
   Workspace ws;
   carve_workspace(p, workspace, &ws);
   hipStream_t s = static_cast<hipStream_t>(stream);
+  // launch errors are read with hipGetLastError after each launch: drop a
+  // stale error left by an earlier, unrelated runtime call of this thread
+  (void)hipGetLastError();
 
   hipError_t e = hipSuccess;
 #define CA_TRY(call)                                                                  \
@@ -145,36 +148,42 @@ static int run_forward(const void* q, const void* k, const void* v, const int32_
       return fail(CA_ERR_HIP, "%s failed: %s", #call, hipGetErrorString(e));          \
   } while (0)
 
-  bool lds_path = false;
+  const uint64_t* codes_in = aux ? aux->codes_in : nullptr;
   if (assign_given) {
     CA_TRY(launch_load_assign(p, aux->assign_in, ws, s));
+    CA_TRY(mark(CA_KERNEL_CENTROIDS, true, s));
+    CA_TRY(launch_csr(p, ws.assign, ws, s));
+    CA_TRY(launch_centroids(p, ws, s));
+    CA_TRY(mark(CA_KERNEL_CENTROIDS, false, s));
+  } else if (kmeans_uses_lds(p)) {
+    // one kernel: hashing, K-means, member lists and centroids
+    CA_TRY(mark(CA_KERNEL_KMEANS, true, s));
+    CA_TRY(launch_cluster_lds(p, codes_in, ws, s));
+    CA_TRY(mark(CA_KERNEL_KMEANS, false, s));
   } else {
-    if (aux && aux->codes_in) {
-      CA_TRY(launch_load_codes(p, aux->codes_in, ws, s));
+    if (codes_in) {
+      CA_TRY(launch_load_codes(p, codes_in, ws, s));
     } else {
       CA_TRY(mark(CA_KERNEL_HASH, true, s));
       CA_TRY(launch_hash(p, ws, s));
       CA_TRY(mark(CA_KERNEL_HASH, false, s));
     }
     CA_TRY(mark(CA_KERNEL_KMEANS, true, s));
-    CA_TRY(launch_kmeans(p, ws, s, &lds_path));
+    CA_TRY(launch_kmeans(p, ws, s));
     CA_TRY(mark(CA_KERNEL_KMEANS, false, s));
+    CA_TRY(mark(CA_KERNEL_CENTROIDS, true, s));
+    CA_TRY(launch_csr(p, ws.assign, ws, s));
+    CA_TRY(launch_centroids(p, ws, s));
+    CA_TRY(mark(CA_KERNEL_CENTROIDS, false, s));
   }
-  // A single key chunk lets the centroid-attention kernel build the member
-  // lists and centroids of its clusters itself; it then only needs the sizes.
-  const bool single_chunk = ws.nchunk == 1;
-  CA_TRY(mark(CA_KERNEL_CENTROIDS, true, s));
-  if (!lds_path || !single_chunk) CA_TRY(launch_csr(p, ws.assign, ws, s));
-  if (!single_chunk) CA_TRY(launch_centroids(p, ws, s));
-  CA_TRY(mark(CA_KERNEL_CENTROIDS, false, s));
   CA_TRY(mark(CA_KERNEL_CENTROID_ATTN, true, s));
   CA_TRY(launch_centroid_attention(p, ws, improved && aux ? aux->topk_in : nullptr, s));
   CA_TRY(mark(CA_KERNEL_CENTROID_ATTN, false, s));
   CA_TRY(mark(CA_KERNEL_OUTPUT, true, s));
   if (!improved && ws.nchunk > 1) {
     CA_TRY(launch_broadcast(p, ws.assign, ws, s));  // also zeroes the padded rows
-  } else if (lengths && (assign_given || (aux && aux->codes_in))) {
-    CA_TRY(launch_pad_zero(p, s));  // otherwise the hashing kernel zeroed them
+  } else if (lengths && (assign_given || (codes_in && !kmeans_uses_lds(p)))) {
+    CA_TRY(launch_pad_zero(p, s));  // otherwise the hashing or clustering kernel zeroed them
   }
   CA_TRY(mark(CA_KERNEL_OUTPUT, false, s));
   g_ev_kernel = 0;

@@ -284,12 +284,7 @@ __global__ __launch_bounds__(256) void attn_tile_kernel(AttnArgs a) {
   __syncthreads();
   if (tid < 16 && j0 + tid < C && a.sizes[static_cast<size_t>(u) * C + j0 + tid] > 0) any_nonempty = 1;
   __syncthreads();
-  if (!any_nonempty) {
-    if constexpr (FUSED)
-      for (int x = tid; x < 16 * D; x += 256)
-        if (j0 + x / D < C) a.qc[(static_cast<size_t>(u) * C + j0) * D + x] = 0.0f;
-    return;
-  }
+  if (!any_nonempty) return;
 
   const int c = lane & 15, g = lane >> 4;
   const T* ku = static_cast<const T*>(a.k) + (static_cast<size_t>(u) * a.N + k0) * D;
@@ -297,89 +292,21 @@ __global__ __launch_bounds__(256) void attn_tile_kernel(AttnArgs a) {
   const int nkt = (kn + 15) / 16;
 
   if constexpr (FUSED) {
-    // ---- member lists (ascending query order) and centroids, Eq. (3) --------
-    int* asg = reinterpret_cast<int*>(logits);  // the logit rows are free until the QK product
-    float* qct = logits + kChunk;               // [16][D]
-    for (int x = tid; x < kn; x += 256) asg[x] = a.assign[static_cast<size_t>(u) * a.N + x];
-    if (tid < 16) moff[tid + 1] = j0 + tid < C ? a.sizes[static_cast<size_t>(u) * C + j0 + tid] : 0;
+    // ---- member lists of the 16 clusters (contiguous in the sorted list) ------
+    const int32_t* ou = a.offsets + static_cast<size_t>(u) * (C + 1);
+    if (tid < 17) moff[tid] = ou[min(j0 + tid, C)];
     __syncthreads();
-    if (tid == 0) {  // sizes -> offsets
-      int run = 0;
-      for (int r = 0; r < 16; ++r) {
-        const int sz = moff[r + 1];
-        moff[r] = run;
-        run += sz;
-      }
-      moff[16] = run;
-    }
+    const int m0 = moff[0], mn = moff[16] - m0;
+    const int32_t* mg = a.members + static_cast<size_t>(u) * a.N + m0;
+    for (int x = tid; x < mn; x += 256) mlist[x] = mg[x];
     __syncthreads();
-    int cnt[4] = {0, 0, 0, 0};
-    for (int base = 0; base < kn; base += 64) {
-      const int i = base + lane;
-      const int ai = i < kn ? asg[i] : -1;
-#pragma unroll
-      for (int rr = 0; rr < 4; ++rr) {
-        const int r = wave * 4 + rr;
-        const uint64_t m = __ballot(ai == j0 + r);
-        if (ai == j0 + r) mlist[moff[r] + cnt[rr] + __popcll(m & lanemask_lt())] = i;
-        cnt[rr] += __popcll(m);
-      }
-    }
-    wave_lds_sync();
-    // fp64 sums in member order; the first 16 members of all four clusters of
-    // the wave are fetched in one batch
-    constexpr int RPS = 64 / D;
-    constexpr int BATCH = 16 / RPS;  // rows per lane per batch
-    const int t = lane % D, rsub = lane / D;
-    const T* qu = static_cast<const T*>(a.q) + static_cast<size_t>(u) * a.N * D;
-    float x[4][BATCH];
-#pragma unroll
-    for (int rr = 0; rr < 4; ++rr) {
-      const int r = wave * 4 + rr;
-      const int sz = moff[r + 1] - moff[r];
-#pragma unroll
-      for (int e = 0; e < BATCH; ++e) {
-        const int m = rsub + e * RPS;
-        x[rr][e] = m < sz ? to_f32(qu[static_cast<size_t>(mlist[moff[r] + m]) * D + t]) : 0.0f;
-      }
-    }
-#pragma unroll
-    for (int rr = 0; rr < 4; ++rr) {
-      const int r = wave * 4 + rr;
-      const int sz = moff[r + 1] - moff[r];
-      const int* ml = mlist + moff[r];
-      double acc = 0.0;
-#pragma unroll
-      for (int e = 0; e < BATCH; ++e) acc += static_cast<double>(x[rr][e]);
-      for (int m0 = 16 + rsub; m0 < sz; m0 += 8 * RPS) {  // larger clusters: eight rows in flight
-        float y[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int m = m0 + e * RPS;
-          y[e] = m < sz ? to_f32(qu[static_cast<size_t>(ml[m]) * D + t]) : 0.0f;
-        }
-#pragma unroll
-        for (int e = 0; e < 8; ++e) acc += static_cast<double>(y[e]);
-      }
-      if (RPS == 2) acc += lane_xor32(acc);
-      const float val = sz > 0 ? static_cast<float>(acc / static_cast<double>(sz)) : 0.0f;
-      if (lane < D) {
-        qct[r * D + t] = val;
-        if (j0 + r < C) a.qc[(static_cast<size_t>(u) * C + j0 + r) * D + t] = val;
-      }
-    }
-    __syncthreads();
+    if (tid < 17) moff[tid] -= m0;
   }
 
   // ---- logits of this chunk -------------------------------------------------
   {
     float bq[KS];
-    if constexpr (FUSED) {
-      const float* qr = logits + kChunk + c * D + g * KS;
-#pragma unroll
-      for (int s = 0; s < KS; ++s) bq[s] = qr[s];
-      __syncthreads();  // every wave holds its centroid operand before the rows are overwritten
-    } else if (j0 + c < C) {
+    if (j0 + c < C) {
       load_row<KS>(a.qc + (static_cast<size_t>(u) * C + j0 + c) * D + g * KS, bq);
     } else {
 #pragma unroll

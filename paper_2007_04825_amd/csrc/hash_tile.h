@@ -1,0 +1,214 @@
+// Sign-of-random-projection hashing of one 16-query tile (Section 3.2.2) on
+// the bf16 matrix cores, exact with respect to the fp64 definition.
+//
+// Bit b of the code of query i is [Q_i . P_b > 0], where the projection is the
+// fp64 sum over t = 0..d-1 in that order (each product of two fp32 values is
+// exact in fp64, so the sum is that of a sequential fma chain).
+//
+// Fast path.  The planes are bf16 values (the hash draws them that way), and an
+// fp32 query value splits exactly into three bf16 parts x = hi + mid + lo
+// (truncation: 8 + 8 + 8 significant bits).  v_mfma_f32_16x16x32_bf16 forms
+// the products exactly and accumulates in fp32, so the result S obeys
+//     |S - Q . P| <= 3d * 2^-24 * (1 + 2^-6) * sum_t |Q_t P_t|
+//                <= 2^-16.3 * |Q| |P|            (d <= 64, Cauchy-Schwarz),
+// and a bf16 part flushed as a denormal adds at most 2^-16 * |Q| |P| more.
+// Every sign with |S| > 2^-14 * |Q| |P| is therefore the exact sign; the
+// projections inside that band (about 1e-4 of them for Gaussian data) are
+// recomputed by their lane as the sequential fp64 fma chain, which reproduces
+// the definition bit for bit.  Norms too small or too large for the fp32 test
+// send the projection to the fp64 chain as well.  bf16 queries need only the
+// hi part.
+//
+// Planes that are not bf16 values make every projection take the fp64 chain
+// (correct, slower).
+//
+// Operand layouts (16x16x32 bf16): lane l holds row (l % 16) and the eight
+// consecutive k of group (l / 16); the result lane l, register r holds
+// [4 (l / 16) + r][l % 16].  Rows are queries, columns planes.
+#pragma once
+#include "common.h"
+
+namespace ca {
+
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ v4f mfma_bf16_16x16x32(v4u a, v4u b, v4f c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(v8bf, a),
+                                                 __builtin_bit_cast(v8bf, b), c, 0, 0, 0);
+}
+
+// B operands of the 64 plane columns (four 16-plane tiles) for D/32 k-chunks,
+// and the squared norm of this lane's plane column in each tile.
+template <int D>
+struct PlaneOps {
+  v4u b[D / 32][4];
+  float n2[4];
+};
+
+// Loads the plane operands of one head; returns false in this lane if any
+// plane value it loaded is not a bf16 value.
+template <int D>
+__device__ __forceinline__ bool load_plane_ops(const float* __restrict__ ph, int n_bits, int lane,
+                                               PlaneOps<D>& P) {
+  const int c = lane & 15, g = lane >> 4;
+  uint32_t low = 0;
+  float sq[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int kc = 0; kc < D / 32; ++kc)
+#pragma unroll
+    for (int pt = 0; pt < 4; ++pt) {
+      const int plane = pt * 16 + c;
+      v4u w = {0u, 0u, 0u, 0u};
+      if (plane < n_bits) {
+        const float* pr = ph + static_cast<size_t>(plane) * D + kc * 32 + 8 * g;
+        const float4 x0 = *reinterpret_cast<const float4*>(pr);
+        const float4 x1 = *reinterpret_cast<const float4*>(pr + 4);
+        const uint32_t u[8] = {__float_as_uint(x0.x), __float_as_uint(x0.y), __float_as_uint(x0.z),
+                               __float_as_uint(x0.w), __float_as_uint(x1.x), __float_as_uint(x1.y),
+                               __float_as_uint(x1.z), __float_as_uint(x1.w)};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          low |= u[e] & 0xffffu;
+          sq[pt] = fmaf(__uint_as_float(u[e]), __uint_as_float(u[e]), sq[pt]);
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) w[e] = (u[2 * e] >> 16) | (u[2 * e + 1] & 0xffff0000u);
+      }
+      P.b[kc][pt] = w;
+    }
+#pragma unroll
+  for (int pt = 0; pt < 4; ++pt) P.n2[pt] = cross_rows_sum(sq[pt]);
+  return low == 0;
+}
+
+// The projection as defined: fp64 fma chain over t = 0..D-1.
+template <int D, typename T>
+__device__ __forceinline__ double exact_projection(const T* __restrict__ qr, const float* __restrict__ pr) {
+  double p = 0.0;
+  for (int t = 0; t < D; ++t) p = fma(static_cast<double>(to_f32(qr[t])), static_cast<double>(pr[t]), p);
+  return p;
+}
+
+// Query operands of one k-chunk: hi / mid / lo parts, and the sum of squares
+// of the eight values.
+struct QueryOps {
+  v4u hi, mid, lo;
+  float sq;
+};
+__device__ __forceinline__ void split3(float x, uint32_t& h, uint32_t& m, uint32_t& l) {
+  const uint32_t u = __float_as_uint(x);
+  h = u & 0xffff0000u;
+  const float r1 = x - __uint_as_float(h);
+  m = __float_as_uint(r1) & 0xffff0000u;
+  const float r2 = r1 - __uint_as_float(m);
+  l = __float_as_uint(r2) & 0xffff0000u;
+}
+__device__ __forceinline__ QueryOps query_ops(const float* __restrict__ p) {
+  const float4 x0 = *reinterpret_cast<const float4*>(p);
+  const float4 x1 = *reinterpret_cast<const float4*>(p + 4);
+  const float x[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+  QueryOps o;
+  o.sq = 0.0f;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    uint32_t h0, m0, l0, h1, m1, l1;
+    split3(x[2 * e], h0, m0, l0);
+    split3(x[2 * e + 1], h1, m1, l1);
+    o.hi[e] = (h0 >> 16) | h1;
+    o.mid[e] = (m0 >> 16) | m1;
+    o.lo[e] = (l0 >> 16) | l1;
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) o.sq = fmaf(x[e], x[e], o.sq);
+  return o;
+}
+__device__ __forceinline__ QueryOps query_ops(const bf16_t* __restrict__ p) {
+  const uint4 x = *reinterpret_cast<const uint4*>(p);
+  QueryOps o;
+  o.hi = v4u{x.x, x.y, x.z, x.w};
+  o.mid = o.lo = v4u{0u, 0u, 0u, 0u};
+  o.sq = 0.0f;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const float a = __uint_as_float(o.hi[e] << 16), b = __uint_as_float(o.hi[e] & 0xffff0000u);
+    o.sq = fmaf(a, a, fmaf(b, b, o.sq));
+  }
+  return o;
+}
+
+// Code of query row0 + (lane % 16) for lanes 0..15 (other lanes: unspecified).
+// qu: the unit's query rows; nq: valid rows from row0 (>= 1); ph: the head's
+// planes [n_bits][D]; exact_all: planes are not bf16 values.
+template <int D, typename T>
+__device__ uint64_t hash_tile(const T* __restrict__ qu, int row0, int nq,
+                              const float* __restrict__ ph, int n_bits, const PlaneOps<D>& P,
+                              bool exact_all, int lane) {
+  const int c = lane & 15, g = lane >> 4;
+  v4f s[4];
+#pragma unroll
+  for (int pt = 0; pt < 4; ++pt) s[pt] = v4f{0.f, 0.f, 0.f, 0.f};
+  float qsq = 0.0f;
+  if (!exact_all) {
+    const T* qr = qu + static_cast<size_t>(row0 + (c < nq ? c : 0)) * D + 8 * g;
+#pragma unroll
+    for (int kc = 0; kc < D / 32; ++kc) {
+      QueryOps o = query_ops(qr + kc * 32);
+      if (c >= nq) o.hi = o.mid = o.lo = v4u{0u, 0u, 0u, 0u};
+      qsq += o.sq;
+#pragma unroll
+      for (int pt = 0; pt < 4; ++pt) {
+        s[pt] = mfma_bf16_16x16x32(o.hi, P.b[kc][pt], s[pt]);
+        if constexpr (sizeof(T) == 4) {
+          s[pt] = mfma_bf16_16x16x32(o.mid, P.b[kc][pt], s[pt]);
+          s[pt] = mfma_bf16_16x16x32(o.lo, P.b[kc][pt], s[pt]);
+        }
+      }
+    }
+  }
+  // |Q|^2 of row c in every lane of column c; lane (c, g) needs rows 4g + r
+  qsq = cross_rows_sum(qsq);
+  float qn2[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) qn2[r] = __shfl(qsq, 4 * g + r);
+  // signs as lane bit masks, bit 4 pt + r; projections inside the band are
+  // recomputed afterwards (rare, divergent)
+  uint32_t posm = 0, uncm = 0;
+#pragma unroll
+  for (int pt = 0; pt < 4; ++pt) {
+    const int plane = pt * 16 + c;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int qq = 4 * g + r;
+      const bool valid = plane < n_bits && qq < nq;
+      const float sv = s[pt][r];
+      const float np = qn2[r] * P.n2[pt];
+      const bool sure = np >= 0x1p-90f && np < 0x1p+100f && sv * sv > 0x1p-28f * np;
+      posm |= static_cast<uint32_t>(valid && sv > 0.0f) << (4 * pt + r);
+      uncm |= static_cast<uint32_t>(valid && (exact_all || !sure)) << (4 * pt + r);
+    }
+  }
+  if (__ballot(uncm != 0u) != 0ull) {
+    uint32_t m = uncm;
+    while (m != 0u) {
+      const int k = __ffs(m) - 1;
+      m &= m - 1;
+      const int pt = k >> 2, r = k & 3;
+      const double p = exact_projection<D, T>(qu + static_cast<size_t>(row0 + 4 * g + r) * D,
+                                              ph + static_cast<size_t>(pt * 16 + c) * D);
+      posm = p > 0.0 ? (posm | (1u << k)) : (posm & ~(1u << k));
+    }
+  }
+  uint64_t code = 0;
+#pragma unroll
+  for (int pt = 0; pt < 4; ++pt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const uint64_t bl = __ballot((posm >> (4 * pt + r)) & 1u);
+      // query qq' = 4 g' + r of the tile sits in field g' of this ballot
+      if (r == (lane & 3)) code |= ((bl >> (16 * ((lane >> 2) & 3))) & 0xffffull) << (16 * pt);
+    }
+  return code;
+}
+
+}  // namespace ca

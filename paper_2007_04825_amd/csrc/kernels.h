@@ -60,9 +60,13 @@ size_t carve_workspace(const Problem& p, void* base, Workspace* ws);
 hipError_t launch_hash(const Problem& p, const Workspace& ws, hipStream_t s);
 hipError_t launch_load_codes(const Problem& p, const uint64_t* codes_in, const Workspace& ws,
                              hipStream_t s);
-// K-means: writes the assignments (and, on the one-workgroup path, the
-// cluster sizes); *lds_path tells whether the one-workgroup path ran.
-hipError_t launch_kmeans(const Problem& p, const Workspace& ws, hipStream_t s, bool* lds_path);
+// One workgroup per unit (n <= kKmLdsMaxN): hashing (or the given codes),
+// K-means, member lists (sizes, offsets, members) and centroids; also zeroes
+// the output rows past each sequence's length.
+hipError_t launch_cluster_lds(const Problem& p, const uint64_t* codes_in, const Workspace& ws,
+                              hipStream_t s);
+// Multi-workgroup K-means on ws.codes: writes the assignments of valid rows.
+hipError_t launch_kmeans(const Problem& p, const Workspace& ws, hipStream_t s);
 hipError_t launch_load_assign(const Problem& p, const int32_t* assign_in, const Workspace& ws,
                               hipStream_t s);
 hipError_t launch_csr(const Problem& p, const int32_t* assign, const Workspace& ws, hipStream_t s);

@@ -30,6 +30,7 @@
 #include <limits.h>
 
 #include "common.h"
+#include "hash_tile.h"
 #include "kernels.h"
 
 namespace ca {
@@ -189,26 +190,74 @@ struct KmShared {
   int nchange;
 };
 
-__global__ __launch_bounds__(kKmThreads) void kmeans_lds_kernel(
-    const uint64_t* __restrict__ codes_g, const int32_t* __restrict__ lengths, int heads, int N,
-    int C, int n_bits, int L, int32_t* __restrict__ assign_g, int32_t* __restrict__ sizes_g) {
+struct FrontArgs {
+  const void* q;
+  const float* planes;
+  const uint64_t* codes_in;  // caller-supplied codes, or null to hash
+  const int32_t* lengths;
+  int heads, N, C, n_bits, L;
+  uint64_t* codes;    // [U][N]
+  int32_t* assign;    // [U][N]
+  int32_t* sizes;     // [U][C]
+  int32_t* offsets;   // [U][C+1]
+  int32_t* members;   // [U][N]
+  float* qc;          // [U][C][D]
+  void* out;          // zeroed past each sequence's length when not null
+};
+
+// One workgroup per unit runs the whole clustering: hashing (or loading the
+// given codes), L K-means rounds with everything resident in LDS, the
+// cluster-sorted member lists and the centroids (Eq. 3).
+template <int D, typename T>
+__global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
   __shared__ KmShared sh;
   const int u = blockIdx.x;
-  const int n = unit_length(lengths, u / heads, N);
+  const int N = f.N, C = f.C, n_bits = f.n_bits;
+  const int n = unit_length(f.lengths, u / f.heads, N);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  int32_t* asg = assign_g + static_cast<size_t>(u) * N;
-  for (int i = n + tid; i < N; i += kKmThreads) asg[i] = -1;
+  const size_t row0 = static_cast<size_t>(u) * N;
+  for (int i = n + tid; i < N; i += kKmThreads) {
+    f.assign[row0 + i] = -1;
+    f.codes[row0 + i] = 0;
+  }
+  if (f.out != nullptr) {
+    T* ou = static_cast<T*>(f.out) + row0 * D;
+    for (int x = n * (D / 4) + tid; x < N * (D / 4); x += kKmThreads)
+      store4(ou + static_cast<size_t>(x) * 4, 0.f, 0.f, 0.f, 0.f);
+  }
   if (n == 0) {
-    for (int j = tid; j < C; j += kKmThreads) sizes_g[static_cast<size_t>(u) * C + j] = 0;
+    for (int j = tid; j < C; j += kKmThreads) f.sizes[static_cast<size_t>(u) * C + j] = 0;
+    for (int j = tid; j <= C; j += kKmThreads) f.offsets[static_cast<size_t>(u) * (C + 1) + j] = 0;
+    for (int x = tid; x < C * D; x += kKmThreads) f.qc[static_cast<size_t>(u) * C * D + x] = 0.f;
     return;
   }
   const int ce = C < n ? C : n;
   const int nct = (ce + 15) / 16;
   const int nqt = (n + 15) / 16;
-  for (int i = tid; i < n; i += kKmThreads) {
-    sh.codes[i] = codes_g[static_cast<size_t>(u) * N + i];
-    sh.assign[i] = -1;
+  const T* qu = static_cast<const T*>(f.q) + row0 * D;
+
+  // ---- codes -----------------------------------------------------------------
+  if (f.codes_in != nullptr) {
+    const uint64_t mask = (1ull << n_bits) - 1;  // n_bits <= 63
+    for (int i = tid; i < n; i += kKmThreads) {
+      const uint64_t x = f.codes_in[row0 + i] & mask;
+      sh.codes[i] = x;
+      f.codes[row0 + i] = x;
+    }
+  } else {
+    const float* ph = f.planes + static_cast<size_t>(u % f.heads) * n_bits * D;
+    PlaneOps<D> P;
+    const bool exact_all = __syncthreads_or(!load_plane_ops<D>(ph, n_bits, lane, P)) != 0;
+    for (int tile = wave; tile < nqt; tile += kKmWaves) {
+      const int r0 = tile * 16;
+      const uint64_t code = hash_tile<D, T>(qu, r0, min(16, n - r0), ph, n_bits, P, exact_all, lane);
+      if (lane < 16 && r0 + lane < n) {
+        sh.codes[r0 + lane] = code;
+        f.codes[row0 + r0 + lane] = code;
+      }
+    }
   }
+  for (int i = tid; i < n; i += kKmThreads) sh.assign[i] = -1;
   for (int x = tid; x < kCmax * kCntStride; x += kKmThreads) sh.cnt[x] = 0;
   for (int j = tid; j < kCmax; j += kKmThreads) sh.size[j] = 0;
   __syncthreads();
@@ -225,8 +274,9 @@ __global__ __launch_bounds__(kKmThreads) void kmeans_lds_kernel(
   const OpMasks qm = op_masks(g, n_bits);
   __syncthreads();
 
+  // ---- K-means ---------------------------------------------------------------
   build_centroid_operands(sh.cop, sh.cent, ce, nct, n_bits, tid, kKmThreads);
-  for (int t = 0; t < L; ++t) {
+  for (int t = 0; t < f.L; ++t) {
     if (tid == 0) sh.nchange = 0;
     __syncthreads();
     // assign: up to four query tiles share every centroid-operand load
@@ -280,7 +330,7 @@ __global__ __launch_bounds__(kKmThreads) void kmeans_lds_kernel(
       }
     }
     __syncthreads();
-    if (t == L - 1) break;
+    if (t == f.L - 1) break;
     // majority update fused with the operand rebuild: thread (tile, lane)
     // forms the 16 bits of k-group g of centroid j (slots past C_eff copy
     // centroid 0 with tie byte 255); an empty cluster keeps its operands
@@ -302,8 +352,90 @@ __global__ __launch_bounds__(kKmThreads) void kmeans_lds_kernel(
     __syncthreads();
   }
 
-  for (int i = tid; i < n; i += kKmThreads) asg[i] = sh.assign[i];
-  for (int j = tid; j < C; j += kKmThreads) sizes_g[static_cast<size_t>(u) * C + j] = j < ce ? sh.size[j] : 0;
+  // ---- member lists, ascending query order per cluster -------------------------
+  int32_t* off = reinterpret_cast<int32_t*>(sh.cnt);  // [kCmax + 1], the counts are dead
+  int32_t* mem = sh.scratch;
+  if (wave == 0) {
+    int sz4[4], local = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int j = 4 * lane + e;
+      sz4[e] = j < ce ? sh.size[j] : 0;
+      local += sz4[e];
+    }
+    int run = wave_incl_scan(local) - local;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      off[4 * lane + e] = run;
+      run += sz4[e];
+    }
+    if (lane == 63) off[kCmax] = run;
+  }
+  __syncthreads();
+  // wave w collects clusters w, w + 16, ...; four of them share each pass over
+  // the assignments
+  for (int jb = wave; jb < ce; jb += 4 * kKmWaves) {
+    int cnt[4] = {0, 0, 0, 0};
+    for (int base = 0; base < n; base += 64) {
+      const int i = base + lane;
+      const int ai = i < n ? sh.assign[i] : -1;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int j = jb + e * kKmWaves;
+        const uint64_t m = __ballot(ai == j);
+        if (ai == j) mem[off[j] + cnt[e] + __popcll(m & lanemask_lt())] = i;
+        cnt[e] += __popcll(m);
+      }
+    }
+  }
+  __syncthreads();
+  for (int i = tid; i < n; i += kKmThreads) {
+    f.assign[row0 + i] = sh.assign[i];
+    f.members[row0 + i] = mem[i];
+  }
+  for (int j = tid; j < C; j += kKmThreads) f.sizes[static_cast<size_t>(u) * C + j] = j < ce ? sh.size[j] : 0;
+  for (int j = tid; j <= C; j += kKmThreads)
+    f.offsets[static_cast<size_t>(u) * (C + 1) + j] = j < ce ? off[j] : n;
+
+  // ---- centroids, Eq. (3): fp64 sums in member order -----------------------------
+  // wave w handles clusters w, w + 16, ...; the first rows of the next cluster
+  // are requested before the current one is summed
+  constexpr int RPS = 64 / D;   // rows per wave step
+  constexpr int BATCH = 8;      // rows per lane per request batch
+  const int t = lane % D, rsub = lane / D;
+  auto fetch = [&](int j, int m0, float* x) {
+    const int sz = sh.size[j];
+    const int* ml = mem + off[j];
+#pragma unroll
+    for (int e = 0; e < BATCH; ++e) {
+      const int m = m0 + rsub + e * RPS;
+      x[e] = m < sz ? to_f32(qu[static_cast<size_t>(ml[m]) * D + t]) : 0.0f;
+    }
+  };
+  float xa[BATCH];
+  if (wave < ce) fetch(wave, 0, xa);
+  for (int j = wave; j < ce; j += kKmWaves) {
+    float xb[BATCH];
+#pragma unroll
+    for (int e = 0; e < BATCH; ++e) xb[e] = 0.0f;
+    if (j + kKmWaves < ce) fetch(j + kKmWaves, 0, xb);
+    const int sz = sh.size[j];
+    double acc = 0.0;
+#pragma unroll
+    for (int e = 0; e < BATCH; ++e) acc += static_cast<double>(xa[e]);
+    for (int m0 = BATCH * RPS; m0 < sz; m0 += BATCH * RPS) {
+      float y[BATCH];
+      fetch(j, m0, y);
+#pragma unroll
+      for (int e = 0; e < BATCH; ++e) acc += static_cast<double>(y[e]);
+    }
+    if (RPS == 2) acc += lane_xor32(acc);
+    const float val = sz > 0 ? static_cast<float>(acc / static_cast<double>(sz)) : 0.0f;
+    if (lane < D) f.qc[(static_cast<size_t>(u) * C + j) * D + t] = val;
+#pragma unroll
+    for (int e = 0; e < BATCH; ++e) xa[e] = xb[e];
+  }
+  for (int x = ce * D + tid; x < C * D; x += kKmThreads) f.qc[static_cast<size_t>(u) * C * D + x] = 0.0f;
 }
 
 // ===========================================================================
@@ -552,15 +684,41 @@ hipError_t launch_csr(const Problem& p, const int32_t* assign, const Workspace& 
   return hipGetLastError();
 }
 
-hipError_t launch_kmeans(const Problem& p, const Workspace& ws, hipStream_t s, bool* lds_path) {
+template <int D, typename T>
+static hipError_t launch_cluster_lds_t(const Problem& p, const uint64_t* codes_in,
+                                       const Workspace& ws, hipStream_t s) {
+  FrontArgs f;
+  f.q = p.q;
+  f.planes = p.planes;
+  f.codes_in = codes_in;
+  f.lengths = p.lengths;
+  f.heads = p.heads;
+  f.N = p.n;
+  f.C = p.C;
+  f.n_bits = p.n_bits;
+  f.L = p.L;
+  f.codes = ws.codes;
+  f.assign = ws.assign;
+  f.sizes = ws.sizes;
+  f.offsets = ws.offsets;
+  f.members = ws.members;
+  f.qc = ws.qc;
+  f.out = p.lengths ? p.out : nullptr;
+  hipLaunchKernelGGL((cluster_lds_kernel<D, T>), dim3(p.units()), dim3(kKmThreads), 0, s, f);
+  return hipGetLastError();
+}
+
+hipError_t launch_cluster_lds(const Problem& p, const uint64_t* codes_in, const Workspace& ws,
+                              hipStream_t s) {
+  if (p.d == 32)
+    return p.dtype == 0 ? launch_cluster_lds_t<32, float>(p, codes_in, ws, s)
+                        : launch_cluster_lds_t<32, bf16_t>(p, codes_in, ws, s);
+  return p.dtype == 0 ? launch_cluster_lds_t<64, float>(p, codes_in, ws, s)
+                      : launch_cluster_lds_t<64, bf16_t>(p, codes_in, ws, s);
+}
+
+hipError_t launch_kmeans(const Problem& p, const Workspace& ws, hipStream_t s) {
   const int U = p.units();
-  if (kmeans_uses_lds(p)) {
-    hipLaunchKernelGGL(kmeans_lds_kernel, dim3(U), dim3(kKmThreads), 0, s, ws.codes, p.lengths,
-                       p.heads, p.n, p.C, p.n_bits, p.L, ws.assign, ws.sizes);
-    *lds_path = true;
-    return hipGetLastError();
-  }
-  *lds_path = false;
   uint64_t* cent0 = ws.cent;
   uint64_t* cent1 = ws.cent + static_cast<size_t>(U) * p.C;
   for (int t = 0; t < p.L; ++t) {

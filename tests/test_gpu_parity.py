@@ -208,3 +208,89 @@ def test_invalid_arguments_enqueue_nothing():
     with pytest.raises(ca.ClusteredAttnError) as e:
         ca.clustered_attention(q, q, q, planes, 10)
     assert e.value.code == ca.CA_ERR_UNSUPPORTED
+
+
+def near_orthogonal_queries(w, seed=0):
+    """Every second query of each (sequence, head) is projected off one plane
+    (in fp64, then stored in the workload dtype), so that its projection on
+    that plane is a rounding-level number: the cases where the matrix-core
+    estimate cannot decide the sign and the exact fp64 chain must."""
+    q = w.q.astype(np.float64).copy()
+    B, H, N, _ = q.shape
+    for b in range(B):
+        for h in range(H):
+            p = w.planes[h].astype(np.float64)
+            rows = np.arange(1, N, 2)
+            pl = p[rows % w.n_bits]
+            coef = np.sum(q[b, h, rows] * pl, axis=1) / np.sum(pl * pl, axis=1)
+            q[b, h, rows] -= coef[:, None] * pl
+    q = q.astype(np.float32)
+    return gen.round_bf16(q) if w.dtype == "bf16" else q
+
+
+def in_band_count(w):
+    """Projections the kernels must recompute in fp64: |p| <= 2^-14 |q| |P|."""
+    cnt = 0
+    B, H = w.q.shape[:2]
+    for b in range(B):
+        n = int(w.lengths[b])
+        for h in range(H):
+            qq = w.q[b, h, :n].astype(np.float64)
+            pp = w.planes[h].astype(np.float64)
+            pr = qq @ pp.T
+            lim = 2.0 ** -14 * np.linalg.norm(qq, axis=1)[:, None] * np.linalg.norm(pp, axis=1)[None]
+            cnt += int(np.sum(np.abs(pr) <= lim))
+    return cnt
+
+
+def oracle_codes(w):
+    B, H, N, _ = w.q.shape
+    codes = np.zeros((B, H, N), np.uint64)
+    for b in range(B):
+        n = int(w.lengths[b])
+        for h in range(H):
+            codes[b, h, :n] = oracle.hash_codes(w.q[b, h, :n], w.planes[h])
+    return codes
+
+
+@pytest.mark.parametrize("path", [1, 2])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("d", [32, 64])
+def test_hash_exact_inside_rounding_band(path, dtype, d):
+    """Hash codes equal the oracle's in every bit, including projections too
+    close to zero for the bf16 matrix-core estimate (recomputed in fp64), on
+    both the one-workgroup clustering kernel and the standalone hash kernel."""
+    import dataclasses
+    import paper_2007_04825_amd as ca
+    base = gen.config_sweep(N=1000, B=2, H=2, d=d, dtype=dtype, C=20, L=2, topk=8)
+    w = dataclasses.replace(base, q=near_orthogonal_queries(base), name=base.name + "_orth")
+    nb = in_band_count(w)
+    print("projections inside the band: %d" % nb)
+    assert nb > 100
+    ref = oracle_codes(w)
+    try:
+        ca.set_kmeans_path(path)
+        got = run_gpu(w, 0)
+    finally:
+        ca.set_kmeans_path(0)
+    assert np.array_equal(got["codes"], ref), "codes differ in %d rows" % int(np.sum(got["codes"] != ref))
+
+
+@pytest.mark.parametrize("path", [1, 2])
+def test_hash_planes_not_bf16(path):
+    """Planes that are not bf16 values take the exact fp64 path for every
+    projection; the codes still equal the oracle's."""
+    import dataclasses
+    import paper_2007_04825_amd as ca
+    base = gen.config_tiny(B=1, H=2, N=700, d=64, C=16, L=2, topk=8)
+    g = np.random.Generator(np.random.Philox(np.random.SeedSequence([gen.SEED_ROOT, 1, 70, 0])))
+    planes = g.standard_normal(base.planes.shape).astype(np.float32)
+    assert np.any(planes.view(np.uint32) & 0xFFFF)
+    w = dataclasses.replace(base, planes=planes, name=base.name + "_fp32planes")
+    ref = oracle_codes(w)
+    try:
+        ca.set_kmeans_path(path)
+        got = run_gpu(w, 0)
+    finally:
+        ca.set_kmeans_path(0)
+    assert np.array_equal(got["codes"], ref)
