@@ -41,31 +41,32 @@ __global__ __launch_bounds__(256) void centroid_kernel(const T* __restrict__ q,
                                                        const int32_t* __restrict__ offsets,
                                                        const int32_t* __restrict__ members,
                                                        int N, int C, float* __restrict__ qc) {
-  constexpr int RPS = 64 / D;  // member rows per step
+  // D lanes per cluster (lane = dimension) add the member rows in ascending
+  // query order, one fp64 addition after the other, eight rows in flight
+  constexpr int GPW = 64 / D;  // clusters per wave
   const int u = blockIdx.y, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int j = blockIdx.x * 4 + wave;
+  const int j = (blockIdx.x * 4 + wave) * GPW + lane / D;
+  const int t = lane % D;
   if (j >= C) return;
   const int sz = sizes[static_cast<size_t>(u) * C + j];
   float* dst = qc + (static_cast<size_t>(u) * C + j) * D;
-  const int t = lane % D, r = lane / D;
   if (sz == 0) {
-    if (lane < D) dst[lane] = 0.0f;
+    dst[t] = 0.0f;
     return;
   }
   const int32_t* mem = members + static_cast<size_t>(u) * N + offsets[static_cast<size_t>(u) * (C + 1) + j];
   const T* qu = q + static_cast<size_t>(u) * N * D;
   double acc = 0.0;
-  int m = r;
-  for (; m + 7 * RPS < sz; m += 8 * RPS) {  // eight rows in flight
+  int m = 0;
+  for (; m + 8 <= sz; m += 8) {
     float x[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) x[e] = to_f32(qu[static_cast<size_t>(mem[m + e * RPS]) * D + t]);
+    for (int e = 0; e < 8; ++e) x[e] = to_f32(qu[static_cast<size_t>(mem[m + e]) * D + t]);
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc += static_cast<double>(x[e]);
   }
-  for (; m < sz; m += RPS) acc += static_cast<double>(to_f32(qu[static_cast<size_t>(mem[m]) * D + t]));
-  if (RPS == 2) acc += lane_xor32(acc);
-  if (lane < D) dst[t] = static_cast<float>(acc / static_cast<double>(sz));
+  for (; m < sz; ++m) acc += static_cast<double>(to_f32(qu[static_cast<size_t>(mem[m]) * D + t]));
+  dst[t] = static_cast<float>(acc / static_cast<double>(sz));
 }
 
 // ---------------------------------------------------------------------------
@@ -658,7 +659,9 @@ __global__ __launch_bounds__(256) void sparse_kernel(AttnArgs a) {
 // ---------------------------------------------------------------------------
 template <int D, typename T>
 static hipError_t launch_centroids_t(const Problem& p, const Workspace& ws, hipStream_t s) {
-  hipLaunchKernelGGL((centroid_kernel<D, T>), dim3((p.C + 3) / 4, p.units()), dim3(256), 0, s,
+  constexpr int per_block = 4 * (64 / D);  // clusters per workgroup
+  hipLaunchKernelGGL((centroid_kernel<D, T>), dim3((p.C + per_block - 1) / per_block, p.units()),
+                     dim3(256), 0, s,
                      static_cast<const T*>(p.q), ws.sizes, ws.offsets, ws.members, p.n, p.C, ws.qc);
   return hipGetLastError();
 }

@@ -38,14 +38,22 @@ __global__ __launch_bounds__(kHashThreads) void hash_kernel(const T* __restrict_
   }
   const int nq = min(kHashQB, n - q0);
   if (nq <= 0) return;  // uniform over the workgroup
+  __shared__ __align__(16) float sp[64 * D];
   const float* ph = planes + static_cast<size_t>(h) * n_bits * D;
+  stage_planes<D>(ph, n_bits, sp, tid, kHashThreads);
+  __syncthreads();
   PlaneOps<D> P;
-  const bool exact_all = __syncthreads_or(!load_plane_ops<D>(ph, n_bits, lane, P)) != 0;
+  const bool exact_all = load_plane_ops<D>(sp, n_bits, lane, P);
   const T* qu = q + static_cast<size_t>(u) * N * D;
   const int ntile = (nq + 15) / 16;
-  for (int tile = wave; tile < ntile; tile += kHashThreads / 64) {
+  constexpr int kStep = kHashThreads / 64;
+  TileRaw<D, T> nxt = load_tile<D, T>(qu, q0 + wave * 16, wave < ntile ? min(16, n - q0 - wave * 16) : 0, lane);
+  for (int tile = wave; tile < ntile; tile += kStep) {
     const int r0 = q0 + tile * 16;
-    const uint64_t code = hash_tile<D, T>(qu, r0, min(16, n - r0), ph, n_bits, P, exact_all, lane);
+    const TileRaw<D, T> cur = nxt;
+    const int t2 = tile + kStep;
+    if (t2 < ntile) nxt = load_tile<D, T>(qu, q0 + t2 * 16, min(16, n - q0 - t2 * 16), lane);
+    const uint64_t code = hash_tile<D, T>(qu, cur, r0, min(16, n - r0), sp, n_bits, P, exact_all, lane);
     if (lane < 16 && r0 + lane < n) cu[r0 + lane] = code;
   }
 }

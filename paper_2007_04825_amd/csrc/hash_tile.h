@@ -46,11 +46,25 @@ struct PlaneOps {
   float n2[4];
 };
 
-// Loads the plane operands of one head; returns false in this lane if any
-// plane value it loaded is not a bf16 value.
+// Copies the n_bits planes of one head [n_bits][D] into sp[64][D] (LDS; rows
+// past n_bits are zero) with the threads of the workgroup, so that the waves
+// read their operands from LDS instead of all fetching the same few kilobytes
+// from L2.  The caller synchronises the workgroup before sp is read.
 template <int D>
-__device__ __forceinline__ bool load_plane_ops(const float* __restrict__ ph, int n_bits, int lane,
-                                               PlaneOps<D>& P) {
+__device__ __forceinline__ void stage_planes(const float* __restrict__ ph, int n_bits, float* sp,
+                                             int tid, int nthreads) {
+  for (int x = tid; x < 64 * D / 4; x += nthreads) {
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (x * 4 < n_bits * D) v = *reinterpret_cast<const float4*>(ph + x * 4);
+    *reinterpret_cast<float4*>(sp + x * 4) = v;
+  }
+}
+
+// Builds this lane's plane operands from the staged planes sp[64][D].  The
+// lanes of a wave read every plane value between them; returns true (in every
+// lane) if one of them is not a bf16 value.
+template <int D>
+__device__ __forceinline__ bool load_plane_ops(const float* sp, int n_bits, int lane, PlaneOps<D>& P) {
   const int c = lane & 15, g = lane >> 4;
   uint32_t low = 0;
   float sq[4] = {0.f, 0.f, 0.f, 0.f};
@@ -61,7 +75,7 @@ __device__ __forceinline__ bool load_plane_ops(const float* __restrict__ ph, int
       const int plane = pt * 16 + c;
       v4u w = {0u, 0u, 0u, 0u};
       if (plane < n_bits) {
-        const float* pr = ph + static_cast<size_t>(plane) * D + kc * 32 + 8 * g;
+        const float* pr = sp + plane * D + kc * 32 + 8 * g;
         const float4 x0 = *reinterpret_cast<const float4*>(pr);
         const float4 x1 = *reinterpret_cast<const float4*>(pr + 4);
         const uint32_t u[8] = {__float_as_uint(x0.x), __float_as_uint(x0.y), __float_as_uint(x0.z),
@@ -79,15 +93,45 @@ __device__ __forceinline__ bool load_plane_ops(const float* __restrict__ ph, int
     }
 #pragma unroll
   for (int pt = 0; pt < 4; ++pt) P.n2[pt] = cross_rows_sum(sq[pt]);
-  return low == 0;
+  return __ballot(low != 0u) != 0ull;
 }
 
-// The projection as defined: fp64 fma chain over t = 0..D-1.
+// The projection as defined: fp64 fma chain over t = 0..D-1.  The operands
+// are fetched sixteen dimensions at a time, all loads of a group in flight
+// together.
 template <int D, typename T>
-__device__ __forceinline__ double exact_projection(const T* __restrict__ qr, const float* __restrict__ pr) {
+__device__ __forceinline__ double exact_projection(const T* __restrict__ qr, const float* pr) {
   double p = 0.0;
-  for (int t = 0; t < D; ++t) p = fma(static_cast<double>(to_f32(qr[t])), static_cast<double>(pr[t]), p);
+#pragma unroll 1
+  for (int t0 = 0; t0 < D; t0 += 16) {
+    float x[16], y[16];
+    load_row<16>(qr + t0, x);
+    load_row<16>(pr + t0, y);
+#pragma unroll
+    for (int t = 0; t < 16; ++t) p = fma(static_cast<double>(x[t]), static_cast<double>(y[t]), p);
+  }
   return p;
+}
+
+// Raw query values of one tile as this lane loads them: row row0 + lane % 16,
+// dimensions kc * 32 + 8 (lane / 16) .. + 7 for each k-chunk kc (the next tile
+// is requested while the current one is on the matrix cores).
+template <int D, typename T>
+struct TileRaw {
+  uint4 w[D / 32][sizeof(T) / 2];  // 8 values: two uint4 of fp32, or one of bf16
+};
+template <int D, typename T>
+__device__ __forceinline__ TileRaw<D, T> load_tile(const T* __restrict__ qu, int row0, int nq,
+                                                   int lane) {
+  const int c = lane & 15, g = lane >> 4;
+  TileRaw<D, T> r;
+  const uint4* p = reinterpret_cast<const uint4*>(qu + static_cast<size_t>(row0 + c) * D + 8 * g);
+#pragma unroll
+  for (int kc = 0; kc < D / 32; ++kc)
+#pragma unroll
+    for (int h = 0; h < static_cast<int>(sizeof(T)) / 2; ++h)
+      r.w[kc][h] = c < nq ? p[kc * (32 * static_cast<int>(sizeof(T)) / 16) + h] : make_uint4(0u, 0u, 0u, 0u);
+  return r;
 }
 
 // Query operands of one k-chunk: hi / mid / lo parts, and the sum of squares
@@ -104,10 +148,10 @@ __device__ __forceinline__ void split3(float x, uint32_t& h, uint32_t& m, uint32
   const float r2 = r1 - __uint_as_float(m);
   l = __float_as_uint(r2) & 0xffff0000u;
 }
-__device__ __forceinline__ QueryOps query_ops(const float* __restrict__ p) {
-  const float4 x0 = *reinterpret_cast<const float4*>(p);
-  const float4 x1 = *reinterpret_cast<const float4*>(p + 4);
-  const float x[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+__device__ __forceinline__ QueryOps query_ops(const uint4 (&w)[2]) {
+  const float x[8] = {__uint_as_float(w[0].x), __uint_as_float(w[0].y), __uint_as_float(w[0].z),
+                      __uint_as_float(w[0].w), __uint_as_float(w[1].x), __uint_as_float(w[1].y),
+                      __uint_as_float(w[1].z), __uint_as_float(w[1].w)};
   QueryOps o;
   o.sq = 0.0f;
 #pragma unroll
@@ -123,10 +167,9 @@ __device__ __forceinline__ QueryOps query_ops(const float* __restrict__ p) {
   for (int e = 0; e < 8; ++e) o.sq = fmaf(x[e], x[e], o.sq);
   return o;
 }
-__device__ __forceinline__ QueryOps query_ops(const bf16_t* __restrict__ p) {
-  const uint4 x = *reinterpret_cast<const uint4*>(p);
+__device__ __forceinline__ QueryOps query_ops(const uint4 (&w)[1]) {
   QueryOps o;
-  o.hi = v4u{x.x, x.y, x.z, x.w};
+  o.hi = v4u{w[0].x, w[0].y, w[0].z, w[0].w};
   o.mid = o.lo = v4u{0u, 0u, 0u, 0u};
   o.sq = 0.0f;
 #pragma unroll
@@ -138,11 +181,12 @@ __device__ __forceinline__ QueryOps query_ops(const bf16_t* __restrict__ p) {
 }
 
 // Code of query row0 + (lane % 16) for lanes 0..15 (other lanes: unspecified).
-// qu: the unit's query rows; nq: valid rows from row0 (>= 1); ph: the head's
-// planes [n_bits][D]; exact_all: planes are not bf16 values.
+// qu: the unit's query rows; raw: this tile as loaded by load_tile; nq: valid
+// rows from row0 (>= 1); sp: the staged planes; exact_all: planes are not
+// bf16 values.
 template <int D, typename T>
-__device__ uint64_t hash_tile(const T* __restrict__ qu, int row0, int nq,
-                              const float* __restrict__ ph, int n_bits, const PlaneOps<D>& P,
+__device__ uint64_t hash_tile(const T* __restrict__ qu, const TileRaw<D, T>& raw, int row0, int nq,
+                              const float* sp, int n_bits, const PlaneOps<D>& P,
                               bool exact_all, int lane) {
   const int c = lane & 15, g = lane >> 4;
   v4f s[4];
@@ -150,11 +194,9 @@ __device__ uint64_t hash_tile(const T* __restrict__ qu, int row0, int nq,
   for (int pt = 0; pt < 4; ++pt) s[pt] = v4f{0.f, 0.f, 0.f, 0.f};
   float qsq = 0.0f;
   if (!exact_all) {
-    const T* qr = qu + static_cast<size_t>(row0 + (c < nq ? c : 0)) * D + 8 * g;
 #pragma unroll
     for (int kc = 0; kc < D / 32; ++kc) {
-      QueryOps o = query_ops(qr + kc * 32);
-      if (c >= nq) o.hi = o.mid = o.lo = v4u{0u, 0u, 0u, 0u};
+      const QueryOps o = query_ops(raw.w[kc]);
       qsq += o.sq;
 #pragma unroll
       for (int pt = 0; pt < 4; ++pt) {
@@ -195,7 +237,7 @@ __device__ uint64_t hash_tile(const T* __restrict__ qu, int row0, int nq,
       m &= m - 1;
       const int pt = k >> 2, r = k & 3;
       const double p = exact_projection<D, T>(qu + static_cast<size_t>(row0 + 4 * g + r) * D,
-                                              ph + static_cast<size_t>(pt * 16 + c) * D);
+                                              sp + (pt * 16 + c) * D);
       posm = p > 0.0 ? (posm | (1u << k)) : (posm & ~(1u << k));
     }
   }

@@ -245,12 +245,21 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
       f.codes[row0 + i] = x;
     }
   } else {
+    // the planes are staged in the scratch area (free until the member lists)
+    static_assert(sizeof(sh.scratch) >= 64 * D * sizeof(float), "plane staging");
+    float* sp = reinterpret_cast<float*>(sh.scratch);
     const float* ph = f.planes + static_cast<size_t>(u % f.heads) * n_bits * D;
+    stage_planes<D>(ph, n_bits, sp, tid, kKmThreads);
+    __syncthreads();
     PlaneOps<D> P;
-    const bool exact_all = __syncthreads_or(!load_plane_ops<D>(ph, n_bits, lane, P)) != 0;
+    const bool exact_all = load_plane_ops<D>(sp, n_bits, lane, P);
+    TileRaw<D, T> nxt = load_tile<D, T>(qu, wave * 16, wave < nqt ? min(16, n - wave * 16) : 0, lane);
     for (int tile = wave; tile < nqt; tile += kKmWaves) {
       const int r0 = tile * 16;
-      const uint64_t code = hash_tile<D, T>(qu, r0, min(16, n - r0), ph, n_bits, P, exact_all, lane);
+      const TileRaw<D, T> cur = nxt;
+      const int t2 = tile + kKmWaves;
+      if (t2 < nqt) nxt = load_tile<D, T>(qu, t2 * 16, min(16, n - t2 * 16), lane);
+      const uint64_t code = hash_tile<D, T>(qu, cur, r0, min(16, n - r0), sp, n_bits, P, exact_all, lane);
       if (lane < 16 && r0 + lane < n) {
         sh.codes[r0 + lane] = code;
         f.codes[row0 + r0 + lane] = code;
@@ -279,57 +288,81 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
   for (int t = 0; t < f.L; ++t) {
     if (tid == 0) sh.nchange = 0;
     __syncthreads();
-    // assign: up to four query tiles share every centroid-operand load
+    // assign (up to four query tiles share every centroid-operand load); the
+    // queries whose cluster changed move their bit counts right away
     for (int s0 = 0; s0 < kMaxQt; s0 += 4) {
       const int left = (nqt - wave + kKmWaves - 1) / kKmWaves - s0;  // tiles of this wave not yet done
       if (left <= 0) break;
       v4i bq[4];
       int best[4];
+      uint64_t mycode[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int qb = (wave + (s0 + e) * kKmWaves) * 16 + c;
-        bq[e] = query_operand_lut(qb < n ? sh.codes[qb] : 0ull, g, qm, sh.qlut);
+        mycode[e] = qb < n ? sh.codes[qb] : 0ull;
+        bq[e] = query_operand_lut(mycode[e], g, qm, sh.qlut);
         best[e] = INT_MIN;
       }
       best_keys_n(left < 4 ? left : 4, sh.cop, nct, bq, best, lane);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int qi = (wave + (s0 + e) * kKmWaves) * 16 + lane;
-        if (lane < 16 && qi < n) {
-          const int j = decode_cluster(best[e], n_bits);
-          const int old = sh.assign[qi];
-          if (j != old) {
-            sh.assign[qi] = j;
-            const int pos = atomicAdd(&sh.nchange, 1);
-            sh.scratch[pos] = (qi << 9) | (old + 1);
+      // lane l now decides query (l % 16) of tile l / 16 of the group; the
+      // queries whose cluster changed move their bit counts
+      const int eq = lane >> 4;
+      const int bsel = eq == 0 ? best[0] : eq == 1 ? best[1] : eq == 2 ? best[2] : best[3];
+      const uint64_t code = eq == 0 ? mycode[0] : eq == 1 ? mycode[1] : eq == 2 ? mycode[2] : mycode[3];
+      const int qi = (wave + (s0 + eq) * kKmWaves) * 16 + c;
+      bool chg = false;
+      int j = 0, old = 0;
+      if (eq < left && qi < n) {
+        j = decode_cluster(bsel, n_bits);
+        old = sh.assign[qi];
+        chg = j != old;
+        if (chg) sh.assign[qi] = j;
+      }
+      const uint64_t cmask = __ballot(chg);
+      const int nchg = __popcll(cmask);
+      if (nchg > 32) {
+        // many (the first round): every changed lane moves its own 32 words,
+        // the word order rotated by lane so that the atomics spread over banks
+        if (chg) {
+          if (old >= 0) {
+            atomicSub(&sh.size[old], 1);
+#pragma unroll 4
+            for (int s = 0; s < 32; ++s) {
+              const int w = (s + lane) & 31;
+              atomicSub(&sh.cnt[old * kCntStride + w], pair_val(code, w));
+            }
+          }
+          atomicAdd(&sh.size[j], 1);
+#pragma unroll 4
+          for (int s = 0; s < 32; ++s) {
+            const int w = (s + lane) & 31;
+            atomicAdd(&sh.cnt[j * kCntStride + w], pair_val(code, w));
+          }
+        }
+      } else {
+        // few: one wave-wide atomic per changed query, lanes 0-31 taking its
+        // words out of the old row and lanes 32-63 adding them to the new one
+        uint64_t cm = cmask;
+        while (cm != 0ull) {
+          const int src = __ffsll(static_cast<unsigned long long>(cm)) - 1;
+          cm &= cm - 1;
+          const int row = lane < 32 ? __builtin_amdgcn_readlane(old, src) : __builtin_amdgcn_readlane(j, src);
+          const uint64_t cs =
+              (static_cast<uint64_t>(static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(code >> 32), src))) << 32) |
+              static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(code), src));
+          const int w = lane & 31;
+          const uint32_t pv = pair_val(cs, w);
+          if (row >= 0) {
+            atomicAdd(&sh.cnt[row * kCntStride + w], lane < 32 ? 0u - pv : pv);
+            if (w == 0) atomicAdd(&sh.size[row], lane < 32 ? -1 : 1);
           }
         }
       }
+      if (lane == 0 && nchg > 0) atomicAdd(&sh.nchange, nchg);
     }
     __syncthreads();
-    // counts of the queries whose cluster changed
-    const int nc = sh.nchange;
-    for (int e = tid; e < nc; e += kKmThreads) {
-      const int x = sh.scratch[e];
-      const int qi = x >> 9, old = (x & 511) - 1;
-      const int nw = sh.assign[qi];
-      const uint64_t code = sh.codes[qi];
-      if (old >= 0) {
-        atomicSub(&sh.size[old], 1);
-#pragma unroll 4
-        for (int s = 0; s < 32; ++s) {
-          const int w = (s + lane) & 31;
-          atomicSub(&sh.cnt[old * kCntStride + w], pair_val(code, w));
-        }
-      }
-      atomicAdd(&sh.size[nw], 1);
-#pragma unroll 4
-      for (int s = 0; s < 32; ++s) {
-        const int w = (s + lane) & 31;
-        atomicAdd(&sh.cnt[nw * kCntStride + w], pair_val(code, w));
-      }
-    }
-    __syncthreads();
+    // no query moved: every later round would repeat this assignment
+    if (sh.nchange == 0) break;
     if (t == f.L - 1) break;
     // majority update fused with the operand rebuild: thread (tile, lane)
     // forms the 16 bits of k-group g of centroid j (slots past C_eff copy
@@ -372,15 +405,18 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
     if (lane == 63) off[kCmax] = run;
   }
   __syncthreads();
-  // wave w collects clusters w, w + 16, ...; four of them share each pass over
-  // the assignments
-  for (int jb = wave; jb < ce; jb += 4 * kKmWaves) {
-    int cnt[4] = {0, 0, 0, 0};
+  // wave w collects clusters w, w + 16, ...; eight of them share each pass
+  // over the assignments (the next 64 are read while the current ones are
+  // compared)
+  for (int jb = wave; jb < ce; jb += 8 * kKmWaves) {
+    int cnt[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    int an = lane < n ? sh.assign[lane] : -1;
     for (int base = 0; base < n; base += 64) {
       const int i = base + lane;
-      const int ai = i < n ? sh.assign[i] : -1;
+      const int ai = an;
+      an = i + 64 < n ? sh.assign[i + 64] : -1;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
+      for (int e = 0; e < 8; ++e) {
         const int j = jb + e * kKmWaves;
         const uint64_t m = __ballot(ai == j);
         if (ai == j) mem[off[j] + cnt[e] + __popcll(m & lanemask_lt())] = i;
@@ -397,41 +433,44 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
   for (int j = tid; j <= C; j += kKmThreads)
     f.offsets[static_cast<size_t>(u) * (C + 1) + j] = j < ce ? off[j] : n;
 
-  // ---- centroids, Eq. (3): fp64 sums in member order -----------------------------
-  // wave w handles clusters w, w + 16, ...; the first rows of the next cluster
-  // are requested before the current one is summed
-  constexpr int RPS = 64 / D;   // rows per wave step
-  constexpr int BATCH = 8;      // rows per lane per request batch
-  const int t = lane % D, rsub = lane / D;
+  // ---- centroids, Eq. (3) ---------------------------------------------------------
+  // D lanes per cluster (lane = dimension) add the member rows in ascending
+  // query order, one fp64 addition after the other; groups take clusters
+  // grp, grp + G, ... and request the first rows of their next cluster before
+  // summing the current one
+  constexpr int GPW = 64 / D;        // lane groups per wave
+  constexpr int G = kKmWaves * GPW;  // lane groups per workgroup
+  constexpr int BATCH = 8;           // rows in flight per lane
+  const int t = lane % D, grp = wave * GPW + lane / D;
   auto fetch = [&](int j, int m0, float* x) {
     const int sz = sh.size[j];
     const int* ml = mem + off[j];
 #pragma unroll
     for (int e = 0; e < BATCH; ++e) {
-      const int m = m0 + rsub + e * RPS;
+      const int m = m0 + e;
       x[e] = m < sz ? to_f32(qu[static_cast<size_t>(ml[m]) * D + t]) : 0.0f;
     }
   };
   float xa[BATCH];
-  if (wave < ce) fetch(wave, 0, xa);
-  for (int j = wave; j < ce; j += kKmWaves) {
+  if (grp < ce) fetch(grp, 0, xa);
+  for (int j = grp; j < ce; j += G) {
     float xb[BATCH];
 #pragma unroll
     for (int e = 0; e < BATCH; ++e) xb[e] = 0.0f;
-    if (j + kKmWaves < ce) fetch(j + kKmWaves, 0, xb);
+    if (j + G < ce) fetch(j + G, 0, xb);
     const int sz = sh.size[j];
     double acc = 0.0;
 #pragma unroll
-    for (int e = 0; e < BATCH; ++e) acc += static_cast<double>(xa[e]);
-    for (int m0 = BATCH * RPS; m0 < sz; m0 += BATCH * RPS) {
+    for (int e = 0; e < BATCH; ++e)
+      if (e < sz) acc += static_cast<double>(xa[e]);
+    for (int m0 = BATCH; m0 < sz; m0 += BATCH) {
       float y[BATCH];
       fetch(j, m0, y);
 #pragma unroll
-      for (int e = 0; e < BATCH; ++e) acc += static_cast<double>(y[e]);
+      for (int e = 0; e < BATCH; ++e)
+        if (m0 + e < sz) acc += static_cast<double>(y[e]);
     }
-    if (RPS == 2) acc += lane_xor32(acc);
-    const float val = sz > 0 ? static_cast<float>(acc / static_cast<double>(sz)) : 0.0f;
-    if (lane < D) f.qc[(static_cast<size_t>(u) * C + j) * D + t] = val;
+    f.qc[(static_cast<size_t>(u) * C + j) * D + t] = sz > 0 ? static_cast<float>(acc / static_cast<double>(sz)) : 0.0f;
 #pragma unroll
     for (int e = 0; e < BATCH; ++e) xa[e] = xb[e];
   }
