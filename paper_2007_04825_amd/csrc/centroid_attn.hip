@@ -116,8 +116,8 @@ __device__ __forceinline__ void store_vec(bf16_t* p, const float* s) {
 //                     B = P^T straight from the S^T result registers.
 // Lane (query c, group g) ends with dims DT*4g .. DT*4g + 4*DT - 1 of its row.
 // ---------------------------------------------------------------------------
-template <int D, typename T, int NKT>
-__device__ void sparse_cluster(const int* tpos, int kk, float mh, const float* vb,
+template <int D, typename T, int NKT, typename PosT>
+__device__ void sparse_cluster(const PosT* tpos, int kk, float mh, const float* vb,
                                const int32_t* mem, int sz, const T* __restrict__ qu,
                                const T* __restrict__ ku, const T* __restrict__ vu,
                                T* __restrict__ ou, float scale) {
@@ -138,7 +138,7 @@ __device__ void sparse_cluster(const int* tpos, int kk, float mh, const float* v
 #pragma unroll
   for (int kt = 0; kt < NKT; ++kt) {
     const int slot = kt * 16 + c;
-    const int key = (kt < nkt && slot < kk) ? tpos[slot] : -1;
+    const int key = (kt < nkt && slot < kk) ? static_cast<int>(tpos[slot]) : -1;
     if (key >= 0) {
       load_row<KS>(ku + static_cast<size_t>(key) * D + g * KS, kf[kt]);
     } else {
@@ -148,7 +148,7 @@ __device__ void sparse_cluster(const int* tpos, int kk, float mh, const float* v
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int sl = kt * 16 + 4 * g + i;
-      const int kv = (kt < nkt && sl < kk) ? tpos[sl] : -1;
+      const int kv = (kt < nkt && sl < kk) ? static_cast<int>(tpos[sl]) : -1;
       if (kv >= 0) {
         load_vec<DT>(vu + static_cast<size_t>(kv) * D + DT * c, vf[kt][i]);
       } else {
@@ -228,7 +228,7 @@ __device__ void sparse_cluster(const int* tpos, int kk, float mh, const float* v
 // ---------------------------------------------------------------------------
 // Centroid attention tile kernel.
 // ---------------------------------------------------------------------------
-constexpr int kLStride = kChunk + 4;  // floats per LDS logit row
+constexpr int kLStride = kChunk + 16;  // floats per LDS logit row (the four rows of a wave fall in distinct banks)
 constexpr int kCandCap = 128;
 
 struct AttnArgs {
@@ -257,19 +257,31 @@ struct AttnArgs {
 
 // MODE: 0 clustered single chunk, 1 improved single chunk, 2 clustered
 // partial, 3 improved partial.
+//
+// Row statistics come from where the data already is: while the logits of a
+// key tile sit in the result registers of the first product, each lane (one
+// of the 16 slices of a centroid row: four waves x four lane groups) keeps its
+// running maximum and, for the improved variant, its four largest logits.
+// The row maximum is the maximum of the slice maxima; the normaliser z is the
+// sum of the same exponentials that the second product uses (plus, in the
+// fused improved case, those of T, which the second product leaves out); the
+// top-k threshold is the k-th largest of the slices' kept values (k <= 32;
+// larger k take it from a sweep of the row).
 template <int D, typename T, int MODE, int NKT>
 __global__ __launch_bounds__(256) void attn_tile_kernel(AttnArgs a) {
   constexpr bool IMPROVED = (MODE & 1) != 0;
   constexpr bool FUSED = MODE < 2;
   constexpr int KS = D / 4, DT = D / 16;
   constexpr int BT = 4;  // key tiles per batch of loads
+  constexpr int NT = 4;  // logits each lane keeps per row for the threshold
   __shared__ __align__(16) float logits[16 * kLStride];
-  __shared__ float rowm[16], rowz[16], rowmass[16];
+  __shared__ float rowm[16], rowmass[16], rowtop[16];
   __shared__ int tcnt[16];
-  __shared__ uint16_t tpos16[IMPROVED && FUSED ? 16 : 1][128];
-  __shared__ int cscr[4][2 * kCandCap];  // per-wave top-k scratch
-  __shared__ int selout[4][128];
-  __shared__ int mlist[FUSED ? kChunk : 1];  // member lists of the 16 clusters
+  __shared__ float zpart[4][16];                               // per-wave sums of P per row
+  __shared__ float smax[16][16];                               // [row][slice] maxima
+  __shared__ __align__(16) float stop[IMPROVED ? 16 : 1][16][NT];  // [row][slice] kept logits
+  __shared__ uint16_t tpos16[IMPROVED ? 16 : 1][kCandCap];     // top-k candidates, then T
+  __shared__ int mlist[FUSED ? kChunk : 1];                    // member lists of the 16 clusters
   __shared__ int moff[17];
   __shared__ int any_nonempty;
 
@@ -281,30 +293,39 @@ __global__ __launch_bounds__(256) void attn_tile_kernel(AttnArgs a) {
   const int C = a.C;
   const int j0 = tile * 16;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  if (tid == 0) any_nonempty = 0;
-  __syncthreads();
-  if (tid < 16 && j0 + tid < C && a.sizes[static_cast<size_t>(u) * C + j0 + tid] > 0) any_nonempty = 1;
-  __syncthreads();
-  if (!any_nonempty) return;
-
   const int c = lane & 15, g = lane >> 4;
   const T* ku = static_cast<const T*>(a.k) + (static_cast<size_t>(u) * a.N + k0) * D;
   const T* vu = static_cast<const T*>(a.v) + (static_cast<size_t>(u) * a.N + k0) * D;
   const int nkt = (kn + 15) / 16;
 
+  // ---- sizes (fused: the member offsets of the 16 clusters) -----------------------
   if constexpr (FUSED) {
-    // ---- member lists of the 16 clusters (contiguous in the sorted list) ------
     const int32_t* ou = a.offsets + static_cast<size_t>(u) * (C + 1);
     if (tid < 17) moff[tid] = ou[min(j0 + tid, C)];
     __syncthreads();
-    const int m0 = moff[0], mn = moff[16] - m0;
-    const int32_t* mg = a.members + static_cast<size_t>(u) * a.N + m0;
-    for (int x = tid; x < mn; x += 256) mlist[x] = mg[x];
+    if (moff[16] == moff[0]) return;  // every cluster of the tile is empty
+  } else {
+    if (tid == 0) any_nonempty = 0;
     __syncthreads();
-    if (tid < 17) moff[tid] -= m0;
+    if (tid < 16 && j0 + tid < C && a.sizes[static_cast<size_t>(u) * C + j0 + tid] > 0) any_nonempty = 1;
+    __syncthreads();
+    if (!any_nonempty) return;
+  }
+  // member lists are requested now and stored after the first product
+  int mreg[kChunk / 256];
+  int m0 = 0, mn = 0;
+  if constexpr (FUSED) {
+    m0 = moff[0];
+    mn = moff[16] - m0;
+    const int32_t* mg = a.members + static_cast<size_t>(u) * a.N + m0;
+#pragma unroll
+    for (int e = 0; e < kChunk / 256; ++e) {
+      const int x = tid + 256 * e;
+      mreg[e] = x < mn ? mg[x] : 0;
+    }
   }
 
-  // ---- logits of this chunk -------------------------------------------------
+  // ---- logits of this chunk, with the slice statistics -------------------------------
   {
     float bq[KS];
     if (j0 + c < C) {
@@ -313,6 +334,10 @@ __global__ __launch_bounds__(256) void attn_tile_kernel(AttnArgs a) {
 #pragma unroll
       for (int s = 0; s < KS; ++s) bq[s] = 0.0f;
     }
+    float lmax = -INFINITY;
+    float top[NT];
+#pragma unroll
+    for (int e = 0; e < NT; ++e) top[e] = -INFINITY;
     for (int kt0 = wave; kt0 < nkt; kt0 += 4 * BT) {
       float ka[BT][KS];
 #pragma unroll
@@ -334,100 +359,122 @@ __global__ __launch_bounds__(256) void attn_tile_kernel(AttnArgs a) {
           for (int s = 0; s < KS; ++s) acc = mfma_f32_16x16x4(ka[b][s], bq[s], acc);
           float o[4];
 #pragma unroll
-          for (int i = 0; i < 4; ++i) o[i] = (kt * 16 + 4 * g + i < kn) ? acc[i] * a.scale : -INFINITY;
+          for (int i = 0; i < 4; ++i) {
+            o[i] = (kt * 16 + 4 * g + i < kn) ? acc[i] * a.scale : -INFINITY;
+            lmax = fmaxf(lmax, o[i]);
+            if constexpr (IMPROVED) {
+              float v = o[i];
+#pragma unroll
+              for (int e = 0; e < NT; ++e) {  // insertion into the descending list
+                const float hi = fmaxf(top[e], v);
+                v = fminf(top[e], v);
+                top[e] = hi;
+              }
+            }
+          }
           *reinterpret_cast<float4*>(&logits[c * kLStride + kt * 16 + 4 * g]) = make_float4(o[0], o[1], o[2], o[3]);
         }
+      }
+    }
+    // slice (wave, g) of row c
+    smax[c][wave * 4 + g] = lmax;
+    if constexpr (IMPROVED)
+      *reinterpret_cast<float4*>(&stop[c][wave * 4 + g][0]) = make_float4(top[0], top[1], top[2], top[3]);
+    if constexpr (FUSED) {
+#pragma unroll
+      for (int e = 0; e < kChunk / 256; ++e) {
+        const int x = tid + 256 * e;
+        if (x < mn) mlist[x] = mreg[e];
       }
     }
   }
   __syncthreads();
 
-  // ---- per-row maximum, normaliser and top-k (wave w owns rows 4w..4w+3) ------
-  const int kk = min(a.topk, kn);
-  for (int rr = 0; rr < 4; ++rr) {
-    const int r = wave * 4 + rr;
+  // ---- row maximum and top-k ----------------------------------------------------------
+  // wave w owns rows 4w..4w+3, one 16-lane group per row, all four at once
+  {
+    const int g4 = lane >> 4, c16 = lane & 15;
+    const int r = wave * 4 + g4;
     const int j = j0 + r;
     float* row = &logits[r * kLStride];
-    float mx, z;
-    const int jsize = !(IMPROVED && j < C) ? 0
-                      : FUSED ? moff[r + 1] - moff[r] : a.sizes[static_cast<size_t>(u) * C + j];
-    if (IMPROVED && j < C && jsize == 0) {
-      // empty cluster: no top-k set, no mass
-      const size_t uj = static_cast<size_t>(u) * C + j;
-      if constexpr (FUSED) {
-        for (int x = lane; x < a.topk; x += 64) a.topk_out[uj * a.topk + x] = -1;
-        if (lane == 0) {
-          a.mass[uj] = 0.0f;
-          tcnt[r] = 0;
-          rowmass[r] = 0.0f;
-        }
-      } else {
-        const size_t cb = (uj * a.nchunk + chunk) * a.topk;
-        for (int x = lane; x < a.topk; x += 64) {
-          a.cand_idx[cb + x] = -1;
-          a.cand_val[cb + x] = -INFINITY;
-        }
-      }
-      mx = 0.0f;
-      z = 1.0f;
-    } else if (IMPROVED && j < C) {
-      const size_t uj = static_cast<size_t>(u) * C + j;
-      int* sel = selout[wave];
+    const float mx = row16_max(smax[r][c16]);
+    if constexpr (IMPROVED) {
+      const int kk = min(a.topk, kn);
+      const size_t uj = static_cast<size_t>(u) * C + (j < C ? j : 0);
+      const int jsize = j >= C ? 0 : FUSED ? moff[r + 1] - moff[r] : a.sizes[uj];
+      uint16_t* cand = tpos16[r];
       int cnt;
       if (FUSED && a.topk_in != nullptr) {
-        // caller-supplied set: entries until the first negative or out-of-range one
+        // caller-supplied set: its entries up to the first negative or
+        // out-of-range one, in the given order
         const int32_t* tin = a.topk_in + uj * a.topk;
-        float m1 = -INFINITY;
-        for (int x = lane; x < kn; x += 64) m1 = fmaxf(m1, row[x]);
-        mx = wave_max(m1);
-        float zz = 0.0f;
-        for (int x = lane; x < kn; x += 64) zz += __expf(row[x] - mx);
-        z = wave_sum(zz);
-        cnt = 0;
-        while (cnt < a.topk && tin[cnt] >= 0 && tin[cnt] < kn) ++cnt;
-        for (int x = lane; x < cnt; x += 64) sel[x] = tin[x];
+        int first_bad = a.topk;
+        for (int x = c16; x < a.topk; x += 16) {
+          const int key = tin[x];
+          if ((key < 0 || key >= kn) && x < first_bad) first_bad = x;
+        }
+        first_bad = -static_cast<int>(row16_max(static_cast<float>(-first_bad)));
+        cnt = jsize > 0 ? min(first_bad, kCandCap) : 0;
+        for (int x = c16; x < cnt; x += 16) cand[x] = static_cast<uint16_t>(tin[x]);
         wave_lds_sync();
       } else {
-        cnt = wave_topk_row<kCandCap>(row, kn, kk, cscr[wave], sel, &mx, &z);
+        const int kr = jsize > 0 ? kk : 0;
+        uint32_t tau;
+        if (kk <= 16 * NT / 2) {
+          uint32_t keys[NT];
+#pragma unroll
+          for (int e = 0; e < NT; ++e) {
+            const float v = stop[r][c16][e];
+            keys[e] = v > -INFINITY ? order_key(v) : 0u;
+          }
+          tau = group_kth_key<NT>(keys, kr);
+        } else if (kk <= 64) {
+          tau = group_row_threshold<8>(row, kn, kr);
+        } else {
+          tau = group_row_threshold<16>(row, kn, kr);
+        }
+        cnt = group_select<kCandCap>(row, kn, kr, tau, cand);
+        // rows whose threshold let too many entries through (many ties): the
+        // whole wave selects them one after the other; its scratch is the
+        // slice area of its own rows, consumed by now
+        const uint64_t over = __ballot(cnt < 0);
+        for (int gg = 0; gg < 4; ++gg) {
+          if (((over >> (16 * gg)) & 1ull) == 0ull) continue;
+          const int rg = wave * 4 + gg;
+          float md, zd;
+          const int cg = wave_topk_row<kCandCap>(&logits[rg * kLStride], kn, kk,
+                                                 reinterpret_cast<int*>(&stop[4 * wave][0][0]),
+                                                 tpos16[rg], &md, &zd);
+          wave_lds_sync();
+          if (g4 == gg) cnt = cg;
+        }
       }
+      // sum over T of exp(s - max) (the numerator of the mass)
+      float tsum = 0.0f;
+      for (int x = c16; x < cnt; x += 16) tsum += __expf(row[cand[x]] - mx);
+      tsum = row16_sum(tsum);
       if constexpr (FUSED) {
-        // mass of T, then mask T out of the row so that P V gives the rest part
-        float msum = 0.0f;
-        for (int x = lane; x < cnt; x += 64) msum += __expf(row[sel[x]] - mx);
-        msum = wave_sum(msum) / z;
+        // T masked out of the row so that P V gives the rest part
         wave_lds_sync();
-        for (int x = lane; x < cnt; x += 64) {
-          tpos16[r][x] = static_cast<uint16_t>(sel[x]);
-          row[sel[x]] = -INFINITY;
-        }
-        for (int x = lane; x < a.topk; x += 64) a.topk_out[uj * a.topk + x] = x < cnt ? sel[x] : -1;
-        if (lane == 0) {
-          rowmass[r] = msum;
-          tcnt[r] = cnt;
-          a.mass[uj] = msum;
-        }
+        for (int x = c16; x < cnt; x += 16) row[cand[x]] = -INFINITY;
+        if (j < C)
+          for (int x = c16; x < a.topk; x += 16) a.topk_out[uj * a.topk + x] = x < cnt ? cand[x] : -1;
+        if (c16 == 0) tcnt[r] = cnt;
       } else {
-        const size_t cb = (uj * a.nchunk + chunk) * a.topk;
-        for (int x = lane; x < a.topk; x += 64) {
-          const bool ok = x < cnt;
-          const int pos = ok ? sel[x] : 0;
-          a.cand_idx[cb + x] = ok ? k0 + pos : -1;
-          a.cand_val[cb + x] = ok ? row[pos] : -INFINITY;
+        if (j < C) {
+          const size_t cb = (uj * a.nchunk + chunk) * a.topk;
+          for (int x = c16; x < a.topk; x += 16) {
+            const bool ok = x < cnt;
+            const int pos = ok ? cand[x] : 0;
+            a.cand_idx[cb + x] = ok ? k0 + pos : -1;
+            a.cand_val[cb + x] = ok ? row[pos] : -INFINITY;
+          }
         }
       }
+      if (c16 == 0) rowtop[r] = tsum;
       wave_lds_sync();
-    } else {
-      float m1 = -INFINITY;
-      for (int x = lane; x < kn; x += 64) m1 = fmaxf(m1, row[x]);
-      mx = wave_max(m1);
-      float zz = 0.0f;
-      for (int x = lane; x < kn; x += 64) zz += __expf(row[x] - mx);
-      z = wave_sum(zz);
     }
-    if (lane == 0) {
-      rowm[r] = mx;
-      rowz[r] = z;
-    }
+    if (c16 == 0) rowm[r] = mx;
   }
   __syncthreads();
 
@@ -435,6 +482,7 @@ __global__ __launch_bounds__(256) void attn_tile_kernel(AttnArgs a) {
   v4f oacc[DT];
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) oacc[dt] = v4f{0.f, 0.f, 0.f, 0.f};
+  float psum = 0.0f;
   {
     const float mc = rowm[c];
     for (int kt0 = wave; kt0 < nkt; kt0 += 4 * BT) {
@@ -457,6 +505,7 @@ __global__ __launch_bounds__(256) void attn_tile_kernel(AttnArgs a) {
         if (kt < nkt) {
           const float4 s4 = *reinterpret_cast<const float4*>(&logits[c * kLStride + kt * 16 + 4 * g]);
           const float p[4] = {__expf(s4.x - mc), __expf(s4.y - mc), __expf(s4.z - mc), __expf(s4.w - mc)};
+          psum += (p[0] + p[1]) + (p[2] + p[3]);
 #pragma unroll
           for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -465,6 +514,8 @@ __global__ __launch_bounds__(256) void attn_tile_kernel(AttnArgs a) {
       }
     }
   }
+  psum = cross_rows_sum(psum);
+  if (g == 0) zpart[wave][c] = psum;
   __syncthreads();  // logits are dead from here on: reuse them
   float* red = logits;                 // [4 waves][16 centroids][D]
   float* vhat = logits + 4 * 16 * D;   // [16][D]
@@ -477,18 +528,26 @@ __global__ __launch_bounds__(256) void attn_tile_kernel(AttnArgs a) {
     const int cc = x / D, dim = x % D;
     const float sum = ((red[(0 * 16 + cc) * D + dim] + red[(1 * 16 + cc) * D + dim]) +
                        red[(2 * 16 + cc) * D + dim]) + red[(3 * 16 + cc) * D + dim];
+    float z = ((zpart[0][cc] + zpart[1][cc]) + zpart[2][cc]) + zpart[3][cc];
+    if constexpr (IMPROVED && FUSED) z += rowtop[cc];
     if (j0 + cc >= C) continue;
     const size_t ujc = static_cast<size_t>(u) * C + j0 + cc;
-    if (FUSED) {
-      const float val = moff[cc + 1] > moff[cc] ? sum / rowz[cc] : 0.0f;
+    if constexpr (FUSED) {
+      const bool nonempty = moff[cc + 1] > moff[cc];
+      const float val = nonempty ? sum / z : 0.0f;
       vhat[cc * D + dim] = val;
       a.vcb[ujc * D + dim] = val;
+      if (IMPROVED && dim == 0) {
+        const float mass = nonempty ? rowtop[cc] / z : 0.0f;
+        rowmass[cc] = mass;
+        a.mass[ujc] = mass;
+      }
     } else {
       const size_t pj = ujc * a.nchunk + chunk;
       a.pacc[pj * D + dim] = sum;
       if (dim == 0) {
         a.pm[pj] = rowm[cc];
-        a.pz[pj] = rowz[cc];
+        a.pz[pj] = z;
       }
     }
   }
@@ -504,24 +563,19 @@ __global__ __launch_bounds__(256) void attn_tile_kernel(AttnArgs a) {
       if (j >= C) break;
       const int sz = moff[r + 1] - moff[r];
       if (sz == 0) continue;
-      const int* mem = mlist + moff[r];
+      const int* mem = mlist + (moff[r] - m0);
       if constexpr (!IMPROVED) {
         // Eq. (6): each member row receives V^c_j; a lane writes 4 dims of a row
         constexpr int LPR = D / 4, RPS = 64 / LPR;
         const int part = lane % LPR, sub = lane / LPR;
         const float4 val = *reinterpret_cast<const float4*>(&vhat[r * D + part * 4]);
-        for (int m0 = sub; m0 < sz; m0 += RPS) {
-          const int qrow = mem[m0];
+        for (int m1 = sub; m1 < sz; m1 += RPS) {
+          const int qrow = mem[m1];
           store4(ou + static_cast<size_t>(qrow) * D + part * 4, val.x, val.y, val.z, val.w);
         }
       } else {
-        // T of this cluster as int positions for the sparse routine (reuse selout)
-        int* tposi = selout[wave];
-        const int cnt = tcnt[r];
-        for (int x = lane; x < cnt; x += 64) tposi[x] = tpos16[r][x];
-        wave_lds_sync();
-        sparse_cluster<D, T, NKT>(tposi, cnt, rowmass[r], &vhat[r * D], mem, sz, qu, ku, vu, ou,
-                                  a.scale);
+        sparse_cluster<D, T, NKT>(tpos16[r], tcnt[r], rowmass[r], &vhat[r * D], mem, sz, qu, ku,
+                                  vu, ou, a.scale);
         wave_lds_sync();
       }
     }

@@ -32,6 +32,7 @@
 #include "common.h"
 #include "hash_tile.h"
 #include "kernels.h"
+#include "select.h"
 
 namespace ca {
 
@@ -405,24 +406,51 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
     if (lane == 63) off[kCmax] = run;
   }
   __syncthreads();
-  // wave w collects clusters w, w + 16, ...; eight of them share each pass
-  // over the assignments (the next 64 are read while the current ones are
-  // compared)
-  for (int jb = wave; jb < ce; jb += 8 * kKmWaves) {
-    int cnt[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    int an = lane < n ? sh.assign[lane] : -1;
-    for (int base = 0; base < n; base += 64) {
-      const int i = base + lane;
-      const int ai = an;
-      an = i + 64 < n ? sh.assign[i + 64] : -1;
+  // counting sort that keeps query order: wave w takes the contiguous query
+  // range [w per, (w + 1) per); within 64 queries, the lanes of one cluster
+  // find each other with nine ballots on the bits of the cluster index
+  int32_t* hist = off + kCmax + 8;  // [kKmWaves][kCmax] per-wave counts, then bases
+  static_assert((kCmax + 8) + kKmWaves * kCmax <= kCmax * kCntStride, "member-list scratch");
+  for (int x = tid; x < kKmWaves * kCmax; x += kKmThreads) hist[x] = 0;
+  const int per = (n + kKmWaves - 1) / kKmWaves;
+  const int q_begin = min(n, wave * per), q_end = min(n, q_begin + per);
+  auto same_cluster = [&](int a) {  // lanes whose a equals this lane's (a in [0, 511])
+    uint64_t eq = ~0ull;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int j = jb + e * kKmWaves;
-        const uint64_t m = __ballot(ai == j);
-        if (ai == j) mem[off[j] + cnt[e] + __popcll(m & lanemask_lt())] = i;
-        cnt[e] += __popcll(m);
-      }
+    for (int b = 0; b < 9; ++b) {
+      const uint64_t m = __ballot((a >> b) & 1);
+      eq &= ((a >> b) & 1) ? m : ~m;
     }
+    return eq;
+  };
+  __syncthreads();
+  for (int base = q_begin; base < q_end; base += 64) {
+    const int i = base + lane;
+    const int a = i < q_end ? sh.assign[i] : 511;
+    const uint64_t eq = same_cluster(a);
+    if (a < kCmax && (eq & lanemask_lt()) == 0ull) hist[wave * kCmax + a] += __popcll(eq);
+  }
+  __syncthreads();
+  for (int j = tid; j < ce; j += kKmThreads) {  // per-wave bases
+    int run = off[j];
+    for (int w = 0; w < kKmWaves; ++w) {
+      const int x = hist[w * kCmax + j];
+      hist[w * kCmax + j] = run;
+      run += x;
+    }
+  }
+  __syncthreads();
+  for (int base = q_begin; base < q_end; base += 64) {
+    const int i = base + lane;
+    const int a = i < q_end ? sh.assign[i] : 511;
+    const uint64_t eq = same_cluster(a);
+    if (a < kCmax) {
+      const int pos = hist[wave * kCmax + a] + __popcll(eq & lanemask_lt());
+      mem[pos] = i;
+    }
+    wave_lds_sync();
+    if (a < kCmax && (eq & lanemask_lt()) == 0ull) hist[wave * kCmax + a] += __popcll(eq);
+    wave_lds_sync();
   }
   __syncthreads();
   for (int i = tid; i < n; i += kKmThreads) {
@@ -440,7 +468,7 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
   // summing the current one
   constexpr int GPW = 64 / D;        // lane groups per wave
   constexpr int G = kKmWaves * GPW;  // lane groups per workgroup
-  constexpr int BATCH = 8;           // rows in flight per lane
+  constexpr int BATCH = 16;          // rows in flight per lane
   const int t = lane % D, grp = wave * GPW + lane / D;
   auto fetch = [&](int j, int m0, float* x) {
     const int sz = sh.size[j];

@@ -23,8 +23,8 @@ __device__ __forceinline__ void wave_lds_sync() {
 // digit of the kk-th key.  After four passes the kk-th key T is known, and a
 // single ordered sweep takes every key > T and the first (kk - #(> T)) keys
 // equal to T.
-template <typename KeyFn>
-__device__ int wave_select_topk(KeyFn key, int m, int kk, int* hist, int* out) {
+template <typename KeyFn, typename OutT>
+__device__ int wave_select_topk(KeyFn key, int m, int kk, int* hist, OutT* out) {
   const int lane = lane_id();
   if (kk <= 0 || m <= 0) return 0;
   uint32_t prefix = 0, pmask = 0;
@@ -82,7 +82,7 @@ __device__ int wave_select_topk(KeyFn key, int m, int kk, int* hist, int* out) {
     const int eq_rank = eq_seen + __popcll(eqmask & lanemask_lt());
     const bool sel = gt || (eq && eq_rank < need);
     const uint64_t selmask = __ballot(sel);
-    if (sel) out[written + __popcll(selmask & lanemask_lt())] = pos;
+    if (sel) out[written + __popcll(selmask & lanemask_lt())] = static_cast<OutT>(pos);
     written += __popcll(selmask);
     eq_seen += __popcll(eqmask);
   }
@@ -119,8 +119,8 @@ __device__ __forceinline__ uint32_t wave_kth_key(uint32_t k1, uint32_t k2, bool 
 // (many ties) the radix selection above runs instead.
 // scratch: 2*CAP ints of LDS private to the wave (candidate values, then
 // candidate positions; the whole area is the radix histogram of the fallback).
-template <int CAP>
-__device__ int wave_topk_row(const float* row, int m, int kk, int* scratch, int* out,
+template <int CAP, typename OutT>
+__device__ int wave_topk_row(const float* row, int m, int kk, int* scratch, OutT* out,
                              float* mx_out, float* z_out) {
   static_assert(2 * CAP >= 256 && CAP <= 128, "scratch layout");
   float* cval = reinterpret_cast<float*>(scratch);
@@ -175,12 +175,139 @@ __device__ int wave_topk_row(const float* row, int m, int kk, int* scratch, int*
     const uint64_t eqmask = __ballot(eq);
     const bool sel = (valid && key > kth) || (eq && eq_seen + __popcll(eqmask & lanemask_lt()) < need);
     const uint64_t selmask = __ballot(sel);
-    if (sel) out[written + __popcll(selmask & lanemask_lt())] = cpos[i];
+    if (sel) out[written + __popcll(selmask & lanemask_lt())] = static_cast<OutT>(cpos[i]);
     written += __popcll(selmask);
     eq_seen += __popcll(eqmask);
   }
   wave_lds_sync();
   return written;
+}
+
+// ---------------------------------------------------------------------------
+// Four rows per wave at once: the 16-lane group g = lane / 16 owns row g, and
+// lane c = lane % 16 of the group reads positions c, c + 16, c + 32, ...
+// Reductions stay inside a group (DPP row operations).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int row16_sum_i(int x) {
+  x += dpp_i<0xB1>(x);
+  x += dpp_i<0x4E>(x);
+  x += dpp_i<0x141>(x);
+  return x + dpp_i<0x140>(x);
+}
+__device__ __forceinline__ uint32_t lanemask_lt16() { return (1u << (threadIdx.x & 15)) - 1u; }
+__device__ __forceinline__ uint32_t group_field(uint64_t ballot) {
+  return static_cast<uint32_t>(ballot >> (threadIdx.x & 48)) & 0xffffu;
+}
+
+// The kk-th largest of the keys held by the group (NK per lane, 0 = none):
+// the largest T with at least kk keys >= T, one bit at a time.
+template <int NK>
+__device__ __forceinline__ uint32_t group_kth_key(const uint32_t* keys, int kk) {
+  uint32_t t = 0;
+  for (int bit = 31; bit >= 0; --bit) {
+    const uint32_t cand = t | (1u << bit);
+    int cnt = 0;
+#pragma unroll
+    for (int e = 0; e < NK; ++e) cnt += keys[e] >= cand ? 1 : 0;
+    if (row16_sum_i(cnt) >= kk) t = cand;
+  }
+  return t;
+}
+
+// Top-kk positions of the group's row row[0..m) (0 <= kk, kk <= m), ties to
+// the smaller position, given a threshold tau that every top-kk entry reaches
+// (its order key): one sweep lists the positions with key >= tau in ascending
+// order in cand[0..CAP); the exact kk-th key among them is found by a second
+// search, and the entries above it plus the first ones equal to it are
+// compacted in place.  Returns the number selected (kk), or -1 if more than
+// CAP positions reached tau (the caller then selects that row another way).
+template <int CAP>
+__device__ int group_select(const float* row, int m, int kk, uint32_t tau, uint16_t* cand) {
+  static_assert(CAP % 16 == 0 && CAP <= 256, "candidate layout");
+  constexpr int PER = CAP / 16;
+  const int c = threadIdx.x & 15;
+  const uint32_t lt = lanemask_lt16();
+  int cnt = 0;
+  for (int i0 = 0; i0 < m; i0 += 64) {  // four reads in flight per lane
+    float x[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int p = i0 + 16 * e + c;
+      x[e] = p < m ? row[p] : 0.0f;
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int p = i0 + 16 * e + c;
+      const bool sel = p < m && order_key(x[e]) >= tau;
+      const uint32_t f = group_field(__ballot(sel));
+      const int idx = cnt + __popc(f & lt);
+      if (sel && idx < CAP) cand[idx] = static_cast<uint16_t>(p);
+      cnt += __popc(f);
+    }
+  }
+  if (cnt > CAP) return -1;
+  wave_lds_sync();
+  int pos[PER];
+  uint32_t ck[PER];
+#pragma unroll
+  for (int e = 0; e < PER; ++e) {
+    const int i = c + 16 * e;
+    pos[e] = i < cnt ? cand[i] : 0;
+  }
+#pragma unroll
+  for (int e = 0; e < PER; ++e) ck[e] = c + 16 * e < cnt ? order_key(row[pos[e]]) : 0u;
+  const uint32_t kth = group_kth_key<PER>(ck, kk);
+  int gt = 0;
+#pragma unroll
+  for (int e = 0; e < PER; ++e) gt += ck[e] > kth ? 1 : 0;
+  const int need = kk - row16_sum_i(gt);
+  wave_lds_sync();
+  int written = 0, eq_seen = 0;
+#pragma unroll
+  for (int e = 0; e < PER; ++e) {
+    const bool eq = ck[e] == kth;  // key 0 (no entry) never equals kth > 0
+    const uint32_t ef = group_field(__ballot(eq));
+    const bool sel = ck[e] > kth || (eq && eq_seen + __popc(ef & lt) < need);
+    const uint32_t sf = group_field(__ballot(sel));
+    if (sel) cand[written + __popc(sf & lt)] = static_cast<uint16_t>(pos[e]);
+    written += __popc(sf);
+    eq_seen += __popc(ef);
+  }
+  wave_lds_sync();
+  return written;
+}
+
+// Threshold for group_select from the row itself: each lane keeps the NT
+// largest values of its positions c, c + 16, ...; the kk-th largest of those
+// 16 * NT values (16 * NT >= kk) is reached by every top-kk entry.
+template <int NT>
+__device__ uint32_t group_row_threshold(const float* row, int m, int kk) {
+  const int c = threadIdx.x & 15;
+  float top[NT];
+#pragma unroll
+  for (int e = 0; e < NT; ++e) top[e] = -INFINITY;
+  for (int i0 = 0; i0 < m; i0 += 64) {
+    float x[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int p = i0 + 16 * e + c;
+      x[e] = p < m ? row[p] : -INFINITY;
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float v = x[e];
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {  // insertion into the descending list
+        const float hi = fmaxf(top[t], v);
+        v = fminf(top[t], v);
+        top[t] = hi;
+      }
+    }
+  }
+  uint32_t keys[NT];
+#pragma unroll
+  for (int e = 0; e < NT; ++e) keys[e] = top[e] > -INFINITY ? order_key(top[e]) : 0u;
+  return group_kth_key<NT>(keys, kk);
 }
 
 }  // namespace ca
