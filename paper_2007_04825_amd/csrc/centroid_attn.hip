@@ -116,60 +116,75 @@ __device__ __forceinline__ void store_vec(bf16_t* p, const float* s) {
 //                     B = P^T straight from the S^T result registers.
 // Lane (query c, group g) ends with dims DT*4g .. DT*4g + 4*DT - 1 of its row.
 // ---------------------------------------------------------------------------
+template <int D, typename T, int NKT>
+struct SparseOps {
+  float kf[NKT][D / 4];     // K_T fragments: key kt * 16 + lane % 16, dims (lane / 16) * D / 4 ..
+  float vf[NKT][4][D / 16]; // V_T^T fragments: key kt * 16 + 4 (lane / 16) + i, dims (lane % 16) * D / 16 ..
+  float bq[D / 4];          // Q of the first member tile
+  int row;                  // this lane's member row of the first tile, or -1
+};
+
+// Requests the operands of one cluster: K_T, V_T and the first member tile.
 template <int D, typename T, int NKT, typename PosT>
-__device__ void sparse_cluster(const PosT* tpos, int kk, float mh, const float* vb,
-                               const int32_t* mem, int sz, const T* __restrict__ qu,
-                               const T* __restrict__ ku, const T* __restrict__ vu,
-                               T* __restrict__ ou, float scale) {
+__device__ __forceinline__ void sparse_load(const PosT* tpos, int kk, const int32_t* mem, int sz,
+                                            const T* __restrict__ qu, const T* __restrict__ ku,
+                                            const T* __restrict__ vu, SparseOps<D, T, NKT>& S) {
   constexpr int KS = D / 4, DT = D / 16;
   const int lane = lane_id(), c = lane & 15, g = lane >> 4;
   const int nkt = (kk + 15) >> 4;
-  // Q rows of the first member tile are requested before the K_T / V_T gathers
-  float bq[KS];
-  int row = c < sz ? mem[c] : -1;
-  if (row >= 0) {
-    load_row<KS>(qu + static_cast<size_t>(row) * D + g * KS, bq);
+  S.row = c < sz ? mem[c] : -1;
+  if (S.row >= 0) {
+    load_row<KS>(qu + static_cast<size_t>(S.row) * D + g * KS, S.bq);
   } else {
 #pragma unroll
-    for (int s = 0; s < KS; ++s) bq[s] = 0.0f;
+    for (int s = 0; s < KS; ++s) S.bq[s] = 0.0f;
   }
-  float kf[NKT][KS];
-  float vf[NKT][4][DT];
 #pragma unroll
   for (int kt = 0; kt < NKT; ++kt) {
     const int slot = kt * 16 + c;
     const int key = (kt < nkt && slot < kk) ? static_cast<int>(tpos[slot]) : -1;
     if (key >= 0) {
-      load_row<KS>(ku + static_cast<size_t>(key) * D + g * KS, kf[kt]);
+      load_row<KS>(ku + static_cast<size_t>(key) * D + g * KS, S.kf[kt]);
     } else {
 #pragma unroll
-      for (int s = 0; s < KS; ++s) kf[kt][s] = 0.0f;
+      for (int s = 0; s < KS; ++s) S.kf[kt][s] = 0.0f;
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int sl = kt * 16 + 4 * g + i;
       const int kv = (kt < nkt && sl < kk) ? static_cast<int>(tpos[sl]) : -1;
       if (kv >= 0) {
-        load_vec<DT>(vu + static_cast<size_t>(kv) * D + DT * c, vf[kt][i]);
+        load_vec<DT>(vu + static_cast<size_t>(kv) * D + DT * c, S.vf[kt][i]);
       } else {
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) vf[kt][i][dt] = 0.0f;
+        for (int dt = 0; dt < DT; ++dt) S.vf[kt][i][dt] = 0.0f;
       }
     }
   }
+}
+
+// Improved values of one cluster's members from its loaded operands.
+template <int D, typename T, int NKT>
+__device__ __forceinline__ void sparse_run(SparseOps<D, T, NKT>& S, int kk, float mh,
+                                           const float* vb, const int32_t* mem, int sz,
+                                           const T* __restrict__ qu, T* __restrict__ ou,
+                                           float scale) {
+  constexpr int KS = D / 4, DT = D / 16;
+  const int lane = lane_id(), c = lane & 15, g = lane >> 4;
+  const int nkt = (kk + 15) >> 4;
   float vbf[4 * DT];
 #pragma unroll
   for (int x = 0; x < 4 * DT; ++x) vbf[x] = vb[DT * 4 * g + x];
-
+  int row = S.row;
   for (int mt = 0; mt < sz; mt += 16) {
     if (mt > 0) {
       const int mi = mt + c;
       row = mi < sz ? mem[mi] : -1;
       if (row >= 0) {
-        load_row<KS>(qu + static_cast<size_t>(row) * D + g * KS, bq);
+        load_row<KS>(qu + static_cast<size_t>(row) * D + g * KS, S.bq);
       } else {
 #pragma unroll
-        for (int s = 0; s < KS; ++s) bq[s] = 0.0f;
+        for (int s = 0; s < KS; ++s) S.bq[s] = 0.0f;
       }
     }
     v4f sacc[NKT];
@@ -179,7 +194,7 @@ __device__ void sparse_cluster(const PosT* tpos, int kk, float mh, const float* 
       sacc[kt] = v4f{0.f, 0.f, 0.f, 0.f};
       if (kt < nkt) {
 #pragma unroll
-        for (int s = 0; s < KS; ++s) sacc[kt] = mfma_f32_16x16x4(kf[kt][s], bq[s], sacc[kt]);
+        for (int s = 0; s < KS; ++s) sacc[kt] = mfma_f32_16x16x4(S.kf[kt][s], S.bq[s], sacc[kt]);
       }
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -210,7 +225,7 @@ __device__ void sparse_cluster(const PosT* tpos, int kk, float mh, const float* 
         for (int i = 0; i < 4; ++i) {
           const float pv = sacc[kt][i] * f;
 #pragma unroll
-          for (int dt = 0; dt < DT; ++dt) oacc[dt] = mfma_f32_16x16x4(vf[kt][i][dt], pv, oacc[dt]);
+          for (int dt = 0; dt < DT; ++dt) oacc[dt] = mfma_f32_16x16x4(S.vf[kt][i][dt], pv, oacc[dt]);
         }
       }
     }
@@ -223,6 +238,16 @@ __device__ void sparse_cluster(const PosT* tpos, int kk, float mh, const float* 
       store_vec<4 * DT>(ou + static_cast<size_t>(row) * D + DT * 4 * g, o);
     }
   }
+}
+
+template <int D, typename T, int NKT, typename PosT>
+__device__ void sparse_cluster(const PosT* tpos, int kk, float mh, const float* vb,
+                               const int32_t* mem, int sz, const T* __restrict__ qu,
+                               const T* __restrict__ ku, const T* __restrict__ vu,
+                               T* __restrict__ ou, float scale) {
+  SparseOps<D, T, NKT> S;
+  sparse_load<D, T, NKT>(tpos, kk, mem, sz, qu, ku, vu, S);
+  sparse_run<D, T, NKT>(S, kk, mh, vb, mem, sz, qu, ou, scale);
 }
 
 // ---------------------------------------------------------------------------
@@ -242,6 +267,7 @@ struct AttnArgs {
   const void* v;
   const int32_t* lengths;
   int heads, N, C, nchunk, topk;
+  int ntile, ncg, units;  // 16-centroid tiles, 4-cluster groups, (batch, head) units
   float scale;
   const int32_t* topk_in;
   float* pm;
@@ -272,8 +298,8 @@ __global__ __launch_bounds__(256) void attn_tile_kernel(AttnArgs a) {
   constexpr bool IMPROVED = (MODE & 1) != 0;
   constexpr bool FUSED = MODE < 2;
   constexpr int KS = D / 4, DT = D / 16;
-  constexpr int BT = 4;  // key tiles per batch of loads
-  constexpr int NT = 4;  // logits each lane keeps per row for the threshold
+  constexpr int BT = 512 / D;          // key tiles per batch of loads (128 registers of operands)
+  constexpr int NT = IMPROVED ? 8 : 1;  // logits each lane keeps per row for the threshold
   __shared__ __align__(16) float logits[16 * kLStride];
   __shared__ float rowm[16], rowmass[16], rowtop[16];
   __shared__ int tcnt[16];
@@ -281,11 +307,12 @@ __global__ __launch_bounds__(256) void attn_tile_kernel(AttnArgs a) {
   __shared__ float smax[16][16];                               // [row][slice] maxima
   __shared__ __align__(16) float stop[IMPROVED ? 16 : 1][16][NT];  // [row][slice] kept logits
   __shared__ uint16_t tpos16[IMPROVED ? 16 : 1][kCandCap];     // top-k candidates, then T
-  __shared__ int mlist[FUSED ? kChunk : 1];                    // member lists of the 16 clusters
   __shared__ int moff[17];
   __shared__ int any_nonempty;
 
-  const int chunk = blockIdx.x, tile = blockIdx.y, u = blockIdx.z;
+  const int wi = xcd_work_item();  // chunk fastest, then tile, then (batch, head)
+  if (wi >= a.nchunk * a.ntile * a.units) return;
+  const int chunk = wi % a.nchunk, tile = (wi / a.nchunk) % a.ntile, u = wi / (a.nchunk * a.ntile);
   const int n = unit_length(a.lengths, u / a.heads, a.N);
   const int k0 = chunk * kChunk;
   if (k0 >= n) return;
@@ -311,7 +338,8 @@ __global__ __launch_bounds__(256) void attn_tile_kernel(AttnArgs a) {
     __syncthreads();
     if (!any_nonempty) return;
   }
-  // member lists are requested now and stored after the first product
+  // member lists are requested now and stored (in the logit area) once the
+  // logits are no longer needed
   int mreg[kChunk / 256];
   int m0 = 0, mn = 0;
   if constexpr (FUSED) {
@@ -378,14 +406,10 @@ __global__ __launch_bounds__(256) void attn_tile_kernel(AttnArgs a) {
     }
     // slice (wave, g) of row c
     smax[c][wave * 4 + g] = lmax;
-    if constexpr (IMPROVED)
-      *reinterpret_cast<float4*>(&stop[c][wave * 4 + g][0]) = make_float4(top[0], top[1], top[2], top[3]);
-    if constexpr (FUSED) {
+    if constexpr (IMPROVED) {
 #pragma unroll
-      for (int e = 0; e < kChunk / 256; ++e) {
-        const int x = tid + 256 * e;
-        if (x < mn) mlist[x] = mreg[e];
-      }
+      for (int e = 0; e < NT; e += 4)
+        *reinterpret_cast<float4*>(&stop[c][wave * 4 + g][e]) = make_float4(top[e], top[e + 1], top[e + 2], top[e + 3]);
     }
   }
   __syncthreads();
@@ -519,6 +543,15 @@ __global__ __launch_bounds__(256) void attn_tile_kernel(AttnArgs a) {
   __syncthreads();  // logits are dead from here on: reuse them
   float* red = logits;                 // [4 waves][16 centroids][D]
   float* vhat = logits + 4 * 16 * D;   // [16][D]
+  int* mlist = reinterpret_cast<int*>(logits + 5 * 16 * D);  // member lists of the 16 clusters
+  static_assert(5 * 16 * D + kChunk <= 16 * kLStride, "logit area reuse");
+  if constexpr (FUSED) {
+#pragma unroll
+    for (int e = 0; e < kChunk / 256; ++e) {
+      const int x = tid + 256 * e;
+      if (x < mn) mlist[x] = mreg[e];
+    }
+  }
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -557,14 +590,14 @@ __global__ __launch_bounds__(256) void attn_tile_kernel(AttnArgs a) {
     // ---- fused outputs: every member row of the 16 clusters ---------------------
     const T* qu = static_cast<const T*>(a.q) + static_cast<size_t>(u) * a.N * D;
     T* ou = static_cast<T*>(a.out) + static_cast<size_t>(u) * a.N * D;
-    for (int rr = 0; rr < 4; ++rr) {
-      const int r = wave * 4 + rr;
-      const int j = j0 + r;
-      if (j >= C) break;
-      const int sz = moff[r + 1] - moff[r];
-      if (sz == 0) continue;
-      const int* mem = mlist + (moff[r] - m0);
-      if constexpr (!IMPROVED) {
+    if constexpr (!IMPROVED) {
+      for (int rr = 0; rr < 4; ++rr) {
+        const int r = wave * 4 + rr;
+        const int j = j0 + r;
+        if (j >= C) break;
+        const int sz = moff[r + 1] - moff[r];
+        if (sz == 0) continue;
+        const int* mem = mlist + (moff[r] - m0);
         // Eq. (6): each member row receives V^c_j; a lane writes 4 dims of a row
         constexpr int LPR = D / 4, RPS = 64 / LPR;
         const int part = lane % LPR, sub = lane / LPR;
@@ -573,10 +606,28 @@ __global__ __launch_bounds__(256) void attn_tile_kernel(AttnArgs a) {
           const int qrow = mem[m1];
           store4(ou + static_cast<size_t>(qrow) * D + part * 4, val.x, val.y, val.z, val.w);
         }
-      } else {
-        sparse_cluster<D, T, NKT>(tpos16[r], tcnt[r], rowmass[r], &vhat[r * D], mem, sz, qu, ku,
-                                  vu, ou, a.scale);
-        wave_lds_sync();
+      }
+    } else {
+      // the operands of PF clusters are requested together, then used
+      constexpr int PER_CLUSTER = NKT * D / 2 + D / 4;  // registers per cluster
+      constexpr int PF = PER_CLUSTER * 4 <= 160 ? 4 : PER_CLUSTER * 2 <= 160 ? 2 : 1;
+      for (int rb = 0; rb < 4; rb += PF) {
+        SparseOps<D, T, NKT> S[PF];
+#pragma unroll
+        for (int e = 0; e < PF; ++e) {
+          const int r = wave * 4 + rb + e;
+          const int sz = j0 + r < C ? moff[r + 1] - moff[r] : 0;
+          if (sz > 0)
+            sparse_load<D, T, NKT>(tpos16[r], tcnt[r], mlist + (moff[r] - m0), sz, qu, ku, vu, S[e]);
+        }
+#pragma unroll
+        for (int e = 0; e < PF; ++e) {
+          const int r = wave * 4 + rb + e;
+          const int sz = j0 + r < C ? moff[r + 1] - moff[r] : 0;
+          if (sz > 0)
+            sparse_run<D, T, NKT>(S[e], tcnt[r], rowmass[r], &vhat[r * D], mlist + (moff[r] - m0), sz,
+                                  qu, ou, a.scale);
+        }
       }
     }
   }
@@ -591,9 +642,11 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   __shared__ int selout[4][128];
   __shared__ float selval[4][128];
   __shared__ float vcs[4][D];
-  const int u = blockIdx.y, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wi = xcd_work_item();  // cluster group fastest, then (batch, head)
+  if (wi >= a.ncg * a.units) return;
+  const int u = wi / a.ncg, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int C = a.C;
-  const int j = blockIdx.x * 4 + wave;
+  const int j = (wi % a.ncg) * 4 + wave;
   if (j >= C) return;
   const size_t uj = static_cast<size_t>(u) * C + j;
   const int sz = a.sizes[uj];
@@ -689,9 +742,11 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
 template <int D, typename T, int NKT>
 __global__ __launch_bounds__(256) void sparse_kernel(AttnArgs a) {
   __shared__ int tp[4][128];
-  const int u = blockIdx.y, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wi = xcd_work_item();  // cluster group fastest, then (batch, head)
+  if (wi >= a.ncg * a.units) return;
+  const int u = wi / a.ncg, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int C = a.C;
-  const int j = blockIdx.x * 4 + wave;
+  const int j = (wi % a.ncg) * 4 + wave;
   if (j >= C) return;
   const size_t uj = static_cast<size_t>(u) * C + j;
   const int sz = a.sizes[uj];
@@ -740,6 +795,9 @@ static AttnArgs make_args(const Problem& p, const Workspace& ws, const int32_t* 
   a.N = p.n;
   a.C = p.C;
   a.nchunk = ws.nchunk;
+  a.ntile = (p.C + 15) / 16;
+  a.ncg = (p.C + 3) / 4;
+  a.units = p.units();
   a.topk = p.topk > 0 ? p.topk : 1;
   a.scale = 1.0f / sqrtf(static_cast<float>(p.d));
   a.topk_in = topk_in;
@@ -763,7 +821,7 @@ static hipError_t launch_attn_nkt(const Problem& p, const Workspace& ws, const i
                                   hipStream_t s) {
   const AttnArgs a = make_args(p, ws, topk_in);
   const bool improved = p.topk > 0;
-  dim3 g1(ws.nchunk, (p.C + 15) / 16, p.units());
+  const dim3 g1(xcd_grid(static_cast<long long>(a.nchunk) * a.ntile * a.units));
   if (ws.nchunk == 1) {
     if (improved)
       hipLaunchKernelGGL((attn_tile_kernel<D, T, 1, NKT>), g1, dim3(256), 0, s, a);
@@ -771,7 +829,7 @@ static hipError_t launch_attn_nkt(const Problem& p, const Workspace& ws, const i
       hipLaunchKernelGGL((attn_tile_kernel<D, T, 0, NKT>), g1, dim3(256), 0, s, a);
     return hipGetLastError();
   }
-  dim3 g2((p.C + 3) / 4, p.units());
+  const dim3 g2(xcd_grid(static_cast<long long>(a.ncg) * a.units));
   if (improved) {
     hipLaunchKernelGGL((attn_tile_kernel<D, T, 3, NKT>), g1, dim3(256), 0, s, a);
     hipLaunchKernelGGL((attn_merge_kernel<D, T, true>), g2, dim3(256), 0, s, a);

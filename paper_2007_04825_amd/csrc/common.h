@@ -193,6 +193,24 @@ __device__ __forceinline__ v4i mfma_i8_16x16x64(v4i a, v4i b, v4i c) {
 }
 
 // ---------------------------------------------------------------------------
+// XCD-aware placement.  The dispatcher hands consecutive workgroups of a
+// launch to the eight XCDs in turn, and each XCD has its own L2.  With the
+// grid padded to a multiple of eight, workgroup L takes work item
+// (L % 8) * (grid / 8) + L / 8, so that consecutive work items (for example
+// the tiles of one (batch, head), which read the same keys and values) run on
+// one XCD and share its L2.
+// ---------------------------------------------------------------------------
+constexpr int kXcds = 8;
+__device__ __forceinline__ int xcd_work_item() {
+  const int per = static_cast<int>(gridDim.x) / kXcds;
+  const int L = static_cast<int>(blockIdx.x);
+  return (L % kXcds) * per + L / kXcds;
+}
+inline unsigned xcd_grid(long long nwork) {
+  return static_cast<unsigned>((nwork + kXcds - 1) / kXcds * kXcds);
+}
+
+// ---------------------------------------------------------------------------
 // Order-preserving map from fp32 to uint32: a < b  <=>  key(a) < key(b).
 // -0 is folded onto +0 so that equal values get equal keys.
 // ---------------------------------------------------------------------------

@@ -247,6 +247,9 @@ __device__ int group_select(const float* row, int m, int kk, uint32_t tau, uint1
   }
   if (cnt > CAP) return -1;
   wave_lds_sync();
+  // exactly kk entries reached the threshold in every row of the wave: the
+  // lists are the selections already
+  if (__ballot(cnt != kk) == 0ull) return cnt;
   int pos[PER];
   uint32_t ck[PER];
 #pragma unroll
