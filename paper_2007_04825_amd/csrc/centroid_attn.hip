@@ -255,6 +255,8 @@ __device__ void sparse_cluster(const PosT* tpos, int kk, float mh, const float* 
 // ---------------------------------------------------------------------------
 constexpr int kLStride = kChunk + 16;  // floats per LDS logit row (the four rows of a wave fall in distinct banks)
 constexpr int kCandCap = 128;
+constexpr int kTileWaves = 8;  // waves per centroid-tile workgroup
+constexpr int kTileThreads = 64 * kTileWaves;
 
 struct AttnArgs {
   const int32_t* assign;
@@ -294,18 +296,20 @@ struct AttnArgs {
 // top-k threshold is the k-th largest of the slices' kept values (k <= 32;
 // larger k take it from a sweep of the row).
 template <int D, typename T, int MODE, int NKT>
-__global__ __launch_bounds__(256) void attn_tile_kernel(AttnArgs a) {
+__global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
   constexpr bool IMPROVED = (MODE & 1) != 0;
   constexpr bool FUSED = MODE < 2;
   constexpr int KS = D / 4, DT = D / 16;
-  constexpr int BT = 512 / D;          // key tiles per batch of loads (128 registers of operands)
-  constexpr int NT = IMPROVED ? 8 : 1;  // logits each lane keeps per row for the threshold
+  constexpr int NW = kTileWaves;       // waves; wave w takes key tiles w, w + NW, ...
+  constexpr int NS = NW * 4;           // slices per row: (wave, lane group)
+  constexpr int BT = 256 / D;          // key tiles per batch of loads (64 registers of operands)
+  constexpr int NT = IMPROVED ? 4 : 1; // logits each lane keeps per row for the threshold
   __shared__ __align__(16) float logits[16 * kLStride];
   __shared__ float rowm[16], rowmass[16], rowtop[16];
   __shared__ int tcnt[16];
-  __shared__ float zpart[4][16];                               // per-wave sums of P per row
-  __shared__ float smax[16][16];                               // [row][slice] maxima
-  __shared__ __align__(16) float stop[IMPROVED ? 16 : 1][16][NT];  // [row][slice] kept logits
+  __shared__ float zpart[NW][16];                              // per-wave sums of P per row
+  __shared__ float smax[16][NS];                               // [row][slice] maxima
+  __shared__ __align__(16) float stop[IMPROVED ? 16 : 1][NS][NT];  // [row][slice] kept logits
   __shared__ uint16_t tpos16[IMPROVED ? 16 : 1][kCandCap];     // top-k candidates, then T
   __shared__ int moff[17];
   __shared__ int any_nonempty;
@@ -340,15 +344,15 @@ __global__ __launch_bounds__(256) void attn_tile_kernel(AttnArgs a) {
   }
   // member lists are requested now and stored (in the logit area) once the
   // logits are no longer needed
-  int mreg[kChunk / 256];
+  int mreg[kChunk / kTileThreads];
   int m0 = 0, mn = 0;
   if constexpr (FUSED) {
     m0 = moff[0];
     mn = moff[16] - m0;
     const int32_t* mg = a.members + static_cast<size_t>(u) * a.N + m0;
 #pragma unroll
-    for (int e = 0; e < kChunk / 256; ++e) {
-      const int x = tid + 256 * e;
+    for (int e = 0; e < kChunk / kTileThreads; ++e) {
+      const int x = tid + kTileThreads * e;
       mreg[e] = x < mn ? mg[x] : 0;
     }
   }
@@ -366,11 +370,11 @@ __global__ __launch_bounds__(256) void attn_tile_kernel(AttnArgs a) {
     float top[NT];
 #pragma unroll
     for (int e = 0; e < NT; ++e) top[e] = -INFINITY;
-    for (int kt0 = wave; kt0 < nkt; kt0 += 4 * BT) {
+    for (int kt0 = wave; kt0 < nkt; kt0 += NW * BT) {
       float ka[BT][KS];
 #pragma unroll
       for (int b = 0; b < BT; ++b) {
-        const int key = (kt0 + 4 * b) * 16 + c;
+        const int key = (kt0 + NW * b) * 16 + c;
         if (key < kn) {
           load_row<KS>(ku + static_cast<size_t>(key) * D + g * KS, ka[b]);
         } else {
@@ -380,7 +384,7 @@ __global__ __launch_bounds__(256) void attn_tile_kernel(AttnArgs a) {
       }
 #pragma unroll
       for (int b = 0; b < BT; ++b) {
-        const int kt = kt0 + 4 * b;
+        const int kt = kt0 + NW * b;
         if (kt < nkt) {
           v4f acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -415,13 +419,14 @@ __global__ __launch_bounds__(256) void attn_tile_kernel(AttnArgs a) {
   __syncthreads();
 
   // ---- row maximum and top-k ----------------------------------------------------------
-  // wave w owns rows 4w..4w+3, one 16-lane group per row, all four at once
-  {
+  // waves 0-3: wave w owns rows 4w..4w+3, one 16-lane group per row, all four at
+  // once; lane c16 of a group reads slices c16 and c16 + 16
+  if (wave < 4) {
     const int g4 = lane >> 4, c16 = lane & 15;
     const int r = wave * 4 + g4;
     const int j = j0 + r;
     float* row = &logits[r * kLStride];
-    const float mx = row16_max(smax[r][c16]);
+    const float mx = row16_max(fmaxf(smax[r][c16], smax[r][c16 + 16]));
     if constexpr (IMPROVED) {
       const int kk = min(a.topk, kn);
       const size_t uj = static_cast<size_t>(u) * C + (j < C ? j : 0);
@@ -444,14 +449,15 @@ __global__ __launch_bounds__(256) void attn_tile_kernel(AttnArgs a) {
       } else {
         const int kr = jsize > 0 ? kk : 0;
         uint32_t tau;
-        if (kk <= 16 * NT / 2) {
-          uint32_t keys[NT];
+        if (kk <= 16 * NT) {  // 2 * NT kept values per lane: at least 2 kk in the row
+          uint32_t keys[2 * NT];
 #pragma unroll
           for (int e = 0; e < NT; ++e) {
-            const float v = stop[r][c16][e];
-            keys[e] = v > -INFINITY ? order_key(v) : 0u;
+            const float v0 = stop[r][c16][e], v1 = stop[r][c16 + 16][e];
+            keys[e] = v0 > -INFINITY ? order_key(v0) : 0u;
+            keys[NT + e] = v1 > -INFINITY ? order_key(v1) : 0u;
           }
-          tau = group_kth_key<NT>(keys, kr);
+          tau = group_kth_key<2 * NT>(keys, kr);
         } else if (kk <= 64) {
           tau = group_row_threshold<8>(row, kn, kr);
         } else {
@@ -509,13 +515,13 @@ __global__ __launch_bounds__(256) void attn_tile_kernel(AttnArgs a) {
   float psum = 0.0f;
   {
     const float mc = rowm[c];
-    for (int kt0 = wave; kt0 < nkt; kt0 += 4 * BT) {
+    for (int kt0 = wave; kt0 < nkt; kt0 += NW * BT) {
       float va[BT][4][DT];
 #pragma unroll
       for (int b = 0; b < BT; ++b)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int key = (kt0 + 4 * b) * 16 + 4 * g + i;
+          const int key = (kt0 + NW * b) * 16 + 4 * g + i;
           if (key < kn) {
             load_vec<DT>(vu + static_cast<size_t>(key) * D + DT * c, va[b][i]);
           } else {
@@ -525,7 +531,7 @@ __global__ __launch_bounds__(256) void attn_tile_kernel(AttnArgs a) {
         }
 #pragma unroll
       for (int b = 0; b < BT; ++b) {
-        const int kt = kt0 + 4 * b;
+        const int kt = kt0 + NW * b;
         if (kt < nkt) {
           const float4 s4 = *reinterpret_cast<const float4*>(&logits[c * kLStride + kt * 16 + 4 * g]);
           const float p[4] = {__expf(s4.x - mc), __expf(s4.y - mc), __expf(s4.z - mc), __expf(s4.w - mc)};
@@ -541,14 +547,14 @@ __global__ __launch_bounds__(256) void attn_tile_kernel(AttnArgs a) {
   psum = cross_rows_sum(psum);
   if (g == 0) zpart[wave][c] = psum;
   __syncthreads();  // logits are dead from here on: reuse them
-  float* red = logits;                 // [4 waves][16 centroids][D]
-  float* vhat = logits + 4 * 16 * D;   // [16][D]
-  int* mlist = reinterpret_cast<int*>(logits + 5 * 16 * D);  // member lists of the 16 clusters
-  static_assert(5 * 16 * D + kChunk <= 16 * kLStride, "logit area reuse");
+  float* red = logits;                 // [NW waves][16 centroids][D]
+  float* vhat = logits + NW * 16 * D;  // [16][D]
+  int* mlist = reinterpret_cast<int*>(logits + (NW + 1) * 16 * D);  // member lists of the 16 clusters
+  static_assert((NW + 1) * 16 * D + kChunk <= 16 * kLStride, "logit area reuse");
   if constexpr (FUSED) {
 #pragma unroll
-    for (int e = 0; e < kChunk / 256; ++e) {
-      const int x = tid + 256 * e;
+    for (int e = 0; e < kChunk / kTileThreads; ++e) {
+      const int x = tid + kTileThreads * e;
       if (x < mn) mlist[x] = mreg[e];
     }
   }
@@ -557,11 +563,14 @@ __global__ __launch_bounds__(256) void attn_tile_kernel(AttnArgs a) {
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) red[(wave * 16 + c) * D + DT * (4 * g + i) + dt] = oacc[dt][i];
   __syncthreads();
-  for (int x = tid; x < 16 * D; x += 256) {
+  for (int x = tid; x < 16 * D; x += kTileThreads) {
     const int cc = x / D, dim = x % D;
-    const float sum = ((red[(0 * 16 + cc) * D + dim] + red[(1 * 16 + cc) * D + dim]) +
-                       red[(2 * 16 + cc) * D + dim]) + red[(3 * 16 + cc) * D + dim];
-    float z = ((zpart[0][cc] + zpart[1][cc]) + zpart[2][cc]) + zpart[3][cc];
+    float sum = 0.0f, z = 0.0f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      sum += red[(w * 16 + cc) * D + dim];
+      z += zpart[w][cc];
+    }
     if constexpr (IMPROVED && FUSED) z += rowtop[cc];
     if (j0 + cc >= C) continue;
     const size_t ujc = static_cast<size_t>(u) * C + j0 + cc;
@@ -590,9 +599,10 @@ __global__ __launch_bounds__(256) void attn_tile_kernel(AttnArgs a) {
     // ---- fused outputs: every member row of the 16 clusters ---------------------
     const T* qu = static_cast<const T*>(a.q) + static_cast<size_t>(u) * a.N * D;
     T* ou = static_cast<T*>(a.out) + static_cast<size_t>(u) * a.N * D;
+    constexpr int RPW = 16 / NW;  // clusters per wave
     if constexpr (!IMPROVED) {
-      for (int rr = 0; rr < 4; ++rr) {
-        const int r = wave * 4 + rr;
+      for (int rr = 0; rr < RPW; ++rr) {
+        const int r = wave * RPW + rr;
         const int j = j0 + r;
         if (j >= C) break;
         const int sz = moff[r + 1] - moff[r];
@@ -610,19 +620,19 @@ __global__ __launch_bounds__(256) void attn_tile_kernel(AttnArgs a) {
     } else {
       // the operands of PF clusters are requested together, then used
       constexpr int PER_CLUSTER = NKT * D / 2 + D / 4;  // registers per cluster
-      constexpr int PF = PER_CLUSTER * 4 <= 160 ? 4 : PER_CLUSTER * 2 <= 160 ? 2 : 1;
-      for (int rb = 0; rb < 4; rb += PF) {
+      constexpr int PF = PER_CLUSTER * RPW <= 64 ? RPW : 1;
+      for (int rb = 0; rb < RPW; rb += PF) {
         SparseOps<D, T, NKT> S[PF];
 #pragma unroll
         for (int e = 0; e < PF; ++e) {
-          const int r = wave * 4 + rb + e;
+          const int r = wave * RPW + rb + e;
           const int sz = j0 + r < C ? moff[r + 1] - moff[r] : 0;
           if (sz > 0)
             sparse_load<D, T, NKT>(tpos16[r], tcnt[r], mlist + (moff[r] - m0), sz, qu, ku, vu, S[e]);
         }
 #pragma unroll
         for (int e = 0; e < PF; ++e) {
-          const int r = wave * 4 + rb + e;
+          const int r = wave * RPW + rb + e;
           const int sz = j0 + r < C ? moff[r + 1] - moff[r] : 0;
           if (sz > 0)
             sparse_run<D, T, NKT>(S[e], tcnt[r], rowmass[r], &vhat[r * D], mlist + (moff[r] - m0), sz,
@@ -824,18 +834,18 @@ static hipError_t launch_attn_nkt(const Problem& p, const Workspace& ws, const i
   const dim3 g1(xcd_grid(static_cast<long long>(a.nchunk) * a.ntile * a.units));
   if (ws.nchunk == 1) {
     if (improved)
-      hipLaunchKernelGGL((attn_tile_kernel<D, T, 1, NKT>), g1, dim3(256), 0, s, a);
+      hipLaunchKernelGGL((attn_tile_kernel<D, T, 1, NKT>), g1, dim3(kTileThreads), 0, s, a);
     else
-      hipLaunchKernelGGL((attn_tile_kernel<D, T, 0, NKT>), g1, dim3(256), 0, s, a);
+      hipLaunchKernelGGL((attn_tile_kernel<D, T, 0, NKT>), g1, dim3(kTileThreads), 0, s, a);
     return hipGetLastError();
   }
   const dim3 g2(xcd_grid(static_cast<long long>(a.ncg) * a.units));
   if (improved) {
-    hipLaunchKernelGGL((attn_tile_kernel<D, T, 3, NKT>), g1, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((attn_tile_kernel<D, T, 3, NKT>), g1, dim3(kTileThreads), 0, s, a);
     hipLaunchKernelGGL((attn_merge_kernel<D, T, true>), g2, dim3(256), 0, s, a);
     hipLaunchKernelGGL((sparse_kernel<D, T, NKT>), g2, dim3(256), 0, s, a);
   } else {
-    hipLaunchKernelGGL((attn_tile_kernel<D, T, 2, NKT>), g1, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((attn_tile_kernel<D, T, 2, NKT>), g1, dim3(kTileThreads), 0, s, a);
     hipLaunchKernelGGL((attn_merge_kernel<D, T, false>), g2, dim3(256), 0, s, a);
   }
   return hipGetLastError();
