@@ -104,6 +104,35 @@ def stage_work(w, stage, variant_topk):
     raise ValueError(stage)
 
 
+def kernel_source_hash():
+    """sha256 over the library's kernel sources (file names and contents)."""
+    import hashlib
+    d = os.path.join(ROOT, "paper_2007_04825_amd", "csrc")
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(d)):
+        if name.endswith((".hip", ".h")):
+            h.update(name.encode())
+            with open(os.path.join(d, name), "rb") as f:
+                h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(kernel_key):
+    """HBM bytes per launch of the given kernel from the committed counter
+    profile (FETCH_SIZE and WRITE_SIZE, each scaled by the same counter's
+    reading for a plain copy of known size), or None when there is no such
+    profile or the kernel sources changed after it was taken."""
+    path = os.path.join(ROOT, "profiles", "speech_b32h6n800_d32_f32_hbm_counters.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        prof = json.load(f)
+    if prof.get("source_sha256") != kernel_source_hash():
+        return None
+    entry = prof.get("kernels", {}).get(kernel_key)
+    return None if entry is None else entry.get("hbm_bytes_per_launch")
+
+
 def cpu_threads():
     """Host threads for the oracle: the CPU share of this process (its affinity
     mask, capped by OMP_NUM_THREADS when set)."""
@@ -258,9 +287,10 @@ def main():
 
     amount, unit, bound, peak = stage_work(w, name, var_topk)
     achieved = amount / (stage_ms * 1e-3) / (1e12 if unit != "GB/s" else 1e9)
+    kernel_key = "%s (%s)" % (name, "iclustered" if var_topk else "clustered")
     roof = {"bound": bound, "achieved": round(achieved, 3), "peak": peak, "unit": unit,
-            "frac": round(achieved / peak, 5), "traffic": None,
-            "kernel": "%s (%s)" % (name, "iclustered" if var_topk else "clustered"),
+            "frac": round(achieved / peak, 5), "traffic": measured_traffic(kernel_key),
+            "kernel": kernel_key,
             "avg_launch_us": round(stage_ms * 1e3, 3)}
     stages_us = {"%s_%s" % (n, "ic" if t else "c"): round(v * 1e3, 2) for (n, t), v in st.items()}
     cpu = None if args.no_cpu_baseline else cpu_baseline(w)
