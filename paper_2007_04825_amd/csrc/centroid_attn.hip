@@ -449,7 +449,7 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
       } else {
         const int kr = jsize > 0 ? kk : 0;
         uint32_t tau;
-        if (kk <= 16 * NT) {  // 2 * NT kept values per lane: at least 2 kk in the row
+        if (kk <= 16 * NT) {  // both slices' lists: 32 * NT values per row, at least 2 kk
           uint32_t keys[2 * NT];
 #pragma unroll
           for (int e = 0; e < NT; ++e) {
@@ -593,14 +593,14 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
       }
     }
   }
-  if constexpr (FUSED) {
+  if constexpr (FUSED && !IMPROVED) {
     __syncthreads();
 
-    // ---- fused outputs: every member row of the 16 clusters ---------------------
+    // ---- fused outputs (clustered): every member row of the 16 clusters ----------
     const T* qu = static_cast<const T*>(a.q) + static_cast<size_t>(u) * a.N * D;
     T* ou = static_cast<T*>(a.out) + static_cast<size_t>(u) * a.N * D;
     constexpr int RPW = 16 / NW;  // clusters per wave
-    if constexpr (!IMPROVED) {
+    {
       for (int rr = 0; rr < RPW; ++rr) {
         const int r = wave * RPW + rr;
         const int j = j0 + r;
@@ -615,28 +615,6 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
         for (int m1 = sub; m1 < sz; m1 += RPS) {
           const int qrow = mem[m1];
           store4(ou + static_cast<size_t>(qrow) * D + part * 4, val.x, val.y, val.z, val.w);
-        }
-      }
-    } else {
-      // the operands of PF clusters are requested together, then used
-      constexpr int PER_CLUSTER = NKT * D / 2 + D / 4;  // registers per cluster
-      constexpr int PF = PER_CLUSTER * RPW <= 64 ? RPW : 1;
-      for (int rb = 0; rb < RPW; rb += PF) {
-        SparseOps<D, T, NKT> S[PF];
-#pragma unroll
-        for (int e = 0; e < PF; ++e) {
-          const int r = wave * RPW + rb + e;
-          const int sz = j0 + r < C ? moff[r + 1] - moff[r] : 0;
-          if (sz > 0)
-            sparse_load<D, T, NKT>(tpos16[r], tcnt[r], mlist + (moff[r] - m0), sz, qu, ku, vu, S[e]);
-        }
-#pragma unroll
-        for (int e = 0; e < PF; ++e) {
-          const int r = wave * RPW + rb + e;
-          const int sz = j0 + r < C ? moff[r + 1] - moff[r] : 0;
-          if (sz > 0)
-            sparse_run<D, T, NKT>(S[e], tcnt[r], rowmass[r], &vhat[r * D], mlist + (moff[r] - m0), sz,
-                                  qu, ou, a.scale);
         }
       }
     }
@@ -762,8 +740,15 @@ __global__ __launch_bounds__(256) void sparse_kernel(AttnArgs a) {
   const int sz = a.sizes[uj];
   if (sz == 0) return;
   const int n = unit_length(a.lengths, u / a.heads, a.N);
-  const int kk = min(a.topk, n);
-  for (int x = lane; x < kk; x += 64) tp[wave][x] = a.topk_out[uj * a.topk + x];
+  // T: the leading non-negative entries (a caller-supplied set may be shorter)
+  const int kmax = min(a.topk, n);
+  int kk = 0;
+  for (int x0 = 0; x0 < kmax; x0 += 64) {
+    const int x = x0 + lane;
+    const int v = x < kmax ? a.topk_out[uj * a.topk + x] : -1;
+    if (v >= 0) tp[wave][x] = v;
+    kk += __popcll(__ballot(v >= 0));
+  }
   wave_lds_sync();
   const int32_t* mem = a.members + static_cast<size_t>(u) * a.N + a.offsets[static_cast<size_t>(u) * (C + 1) + j];
   const size_t base = static_cast<size_t>(u) * a.N * D;
@@ -832,14 +817,18 @@ static hipError_t launch_attn_nkt(const Problem& p, const Workspace& ws, const i
   const AttnArgs a = make_args(p, ws, topk_in);
   const bool improved = p.topk > 0;
   const dim3 g1(xcd_grid(static_cast<long long>(a.nchunk) * a.ntile * a.units));
+  const dim3 g2(xcd_grid(static_cast<long long>(a.ncg) * a.units));
   if (ws.nchunk == 1) {
-    if (improved)
+    if (improved) {
+      // the sparse part runs as its own kernel: its gathers want many waves in
+      // flight, which the LDS-heavy tile kernel cannot offer
       hipLaunchKernelGGL((attn_tile_kernel<D, T, 1, NKT>), g1, dim3(kTileThreads), 0, s, a);
-    else
+      hipLaunchKernelGGL((sparse_kernel<D, T, NKT>), g2, dim3(256), 0, s, a);
+    } else {
       hipLaunchKernelGGL((attn_tile_kernel<D, T, 0, NKT>), g1, dim3(kTileThreads), 0, s, a);
+    }
     return hipGetLastError();
   }
-  const dim3 g2(xcd_grid(static_cast<long long>(a.ncg) * a.units));
   if (improved) {
     hipLaunchKernelGGL((attn_tile_kernel<D, T, 3, NKT>), g1, dim3(kTileThreads), 0, s, a);
     hipLaunchKernelGGL((attn_merge_kernel<D, T, true>), g2, dim3(256), 0, s, a);

@@ -136,15 +136,21 @@ __device__ __forceinline__ int best_key(const v4i* cop, int nct, v4i bq, int lan
 template <int NG>
 __device__ __forceinline__ void best_keys(const v4i* cop, int nct, const v4i* bq, int* best, int lane) {
   const v4i zero = {0, 0, 0, 0};
-  v4i a = cop[lane];
-  for (int ct = 0; ct < nct; ++ct) {
-    const v4i an = cop[(ct + 1 < nct ? ct + 1 : ct) * 64 + lane];
-    v4i d[NG];
+  for (int ct0 = 0; ct0 < nct; ct0 += 4) {
+    // four centroid tiles requested together, then 4 x NG independent MFMAs
+    v4i a[4];
 #pragma unroll
-    for (int e = 0; e < NG; ++e) d[e] = mfma_i8_16x16x64(a, bq[e], zero);
+    for (int q = 0; q < 4; ++q) a[q] = cop[min(ct0 + q, nct - 1) * 64 + lane];
 #pragma unroll
-    for (int e = 0; e < NG; ++e) best[e] = max(best[e], max(max(d[e][0], d[e][1]), max(d[e][2], d[e][3])));
-    a = an;
+    for (int q = 0; q < 4; ++q) {
+      if (ct0 + q < nct) {
+        v4i d[NG];
+#pragma unroll
+        for (int e = 0; e < NG; ++e) d[e] = mfma_i8_16x16x64(a[q], bq[e], zero);
+#pragma unroll
+        for (int e = 0; e < NG; ++e) best[e] = max(best[e], max(max(d[e][0], d[e][1]), max(d[e][2], d[e][3])));
+      }
+    }
   }
 #pragma unroll
   for (int e = 0; e < NG; ++e) {
@@ -286,6 +292,16 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
 
   // ---- K-means ---------------------------------------------------------------
   build_centroid_operands(sh.cop, sh.cent, ce, nct, n_bits, tid, kKmThreads);
+  // operands of this wave's first four query tiles, built once: the codes
+  // never change (tiles past those are rebuilt in each round)
+  v4i bq0[4];
+  uint64_t code0[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int qb = (wave + e * kKmWaves) * 16 + c;
+    code0[e] = qb < n ? sh.codes[qb] : 0ull;
+    bq0[e] = query_operand_lut(code0[e], g, qm, sh.qlut);
+  }
   for (int t = 0; t < f.L; ++t) {
     if (tid == 0) sh.nchange = 0;
     __syncthreads();
@@ -299,9 +315,14 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
       uint64_t mycode[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const int qb = (wave + (s0 + e) * kKmWaves) * 16 + c;
-        mycode[e] = qb < n ? sh.codes[qb] : 0ull;
-        bq[e] = query_operand_lut(mycode[e], g, qm, sh.qlut);
+        if (s0 == 0) {
+          mycode[e] = code0[e];
+          bq[e] = bq0[e];
+        } else {
+          const int qb = (wave + (s0 + e) * kKmWaves) * 16 + c;
+          mycode[e] = qb < n ? sh.codes[qb] : 0ull;
+          bq[e] = query_operand_lut(mycode[e], g, qm, sh.qlut);
+        }
         best[e] = INT_MIN;
       }
       best_keys_n(left < 4 ? left : 4, sh.cop, nct, bq, best, lane);
@@ -464,11 +485,11 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
   // ---- centroids, Eq. (3) ---------------------------------------------------------
   // D lanes per cluster (lane = dimension) add the member rows in ascending
   // query order, one fp64 addition after the other; groups take clusters
-  // grp, grp + G, ... and request the first rows of their next cluster before
-  // summing the current one
+  // grp, grp + G, ..., four at a time with the first rows of all four
+  // requested together
   constexpr int GPW = 64 / D;        // lane groups per wave
   constexpr int G = kKmWaves * GPW;  // lane groups per workgroup
-  constexpr int BATCH = 16;          // rows in flight per lane
+  constexpr int BATCH = 8;           // rows per cluster requested up front
   const int t = lane % D, grp = wave * GPW + lane / D;
   auto fetch = [&](int j, int m0, float* x) {
     const int sz = sh.size[j];
@@ -479,28 +500,42 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
       x[e] = m < sz ? to_f32(qu[static_cast<size_t>(ml[m]) * D + t]) : 0.0f;
     }
   };
-  float xa[BATCH];
-  if (grp < ce) fetch(grp, 0, xa);
-  for (int j = grp; j < ce; j += G) {
-    float xb[BATCH];
+  for (int j0c = grp; j0c < ce; j0c += 4 * G) {
+    float xa[4][BATCH];
 #pragma unroll
-    for (int e = 0; e < BATCH; ++e) xb[e] = 0.0f;
-    if (j + G < ce) fetch(j + G, 0, xb);
-    const int sz = sh.size[j];
-    double acc = 0.0;
+    for (int q = 0; q < 4; ++q) {
+      const int j = j0c + q * G;
+      if (j < ce) {
+        fetch(j, 0, xa[q]);
+      } else {
 #pragma unroll
-    for (int e = 0; e < BATCH; ++e)
-      if (e < sz) acc += static_cast<double>(xa[e]);
-    for (int m0 = BATCH; m0 < sz; m0 += BATCH) {
-      float y[BATCH];
-      fetch(j, m0, y);
+        for (int e = 0; e < BATCH; ++e) xa[q][e] = 0.0f;
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int j = j0c + q * G;
+      if (j >= ce) break;
+      const int sz = sh.size[j];
+      double acc = 0.0;
 #pragma unroll
       for (int e = 0; e < BATCH; ++e)
-        if (m0 + e < sz) acc += static_cast<double>(y[e]);
-    }
-    f.qc[(static_cast<size_t>(u) * C + j) * D + t] = sz > 0 ? static_cast<float>(acc / static_cast<double>(sz)) : 0.0f;
+        if (e < sz) acc += static_cast<double>(xa[q][e]);
+      // larger clusters: 16 more rows in flight at a time
+      const int* ml = mem + off[j];
+      for (int m0 = BATCH; m0 < sz; m0 += 16) {
+        float y[16];
 #pragma unroll
-    for (int e = 0; e < BATCH; ++e) xa[e] = xb[e];
+        for (int e = 0; e < 16; ++e) {
+          const int m = m0 + e;
+          y[e] = m < sz ? to_f32(qu[static_cast<size_t>(ml[m]) * D + t]) : 0.0f;
+        }
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+          if (m0 + e < sz) acc += static_cast<double>(y[e]);
+      }
+      f.qc[(static_cast<size_t>(u) * C + j) * D + t] = sz > 0 ? static_cast<float>(acc / static_cast<double>(sz)) : 0.0f;
+    }
   }
   for (int x = ce * D + tid; x < C * D; x += kKmThreads) f.qc[static_cast<size_t>(u) * C * D + x] = 0.0f;
 }

@@ -199,19 +199,58 @@ __device__ __forceinline__ uint32_t group_field(uint64_t ballot) {
   return static_cast<uint32_t>(ballot >> (threadIdx.x & 48)) & 0xffffu;
 }
 
+// Bitwise AND / OR / integer max over the 16 lanes of a row.
+__device__ __forceinline__ uint32_t row16_and(uint32_t x) {
+  x &= static_cast<uint32_t>(dpp_i<0xB1>(static_cast<int>(x)));
+  x &= static_cast<uint32_t>(dpp_i<0x4E>(static_cast<int>(x)));
+  x &= static_cast<uint32_t>(dpp_i<0x141>(static_cast<int>(x)));
+  return x & static_cast<uint32_t>(dpp_i<0x140>(static_cast<int>(x)));
+}
+__device__ __forceinline__ uint32_t row16_or(uint32_t x) {
+  x |= static_cast<uint32_t>(dpp_i<0xB1>(static_cast<int>(x)));
+  x |= static_cast<uint32_t>(dpp_i<0x4E>(static_cast<int>(x)));
+  x |= static_cast<uint32_t>(dpp_i<0x141>(static_cast<int>(x)));
+  return x | static_cast<uint32_t>(dpp_i<0x140>(static_cast<int>(x)));
+}
+__device__ __forceinline__ int wave_max_i(int x) {
+  x = max(x, dpp_i<0xB1>(x));
+  x = max(x, dpp_i<0x4E>(x));
+  x = max(x, dpp_i<0x141>(x));
+  x = max(x, dpp_i<0x140>(x));
+  return cross_rows_max(x);
+}
+
 // The kk-th largest of the keys held by the group (NK per lane, 0 = none):
-// the largest T with at least kk keys >= T, one bit at a time.
+// the largest T with at least kk keys >= T, one bit at a time from the most
+// significant down.  The bits that all of the group's keys share are taken as
+// they are (the answer is one of the keys), so the search starts at the
+// highest bit where they differ; the loop runs to the wave's highest such
+// bit, and the extra steps leave a group's result unchanged.  kk = 0 gives
+// 0xffffffff (nothing reaches it).
 template <int NK>
 __device__ __forceinline__ uint32_t group_kth_key(const uint32_t* keys, int kk) {
-  uint32_t t = 0;
-  for (int bit = 31; bit >= 0; --bit) {
+  uint32_t a = 0xffffffffu, o = 0u;
+#pragma unroll
+  for (int e = 0; e < NK; ++e) {
+    if (keys[e] != 0u) {
+      a &= keys[e];
+      o |= keys[e];
+    }
+  }
+  a = row16_and(a);
+  o = row16_or(o);
+  const uint32_t diff = (o != 0u) ? (a ^ o) : 0u;
+  const int hb = diff != 0u ? 31 - __clz(static_cast<int>(diff)) : -1;
+  uint32_t t = hb >= 0 ? (o & ~((2u << hb) - 1u)) : o;  // the common prefix, zeros below
+  const int top = __builtin_amdgcn_readfirstlane(wave_max_i(hb));  // uniform loop bound
+  for (int bit = top; bit >= 0; --bit) {
     const uint32_t cand = t | (1u << bit);
     int cnt = 0;
 #pragma unroll
     for (int e = 0; e < NK; ++e) cnt += keys[e] >= cand ? 1 : 0;
     if (row16_sum_i(cnt) >= kk) t = cand;
   }
-  return t;
+  return kk > 0 ? t : 0xffffffffu;
 }
 
 // Top-kk positions of the group's row row[0..m) (0 <= kk, kk <= m), ties to
