@@ -78,12 +78,8 @@ def stage_work(w, stage, variant_topk):
     nsum = int(w.lengths.astype(np.int64).sum()) * H        # valid queries = valid keys
     s = 4 if w.dtype == "f32" else 2
     if stage == "centroid_attn":
-        # Q^c K^T and A^c V: 2 * C * n * d flops each, per (sequence, head); the
-        # improved variant's kernel also does the sparse part, Q_i K_T^T and
-        # A^t V_T: 2 * n * k * d flops each
+        # Q^c K^T and A^c V: 2 * C * n * d flops each, per (sequence, head)
         flops = 4.0 * w.C * nsum * D
-        if variant_topk:
-            flops += 4.0 * nsum * variant_topk * D
         return flops, "TFLOP/s", "mfma", PEAKS["fp32_mfma_TFLOPs"]
     if stage == "kmeans":
         # L rounds x n x C Hamming distances, each a 64-entry int8 dot product
@@ -94,7 +90,9 @@ def stage_work(w, stage, variant_topk):
         return byts, "GB/s", "hbm", PEAKS["hbm_GBps"]
     if stage == "output":
         if variant_topk:
-            byts = 2 * nsum * D * s                             # gather Q, scatter out
+            # improved per-query part: gather Q, the T rows of K and V (C k rows
+            # each per sequence and head), scatter out
+            byts = 2 * nsum * D * s + 2 * H * w.q.shape[0] * w.C * variant_topk * D * s
         else:
             byts = nsum * D * s + nsum * 4                      # write out, read assign
         return byts, "GB/s", "hbm", PEAKS["hbm_GBps"]

@@ -180,6 +180,7 @@ static int run_forward(const void* q, const void* k, const void* v, const int32_
   CA_TRY(launch_centroid_attention(p, ws, improved && aux ? aux->topk_in : nullptr, s));
   CA_TRY(mark(CA_KERNEL_CENTROID_ATTN, false, s));
   CA_TRY(mark(CA_KERNEL_OUTPUT, true, s));
+  if (improved) CA_TRY(launch_sparse(p, ws, s));
   if (!improved && ws.nchunk > 1) {
     CA_TRY(launch_broadcast(p, ws.assign, ws, s));  // also zeroes the padded rows
   } else if (lengths && (assign_given || (codes_in && !kmeans_uses_lds(p)))) {

@@ -295,7 +295,7 @@ struct AttnArgs {
 // fused improved case, those of T, which the second product leaves out); the
 // top-k threshold is the k-th largest of the slices' kept values (k <= 32;
 // larger k take it from a sweep of the row).
-template <int D, typename T, int MODE, int NKT>
+template <int D, typename T, int MODE>
 __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
   constexpr bool IMPROVED = (MODE & 1) != 0;
   constexpr bool FUSED = MODE < 2;
@@ -811,53 +811,58 @@ static AttnArgs make_args(const Problem& p, const Workspace& ws, const int32_t* 
 // Key tiles of the register-resident sparse routine (k <= 16 * NKT).
 static int sparse_tiles(int topk) { return topk <= 16 ? 1 : topk <= 32 ? 2 : topk <= 64 ? 4 : 8; }
 
-template <int D, typename T, int NKT>
-static hipError_t launch_attn_nkt(const Problem& p, const Workspace& ws, const int32_t* topk_in,
-                                  hipStream_t s) {
+template <int D, typename T>
+static hipError_t launch_attn_t(const Problem& p, const Workspace& ws, const int32_t* topk_in,
+                                hipStream_t s) {
   const AttnArgs a = make_args(p, ws, topk_in);
   const bool improved = p.topk > 0;
   const dim3 g1(xcd_grid(static_cast<long long>(a.nchunk) * a.ntile * a.units));
   const dim3 g2(xcd_grid(static_cast<long long>(a.ncg) * a.units));
   if (ws.nchunk == 1) {
-    if (improved) {
-      // the sparse part runs as its own kernel: its gathers want many waves in
-      // flight, which the LDS-heavy tile kernel cannot offer
-      hipLaunchKernelGGL((attn_tile_kernel<D, T, 1, NKT>), g1, dim3(kTileThreads), 0, s, a);
-      hipLaunchKernelGGL((sparse_kernel<D, T, NKT>), g2, dim3(256), 0, s, a);
-    } else {
-      hipLaunchKernelGGL((attn_tile_kernel<D, T, 0, NKT>), g1, dim3(kTileThreads), 0, s, a);
-    }
+    if (improved)
+      hipLaunchKernelGGL((attn_tile_kernel<D, T, 1>), g1, dim3(kTileThreads), 0, s, a);
+    else
+      hipLaunchKernelGGL((attn_tile_kernel<D, T, 0>), g1, dim3(kTileThreads), 0, s, a);
     return hipGetLastError();
   }
   if (improved) {
-    hipLaunchKernelGGL((attn_tile_kernel<D, T, 3, NKT>), g1, dim3(kTileThreads), 0, s, a);
+    hipLaunchKernelGGL((attn_tile_kernel<D, T, 3>), g1, dim3(kTileThreads), 0, s, a);
     hipLaunchKernelGGL((attn_merge_kernel<D, T, true>), g2, dim3(256), 0, s, a);
-    hipLaunchKernelGGL((sparse_kernel<D, T, NKT>), g2, dim3(256), 0, s, a);
   } else {
-    hipLaunchKernelGGL((attn_tile_kernel<D, T, 2, NKT>), g1, dim3(kTileThreads), 0, s, a);
+    hipLaunchKernelGGL((attn_tile_kernel<D, T, 2>), g1, dim3(kTileThreads), 0, s, a);
     hipLaunchKernelGGL((attn_merge_kernel<D, T, false>), g2, dim3(256), 0, s, a);
   }
   return hipGetLastError();
 }
 
+// The per-query improved values run as their own kernel: their gathers of the
+// T rows want many waves in flight, which the LDS-heavy tile kernel cannot
+// offer.
 template <int D, typename T>
-static hipError_t launch_attn_dt(const Problem& p, const Workspace& ws, const int32_t* topk_in,
-                                 hipStream_t s) {
-  if (p.topk <= 0) return launch_attn_nkt<D, T, 1>(p, ws, topk_in, s);
+static hipError_t launch_sparse_t(const Problem& p, const Workspace& ws, hipStream_t s) {
+  const AttnArgs a = make_args(p, ws, nullptr);
+  const dim3 g2(xcd_grid(static_cast<long long>(a.ncg) * a.units));
   switch (sparse_tiles(p.topk)) {
-    case 1: return launch_attn_nkt<D, T, 1>(p, ws, topk_in, s);
-    case 2: return launch_attn_nkt<D, T, 2>(p, ws, topk_in, s);
-    case 4: return launch_attn_nkt<D, T, 4>(p, ws, topk_in, s);
-    default: return launch_attn_nkt<D, T, 8>(p, ws, topk_in, s);
+    case 1: hipLaunchKernelGGL((sparse_kernel<D, T, 1>), g2, dim3(256), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((sparse_kernel<D, T, 2>), g2, dim3(256), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((sparse_kernel<D, T, 4>), g2, dim3(256), 0, s, a); break;
+    default: hipLaunchKernelGGL((sparse_kernel<D, T, 8>), g2, dim3(256), 0, s, a); break;
   }
+  return hipGetLastError();
 }
 
-// Centroid attention and everything after it: clustered -> out via Eq. (6),
-// improved -> top-k, mass, rest part and the improved values.
+// Centroid attention: softmax statistics, values (and, clustered in one key
+// chunk, the output rows via Eq. (6)); improved: top-k, mass and rest part.
 hipError_t launch_centroid_attention(const Problem& p, const Workspace& ws, const int32_t* topk_in,
                                      hipStream_t s) {
-  if (p.d == 32) return p.dtype == 0 ? launch_attn_dt<32, float>(p, ws, topk_in, s) : launch_attn_dt<32, bf16_t>(p, ws, topk_in, s);
-  return p.dtype == 0 ? launch_attn_dt<64, float>(p, ws, topk_in, s) : launch_attn_dt<64, bf16_t>(p, ws, topk_in, s);
+  if (p.d == 32) return p.dtype == 0 ? launch_attn_t<32, float>(p, ws, topk_in, s) : launch_attn_t<32, bf16_t>(p, ws, topk_in, s);
+  return p.dtype == 0 ? launch_attn_t<64, float>(p, ws, topk_in, s) : launch_attn_t<64, bf16_t>(p, ws, topk_in, s);
+}
+
+// Improved values of every member query (Section 3.3).
+hipError_t launch_sparse(const Problem& p, const Workspace& ws, hipStream_t s) {
+  if (p.d == 32) return p.dtype == 0 ? launch_sparse_t<32, float>(p, ws, s) : launch_sparse_t<32, bf16_t>(p, ws, s);
+  return p.dtype == 0 ? launch_sparse_t<64, float>(p, ws, s) : launch_sparse_t<64, bf16_t>(p, ws, s);
 }
 
 }  // namespace ca

@@ -71,11 +71,12 @@ hipError_t launch_load_assign(const Problem& p, const int32_t* assign_in, const 
                               hipStream_t s);
 hipError_t launch_csr(const Problem& p, const int32_t* assign, const Workspace& ws, hipStream_t s);
 hipError_t launch_centroids(const Problem& p, const Workspace& ws, hipStream_t s);
-// Centroid attention and, when every sequence fits in one key chunk, the
-// output rows; for longer sequences the improved output rows as well (the
-// clustered ones then come from launch_broadcast).
+// Centroid attention: softmax statistics and values; clustered in one key
+// chunk also the output rows (otherwise launch_broadcast writes them);
+// improved: top-k, mass and rest part (launch_sparse then writes the rows).
 hipError_t launch_centroid_attention(const Problem& p, const Workspace& ws, const int32_t* topk_in,
                                      hipStream_t s);
+hipError_t launch_sparse(const Problem& p, const Workspace& ws, hipStream_t s);
 hipError_t launch_broadcast(const Problem& p, const int32_t* assign, const Workspace& ws,
                             hipStream_t s);
 hipError_t launch_pad_zero(const Problem& p, hipStream_t s);
