@@ -138,18 +138,23 @@ __device__ __forceinline__ void best_keys(const v4i* cop, int nct, const v4i* bq
   const v4i zero = {0, 0, 0, 0};
   for (int ct0 = 0; ct0 < nct; ct0 += 4) {
     // four centroid tiles requested together, then 4 x NG independent MFMAs
+    // (past the last tile the last one repeats, which leaves the maxima as
+    // they are and keeps the sequence free of branches)
     v4i a[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) a[q] = cop[min(ct0 + q, nct - 1) * 64 + lane];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      if (ct0 + q < nct) {
-        v4i d[NG];
+    for (int q0 = 0; q0 < 4; q0 += 2) {  // two tiles' products in flight at a time
+      v4i d[2][NG];
 #pragma unroll
-        for (int e = 0; e < NG; ++e) d[e] = mfma_i8_16x16x64(a[q], bq[e], zero);
+      for (int q = 0; q < 2; ++q)
 #pragma unroll
-        for (int e = 0; e < NG; ++e) best[e] = max(best[e], max(max(d[e][0], d[e][1]), max(d[e][2], d[e][3])));
-      }
+        for (int e = 0; e < NG; ++e) d[q][e] = mfma_i8_16x16x64(a[q0 + q], bq[e], zero);
+#pragma unroll
+      for (int q = 0; q < 2; ++q)
+#pragma unroll
+        for (int e = 0; e < NG; ++e)
+          best[e] = max(best[e], max(max(d[q][e][0], d[q][e][1]), max(d[q][e][2], d[q][e][3])));
     }
   }
 #pragma unroll
@@ -194,7 +199,7 @@ struct KmShared {
   uint64_t cent[kCmax];
   v4i cop[kCmax / 16 * 64];
   uint2 qlut[256];
-  int nchange;
+  int nchange[2];  // queries moved in the current round (double buffered)
 };
 
 struct FrontArgs {
@@ -276,6 +281,7 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
   for (int i = tid; i < n; i += kKmThreads) sh.assign[i] = -1;
   for (int x = tid; x < kCmax * kCntStride; x += kKmThreads) sh.cnt[x] = 0;
   for (int j = tid; j < kCmax; j += kKmThreads) sh.size[j] = 0;
+  if (tid < 2) sh.nchange[tid] = 0;
   __syncthreads();
   for (int j = tid; j < ce; j += kKmThreads)
     sh.cent[j] = sh.codes[(static_cast<int64_t>(j) * n) / ce];
@@ -292,6 +298,7 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
 
   // ---- K-means ---------------------------------------------------------------
   build_centroid_operands(sh.cop, sh.cent, ce, nct, n_bits, tid, kKmThreads);
+  __syncthreads();  // the first assign step reads every centroid operand
   // operands of this wave's first four query tiles, built once: the codes
   // never change (tiles past those are rebuilt in each round)
   v4i bq0[4];
@@ -303,8 +310,8 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
     bq0[e] = query_operand_lut(code0[e], g, qm, sh.qlut);
   }
   for (int t = 0; t < f.L; ++t) {
-    if (tid == 0) sh.nchange = 0;
-    __syncthreads();
+    // round t counts in nchange[t & 1]; the other one is cleared during this
+    // round's update, after every thread has read it in the previous round
     // assign (up to four query tiles share every centroid-operand load); the
     // queries whose cluster changed move their bit counts right away
     for (int s0 = 0; s0 < kMaxQt; s0 += 4) {
@@ -380,12 +387,13 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
           }
         }
       }
-      if (lane == 0 && nchg > 0) atomicAdd(&sh.nchange, nchg);
+      if (lane == 0 && nchg > 0) atomicAdd(&sh.nchange[t & 1], nchg);
     }
     __syncthreads();
     // no query moved: every later round would repeat this assignment
-    if (sh.nchange == 0) break;
+    if (sh.nchange[t & 1] == 0) break;
     if (t == f.L - 1) break;
+    if (tid == 0) sh.nchange[(t + 1) & 1] = 0;
     // majority update fused with the operand rebuild: thread (tile, lane)
     // forms the 16 bits of k-group g of centroid j (slots past C_eff copy
     // centroid 0 with tie byte 255); an empty cluster keeps its operands
