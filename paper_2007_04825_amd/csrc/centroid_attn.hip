@@ -288,12 +288,12 @@ struct AttnArgs {
 //
 // Row statistics come from where the data already is: while the logits of a
 // key tile sit in the result registers of the first product, each lane (one
-// of the 16 slices of a centroid row: four waves x four lane groups) keeps its
+// of the 32 slices of a centroid row: eight waves x four lane groups) keeps its
 // running maximum and, for the improved variant, its four largest logits.
 // The row maximum is the maximum of the slice maxima; the normaliser z is the
 // sum of the same exponentials that the second product uses (plus, in the
 // fused improved case, those of T, which the second product leaves out); the
-// top-k threshold is the k-th largest of the slices' kept values (k <= 32;
+// top-k threshold is the k-th largest of the slices' kept values (k <= 64;
 // larger k take it from a sweep of the row).
 template <int D, typename T, int MODE>
 __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
@@ -419,14 +419,16 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
   __syncthreads();
 
   // ---- row maximum and top-k ----------------------------------------------------------
-  // waves 0-3: wave w owns rows 4w..4w+3, one 16-lane group per row, all four at
-  // once; lane c16 of a group reads slices c16 and c16 + 16
-  if (wave < 4) {
-    const int g4 = lane >> 4, c16 = lane & 15;
-    const int r = wave * 4 + g4;
+  // wave w owns rows 2w and 2w + 1, one 32-lane group per row, both at once;
+  // lane c32 of a group reads slice c32
+  static_assert(NW == 8 && NS == 32, "two rows per wave, one slice per lane");
+  {
+    constexpr int GL = 32;
+    const int g2 = lane >> 5, c32 = lane & 31;
+    const int r = wave * 2 + g2;
     const int j = j0 + r;
     float* row = &logits[r * kLStride];
-    const float mx = row16_max(fmaxf(smax[r][c16], smax[r][c16 + 16]));
+    const float mx = grp_max<GL>(smax[r][c32]);
     if constexpr (IMPROVED) {
       const int kk = min(a.topk, kn);
       const size_t uj = static_cast<size_t>(u) * C + (j < C ? j : 0);
@@ -438,62 +440,59 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
         // out-of-range one, in the given order
         const int32_t* tin = a.topk_in + uj * a.topk;
         int first_bad = a.topk;
-        for (int x = c16; x < a.topk; x += 16) {
+        for (int x = c32; x < a.topk; x += GL) {
           const int key = tin[x];
           if ((key < 0 || key >= kn) && x < first_bad) first_bad = x;
         }
-        first_bad = -static_cast<int>(row16_max(static_cast<float>(-first_bad)));
+        first_bad = -static_cast<int>(grp_max<GL>(static_cast<float>(-first_bad)));
         cnt = jsize > 0 ? min(first_bad, kCandCap) : 0;
-        for (int x = c16; x < cnt; x += 16) cand[x] = static_cast<uint16_t>(tin[x]);
+        for (int x = c32; x < cnt; x += GL) cand[x] = static_cast<uint16_t>(tin[x]);
         wave_lds_sync();
       } else {
         const int kr = jsize > 0 ? kk : 0;
         uint32_t tau;
-        if (kk <= 16 * NT) {  // both slices' lists: 32 * NT values per row, at least 2 kk
-          uint32_t keys[2 * NT];
+        if (kk <= 16 * NT) {  // the slices' lists: 32 * NT values per row, at least 2 kk
+          uint32_t keys[NT];
 #pragma unroll
           for (int e = 0; e < NT; ++e) {
-            const float v0 = stop[r][c16][e], v1 = stop[r][c16 + 16][e];
-            keys[e] = v0 > -INFINITY ? order_key(v0) : 0u;
-            keys[NT + e] = v1 > -INFINITY ? order_key(v1) : 0u;
+            const float v = stop[r][c32][e];
+            keys[e] = v > -INFINITY ? order_key(v) : 0u;
           }
-          tau = group_kth_key<2 * NT>(keys, kr);
-        } else if (kk <= 64) {
-          tau = group_row_threshold<8>(row, kn, kr);
-        } else {
-          tau = group_row_threshold<16>(row, kn, kr);
+          tau = group_kth_key<NT, GL>(keys, kr);
+        } else {  // a sweep of the row: 8 values per lane, 256 per row, at least 2 kk
+          tau = group_row_threshold<8, GL>(row, kn, kr);
         }
-        cnt = group_select<kCandCap>(row, kn, kr, tau, cand);
+        cnt = group_select<kCandCap, GL>(row, kn, kr, tau, cand);
         // rows whose threshold let too many entries through (many ties): the
         // whole wave selects them one after the other; its scratch is the
-        // slice area of its own rows, consumed by now
+        // slice area of its own two rows, consumed by now
         const uint64_t over = __ballot(cnt < 0);
-        for (int gg = 0; gg < 4; ++gg) {
-          if (((over >> (16 * gg)) & 1ull) == 0ull) continue;
-          const int rg = wave * 4 + gg;
+        for (int gg = 0; gg < 2; ++gg) {
+          if (((over >> (32 * gg)) & 1ull) == 0ull) continue;
+          const int rg = wave * 2 + gg;
           float md, zd;
           const int cg = wave_topk_row<kCandCap>(&logits[rg * kLStride], kn, kk,
-                                                 reinterpret_cast<int*>(&stop[4 * wave][0][0]),
+                                                 reinterpret_cast<int*>(&stop[2 * wave][0][0]),
                                                  tpos16[rg], &md, &zd);
           wave_lds_sync();
-          if (g4 == gg) cnt = cg;
+          if (g2 == gg) cnt = cg;
         }
       }
       // sum over T of exp(s - max) (the numerator of the mass)
       float tsum = 0.0f;
-      for (int x = c16; x < cnt; x += 16) tsum += __expf(row[cand[x]] - mx);
-      tsum = row16_sum(tsum);
+      for (int x = c32; x < cnt; x += GL) tsum += __expf(row[cand[x]] - mx);
+      tsum = grp_sum<GL>(tsum);
       if constexpr (FUSED) {
         // T masked out of the row so that P V gives the rest part
         wave_lds_sync();
-        for (int x = c16; x < cnt; x += 16) row[cand[x]] = -INFINITY;
+        for (int x = c32; x < cnt; x += GL) row[cand[x]] = -INFINITY;
         if (j < C)
-          for (int x = c16; x < a.topk; x += 16) a.topk_out[uj * a.topk + x] = x < cnt ? cand[x] : -1;
-        if (c16 == 0) tcnt[r] = cnt;
+          for (int x = c32; x < a.topk; x += GL) a.topk_out[uj * a.topk + x] = x < cnt ? cand[x] : -1;
+        if (c32 == 0) tcnt[r] = cnt;
       } else {
         if (j < C) {
           const size_t cb = (uj * a.nchunk + chunk) * a.topk;
-          for (int x = c16; x < a.topk; x += 16) {
+          for (int x = c32; x < a.topk; x += GL) {
             const bool ok = x < cnt;
             const int pos = ok ? cand[x] : 0;
             a.cand_idx[cb + x] = ok ? k0 + pos : -1;
@@ -501,10 +500,10 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
           }
         }
       }
-      if (c16 == 0) rowtop[r] = tsum;
+      if (c32 == 0) rowtop[r] = tsum;
       wave_lds_sync();
     }
-    if (c16 == 0) rowm[r] = mx;
+    if (c32 == 0) rowm[r] = mx;
   }
   __syncthreads();
 

@@ -184,9 +184,10 @@ __device__ int wave_topk_row(const float* row, int m, int kk, int* scratch, OutT
 }
 
 // ---------------------------------------------------------------------------
-// Four rows per wave at once: the 16-lane group g = lane / 16 owns row g, and
-// lane c = lane % 16 of the group reads positions c, c + 16, c + 32, ...
-// Reductions stay inside a group (DPP row operations).
+// Rows handled by lane groups: with GL-lane groups (GL = 16 or 32), group
+// g = lane / GL owns a row and lane c = lane % GL of the group reads positions
+// c, c + GL, c + 2 GL, ...  Reductions stay inside a group: DPP row operations
+// within 16 lanes and, for 32-lane groups, one swap between the two rows.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ int row16_sum_i(int x) {
   x += dpp_i<0xB1>(x);
@@ -194,12 +195,6 @@ __device__ __forceinline__ int row16_sum_i(int x) {
   x += dpp_i<0x141>(x);
   return x + dpp_i<0x140>(x);
 }
-__device__ __forceinline__ uint32_t lanemask_lt16() { return (1u << (threadIdx.x & 15)) - 1u; }
-__device__ __forceinline__ uint32_t group_field(uint64_t ballot) {
-  return static_cast<uint32_t>(ballot >> (threadIdx.x & 48)) & 0xffffu;
-}
-
-// Bitwise AND / OR / integer max over the 16 lanes of a row.
 __device__ __forceinline__ uint32_t row16_and(uint32_t x) {
   x &= static_cast<uint32_t>(dpp_i<0xB1>(static_cast<int>(x)));
   x &= static_cast<uint32_t>(dpp_i<0x4E>(static_cast<int>(x)));
@@ -220,6 +215,40 @@ __device__ __forceinline__ int wave_max_i(int x) {
   return cross_rows_max(x);
 }
 
+template <int GL> __device__ __forceinline__ int grp_sum_i(int x) {
+  x = row16_sum_i(x);
+  if constexpr (GL == 32) x += lane_xor16(x);
+  return x;
+}
+template <int GL> __device__ __forceinline__ float grp_sum(float x) {
+  x = row16_sum(x);
+  if constexpr (GL == 32) x += lane_xor16(x);
+  return x;
+}
+template <int GL> __device__ __forceinline__ float grp_max(float x) {
+  x = row16_max(x);
+  if constexpr (GL == 32) x = fmaxf(x, lane_xor16(x));
+  return x;
+}
+template <int GL> __device__ __forceinline__ uint32_t grp_and(uint32_t x) {
+  x = row16_and(x);
+  if constexpr (GL == 32) x &= lane_xor16_u(x);
+  return x;
+}
+template <int GL> __device__ __forceinline__ uint32_t grp_or(uint32_t x) {
+  x = row16_or(x);
+  if constexpr (GL == 32) x |= lane_xor16_u(x);
+  return x;
+}
+// This lane's group's bits of a wave ballot, and the lanes of the group below this one.
+template <int GL> __device__ __forceinline__ uint32_t grp_field(uint64_t ballot) {
+  const uint64_t f = ballot >> (threadIdx.x & (64 - GL));
+  return GL == 32 ? static_cast<uint32_t>(f) : static_cast<uint32_t>(f) & 0xffffu;
+}
+template <int GL> __device__ __forceinline__ uint32_t grp_lanemask_lt() {
+  return (1u << (threadIdx.x & (GL - 1))) - 1u;
+}
+
 // The kk-th largest of the keys held by the group (NK per lane, 0 = none):
 // the largest T with at least kk keys >= T, one bit at a time from the most
 // significant down.  The bits that all of the group's keys share are taken as
@@ -227,7 +256,7 @@ __device__ __forceinline__ int wave_max_i(int x) {
 // highest bit where they differ; the loop runs to the wave's highest such
 // bit, and the extra steps leave a group's result unchanged.  kk = 0 gives
 // 0xffffffff (nothing reaches it).
-template <int NK>
+template <int NK, int GL>
 __device__ __forceinline__ uint32_t group_kth_key(const uint32_t* keys, int kk) {
   uint32_t a = 0xffffffffu, o = 0u;
 #pragma unroll
@@ -237,8 +266,8 @@ __device__ __forceinline__ uint32_t group_kth_key(const uint32_t* keys, int kk) 
       o |= keys[e];
     }
   }
-  a = row16_and(a);
-  o = row16_or(o);
+  a = grp_and<GL>(a);
+  o = grp_or<GL>(o);
   const uint32_t diff = (o != 0u) ? (a ^ o) : 0u;
   const int hb = diff != 0u ? 31 - __clz(static_cast<int>(diff)) : -1;
   uint32_t t = hb >= 0 ? (o & ~((2u << hb) - 1u)) : o;  // the common prefix, zeros below
@@ -248,7 +277,7 @@ __device__ __forceinline__ uint32_t group_kth_key(const uint32_t* keys, int kk) 
     int cnt = 0;
 #pragma unroll
     for (int e = 0; e < NK; ++e) cnt += keys[e] >= cand ? 1 : 0;
-    if (row16_sum_i(cnt) >= kk) t = cand;
+    if (grp_sum_i<GL>(cnt) >= kk) t = cand;
   }
   return kk > 0 ? t : 0xffffffffu;
 }
@@ -256,29 +285,31 @@ __device__ __forceinline__ uint32_t group_kth_key(const uint32_t* keys, int kk) 
 // Top-kk positions of the group's row row[0..m) (0 <= kk, kk <= m), ties to
 // the smaller position, given a threshold tau that every top-kk entry reaches
 // (its order key): one sweep lists the positions with key >= tau in ascending
-// order in cand[0..CAP); the exact kk-th key among them is found by a second
-// search, and the entries above it plus the first ones equal to it are
-// compacted in place.  Returns the number selected (kk), or -1 if more than
-// CAP positions reached tau (the caller then selects that row another way).
-template <int CAP>
+// order in cand[0..CAP); unless exactly kk reached tau in every row of the
+// wave, the exact kk-th key among them is found by a second search, and the
+// entries above it plus the first ones equal to it are compacted in place.
+// Returns the number selected (kk), or -1 if more than CAP positions reached
+// tau (the caller then selects that row another way).
+template <int CAP, int GL>
 __device__ int group_select(const float* row, int m, int kk, uint32_t tau, uint16_t* cand) {
-  static_assert(CAP % 16 == 0 && CAP <= 256, "candidate layout");
-  constexpr int PER = CAP / 16;
-  const int c = threadIdx.x & 15;
-  const uint32_t lt = lanemask_lt16();
+  static_assert(CAP % GL == 0 && CAP <= 256, "candidate layout");
+  constexpr int PER = CAP / GL;
+  constexpr int SW = 64 / GL;  // positions per lane read together in the sweep
+  const int c = threadIdx.x & (GL - 1);
+  const uint32_t lt = grp_lanemask_lt<GL>();
   int cnt = 0;
-  for (int i0 = 0; i0 < m; i0 += 64) {  // four reads in flight per lane
-    float x[4];
+  for (int i0 = 0; i0 < m; i0 += SW * GL) {
+    float x[SW];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int p = i0 + 16 * e + c;
+    for (int e = 0; e < SW; ++e) {
+      const int p = i0 + GL * e + c;
       x[e] = p < m ? row[p] : 0.0f;
     }
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int p = i0 + 16 * e + c;
+    for (int e = 0; e < SW; ++e) {
+      const int p = i0 + GL * e + c;
       const bool sel = p < m && order_key(x[e]) >= tau;
-      const uint32_t f = group_field(__ballot(sel));
+      const uint32_t f = grp_field<GL>(__ballot(sel));
       const int idx = cnt + __popc(f & lt);
       if (sel && idx < CAP) cand[idx] = static_cast<uint16_t>(p);
       cnt += __popc(f);
@@ -286,31 +317,29 @@ __device__ int group_select(const float* row, int m, int kk, uint32_t tau, uint1
   }
   if (cnt > CAP) return -1;
   wave_lds_sync();
-  // exactly kk entries reached the threshold in every row of the wave: the
-  // lists are the selections already
   if (__ballot(cnt != kk) == 0ull) return cnt;
   int pos[PER];
   uint32_t ck[PER];
 #pragma unroll
   for (int e = 0; e < PER; ++e) {
-    const int i = c + 16 * e;
+    const int i = c + GL * e;
     pos[e] = i < cnt ? cand[i] : 0;
   }
 #pragma unroll
-  for (int e = 0; e < PER; ++e) ck[e] = c + 16 * e < cnt ? order_key(row[pos[e]]) : 0u;
-  const uint32_t kth = group_kth_key<PER>(ck, kk);
+  for (int e = 0; e < PER; ++e) ck[e] = c + GL * e < cnt ? order_key(row[pos[e]]) : 0u;
+  const uint32_t kth = group_kth_key<PER, GL>(ck, kk);
   int gt = 0;
 #pragma unroll
   for (int e = 0; e < PER; ++e) gt += ck[e] > kth ? 1 : 0;
-  const int need = kk - row16_sum_i(gt);
+  const int need = kk - grp_sum_i<GL>(gt);
   wave_lds_sync();
   int written = 0, eq_seen = 0;
 #pragma unroll
   for (int e = 0; e < PER; ++e) {
     const bool eq = ck[e] == kth;  // key 0 (no entry) never equals kth > 0
-    const uint32_t ef = group_field(__ballot(eq));
+    const uint32_t ef = grp_field<GL>(__ballot(eq));
     const bool sel = ck[e] > kth || (eq && eq_seen + __popc(ef & lt) < need);
-    const uint32_t sf = group_field(__ballot(sel));
+    const uint32_t sf = grp_field<GL>(__ballot(sel));
     if (sel) cand[written + __popc(sf & lt)] = static_cast<uint16_t>(pos[e]);
     written += __popc(sf);
     eq_seen += __popc(ef);
@@ -320,23 +349,24 @@ __device__ int group_select(const float* row, int m, int kk, uint32_t tau, uint1
 }
 
 // Threshold for group_select from the row itself: each lane keeps the NT
-// largest values of its positions c, c + 16, ...; the kk-th largest of those
-// 16 * NT values (16 * NT >= kk) is reached by every top-kk entry.
-template <int NT>
+// largest values of its positions; the kk-th largest of those GL * NT values
+// (GL * NT >= kk) is reached by every top-kk entry.
+template <int NT, int GL>
 __device__ uint32_t group_row_threshold(const float* row, int m, int kk) {
-  const int c = threadIdx.x & 15;
+  constexpr int SW = 64 / GL;
+  const int c = threadIdx.x & (GL - 1);
   float top[NT];
 #pragma unroll
   for (int e = 0; e < NT; ++e) top[e] = -INFINITY;
-  for (int i0 = 0; i0 < m; i0 += 64) {
-    float x[4];
+  for (int i0 = 0; i0 < m; i0 += SW * GL) {
+    float x[SW];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int p = i0 + 16 * e + c;
+    for (int e = 0; e < SW; ++e) {
+      const int p = i0 + GL * e + c;
       x[e] = p < m ? row[p] : -INFINITY;
     }
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
+    for (int e = 0; e < SW; ++e) {
       float v = x[e];
 #pragma unroll
       for (int t = 0; t < NT; ++t) {  // insertion into the descending list
@@ -349,7 +379,7 @@ __device__ uint32_t group_row_threshold(const float* row, int m, int kk) {
   uint32_t keys[NT];
 #pragma unroll
   for (int e = 0; e < NT; ++e) keys[e] = top[e] > -INFINITY ? order_key(top[e]) : 0u;
-  return group_kth_key<NT>(keys, kk);
+  return group_kth_key<NT, GL>(keys, kk);
 }
 
 }  // namespace ca
