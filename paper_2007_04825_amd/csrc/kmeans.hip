@@ -482,6 +482,86 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
     wave_lds_sync();
   }
   __syncthreads();
+  // ---- centroids, Eq. (3) ---------------------------------------------------------
+  // D lanes (lane = dimension) per group; group g takes the sorted positions
+  // [g per, (g + 1) per), all of its member rows requested together, and adds
+  // them in order, one fp64 addition after the other.  A cluster that lies
+  // inside the range is finished there; one cut by range ends leaves partial
+  // sums in LDS (slot 0: the piece at the start of a range, slot 1: the piece
+  // at its end), which the group holding the cluster's first row adds up in
+  // range order after a barrier.
+  constexpr int GPW = 64 / D;        // groups per wave
+  constexpr int G = kKmWaves * GPW;  // groups per workgroup
+  constexpr int RB = 32;             // rows in flight per lane
+  double* cut = reinterpret_cast<double*>(sh.codes);  // [G][2][D]; the codes are dead
+  static_assert(sizeof(sh.codes) >= static_cast<size_t>(G) * 2 * D * sizeof(double), "partial sums");
+  {
+    const int t = lane % D, grp = wave * GPW + lane / D;
+    const int per = (n + G - 1) / G;
+    const int p0 = min(n, grp * per), p1 = min(n, p0 + per);
+    float* qcu = f.qc + static_cast<size_t>(u) * C * D;
+    int j = 0, start = 0, end = 0;
+    if (p0 < p1) {  // cluster of position p0
+      j = sh.assign[mem[p0]];
+      start = off[j];
+      end = off[j + 1];
+    }
+    int s1j = -1, s1start = 0, s1end = 0;  // the cluster cut at the end of the range
+    double acc = 0.0;
+    for (int b0 = p0; b0 < p1; b0 += RB) {
+      // positions past the range repeat its last row (straight-line loads)
+      int mi[RB];
+#pragma unroll
+      for (int e = 0; e < RB; ++e) mi[e] = mem[min(b0 + e, p1 - 1)];
+      float x[RB];
+#pragma unroll
+      for (int e = 0; e < RB; ++e) x[e] = to_f32(qu[static_cast<size_t>(mi[e]) * D + t]);
+#pragma unroll
+      for (int e = 0; e < RB; ++e) {
+        const int p = b0 + e;
+        if (p >= p1) continue;
+        acc += static_cast<double>(x[e]);
+        if (p + 1 == end) {  // cluster j ends here
+          if (start >= p0) {
+            qcu[j * D + t] = static_cast<float>(acc / static_cast<double>(end - start));
+          } else {
+            cut[(grp * 2 + 0) * D + t] = acc;
+          }
+          acc = 0.0;
+          if (p + 1 < p1) {  // next non-empty cluster, starting at p + 1
+            do {
+              ++j;
+              end = off[j + 1];
+            } while (end == p + 1);
+            start = p + 1;
+          }
+        } else if (p + 1 == p1) {  // the range ends inside cluster j
+          if (start < p0) {
+            cut[(grp * 2 + 0) * D + t] = acc;
+          } else {
+            cut[(grp * 2 + 1) * D + t] = acc;
+            s1j = j;
+            s1start = start;
+            s1end = end;
+          }
+        }
+      }
+    }
+    // clusters with no member, and slots past C_eff
+    for (int x = tid; x < C * D; x += kKmThreads) {
+      const int jj = x / D;
+      if (jj >= ce || sh.size[jj] == 0) qcu[x] = 0.0f;
+    }
+    __syncthreads();
+    if (s1j >= 0) {
+      double sum = cut[(grp * 2 + 1) * D + t];
+      const int g_last = (s1end - 1) / per;
+      for (int gg = grp + 1; gg <= g_last; ++gg) sum += cut[(gg * 2 + 0) * D + t];
+      qcu[s1j * D + t] = static_cast<float>(sum / static_cast<double>(s1end - s1start));
+    }
+  }
+  // the clustering itself, written last so that the row loads above do not
+  // wait behind these stores
   for (int i = tid; i < n; i += kKmThreads) {
     f.assign[row0 + i] = sh.assign[i];
     f.members[row0 + i] = mem[i];
@@ -489,63 +569,6 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
   for (int j = tid; j < C; j += kKmThreads) f.sizes[static_cast<size_t>(u) * C + j] = j < ce ? sh.size[j] : 0;
   for (int j = tid; j <= C; j += kKmThreads)
     f.offsets[static_cast<size_t>(u) * (C + 1) + j] = j < ce ? off[j] : n;
-
-  // ---- centroids, Eq. (3) ---------------------------------------------------------
-  // D lanes per cluster (lane = dimension) add the member rows in ascending
-  // query order, one fp64 addition after the other; groups take clusters
-  // grp, grp + G, ..., four at a time with the first rows of all four
-  // requested together
-  constexpr int GPW = 64 / D;        // lane groups per wave
-  constexpr int G = kKmWaves * GPW;  // lane groups per workgroup
-  constexpr int BATCH = 8;           // rows per cluster requested up front
-  const int t = lane % D, grp = wave * GPW + lane / D;
-  auto fetch = [&](int j, int m0, float* x) {
-    const int sz = sh.size[j];
-    const int* ml = mem + off[j];
-#pragma unroll
-    for (int e = 0; e < BATCH; ++e) {
-      const int m = m0 + e;
-      x[e] = m < sz ? to_f32(qu[static_cast<size_t>(ml[m]) * D + t]) : 0.0f;
-    }
-  };
-  for (int j0c = grp; j0c < ce; j0c += 4 * G) {
-    float xa[4][BATCH];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int j = j0c + q * G;
-      if (j < ce) {
-        fetch(j, 0, xa[q]);
-      } else {
-#pragma unroll
-        for (int e = 0; e < BATCH; ++e) xa[q][e] = 0.0f;
-      }
-    }
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int j = j0c + q * G;
-      if (j >= ce) break;
-      const int sz = sh.size[j];
-      double acc = 0.0;
-#pragma unroll
-      for (int e = 0; e < BATCH; ++e)
-        if (e < sz) acc += static_cast<double>(xa[q][e]);
-      // larger clusters: 16 more rows in flight at a time
-      const int* ml = mem + off[j];
-      for (int m0 = BATCH; m0 < sz; m0 += 16) {
-        float y[16];
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int m = m0 + e;
-          y[e] = m < sz ? to_f32(qu[static_cast<size_t>(ml[m]) * D + t]) : 0.0f;
-        }
-#pragma unroll
-        for (int e = 0; e < 16; ++e)
-          if (m0 + e < sz) acc += static_cast<double>(y[e]);
-      }
-      f.qc[(static_cast<size_t>(u) * C + j) * D + t] = sz > 0 ? static_cast<float>(acc / static_cast<double>(sz)) : 0.0f;
-    }
-  }
-  for (int x = ce * D + tid; x < C * D; x += kKmThreads) f.qc[static_cast<size_t>(u) * C * D + x] = 0.0f;
 }
 
 // ===========================================================================
