@@ -249,13 +249,15 @@ template <int GL> __device__ __forceinline__ uint32_t grp_lanemask_lt() {
   return (1u << (threadIdx.x & (GL - 1))) - 1u;
 }
 
-// The kk-th largest of the keys held by the group (NK per lane, 0 = none):
-// the largest T with at least kk keys >= T, one bit at a time from the most
-// significant down.  The bits that all of the group's keys share are taken as
-// they are (the answer is one of the keys), so the search starts at the
-// highest bit where they differ; the loop runs to the wave's highest such
-// bit, and the extra steps leave a group's result unchanged.  kk = 0 gives
-// 0xffffffff (nothing reaches it).
+// A threshold for the kk largest of the keys held by the group (NK per lane,
+// 0 = none), built one bit at a time from the most significant down: the
+// largest T with at least kk keys >= T (the kk-th largest key), unless a
+// prefix that exactly kk keys reach turns up first, which ends the group's
+// search (the same keys reach it: the kk largest).  The bits that all of the
+// group's keys share are taken as they are, so the search starts at the
+// highest bit where they differ; the loop runs to the wave's highest such bit
+// or until every group has stopped, and the extra steps leave a group's
+// result unchanged.  kk = 0 gives 0xffffffff (nothing reaches it).
 template <int NK, int GL>
 __device__ __forceinline__ uint32_t group_kth_key(const uint32_t* keys, int kk) {
   uint32_t a = 0xffffffffu, o = 0u;
@@ -272,12 +274,20 @@ __device__ __forceinline__ uint32_t group_kth_key(const uint32_t* keys, int kk) 
   const int hb = diff != 0u ? 31 - __clz(static_cast<int>(diff)) : -1;
   uint32_t t = hb >= 0 ? (o & ~((2u << hb) - 1u)) : o;  // the common prefix, zeros below
   const int top = __builtin_amdgcn_readfirstlane(wave_max_i(hb));  // uniform loop bound
+  // a group stops as soon as exactly kk keys reach t: every later step would
+  // keep that same set of keys
+  bool done = kk <= 0;
   for (int bit = top; bit >= 0; --bit) {
+    if (__ballot(!done) == 0ull) break;
     const uint32_t cand = t | (1u << bit);
     int cnt = 0;
 #pragma unroll
     for (int e = 0; e < NK; ++e) cnt += keys[e] >= cand ? 1 : 0;
-    if (grp_sum_i<GL>(cnt) >= kk) t = cand;
+    const int tot = grp_sum_i<GL>(cnt);
+    if (!done && tot >= kk) {
+      t = cand;
+      done = tot == kk;
+    }
   }
   return kk > 0 ? t : 0xffffffffu;
 }
