@@ -248,6 +248,24 @@ template <int GL> __device__ __forceinline__ uint32_t grp_field(uint64_t ballot)
 template <int GL> __device__ __forceinline__ uint32_t grp_lanemask_lt() {
   return (1u << (threadIdx.x & (GL - 1))) - 1u;
 }
+// Inclusive prefix sum over the lanes of this lane's group.
+template <int GL> __device__ __forceinline__ int grp_incl_scan_i(int x) {
+  x += dpp_i<0x111>(x);  // row_shr:1 (lanes shifted in from outside the row read 0)
+  x += dpp_i<0x112>(x);  // row_shr:2
+  x += dpp_i<0x114>(x);  // row_shr:4
+  x += dpp_i<0x118>(x);  // row_shr:8
+  if constexpr (GL == 32) {
+    const int r15 = __builtin_amdgcn_readlane(x, 15), r47 = __builtin_amdgcn_readlane(x, 47);
+    if (threadIdx.x & 16) x += (threadIdx.x & 32) ? r47 : r15;
+  }
+  return x;
+}
+// A float f with (x >= f) == (order_key(x) >= tau) for every finite x.
+__device__ __forceinline__ float key_threshold(uint32_t tau) {
+  if (tau > 0xff7fffffu) return INFINITY;  // above every finite key
+  tau = tau > 0x00800000u ? tau : 0x00800000u;  // every finite key is at least this
+  return __uint_as_float((tau & 0x80000000u) ? (tau & 0x7fffffffu) : ~tau);
+}
 
 // A threshold for the kk largest of the keys held by the group (NK per lane,
 // 0 = none), built one bit at a time from the most significant down: the
@@ -304,28 +322,35 @@ template <int CAP, int GL>
 __device__ int group_select(const float* row, int m, int kk, uint32_t tau, uint16_t* cand) {
   static_assert(CAP % GL == 0 && CAP <= 256, "candidate layout");
   constexpr int PER = CAP / GL;
-  constexpr int SW = 64 / GL;  // positions per lane read together in the sweep
   const int c = threadIdx.x & (GL - 1);
   const uint32_t lt = grp_lanemask_lt<GL>();
-  int cnt = 0;
-  for (int i0 = 0; i0 < m; i0 += SW * GL) {
-    float x[SW];
+  // each lane sweeps its own block of L consecutive positions (L odd, so the
+  // lanes' reads fall in distinct LDS banks); lane order is then position
+  // order, and one prefix sum over the group places every lane's hits
+  const int L = ((m + GL - 1) / GL) | 1;
+  const int base = c * L;
+  const float tf = key_threshold(tau);
+  uint64_t hits = 0ull;  // bit i: position base + i reaches tau
+  for (int i0 = 0; i0 < L; i0 += 8) {
+    float x[8];
 #pragma unroll
-    for (int e = 0; e < SW; ++e) {
-      const int p = i0 + GL * e + c;
-      x[e] = p < m ? row[p] : 0.0f;
+    for (int e = 0; e < 8; ++e) {
+      const int p = base + i0 + e;
+      x[e] = (i0 + e < L && p < m) ? row[p] : -INFINITY;
     }
 #pragma unroll
-    for (int e = 0; e < SW; ++e) {
-      const int p = i0 + GL * e + c;
-      const bool sel = p < m && order_key(x[e]) >= tau;
-      const uint32_t f = grp_field<GL>(__ballot(sel));
-      const int idx = cnt + __popc(f & lt);
-      if (sel && idx < CAP) cand[idx] = static_cast<uint16_t>(p);
-      cnt += __popc(f);
-    }
+    for (int e = 0; e < 8; ++e)
+      if (x[e] >= tf) hits |= 1ull << (i0 + e);
   }
+  const int mine = __popcll(hits);
+  const int cnt = grp_sum_i<GL>(mine);
   if (cnt > CAP) return -1;
+  int at = grp_incl_scan_i<GL>(mine) - mine;
+  while (hits != 0ull) {
+    const int i = __ffsll(static_cast<unsigned long long>(hits)) - 1;
+    hits &= hits - 1ull;
+    cand[at++] = static_cast<uint16_t>(base + i);
+  }
   wave_lds_sync();
   if (__ballot(cnt != kk) == 0ull) return cnt;
   int pos[PER];
