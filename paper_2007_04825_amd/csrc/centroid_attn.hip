@@ -254,6 +254,7 @@ __device__ void sparse_cluster(const PosT* tpos, int kk, float mh, const float* 
 // Centroid attention tile kernel.
 // ---------------------------------------------------------------------------
 constexpr int kLStride = kChunk + 16;  // floats per LDS logit row (the four rows of a wave fall in distinct banks)
+static_assert(kLStride >= kChunk, "rows padded for the top-k sweep: 32 grp_block_len(kChunk) <= kChunk");
 constexpr int kCandCap = 128;
 constexpr int kTileWaves = 8;  // waves per centroid-tile workgroup
 constexpr int kTileThreads = 64 * kTileWaves;
@@ -414,6 +415,9 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
 #pragma unroll
       for (int e = 0; e < NT; e += 4)
         *reinterpret_cast<float4*>(&stop[c][wave * 4 + g][e]) = make_float4(top[e], top[e + 1], top[e + 2], top[e + 3]);
+      // the top-k sweep reads each row up to 32 grp_block_len(kn): -inf past the last key tile
+      const int w = 32 * grp_block_len<32>(kn) - nkt * 16;
+      for (int x = tid; x < 16 * w; x += kTileThreads) logits[(x / w) * kLStride + nkt * 16 + x % w] = -INFINITY;
     }
   }
   __syncthreads();

@@ -260,6 +260,13 @@ template <int GL> __device__ __forceinline__ int grp_incl_scan_i(int x) {
   }
   return x;
 }
+// Positions per lane when a group sweeps a row of m <= 32 GL entries in
+// contiguous blocks: ceil(m / GL), made odd where that stays within 32 so
+// that the lanes' LDS reads fall in distinct banks.
+template <int GL> __device__ __forceinline__ int grp_block_len(int m) {
+  const int l = (m + GL - 1) / GL;
+  return (l & 1) || l >= 32 ? l : l + 1;
+}
 // A float f with (x >= f) == (order_key(x) >= tau) for every finite x.
 __device__ __forceinline__ float key_threshold(uint32_t tau) {
   if (tau > 0xff7fffffu) return INFINITY;  // above every finite key
@@ -312,7 +319,8 @@ __device__ __forceinline__ uint32_t group_kth_key(const uint32_t* keys, int kk) 
 
 // Top-kk positions of the group's row row[0..m) (0 <= kk, kk <= m), ties to
 // the smaller position, given a threshold tau that every top-kk entry reaches
-// (its order key): one sweep lists the positions with key >= tau in ascending
+// (its order key).  The row is read up to GL * grp_block_len(m), and the
+// entries from m on must be -inf: one sweep lists the positions with key >= tau in ascending
 // order in cand[0..CAP); unless exactly kk reached tau in every row of the
 // wave, the exact kk-th key among them is found by a second search, and the
 // entries above it plus the first ones equal to it are compacted in place.
@@ -324,31 +332,29 @@ __device__ int group_select(const float* row, int m, int kk, uint32_t tau, uint1
   constexpr int PER = CAP / GL;
   const int c = threadIdx.x & (GL - 1);
   const uint32_t lt = grp_lanemask_lt<GL>();
-  // each lane sweeps its own block of L consecutive positions (L odd, so the
-  // lanes' reads fall in distinct LDS banks); lane order is then position
-  // order, and one prefix sum over the group places every lane's hits
-  const int L = ((m + GL - 1) / GL) | 1;
+  // each lane sweeps its own block of L consecutive positions, so lane order
+  // is position order, and one prefix sum over the group places every
+  // lane's hits
+  const int L = grp_block_len<GL>(m);
   const int base = c * L;
   const float tf = key_threshold(tau);
-  uint64_t hits = 0ull;  // bit i: position base + i reaches tau
+  uint32_t hits = 0u;  // bit i: position base + i reaches tau
   for (int i0 = 0; i0 < L; i0 += 8) {
     float x[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int p = base + i0 + e;
-      x[e] = (i0 + e < L && p < m) ? row[p] : -INFINITY;
-    }
+    for (int e = 0; e < 8; ++e) x[e] = i0 + e < L ? row[base + i0 + e] : -INFINITY;
+    uint32_t h8 = 0u;
 #pragma unroll
-    for (int e = 0; e < 8; ++e)
-      if (x[e] >= tf) hits |= 1ull << (i0 + e);
+    for (int e = 0; e < 8; ++e) h8 |= x[e] >= tf ? (1u << e) : 0u;
+    hits |= h8 << i0;
   }
-  const int mine = __popcll(hits);
+  const int mine = __popc(hits);
   const int cnt = grp_sum_i<GL>(mine);
   if (cnt > CAP) return -1;
   int at = grp_incl_scan_i<GL>(mine) - mine;
-  while (hits != 0ull) {
-    const int i = __ffsll(static_cast<unsigned long long>(hits)) - 1;
-    hits &= hits - 1ull;
+  while (hits != 0u) {
+    const int i = __ffs(static_cast<int>(hits)) - 1;
+    hits &= hits - 1u;
     cand[at++] = static_cast<uint16_t>(base + i);
   }
   wave_lds_sync();
