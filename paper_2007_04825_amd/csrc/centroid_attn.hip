@@ -329,6 +329,10 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
   const T* ku = static_cast<const T*>(a.k) + (static_cast<size_t>(u) * a.N + k0) * D;
   const T* vu = static_cast<const T*>(a.v) + (static_cast<size_t>(u) * a.N + k0) * D;
   const int nkt = (kn + 15) / 16;
+  // the chunk's keys and values as buffers: rows past kn read as 0
+  constexpr uint32_t ESZ = sizeof(T);
+  const __amdgpu_buffer_rsrc_t rk = make_rsrc(ku, static_cast<uint32_t>(kn) * D * ESZ);
+  const __amdgpu_buffer_rsrc_t rv = make_rsrc(vu, static_cast<uint32_t>(kn) * D * ESZ);
 
   // ---- sizes (fused: the member offsets of the 16 clusters) -----------------------
   if constexpr (FUSED) {
@@ -361,11 +365,10 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
   // ---- logits of this chunk, with the slice statistics -------------------------------
   {
     float bq[KS];
-    if (j0 + c < C) {
-      load_row<KS>(a.qc + (static_cast<size_t>(u) * C + j0 + c) * D + g * KS, bq);
-    } else {
-#pragma unroll
-      for (int s = 0; s < KS; ++s) bq[s] = 0.0f;
+    {
+      const __amdgpu_buffer_rsrc_t rq =
+          make_rsrc(a.qc + (static_cast<size_t>(u) * C + j0) * D, static_cast<uint32_t>(min(16, C - j0)) * D * 4);
+      buf_load<KS>(rq, (c * D + g * KS) * 4, 0, bq, float{});
     }
     float lmax = -INFINITY;
     float top[NT];
@@ -373,11 +376,11 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
     for (int e = 0; e < NT; ++e) top[e] = -INFINITY;
     for (int kt0 = wave; kt0 < nkt; kt0 += NW * BT) {
       float ka[BT][KS];
+      const uint32_t voff = ((kt0 * 16 + c) * D + g * KS) * ESZ;
 #pragma unroll
       for (int b = 0; b < BT; ++b) {
-        const int key = (kt0 + NW * b) * 16 + c;
-        if (key < kn) {
-          load_row<KS>(ku + static_cast<size_t>(key) * D + g * KS, ka[b]);
+        if (kt0 + NW * b < nkt) {  // whole tiles past the chunk are not requested
+          buf_load<KS>(rk, voff, NW * b * 16 * D * ESZ, ka[b], T{});
         } else {
 #pragma unroll
           for (int s = 0; s < KS; ++s) ka[b][s] = 0.0f;
@@ -520,13 +523,13 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
     const float mc = rowm[c];
     for (int kt0 = wave; kt0 < nkt; kt0 += NW * BT) {
       float va[BT][4][DT];
+      const uint32_t voff = ((kt0 * 16 + 4 * g) * D + DT * c) * ESZ;
 #pragma unroll
       for (int b = 0; b < BT; ++b)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int key = (kt0 + NW * b) * 16 + 4 * g + i;
-          if (key < kn) {
-            load_vec<DT>(vu + static_cast<size_t>(key) * D + DT * c, va[b][i]);
+          if (kt0 + NW * b < nkt) {
+            buf_load<DT>(rv, voff, (NW * b * 16 + i) * D * ESZ, va[b][i], T{});
           } else {
 #pragma unroll
             for (int dt = 0; dt < DT; ++dt) va[b][i][dt] = 0.0f;

@@ -214,6 +214,60 @@ inline unsigned xcd_grid(long long nwork) {
 // Order-preserving map from fp32 to uint32: a < b  <=>  key(a) < key(b).
 // -0 is folded onto +0 so that equal values get equal keys.
 // ---------------------------------------------------------------------------
+// ---------------------------------------------------------------------------
+// Buffer loads: a resource covering [base, base + bytes) turns every load into
+// a 32-bit lane offset plus a uniform offset, and reads past the end return 0
+// (so tile edges need no guards).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, static_cast<int>(bytes), 0x00020000);
+}
+// CNT consecutive elements (fp32 or bf16) at byte offset voff + soff, as fp32.
+template <int CNT>
+__device__ __forceinline__ void buf_load(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff, float* d, float) {
+  if constexpr (CNT == 1) {
+    d[0] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
+  } else if constexpr (CNT == 2) {
+    const auto t = __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0);
+    d[0] = __uint_as_float(t[0]);
+    d[1] = __uint_as_float(t[1]);
+  } else {
+    static_assert(CNT % 4 == 0, "vector width");
+#pragma unroll
+    for (int i = 0; i < CNT; i += 4) {
+      const auto t = __builtin_amdgcn_raw_buffer_load_b128(r, voff + 4 * i, soff, 0);
+      d[i] = __uint_as_float(t[0]);
+      d[i + 1] = __uint_as_float(t[1]);
+      d[i + 2] = __uint_as_float(t[2]);
+      d[i + 3] = __uint_as_float(t[3]);
+    }
+  }
+}
+template <int CNT>
+__device__ __forceinline__ void buf_load(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff, float* d, bf16_t) {
+  auto two = [&](uint32_t w, float* o) {
+    o[0] = __uint_as_float(w << 16);
+    o[1] = __uint_as_float(w & 0xffff0000u);
+  };
+  if constexpr (CNT == 2) {
+    two(__builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0), d);
+  } else if constexpr (CNT == 4) {
+    const auto t = __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0);
+    two(t[0], d);
+    two(t[1], d + 2);
+  } else {
+    static_assert(CNT % 8 == 0, "vector width");
+#pragma unroll
+    for (int i = 0; i < CNT; i += 8) {
+      const auto t = __builtin_amdgcn_raw_buffer_load_b128(r, voff + 2 * i, soff, 0);
+      two(t[0], d + i);
+      two(t[1], d + i + 2);
+      two(t[2], d + i + 4);
+      two(t[3], d + i + 6);
+    }
+  }
+}
+
 __device__ __forceinline__ uint32_t order_key(float f) {
   uint32_t u = __float_as_uint(f == 0.0f ? 0.0f : f);
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
