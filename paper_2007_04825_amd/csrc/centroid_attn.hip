@@ -1,26 +1,30 @@
 // Centroids (Eq. 3), centroid attention (Eqs. 4-5), the top-k keys of each
-// cluster with their attention mass (Section 3.3) and, when a sequence fits
-// in one key chunk, the per-query outputs (Eq. 6 or the improved values).
+// cluster with their attention mass (Section 3.3) and the per-query outputs
+// (Eq. 6 or the improved values).
 //
 // centroid_kernel: one wave per cluster sums the member rows of Q in fp64
-//   (members in ascending query order) and divides by the cluster size.
+//   (members in ascending query order) and divides by the cluster size (used
+//   when the keys take several chunks; otherwise the clustering kernel forms
+//   the centroids).
 //
-// attn_tile_kernel: one workgroup per (unit, 16 centroids, 1024-key chunk).
-//   Logits S^T = K Q^c^T come from v_mfma_f32_16x16x4f32 with keys as rows
-//   and centroids as columns, scaled by 1/sqrt(d), masked past the valid
-//   length and kept in LDS (A^c is never written to memory).  K rows are
-//   fetched four tiles at a time so that their latencies overlap.  One wave
-//   per centroid row then finds the row maximum m, z = sum exp(s - m) and,
-//   for the improved variant, the top-k set.  V^T P^T accumulates the values
-//   on the matrix cores: the result registers of the first product are in the
-//   B-operand layout of the second (key 4g+i of a tile sits in lane group g,
-//   register i), so P never leaves registers.
-//   * single chunk (n <= 1024): the workgroup finishes the clusters itself.
-//     For the improved variant the top-k keys are masked out of P, so the
-//     product yields the rest part V^b = sum_{l not in T} A^c_l V_l directly,
-//     and m_j = sum_{l in T} A^c_l.  It then writes every member row: V^c for
-//     the clustered variant, m_j * softmax_T(q K_T^T / sqrt d) V_T + V^b for
-//     the improved one (sparse_cluster below).
+// attn_tile_kernel: one workgroup of eight waves per (unit, 16 centroids,
+//   1024-key chunk).  Logits S^T = K Q^c^T come from v_mfma_f32_16x16x4f32
+//   with keys as rows and centroids as columns, scaled by 1/sqrt(d), masked
+//   past the valid length and kept in LDS (A^c is never written to memory);
+//   while they sit in the result registers every lane also keeps the maximum
+//   and, for the improved variant, the four largest logits of its slice of
+//   the row.  Two rows per wave (one 32-lane group each) then take the row
+//   maximum m from the slice maxima and, for the improved variant, the top-k
+//   set: a threshold from the slices' kept logits, one sweep for the
+//   positions that reach it.  V^T P^T accumulates the values on the matrix
+//   cores: the result registers of the first product are in the B-operand
+//   layout of the second (key 4g+i of a tile sits in lane group g, register
+//   i), so P never leaves registers.
+//   * single chunk (n <= 1024): the workgroup finishes the clusters.  The
+//     clustered variant writes V^c to every member row (Eq. 6).  For the
+//     improved variant the top-k keys are masked out of P, so the product
+//     yields the rest part V^b = sum_{l not in T} A^c_l V_l directly, and
+//     m_j = sum_{l in T} A^c_l; sparse_kernel then writes the member rows.
 //   * several chunks: it writes (m, z, unnormalised values, top-k candidates)
 //     of its chunk; attn_merge_kernel combines the chunks (log-sum-exp rule),
 //     selects T among the candidates and forms m_j and V^b = V^c - sum_T A^c V.
@@ -103,151 +107,6 @@ template <int W>
 __device__ __forceinline__ void store_vec(bf16_t* p, const float* s) {
 #pragma unroll
   for (int i = 0; i < W; i += 4) store4(p + i, s[i], s[i + 1], s[i + 2], s[i + 3]);
-}
-
-// ---------------------------------------------------------------------------
-// Improved values of one cluster (one wave), Section 3.3 / supplementary
-// decomposition: for each member i,
-//   out_i = mh * sum_{l in T} softmax_T(Q_i K_l / sqrt d)_l V_l + vb.
-// tpos[0..kk) are the key indices of T (LDS or global).  The K_T and V_T
-// operand fragments stay in registers for all member tiles.
-//   S^T = K_T Q^T : A = K_T rows (key kt*16 + lane%16, dims g*KS..), B = Q^T
-//   O^T = V_T^T P^T: A = V_T^T (dims DT*(lane%16)+dt, key kt*16+4g+i),
-//                     B = P^T straight from the S^T result registers.
-// Lane (query c, group g) ends with dims DT*4g .. DT*4g + 4*DT - 1 of its row.
-// ---------------------------------------------------------------------------
-template <int D, typename T, int NKT>
-struct SparseOps {
-  float kf[NKT][D / 4];     // K_T fragments: key kt * 16 + lane % 16, dims (lane / 16) * D / 4 ..
-  float vf[NKT][4][D / 16]; // V_T^T fragments: key kt * 16 + 4 (lane / 16) + i, dims (lane % 16) * D / 16 ..
-  float bq[D / 4];          // Q of the first member tile
-  int row;                  // this lane's member row of the first tile, or -1
-};
-
-// Requests the operands of one cluster: K_T, V_T and the first member tile.
-template <int D, typename T, int NKT, typename PosT>
-__device__ __forceinline__ void sparse_load(const PosT* tpos, int kk, const int32_t* mem, int sz,
-                                            const T* __restrict__ qu, const T* __restrict__ ku,
-                                            const T* __restrict__ vu, SparseOps<D, T, NKT>& S) {
-  constexpr int KS = D / 4, DT = D / 16;
-  const int lane = lane_id(), c = lane & 15, g = lane >> 4;
-  const int nkt = (kk + 15) >> 4;
-  S.row = c < sz ? mem[c] : -1;
-  if (S.row >= 0) {
-    load_row<KS>(qu + static_cast<size_t>(S.row) * D + g * KS, S.bq);
-  } else {
-#pragma unroll
-    for (int s = 0; s < KS; ++s) S.bq[s] = 0.0f;
-  }
-#pragma unroll
-  for (int kt = 0; kt < NKT; ++kt) {
-    const int slot = kt * 16 + c;
-    const int key = (kt < nkt && slot < kk) ? static_cast<int>(tpos[slot]) : -1;
-    if (key >= 0) {
-      load_row<KS>(ku + static_cast<size_t>(key) * D + g * KS, S.kf[kt]);
-    } else {
-#pragma unroll
-      for (int s = 0; s < KS; ++s) S.kf[kt][s] = 0.0f;
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int sl = kt * 16 + 4 * g + i;
-      const int kv = (kt < nkt && sl < kk) ? static_cast<int>(tpos[sl]) : -1;
-      if (kv >= 0) {
-        load_vec<DT>(vu + static_cast<size_t>(kv) * D + DT * c, S.vf[kt][i]);
-      } else {
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) S.vf[kt][i][dt] = 0.0f;
-      }
-    }
-  }
-}
-
-// Improved values of one cluster's members from its loaded operands.
-template <int D, typename T, int NKT>
-__device__ __forceinline__ void sparse_run(SparseOps<D, T, NKT>& S, int kk, float mh,
-                                           const float* vb, const int32_t* mem, int sz,
-                                           const T* __restrict__ qu, T* __restrict__ ou,
-                                           float scale) {
-  constexpr int KS = D / 4, DT = D / 16;
-  const int lane = lane_id(), c = lane & 15, g = lane >> 4;
-  const int nkt = (kk + 15) >> 4;
-  float vbf[4 * DT];
-#pragma unroll
-  for (int x = 0; x < 4 * DT; ++x) vbf[x] = vb[DT * 4 * g + x];
-  int row = S.row;
-  for (int mt = 0; mt < sz; mt += 16) {
-    if (mt > 0) {
-      const int mi = mt + c;
-      row = mi < sz ? mem[mi] : -1;
-      if (row >= 0) {
-        load_row<KS>(qu + static_cast<size_t>(row) * D + g * KS, S.bq);
-      } else {
-#pragma unroll
-        for (int s = 0; s < KS; ++s) S.bq[s] = 0.0f;
-      }
-    }
-    v4f sacc[NKT];
-    float mx = -INFINITY;
-#pragma unroll
-    for (int kt = 0; kt < NKT; ++kt) {
-      sacc[kt] = v4f{0.f, 0.f, 0.f, 0.f};
-      if (kt < nkt) {
-#pragma unroll
-        for (int s = 0; s < KS; ++s) sacc[kt] = mfma_f32_16x16x4(S.kf[kt][s], S.bq[s], sacc[kt]);
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float sv = (kt < nkt && kt * 16 + 4 * g + i < kk) ? sacc[kt][i] * scale : -INFINITY;
-        sacc[kt][i] = sv;
-        mx = fmaxf(mx, sv);
-      }
-    }
-    mx = cross_rows_max(mx);
-    float z = 0.0f;
-#pragma unroll
-    for (int kt = 0; kt < NKT; ++kt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float e = __expf(sacc[kt][i] - mx);
-        sacc[kt][i] = e;
-        z += e;
-      }
-    z = cross_rows_sum(z);
-    const float f = mh / z;
-    v4f oacc[DT];
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) oacc[dt] = v4f{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int kt = 0; kt < NKT; ++kt) {
-      if (kt < nkt) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float pv = sacc[kt][i] * f;
-#pragma unroll
-          for (int dt = 0; dt < DT; ++dt) oacc[dt] = mfma_f32_16x16x4(S.vf[kt][i][dt], pv, oacc[dt]);
-        }
-      }
-    }
-    if (row >= 0) {
-      float o[4 * DT];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) o[i * DT + dt] = oacc[dt][i] + vbf[i * DT + dt];
-      store_vec<4 * DT>(ou + static_cast<size_t>(row) * D + DT * 4 * g, o);
-    }
-  }
-}
-
-template <int D, typename T, int NKT, typename PosT>
-__device__ void sparse_cluster(const PosT* tpos, int kk, float mh, const float* vb,
-                               const int32_t* mem, int sz, const T* __restrict__ qu,
-                               const T* __restrict__ ku, const T* __restrict__ vu,
-                               T* __restrict__ ou, float scale) {
-  SparseOps<D, T, NKT> S;
-  sparse_load<D, T, NKT>(tpos, kk, mem, sz, qu, ku, vu, S);
-  sparse_run<D, T, NKT>(S, kk, mh, vb, mem, sz, qu, ou, scale);
 }
 
 // ---------------------------------------------------------------------------
@@ -731,37 +590,156 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Improved values for the several-chunk case: one wave per cluster.
+// Improved values (Section 3.3 with the supplementary decomposition), one
+// wave per cluster j: for every member i,
+//   out_i = m_j * sum_{l in T} softmax_T(q_i k_l / sqrt d)_l v_l + V^b_j.
+// The loads come in three dependent rounds: size, offset, m_j, V^b_j and T;
+// then the member indices with the K_T and V_T rows; then the member rows of
+// Q.  Member tiles after the first are requested one tile ahead.
+//   S^T = K_T Q^T : A = K_T rows (slot kt*16 + lane%16, dims g*KS..), B = Q^T
+//   O^T = V_T^T P^T: A = V_T^T (dims DT*(lane%16)+dt, slot kt*16+4g+i),
+//                     B = P^T straight from the S^T result registers.
+// Lane (query c, group g) ends with dims DT*4g .. DT*4g + 4*DT - 1 of its row.
 // ---------------------------------------------------------------------------
 template <int D, typename T, int NKT>
 __global__ __launch_bounds__(256) void sparse_kernel(AttnArgs a) {
-  __shared__ int tp[4][128];
+  constexpr int KS = D / 4, DT = D / 16;
+  constexpr uint32_t ESZ = sizeof(T);
+  constexpr uint32_t kNone = 0x80000000u;  // past every buffer: loads read 0, stores are dropped
+  __shared__ int tp[4][kCandCap];
   const int wi = xcd_work_item();  // cluster group fastest, then (batch, head)
   if (wi >= a.ncg * a.units) return;
   const int u = wi / a.ncg, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int c = lane & 15, g = lane >> 4;
   const int C = a.C;
   const int j = (wi % a.ncg) * 4 + wave;
   if (j >= C) return;
   const size_t uj = static_cast<size_t>(u) * C + j;
+
+  // ---- round 1: the cluster's size, offset, m_j, V^b_j and T -----------------------
   const int sz = a.sizes[uj];
+  const int off = a.offsets[static_cast<size_t>(u) * (C + 1) + j];
+  const float mh = a.mass[uj];
+  int tv[kCandCap / 64];
+#pragma unroll
+  for (int e = 0; e < kCandCap / 64; ++e) {
+    const int x = lane + 64 * e;
+    tv[e] = x < a.topk ? a.topk_out[uj * a.topk + x] : -1;
+  }
+  float vbf[4 * DT];
+  load_row<4 * DT>(a.vcb + uj * D + DT * 4 * g, vbf);
   if (sz == 0) return;
-  const int n = unit_length(a.lengths, u / a.heads, a.N);
   // T: the leading non-negative entries (a caller-supplied set may be shorter)
-  const int kmax = min(a.topk, n);
   int kk = 0;
-  for (int x0 = 0; x0 < kmax; x0 += 64) {
-    const int x = x0 + lane;
-    const int v = x < kmax ? a.topk_out[uj * a.topk + x] : -1;
-    if (v >= 0) tp[wave][x] = v;
-    kk += __popcll(__ballot(v >= 0));
+#pragma unroll
+  for (int e = 0; e < kCandCap / 64; ++e) {
+    if (tv[e] >= 0) tp[wave][lane + 64 * e] = tv[e];
+    kk += __popcll(__ballot(tv[e] >= 0));
   }
   wave_lds_sync();
-  const int32_t* mem = a.members + static_cast<size_t>(u) * a.N + a.offsets[static_cast<size_t>(u) * (C + 1) + j];
+  const int nkt = (kk + 15) >> 4;
+
+  // ---- round 2: member indices of the first two tiles, K_T and V_T -------------------
+  const int32_t* mem = a.members + static_cast<size_t>(u) * a.N + off;
+  int row0 = c < sz ? mem[c] : -1;
+  int row1 = 16 + c < sz ? mem[16 + c] : -1;
   const size_t base = static_cast<size_t>(u) * a.N * D;
-  sparse_cluster<D, T, NKT>(tp[wave], kk, a.mass[uj], a.vcb + uj * D, mem, sz,
-                            static_cast<const T*>(a.q) + base, static_cast<const T*>(a.k) + base,
-                            static_cast<const T*>(a.v) + base, static_cast<T*>(a.out) + base,
-                            a.scale);
+  const uint32_t ubytes = static_cast<uint32_t>(a.N) * D * ESZ;
+  const __amdgpu_buffer_rsrc_t rq = make_rsrc(static_cast<const T*>(a.q) + base, ubytes);
+  const __amdgpu_buffer_rsrc_t rk = make_rsrc(static_cast<const T*>(a.k) + base, ubytes);
+  const __amdgpu_buffer_rsrc_t rv = make_rsrc(static_cast<const T*>(a.v) + base, ubytes);
+  const __amdgpu_buffer_rsrc_t ro = make_rsrc(static_cast<T*>(a.out) + base, ubytes);
+  float kf[NKT][KS];     // K_T: slot kt * 16 + lane % 16, dims (lane / 16) * KS ..
+  float vf[NKT][4][DT];  // V_T^T: slot kt * 16 + 4 (lane / 16) + i, dims (lane % 16) * DT ..
+#pragma unroll
+  for (int kt = 0; kt < NKT; ++kt) {
+    if (kt < nkt) {
+      const int slot = kt * 16 + c;
+      buf_load<KS>(rk, slot < kk ? static_cast<uint32_t>(tp[wave][slot]) * D * ESZ + g * KS * ESZ : kNone, 0,
+                   kf[kt], T{});
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int sl = kt * 16 + 4 * g + i;
+        buf_load<DT>(rv, sl < kk ? static_cast<uint32_t>(tp[wave][sl]) * D * ESZ + DT * c * ESZ : kNone, 0,
+                     vf[kt][i], T{});
+      }
+    } else {
+#pragma unroll
+      for (int s = 0; s < KS; ++s) kf[kt][s] = 0.0f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) vf[kt][i][dt] = 0.0f;
+    }
+  }
+  auto qoff = [&](int row) { return row >= 0 ? static_cast<uint32_t>(row) * D * ESZ + g * KS * ESZ : kNone; };
+
+  // ---- round 3: member rows of Q, one tile of 16 at a time -------------------------
+  float bq[KS];
+  buf_load<KS>(rq, qoff(row0), 0, bq, T{});
+  for (int mt = 0; mt < sz; mt += 16) {
+    const bool more = mt + 16 < sz;
+    float nbq[KS];
+    int row2 = -1;
+    if (more) {
+      buf_load<KS>(rq, qoff(row1), 0, nbq, T{});
+      row2 = mt + 32 + c < sz ? mem[mt + 32 + c] : -1;
+    }
+    v4f sacc[NKT];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt) {
+      sacc[kt] = v4f{0.f, 0.f, 0.f, 0.f};
+      if (kt < nkt) {
+#pragma unroll
+        for (int s = 0; s < KS; ++s) sacc[kt] = mfma_f32_16x16x4(kf[kt][s], bq[s], sacc[kt]);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float sv = (kt < nkt && kt * 16 + 4 * g + i < kk) ? sacc[kt][i] * a.scale : -INFINITY;
+        sacc[kt][i] = sv;
+        mx = fmaxf(mx, sv);
+      }
+    }
+    mx = cross_rows_max(mx);
+    float z = 0.0f;
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float e = __expf(sacc[kt][i] - mx);
+        sacc[kt][i] = e;
+        z += e;
+      }
+    z = cross_rows_sum(z);
+    const float f = mh / z;
+    v4f oacc[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) oacc[dt] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt) {
+      if (kt < nkt) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float pv = sacc[kt][i] * f;
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) oacc[dt] = mfma_f32_16x16x4(vf[kt][i][dt], pv, oacc[dt]);
+        }
+      }
+    }
+    float o[4 * DT];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) o[i * DT + dt] = oacc[dt][i] + vbf[i * DT + dt];
+    buf_store<4 * DT>(ro, row0 >= 0 ? static_cast<uint32_t>(row0) * D * ESZ + DT * 4 * g * ESZ : kNone, 0, o, T{});
+    row0 = row1;
+    row1 = row2;
+    if (more) {
+#pragma unroll
+      for (int s = 0; s < KS; ++s) bq[s] = nbq[s];
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------

@@ -268,6 +268,38 @@ __device__ __forceinline__ void buf_load(__amdgpu_buffer_rsrc_t r, uint32_t voff
   }
 }
 
+// CNT consecutive fp32 values stored at byte offset voff + soff as the
+// element type (bf16: rounded to nearest even); stores past the end are dropped.
+template <int CNT>
+__device__ __forceinline__ void buf_store(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff, const float* s, float) {
+  static_assert(CNT % 4 == 0, "vector width");
+  typedef unsigned int u4 __attribute__((ext_vector_type(4)));
+#pragma unroll
+  for (int i = 0; i < CNT; i += 4) {
+    const u4 t = {__float_as_uint(s[i]), __float_as_uint(s[i + 1]), __float_as_uint(s[i + 2]), __float_as_uint(s[i + 3])};
+    __builtin_amdgcn_raw_buffer_store_b128(t, r, voff + 4 * i, soff, 0);
+  }
+}
+template <int CNT>
+__device__ __forceinline__ void buf_store(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff, const float* s, bf16_t) {
+  static_assert(CNT % 4 == 0, "vector width");
+  auto pack = [&](int i) {
+    return static_cast<uint32_t>(f32_to_bf16_bits(s[i])) | (static_cast<uint32_t>(f32_to_bf16_bits(s[i + 1])) << 16);
+  };
+  if constexpr (CNT % 8 == 0) {
+    typedef unsigned int u4 __attribute__((ext_vector_type(4)));
+#pragma unroll
+    for (int i = 0; i < CNT; i += 8) {
+      const u4 t = {pack(i), pack(i + 2), pack(i + 4), pack(i + 6)};
+      __builtin_amdgcn_raw_buffer_store_b128(t, r, voff + 2 * i, soff, 0);
+    }
+  } else {
+    typedef unsigned int u2 __attribute__((ext_vector_type(2)));
+    const u2 t = {pack(0), pack(2)};
+    __builtin_amdgcn_raw_buffer_store_b64(t, r, voff, soff, 0);
+  }
+}
+
 __device__ __forceinline__ uint32_t order_key(float f) {
   uint32_t u = __float_as_uint(f == 0.0f ? 0.0f : f);
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
