@@ -3,9 +3,8 @@
 // (Eq. 6 or the improved values).
 //
 // centroid_kernel: one wave per cluster sums the member rows of Q in fp64
-//   (members in ascending query order) and divides by the cluster size (used
-//   when the keys take several chunks; otherwise the clustering kernel forms
-//   the centroids).
+//   (members in ascending query order) and divides by the cluster size (the
+//   single-workgroup clustering kernel forms its centroids itself).
 //
 // attn_tile_kernel: one workgroup of eight waves per (unit, 16 centroids,
 //   1024-key chunk).  Logits S^T = K Q^c^T come from v_mfma_f32_16x16x4f32
