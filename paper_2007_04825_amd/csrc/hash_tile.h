@@ -24,7 +24,9 @@
 //
 // Operand layouts (16x16x32 bf16): lane l holds row (l % 16) and the eight
 // consecutive k of group (l / 16); the result lane l, register r holds
-// [4 (l / 16) + r][l % 16].  Rows are queries, columns planes.
+// [4 (l / 16) + r][l % 16].  Rows are planes, columns queries, so that a lane
+// ends with sixteen signs of one query (planes 16 pt + 4 (l / 16) + r) and
+// four lanes together hold its whole code.
 #pragma once
 #include "common.h"
 
@@ -38,12 +40,15 @@ __device__ __forceinline__ v4f mfma_bf16_16x16x32(v4u a, v4u b, v4f c) {
                                                  __builtin_bit_cast(v8bf, b), c, 0, 0, 0);
 }
 
-// B operands of the 64 plane columns (four 16-plane tiles) for D/32 k-chunks,
-// and the squared norm of this lane's plane column in each tile.
+// A operands of the 64 plane rows (four 16-plane tiles) for D/32 k-chunks,
+// and, for the planes whose signs this lane receives (16 pt + 4 (lane / 16) +
+// r), 2^-28 |P|^2 and whether they exist (bit 4 pt + r).
 template <int D>
 struct PlaneOps {
   v4u b[D / 32][4];
-  float n2[4];
+  float thr[4][4];
+  uint32_t valid;
+  bool norms_ok;  // every plane norm within the range of the fp32 test
 };
 
 // Copies the n_bits planes of one head [n_bits][D] into sp[64][D] (LDS; rows
@@ -91,8 +96,20 @@ __device__ __forceinline__ bool load_plane_ops(const float* sp, int n_bits, int 
       }
       P.b[kc][pt] = w;
     }
+  bool ok = true;
+  P.valid = 0u;
 #pragma unroll
-  for (int pt = 0; pt < 4; ++pt) P.n2[pt] = cross_rows_sum(sq[pt]);
+  for (int pt = 0; pt < 4; ++pt) {
+    const float n2 = cross_rows_sum(sq[pt]);  // |P|^2 of plane 16 pt + lane % 16
+    if (pt * 16 + c < n_bits) ok = ok && n2 >= 0x1p-45f && n2 < 0x1p+50f;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int src = 4 * g + r;  // lane holding plane 16 pt + 4 g + r
+      P.thr[pt][r] = 0x1p-28f * __shfl(n2, src);
+      if (pt * 16 + src < n_bits) P.valid |= 1u << (4 * pt + r);
+    }
+  }
+  P.norms_ok = __ballot(!ok) == 0ull;
   return __ballot(low != 0u) != 0ull;
 }
 
@@ -180,7 +197,7 @@ __device__ __forceinline__ QueryOps query_ops(const uint4 (&w)[1]) {
   return o;
 }
 
-// Code of query row0 + (lane % 16) for lanes 0..15 (other lanes: unspecified).
+// Code of query row0 + (lane % 16) (every lane of that column returns it).
 // qu: the unit's query rows; raw: this tile as loaded by load_tile; nq: valid
 // rows from row0 (>= 1); sp: the staged planes; exact_all: planes are not
 // bf16 values.
@@ -200,57 +217,46 @@ __device__ uint64_t hash_tile(const T* __restrict__ qu, const TileRaw<D, T>& raw
       qsq += o.sq;
 #pragma unroll
       for (int pt = 0; pt < 4; ++pt) {
-        s[pt] = mfma_bf16_16x16x32(o.hi, P.b[kc][pt], s[pt]);
+        s[pt] = mfma_bf16_16x16x32(P.b[kc][pt], o.hi, s[pt]);
         if constexpr (sizeof(T) == 4) {
-          s[pt] = mfma_bf16_16x16x32(o.mid, P.b[kc][pt], s[pt]);
-          s[pt] = mfma_bf16_16x16x32(o.lo, P.b[kc][pt], s[pt]);
+          s[pt] = mfma_bf16_16x16x32(P.b[kc][pt], o.mid, s[pt]);
+          s[pt] = mfma_bf16_16x16x32(P.b[kc][pt], o.lo, s[pt]);
         }
       }
     }
   }
-  // |Q|^2 of row c in every lane of column c; lane (c, g) needs rows 4g + r
-  qsq = cross_rows_sum(qsq);
-  float qn2[4];
+  qsq = cross_rows_sum(qsq);  // |Q|^2 of query c in all four lanes of column c
+  // signs and certainties as lane bit masks, bit 4 pt + r = plane 16 pt + 4 g + r
+  uint32_t pos = 0u, sure = 0u;
 #pragma unroll
-  for (int r = 0; r < 4; ++r) qn2[r] = __shfl(qsq, 4 * g + r);
-  // signs as lane bit masks, bit 4 pt + r; projections inside the band are
-  // recomputed afterwards (rare, divergent)
-  uint32_t posm = 0, uncm = 0;
-#pragma unroll
-  for (int pt = 0; pt < 4; ++pt) {
-    const int plane = pt * 16 + c;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int qq = 4 * g + r;
-      const bool valid = plane < n_bits && qq < nq;
-      const float sv = s[pt][r];
-      const float np = qn2[r] * P.n2[pt];
-      const bool sure = np >= 0x1p-90f && np < 0x1p+100f && sv * sv > 0x1p-28f * np;
-      posm |= static_cast<uint32_t>(valid && sv > 0.0f) << (4 * pt + r);
-      uncm |= static_cast<uint32_t>(valid && (exact_all || !sure)) << (4 * pt + r);
-    }
+  for (int k = 15; k >= 0; --k) {
+    const float sv = s[k >> 2][k & 3];
+    pos = (pos << 1) | (sv > 0.0f ? 1u : 0u);
+    sure = (sure << 1) | (sv * sv > qsq * P.thr[k >> 2][k & 3] ? 1u : 0u);
   }
-  if (__ballot(uncm != 0u) != 0ull) {
-    uint32_t m = uncm;
+  const uint32_t valid = c < nq ? P.valid : 0u;
+  const bool fast = !exact_all && P.norms_ok && qsq >= 0x1p-45f && qsq < 0x1p+50f;
+  const uint32_t unc = fast ? (valid & ~sure) : valid;
+  pos &= valid;
+  // projections inside the band: the fp64 chain (rare, divergent)
+  if (__ballot(unc != 0u) != 0ull) {
+    uint32_t m = unc;
     while (m != 0u) {
       const int k = __ffs(m) - 1;
       m &= m - 1;
-      const int pt = k >> 2, r = k & 3;
-      const double p = exact_projection<D, T>(qu + static_cast<size_t>(row0 + 4 * g + r) * D,
-                                              sp + (pt * 16 + c) * D);
-      posm = p > 0.0 ? (posm | (1u << k)) : (posm & ~(1u << k));
+      const double p = exact_projection<D, T>(qu + static_cast<size_t>(row0 + c) * D,
+                                              sp + ((k >> 2) * 16 + 4 * g + (k & 3)) * D);
+      pos = p > 0.0 ? (pos | (1u << k)) : (pos & ~(1u << k));
     }
   }
-  uint64_t code = 0;
-#pragma unroll
-  for (int pt = 0; pt < 4; ++pt)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const uint64_t bl = __ballot((posm >> (4 * pt + r)) & 1u);
-      // query qq' = 4 g' + r of the tile sits in field g' of this ballot
-      if (r == (lane & 3)) code |= ((bl >> (16 * ((lane >> 2) & 3))) & 0xffffull) << (16 * pt);
-    }
-  return code;
+  // this lane's 16 bits in place, then OR over the four lanes of the column
+  uint32_t lo = ((pos & 0xfu) | ((pos & 0xf0u) << 12)) << (4 * g);
+  uint32_t hi = (((pos >> 8) & 0xfu) | (((pos >> 12) & 0xfu) << 16)) << (4 * g);
+  lo |= lane_xor16_u(lo);
+  hi |= lane_xor16_u(hi);
+  lo |= lane_xor32_u(lo);
+  hi |= lane_xor32_u(hi);
+  return (static_cast<uint64_t>(hi) << 32) | lo;
 }
 
 }  // namespace ca
