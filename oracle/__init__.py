@@ -64,6 +64,12 @@ def _load():
     lib.orc_forward.argtypes = [dp, dp, dp, i32p, i32, i32, i64, i32, dp, i32, i32,
                                 i32, i32, i32, dp, u64p, i32p, i32p, dp, i32p, dp, dp]
     lib.orc_forward.restype = i32
+    lib.orc_clustered_backward.argtypes = [dp, dp, dp, i64, i32, i32p, i32, dp, dp, dp, dp]
+    lib.orc_iclustered_backward.argtypes = [dp, dp, dp, i64, i32, i32p, i32, i32, i32p, dp,
+                                            dp, dp, dp]
+    lib.orc_backward.argtypes = [dp, dp, dp, i32p, i32, i32, i64, i32, i32, i32, i32p, i32p,
+                                 dp, i32, dp, dp, dp]
+    lib.orc_backward.restype = i32
     _lib = lib
     return lib
 
@@ -231,3 +237,59 @@ def forward(q, k, v, lengths, planes, C, n_bits, L, topk_=0, num_threads=None,
     if rc != 0:
         raise ValueError("oracle rejected the arguments")
     return res
+
+
+def clustered_backward(q, k, v, assign, C, dout):
+    """Gradients (dq, dk, dv) of clustered attention of one (batch, head) for a
+    fixed partition, given the output gradient dout [n, d]."""
+    q, k, v, dout = _f64(q), _f64(k), _f64(v), _f64(dout)
+    assign = np.ascontiguousarray(assign, dtype=np.int32)
+    n, d = q.shape
+    dq, dk, dv = (np.zeros((n, d), np.float64) for _ in range(3))
+    P = ctypes.c_double
+    _load().orc_clustered_backward(_ptr(q, P), _ptr(k, P), _ptr(v, P), n, d,
+                                   _ptr(assign, ctypes.c_int32), C, _ptr(dout, P),
+                                   _ptr(dq, P), _ptr(dk, P), _ptr(dv, P))
+    return dq, dk, dv
+
+
+def iclustered_backward(q, k, v, assign, C, topk_, dout, topk_in=None):
+    """Gradients (dq, dk, dv) of improved clustered attention of one (batch,
+    head) for a fixed partition and fixed top-k sets (selected as in the
+    forward pass when topk_in is None)."""
+    q, k, v, dout = _f64(q), _f64(k), _f64(v), _f64(dout)
+    assign = np.ascontiguousarray(assign, dtype=np.int32)
+    n, d = q.shape
+    dq, dk, dv = (np.zeros((n, d), np.float64) for _ in range(3))
+    tin = None if topk_in is None else np.ascontiguousarray(topk_in, dtype=np.int32)
+    P = ctypes.c_double
+    _load().orc_iclustered_backward(_ptr(q, P), _ptr(k, P), _ptr(v, P), n, d,
+                                    _ptr(assign, ctypes.c_int32), C, topk_,
+                                    _ptr(tin, ctypes.c_int32), _ptr(dout, P),
+                                    _ptr(dq, P), _ptr(dk, P), _ptr(dv, P))
+    return dq, dk, dv
+
+
+def backward(q, k, v, lengths, C, topk_, assign, topk_sets, dout, num_threads=None):
+    """Gradients over [B, H, N, d] inputs for the partition (assign [B, H, N])
+    and, for topk_ >= 1, the top-k sets (topk_sets [B, H, C, topk_]) of a
+    forward pass.  Returns (dq, dk, dv); padded rows get zero gradients."""
+    q, k, v, dout = _f64(q), _f64(k), _f64(v), _f64(dout)
+    B, H, N, d = q.shape
+    lens = None if lengths is None else np.ascontiguousarray(lengths, dtype=np.int32)
+    assign = np.ascontiguousarray(assign, dtype=np.int32)
+    ts = None
+    if topk_ > 0 and topk_sets is not None:
+        ts = np.ascontiguousarray(topk_sets, dtype=np.int32)
+        assert ts.shape == (B, H, C, topk_)
+    dq, dk, dv = (np.zeros((B, H, N, d), np.float64) for _ in range(3))
+    if num_threads is None:
+        num_threads = os.cpu_count() or 1
+    P = ctypes.c_double
+    rc = _load().orc_backward(_ptr(q, P), _ptr(k, P), _ptr(v, P), _ptr(lens, ctypes.c_int32),
+                              B, H, N, d, C, topk_, _ptr(assign, ctypes.c_int32),
+                              _ptr(ts, ctypes.c_int32), _ptr(dout, P), int(num_threads),
+                              _ptr(dq, P), _ptr(dk, P), _ptr(dv, P))
+    if rc != 0:
+        raise ValueError("oracle rejected the arguments")
+    return dq, dk, dv

@@ -28,6 +28,12 @@
  *     C_eff = min(C, n), k_eff = min(k, n).
  *   - the top-k set ranks keys by their centroid logit (equivalently by A^c,
  *     softmax being monotone); a tie goes to the smaller key index.
+ *   - gradients (the paper trains through the operator but writes no
+ *     backward pass): the partition and the top-k sets are discrete and held
+ *     constant; the gradient flows through the centroids (Eq. 3), the
+ *     centroid softmax (Eq. 4-5), the broadcast (Eq. 6) and, for the improved
+ *     variant, through the exact top-k logits, the mass m_j and the rest
+ *     part Vb_j, all of which depend on the centroid attention.
  *
  * Parity status: every function here is pinned by the CPU test-suite against
  * closed forms, brute force or special cases; none is marked unpinned.
@@ -494,6 +500,259 @@ int orc_forward(const double* q, const double* k, const double* v,
     free(vcb);
     free(tk);
     free(ms);
+  }
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Gradients.  The softmax rule: for a = softmax(s) and an upstream gradient  */
+/* g_a on a, the gradient on s is a_l (g_a,l - sum_r a_r g_a,r).              */
+/* ------------------------------------------------------------------------ */
+static void softmax_backward(const double* a, const double* ga, int64_t n, double* gs) {
+  double dot = 0.0;
+  for (int64_t l = 0; l < n; ++l) dot += a[l] * ga[l];
+  for (int64_t l = 0; l < n; ++l) gs[l] = a[l] * (ga[l] - dot);
+}
+
+/* Centroid part shared by both variants, for one non-empty cluster j: given */
+/* the row a = A^c_j, the logit gradient gs (of s_jl = Q^c_j . K_l / sqrt(d)),*/
+/* adds (1/sqrt(d)) gs_l Q^c_j to dk_l and returns dQ^c_j in dqc.            */
+static void centroid_logit_backward(const double* qcj, const double* k, int64_t n, int d,
+                                    const double* gs, double* dk, double* dqc) {
+  const double scale = 1.0 / sqrt((double)d);
+  for (int t = 0; t < d; ++t) dqc[t] = 0.0;
+  for (int64_t l = 0; l < n; ++l) {
+    for (int t = 0; t < d; ++t) {
+      dqc[t] += scale * gs[l] * k[l * d + t];
+      dk[l * d + t] += scale * gs[l] * qcj[t];
+    }
+  }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Backward pass of clustered attention (Eq. 3-6) for one (batch, head) given */
+/* the partition, which is held constant.  dout, dq, dk, dv are [n][d].       */
+/*   Eq. 6:  G_j = sum_{i in S_j} dout_i                                      */
+/*   Eq. 5:  dV_l += sum_j A^c_jl G_j;   gA_jl = G_j . V_l                    */
+/*   Eq. 4:  gs_j = softmax rule(A^c_j, gA_j); dQ^c_j, dK from s_jl           */
+/*   Eq. 3:  dQ_i = dQ^c_{a_i} / |S_{a_i}|                                    */
+/* ------------------------------------------------------------------------ */
+void orc_clustered_backward(const double* q, const double* k, const double* v,
+                            int64_t n, int d, const int32_t* assign, int C,
+                            const double* dout, double* dq, double* dk, double* dv) {
+  const int64_t nn = n > 0 ? n : 1;
+  double* qc = (double*)malloc(sizeof(double) * (size_t)C * d);
+  int64_t* sizes = (int64_t*)malloc(sizeof(int64_t) * (size_t)C);
+  double* s = (double*)malloc(sizeof(double) * (size_t)nn);
+  double* a = (double*)malloc(sizeof(double) * (size_t)nn);
+  double* ga = (double*)malloc(sizeof(double) * (size_t)nn);
+  double* gs = (double*)malloc(sizeof(double) * (size_t)nn);
+  double* G = (double*)malloc(sizeof(double) * (size_t)d);
+  double* dqc = (double*)calloc((size_t)C * d, sizeof(double));
+  for (int64_t x = 0; x < n * d; ++x) dq[x] = dk[x] = dv[x] = 0.0;
+  orc_centroids(q, n, d, assign, C, qc, sizes);
+  for (int j = 0; j < C; ++j) {
+    if (sizes[j] == 0) continue;
+    for (int t = 0; t < d; ++t) G[t] = 0.0;
+    for (int64_t i = 0; i < n; ++i)
+      if (assign[i] == j)
+        for (int t = 0; t < d; ++t) G[t] += dout[i * d + t];
+    orc_centroid_row(qc + (int64_t)j * d, k, n, d, s, a);
+    for (int64_t l = 0; l < n; ++l) {
+      double g = 0.0;
+      for (int t = 0; t < d; ++t) {
+        dv[l * d + t] += a[l] * G[t];
+        g += G[t] * v[l * d + t];
+      }
+      ga[l] = g;
+    }
+    softmax_backward(a, ga, n, gs);
+    centroid_logit_backward(qc + (int64_t)j * d, k, n, d, gs, dk, dqc + (int64_t)j * d);
+  }
+  for (int64_t i = 0; i < n; ++i) {
+    const int j = assign[i];
+    for (int t = 0; t < d; ++t) dq[i * d + t] = dqc[(int64_t)j * d + t] / (double)sizes[j];
+  }
+  free(qc);
+  free(sizes);
+  free(s);
+  free(a);
+  free(ga);
+  free(gs);
+  free(G);
+  free(dqc);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Backward pass of improved clustered attention for one (batch, head) given  */
+/* the partition and the top-k sets T (C x topk, -1 padded; NULL selects them */
+/* as the forward does), all held constant.  For i in S_j the forward is      */
+/*   w_i   = softmax_{l in T_j}(t_il),  t_il = Q_i . K_l / sqrt(d)            */
+/*   U_i   = sum_{l in T_j} w_il V_l,   out_i = m_j U_i + Vb_j,               */
+/*   m_j   = sum_{l in T_j} A^c_jl,     Vb_j = sum_{l not in T_j} A^c_jl V_l, */
+/* so, with g_i = dout_i:                                                     */
+/*   dm_j  = sum_{i in S_j} g_i . U_i,  dVb_j = sum_{i in S_j} g_i            */
+/*   top-k part:  dV_l += m_j w_il g_i;  gw_il = m_j g_i . V_l;               */
+/*                gt_i = softmax rule(w_i, gw_i);  dQ_i, dK_l from t_il       */
+/*   centroid part:  gA_jl = dm_j (l in T_j), dVb_j . V_l (otherwise);        */
+/*                   dV_l += A^c_jl dVb_j (l not in T_j);                      */
+/*                   gs_j = softmax rule(A^c_j, gA_j); dQ^c_j, dK from s_jl;  */
+/*                   dQ_i += dQ^c_{a_i} / |S_{a_i}|.                          */
+/* ------------------------------------------------------------------------ */
+void orc_iclustered_backward(const double* q, const double* k, const double* v,
+                             int64_t n, int d, const int32_t* assign, int C, int topk,
+                             const int32_t* topk_in, const double* dout,
+                             double* dq, double* dk, double* dv) {
+  const double scale = 1.0 / sqrt((double)d);
+  const int64_t nn = n > 0 ? n : 1;
+  const int ke = (int64_t)topk < n ? topk : (int)n;
+  const int kc = ke > 0 ? ke : 1;
+  double* qc = (double*)malloc(sizeof(double) * (size_t)C * d);
+  int64_t* sizes = (int64_t*)malloc(sizeof(int64_t) * (size_t)C);
+  double* s = (double*)malloc(sizeof(double) * (size_t)nn);
+  double* a = (double*)malloc(sizeof(double) * (size_t)nn);
+  double* ga = (double*)malloc(sizeof(double) * (size_t)nn);
+  double* gs = (double*)malloc(sizeof(double) * (size_t)nn);
+  char* in_t = (char*)malloc((size_t)nn);
+  int32_t* tj = (int32_t*)malloc(sizeof(int32_t) * (size_t)(topk > kc ? topk : kc));
+  double* w = (double*)malloc(sizeof(double) * (size_t)(topk > kc ? topk : kc));
+  double* gw = (double*)malloc(sizeof(double) * (size_t)(topk > kc ? topk : kc));
+  double* gt = (double*)malloc(sizeof(double) * (size_t)(topk > kc ? topk : kc));
+  double* U = (double*)malloc(sizeof(double) * (size_t)d);
+  double* dVb = (double*)malloc(sizeof(double) * (size_t)d);
+  double* dqc = (double*)calloc((size_t)C * d, sizeof(double));
+  for (int64_t x = 0; x < n * d; ++x) dq[x] = dk[x] = dv[x] = 0.0;
+  orc_centroids(q, n, d, assign, C, qc, sizes);
+  for (int j = 0; j < C; ++j) {
+    if (sizes[j] == 0) continue;
+    orc_centroid_row(qc + (int64_t)j * d, k, n, d, s, a);
+    int kj;
+    if (topk_in) {
+      kj = 0;
+      while (kj < topk && topk_in[(int64_t)j * topk + kj] >= 0) {
+        tj[kj] = topk_in[(int64_t)j * topk + kj];
+        ++kj;
+      }
+    } else {
+      kj = orc_topk(s, n, ke, tj);
+    }
+    memset(in_t, 0, (size_t)nn);
+    double m = 0.0;
+    for (int r = 0; r < kj; ++r) {
+      in_t[tj[r]] = 1;
+      m += a[tj[r]];
+    }
+    double dm = 0.0;
+    for (int t = 0; t < d; ++t) dVb[t] = 0.0;
+    /* top-k part, query by query */
+    for (int64_t i = 0; i < n; ++i) {
+      if (assign[i] != j) continue;
+      const double* g = dout + i * d;
+      double mx = -INFINITY;
+      for (int r = 0; r < kj; ++r) {
+        double dot = 0.0;
+        for (int t = 0; t < d; ++t) dot += q[i * d + t] * k[(int64_t)tj[r] * d + t];
+        w[r] = dot * scale;
+        if (w[r] > mx) mx = w[r];
+      }
+      double z = 0.0;
+      for (int r = 0; r < kj; ++r) {
+        w[r] = exp(w[r] - mx);
+        z += w[r];
+      }
+      for (int r = 0; r < kj; ++r) w[r] /= z;
+      for (int t = 0; t < d; ++t) {
+        double acc = 0.0;
+        for (int r = 0; r < kj; ++r) acc += w[r] * v[(int64_t)tj[r] * d + t];
+        U[t] = acc;
+      }
+      for (int t = 0; t < d; ++t) {
+        dm += g[t] * U[t];
+        dVb[t] += g[t];
+      }
+      for (int r = 0; r < kj; ++r) {
+        const int64_t l = tj[r];
+        double dot = 0.0;
+        for (int t = 0; t < d; ++t) {
+          dv[l * d + t] += m * w[r] * g[t];
+          dot += g[t] * v[l * d + t];
+        }
+        gw[r] = m * dot;
+      }
+      softmax_backward(w, gw, kj, gt);
+      for (int r = 0; r < kj; ++r) {
+        const int64_t l = tj[r];
+        for (int t = 0; t < d; ++t) {
+          dq[i * d + t] += scale * gt[r] * k[l * d + t];
+          dk[l * d + t] += scale * gt[r] * q[i * d + t];
+        }
+      }
+    }
+    /* centroid part */
+    for (int64_t l = 0; l < n; ++l) {
+      if (in_t[l]) {
+        ga[l] = dm;
+      } else {
+        double dot = 0.0;
+        for (int t = 0; t < d; ++t) {
+          dv[l * d + t] += a[l] * dVb[t];
+          dot += dVb[t] * v[l * d + t];
+        }
+        ga[l] = dot;
+      }
+    }
+    softmax_backward(a, ga, n, gs);
+    centroid_logit_backward(qc + (int64_t)j * d, k, n, d, gs, dk, dqc + (int64_t)j * d);
+  }
+  for (int64_t i = 0; i < n; ++i) {
+    const int j = assign[i];
+    for (int t = 0; t < d; ++t) dq[i * d + t] += dqc[(int64_t)j * d + t] / (double)sizes[j];
+  }
+  free(qc);
+  free(sizes);
+  free(s);
+  free(a);
+  free(ga);
+  free(gs);
+  free(in_t);
+  free(tj);
+  free(w);
+  free(gw);
+  free(gt);
+  free(U);
+  free(dVb);
+  free(dqc);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Backward pass over a batch, for the partition (assign [B][H][N], -1 on     */
+/* padded rows) and, for topk >= 1, the top-k sets (topk_sets [B][H][C][topk],*/
+/* -1 padded) of a forward pass.  dout, dq, dk, dv are [B][H][N][d]; rows at  */
+/* positions >= length get zero gradients.  Returns 0, or -1 on invalid args. */
+/* ------------------------------------------------------------------------ */
+int orc_backward(const double* q, const double* k, const double* v,
+                 const int32_t* lengths, int batch, int heads, int64_t N, int d, int C,
+                 int topk, const int32_t* assign, const int32_t* topk_sets,
+                 const double* dout, int num_threads, double* dq, double* dk, double* dv) {
+  if (batch < 0 || heads < 0 || N < 0 || d < 1 || C < 1) return -1;
+  const int64_t units = (int64_t)batch * heads;
+  const int nth = num_threads > 0 ? num_threads : omp_get_max_threads();
+#pragma omp parallel for schedule(dynamic, 1) num_threads(nth)
+  for (int64_t u = 0; u < units; ++u) {
+    const int b = (int)(u / heads);
+    int64_t n = lengths ? lengths[b] : N;
+    if (n < 0) n = 0;
+    if (n > N) n = N;
+    const int64_t off = u * N * d;
+    for (int64_t x = 0; x < N * d; ++x) dq[off + x] = dk[off + x] = dv[off + x] = 0.0;
+    if (n == 0) continue;
+    if (topk <= 0)
+      orc_clustered_backward(q + off, k + off, v + off, n, d, assign + u * N, C, dout + off,
+                             dq + off, dk + off, dv + off);
+    else
+      orc_iclustered_backward(q + off, k + off, v + off, n, d, assign + u * N, C, topk,
+                              topk_sets ? topk_sets + u * C * topk : NULL, dout + off,
+                              dq + off, dk + off, dv + off);
   }
   return 0;
 }

@@ -35,4 +35,15 @@ int orc_forward(const double* q, const double* k, const double* v,
                 int num_threads, double* out, uint64_t* codes_out,
                 int32_t* assign_out, int32_t* sizes_out, double* qc_out,
                 int32_t* topk_out, double* mass_out, double* vcb_out);
+void orc_clustered_backward(const double* q, const double* k, const double* v,
+                            int64_t n, int d, const int32_t* assign, int C,
+                            const double* dout, double* dq, double* dk, double* dv);
+void orc_iclustered_backward(const double* q, const double* k, const double* v,
+                             int64_t n, int d, const int32_t* assign, int C, int topk,
+                             const int32_t* topk_in, const double* dout,
+                             double* dq, double* dk, double* dv);
+int orc_backward(const double* q, const double* k, const double* v,
+                 const int32_t* lengths, int batch, int heads, int64_t N, int d, int C,
+                 int topk, const int32_t* assign, const int32_t* topk_sets,
+                 const double* dout, int num_threads, double* dq, double* dk, double* dv);
 #endif
