@@ -8,7 +8,8 @@ seeded by ``SeedSequence([200704825, config, stream, extra])``, rounded to
 fp32 (round-to-nearest-even), and, where the workload is bf16, rounded again to
 the nearest bf16 value (ties to even) while being stored in a float32 array.
 The stream ids are: 0 query noise, 1 keys, 2 values, 3 mixture means,
-4 query labels, 5 lengths, 6 drift phases, 7 hyperplanes, 8 key labels.
+4 query labels, 5 lengths, 6 drift phases, 7 hyperplanes, 8 key labels,
+9 output gradients (backward-pass tests and benchmark).
 
 The paper's workloads (speech encoders on WSJ / Switchboard, a RoBERTa encoder
 on GLUE / SQuAD, and the synthetic length sweep of its time benchmark) are
@@ -181,3 +182,16 @@ def random_unit(seed, n, d, scale=1.0, dtype="f32"):
     if dtype == "bf16":
         x = round_bf16(x)
     return x[0], x[1], x[2]
+
+
+def output_gradient(w: Workload, extra: int = 0, pad_value: float = 0.0) -> np.ndarray:
+    """An upstream gradient for the attention output of workload w: iid N(0, 1)
+    of the output's shape, rounded like the inputs (fp32, then bf16 for bf16
+    workloads); rows past each sequence's length hold pad_value."""
+    cfg = {"tiny": 1, "speech": 2, "sweep": 3, "encoder": 4, "long": 5}.get(w.name.split("_")[0], 0)
+    g = rng(cfg, 9, extra).standard_normal(w.q.shape).astype(np.float32)
+    if w.dtype == "bf16":
+        g = round_bf16(g)
+    N = w.q.shape[2]
+    pad = np.arange(N)[None, None, :, None] >= w.lengths[:, None, None, None]
+    return np.where(pad, np.float32(pad_value), g).astype(np.float32)

@@ -23,8 +23,10 @@
  *   C_eff = min(C, length) clusters and k_eff = min(k, length) keys.
  * - workspace is a DEVICE buffer of at least ca_workspace_bytes(...) bytes,
  *   owned by the caller and 256-byte aligned; its contents on entry do not
- *   matter and on exit are unspecified.  The library allocates no device
- *   memory in a forward call.
+ *   matter.  On exit it holds the forward pass's state (partition,
+ *   centroids, top-k sets, softmax statistics), which the backward entry
+ *   points below read; nothing else about its contents is specified.  The
+ *   library allocates no device memory in a forward or backward call.
  * - stream is a hipStream_t (NULL = the null stream).  All work is enqueued
  *   on it and the call returns without synchronising.  Arguments are
  *   validated on the host before anything is enqueued: on an error nothing
@@ -39,6 +41,10 @@
  * Supported sizes: d in {32, 64}; 1 <= n_bits <= 63; 1 <= C <= 256;
  * 1 <= L <= 1000; 1 <= k <= 128; 1 <= n <= 1048576; 1 <= batch*heads <= 65535
  * and batch*heads*n < 2^31.
+ *
+ * The backward entry points (clustered_attention_bwd, iclustered_attention_bwd)
+ * follow the same conventions; their gradient outputs are fp32 for both
+ * input dtypes.
  */
 #ifndef CLUSTERED_ATTN_H
 #define CLUSTERED_ATTN_H
@@ -142,6 +148,69 @@ int iclustered_attention_fwd(const void* q, const void* k, const void* v,
                              int n_clusters, int n_bits, int lloyd_iters,
                              int topk, void* out, void* workspace,
                              size_t workspace_bytes, const ca_aux* aux,
+                             void* stream);
+
+/*
+ * Backward pass.  The paper trains through the operator (Section 4) without
+ * writing its gradient; here the partition (Section 3.2.2) and the top-k
+ * sets (Section 3.3) are discrete and held constant, and the gradient flows
+ * through the centroids (Eq. 3), the centroid softmax and values (Eqs. 4-5),
+ * the broadcast (Eq. 6) and, for the improved variant, through the exact
+ * top-k logits, the mass m_j and the rest part of the supplementary
+ * decomposition (all three depend on Q, K and V).
+ *
+ * Bytes of bwd_workspace that clustered_attention_bwd (topk = 0) or
+ * iclustered_attention_bwd (topk >= 1) needs; 0 for invalid sizes.
+ */
+size_t ca_backward_workspace_bytes(int batch, int heads, int n, int d, int dtype,
+                                   int n_clusters, int topk);
+
+/*
+ * Gradients of the clustered attention forward pass (the same arguments as
+ * clustered_attention_fwd) with respect to q, k and v, for the output
+ * gradient dout ([batch][heads][n][d], element type dtype, DEVICE):
+ *   G_j = sum of dout_i over the members of cluster j;
+ *   dV_l = sum_j A^c_jl G_j;  dS_jl = A^c_jl (G_j . V_l - G_j . V^c_j);
+ *   dK_l = sum_j dS_jl Q^c_j / sqrt(d);  dQ_i = sum_l dS_{a_i,l} K_l / (sqrt(d) |S_{a_i}|).
+ * workspace must be the buffer of the forward call made last with the same
+ * q, k, v, lengths and sizes (clustered_attention_fwd, n_clusters as given),
+ * unchanged since; it is only read.  dq, dk, dv are DEVICE fp32
+ * [batch][heads][n][d], written fully (rows past a length get 0).
+ * bwd_workspace is a caller-owned DEVICE buffer of at least
+ * ca_backward_workspace_bytes bytes, 256-byte aligned, contents irrelevant.
+ * Enqueued on stream; validation before any launch; deterministic (no
+ * floating-point atomics).
+ */
+int clustered_attention_bwd(const void* q, const void* k, const void* v,
+                            const int32_t* lengths, int batch, int heads, int n,
+                            int d, int dtype, int n_clusters, const void* dout,
+                            float* dq, float* dk, float* dv, const void* workspace,
+                            size_t workspace_bytes, void* bwd_workspace,
+                            size_t bwd_workspace_bytes, void* stream);
+
+/*
+ * Gradients of the improved clustered attention forward pass (Section 3.3,
+ * Eq. 11 in its supplementary decomposition), with the top-k sets of the
+ * forward call held constant.  For query i in cluster j, with
+ * w_i = softmax_{T_j}(Q_i K_l / sqrt(d)), U_i = sum_{l in T_j} w_il V_l and
+ * g_i = dout_i:
+ *   dm_j = sum_i g_i . U_i;  gt_il = m_j w_il (g_i . V_l - g_i . U_i);
+ *   top-k part:    dQ_i += sum_l gt_il K_l / sqrt(d),
+ *                  dK_l += sum_i gt_il Q_i / sqrt(d),  dV_l += m_j sum_i w_il g_i;
+ *   centroid part: gA_jl = dm_j on T_j, G_j . V_l elsewhere;
+ *                  dV_l += sum_j [l not in T_j] A^c_jl G_j;
+ *                  dS_jl = A^c_jl (gA_jl - sum_l' A^c_jl' gA_jl'), then dQ^c,
+ *                  dK and dQ as for the clustered variant.
+ * workspace must be that of the last iclustered_attention_fwd call with the
+ * same inputs, n_clusters and topk; other arguments as for
+ * clustered_attention_bwd.
+ */
+int iclustered_attention_bwd(const void* q, const void* k, const void* v,
+                             const int32_t* lengths, int batch, int heads, int n,
+                             int d, int dtype, int n_clusters, int topk,
+                             const void* dout, float* dq, float* dk, float* dv,
+                             const void* workspace, size_t workspace_bytes,
+                             void* bwd_workspace, size_t bwd_workspace_bytes,
                              void* stream);
 
 /* Message describing the last non-zero status returned on this thread. */

@@ -17,6 +17,8 @@ __all__ = [
     "CA_F32", "CA_BF16", "Aux", "ClusteredAttnError", "library", "lib_path",
     "workspace_bytes", "clustered_attention_fwd", "iclustered_attention_fwd",
     "clustered_attention", "iclustered_attention", "set_kmeans_path", "EXPORTED_SYMBOLS",
+    "backward_workspace_bytes", "clustered_attention_bwd", "iclustered_attention_bwd",
+    "clustered_attention_backward", "iclustered_attention_backward",
 ]
 
 CA_OK = 0
@@ -28,7 +30,9 @@ CA_F32 = 0
 CA_BF16 = 1
 
 EXPORTED_SYMBOLS = ("ca_workspace_bytes", "clustered_attention_fwd", "iclustered_attention_fwd",
-                    "ca_last_error", "ca_version", "ca_set_kmeans_path", "ca_time_next_stage")
+                    "ca_last_error", "ca_version", "ca_set_kmeans_path", "ca_time_next_stage",
+                    "ca_backward_workspace_bytes", "clustered_attention_bwd",
+                    "iclustered_attention_bwd")
 CA_KERNEL_HASH, CA_KERNEL_KMEANS, CA_KERNEL_CENTROIDS, CA_KERNEL_CENTROID_ATTN, CA_KERNEL_OUTPUT = \
     1, 2, 3, 4, 5
 STAGES = {"hash": 1, "kmeans": 2, "centroids": 3, "centroid_attn": 4, "output": 5}
@@ -75,6 +79,14 @@ def library():
     lib.ca_set_kmeans_path.restype = i32
     lib.ca_time_next_stage.argtypes = [i32, vp, vp]
     lib.ca_time_next_stage.restype = i32
+    lib.ca_backward_workspace_bytes.argtypes = [i32] * 7
+    lib.ca_backward_workspace_bytes.restype = sz
+    bcommon = [vp, vp, vp, vp, i32, i32, i32, i32, i32, i32]
+    btail = [vp, vp, vp, vp, vp, sz, vp, sz, vp]
+    lib.clustered_attention_bwd.argtypes = bcommon + btail
+    lib.clustered_attention_bwd.restype = i32
+    lib.iclustered_attention_bwd.argtypes = bcommon + [i32] + btail
+    lib.iclustered_attention_bwd.restype = i32
     _lib = lib
     return lib
 
@@ -86,6 +98,30 @@ def _check(rc: int):
 
 def workspace_bytes(batch, heads, n, d, dtype, n_clusters, n_bits, topk=0) -> int:
     return int(library().ca_workspace_bytes(batch, heads, n, d, dtype, n_clusters, n_bits, topk))
+
+
+def backward_workspace_bytes(batch, heads, n, d, dtype, n_clusters, topk=0) -> int:
+    return int(library().ca_backward_workspace_bytes(batch, heads, n, d, dtype, n_clusters, topk))
+
+
+def clustered_attention_bwd(q, k, v, lengths, batch, heads, n, d, dtype, n_clusters, dout, dq, dk,
+                            dv, workspace, workspace_nbytes, bwd_workspace, bwd_workspace_nbytes,
+                            stream=None):
+    """Raw call with integer device addresses; returns the status code."""
+    return library().clustered_attention_bwd(q, k, v, lengths, batch, heads, n, d, dtype,
+                                             n_clusters, dout, dq, dk, dv, workspace,
+                                             workspace_nbytes, bwd_workspace,
+                                             bwd_workspace_nbytes, stream)
+
+
+def iclustered_attention_bwd(q, k, v, lengths, batch, heads, n, d, dtype, n_clusters, topk, dout,
+                             dq, dk, dv, workspace, workspace_nbytes, bwd_workspace,
+                             bwd_workspace_nbytes, stream=None):
+    """Raw call with integer device addresses; returns the status code."""
+    return library().iclustered_attention_bwd(q, k, v, lengths, batch, heads, n, d, dtype,
+                                              n_clusters, topk, dout, dq, dk, dv, workspace,
+                                              workspace_nbytes, bwd_workspace,
+                                              bwd_workspace_nbytes, stream)
 
 
 def time_next_stage(stage: int, start_event, stop_event):
@@ -217,3 +253,48 @@ def iclustered_attention(q, k, v, planes, n_clusters=100, n_bits=63, lloyd_iters
                                     _ptr(planes), B, H, N, D, dt, n_clusters, n_bits, lloyd_iters,
                                     topk, out.data_ptr(), ws.data_ptr(), need, aux, stream))
     return out
+
+
+def _backward(q, k, v, dout, n_clusters, topk, lengths, workspace, bwd_workspace, grads):
+    torch = _torch()
+    B, H, N, D = _prepare(q, k, v, None, lengths)
+    if dout.shape != q.shape or dout.dtype != q.dtype or not dout.is_contiguous():
+        raise ValueError("dout must be a contiguous tensor like q")
+    if workspace is None:
+        raise ValueError("workspace: pass the buffer that the forward call used")
+    dt = _dtype_code(q)
+    bneed = backward_workspace_bytes(B, H, N, D, dt, n_clusters, topk)
+    if bneed == 0:
+        bneed = 1  # invalid sizes: the call below reports why
+    bws = _workspace(bneed, q.device, bwd_workspace)
+    if grads is None:
+        grads = tuple(torch.empty(q.shape, dtype=torch.float32, device=q.device) for _ in range(3))
+    dq, dk, dv = grads
+    stream = torch.cuda.current_stream(q.device).cuda_stream
+    wbytes = workspace.numel() * workspace.element_size()
+    if topk > 0:
+        rc = iclustered_attention_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), _ptr(lengths), B, H,
+                                      N, D, dt, n_clusters, topk, dout.data_ptr(), dq.data_ptr(),
+                                      dk.data_ptr(), dv.data_ptr(), workspace.data_ptr(), wbytes,
+                                      bws.data_ptr(), bws.numel(), stream)
+    else:
+        rc = clustered_attention_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), _ptr(lengths), B, H,
+                                     N, D, dt, n_clusters, dout.data_ptr(), dq.data_ptr(),
+                                     dk.data_ptr(), dv.data_ptr(), workspace.data_ptr(), wbytes,
+                                     bws.data_ptr(), bws.numel(), stream)
+    _check(rc)
+    return dq, dk, dv
+
+
+def clustered_attention_backward(q, k, v, dout, n_clusters, workspace, lengths=None,
+                                 bwd_workspace=None, grads=None):
+    """Gradients (dq, dk, dv), fp32, of the clustered forward call that last
+    used ``workspace`` with these inputs (partition held constant)."""
+    return _backward(q, k, v, dout, n_clusters, 0, lengths, workspace, bwd_workspace, grads)
+
+
+def iclustered_attention_backward(q, k, v, dout, n_clusters, topk, workspace, lengths=None,
+                                  bwd_workspace=None, grads=None):
+    """Gradients (dq, dk, dv), fp32, of the improved clustered forward call
+    that last used ``workspace`` (partition and top-k sets held constant)."""
+    return _backward(q, k, v, dout, n_clusters, topk, lengths, workspace, bwd_workspace, grads)

@@ -70,6 +70,36 @@ size_t carve_workspace(const Problem& p, void* base, Workspace* ws) {
   w.topk = static_cast<int32_t*>(take(p.topk > 0 ? U * C * K * 4 : 0));
   w.mass = static_cast<float*>(take(p.topk > 0 ? U * C * 4 : 0));
   w.vcb = static_cast<float*>(take(U * C * D * 4));
+  w.stats = static_cast<float*>(take(U * C * 2 * 4));
+  if (ws) *ws = w;
+  return off;
+}
+
+size_t carve_bwd_workspace(const BwdProblem& p, void* base, BwdWorkspace* ws) {
+  const size_t U = static_cast<size_t>(p.batch) * p.heads;
+  const size_t N = static_cast<size_t>(p.n);
+  const size_t C = static_cast<size_t>(p.C);
+  const size_t D = static_cast<size_t>(p.d);
+  const size_t K = static_cast<size_t>(p.topk > 0 ? p.topk : 1);
+  const size_t nkb = static_cast<size_t>(bwd_key_blocks(p.n));
+  const bool improved = p.topk > 0;
+  BwdWorkspace w;
+  size_t off = 0;
+  auto take = [&](size_t bytes) -> void* {
+    void* ptr = base ? static_cast<void*>(static_cast<char*>(base) + off) : nullptr;
+    off += align_up(bytes);
+    return ptr;
+  };
+  w.G = static_cast<float*>(take(U * C * D * 4));
+  w.delta = static_cast<float*>(take(U * C * 4));
+  w.dm = static_cast<float*>(take(U * C * 4));
+  w.dqc_part = static_cast<float*>(take(U * nkb * C * D * 4));
+  w.dqc = static_cast<float*>(take(U * C * D * 4));
+  w.part_k = static_cast<float*>(take(improved ? U * C * K * D * 4 : 0));
+  w.part_v = static_cast<float*>(take(improved ? U * C * K * D * 4 : 0));
+  w.icnt = static_cast<int32_t*>(take(improved ? U * (N + 1) * 4 : 0));
+  w.ioff = static_cast<int32_t*>(take(improved ? U * (N + 1) * 4 : 0));
+  w.ilist = static_cast<int32_t*>(take(improved ? U * C * K * 4 : 0));
   if (ws) *ws = w;
   return off;
 }
@@ -208,6 +238,66 @@ static int run_forward(const void* q, const void* k, const void* v, const int32_
   return CA_OK;
 }
 
+static int run_backward(const void* q, const void* k, const void* v, const int32_t* lengths,
+                        int batch, int heads, int n, int d, int dtype, int C, int topk,
+                        const void* dout, float* dq, float* dk, float* dv, const void* workspace,
+                        size_t workspace_bytes, void* bwd_workspace, size_t bwd_workspace_bytes,
+                        void* stream) {
+  const bool improved = topk > 0;
+  int rc = check_sizes(batch, heads, n, d, dtype, C, 1, 1, topk, improved);
+  if (rc != CA_OK) return rc;
+  if (!q || !k || !v || !dout || !dq || !dk || !dv)
+    return fail(CA_ERR_INVALID_ARG, "q, k, v, dout, dq, dk and dv must not be NULL");
+  Problem p;
+  memset(&p, 0, sizeof(p));
+  p.batch = batch;
+  p.heads = heads;
+  p.n = n;
+  p.d = d;
+  p.dtype = dtype;
+  p.C = C;
+  p.n_bits = 1;
+  p.L = 1;
+  p.topk = improved ? topk : 0;
+  const size_t need = carve_workspace(p, nullptr, nullptr);
+  if (!workspace) return fail(CA_ERR_WORKSPACE, "workspace (the forward pass's) must not be NULL");
+  if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0)
+    return fail(CA_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if (workspace_bytes < need)
+    return fail(CA_ERR_WORKSPACE, "workspace too small: %zu bytes given, %zu needed", workspace_bytes, need);
+  Workspace fws;
+  carve_workspace(p, const_cast<void*>(workspace), &fws);
+  BwdProblem b;
+  b.batch = batch;
+  b.heads = heads;
+  b.n = n;
+  b.d = d;
+  b.dtype = dtype;
+  b.C = C;
+  b.topk = p.topk;
+  b.q = q;
+  b.k = k;
+  b.v = v;
+  b.dout = dout;
+  b.lengths = lengths;
+  b.fws = &fws;
+  b.dq = dq;
+  b.dk = dk;
+  b.dv = dv;
+  const size_t bneed = carve_bwd_workspace(b, nullptr, nullptr);
+  if (!bwd_workspace) return fail(CA_ERR_WORKSPACE, "bwd_workspace must not be NULL (%zu bytes needed)", bneed);
+  if (reinterpret_cast<uintptr_t>(bwd_workspace) % 256 != 0)
+    return fail(CA_ERR_WORKSPACE, "bwd_workspace must be 256-byte aligned");
+  if (bwd_workspace_bytes < bneed)
+    return fail(CA_ERR_WORKSPACE, "bwd_workspace too small: %zu bytes given, %zu needed",
+                bwd_workspace_bytes, bneed);
+  carve_bwd_workspace(b, bwd_workspace, &b.bws);
+  (void)hipGetLastError();
+  const hipError_t e = launch_backward(b, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(CA_ERR_HIP, "backward launch failed: %s", hipGetErrorString(e));
+  return CA_OK;
+}
+
 }  // namespace ca
 
 extern "C" {
@@ -253,6 +343,51 @@ int iclustered_attention_fwd(const void* q, const void* k, const void* v, const 
     if (topk < 1) return ca::fail(CA_ERR_INVALID_ARG, "topk must be >= 1 (got %d)", topk);
     return ca::run_forward(q, k, v, lengths, planes, batch, heads, n, d, dtype, n_clusters,
                            n_bits, lloyd_iters, topk, out, workspace, workspace_bytes, aux, stream);
+  } catch (...) {
+    return ca::fail(CA_ERR_HIP, "unexpected C++ exception");
+  }
+}
+
+size_t ca_backward_workspace_bytes(int batch, int heads, int n, int d, int dtype, int n_clusters,
+                                   int topk) {
+  const bool improved = topk > 0;
+  if (ca::check_sizes(batch, heads, n, d, dtype, n_clusters, 1, 1, topk, improved) != CA_OK) return 0;
+  ca::BwdProblem b;
+  memset(&b, 0, sizeof(b));
+  b.batch = batch;
+  b.heads = heads;
+  b.n = n;
+  b.d = d;
+  b.dtype = dtype;
+  b.C = n_clusters;
+  b.topk = improved ? topk : 0;
+  return ca::carve_bwd_workspace(b, nullptr, nullptr);
+}
+
+int clustered_attention_bwd(const void* q, const void* k, const void* v, const int32_t* lengths,
+                            int batch, int heads, int n, int d, int dtype, int n_clusters,
+                            const void* dout, float* dq, float* dk, float* dv,
+                            const void* workspace, size_t workspace_bytes, void* bwd_workspace,
+                            size_t bwd_workspace_bytes, void* stream) {
+  try {
+    return ca::run_backward(q, k, v, lengths, batch, heads, n, d, dtype, n_clusters, 0, dout, dq,
+                            dk, dv, workspace, workspace_bytes, bwd_workspace,
+                            bwd_workspace_bytes, stream);
+  } catch (...) {
+    return ca::fail(CA_ERR_HIP, "unexpected C++ exception");
+  }
+}
+
+int iclustered_attention_bwd(const void* q, const void* k, const void* v, const int32_t* lengths,
+                             int batch, int heads, int n, int d, int dtype, int n_clusters,
+                             int topk, const void* dout, float* dq, float* dk, float* dv,
+                             const void* workspace, size_t workspace_bytes, void* bwd_workspace,
+                             size_t bwd_workspace_bytes, void* stream) {
+  try {
+    if (topk < 1) return ca::fail(CA_ERR_INVALID_ARG, "topk must be >= 1 (got %d)", topk);
+    return ca::run_backward(q, k, v, lengths, batch, heads, n, d, dtype, n_clusters, topk, dout,
+                            dq, dk, dv, workspace, workspace_bytes, bwd_workspace,
+                            bwd_workspace_bytes, stream);
   } catch (...) {
     return ca::fail(CA_ERR_HIP, "unexpected C++ exception");
   }

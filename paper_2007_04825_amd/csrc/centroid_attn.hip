@@ -139,6 +139,7 @@ struct AttnArgs {
   int32_t* topk_out;
   float* mass;
   float* vcb;
+  float* stats;
   void* out;
 };
 
@@ -443,6 +444,10 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
       const float val = nonempty ? sum / z : 0.0f;
       vhat[cc * D + dim] = val;
       a.vcb[ujc * D + dim] = val;
+      if (dim == 0) {  // softmax statistics for the backward pass
+        a.stats[ujc * 2] = rowm[cc];
+        a.stats[ujc * 2 + 1] = z;
+      }
       if (IMPROVED && dim == 0) {
         const float mass = nonempty ? rowtop[cc] / z : 0.0f;
         rowmass[cc] = mass;
@@ -520,6 +525,10 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   float Z = 0.0f;
   for (int x = lane; x < nch; x += 64) Z += pzj[x] * __expf(pmj[x] - M);
   Z = wave_sum(Z);
+  if (lane == 0) {  // softmax statistics for the backward pass
+    a.stats[uj * 2] = M;
+    a.stats[uj * 2 + 1] = Z;
+  }
   // V^c = sum_chunks exp(m_c - M) acc_c / Z   (lane -> dimension)
   constexpr int RPS = 64 / D;
   const int t = lane % D, r = lane / D;
@@ -787,6 +796,7 @@ static AttnArgs make_args(const Problem& p, const Workspace& ws, const int32_t* 
   a.topk_out = ws.topk;
   a.mass = ws.mass;
   a.vcb = ws.vcb;
+  a.stats = ws.stats;
   a.out = p.out;
   return a;
 }

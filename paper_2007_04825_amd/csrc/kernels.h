@@ -48,6 +48,7 @@ struct Workspace {
   int32_t* topk;        // [U][C][k]
   float* mass;          // [U][C]
   float* vcb;           // [U][C][d]
+  float* stats;         // [U][C][2] row maximum and normaliser of the centroid softmax
   int nblk;             // ceil(N / kKmBlockQ)
   int ncsr;             // ceil(N / kCsrBlockQ)
   int nchunk;           // ceil(N / kChunk)
@@ -80,6 +81,36 @@ hipError_t launch_sparse(const Problem& p, const Workspace& ws, hipStream_t s);
 hipError_t launch_broadcast(const Problem& p, const int32_t* assign, const Workspace& ws,
                             hipStream_t s);
 hipError_t launch_pad_zero(const Problem& p, hipStream_t s);
+
+// Backward pass: scratch buffers carved from the caller's backward workspace.
+struct BwdWorkspace {
+  float* G;         // [U][C][d]   sum of the members' output gradients
+  float* delta;     // [U][C]
+  float* dm;        // [U][C]      gradient of the mass (improved)
+  float* dqc_part;  // [U][nkb][C][d] centroid-gradient partials per key block
+  float* dqc;       // [U][C][d]
+  float* part_k;    // [U][C][k][d] key-gradient partials of the top-k rows (improved)
+  float* part_v;    // [U][C][k][d]
+  int32_t* icnt;    // [U][n+1]    inverse index of the top-k sets: counts / cursors
+  int32_t* ioff;    // [U][n+1]    offsets
+  int32_t* ilist;   // [U][C*k]    entries j*k + r per key
+};
+struct BwdProblem {
+  int batch, heads, n, d, dtype, C, topk;  // topk = 0 for the clustered variant
+  const void* q;
+  const void* k;
+  const void* v;
+  const void* dout;
+  const int32_t* lengths;
+  const Workspace* fws;  // the forward pass's state
+  BwdWorkspace bws;
+  float* dq;
+  float* dk;
+  float* dv;
+};
+int bwd_key_blocks(int n);
+size_t carve_bwd_workspace(const BwdProblem& p, void* base, BwdWorkspace* ws);
+hipError_t launch_backward(const BwdProblem& p, hipStream_t s);
 
 // Which K-means path runs: 0 automatic, 1 one workgroup per unit, 2 multi-workgroup.
 void set_kmeans_path(int path);

@@ -170,3 +170,64 @@ def check_end_to_end(w, topk):
     print("max abs error: %.3g (tolerance %.0e)" % (err, tol(w)))
     assert err <= tol(w)
     assert np.all(got["out"][~vm] == 0), "padded rows must be 0"
+
+
+def run_gpu_backward(w, topk, dout, lengths=True, assign_in=None, C=None, repeat=1):
+    """Forward on the GPU (keeping its workspace), then the backward for the
+    output gradient dout [B, H, N, d].  Returns (grads, fwd) where grads is a
+    list (one per repeat) of (dq, dk, dv) float64 arrays and fwd holds the
+    forward's exported partition and top-k sets."""
+    import paper_2007_04825_amd as ca
+    torch = torch_mod()
+    C = w.C if C is None else C
+    B, H, N, D = w.q.shape
+    qd, kd, vd = to_dev(w.q, w.dtype), to_dev(w.k, w.dtype), to_dev(w.v, w.dtype)
+    gd = to_dev(np.ascontiguousarray(dout, dtype=np.float32), w.dtype)
+    planes = torch.from_numpy(np.ascontiguousarray(w.planes)).cuda()
+    lens = torch.from_numpy(w.lengths.astype(np.int32)).cuda() if lengths else None
+    U = B * H
+    kk = max(topk, 1)
+    dt = ca.CA_F32 if w.dtype == "f32" else ca.CA_BF16
+    ws = torch.empty(ca.workspace_bytes(B, H, N, D, dt, C, w.n_bits, topk), dtype=torch.uint8,
+                     device="cuda")
+    ex = dict(assign_out=torch.zeros((U, N), dtype=torch.int32, device="cuda"),
+              topk_out=torch.zeros((U, C, kk), dtype=torch.int32, device="cuda"),
+              sizes_out=torch.zeros((U, C), dtype=torch.int32, device="cuda"))
+    inj = {}
+    if assign_in is not None:
+        inj["assign_in"] = torch.from_numpy(np.ascontiguousarray(assign_in, dtype=np.int32)).cuda()
+    aux = ca.make_aux(**ex, **inj)
+    if topk > 0:
+        ca.iclustered_attention(qd, kd, vd, planes, C, w.n_bits, w.L, topk, lengths=lens,
+                                workspace=ws, aux=aux)
+    else:
+        ca.clustered_attention(qd, kd, vd, planes, C, w.n_bits, w.L, lengths=lens, workspace=ws,
+                               aux=aux)
+    grads = []
+    for _ in range(repeat):
+        if topk > 0:
+            g = ca.iclustered_attention_backward(qd, kd, vd, gd, C, topk, ws, lengths=lens)
+        else:
+            g = ca.clustered_attention_backward(qd, kd, vd, gd, C, ws, lengths=lens)
+        torch.cuda.synchronize()
+        grads.append(tuple(x.cpu().numpy().astype(np.float64) for x in g))
+    fwd = {"assign": ex["assign_out"].cpu().numpy().reshape(B, H, N),
+           "topk": ex["topk_out"].cpu().numpy().reshape(B, H, C, kk),
+           "sizes": ex["sizes_out"].cpu().numpy().reshape(B, H, C)}
+    return grads, fwd
+
+
+def oracle_backward_for(w, topk, dout, fwd, C=None, lengths=True):
+    """The oracle's gradients for the GPU forward's partition and top-k sets
+    (so that a near-tie difference in T cannot mask a gradient error)."""
+    C = w.C if C is None else C
+    q = np.nan_to_num(w.q, nan=0.0)
+    g = np.nan_to_num(np.asarray(dout, np.float64), nan=0.0)
+    if w.dtype == "bf16":
+        import gen
+        g = gen.round_bf16(g.astype(np.float32)).astype(np.float64)
+    else:
+        g = g.astype(np.float32).astype(np.float64)
+    lens = w.lengths if lengths else None
+    return oracle.backward(q, w.k, w.v, lens, C, topk, fwd["assign"],
+                           fwd["topk"] if topk else None, g)
