@@ -171,6 +171,133 @@ def cpu_baseline(w, min_seconds=10.0, max_passes=1000):
             "sample": "%d passes of the full workload, both variants (%.1f s)" % (passes, el)}
 
 
+def cpu_baseline_backward(w, fwd_exports, dout, min_seconds=10.0, max_passes=1000):
+    """Times the fp64 oracle's backward pass (both variants) on the same
+    workload, partitions and top-k sets, for at least min_seconds."""
+    import oracle
+    threads = cpu_threads()
+    q = np.nan_to_num(w.q, nan=0.0)
+    passes, t0 = 0, time.perf_counter()
+    while True:
+        for topk, fx in fwd_exports:
+            oracle.backward(q, w.k, w.v, w.lengths, w.C, topk, fx["assign"], fx["topk"] if topk else None,
+                            dout, num_threads=threads)
+        passes += 1
+        el = time.perf_counter() - t0
+        if el >= min_seconds or passes >= max_passes:
+            break
+    queries = 2 * w.queries() * passes
+    return {"value": queries / el, "unit": "queries/s", "cores": threads, "kind": "oracle",
+            "sample": "%d passes of the full workload's backward, both variants (%.1f s)" % (passes, el)}
+
+
+def bench_backward(args):
+    """Times one backward step: the clustered and the improved backward pass
+    over the speech workload, each for the forward call whose workspace it
+    reads (both forwards run once before the timed region)."""
+    import torch
+
+    import gen
+    import paper_2007_04825_amd as ca
+
+    w = gen.make_config(2)
+    B, H, N, D = w.q.shape
+    dev = torch.device("cuda:0")
+    q, k, v = (torch.from_numpy(x).to(dev) for x in (w.q, w.k, w.v))
+    planes = torch.from_numpy(w.planes).to(dev)
+    lengths = torch.from_numpy(w.lengths).to(dev)
+    dout_np = gen.output_gradient(w)
+    dout = torch.from_numpy(dout_np).to(dev)
+    U = B * H
+    ws, bws, grads, exports = {}, {}, {}, []
+    for topk in (0, w.topk):
+        ws[topk] = torch.empty(ca.workspace_bytes(B, H, N, D, 0, w.C, w.n_bits, topk), dtype=torch.uint8,
+                               device=dev)
+        bws[topk] = torch.empty(ca.backward_workspace_bytes(B, H, N, D, 0, w.C, topk), dtype=torch.uint8,
+                                device=dev)
+        grads[topk] = tuple(torch.empty_like(q) for _ in range(3))
+        ex = {"assign_out": torch.zeros((U, N), dtype=torch.int32, device=dev),
+              "topk_out": torch.zeros((U, w.C, max(topk, 1)), dtype=torch.int32, device=dev)}
+        aux = ca.make_aux(**ex)
+        if topk:
+            ca.iclustered_attention(q, k, v, planes, w.C, w.n_bits, w.L, topk, lengths=lengths,
+                                    workspace=ws[topk], aux=aux)
+        else:
+            ca.clustered_attention(q, k, v, planes, w.C, w.n_bits, w.L, lengths=lengths,
+                                   workspace=ws[topk], aux=aux)
+        torch.cuda.synchronize()
+        exports.append((topk, {"assign": ex["assign_out"].cpu().numpy().reshape(B, H, N),
+                               "topk": ex["topk_out"].cpu().numpy().reshape(B, H, w.C, max(topk, 1))}))
+
+    def bwd(topk):
+        if topk:
+            ca.iclustered_attention_backward(q, k, v, dout, w.C, topk, ws[topk], lengths=lengths,
+                                             bwd_workspace=bws[topk], grads=grads[topk])
+        else:
+            ca.clustered_attention_backward(q, k, v, dout, w.C, ws[topk], lengths=lengths,
+                                            bwd_workspace=bws[topk], grads=grads[topk])
+
+    hip = Hip()
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    lib = ca.library()
+    for _ in range(args.warmup):
+        bwd(0)
+        bwd(w.topk)
+    torch.cuda.synchronize()
+    # which variant's centroid kernel is larger
+    tk = {}
+    for topk in (0, w.topk):
+        e0, e1 = hip.event(), hip.event()
+        assert lib.ca_time_next_stage(ca.CA_KERNEL_BWD_CENTROID, e0, e1) == 0
+        bwd(topk)
+        tk[topk] = hip.elapsed_ms(e0, e1)
+    var = max(tk, key=tk.get)
+    EV_EVERY = 8
+    evs = [(hip.event(light=True), hip.event(light=True)) if i % EV_EVERY == 0 else None
+           for i in range(args.steps)]
+    t_start, t_stop = hip.event(), hip.event()
+    torch.cuda.synchronize()
+    hip.record(t_start, stream)
+    for i in range(args.steps):
+        for topk in (0, w.topk):
+            if topk == var and evs[i] is not None:
+                assert lib.ca_time_next_stage(ca.CA_KERNEL_BWD_CENTROID, evs[i][0], evs[i][1]) == 0
+            bwd(topk)
+    hip.record(t_stop, stream)
+    torch.cuda.synchronize()
+    ms_per_step = hip.elapsed_ms(t_start, t_stop) / args.steps
+    timed = [e for e in evs if e is not None]
+    stage_ms = sum(hip.elapsed_ms(a, b) for a, b in timed) / len(timed)
+    nsum = int(w.lengths.astype(np.int64).sum()) * H
+    flops = 10.0 * w.C * nsum * D  # five C x n x d products per unit (S, gA, dQ^c, dK, dV)
+    achieved = flops / (stage_ms * 1e-3) / 1e12
+    peak = PEAKS["fp32_mfma_TFLOPs"]
+    cpu = None if args.no_cpu_baseline else cpu_baseline_backward(w, exports, dout_np)
+    rec = {
+        "metric": "gradient queries/sec/GPU of clustered & i-clustered attn bwd",
+        "value": round(2 * w.queries() / (ms_per_step * 1e-3), 1),
+        "unit": "queries/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "speech-encoder layer: batch 32, heads 6, N 800 (lengths 400-800), "
+                               "d 32, fp32, C 100, k 32; backward of clustered + i-clustered",
+                   "global_batch": B, "seq_len": N, "parallelism": "none"},
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak, "unit": "TFLOP/s",
+                     "frac": round(achieved / peak, 5), "traffic": None,
+                     "kernel": "bwd_centroid (%s)" % ("iclustered" if var else "clustered"),
+                     "avg_launch_us": round(stage_ms * 1e3, 3)},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(rec))
+
+
 def copy_calibration(nbytes):
     """A plain device-to-device copy of known size, for scaling HBM counters."""
     import torch
@@ -191,6 +318,8 @@ def main():
                     choices=["auto", "hash", "kmeans", "centroids", "centroid_attn", "output"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES")
+    ap.add_argument("--backward", action="store_true",
+                    help="time the backward pass instead (its own JSON line)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the forward pass of each (sequence, head) is "
@@ -199,6 +328,9 @@ def main():
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
+        return
+    if args.backward:
+        bench_backward(args)
         return
 
     import torch

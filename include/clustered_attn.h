@@ -226,16 +226,20 @@ int ca_version(void);
  *   CA_KERNEL_CENTROIDS      query centroids (Eq. 3)
  *   CA_KERNEL_CENTROID_ATTN  centroid attention, top-k and mass (Eqs. 4-5, Section 3.3)
  *   CA_KERNEL_OUTPUT         broadcast (Eq. 6) or the improved per-query part
+ *   CA_KERNEL_BWD_CENTROID   (backward calls) the centroid part of the
+ *                            gradient: dK, dV and the dQ^c partials
  */
 #define CA_KERNEL_HASH 1
 #define CA_KERNEL_KMEANS 2
 #define CA_KERNEL_CENTROIDS 3
 #define CA_KERNEL_CENTROID_ATTN 4
 #define CA_KERNEL_OUTPUT 5
+#define CA_KERNEL_BWD_CENTROID 6
 
 /*
  * Profiling hook for callers that time one stage with HIP events: in the
- * next forward call made by this thread, hipEventRecord(start_event) is
+ * next forward call (backward call for CA_KERNEL_BWD_CENTROID) made by this
+ * thread, hipEventRecord(start_event) is
  * enqueued on the call's stream just before the stage's kernels and
  * hipEventRecord(stop_event) just after them; the hook is then disarmed.
  * start_event and stop_event are hipEvent_t owned by the caller.  stage 0

@@ -32,10 +32,11 @@
 //   bwd_dqc_reduce_kernel, bwd_dq_kernel: dQ^c over the key blocks in order,
 //     then dQ_i.
 //   improved only: the partial key/value gradients of the T rows reach dK and
-//     dV through an inverse index (key -> entries (j, r) with T_j[r] = key):
-//     counts, a prefix sum, a fill and a per-key sort of the entry numbers,
-//     so that every key adds its entries in ascending (j, r) order.  No
-//     floating-point atomics: the result is deterministic.
+//     dV through an inverse index (key -> entries (j, r) with T_j[r] = key)
+//     built by bwd_index_kernel; bwd_index_gather_kernel adds each key's
+//     entries as 64-bit fixed-point integers, whose sum does not depend on
+//     the order.  No floating-point atomics: the result is deterministic.
+#include <limits.h>
 #include <math.h>
 
 #include "common.h"
@@ -46,6 +47,7 @@ namespace ca {
 
 constexpr int kBwdKeys = 128;  // keys per workgroup of bwd_tile_kernel
 constexpr int kBwdWaves = 8;   // waves per workgroup of bwd_tile_kernel (one key tile each)
+constexpr int kIdxKeys = 8192;  // keys per workgroup of bwd_index_kernel
 
 struct BwdArgs {
   const void* q;
@@ -73,9 +75,10 @@ struct BwdArgs {
   float* dqc;       // [U][C][D]
   float* part_k;    // [U][C][topk][D]
   float* part_v;    // [U][C][topk][D]
-  int32_t* icnt;    // [U][N + 1]
-  int32_t* ioff;    // [U][N + 1]
-  int32_t* ilist;   // [U][C * topk]
+  int32_t* icnt;    // [U][N]  entries per key
+  int32_t* ioff;    // [U][N]  first entry of each key within its key range's list
+  int32_t* ilist;   // [U][nrange][C * topk] entry numbers j * topk + r
+  int nrange;       // key ranges of kIdxKeys keys per unit
   float* dq;
   float* dk;
   float* dv;
@@ -133,7 +136,6 @@ __global__ __launch_bounds__(256) void bwd_cluster_sums_kernel(BwdArgs a) {
 //   dK_T += gt^T Q / sqrt d,  dV_T += m_j w^T g  (LDS accumulators; the
 //   products over the queries take w and gt transposed through LDS)
 // and G_j = sum g_i, dm_j = sum_i rho_i, delta_j = m_j dm_j + G_j . V^b_j.
-// Each T entry is also counted for the inverse index.
 // ---------------------------------------------------------------------------
 template <int D, int NKT>
 struct SparseBwdShared {
@@ -189,9 +191,6 @@ __global__ __launch_bounds__(64) void bwd_sparse_kernel(BwdArgs a) {
   const __amdgpu_buffer_rsrc_t rv = make_rsrc(static_cast<const T*>(a.v) + base, ubytes);
   const __amdgpu_buffer_rsrc_t rg = make_rsrc(static_cast<const T*>(a.dout) + base, ubytes);
   wave_lds_sync();
-  // inverse-index counts of the T entries
-  int32_t* icu = a.icnt + static_cast<size_t>(u) * (a.N + 1);
-  for (int x = lane; x < kk; x += 64) atomicAdd(&icu[sh.tp[x]], 1);
   // T rows of K and V into LDS (rows past kk are zero); 4 lanes per row
   constexpr int RL = D / 4;  // values per lane
   for (int r0 = 0; r0 < KP; r0 += 16) {
@@ -603,110 +602,142 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(BwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Inverse index of the top-k sets (improved).
+// Inverse index of the top-k sets (improved): one workgroup per (unit, range
+// of kIdxKeys keys).  Counts per key (LDS atomics, order-free), an exclusive
+// prefix sum, then every entry takes a slot of its key.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void bwd_zero_counts_kernel(int32_t* icnt, size_t count) {
-  const size_t x = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x;
-  if (x < count) icnt[x] = 0;
-}
-
-// Exclusive prefix sum of the counts of one unit (one workgroup per unit);
-// the counts are reset to 0 to serve as fill cursors.
-__global__ __launch_bounds__(1024) void bwd_index_scan_kernel(BwdArgs a) {
+__global__ __launch_bounds__(1024) void bwd_index_kernel(BwdArgs a) {
+  __shared__ int cnt[kIdxKeys];
+  __shared__ int off[kIdxKeys];
   __shared__ int wsum[16];
-  __shared__ int carry;
-  const int u = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const size_t rowb = static_cast<size_t>(u) * (a.N + 1);
-  if (tid == 0) carry = 0;
+  const int u = blockIdx.x / a.nrange, range = blockIdx.x % a.nrange;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n = unit_length(a.lengths, u / a.heads, a.N);
+  const int lo = range * kIdxKeys, hi = min(n, lo + kIdxKeys);
+  if (lo >= hi) return;
+  const int C = a.C, K = a.topk;
+  const int32_t* ts = a.tsets + static_cast<size_t>(u) * C * K;
+  const int32_t* sz = a.sizes + static_cast<size_t>(u) * C;
+  for (int x = tid; x < kIdxKeys; x += 1024) cnt[x] = 0;
   __syncthreads();
-  for (int x0 = 0; x0 < a.N + 1; x0 += 1024) {
-    const int x = x0 + tid;
-    const int v = x < a.N + 1 ? a.icnt[rowb + x] : 0;
-    const int incl = wave_incl_scan(v);
-    if (lane == 63) wsum[wave] = incl;
-    __syncthreads();
-    int before = carry;
-    for (int w = 0; w < wave; ++w) before += wsum[w];
-    if (x < a.N + 1) {
-      a.ioff[rowb + x] = before + incl - v;
-      a.icnt[rowb + x] = 0;
+  for (int x = tid; x < C * K; x += 1024) {
+    if (sz[x / K] == 0) continue;  // no list for an empty cluster
+    const int key = ts[x];
+    if (key >= lo && key < hi) atomicAdd(&cnt[key - lo], 1);
+  }
+  __syncthreads();
+  // exclusive prefix sum of cnt[0 .. hi - lo), 8 keys per thread
+  const int m = hi - lo;
+  int local[kIdxKeys / 1024], tot = 0;
+#pragma unroll
+  for (int e = 0; e < kIdxKeys / 1024; ++e) {
+    const int x = tid * (kIdxKeys / 1024) + e;
+    local[e] = x < m ? cnt[x] : 0;
+    tot += local[e];
+  }
+  const int incl = wave_incl_scan(tot);
+  if (lane == 63) wsum[wave] = incl;
+  __syncthreads();
+  int run = incl - tot;
+  for (int w = 0; w < wave; ++w) run += wsum[w];
+  int32_t* icu = a.icnt + static_cast<size_t>(u) * a.N;
+  int32_t* iou = a.ioff + static_cast<size_t>(u) * a.N;
+#pragma unroll
+  for (int e = 0; e < kIdxKeys / 1024; ++e) {
+    const int x = tid * (kIdxKeys / 1024) + e;
+    if (x < m) {
+      off[x] = run;
+      icu[lo + x] = local[e];
+      iou[lo + x] = run;
+      cnt[x] = 0;  // now the fill cursor
     }
-    __syncthreads();
-    if (tid == 1023) carry = before + incl;
-    __syncthreads();
+    run += local[e];
+  }
+  __syncthreads();
+  // each entry takes a slot of its key, in no particular order (the gather's
+  // sum does not depend on it)
+  int32_t* L = a.ilist + (static_cast<size_t>(u) * a.nrange + range) * C * K;
+  for (int x = tid; x < C * K; x += 1024) {
+    if (sz[x / K] == 0) continue;
+    const int key = ts[x];
+    if (key >= lo && key < hi) L[off[key - lo] + atomicAdd(&cnt[key - lo], 1)] = x;
   }
 }
 
-// Places each T entry (j, r) of a unit under its key.
-__global__ __launch_bounds__(256) void bwd_index_fill_kernel(BwdArgs a) {
-  const size_t x = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x;
-  const size_t per = static_cast<size_t>(a.C) * a.topk;
-  if (x >= per * a.units) return;
-  const int u = static_cast<int>(x / per);
-  const int e = static_cast<int>(x % per);
-  if (a.sizes[static_cast<size_t>(u) * a.C + e / a.topk] == 0) return;  // no list for an empty cluster
-  const int key = a.tsets[x];
-  if (key < 0) return;
-  const size_t rowb = static_cast<size_t>(u) * (a.N + 1);
-  const int pos = a.ioff[rowb + key] + atomicAdd(&a.icnt[rowb + key], 1);
-  a.ilist[per * u + pos] = e;
+// dK_l and dV_l receive the top-k parts of the entries of key l: one thread
+// per (key, four dimensions) adds the partial rows as 64-bit fixed-point
+// integers (2^-32 units; integer addition is exact and associative, so the
+// order of the entries does not matter and the result is deterministic),
+// then rounds the sum once into fp32.  A term is converted exactly when
+// |x| >= 2^-8 (x * 2^32 is then an integer in fp32) and to the nearest unit
+// otherwise; terms are clamped to |x| <= 2^22 so that no sum of at most 256
+// of them leaves the int64 range.
+__device__ __forceinline__ long long to_fixed32(float x) {
+  x = fminf(fmaxf(x, -4194304.0f), 4194304.0f);
+  return __float2ll_rn(x * 4294967296.0f);
 }
-
-// Sorts each key's entries ascending (insertion sort; lists are short), so
-// that the gather adds them in a fixed order.
-__global__ __launch_bounds__(256) void bwd_index_sort_kernel(BwdArgs a) {
-  const size_t x = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x;
-  if (x >= static_cast<size_t>(a.units) * a.N) return;
-  const int u = static_cast<int>(x / a.N), key = static_cast<int>(x % a.N);
-  const size_t rowb = static_cast<size_t>(u) * (a.N + 1);
-  const int b = a.ioff[rowb + key], e = a.ioff[rowb + key + 1];
-  if (e - b < 2) return;
-  int32_t* L = a.ilist + static_cast<size_t>(a.C) * a.topk * u;
-  for (int p = b + 1; p < e; ++p) {
-    const int val = L[p];
-    int q = p - 1;
-    while (q >= b && L[q] > val) {
-      L[q + 1] = L[q];
-      --q;
-    }
-    L[q + 1] = val;
-  }
-}
-
-// dK_l and dV_l receive the partials of the T entries of key l, in order.
 template <int D>
 __global__ __launch_bounds__(256) void bwd_index_gather_kernel(BwdArgs a) {
+  constexpr int Q4 = D / 4;
   const size_t x = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x;
-  if (x >= static_cast<size_t>(a.units) * a.N * D) return;
-  const int dim = static_cast<int>(x % D);
-  const size_t ul = x / D;
+  if (x >= static_cast<size_t>(a.units) * a.N * Q4) return;
+  const int part = static_cast<int>(x % Q4);
+  const size_t ul = x / Q4;
   const int u = static_cast<int>(ul / a.N), key = static_cast<int>(ul % a.N);
-  const size_t rowb = static_cast<size_t>(u) * (a.N + 1);
-  const int b = a.ioff[rowb + key], e = a.ioff[rowb + key + 1];
-  if (b == e) return;
+  const int n = unit_length(a.lengths, u / a.heads, a.N);
+  if (key >= n) return;
+  const int cnt = a.icnt[ul];
+  if (cnt == 0) return;
   const size_t per = static_cast<size_t>(a.C) * a.topk;
-  const int32_t* L = a.ilist + per * u;
-  const float* pk = a.part_k + per * u * D;
-  const float* pv = a.part_v + per * u * D;
-  float sk = a.dk[x], sv = a.dv[x];
-  for (int p = b; p < e; ++p) {
-    const size_t ent = static_cast<size_t>(L[p]);
-    sk += pk[ent * D + dim];
-    sv += pv[ent * D + dim];
+  const int32_t* L = a.ilist + (static_cast<size_t>(u) * a.nrange + key / kIdxKeys) * per + a.ioff[ul];
+  const float4* pk = reinterpret_cast<const float4*>(a.part_k + static_cast<size_t>(u) * per * D);
+  const float4* pv = reinterpret_cast<const float4*>(a.part_v + static_cast<size_t>(u) * per * D);
+  long long ak[4] = {0, 0, 0, 0}, av[4] = {0, 0, 0, 0};
+  constexpr int B = 8;  // entries in flight
+  for (int t0 = 0; t0 < cnt; t0 += B) {
+    int e[B];
+#pragma unroll
+    for (int t = 0; t < B; ++t) e[t] = t0 + t < cnt ? L[t0 + t] : -1;
+    float4 k4[B], v4[B];
+#pragma unroll
+    for (int t = 0; t < B; ++t) {
+      k4[t] = e[t] >= 0 ? pk[static_cast<size_t>(e[t]) * Q4 + part] : make_float4(0.f, 0.f, 0.f, 0.f);
+      v4[t] = e[t] >= 0 ? pv[static_cast<size_t>(e[t]) * Q4 + part] : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int t = 0; t < B; ++t) {
+      ak[0] += to_fixed32(k4[t].x); ak[1] += to_fixed32(k4[t].y);
+      ak[2] += to_fixed32(k4[t].z); ak[3] += to_fixed32(k4[t].w);
+      av[0] += to_fixed32(v4[t].x); av[1] += to_fixed32(v4[t].y);
+      av[2] += to_fixed32(v4[t].z); av[3] += to_fixed32(v4[t].w);
+    }
   }
-  a.dk[x] = sk;
-  a.dv[x] = sv;
+  constexpr double kUnit = 1.0 / 4294967296.0;
+  float4* dk4 = reinterpret_cast<float4*>(a.dk) + ul * Q4 + part;
+  float4* dv4 = reinterpret_cast<float4*>(a.dv) + ul * Q4 + part;
+  float4 sk = *dk4, sv = *dv4;
+  sk.x = static_cast<float>(static_cast<double>(sk.x) + static_cast<double>(ak[0]) * kUnit);
+  sk.y = static_cast<float>(static_cast<double>(sk.y) + static_cast<double>(ak[1]) * kUnit);
+  sk.z = static_cast<float>(static_cast<double>(sk.z) + static_cast<double>(ak[2]) * kUnit);
+  sk.w = static_cast<float>(static_cast<double>(sk.w) + static_cast<double>(ak[3]) * kUnit);
+  sv.x = static_cast<float>(static_cast<double>(sv.x) + static_cast<double>(av[0]) * kUnit);
+  sv.y = static_cast<float>(static_cast<double>(sv.y) + static_cast<double>(av[1]) * kUnit);
+  sv.z = static_cast<float>(static_cast<double>(sv.z) + static_cast<double>(av[2]) * kUnit);
+  sv.w = static_cast<float>(static_cast<double>(sv.w) + static_cast<double>(av[3]) * kUnit);
+  *dk4 = sk;
+  *dv4 = sv;
 }
 
 // ---------------------------------------------------------------------------
 // Host side.
 // ---------------------------------------------------------------------------
 int bwd_key_blocks(int n) { return (n + kBwdKeys - 1) / kBwdKeys; }
+int bwd_key_ranges(int n) { return (n + kIdxKeys - 1) / kIdxKeys; }
 
 static int sparse_bwd_tiles(int topk) { return topk <= 16 ? 1 : topk <= 32 ? 2 : topk <= 64 ? 4 : 8; }
 
 template <int D, typename T>
-static hipError_t launch_backward_t(const BwdProblem& p, hipStream_t s) {
+static hipError_t launch_backward_t(const BwdProblem& p, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   BwdArgs a;
   a.q = p.q;
   a.k = p.k;
@@ -739,6 +770,7 @@ static hipError_t launch_backward_t(const BwdProblem& p, hipStream_t s) {
   a.icnt = p.bws.icnt;
   a.ioff = p.bws.ioff;
   a.ilist = p.bws.ilist;
+  a.nrange = bwd_key_ranges(p.n);
   a.dq = p.dq;
   a.dk = p.dk;
   a.dv = p.dv;
@@ -747,8 +779,7 @@ static hipError_t launch_backward_t(const BwdProblem& p, hipStream_t s) {
   auto blocks = [](long long count) { return dim3(static_cast<unsigned>((count + 255) / 256)); };
   hipError_t e;
   if (improved) {
-    const long long ncnt = U * (p.n + 1);
-    hipLaunchKernelGGL(bwd_zero_counts_kernel, blocks(ncnt), dim3(256), 0, s, a.icnt, static_cast<size_t>(ncnt));
+    hipLaunchKernelGGL(bwd_index_kernel, dim3(static_cast<unsigned>(U * a.nrange)), dim3(1024), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const dim3 gs(xcd_grid(static_cast<long long>(p.C) * U));
     switch (sparse_bwd_tiles(p.topk)) {
@@ -764,11 +795,13 @@ static hipError_t launch_backward_t(const BwdProblem& p, hipStream_t s) {
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const dim3 gt(xcd_grid(static_cast<long long>(a.nkb) * U));
+  if (ev0 && (e = hipEventRecord(ev0, s)) != hipSuccess) return e;
   if (improved)
     hipLaunchKernelGGL((bwd_tile_kernel<D, T, true>), gt, dim3(64 * kBwdWaves), 0, s, a);
   else
     hipLaunchKernelGGL((bwd_tile_kernel<D, T, false>), gt, dim3(64 * kBwdWaves), 0, s, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (ev1 && (e = hipEventRecord(ev1, s)) != hipSuccess) return e;
   hipLaunchKernelGGL((bwd_dqc_reduce_kernel<D>), blocks(U * p.C * D), dim3(256), 0, s, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (improved)
@@ -777,21 +810,16 @@ static hipError_t launch_backward_t(const BwdProblem& p, hipStream_t s) {
     hipLaunchKernelGGL((bwd_dq_kernel<D, false>), blocks(U * p.n * D), dim3(256), 0, s, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (improved) {
-    hipLaunchKernelGGL(bwd_index_scan_kernel, dim3(static_cast<unsigned>(U)), dim3(1024), 0, s, a);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(bwd_index_fill_kernel, blocks(U * p.C * p.topk), dim3(256), 0, s, a);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(bwd_index_sort_kernel, blocks(U * p.n), dim3(256), 0, s, a);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL((bwd_index_gather_kernel<D>), blocks(U * p.n * D), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((bwd_index_gather_kernel<D>), blocks(U * p.n * (D / 4)), dim3(256), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   return hipSuccess;
 }
 
-hipError_t launch_backward(const BwdProblem& p, hipStream_t s) {
-  if (p.d == 32) return p.dtype == 0 ? launch_backward_t<32, float>(p, s) : launch_backward_t<32, bf16_t>(p, s);
-  return p.dtype == 0 ? launch_backward_t<64, float>(p, s) : launch_backward_t<64, bf16_t>(p, s);
+hipError_t launch_backward(const BwdProblem& p, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+  if (p.d == 32)
+    return p.dtype == 0 ? launch_backward_t<32, float>(p, s, ev0, ev1) : launch_backward_t<32, bf16_t>(p, s, ev0, ev1);
+  return p.dtype == 0 ? launch_backward_t<64, float>(p, s, ev0, ev1) : launch_backward_t<64, bf16_t>(p, s, ev0, ev1);
 }
 
 }  // namespace ca

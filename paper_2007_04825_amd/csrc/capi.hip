@@ -97,9 +97,10 @@ size_t carve_bwd_workspace(const BwdProblem& p, void* base, BwdWorkspace* ws) {
   w.dqc = static_cast<float*>(take(U * C * D * 4));
   w.part_k = static_cast<float*>(take(improved ? U * C * K * D * 4 : 0));
   w.part_v = static_cast<float*>(take(improved ? U * C * K * D * 4 : 0));
-  w.icnt = static_cast<int32_t*>(take(improved ? U * (N + 1) * 4 : 0));
-  w.ioff = static_cast<int32_t*>(take(improved ? U * (N + 1) * 4 : 0));
-  w.ilist = static_cast<int32_t*>(take(improved ? U * C * K * 4 : 0));
+  const size_t nrange = static_cast<size_t>(bwd_key_ranges(p.n));
+  w.icnt = static_cast<int32_t*>(take(improved ? U * N * 4 : 0));
+  w.ioff = static_cast<int32_t*>(take(improved ? U * N * 4 : 0));
+  w.ilist = static_cast<int32_t*>(take(improved ? U * nrange * C * K * 4 : 0));
   if (ws) *ws = w;
   return off;
 }
@@ -293,7 +294,10 @@ static int run_backward(const void* q, const void* k, const void* v, const int32
                 bwd_workspace_bytes, bneed);
   carve_bwd_workspace(b, bwd_workspace, &b.bws);
   (void)hipGetLastError();
-  const hipError_t e = launch_backward(b, static_cast<hipStream_t>(stream));
+  const bool timed = g_ev_kernel == CA_KERNEL_BWD_CENTROID;
+  const hipError_t e = launch_backward(b, static_cast<hipStream_t>(stream), timed ? g_ev_start : nullptr,
+                                       timed ? g_ev_stop : nullptr);
+  if (timed) g_ev_kernel = 0;
   if (e != hipSuccess) return fail(CA_ERR_HIP, "backward launch failed: %s", hipGetErrorString(e));
   return CA_OK;
 }
@@ -398,7 +402,7 @@ const char* ca_last_error(void) { return ca::g_last_error.c_str(); }
 int ca_version(void) { return 100; }
 
 int ca_time_next_stage(int stage, void* start_event, void* stop_event) {
-  if (stage < 0 || stage > CA_KERNEL_OUTPUT || (stage != 0 && (!start_event || !stop_event)))
+  if (stage < 0 || stage > CA_KERNEL_BWD_CENTROID || (stage != 0 && (!start_event || !stop_event)))
     return ca::fail(CA_ERR_INVALID_ARG, "invalid stage %d or null event", stage);
   ca::g_ev_kernel = stage;
   ca::g_ev_start = static_cast<hipEvent_t>(start_event);

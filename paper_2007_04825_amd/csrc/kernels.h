@@ -91,9 +91,9 @@ struct BwdWorkspace {
   float* dqc;       // [U][C][d]
   float* part_k;    // [U][C][k][d] key-gradient partials of the top-k rows (improved)
   float* part_v;    // [U][C][k][d]
-  int32_t* icnt;    // [U][n+1]    inverse index of the top-k sets: counts / cursors
-  int32_t* ioff;    // [U][n+1]    offsets
-  int32_t* ilist;   // [U][C*k]    entries j*k + r per key
+  int32_t* icnt;    // [U][n]      inverse index of the top-k sets: entries per key
+  int32_t* ioff;    // [U][n]      first entry of each key in its key range's list
+  int32_t* ilist;   // [U][nrange][C*k] entries j*k + r
 };
 struct BwdProblem {
   int batch, heads, n, d, dtype, C, topk;  // topk = 0 for the clustered variant
@@ -109,8 +109,10 @@ struct BwdProblem {
   float* dv;
 };
 int bwd_key_blocks(int n);
+int bwd_key_ranges(int n);
 size_t carve_bwd_workspace(const BwdProblem& p, void* base, BwdWorkspace* ws);
-hipError_t launch_backward(const BwdProblem& p, hipStream_t s);
+// ev_start / ev_stop (may be null) are recorded around bwd_tile_kernel.
+hipError_t launch_backward(const BwdProblem& p, hipStream_t s, hipEvent_t ev_start, hipEvent_t ev_stop);
 
 // Which K-means path runs: 0 automatic, 1 one workgroup per unit, 2 multi-workgroup.
 void set_kmeans_path(int path);
