@@ -272,6 +272,7 @@ def bench_backward(args):
     flops = 10.0 * w.C * nsum * D  # five C x n x d products per unit (S, gA, dQ^c, dK, dV)
     achieved = flops / (stage_ms * 1e-3) / 1e12
     peak = PEAKS["fp32_mfma_TFLOPs"]
+    kernel_key = "bwd_centroid (%s)" % ("iclustered" if var else "clustered")
     cpu = None if args.no_cpu_baseline else cpu_baseline_backward(w, exports, dout_np)
     rec = {
         "metric": "gradient queries/sec/GPU of clustered & i-clustered attn bwd",
@@ -290,9 +291,8 @@ def bench_backward(args):
                                "d 32, fp32, C 100, k 32; backward of clustered + i-clustered",
                    "global_batch": B, "seq_len": N, "parallelism": "none"},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak, "unit": "TFLOP/s",
-                     "frac": round(achieved / peak, 5), "traffic": None,
-                     "kernel": "bwd_centroid (%s)" % ("iclustered" if var else "clustered"),
-                     "avg_launch_us": round(stage_ms * 1e3, 3)},
+                     "frac": round(achieved / peak, 5), "traffic": measured_traffic(kernel_key),
+                     "kernel": kernel_key, "avg_launch_us": round(stage_ms * 1e3, 3)},
         "cpu_baseline": cpu,
     }
     print(json.dumps(rec))
