@@ -298,6 +298,89 @@ def bench_backward(args):
     print(json.dumps(rec))
 
 
+def bench_sweep(args):
+    """Length sweep in the protocol of the paper's time benchmark: one
+    attention layer of 8 heads x 64 over N = 2^10 .. 2^15 (batch 1, fp32,
+    iid N(0, 1) inputs, C 100, B 63, L 10, k 32), each variant's forward and
+    forward + backward timed with HIP events (median of repetitions after
+    warm-up), next to exact softmax attention (torch's scaled_dot_product_attention,
+    fp32, its backward through autograd).  Prints one JSON line per N with
+    times per (query, head)."""
+    import torch
+
+    import gen
+    import paper_2007_04825_amd as ca
+
+    dev = torch.device("cuda:0")
+    hip = Hip()
+    stream = torch.cuda.current_stream(dev).cuda_stream
+
+    def timed(fn, reps):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = hip.event(), hip.event()
+            hip.record(e0, stream)
+            fn()
+            hip.record(e1, stream)
+            ts.append(hip.elapsed_ms(e0, e1))
+            hip.destroy(e0)
+            hip.destroy(e1)
+        return float(np.median(ts))
+
+    for logn in range(10, 16):
+        N = 1 << logn
+        w = gen.config_sweep(N, dtype="f32")
+        B, H, _, D = w.q.shape
+        q, k, v = (torch.from_numpy(x).to(dev) for x in (w.q, w.k, w.v))
+        planes = torch.from_numpy(w.planes).to(dev)
+        dout = torch.from_numpy(gen.output_gradient(w)).to(dev)
+        reps = 20 if N <= 8192 else 8
+        rec = {"N": N, "heads": H, "d": D, "dtype": "f32", "unit": "us per (query, head)"}
+        for name, topk in (("clustered", 0), ("iclustered", w.topk)):
+            ws = torch.empty(ca.workspace_bytes(B, H, N, D, 0, w.C, w.n_bits, topk), dtype=torch.uint8, device=dev)
+            bws = torch.empty(ca.backward_workspace_bytes(B, H, N, D, 0, w.C, topk), dtype=torch.uint8, device=dev)
+            out = torch.empty_like(q)
+            grads = tuple(torch.empty_like(q) for _ in range(3))
+
+            def fwd():
+                if topk:
+                    ca.iclustered_attention(q, k, v, planes, w.C, w.n_bits, w.L, topk, out=out, workspace=ws)
+                else:
+                    ca.clustered_attention(q, k, v, planes, w.C, w.n_bits, w.L, out=out, workspace=ws)
+
+            def fwd_bwd():
+                fwd()
+                if topk:
+                    ca.iclustered_attention_backward(q, k, v, dout, w.C, topk, ws, bwd_workspace=bws, grads=grads)
+                else:
+                    ca.clustered_attention_backward(q, k, v, dout, w.C, ws, bwd_workspace=bws, grads=grads)
+
+            rec[name + "_fwd"] = timed(fwd, reps) * 1e3 / (N * H)
+            rec[name + "_fwd_bwd"] = timed(fwd_bwd, reps) * 1e3 / (N * H)
+            del ws, bws, out, grads
+        tq, tk, tv = (x.clone().requires_grad_(True) for x in (q, k, v))
+
+        def exact_fwd():
+            with torch.no_grad():
+                torch.nn.functional.scaled_dot_product_attention(tq, tk, tv)
+
+        def exact_fwd_bwd():
+            o = torch.nn.functional.scaled_dot_product_attention(tq, tk, tv)
+            o.backward(dout)
+
+        rec["exact_fwd"] = timed(exact_fwd, reps) * 1e3 / (N * H)
+        rec["exact_fwd_bwd"] = timed(exact_fwd_bwd, reps) * 1e3 / (N * H)
+        for key in list(rec):
+            if isinstance(rec[key], float):
+                rec[key] = round(rec[key], 6)
+        print(json.dumps(rec), flush=True)
+        del q, k, v, planes, dout, tq, tk, tv
+        torch.cuda.empty_cache()
+
+
 def copy_calibration(nbytes):
     """A plain device-to-device copy of known size, for scaling HBM counters."""
     import torch
@@ -320,6 +403,8 @@ def main():
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES")
     ap.add_argument("--backward", action="store_true",
                     help="time the backward pass instead (its own JSON line)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="length sweep against exact attention (one JSON line per length)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the forward pass of each (sequence, head) is "
@@ -331,6 +416,9 @@ def main():
         return
     if args.backward:
         bench_backward(args)
+        return
+    if args.sweep:
+        bench_sweep(args)
         return
 
     import torch

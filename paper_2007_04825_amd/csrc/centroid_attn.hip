@@ -61,12 +61,19 @@ __global__ __launch_bounds__(256) void centroid_kernel(const T* __restrict__ q,
   const T* qu = q + static_cast<size_t>(u) * N * D;
   double acc = 0.0;
   int m = 0;
-  for (; m + 8 <= sz; m += 8) {
-    float x[8];
+  // 32 member rows in flight, their indices requested one batch ahead
+  constexpr int RB = 32;
+  int mi[RB];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) x[e] = to_f32(qu[static_cast<size_t>(mem[m + e]) * D + t]);
+  for (int e = 0; e < RB; ++e) mi[e] = mem[min(e, sz - 1)];
+  for (; m + RB <= sz; m += RB) {
+    float x[RB];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) acc += static_cast<double>(x[e]);
+    for (int e = 0; e < RB; ++e) x[e] = to_f32(qu[static_cast<size_t>(mi[e]) * D + t]);
+#pragma unroll
+    for (int e = 0; e < RB; ++e) mi[e] = mem[min(m + RB + e, sz - 1)];
+#pragma unroll
+    for (int e = 0; e < RB; ++e) acc += static_cast<double>(x[e]);
   }
   for (; m < sz; ++m) acc += static_cast<double>(to_f32(qu[static_cast<size_t>(mem[m]) * D + t]));
   dst[t] = static_cast<float>(acc / static_cast<double>(sz));
@@ -114,6 +121,7 @@ __device__ __forceinline__ void store_vec(bf16_t* p, const float* s) {
 constexpr int kLStride = kChunk + 16;  // floats per LDS logit row (the four rows of a wave fall in distinct banks)
 static_assert(kLStride >= kChunk, "rows padded for the top-k sweep: 32 grp_block_len(kChunk) <= kChunk");
 constexpr int kCandCap = 128;
+constexpr int kSparseChunk = 64;  // members per work item of sparse_kernel
 constexpr int kTileWaves = 8;  // waves per centroid-tile workgroup
 constexpr int kTileThreads = 64 * kTileWaves;
 
@@ -129,6 +137,7 @@ struct AttnArgs {
   const int32_t* lengths;
   int heads, N, C, nchunk, topk;
   int ntile, ncg, units;  // 16-centroid tiles, 4-cluster groups, (batch, head) units
+  int nsg;                // groups of four sparse_kernel work items per unit
   float scale;
   const int32_t* topk_in;
   float* pm;
@@ -599,7 +608,8 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
 
 // ---------------------------------------------------------------------------
 // Improved values (Section 3.3 with the supplementary decomposition), one
-// wave per cluster j: for every member i,
+// wave per (cluster j, chunk of up to kSparseChunk members), so that large
+// clusters spread over many waves: for every member i,
 //   out_i = m_j * sum_{l in T} softmax_T(q_i k_l / sqrt d)_l v_l + V^b_j.
 // The loads come in three dependent rounds: size, offset, m_j, V^b_j and T;
 // then the member indices with the K_T and V_T rows; then the member rows of
@@ -615,18 +625,44 @@ __global__ __launch_bounds__(256) void sparse_kernel(AttnArgs a) {
   constexpr uint32_t ESZ = sizeof(T);
   constexpr uint32_t kNone = 0x80000000u;  // past every buffer: loads read 0, stores are dropped
   __shared__ int tp[4][kCandCap];
-  const int wi = xcd_work_item();  // cluster group fastest, then (batch, head)
-  if (wi >= a.ncg * a.units) return;
-  const int u = wi / a.ncg, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wi = xcd_work_item();  // item group fastest, then (batch, head)
+  if (wi >= a.nsg * a.units) return;
+  const int u = wi / a.nsg, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int c = lane & 15, g = lane >> 4;
   const int C = a.C;
-  const int j = (wi % a.ncg) * 4 + wave;
+  // Work item t of the unit: for t < C the first kSparseChunk members of
+  // cluster t; for t >= C the further chunks of the clusters that have more,
+  // in cluster order (located by a prefix sum over the clusters).
+  const int t = (wi % a.nsg) * 4 + wave;
+  int j = t, chunk = 0;
+  if (t >= C) {
+    const int32_t* su = a.sizes + static_cast<size_t>(u) * C;
+    const int want = t - C;
+    int run = 0;
+    j = -1;
+    for (int x0 = 0; x0 < C; x0 += 64) {
+      const int x = x0 + lane;
+      const int s = x < C ? su[x] : 0;
+      const int extra = s > kSparseChunk ? (s - 1) / kSparseChunk : 0;
+      const int incl = wave_incl_scan(extra);
+      const uint64_t hit = __ballot(want >= run + incl - extra && want < run + incl);
+      if (hit != 0ull) {
+        const int src = __ffsll(static_cast<unsigned long long>(hit)) - 1;
+        j = x0 + src;
+        chunk = 1 + want - (run + __builtin_amdgcn_readlane(incl - extra, src));
+        break;
+      }
+      run += __builtin_amdgcn_readlane(incl, 63);
+    }
+    if (j < 0) return;  // past the unit's last chunk
+  }
   if (j >= C) return;
   const size_t uj = static_cast<size_t>(u) * C + j;
 
   // ---- round 1: the cluster's size, offset, m_j, V^b_j and T -----------------------
-  const int sz = a.sizes[uj];
-  const int off = a.offsets[static_cast<size_t>(u) * (C + 1) + j];
+  const int sz_all = a.sizes[uj];
+  const int sz = min(kSparseChunk, sz_all - chunk * kSparseChunk);  // members of this item
+  const int off = a.offsets[static_cast<size_t>(u) * (C + 1) + j] + chunk * kSparseChunk;
   const float mh = a.mass[uj];
   int tv[kCandCap / 64];
 #pragma unroll
@@ -636,7 +672,7 @@ __global__ __launch_bounds__(256) void sparse_kernel(AttnArgs a) {
   }
   float vbf[4 * DT];
   load_row<4 * DT>(a.vcb + uj * D + DT * 4 * g, vbf);
-  if (sz == 0) return;
+  if (sz <= 0) return;
   // T: the leading non-negative entries (a caller-supplied set may be shorter)
   int kk = 0;
 #pragma unroll
@@ -784,6 +820,8 @@ static AttnArgs make_args(const Problem& p, const Workspace& ws, const int32_t* 
   a.nchunk = ws.nchunk;
   a.ntile = (p.C + 15) / 16;
   a.ncg = (p.C + 3) / 4;
+  // at most C + n / kSparseChunk (cluster, member chunk) items per unit
+  a.nsg = (p.C + (p.n + kSparseChunk - 1) / kSparseChunk + 3) / 4;
   a.units = p.units();
   a.topk = p.topk > 0 ? p.topk : 1;
   a.scale = 1.0f / sqrtf(static_cast<float>(p.d));
@@ -834,7 +872,7 @@ static hipError_t launch_attn_t(const Problem& p, const Workspace& ws, const int
 template <int D, typename T>
 static hipError_t launch_sparse_t(const Problem& p, const Workspace& ws, hipStream_t s) {
   const AttnArgs a = make_args(p, ws, nullptr);
-  const dim3 g2(xcd_grid(static_cast<long long>(a.ncg) * a.units));
+  const dim3 g2(xcd_grid(static_cast<long long>(a.nsg) * a.units));
   switch (sparse_tiles(p.topk)) {
     case 1: hipLaunchKernelGGL((sparse_kernel<D, T, 1>), g2, dim3(256), 0, s, a); break;
     case 2: hipLaunchKernelGGL((sparse_kernel<D, T, 2>), g2, dim3(256), 0, s, a); break;

@@ -132,19 +132,32 @@ __device__ __forceinline__ int best_key(const v4i* cop, int nct, v4i bq, int lan
 }
 
 // Best keys of NG 16-query tiles at once: one centroid-operand load feeds NG
-// independent MFMAs, and the next operand is fetched before they issue.
-template <int NG>
+// independent MFMAs, and the next operand is fetched before they issue.  Four
+// centroid tiles are requested together (past the last tile the last one
+// repeats); EXACT_TAIL takes an odd last tile alone instead of pairing it
+// with a repeat, which saves its products but (measured) slows the
+// one-workgroup-per-unit kernel, whose schedule favours the branch-free form.
+template <int NG, bool EXACT_TAIL>
 __device__ __forceinline__ void best_keys(const v4i* cop, int nct, const v4i* bq, int* best, int lane) {
   const v4i zero = {0, 0, 0, 0};
   for (int ct0 = 0; ct0 < nct; ct0 += 4) {
-    // four centroid tiles requested together, then 4 x NG independent MFMAs
-    // (past the last tile the last one repeats, which leaves the maxima as
-    // they are and keeps the sequence free of branches)
     v4i a[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) a[q] = cop[min(ct0 + q, nct - 1) * 64 + lane];
 #pragma unroll
     for (int q0 = 0; q0 < 4; q0 += 2) {  // two tiles' products in flight at a time
+      if constexpr (EXACT_TAIL) {
+        const int rem = nct - ct0 - q0;  // tiles left from here (uniform)
+        if (rem <= 0) break;
+        if (rem == 1) {
+          v4i d1[NG];
+#pragma unroll
+          for (int e = 0; e < NG; ++e) d1[e] = mfma_i8_16x16x64(a[q0], bq[e], zero);
+#pragma unroll
+          for (int e = 0; e < NG; ++e) best[e] = max(best[e], max(max(d1[e][0], d1[e][1]), max(d1[e][2], d1[e][3])));
+          break;
+        }
+      }
       v4i d[2][NG];
 #pragma unroll
       for (int q = 0; q < 2; ++q)
@@ -162,13 +175,14 @@ __device__ __forceinline__ void best_keys(const v4i* cop, int nct, const v4i* bq
     best[e] = cross_rows_max(best[e]);
   }
 }
+template <bool EXACT_TAIL>
 __device__ __forceinline__ void best_keys_n(int ng, const v4i* cop, int nct, const v4i* bq,
                                             int* best, int lane) {
   switch (ng) {
-    case 1: best_keys<1>(cop, nct, bq, best, lane); break;
-    case 2: best_keys<2>(cop, nct, bq, best, lane); break;
-    case 3: best_keys<3>(cop, nct, bq, best, lane); break;
-    default: best_keys<4>(cop, nct, bq, best, lane); break;
+    case 1: best_keys<1, EXACT_TAIL>(cop, nct, bq, best, lane); break;
+    case 2: best_keys<2, EXACT_TAIL>(cop, nct, bq, best, lane); break;
+    case 3: best_keys<3, EXACT_TAIL>(cop, nct, bq, best, lane); break;
+    default: best_keys<4, EXACT_TAIL>(cop, nct, bq, best, lane); break;
   }
 }
 
@@ -332,7 +346,7 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
         }
         best[e] = INT_MIN;
       }
-      best_keys_n(left < 4 ? left : 4, sh.cop, nct, bq, best, lane);
+      best_keys_n<false>(left < 4 ? left : 4, sh.cop, nct, bq, best, lane);
       // lane l now decides query (l % 16) of tile l / 16 of the group; the
       // queries whose cluster changed move their bit counts
       const int eq = lane >> 4;
@@ -574,9 +588,9 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
 // ===========================================================================
 // Multi-workgroup path: one launch pair per Lloyd round.
 // ===========================================================================
-constexpr int kKbThreads = 256;
+constexpr int kKbThreads = 512;
 constexpr int kKbWaves = kKbThreads / 64;
-static_assert(kKmBlockQ == kMaxQt * 16 * kKbWaves, "tile budget");
+static_assert(kKmBlockQ <= kMaxQt * 16 * kKbWaves, "tile budget");
 
 __global__ __launch_bounds__(kKbThreads) void kmeans_assign_kernel(
     const uint64_t* __restrict__ codes_g, const int32_t* __restrict__ lengths, int heads, int N,
@@ -623,7 +637,7 @@ __global__ __launch_bounds__(kKbThreads) void kmeans_assign_kernel(
       bq[e] = query_operand(qi < nq ? lcodes[qi] : 0ull, g, qm);
       best[e] = INT_MIN;
     }
-    best_keys_n(left < 4 ? left : 4, cop, nct, bq, best, lane);
+    best_keys_n<true>(left < 4 ? left : 4, cop, nct, bq, best, lane);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int qo = (wave + (s0 + e) * kKbWaves) * 16 + lane;
@@ -667,11 +681,25 @@ __global__ __launch_bounds__(256) void kmeans_reduce_kernel(
   if (j >= ce) return;
   const int nb = (n + kKmBlockQ - 1) / kKmBlockQ;
   int cnt = 0, sz = 0;
-  for (int blk = 0; blk < nb; ++blk) {
-    const size_t base = (static_cast<size_t>(u) * nblk + blk) * C + j;
-    const uint32_t dw = part[base * 32 + (lane >> 1)];
-    cnt += static_cast<int>((dw >> ((lane & 1) * 16)) & 0xffffu);
-    sz += part_sizes[base];
+  // eight blocks' partials requested at a time (integer sums: any order)
+  constexpr int RB = 8;
+  for (int b0 = 0; b0 < nb; b0 += RB) {
+    uint32_t dw[RB];
+    int ps[RB];
+#pragma unroll
+    for (int e = 0; e < RB; ++e) {
+      const int blk = min(b0 + e, nb - 1);
+      const size_t base = (static_cast<size_t>(u) * nblk + blk) * C + j;
+      dw[e] = part[base * 32 + (lane >> 1)];
+      ps[e] = part_sizes[base];
+    }
+#pragma unroll
+    for (int e = 0; e < RB; ++e) {
+      if (b0 + e < nb) {
+        cnt += static_cast<int>((dw[e] >> ((lane & 1) * 16)) & 0xffffu);
+        sz += ps[e];
+      }
+    }
   }
   const uint64_t bits = __ballot(2 * cnt > sz);
   if (lane == 0)
@@ -714,13 +742,21 @@ __global__ __launch_bounds__(256) void csr_scan_kernel(int32_t* __restrict__ csr
   const int n = unit_length(lengths, u / heads, N);
   const int nb = (n + kCsrBlockQ - 1) / kCsrBlockQ;
   int run = 0;
-  if (j < C)
-    for (int blk = 0; blk < nb; ++blk) {
-      int32_t* x = &csr_cnt[(static_cast<size_t>(u) * ncsr + blk) * C + j];
-      const int v = *x;
-      *x = run;
-      run += v;
+  if (j < C) {
+    // exclusive prefix over the blocks, sixteen block counts requested at a time
+    constexpr int RB = 16;
+    for (int b0 = 0; b0 < nb; b0 += RB) {
+      int v[RB];
+#pragma unroll
+      for (int e = 0; e < RB; ++e)
+        v[e] = b0 + e < nb ? csr_cnt[(static_cast<size_t>(u) * ncsr + b0 + e) * C + j] : 0;
+#pragma unroll
+      for (int e = 0; e < RB; ++e) {
+        if (b0 + e < nb) csr_cnt[(static_cast<size_t>(u) * ncsr + b0 + e) * C + j] = run;
+        run += v[e];
+      }
     }
+  }
   const int incl = wave_incl_scan(run);
   if (lane == 63) wtot[wave] = incl;
   __syncthreads();
@@ -789,8 +825,10 @@ int kmeans_uses_lds(const Problem& p) {
   if (g_kmeans_path == 1) return 1;
   if (g_kmeans_path == 2) return 0;
   // One workgroup per unit when there are enough units to occupy the chip
-  // or the sequences are short; otherwise spread each unit over workgroups.
-  return (p.units() >= 128 || p.n <= 1024) ? 1 : 0;
+  // or the sequences are short; otherwise spread each unit over workgroups
+  // (its chain of per-round launches costs about 0.25 ms, which a single
+  // workgroup per unit beats up to n = 2048 even with 8 units).
+  return (p.units() >= 128 || p.n <= 2048) ? 1 : 0;
 }
 
 hipError_t launch_load_assign(const Problem& p, const int32_t* assign_in, const Workspace& ws,
