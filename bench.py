@@ -298,14 +298,175 @@ def bench_backward(args):
     print(json.dumps(rec))
 
 
+def _timed(hip, stream, fn, reps):
+    """Median of reps HIP-event timings of fn (ms) after three untimed calls."""
+    import torch
+    for _ in range(3):
+        fn()
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(reps):
+        e0, e1 = hip.event(), hip.event()
+        hip.record(e0, stream)
+        fn()
+        hip.record(e1, stream)
+        ts.append(hip.elapsed_ms(e0, e1))
+        hip.destroy(e0)
+        hip.destroy(e1)
+    return float(np.median(ts))
+
+
+def _length_point(w, reps, hip, stream, exact_batch=None):
+    """Times one workload at one length: each variant's forward and forward +
+    backward, and (exact_batch > 0) torch's fp32 scaled_dot_product_attention
+    with its autograd backward on the first exact_batch sequences.  Returns
+    {name: (ms, peak bytes beyond the resident inputs, sequences)}; the peak
+    covers the workspaces, outputs and gradients that each path allocates
+    through torch."""
+    import torch
+
+    import gen
+    import paper_2007_04825_amd as ca
+
+    dev = torch.device("cuda:0")
+    B, H, N, D = w.q.shape
+    dt = ca.CA_F32 if w.dtype == "f32" else ca.CA_BF16
+    tdt = torch.float32 if w.dtype == "f32" else torch.bfloat16
+    q, k, v = (torch.from_numpy(x).to(dev).to(tdt) for x in (w.q, w.k, w.v))
+    planes = torch.from_numpy(w.planes).to(dev)
+    dout = torch.from_numpy(gen.output_gradient(w)).to(dev).to(tdt)
+    res = {}
+
+    def peak_of(run):
+        torch.cuda.synchronize()
+        base = torch.cuda.memory_allocated()
+        torch.cuda.reset_peak_memory_stats()
+        run()
+        torch.cuda.synchronize()
+        return torch.cuda.max_memory_allocated() - base
+
+    for name, topk in (("clustered", 0), ("iclustered", w.topk)):
+        state = {}
+
+        def alloc():
+            state["ws"] = torch.empty(ca.workspace_bytes(B, H, N, D, dt, w.C, w.n_bits, topk),
+                                      dtype=torch.uint8, device=dev)
+            state["bws"] = torch.empty(ca.backward_workspace_bytes(B, H, N, D, dt, w.C, topk),
+                                       dtype=torch.uint8, device=dev)
+            state["out"] = torch.empty_like(q)
+            state["grads"] = tuple(torch.empty(q.shape, dtype=torch.float32, device=dev) for _ in range(3))
+
+        def fwd():
+            if topk:
+                ca.iclustered_attention(q, k, v, planes, w.C, w.n_bits, w.L, topk, out=state["out"],
+                                        workspace=state["ws"])
+            else:
+                ca.clustered_attention(q, k, v, planes, w.C, w.n_bits, w.L, out=state["out"],
+                                       workspace=state["ws"])
+
+        def fwd_bwd():
+            fwd()
+            if topk:
+                ca.iclustered_attention_backward(q, k, v, dout, w.C, topk, state["ws"],
+                                                 bwd_workspace=state["bws"], grads=state["grads"])
+            else:
+                ca.clustered_attention_backward(q, k, v, dout, w.C, state["ws"],
+                                                bwd_workspace=state["bws"], grads=state["grads"])
+
+        mem = peak_of(lambda: (alloc(), fwd_bwd()))
+        res[name + "_fwd"] = (_timed(hip, stream, fwd, reps), None, B)
+        res[name + "_fwd_bwd"] = (_timed(hip, stream, fwd_bwd, reps), mem, B)
+        state.clear()
+    if exact_batch:
+        be = min(B, exact_batch)
+        tq, tk, tv = (x[:be].float().clone().requires_grad_(True) for x in (q, k, v))
+        g32 = dout[:be].float().contiguous()
+
+        def exact_fwd():
+            with torch.no_grad():
+                torch.nn.functional.scaled_dot_product_attention(tq, tk, tv)
+
+        def exact_fwd_bwd():
+            o = torch.nn.functional.scaled_dot_product_attention(tq, tk, tv)
+            o.backward(g32)
+
+        res["exact_fwd"] = (_timed(hip, stream, exact_fwd, reps), None, be)
+        mem = peak_of(exact_fwd_bwd)
+        for x in (tq, tk, tv):
+            x.grad = None
+        res["exact_fwd_bwd"] = (_timed(hip, stream, exact_fwd_bwd, reps), mem, be)
+        del tq, tk, tv, g32
+    del q, k, v, planes, dout
+    torch.cuda.empty_cache()
+    return res
+
+
 def bench_sweep(args):
-    """Length sweep in the protocol of the paper's time benchmark: one
-    attention layer of 8 heads x 64 over N = 2^10 .. 2^15 (batch 1, fp32,
-    iid N(0, 1) inputs, C 100, B 63, L 10, k 32), each variant's forward and
-    forward + backward timed with HIP events (median of repetitions after
-    warm-up), next to exact softmax attention (torch's scaled_dot_product_attention,
-    fp32, its backward through autograd).  Prints one JSON line per N with
-    times per (query, head)."""
+    """Length sweep: batch 1, 8 heads x 64, N = 2^10 .. 2^15, fp32 and bf16
+    storage (iid N(0, 1) inputs, C 100, B 63, L 10, k 32); each variant's
+    forward and forward + backward timed with HIP events (median of repetitions
+    after warm-up) next to exact softmax attention (torch's fp32
+    scaled_dot_product_attention, its backward through autograd).  One JSON
+    line per (N, dtype) with times per (query, head)."""
+    import torch
+
+    import gen
+
+    dev = torch.device("cuda:0")
+    hip = Hip()
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    for dtype in ("f32", "bf16"):
+        for logn in range(10, 16):
+            N = 1 << logn
+            w = gen.config_sweep(N, dtype=dtype)
+            B, H, _, D = w.q.shape
+            res = _length_point(w, 20 if N <= 8192 else 8, hip, stream,
+                                exact_batch=B if dtype == "f32" else None)
+            rec = {"N": N, "heads": H, "d": D, "dtype": dtype, "unit": "us per (query, head)"}
+            for key, (ms, _, nb) in res.items():
+                rec[key] = round(ms * 1e3 / (nb * N * H), 6)
+            print(json.dumps(rec), flush=True)
+
+
+def bench_fig4(args):
+    """The paper's time and memory benchmark protocol: one attention layer of
+    6 heads x 64, N = 2^9 .. 2^15, as many sequences per call as the path is
+    given (a budget of 2^17 tokens, so batch = 2^17 / N), C 100, B 63, L 10,
+    k 32, fp32, iid N(0, 1) inputs.  Reports GPU time and the peak memory
+    beyond the resident inputs per sequence element, forward and forward +
+    backward, for both variants and exact attention.  Exact attention takes at
+    most 2^32 / (6 N^2) sequences per call (at least one), which keeps one
+    N x N fp32 tensor per call under 17 GB whichever backend torch picks.  The
+    projections and the feed-forward layer of the paper's one-layer model lie
+    outside the path and are not timed."""
+    import torch
+
+    import gen
+
+    dev = torch.device("cuda:0")
+    hip = Hip()
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    budget = 1 << 17
+    for logn in range(9, 16):
+        N = 1 << logn
+        B = max(1, budget // N)
+        w = gen.config_sweep(N, dtype="f32", B=B, H=6, d=64)
+        be = max(1, min(B, (1 << 32) // (6 * N * N)))
+        res = _length_point(w, 10 if N <= 4096 else 5, hip, stream, exact_batch=be)
+        rec = {"N": N, "batch": B, "exact_batch": be, "heads": 6, "d": 64, "dtype": "f32",
+               "unit": "us per element; bytes per element"}
+        for key, (ms, mem, nb) in res.items():
+            rec[key + "_us"] = round(ms * 1e3 / (nb * N), 6)
+            if mem is not None:
+                rec[key + "_bytes"] = round(mem / (nb * N), 1)
+        print(json.dumps(rec), flush=True)
+
+
+def bench_long(args):
+    """Long-context stress: batch 1, 8 heads x 64, N = 65536, bf16 storage,
+    C 200, B 63, L 15, k 64, improved clustered attention only.  One JSON line:
+    the forward's time (median of HIP-event timings), queries per second, and
+    each stage's time from separate calls."""
     import torch
 
     import gen
@@ -314,71 +475,40 @@ def bench_sweep(args):
     dev = torch.device("cuda:0")
     hip = Hip()
     stream = torch.cuda.current_stream(dev).cuda_stream
+    w = gen.config_long()
+    B, H, N, D = w.q.shape
+    q, k, v = (torch.from_numpy(x).to(dev).to(torch.bfloat16) for x in (w.q, w.k, w.v))
+    planes = torch.from_numpy(w.planes).to(dev)
+    ws = torch.empty(ca.workspace_bytes(B, H, N, D, ca.CA_BF16, w.C, w.n_bits, w.topk),
+                     dtype=torch.uint8, device=dev)
+    out = torch.empty_like(q)
 
-    def timed(fn, reps):
-        for _ in range(3):
-            fn()
-        torch.cuda.synchronize()
+    def fwd():
+        ca.iclustered_attention(q, k, v, planes, w.C, w.n_bits, w.L, w.topk, out=out, workspace=ws)
+
+    ms = _timed(hip, stream, fwd, max(3, args.steps // 20))
+    stages = {}
+    lib = ca.library()
+    for name, sid in ca.STAGES.items():
         ts = []
-        for _ in range(reps):
+        for _ in range(3):
             e0, e1 = hip.event(), hip.event()
-            hip.record(e0, stream)
-            fn()
-            hip.record(e1, stream)
-            ts.append(hip.elapsed_ms(e0, e1))
+            assert lib.ca_time_next_stage(sid, e0, e1) == 0
+            fwd()
+            t = hip.elapsed_ms(e0, e1)
             hip.destroy(e0)
             hip.destroy(e1)
-        return float(np.median(ts))
-
-    for logn in range(10, 16):
-        N = 1 << logn
-        w = gen.config_sweep(N, dtype="f32")
-        B, H, _, D = w.q.shape
-        q, k, v = (torch.from_numpy(x).to(dev) for x in (w.q, w.k, w.v))
-        planes = torch.from_numpy(w.planes).to(dev)
-        dout = torch.from_numpy(gen.output_gradient(w)).to(dev)
-        reps = 20 if N <= 8192 else 8
-        rec = {"N": N, "heads": H, "d": D, "dtype": "f32", "unit": "us per (query, head)"}
-        for name, topk in (("clustered", 0), ("iclustered", w.topk)):
-            ws = torch.empty(ca.workspace_bytes(B, H, N, D, 0, w.C, w.n_bits, topk), dtype=torch.uint8, device=dev)
-            bws = torch.empty(ca.backward_workspace_bytes(B, H, N, D, 0, w.C, topk), dtype=torch.uint8, device=dev)
-            out = torch.empty_like(q)
-            grads = tuple(torch.empty_like(q) for _ in range(3))
-
-            def fwd():
-                if topk:
-                    ca.iclustered_attention(q, k, v, planes, w.C, w.n_bits, w.L, topk, out=out, workspace=ws)
-                else:
-                    ca.clustered_attention(q, k, v, planes, w.C, w.n_bits, w.L, out=out, workspace=ws)
-
-            def fwd_bwd():
-                fwd()
-                if topk:
-                    ca.iclustered_attention_backward(q, k, v, dout, w.C, topk, ws, bwd_workspace=bws, grads=grads)
-                else:
-                    ca.clustered_attention_backward(q, k, v, dout, w.C, ws, bwd_workspace=bws, grads=grads)
-
-            rec[name + "_fwd"] = timed(fwd, reps) * 1e3 / (N * H)
-            rec[name + "_fwd_bwd"] = timed(fwd_bwd, reps) * 1e3 / (N * H)
-            del ws, bws, out, grads
-        tq, tk, tv = (x.clone().requires_grad_(True) for x in (q, k, v))
-
-        def exact_fwd():
-            with torch.no_grad():
-                torch.nn.functional.scaled_dot_product_attention(tq, tk, tv)
-
-        def exact_fwd_bwd():
-            o = torch.nn.functional.scaled_dot_product_attention(tq, tk, tv)
-            o.backward(dout)
-
-        rec["exact_fwd"] = timed(exact_fwd, reps) * 1e3 / (N * H)
-        rec["exact_fwd_bwd"] = timed(exact_fwd_bwd, reps) * 1e3 / (N * H)
-        for key in list(rec):
-            if isinstance(rec[key], float):
-                rec[key] = round(rec[key], 6)
-        print(json.dumps(rec), flush=True)
-        del q, k, v, planes, dout, tq, tk, tv
-        torch.cuda.empty_cache()
+            if t is None:
+                break
+            ts.append(t)
+        if ts:
+            stages[name] = round(float(np.median(ts)) * 1e3, 1)
+    print(json.dumps({"metric": "queries/sec/GPU of i-clustered attn fwd (long context)",
+                      "value": round(B * N / (ms * 1e-3), 1), "unit": "queries/s",
+                      "ms_per_call": round(ms, 4), "dtype": "bf16", "data": "synthetic",
+                      "config": {"workload": "long-context stress: batch 1, heads 8, N 65536, d 64, bf16, "
+                                             "C 200, B 63, L 15, k 64; i-clustered"},
+                      "stages_us": stages}), flush=True)
 
 
 def copy_calibration(nbytes):
@@ -405,6 +535,10 @@ def main():
                     help="time the backward pass instead (its own JSON line)")
     ap.add_argument("--sweep", action="store_true",
                     help="length sweep against exact attention (one JSON line per length)")
+    ap.add_argument("--long", action="store_true",
+                    help="time the N = 65536 long-context forward (its own JSON line)")
+    ap.add_argument("--fig4", action="store_true",
+                    help="time and memory per sequence element in the paper's benchmark protocol")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the forward pass of each (sequence, head) is "
@@ -419,6 +553,12 @@ def main():
         return
     if args.sweep:
         bench_sweep(args)
+        return
+    if args.fig4:
+        bench_fig4(args)
+        return
+    if args.long:
+        bench_long(args)
         return
 
     import torch
