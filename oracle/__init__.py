@@ -70,6 +70,10 @@ def _load():
     lib.orc_backward.argtypes = [dp, dp, dp, i32p, i32, i32, i64, i32, i32, i32, i32p, i32p,
                                  dp, i32, dp, dp, dp]
     lib.orc_backward.restype = i32
+    lib.orc_oracle_top.argtypes = [dp, dp, dp, i64, i32, i32, dp, i32p]
+    lib.orc_oracle_top_forward.argtypes = [dp, dp, dp, i32p, i32, i32, i64, i32, i32, i32, dp,
+                                           i32p]
+    lib.orc_oracle_top_forward.restype = i32
     _lib = lib
     return lib
 
@@ -293,3 +297,37 @@ def backward(q, k, v, lengths, C, topk_, assign, topk_sets, dout, num_threads=No
     if rc != 0:
         raise ValueError("oracle rejected the arguments")
     return dq, dk, dv
+
+
+def oracle_top_unit(q, k, v, topk_):
+    """Oracle-top for one (sequence, head) of n queries and keys: each query
+    attends to its topk_ keys of highest logit only, with the softmax
+    renormalised over them.  Returns (out [n, d], T [n, topk_], -1 padded)."""
+    q, k, v = _f64(q), _f64(k), _f64(v)
+    n, d = q.shape
+    out = np.zeros((n, d), np.float64)
+    t = np.full((n, topk_), -1, np.int32)
+    P = ctypes.c_double
+    _load().orc_oracle_top(_ptr(q, P), _ptr(k, P), _ptr(v, P), n, d, topk_, _ptr(out, P),
+                           _ptr(t, ctypes.c_int32))
+    return out, t
+
+
+def oracle_top(q, k, v, lengths, topk_, num_threads=None):
+    """Oracle-top over [B, H, N, d] inputs with per-sequence lengths (None: all
+    N).  Returns (out [B, H, N, d], T [B, H, N, topk_]); padded rows give 0 and
+    -1."""
+    q, k, v = _f64(q), _f64(k), _f64(v)
+    B, H, N, d = q.shape
+    lens = None if lengths is None else np.ascontiguousarray(lengths, dtype=np.int32)
+    out = np.zeros((B, H, N, d), np.float64)
+    t = np.full((B, H, N, topk_), -1, np.int32)
+    if num_threads is None:
+        num_threads = os.cpu_count() or 1
+    P = ctypes.c_double
+    rc = _load().orc_oracle_top_forward(_ptr(q, P), _ptr(k, P), _ptr(v, P),
+                                        _ptr(lens, ctypes.c_int32), B, H, N, d, topk_,
+                                        int(num_threads), _ptr(out, P), _ptr(t, ctypes.c_int32))
+    if rc != 0:
+        raise ValueError("oracle rejected the arguments")
+    return out, t

@@ -28,6 +28,9 @@
  *     C_eff = min(C, n), k_eff = min(k, n).
  *   - the top-k set ranks keys by their centroid logit (equivalently by A^c,
  *     softmax being monotone); a tie goes to the smaller key index.
+ *   - oracle-top (the paper's comparison variant that keeps each query's k
+ *     keys of highest attention): the weights are the softmax renormalised
+ *     over those k keys; the ranking and its ties follow the top-k rule above.
  *   - gradients (the paper trains through the operator but writes no
  *     backward pass): the partition and the top-k sets are discrete and held
  *     constant; the gradient flows through the centroids (Eq. 3), the
@@ -753,6 +756,69 @@ int orc_backward(const double* q, const double* k, const double* v,
       orc_iclustered_backward(q + off, k + off, v + off, n, d, assign + u * N, C, topk,
                               topk_sets ? topk_sets + u * C * topk : NULL, dout + off,
                               dq + off, dk + off, dv + off);
+  }
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Oracle-top (the comparison variant of Sec. 4.2's approximation study):     */
+/* each query keeps only the k keys of highest attention, i.e. of highest     */
+/* exact logit Q_i . K_l / sqrt(d) (softmax is monotone; a tie goes to the     */
+/* smaller key index), and attends to those alone: out_i =                     */
+/* sum_{l in T_i} softmax_{T_i}(Q_i . K_l / sqrt(d)) V_l.  The weights are     */
+/* renormalised over T_i.  k_eff = min(k, n).  topk_out (n x k, may be NULL)   */
+/* receives T_i in ascending key order, -1 past k_eff.                         */
+/* ------------------------------------------------------------------------ */
+void orc_oracle_top(const double* q, const double* k, const double* v, int64_t n,
+                    int d, int topk, double* out, int32_t* topk_out) {
+  const double scale = 1.0 / sqrt((double)d);
+  double* s = (double*)malloc(sizeof(double) * (size_t)(n > 0 ? n : 1));
+  int32_t* t = (int32_t*)malloc(sizeof(int32_t) * (size_t)(topk > 0 ? topk : 1));
+  for (int64_t i = 0; i < n; ++i) {
+    for (int64_t l = 0; l < n; ++l) {
+      double dot = 0.0;
+      for (int x = 0; x < d; ++x) dot += q[i * d + x] * k[l * d + x];
+      s[l] = dot * scale;
+    }
+    const int ke = orc_topk(s, n, topk, t); /* T_i */
+    double m = -INFINITY;
+    for (int r = 0; r < ke; ++r)
+      if (s[t[r]] > m) m = s[t[r]];
+    double z = 0.0;
+    for (int r = 0; r < ke; ++r) z += exp(s[t[r]] - m);
+    for (int x = 0; x < d; ++x) {
+      double acc = 0.0;
+      for (int r = 0; r < ke; ++r) acc += (exp(s[t[r]] - m) / z) * v[(int64_t)t[r] * d + x];
+      out[i * d + x] = acc;
+    }
+    if (topk_out)
+      for (int r = 0; r < topk; ++r) topk_out[i * topk + r] = r < ke ? t[r] : -1;
+  }
+  free(t);
+  free(s);
+}
+
+/* Oracle-top over a padded batch [batch][heads][N][d] with per-sequence valid */
+/* lengths (NULL: all N); padded rows of out are 0 and of topk_out -1.  Units  */
+/* run in parallel over num_threads threads.  Returns 0, or -1 for bad sizes.  */
+int orc_oracle_top_forward(const double* q, const double* k, const double* v,
+                           const int32_t* lengths, int batch, int heads, int64_t N, int d,
+                           int topk, int num_threads, double* out, int32_t* topk_out) {
+  if (batch < 1 || heads < 1 || N < 1 || d < 1 || topk < 1) return -1;
+  if (lengths)
+    for (int b = 0; b < batch; ++b)
+      if (lengths[b] < 0 || lengths[b] > N) return -1;
+  const int64_t units = (int64_t)batch * heads;
+  const int nth = num_threads > 0 ? num_threads : omp_get_max_threads();
+#pragma omp parallel for schedule(dynamic, 1) num_threads(nth)
+  for (int64_t u = 0; u < units; ++u) {
+    const int64_t n = lengths ? lengths[u / heads] : N;
+    double* o = out + u * N * d;
+    for (int64_t x = 0; x < N * d; ++x) o[x] = 0.0;
+    int32_t* tk = topk_out ? topk_out + u * N * topk : NULL;
+    if (tk)
+      for (int64_t x = 0; x < N * topk; ++x) tk[x] = -1;
+    orc_oracle_top(q + u * N * d, k + u * N * d, v + u * N * d, n, d, topk, o, tk);
   }
   return 0;
 }

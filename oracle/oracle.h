@@ -46,4 +46,9 @@ int orc_backward(const double* q, const double* k, const double* v,
                  const int32_t* lengths, int batch, int heads, int64_t N, int d, int C,
                  int topk, const int32_t* assign, const int32_t* topk_sets,
                  const double* dout, int num_threads, double* dq, double* dk, double* dv);
+void orc_oracle_top(const double* q, const double* k, const double* v, int64_t n,
+                    int d, int topk, double* out, int32_t* topk_out);
+int orc_oracle_top_forward(const double* q, const double* k, const double* v,
+                           const int32_t* lengths, int batch, int heads, int64_t N, int d,
+                           int topk, int num_threads, double* out, int32_t* topk_out);
 #endif
