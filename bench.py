@@ -511,6 +511,81 @@ def bench_long(args):
                       "stages_us": stages}), flush=True)
 
 
+def bench_oracle_top(args):
+    """Oracle-top attention (each query keeps its k = 32 keys of highest logit)
+    on the speech-encoder workload: one JSON line with the throughput, the
+    roofline entry of its tile kernel (the n x n logits on the fp32 matrix
+    cores, 2 n^2 d flops per (sequence, head); the top-k rows add 2 n k d) and
+    the fp64 oracle timed on the host."""
+    import torch
+
+    import gen
+    import oracle
+    import paper_2007_04825_amd as ca
+
+    w = gen.make_config(2)
+    B, H, N, D = w.q.shape
+    dev = torch.device("cuda:0")
+    hip = Hip()
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    q, k, v = (torch.from_numpy(x).to(dev) for x in (w.q, w.k, w.v))
+    lengths = torch.from_numpy(w.lengths).to(dev)
+    ws = torch.empty(ca.oracle_top_workspace_bytes(B, H, N, D, ca.CA_F32, w.topk), dtype=torch.uint8,
+                     device=dev)
+    out = torch.empty_like(q)
+
+    def step():
+        ca.oracle_top_attention(q, k, v, w.topk, lengths=lengths, out=out, workspace=ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = hip.event(), hip.event()
+    hip.record(e0, stream)
+    for _ in range(args.steps):
+        step()
+    hip.record(e1, stream)
+    ms = hip.elapsed_ms(e0, e1) / args.steps
+    # the tile kernel alone, from the library's event hook
+    lib = ca.library()
+    kts = []
+    for _ in range(20):
+        a0, a1 = hip.event(), hip.event()
+        assert lib.ca_time_next_stage(ca.CA_KERNEL_CENTROID_ATTN, a0, a1) == 0
+        step()
+        kts.append(hip.elapsed_ms(a0, a1))
+        hip.destroy(a0)
+        hip.destroy(a1)
+    kus = float(np.mean(kts)) * 1e3
+    lens = w.lengths.astype(np.float64)
+    flops = float(H * (2.0 * (lens ** 2).sum() * D + 2.0 * lens.sum() * w.topk * D))
+    achieved = flops / (kus * 1e-6) / 1e12
+    nq = int(w.lengths.sum()) * H
+    rec = {"metric": "queries/sec/GPU of oracle-top attn fwd", "value": round(nq / (ms * 1e-3), 1),
+           "unit": "queries/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+           "ms_per_step": round(ms, 5), "higher_is_better": True, "dtype": "f32",
+           "data": "synthetic",
+           "config": {"workload": "speech-encoder layer: batch 32, heads 6, N 800 (lengths 400-800), "
+                                  "d 32, fp32, k 32; oracle-top"},
+           "roofline": {"bound": "mfma", "achieved": round(achieved, 3),
+                        "peak": PEAKS["fp32_mfma_TFLOPs"], "unit": "TFLOP/s",
+                        "frac": round(achieved / PEAKS["fp32_mfma_TFLOPs"], 5), "traffic": None,
+                        "kernel": "attn_tile_kernel (oracle-top)", "avg_launch_us": round(kus, 3)}}
+    if not args.no_cpu_baseline:
+        threads = cpu_threads()
+        passes, t0 = 0, time.perf_counter()
+        while True:
+            oracle.oracle_top(w.q, w.k, w.v, w.lengths, w.topk, num_threads=threads)
+            passes += 1
+            el = time.perf_counter() - t0
+            if el >= 10.0:
+                break
+        rec["cpu_baseline"] = {"value": round(nq * passes / el, 1), "unit": "queries/s",
+                               "cores": threads, "kind": "oracle",
+                               "sample": "%d passes of the full workload (%.1f s)" % (passes, el)}
+    print(json.dumps(rec), flush=True)
+
+
 def copy_calibration(nbytes):
     """A plain device-to-device copy of known size, for scaling HBM counters."""
     import torch
@@ -535,6 +610,8 @@ def main():
                     help="time the backward pass instead (its own JSON line)")
     ap.add_argument("--sweep", action="store_true",
                     help="length sweep against exact attention (one JSON line per length)")
+    ap.add_argument("--oracle-top", action="store_true",
+                    help="time oracle-top attention on the speech workload (its own JSON line)")
     ap.add_argument("--long", action="store_true",
                     help="time the N = 65536 long-context forward (its own JSON line)")
     ap.add_argument("--fig4", action="store_true",
@@ -559,6 +636,9 @@ def main():
         return
     if args.long:
         bench_long(args)
+        return
+    if args.oracle_top:
+        bench_oracle_top(args)
         return
 
     import torch

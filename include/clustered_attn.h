@@ -213,6 +213,32 @@ int iclustered_attention_bwd(const void* q, const void* k, const void* v,
                              void* bwd_workspace, size_t bwd_workspace_bytes,
                              void* stream);
 
+/*
+ * Oracle-top attention: the comparison variant of the approximation study
+ * (Section 4.2) in which each query keeps only its k keys of highest
+ * attention.  For every valid query i of a unit, T_i is the set of
+ * k_eff = min(k, length) keys with the largest logits Q_i . K_l / sqrt(d)
+ * (a tie goes to the smaller key index), and
+ *   out_i = sum_{l in T_i} softmax_{T_i}(Q_i . K_l / sqrt(d))_l V_l,
+ * the softmax renormalised over T_i.  No hashing or clustering takes place;
+ * the cost is that of exact attention, O(n^2 d) per unit.
+ * q, k, v, out, lengths, dtype, stream: as above.  topk_out is NULL or a
+ * DEVICE int32[batch][heads][n][topk]: T_i in ascending key order, -1 past
+ * k_eff and for padded rows.  workspace: at least
+ * ca_oracle_top_workspace_bytes(...) bytes, 256-byte aligned, contents
+ * irrelevant; it grows as n * ceil(n / 1024) * topk per unit.
+ * Sizes as above (n_clusters, n_bits and lloyd_iters do not apply).
+ * Passing the same pointer as q and k gives the shared-QK input mode of the
+ * same study (keys equal to the queries); every entry point of this library
+ * accepts that aliasing, since q and k are only read.
+ */
+size_t ca_oracle_top_workspace_bytes(int batch, int heads, int n, int d, int dtype,
+                                     int topk);
+int oracle_top_attention_fwd(const void* q, const void* k, const void* v,
+                             const int32_t* lengths, int batch, int heads, int n,
+                             int d, int dtype, int topk, void* out, int32_t* topk_out,
+                             void* workspace, size_t workspace_bytes, void* stream);
+
 /* Message describing the last non-zero status returned on this thread. */
 const char* ca_last_error(void);
 
@@ -224,7 +250,8 @@ int ca_version(void);
  *   CA_KERNEL_HASH           hashing of the queries (Section 3.2.2)
  *   CA_KERNEL_KMEANS         the L Lloyd rounds of Hamming K-means
  *   CA_KERNEL_CENTROIDS      query centroids (Eq. 3)
- *   CA_KERNEL_CENTROID_ATTN  centroid attention, top-k and mass (Eqs. 4-5, Section 3.3)
+ *   CA_KERNEL_CENTROID_ATTN  centroid attention, top-k and mass (Eqs. 4-5, Section 3.3);
+ *                            in an oracle-top call, its whole work
  *   CA_KERNEL_OUTPUT         broadcast (Eq. 6) or the improved per-query part
  *   CA_KERNEL_BWD_CENTROID   (backward calls) the centroid part of the
  *                            gradient: dK, dV and the dQ^c partials

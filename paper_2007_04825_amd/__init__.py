@@ -19,6 +19,7 @@ __all__ = [
     "clustered_attention", "iclustered_attention", "set_kmeans_path", "EXPORTED_SYMBOLS",
     "backward_workspace_bytes", "clustered_attention_bwd", "iclustered_attention_bwd",
     "clustered_attention_backward", "iclustered_attention_backward",
+    "oracle_top_workspace_bytes", "oracle_top_attention_fwd", "oracle_top_attention",
 ]
 
 CA_OK = 0
@@ -32,7 +33,8 @@ CA_BF16 = 1
 EXPORTED_SYMBOLS = ("ca_workspace_bytes", "clustered_attention_fwd", "iclustered_attention_fwd",
                     "ca_last_error", "ca_version", "ca_set_kmeans_path", "ca_time_next_stage",
                     "ca_backward_workspace_bytes", "clustered_attention_bwd",
-                    "iclustered_attention_bwd")
+                    "iclustered_attention_bwd", "ca_oracle_top_workspace_bytes",
+                    "oracle_top_attention_fwd")
 CA_KERNEL_HASH, CA_KERNEL_KMEANS, CA_KERNEL_CENTROIDS, CA_KERNEL_CENTROID_ATTN, CA_KERNEL_OUTPUT = \
     1, 2, 3, 4, 5
 CA_KERNEL_BWD_CENTROID = 6
@@ -88,6 +90,10 @@ def library():
     lib.clustered_attention_bwd.restype = i32
     lib.iclustered_attention_bwd.argtypes = bcommon + [i32] + btail
     lib.iclustered_attention_bwd.restype = i32
+    lib.ca_oracle_top_workspace_bytes.argtypes = [i32] * 6
+    lib.ca_oracle_top_workspace_bytes.restype = sz
+    lib.oracle_top_attention_fwd.argtypes = [vp, vp, vp, vp] + [i32] * 6 + [vp, vp, vp, sz, vp]
+    lib.oracle_top_attention_fwd.restype = i32
     _lib = lib
     return lib
 
@@ -123,6 +129,17 @@ def iclustered_attention_bwd(q, k, v, lengths, batch, heads, n, d, dtype, n_clus
                                               n_clusters, topk, dout, dq, dk, dv, workspace,
                                               workspace_nbytes, bwd_workspace,
                                               bwd_workspace_nbytes, stream)
+
+
+def oracle_top_workspace_bytes(batch, heads, n, d, dtype, topk) -> int:
+    return int(library().ca_oracle_top_workspace_bytes(batch, heads, n, d, dtype, topk))
+
+
+def oracle_top_attention_fwd(q, k, v, lengths, batch, heads, n, d, dtype, topk, out, topk_out,
+                             workspace, workspace_nbytes, stream=None):
+    """Raw call with integer device addresses; returns the status code."""
+    return library().oracle_top_attention_fwd(q, k, v, lengths, batch, heads, n, d, dtype, topk,
+                                              out, topk_out, workspace, workspace_nbytes, stream)
 
 
 def time_next_stage(stage: int, start_event, stop_event):
@@ -253,6 +270,33 @@ def iclustered_attention(q, k, v, planes, n_clusters=100, n_bits=63, lloyd_iters
     _check(iclustered_attention_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), _ptr(lengths),
                                     _ptr(planes), B, H, N, D, dt, n_clusters, n_bits, lloyd_iters,
                                     topk, out.data_ptr(), ws.data_ptr(), need, aux, stream))
+    return out
+
+
+def oracle_top_attention(q, k, v, topk=32, lengths=None, out=None, topk_out=None,
+                         workspace=None):
+    """Oracle-top attention (each query attends to its topk keys of highest
+    logit only, softmax renormalised over them) on torch device tensors.
+    topk_out: optional int32 device tensor [batch, heads, n, topk] that
+    receives the sets.  Pass k=q for the shared-QK input mode."""
+    torch = _torch()
+    B, H, N, D = _prepare(q, k, v, None, lengths)
+    dt = _dtype_code(q)
+    need = oracle_top_workspace_bytes(B, H, N, D, dt, topk)
+    if need == 0:
+        _check(library().oracle_top_attention_fwd(None, None, None, None, B, H, N, D, dt, topk,
+                                                  None, None, None, 0, None))
+    if topk_out is not None and (topk_out.dtype != torch.int32 or not topk_out.is_cuda
+                                 or not topk_out.is_contiguous()
+                                 or tuple(topk_out.shape) != (B, H, N, topk)):
+        raise ValueError("topk_out must be a contiguous int32 device tensor [batch, heads, n, topk]")
+    ws = _workspace(need, q.device, workspace)
+    if out is None:
+        out = torch.empty_like(q)
+    stream = torch.cuda.current_stream(q.device).cuda_stream
+    _check(oracle_top_attention_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), _ptr(lengths), B, H,
+                                    N, D, dt, topk, out.data_ptr(), _ptr(topk_out), ws.data_ptr(),
+                                    need, stream))
     return out
 
 

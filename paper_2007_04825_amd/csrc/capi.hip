@@ -105,6 +105,27 @@ size_t carve_bwd_workspace(const BwdProblem& p, void* base, BwdWorkspace* ws) {
   return off;
 }
 
+size_t carve_otop_workspace(const Problem& p, void* base, Workspace* ws) {
+  const size_t U = static_cast<size_t>(p.units());
+  const size_t N = static_cast<size_t>(p.n);
+  const size_t K = static_cast<size_t>(p.topk > 0 ? p.topk : 1);
+  Workspace w{};
+  w.nchunk = (p.n + kChunk - 1) / kChunk;
+  size_t off = 0;
+  auto take = [&](size_t bytes) -> void* {
+    void* ptr = base ? static_cast<void*>(static_cast<char*>(base) + off) : nullptr;
+    off += align_up(bytes);
+    return ptr;
+  };
+  w.topk = static_cast<int32_t*>(take(U * N * K * 4));
+  if (w.nchunk > 1) {
+    w.cand_idx = static_cast<int32_t*>(take(U * N * w.nchunk * K * 4));
+    w.cand_val = static_cast<float*>(take(U * N * w.nchunk * K * 4));
+  }
+  if (ws) *ws = w;
+  return off;
+}
+
 // Returns CA_OK or an error code (message recorded) for the given sizes.
 static int check_sizes(int batch, int heads, int n, int d, int dtype, int C, int n_bits, int L,
                        int topk, bool improved) {
@@ -236,6 +257,46 @@ static int run_forward(const void* q, const void* k, const void* v, const int32_
     }
   }
 #undef CA_TRY
+  return CA_OK;
+}
+
+static int run_oracle_top(const void* q, const void* k, const void* v, const int32_t* lengths,
+                          int batch, int heads, int n, int d, int dtype, int topk, void* out,
+                          int32_t* topk_out, void* workspace, size_t workspace_bytes,
+                          void* stream) {
+  int rc = check_sizes(batch, heads, n, d, dtype, 1, 1, 1, topk, true);
+  if (rc != CA_OK) return rc;
+  if (!q || !k || !v || !out) return fail(CA_ERR_INVALID_ARG, "q, k, v and out must not be NULL");
+  Problem p;
+  memset(&p, 0, sizeof(p));
+  p.batch = batch;
+  p.heads = heads;
+  p.n = n;
+  p.d = d;
+  p.dtype = dtype;
+  p.C = n;  // one row per query
+  p.topk = topk;
+  p.q = q;
+  p.k = k;
+  p.v = v;
+  p.lengths = lengths;
+  p.out = out;
+  const size_t need = carve_otop_workspace(p, nullptr, nullptr);
+  if (!workspace) return fail(CA_ERR_WORKSPACE, "workspace must not be NULL (%zu bytes needed)", need);
+  if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0)
+    return fail(CA_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if (workspace_bytes < need)
+    return fail(CA_ERR_WORKSPACE, "workspace too small: %zu bytes given, %zu needed", workspace_bytes, need);
+  Workspace ws;
+  carve_otop_workspace(p, workspace, &ws);
+  if (topk_out) ws.topk = topk_out;  // the kernels write the sets in place
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  (void)hipGetLastError();
+  hipError_t e = mark(CA_KERNEL_CENTROID_ATTN, true, s);
+  if (e == hipSuccess) e = launch_oracle_top(p, ws, s);
+  if (e == hipSuccess) e = mark(CA_KERNEL_CENTROID_ATTN, false, s);
+  g_ev_kernel = 0;
+  if (e != hipSuccess) return fail(CA_ERR_HIP, "oracle-top launch failed: %s", hipGetErrorString(e));
   return CA_OK;
 }
 
@@ -392,6 +453,33 @@ int iclustered_attention_bwd(const void* q, const void* k, const void* v, const 
     return ca::run_backward(q, k, v, lengths, batch, heads, n, d, dtype, n_clusters, topk, dout,
                             dq, dk, dv, workspace, workspace_bytes, bwd_workspace,
                             bwd_workspace_bytes, stream);
+  } catch (...) {
+    return ca::fail(CA_ERR_HIP, "unexpected C++ exception");
+  }
+}
+
+size_t ca_oracle_top_workspace_bytes(int batch, int heads, int n, int d, int dtype, int topk) {
+  if (ca::check_sizes(batch, heads, n, d, dtype, 1, 1, 1, topk, true) != CA_OK) return 0;
+  ca::Problem p;
+  memset(&p, 0, sizeof(p));
+  p.batch = batch;
+  p.heads = heads;
+  p.n = n;
+  p.d = d;
+  p.dtype = dtype;
+  p.C = n;
+  p.topk = topk;
+  return ca::carve_otop_workspace(p, nullptr, nullptr);
+}
+
+int oracle_top_attention_fwd(const void* q, const void* k, const void* v, const int32_t* lengths,
+                             int batch, int heads, int n, int d, int dtype, int topk, void* out,
+                             int32_t* topk_out, void* workspace, size_t workspace_bytes,
+                             void* stream) {
+  try {
+    if (topk < 1) return ca::fail(CA_ERR_INVALID_ARG, "topk must be >= 1 (got %d)", topk);
+    return ca::run_oracle_top(q, k, v, lengths, batch, heads, n, d, dtype, topk, out, topk_out,
+                              workspace, workspace_bytes, stream);
   } catch (...) {
     return ca::fail(CA_ERR_HIP, "unexpected C++ exception");
   }

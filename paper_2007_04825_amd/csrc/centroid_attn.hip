@@ -153,7 +153,11 @@ struct AttnArgs {
 };
 
 // MODE: 0 clustered single chunk, 1 improved single chunk, 2 clustered
-// partial, 3 improved partial.
+// partial, 3 improved partial, 4 oracle-top single chunk, 5 oracle-top
+// partial.  In the oracle-top modes the rows are the queries themselves
+// (row j = query j of the unit): the top-k search is the improved one, and
+// the fused mode writes each query's output from its T straight away (no
+// values phase); the partial mode stops after its candidates.
 //
 // Row statistics come from where the data already is: while the logits of a
 // key tile sit in the result registers of the first product, each lane (one
@@ -166,8 +170,9 @@ struct AttnArgs {
 // larger k take it from a sweep of the row).
 template <int D, typename T, int MODE>
 __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
-  constexpr bool IMPROVED = (MODE & 1) != 0;
-  constexpr bool FUSED = MODE < 2;
+  constexpr bool OTOP = MODE >= 4;
+  constexpr bool IMPROVED = (MODE & 1) != 0 || OTOP;
+  constexpr bool FUSED = MODE < 2 || MODE == 4;
   constexpr int KS = D / 4, DT = D / 16;
   constexpr int NW = kTileWaves;       // waves; wave w takes key tiles w, w + NW, ...
   constexpr int NS = NW * 4;           // slices per row: (wave, lane group)
@@ -187,6 +192,20 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
   if (wi >= a.nchunk * a.ntile * a.units) return;
   const int chunk = wi % a.nchunk, tile = (wi / a.nchunk) % a.ntile, u = wi / (a.nchunk * a.ntile);
   const int n = unit_length(a.lengths, u / a.heads, a.N);
+  if constexpr (OTOP) {
+    const int r0 = tile * 16;
+    if (r0 >= n) {  // rows past the sequence: zero output, no top-k set (the merge
+                    // writes them when there are several chunks)
+      if constexpr (FUSED) {
+        T* ou = static_cast<T*>(a.out) + (static_cast<size_t>(u) * a.N + r0) * D;
+        for (int x = threadIdx.x; x < 16 * D; x += kTileThreads)
+          if (r0 + x / D < a.C) store1(ou + x, 0.0f);
+        for (int x = threadIdx.x; x < 16 * a.topk; x += kTileThreads)
+          if (r0 + x / a.topk < a.C) a.topk_out[(static_cast<size_t>(u) * a.C + r0) * a.topk + x] = -1;
+      }
+      return;
+    }
+  }
   const int k0 = chunk * kChunk;
   if (k0 >= n) return;
   const int kn = min(kChunk, n - k0);
@@ -203,7 +222,8 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
   const __amdgpu_buffer_rsrc_t rv = make_rsrc(vu, static_cast<uint32_t>(kn) * D * ESZ);
 
   // ---- sizes (fused: the member offsets of the 16 clusters) -----------------------
-  if constexpr (FUSED) {
+  if constexpr (OTOP) {
+  } else if constexpr (FUSED) {
     const int32_t* ou = a.offsets + static_cast<size_t>(u) * (C + 1);
     if (tid < 17) moff[tid] = ou[min(j0 + tid, C)];
     __syncthreads();
@@ -219,7 +239,7 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
   // logits are no longer needed
   int mreg[kChunk / kTileThreads];
   int m0 = 0, mn = 0;
-  if constexpr (FUSED) {
+  if constexpr (FUSED && !OTOP) {
     m0 = moff[0];
     mn = moff[16] - m0;
     const int32_t* mg = a.members + static_cast<size_t>(u) * a.N + m0;
@@ -233,7 +253,12 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
   // ---- logits of this chunk, with the slice statistics -------------------------------
   {
     float bq[KS];
-    {
+    if constexpr (OTOP) {  // the query rows j0 .. j0 + 15 (rows past n read as 0)
+      const __amdgpu_buffer_rsrc_t rq =
+          make_rsrc(static_cast<const T*>(a.q) + (static_cast<size_t>(u) * a.N + j0) * D,
+                    static_cast<uint32_t>(min(16, n - j0)) * D * ESZ);
+      buf_load<KS>(rq, (c * D + g * KS) * ESZ, 0, bq, T{});
+    } else {
       const __amdgpu_buffer_rsrc_t rq =
           make_rsrc(a.qc + (static_cast<size_t>(u) * C + j0) * D, static_cast<uint32_t>(min(16, C - j0)) * D * 4);
       buf_load<KS>(rq, (c * D + g * KS) * 4, 0, bq, float{});
@@ -307,10 +332,10 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
     if constexpr (IMPROVED) {
       const int kk = min(a.topk, kn);
       const size_t uj = static_cast<size_t>(u) * C + (j < C ? j : 0);
-      const int jsize = j >= C ? 0 : FUSED ? moff[r + 1] - moff[r] : a.sizes[uj];
+      const int jsize = OTOP ? (j < n ? 1 : 0) : j >= C ? 0 : FUSED ? moff[r + 1] - moff[r] : a.sizes[uj];
       uint16_t* cand = tpos16[r];
       int cnt;
-      if (FUSED && a.topk_in != nullptr) {
+      if (FUSED && !OTOP && a.topk_in != nullptr) {
         // caller-supplied set: its entries up to the first negative or
         // out-of-range one, in the given order
         const int32_t* tin = a.topk_in + uj * a.topk;
@@ -357,7 +382,40 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
       float tsum = 0.0f;
       for (int x = c32; x < cnt; x += GL) tsum += __expf(row[cand[x]] - mx);
       tsum = grp_sum<GL>(tsum);
-      if constexpr (FUSED) {
+      if constexpr (OTOP && FUSED) {
+        // out_j = sum_{l in T} exp(s_l - m) v_l / sum_{l in T} exp(s_l - m), the
+        // row maximum m being in T; lane c32 takes dims c32 (and c32 + 32),
+        // eight value rows in flight
+        constexpr int DPL = D / GL;
+        const T* vrow = static_cast<const T*>(a.v) + static_cast<size_t>(u) * a.N * D;
+        float o[DPL];
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) o[e] = 0.0f;
+        for (int x0 = 0; x0 < cnt; x0 += 8) {
+          int pos[8];
+          float pv[8], vv[8][DPL];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) pos[e] = x0 + e < cnt ? cand[x0 + e] : -1;
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+#pragma unroll
+            for (int f = 0; f < DPL; ++f)
+              vv[e][f] = pos[e] >= 0 ? to_f32(vrow[static_cast<size_t>(pos[e]) * D + c32 + GL * f]) : 0.0f;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) pv[e] = pos[e] >= 0 ? __expf(row[pos[e]] - mx) : 0.0f;
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+#pragma unroll
+            for (int f = 0; f < DPL; ++f) o[f] = fmaf(pv[e], vv[e][f], o[f]);
+        }
+        const float inv = cnt > 0 ? 1.0f / tsum : 0.0f;
+        if (j < C) {
+          T* orow = static_cast<T*>(a.out) + (static_cast<size_t>(u) * a.N + j) * D;
+#pragma unroll
+          for (int f = 0; f < DPL; ++f) store1(orow + c32 + GL * f, o[f] * inv);
+          for (int x = c32; x < a.topk; x += GL) a.topk_out[uj * a.topk + x] = x < cnt ? cand[x] : -1;
+        }
+      } else if constexpr (FUSED) {
         // T masked out of the row so that P V gives the rest part
         wave_lds_sync();
         for (int x = c32; x < cnt; x += GL) row[cand[x]] = -INFINITY;
@@ -380,6 +438,7 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
     }
     if (c32 == 0) rowm[r] = mx;
   }
+  if constexpr (OTOP) return;  // outputs written, or candidates for the merge
   __syncthreads();
 
   // ---- values: O^T = V^T P^T (P = exp(S - m), T masked in the fused improved case)
@@ -500,9 +559,12 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Merge of the chunks (several chunks only).
+// Merge of the chunks (several chunks only).  OTOP (oracle-top, IMPROVED
+// set): row j is query j; its T comes from the chunks' candidates as in the
+// improved case, and the output row is the softmax over T of the candidates'
+// logits applied to the T rows of V.
 // ---------------------------------------------------------------------------
-template <int D, typename T, bool IMPROVED>
+template <int D, typename T, bool IMPROVED, bool OTOP = false>
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   __shared__ int cscr[4][2 * kCandCap];  // per-wave top-k scratch
   __shared__ int selout[4][128];
@@ -515,46 +577,52 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   const int j = (wi % a.ncg) * 4 + wave;
   if (j >= C) return;
   const size_t uj = static_cast<size_t>(u) * C + j;
-  const int sz = a.sizes[uj];
+  const int n = unit_length(a.lengths, u / a.heads, a.N);
+  const int sz = OTOP ? (j < n ? 1 : 0) : a.sizes[uj];
   if (sz == 0) {
-    for (int x = lane; x < D; x += 64) a.vcb[uj * D + x] = 0.0f;
+    if constexpr (OTOP) {  // padded row
+      T* orow = static_cast<T*>(a.out) + (static_cast<size_t>(u) * a.N + j) * D;
+      for (int x = lane; x < D; x += 64) store1(orow + x, 0.0f);
+    } else {
+      for (int x = lane; x < D; x += 64) a.vcb[uj * D + x] = 0.0f;
+    }
     if (IMPROVED) {
       for (int x = lane; x < a.topk; x += 64) a.topk_out[uj * a.topk + x] = -1;
-      if (lane == 0) a.mass[uj] = 0.0f;
+      if (!OTOP && lane == 0) a.mass[uj] = 0.0f;
     }
     return;
   }
-  const int n = unit_length(a.lengths, u / a.heads, a.N);
   const int nch = (n + kChunk - 1) / kChunk;
-  const float* pmj = a.pm + uj * a.nchunk;
-  const float* pzj = a.pz + uj * a.nchunk;
-  float M = -INFINITY;
-  for (int x = lane; x < nch; x += 64) M = fmaxf(M, pmj[x]);
-  M = wave_max(M);
-  float Z = 0.0f;
-  for (int x = lane; x < nch; x += 64) Z += pzj[x] * __expf(pmj[x] - M);
-  Z = wave_sum(Z);
-  if (lane == 0) {  // softmax statistics for the backward pass
-    a.stats[uj * 2] = M;
-    a.stats[uj * 2 + 1] = Z;
-  }
-  // V^c = sum_chunks exp(m_c - M) acc_c / Z   (lane -> dimension)
   constexpr int RPS = 64 / D;
   const int t = lane % D, r = lane / D;
-  float acc = 0.0f;
-  for (int x = r; x < nch; x += RPS) acc += __expf(pmj[x] - M) * a.pacc[(uj * a.nchunk + x) * D + t];
-  if (RPS == 2) acc += lane_xor32(acc);
-  const float vc = acc / Z;
-  if (!IMPROVED) {
-    if (lane < D) a.vcb[uj * D + t] = vc;
-    return;
+  float M = -INFINITY, Z = 0.0f;
+  if constexpr (!OTOP) {
+    const float* pmj = a.pm + uj * a.nchunk;
+    const float* pzj = a.pz + uj * a.nchunk;
+    for (int x = lane; x < nch; x += 64) M = fmaxf(M, pmj[x]);
+    M = wave_max(M);
+    for (int x = lane; x < nch; x += 64) Z += pzj[x] * __expf(pmj[x] - M);
+    Z = wave_sum(Z);
+    if (lane == 0) {  // softmax statistics for the backward pass
+      a.stats[uj * 2] = M;
+      a.stats[uj * 2 + 1] = Z;
+    }
+    // V^c = sum_chunks exp(m_c - M) acc_c / Z   (lane -> dimension)
+    float acc = 0.0f;
+    for (int x = r; x < nch; x += RPS) acc += __expf(pmj[x] - M) * a.pacc[(uj * a.nchunk + x) * D + t];
+    if (RPS == 2) acc += lane_xor32(acc);
+    const float vc = acc / Z;
+    if (!IMPROVED) {
+      if (lane < D) a.vcb[uj * D + t] = vc;
+      return;
+    }
+    if (lane < D) vcs[wave][t] = vc;
   }
-  if (lane < D) vcs[wave][t] = vc;
   const int kk = min(a.topk, n);
   const T* ku = static_cast<const T*>(a.k) + static_cast<size_t>(u) * a.N * D;
   const T* vu = static_cast<const T*>(a.v) + static_cast<size_t>(u) * a.N * D;
   int cnt;
-  if (a.topk_in != nullptr) {
+  if (!OTOP && a.topk_in != nullptr) {
     // caller-supplied set: entries until the first negative or out-of-range one;
     // their logits are recomputed
     const int32_t* tin = a.topk_in + uj * a.topk;
@@ -582,6 +650,12 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
     }
   }
   wave_lds_sync();
+  if constexpr (OTOP) {  // softmax over T alone
+    for (int x = lane; x < cnt; x += 64) M = fmaxf(M, selval[wave][x]);
+    M = wave_max(M);
+    for (int x = lane; x < cnt; x += 64) Z += __expf(selval[wave][x] - M);
+    Z = wave_sum(Z);
+  }
   // m_j and the top-k part of A^c V (eight value rows in flight per lane group)
   float msum = 0.0f;
   for (int x = lane; x < cnt; x += 64) msum += __expf(selval[wave][x] - M) / Z;
@@ -601,8 +675,12 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   for (; x < cnt; x += RPS)
     top += (__expf(selval[wave][x] - M) / Z) * to_f32(vu[static_cast<size_t>(selout[wave][x]) * D + t]);
   if (RPS == 2) top += lane_xor32(top);
-  if (lane < D) a.vcb[uj * D + t] = vcs[wave][t] - top;
   for (int y = lane; y < a.topk; y += 64) a.topk_out[uj * a.topk + y] = y < cnt ? selout[wave][y] : -1;
+  if constexpr (OTOP) {
+    if (lane < D) store1(static_cast<T*>(a.out) + (static_cast<size_t>(u) * a.N + j) * D + t, top);
+    return;
+  }
+  if (lane < D) a.vcb[uj * D + t] = vcs[wave][t] - top;
   if (lane == 0) a.mass[uj] = msum;
 }
 
@@ -880,6 +958,27 @@ static hipError_t launch_sparse_t(const Problem& p, const Workspace& ws, hipStre
     default: hipLaunchKernelGGL((sparse_kernel<D, T, 8>), g2, dim3(256), 0, s, a); break;
   }
   return hipGetLastError();
+}
+
+// Oracle-top: the improved top-k search on the query rows themselves (C = n
+// rows per unit), each output row from its own T.
+template <int D, typename T>
+static hipError_t launch_otop_t(const Problem& p, const Workspace& ws, hipStream_t s) {
+  const AttnArgs a = make_args(p, ws, nullptr);
+  const dim3 g1(xcd_grid(static_cast<long long>(a.nchunk) * a.ntile * a.units));
+  if (ws.nchunk == 1) {
+    hipLaunchKernelGGL((attn_tile_kernel<D, T, 4>), g1, dim3(kTileThreads), 0, s, a);
+    return hipGetLastError();
+  }
+  const dim3 g2(xcd_grid(static_cast<long long>(a.ncg) * a.units));
+  hipLaunchKernelGGL((attn_tile_kernel<D, T, 5>), g1, dim3(kTileThreads), 0, s, a);
+  hipLaunchKernelGGL((attn_merge_kernel<D, T, true, true>), g2, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_oracle_top(const Problem& p, const Workspace& ws, hipStream_t s) {
+  if (p.d == 32) return p.dtype == 0 ? launch_otop_t<32, float>(p, ws, s) : launch_otop_t<32, bf16_t>(p, ws, s);
+  return p.dtype == 0 ? launch_otop_t<64, float>(p, ws, s) : launch_otop_t<64, bf16_t>(p, ws, s);
 }
 
 // Centroid attention: softmax statistics, values (and, clustered in one key

@@ -57,6 +57,10 @@ __device__ __forceinline__ void load_row(const bf16_t* __restrict__ p, float* ds
   }
 }
 
+// Stores one fp32 value as the output element type.
+__device__ __forceinline__ void store1(float* p, float x) { *p = x; }
+__device__ __forceinline__ void store1(bf16_t* p, float x) { p->x = f32_to_bf16_bits(x); }
+
 // Stores 4 consecutive fp32 values (aligned) as the output element type.
 __device__ __forceinline__ void store4(float* p, float a, float b, float c, float d) {
   *reinterpret_cast<float4*>(p) = make_float4(a, b, c, d);

@@ -56,6 +56,12 @@ struct Workspace {
 
 // Carves the workspace; returns the bytes needed (ws may be null to only size it).
 size_t carve_workspace(const Problem& p, void* base, Workspace* ws);
+// Oracle-top (p.C = p.n, one row per query): carves topk [U][N][k] and, for
+// several key chunks, cand_idx and cand_val [U][N][nchunk][k]; the other
+// fields are null.
+size_t carve_otop_workspace(const Problem& p, void* base, Workspace* ws);
+// Oracle-top outputs and top-k sets (into ws.topk).
+hipError_t launch_oracle_top(const Problem& p, const Workspace& ws, hipStream_t s);
 
 // Hashing; also writes 0 to the output rows past each sequence's length.
 hipError_t launch_hash(const Problem& p, const Workspace& ws, hipStream_t s);

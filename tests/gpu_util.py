@@ -21,16 +21,18 @@ def to_dev(x, dtype):
 
 
 def run_gpu(w, topk, codes_in=None, assign_in=None, topk_in=None, lengths=True, C=None, L=None,
-            q=None):
-    """Runs the library on workload w.  topk = 0 -> clustered variant.
-    Returns a dict of numpy arrays (out as float64)."""
+            q=None, shared_qk=False):
+    """Runs the library on workload w.  topk = 0 -> clustered variant;
+    shared_qk passes the query buffer as the keys too.  Returns a dict of
+    numpy arrays (out as float64)."""
     import paper_2007_04825_amd as ca
     torch = torch_mod()
     C = w.C if C is None else C
     L = w.L if L is None else L
     qn = w.q if q is None else q
     B, H, N, D = qn.shape
-    qd, kd, vd = to_dev(qn, w.dtype), to_dev(w.k, w.dtype), to_dev(w.v, w.dtype)
+    qd, vd = to_dev(qn, w.dtype), to_dev(w.v, w.dtype)
+    kd = qd if shared_qk else to_dev(w.k, w.dtype)
     planes = torch.from_numpy(np.ascontiguousarray(w.planes)).cuda()
     lens = torch.from_numpy(w.lengths.astype(np.int32)).cuda() if lengths else None
     U = B * H
@@ -138,13 +140,13 @@ def band_masks(w):
     return masks
 
 
-def check_end_to_end(w, topk):
+def check_end_to_end(w, topk, shared_qk=False):
     """Whole forward on the GPU against the oracle on the same inputs: codes,
     assignments, sizes and centroids exactly (centroids to fp32 rounding), top-k
     sets up to near ties, masses, and outputs within the dtype's tolerance
     (rows of clusters with a near-tie top-k difference are left out)."""
     ref = run_oracle(w, topk)
-    got = run_gpu(w, topk)
+    got = run_gpu(w, topk, shared_qk=shared_qk)
     vm = valid_mask(w)
     band = band_masks(w)
     print("band bits: %d" % sum(bin(int(x)).count("1") for x in band[band != 0]))
@@ -153,7 +155,7 @@ def check_end_to_end(w, topk):
     if not np.array_equal(got["codes"], ref["codes"]):
         # a bit inside the band differs: the later stages are compared on the
         # oracle's codes
-        got = run_gpu(w, topk, codes_in=ref["codes"])
+        got = run_gpu(w, topk, codes_in=ref["codes"], shared_qk=shared_qk)
     assert np.array_equal(got["assign"], ref["assign"]), "assignments differ"
     assert np.array_equal(got["sizes"], ref["sizes"]), "cluster sizes differ"
     np.testing.assert_allclose(got["centroids"], ref["qc"], rtol=0, atol=2e-6)

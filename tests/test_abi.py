@@ -82,3 +82,38 @@ def test_kmeans_path_switch_validation():
     lib = ca.library()
     assert lib.ca_set_kmeans_path(3) == ca.CA_ERR_INVALID_ARG
     assert lib.ca_set_kmeans_path(0) == ca.CA_OK
+
+
+def test_oracle_top_workspace_bytes():
+    one = ca.oracle_top_workspace_bytes(1, 1, 1024, 32, ca.CA_F32, 32)
+    assert one >= 1024 * 32 * 4
+    # several key chunks add the per-chunk candidate lists
+    two = ca.oracle_top_workspace_bytes(1, 1, 2048, 32, ca.CA_F32, 32)
+    assert two >= 2048 * 32 * 4 + 2 * 2048 * 2 * 32 * 4
+    for bad in [(0, 1, 64, 32, 0, 8), (1, 1, 64, 16, 0, 8), (1, 1, 64, 32, 0, 0),
+                (1, 1, 64, 32, 0, 200), (1, 1, 64, 32, 3, 8)]:
+        assert ca.oracle_top_workspace_bytes(*bad) == 0, bad
+
+
+@pytest.mark.parametrize("args,code", [
+    (dict(batch=0), ca.CA_ERR_INVALID_ARG),
+    (dict(d=16), ca.CA_ERR_UNSUPPORTED),
+    (dict(dtype=5), ca.CA_ERR_INVALID_ARG),
+    (dict(topk=0), ca.CA_ERR_INVALID_ARG),
+    (dict(topk=200), ca.CA_ERR_UNSUPPORTED),
+    (dict(v=None), ca.CA_ERR_INVALID_ARG),
+    (dict(out=None), ca.CA_ERR_INVALID_ARG),
+    (dict(ws=None), ca.CA_ERR_WORKSPACE),
+    (dict(ws_bytes=16), ca.CA_ERR_WORKSPACE),
+    (dict(ws=0x1001), ca.CA_ERR_WORKSPACE),
+])
+def test_oracle_top_invalid_arguments_rejected_on_host(args, code):
+    """Validation runs before any HIP call; the dummy addresses are never used."""
+    p = dict(q=0x1000, k=0x1000, v=0x1000, lengths=None, batch=1, heads=2, n=64, d=32, dtype=0,
+             topk=4, out=0x1000, topk_out=None, ws=0x10000, ws_bytes=16 << 20)
+    p.update(args)
+    rc = ca.oracle_top_attention_fwd(p["q"], p["k"], p["v"], p["lengths"], p["batch"], p["heads"],
+                                     p["n"], p["d"], p["dtype"], p["topk"], p["out"], p["topk_out"],
+                                     p["ws"], p["ws_bytes"])
+    assert rc == code
+    assert len(ca.library().ca_last_error()) > 0
