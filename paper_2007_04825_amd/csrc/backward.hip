@@ -31,11 +31,13 @@
 //     accumulate in registers, dQ^c leaves one partial per key block.
 //   bwd_dqc_reduce_kernel, bwd_dq_kernel: dQ^c over the key blocks in order,
 //     then dQ_i.
-//   improved only: the partial key/value gradients of the T rows reach dK and
-//     dV through an inverse index (key -> entries (j, r) with T_j[r] = key)
-//     built by bwd_index_kernel; bwd_index_gather_kernel adds each key's
-//     entries as 64-bit fixed-point integers, whose sum does not depend on
-//     the order.  No floating-point atomics: the result is deterministic.
+//   improved only: bwd_index_kernel (first) gives every entry (j, r) of the
+//     top-k sets a slot in a per-unit list ordered by key; bwd_sparse_kernel
+//     writes the partial key/value gradient row of the entry into that slot,
+//     so each key's partials lie together, and bwd_index_gather_kernel adds
+//     them into dK and dV as 64-bit fixed-point integers, whose sum does not
+//     depend on the order of the slots.  No floating-point atomics: the
+//     result is deterministic.
 #include <limits.h>
 #include <math.h>
 
@@ -73,12 +75,11 @@ struct BwdArgs {
   float* dm;        // [U][C]
   float* dqc_part;  // [U][nkb][C][D]
   float* dqc;       // [U][C][D]
-  float* part_k;    // [U][C][topk][D]
-  float* part_v;    // [U][C][topk][D]
+  float* part_k;    // [U][C * topk][D] rows in key order: slot epos[j * topk + r]
+  float* part_v;    // [U][C * topk][D]
   int32_t* icnt;    // [U][N]  entries per key
-  int32_t* ioff;    // [U][N]  first entry of each key within its key range's list
-  int32_t* ilist;   // [U][nrange][C * topk] entry numbers j * topk + r
-  int nrange;       // key ranges of kIdxKeys keys per unit
+  int32_t* ioff;    // [U][N]  first slot of each key (the unit's entries in key order)
+  int32_t* epos;    // [U][C * topk] slot of entry (j, r) with T_j[r] = key
   float* dq;
   float* dk;
   float* dv;
@@ -150,6 +151,7 @@ struct SparseBwdShared {
   float wt[KP][17];
   float gtt[KP][17];
   int tp[KP];
+  int ep[KP];  // slots of the partial rows
 };
 
 template <int D, typename T, int NKT>
@@ -180,7 +182,10 @@ __global__ __launch_bounds__(64) void bwd_sparse_kernel(BwdArgs a) {
   for (int x0 = 0; x0 < KP; x0 += 64) {
     const int x = x0 + lane;
     const int key = x < a.topk ? a.tsets[uj * a.topk + x] : -1;
-    if (x < KP) sh.tp[x] = key;
+    if (x < KP) {
+      sh.tp[x] = key;
+      sh.ep[x] = key >= 0 ? a.epos[uj * a.topk + x] : 0;
+    }
     kk += __popcll(__ballot(key >= 0));
   }
   const int nkt = (kk + 15) >> 4;
@@ -370,12 +375,16 @@ __global__ __launch_bounds__(64) void bwd_sparse_kernel(BwdArgs a) {
     a.dm[uj] = dmj;
     a.delta[uj] = mh * dmj + gvb;
   }
-  // partial key and value gradients of the T rows
-  float* pk = a.part_k + uj * a.topk * D;
-  float* pv = a.part_v + uj * a.topk * D;
-  for (int x = lane; x < kk * D; x += 64) {
-    pk[x] = sh.acck[x / D][x % D] * a.scale;
-    pv[x] = sh.accv[x / D][x % D];
+  // partial key and value gradients of the T rows, each into its key's slot
+  float* pk = a.part_k + static_cast<size_t>(u) * C * a.topk * D;
+  float* pv = a.part_v + static_cast<size_t>(u) * C * a.topk * D;
+  constexpr int LPR = D / 4;  // lanes per row, four dims each
+  for (int x = lane; x < kk * LPR; x += 64) {
+    const int r = x / LPR, c4 = (x % LPR) * 4;
+    const size_t at = static_cast<size_t>(sh.ep[r]) * D + c4;
+    const float4 k4 = *reinterpret_cast<const float4*>(&sh.acck[r][c4]);
+    *reinterpret_cast<float4*>(pk + at) = make_float4(k4.x * a.scale, k4.y * a.scale, k4.z * a.scale, k4.w * a.scale);
+    *reinterpret_cast<float4*>(pv + at) = *reinterpret_cast<const float4*>(&sh.accv[r][c4]);
   }
 }
 
@@ -602,65 +611,73 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(BwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Inverse index of the top-k sets (improved): one workgroup per (unit, range
-// of kIdxKeys keys).  Counts per key (LDS atomics, order-free), an exclusive
-// prefix sum, then every entry takes a slot of its key.
+// Inverse index of the top-k sets (improved): one workgroup per unit walks
+// its keys in ranges of kIdxKeys.  Per range: counts per key (LDS atomics,
+// order-free), an exclusive prefix sum continuing the previous ranges' total,
+// then every entry takes a slot of its key.  The slots of one key are
+// consecutive; their order among the key's entries is not fixed (the
+// gather's sum does not depend on it).
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(1024) void bwd_index_kernel(BwdArgs a) {
   __shared__ int cnt[kIdxKeys];
   __shared__ int off[kIdxKeys];
   __shared__ int wsum[16];
-  const int u = blockIdx.x / a.nrange, range = blockIdx.x % a.nrange;
+  const int u = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n = unit_length(a.lengths, u / a.heads, a.N);
-  const int lo = range * kIdxKeys, hi = min(n, lo + kIdxKeys);
-  if (lo >= hi) return;
   const int C = a.C, K = a.topk;
   const int32_t* ts = a.tsets + static_cast<size_t>(u) * C * K;
   const int32_t* sz = a.sizes + static_cast<size_t>(u) * C;
-  for (int x = tid; x < kIdxKeys; x += 1024) cnt[x] = 0;
-  __syncthreads();
-  for (int x = tid; x < C * K; x += 1024) {
-    if (sz[x / K] == 0) continue;  // no list for an empty cluster
-    const int key = ts[x];
-    if (key >= lo && key < hi) atomicAdd(&cnt[key - lo], 1);
-  }
-  __syncthreads();
-  // exclusive prefix sum of cnt[0 .. hi - lo), 8 keys per thread
-  const int m = hi - lo;
-  int local[kIdxKeys / 1024], tot = 0;
-#pragma unroll
-  for (int e = 0; e < kIdxKeys / 1024; ++e) {
-    const int x = tid * (kIdxKeys / 1024) + e;
-    local[e] = x < m ? cnt[x] : 0;
-    tot += local[e];
-  }
-  const int incl = wave_incl_scan(tot);
-  if (lane == 63) wsum[wave] = incl;
-  __syncthreads();
-  int run = incl - tot;
-  for (int w = 0; w < wave; ++w) run += wsum[w];
   int32_t* icu = a.icnt + static_cast<size_t>(u) * a.N;
   int32_t* iou = a.ioff + static_cast<size_t>(u) * a.N;
-#pragma unroll
-  for (int e = 0; e < kIdxKeys / 1024; ++e) {
-    const int x = tid * (kIdxKeys / 1024) + e;
-    if (x < m) {
-      off[x] = run;
-      icu[lo + x] = local[e];
-      iou[lo + x] = run;
-      cnt[x] = 0;  // now the fill cursor
+  int32_t* ep = a.epos + static_cast<size_t>(u) * C * K;
+  int base = 0;  // slots taken by the earlier ranges
+  for (int lo = 0; lo < n; lo += kIdxKeys) {
+    const int hi = min(n, lo + kIdxKeys);
+    for (int x = tid; x < kIdxKeys; x += 1024) cnt[x] = 0;
+    __syncthreads();
+    for (int x = tid; x < C * K; x += 1024) {
+      if (sz[x / K] == 0) continue;  // no list for an empty cluster
+      const int key = ts[x];
+      if (key >= lo && key < hi) atomicAdd(&cnt[key - lo], 1);
     }
-    run += local[e];
-  }
-  __syncthreads();
-  // each entry takes a slot of its key, in no particular order (the gather's
-  // sum does not depend on it)
-  int32_t* L = a.ilist + (static_cast<size_t>(u) * a.nrange + range) * C * K;
-  for (int x = tid; x < C * K; x += 1024) {
-    if (sz[x / K] == 0) continue;
-    const int key = ts[x];
-    if (key >= lo && key < hi) L[off[key - lo] + atomicAdd(&cnt[key - lo], 1)] = x;
+    __syncthreads();
+    // exclusive prefix sum of cnt[0 .. hi - lo), 8 keys per thread
+    const int m = hi - lo;
+    int local[kIdxKeys / 1024], tot = 0;
+#pragma unroll
+    for (int e = 0; e < kIdxKeys / 1024; ++e) {
+      const int x = tid * (kIdxKeys / 1024) + e;
+      local[e] = x < m ? cnt[x] : 0;
+      tot += local[e];
+    }
+    const int incl = wave_incl_scan(tot);
+    if (lane == 63) wsum[wave] = incl;
+    __syncthreads();
+    int run = base + incl - tot, total = 0;
+    for (int w = 0; w < 16; ++w) {
+      if (w < wave) run += wsum[w];
+      total += wsum[w];
+    }
+#pragma unroll
+    for (int e = 0; e < kIdxKeys / 1024; ++e) {
+      const int x = tid * (kIdxKeys / 1024) + e;
+      if (x < m) {
+        off[x] = run;
+        icu[lo + x] = local[e];
+        iou[lo + x] = run;
+        cnt[x] = 0;  // now the fill cursor
+      }
+      run += local[e];
+    }
+    __syncthreads();
+    for (int x = tid; x < C * K; x += 1024) {
+      if (sz[x / K] == 0) continue;
+      const int key = ts[x];
+      if (key >= lo && key < hi) ep[x] = off[key - lo] + atomicAdd(&cnt[key - lo], 1);
+    }
+    base += total;
+    __syncthreads();  // before the next range clears the tables
   }
 }
 
@@ -688,21 +705,19 @@ __global__ __launch_bounds__(256) void bwd_index_gather_kernel(BwdArgs a) {
   if (key >= n) return;
   const int cnt = a.icnt[ul];
   if (cnt == 0) return;
-  const size_t per = static_cast<size_t>(a.C) * a.topk;
-  const int32_t* L = a.ilist + (static_cast<size_t>(u) * a.nrange + key / kIdxKeys) * per + a.ioff[ul];
-  const float4* pk = reinterpret_cast<const float4*>(a.part_k + static_cast<size_t>(u) * per * D);
-  const float4* pv = reinterpret_cast<const float4*>(a.part_v + static_cast<size_t>(u) * per * D);
+  // the key's partial rows are the consecutive slots ioff .. ioff + cnt - 1
+  const size_t first = static_cast<size_t>(u) * a.C * a.topk + a.ioff[ul];
+  const float4* pk = reinterpret_cast<const float4*>(a.part_k) + first * Q4 + part;
+  const float4* pv = reinterpret_cast<const float4*>(a.part_v) + first * Q4 + part;
   long long ak[4] = {0, 0, 0, 0}, av[4] = {0, 0, 0, 0};
-  constexpr int B = 8;  // entries in flight
+  constexpr int B = 4;  // entries in flight (consecutive rows)
   for (int t0 = 0; t0 < cnt; t0 += B) {
-    int e[B];
-#pragma unroll
-    for (int t = 0; t < B; ++t) e[t] = t0 + t < cnt ? L[t0 + t] : -1;
     float4 k4[B], v4[B];
 #pragma unroll
     for (int t = 0; t < B; ++t) {
-      k4[t] = e[t] >= 0 ? pk[static_cast<size_t>(e[t]) * Q4 + part] : make_float4(0.f, 0.f, 0.f, 0.f);
-      v4[t] = e[t] >= 0 ? pv[static_cast<size_t>(e[t]) * Q4 + part] : make_float4(0.f, 0.f, 0.f, 0.f);
+      const bool ok = t0 + t < cnt;
+      k4[t] = ok ? pk[static_cast<size_t>(t0 + t) * Q4] : make_float4(0.f, 0.f, 0.f, 0.f);
+      v4[t] = ok ? pv[static_cast<size_t>(t0 + t) * Q4] : make_float4(0.f, 0.f, 0.f, 0.f);
     }
 #pragma unroll
     for (int t = 0; t < B; ++t) {
@@ -732,7 +747,6 @@ __global__ __launch_bounds__(256) void bwd_index_gather_kernel(BwdArgs a) {
 // Host side.
 // ---------------------------------------------------------------------------
 int bwd_key_blocks(int n) { return (n + kBwdKeys - 1) / kBwdKeys; }
-int bwd_key_ranges(int n) { return (n + kIdxKeys - 1) / kIdxKeys; }
 
 static int sparse_bwd_tiles(int topk) { return topk <= 16 ? 1 : topk <= 32 ? 2 : topk <= 64 ? 4 : 8; }
 
@@ -769,8 +783,7 @@ static hipError_t launch_backward_t(const BwdProblem& p, hipStream_t s, hipEvent
   a.part_v = p.bws.part_v;
   a.icnt = p.bws.icnt;
   a.ioff = p.bws.ioff;
-  a.ilist = p.bws.ilist;
-  a.nrange = bwd_key_ranges(p.n);
+  a.epos = p.bws.epos;
   a.dq = p.dq;
   a.dk = p.dk;
   a.dv = p.dv;
@@ -779,7 +792,7 @@ static hipError_t launch_backward_t(const BwdProblem& p, hipStream_t s, hipEvent
   auto blocks = [](long long count) { return dim3(static_cast<unsigned>((count + 255) / 256)); };
   hipError_t e;
   if (improved) {
-    hipLaunchKernelGGL(bwd_index_kernel, dim3(static_cast<unsigned>(U * a.nrange)), dim3(1024), 0, s, a);
+    hipLaunchKernelGGL(bwd_index_kernel, dim3(static_cast<unsigned>(U)), dim3(1024), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const dim3 gs(xcd_grid(static_cast<long long>(p.C) * U));
     switch (sparse_bwd_tiles(p.topk)) {

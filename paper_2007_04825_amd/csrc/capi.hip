@@ -97,10 +97,9 @@ size_t carve_bwd_workspace(const BwdProblem& p, void* base, BwdWorkspace* ws) {
   w.dqc = static_cast<float*>(take(U * C * D * 4));
   w.part_k = static_cast<float*>(take(improved ? U * C * K * D * 4 : 0));
   w.part_v = static_cast<float*>(take(improved ? U * C * K * D * 4 : 0));
-  const size_t nrange = static_cast<size_t>(bwd_key_ranges(p.n));
   w.icnt = static_cast<int32_t*>(take(improved ? U * N * 4 : 0));
   w.ioff = static_cast<int32_t*>(take(improved ? U * N * 4 : 0));
-  w.ilist = static_cast<int32_t*>(take(improved ? U * nrange * C * K * 4 : 0));
+  w.epos = static_cast<int32_t*>(take(improved ? U * C * K * 4 : 0));
   if (ws) *ws = w;
   return off;
 }

@@ -95,11 +95,11 @@ struct BwdWorkspace {
   float* dm;        // [U][C]      gradient of the mass (improved)
   float* dqc_part;  // [U][nkb][C][d] centroid-gradient partials per key block
   float* dqc;       // [U][C][d]
-  float* part_k;    // [U][C][k][d] key-gradient partials of the top-k rows (improved)
-  float* part_v;    // [U][C][k][d]
+  float* part_k;    // [U][C*k][d] key-gradient partials of the top-k rows (improved), key order
+  float* part_v;    // [U][C*k][d]
   int32_t* icnt;    // [U][n]      inverse index of the top-k sets: entries per key
-  int32_t* ioff;    // [U][n]      first entry of each key in its key range's list
-  int32_t* ilist;   // [U][nrange][C*k] entries j*k + r
+  int32_t* ioff;    // [U][n]      first slot of each key in the unit's key-ordered list
+  int32_t* epos;    // [U][C*k]    slot of entry (j, r)
 };
 struct BwdProblem {
   int batch, heads, n, d, dtype, C, topk;  // topk = 0 for the clustered variant
@@ -115,7 +115,6 @@ struct BwdProblem {
   float* dv;
 };
 int bwd_key_blocks(int n);
-int bwd_key_ranges(int n);
 size_t carve_bwd_workspace(const BwdProblem& p, void* base, BwdWorkspace* ws);
 // ev_start / ev_stop (may be null) are recorded around bwd_tile_kernel.
 hipError_t launch_backward(const BwdProblem& p, hipStream_t s, hipEvent_t ev_start, hipEvent_t ev_stop);
