@@ -152,9 +152,9 @@ struct AttnArgs {
   void* out;
 };
 
-// MODE: 0 clustered single chunk, 1 improved single chunk, 2 clustered
-// partial, 3 improved partial, 4 oracle-top single chunk, 5 oracle-top
-// partial.  In the oracle-top modes the rows are the queries themselves
+// MODE: 1 improved single chunk, 2 clustered partial, 3 improved partial,
+// 4 oracle-top single chunk, 5 oracle-top partial (the clustered variant in
+// a single chunk is attn_flash_kernel).  In the oracle-top modes the rows are the queries themselves
 // (row j = query j of the unit): the top-k search is the improved one, and
 // the fused mode writes each query's output from its T straight away (no
 // values phase); the partial mode stops after its candidates.
@@ -170,6 +170,7 @@ struct AttnArgs {
 // larger k take it from a sweep of the row).
 template <int D, typename T, int MODE>
 __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
+  static_assert(MODE >= 1 && MODE <= 5, "mode");
   constexpr bool OTOP = MODE >= 4;
   constexpr bool IMPROVED = (MODE & 1) != 0 || OTOP;
   constexpr bool FUSED = MODE < 2 || MODE == 4;
@@ -234,20 +235,6 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
     if (tid < 16 && j0 + tid < C && a.sizes[static_cast<size_t>(u) * C + j0 + tid] > 0) any_nonempty = 1;
     __syncthreads();
     if (!any_nonempty) return;
-  }
-  // member lists are requested now and stored (in the logit area) once the
-  // logits are no longer needed
-  int mreg[kChunk / kTileThreads];
-  int m0 = 0, mn = 0;
-  if constexpr (FUSED && !OTOP) {
-    m0 = moff[0];
-    mn = moff[16] - m0;
-    const int32_t* mg = a.members + static_cast<size_t>(u) * a.N + m0;
-#pragma unroll
-    for (int e = 0; e < kChunk / kTileThreads; ++e) {
-      const int x = tid + kTileThreads * e;
-      mreg[e] = x < mn ? mg[x] : 0;
-    }
   }
 
   // ---- logits of this chunk, with the slice statistics -------------------------------
@@ -480,17 +467,8 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
   psum = cross_rows_sum(psum);
   if (g == 0) zpart[wave][c] = psum;
   __syncthreads();  // logits are dead from here on: reuse them
-  float* red = logits;                 // [NW waves][16 centroids][D]
-  float* vhat = logits + NW * 16 * D;  // [16][D]
-  int* mlist = reinterpret_cast<int*>(logits + (NW + 1) * 16 * D);  // member lists of the 16 clusters
-  static_assert((NW + 1) * 16 * D + kChunk <= 16 * kLStride, "logit area reuse");
-  if constexpr (FUSED) {
-#pragma unroll
-    for (int e = 0; e < kChunk / kTileThreads; ++e) {
-      const int x = tid + kTileThreads * e;
-      if (x < mn) mlist[x] = mreg[e];
-    }
-  }
+  float* red = logits;  // [NW waves][16 centroids][D]
+  static_assert(NW * 16 * D <= 16 * kLStride, "logit area reuse");
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -510,7 +488,6 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
     if constexpr (FUSED) {
       const bool nonempty = moff[cc + 1] > moff[cc];
       const float val = nonempty ? sum / z : 0.0f;
-      vhat[cc * D + dim] = val;
       a.vcb[ujc * D + dim] = val;
       if (dim == 0) {  // softmax statistics for the backward pass
         a.stats[ujc * 2] = rowm[cc];
@@ -530,30 +507,173 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
       }
     }
   }
-  if constexpr (FUSED && !IMPROVED) {
-    __syncthreads();
+}
 
-    // ---- fused outputs (clustered): every member row of the 16 clusters ----------
-    const T* qu = static_cast<const T*>(a.q) + static_cast<size_t>(u) * a.N * D;
-    T* ou = static_cast<T*>(a.out) + static_cast<size_t>(u) * a.N * D;
-    constexpr int RPW = 16 / NW;  // clusters per wave
-    {
-      for (int rr = 0; rr < RPW; ++rr) {
-        const int r = wave * RPW + rr;
-        const int j = j0 + r;
-        if (j >= C) break;
-        const int sz = moff[r + 1] - moff[r];
-        if (sz == 0) continue;
-        const int* mem = mlist + (moff[r] - m0);
-        // Eq. (6): each member row receives V^c_j; a lane writes 4 dims of a row
-        constexpr int LPR = D / 4, RPS = 64 / LPR;
-        const int part = lane % LPR, sub = lane / LPR;
-        const float4 val = *reinterpret_cast<const float4*>(&vhat[r * D + part * 4]);
-        for (int m1 = sub; m1 < sz; m1 += RPS) {
-          const int qrow = mem[m1];
-          store4(ou + static_cast<size_t>(qrow) * D + part * 4, val.x, val.y, val.z, val.w);
-        }
-      }
+// ---------------------------------------------------------------------------
+// Clustered centroid attention over one key chunk in a single pass (Eqs. 4-6):
+// the centroid logits never leave the registers.  Wave w takes key tiles
+// w, w + kFlashWaves, ...; for each tile the logits S^T = K Q^c^T come from
+// the fp32 matrix cores in the layout that the second product wants for P^T,
+// so each lane keeps, for its centroid column, a running maximum m, the sum z
+// of exp(s - m) over its keys and the partial O^T = V^T P^T, both rescaled by
+// exp(m_old - m_new) when the maximum grows.  The waves' (m, z, O) are merged
+// in LDS (log-sum-exp), which gives V^c_j and the softmax statistics; then
+// every member row receives V^c_j (Eq. 6).
+// ---------------------------------------------------------------------------
+constexpr int kFlashWaves = 8;
+constexpr int kFlashThreads = 64 * kFlashWaves;
+
+template <int D, typename T>
+__global__ __launch_bounds__(kFlashThreads) void attn_flash_kernel(AttnArgs a) {
+  constexpr int KS = D / 4, DT = D / 16, NW = kFlashWaves;
+  constexpr uint32_t ESZ = sizeof(T);
+  __shared__ float red[NW][16][D + 1];  // per-wave O^T partials, [wave][centroid][dim]
+  __shared__ float wm[NW][16], wz[NW][16];
+  __shared__ __align__(16) float vhat[16][D];
+  __shared__ int moff[17];
+  __shared__ int mlist[kChunk];
+
+  const int wi = xcd_work_item();  // tile fastest, then (batch, head)
+  if (wi >= a.ntile * a.units) return;
+  const int tile = wi % a.ntile, u = wi / a.ntile;
+  const int n = unit_length(a.lengths, u / a.heads, a.N);
+  const int C = a.C;
+  const int j0 = tile * 16;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int c = lane & 15, g = lane >> 4;
+  const int32_t* ou = a.offsets + static_cast<size_t>(u) * (C + 1);
+  if (tid < 17) moff[tid] = ou[min(j0 + tid, C)];
+  __syncthreads();
+  if (moff[16] == moff[0] || n == 0) return;  // every cluster of the tile is empty
+  const int m0 = moff[0], mn = moff[16] - m0;
+  // the member lists are requested now and stored once the products are done
+  constexpr int MPT = kChunk / kFlashThreads;
+  int mreg[MPT];
+  {
+    const int32_t* mg = a.members + static_cast<size_t>(u) * a.N + m0;
+#pragma unroll
+    for (int e = 0; e < MPT; ++e) {
+      const int x = tid + kFlashThreads * e;
+      mreg[e] = x < mn ? mg[x] : 0;
+    }
+  }
+  const T* ku = static_cast<const T*>(a.k) + static_cast<size_t>(u) * a.N * D;
+  const T* vu = static_cast<const T*>(a.v) + static_cast<size_t>(u) * a.N * D;
+  const __amdgpu_buffer_rsrc_t rk = make_rsrc(ku, static_cast<uint32_t>(n) * D * ESZ);
+  const __amdgpu_buffer_rsrc_t rv = make_rsrc(vu, static_cast<uint32_t>(n) * D * ESZ);
+  const int nkt = (n + 15) / 16;
+  float bq[KS];
+  {
+    const __amdgpu_buffer_rsrc_t rq =
+        make_rsrc(a.qc + (static_cast<size_t>(u) * C + j0) * D, static_cast<uint32_t>(min(16, C - j0)) * D * 4);
+    buf_load<KS>(rq, (c * D + g * KS) * 4, 0, bq, float{});
+  }
+  float mrun = -INFINITY, zl = 0.0f;
+  v4f oacc[DT];
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt) oacc[dt] = v4f{0.f, 0.f, 0.f, 0.f};
+  // software pipeline over this wave's key tiles kt = wave, wave + NW, ...:
+  // PD tiles are requested ahead of the one in the products, in PD + 1
+  // register buffers used in turn (the loop is unrolled so that no buffer is
+  // copied); every load is issued, rows past n reading as 0, so that the
+  // compiler counts them and each tile waits only for its own rows
+  constexpr int PD = 1;
+  float kbuf[PD + 1][KS], vbuf[PD + 1][4][DT];
+  auto load_tile = [&](int kt, float* kx, float (*vx)[DT]) {
+    buf_load<KS>(rk, ((kt * 16 + c) * D + g * KS) * ESZ, 0, kx, T{});
+    const uint32_t voff = ((kt * 16 + 4 * g) * D + DT * c) * ESZ;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) buf_load<DT>(rv, voff, i * D * ESZ, vx[i], T{});
+  };
+  auto step = [&](int kt, const float* kx, const float (*vx)[DT]) {
+    v4f acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < KS; ++s) acc = mfma_f32_16x16x4(kx[s], bq[s], acc);
+    float o[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) o[i] = (kt * 16 + 4 * g + i < n) ? acc[i] * a.scale : -INFINITY;
+    // key kt * 16 is valid, so the tile maximum of every column is finite
+    const float tmax = cross_rows_max(fmaxf(fmaxf(o[0], o[1]), fmaxf(o[2], o[3])));
+    const float mnew = fmaxf(mrun, tmax);
+    const float alpha = __expf(mrun - mnew);  // 0 on the first tile
+    mrun = mnew;
+    float p[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) p[i] = __expf(o[i] - mnew);
+    zl = zl * alpha + ((p[0] + p[1]) + (p[2] + p[3]));
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) oacc[dt][r] *= alpha;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) oacc[dt] = mfma_f32_16x16x4(vx[i][dt], p[i], oacc[dt]);
+  };
+#pragma unroll
+  for (int e = 0; e < PD; ++e) load_tile(wave + NW * e, kbuf[e], vbuf[e]);
+  for (int kt0 = wave; kt0 < nkt; kt0 += (PD + 1) * NW) {
+#pragma unroll
+    for (int e = 0; e <= PD; ++e) {
+      const int kt = kt0 + NW * e;
+      // the buffer of the tile PD ahead is the one that the previous step freed
+      load_tile(kt + NW * PD, kbuf[(e + PD) % (PD + 1)], vbuf[(e + PD) % (PD + 1)]);
+      if (kt < nkt) step(kt, kbuf[e], vbuf[e]);
+    }
+  }
+  const float zc = cross_rows_sum(zl);
+  if (g == 0) {
+    wm[wave][c] = mrun;
+    wz[wave][c] = zc;
+  }
+#pragma unroll
+  for (int r = 0; r < 4; ++r)
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) red[wave][c][DT * (4 * g + r) + dt] = oacc[dt][r];
+#pragma unroll
+  for (int e = 0; e < MPT; ++e) {
+    const int x = tid + kFlashThreads * e;
+    if (x < mn) mlist[x] = mreg[e];
+  }
+  __syncthreads();
+  for (int x = tid; x < 16 * D; x += kFlashThreads) {
+    const int cc = x / D, dim = x % D;
+    float M = wm[0][cc];
+#pragma unroll
+    for (int w = 1; w < NW; ++w) M = fmaxf(M, wm[w][cc]);
+    float Z = 0.0f, O = 0.0f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      const float f = __expf(wm[w][cc] - M);  // 0 for a wave without keys
+      Z += f * wz[w][cc];
+      O += f * red[w][cc][dim];
+    }
+    if (j0 + cc >= C) continue;
+    const size_t ujc = static_cast<size_t>(u) * C + j0 + cc;
+    const bool nonempty = moff[cc + 1] > moff[cc];
+    const float val = nonempty ? O / Z : 0.0f;
+    vhat[cc][dim] = val;
+    a.vcb[ujc * D + dim] = val;
+    if (dim == 0) {  // softmax statistics for the backward pass
+      a.stats[ujc * 2] = M;
+      a.stats[ujc * 2 + 1] = Z;
+    }
+  }
+  __syncthreads();
+  // Eq. (6): each member row receives V^c_j; a lane writes 4 dims of a row
+  T* out = static_cast<T*>(a.out) + static_cast<size_t>(u) * a.N * D;
+  constexpr int RPW = 16 / NW;  // clusters per wave
+  constexpr int LPR = D / 4, RPS = 64 / LPR;
+  const int part = lane % LPR, sub = lane / LPR;
+  for (int rr = 0; rr < RPW; ++rr) {
+    const int r = wave * RPW + rr;
+    if (j0 + r >= C) break;
+    const int sz = moff[r + 1] - moff[r];
+    const int* mem = mlist + (moff[r] - m0);
+    const float4 val = *reinterpret_cast<const float4*>(&vhat[r][part * 4]);
+    for (int m1 = sub; m1 < sz; m1 += RPS) {
+      const int qrow = mem[m1];
+      store4(out + static_cast<size_t>(qrow) * D + part * 4, val.x, val.y, val.z, val.w);
     }
   }
 }
@@ -931,7 +1051,7 @@ static hipError_t launch_attn_t(const Problem& p, const Workspace& ws, const int
     if (improved)
       hipLaunchKernelGGL((attn_tile_kernel<D, T, 1>), g1, dim3(kTileThreads), 0, s, a);
     else
-      hipLaunchKernelGGL((attn_tile_kernel<D, T, 0>), g1, dim3(kTileThreads), 0, s, a);
+      hipLaunchKernelGGL((attn_flash_kernel<D, T>), g1, dim3(kFlashThreads), 0, s, a);
     return hipGetLastError();
   }
   if (improved) {
