@@ -572,53 +572,124 @@ __global__ __launch_bounds__(kFlashThreads) void attn_flash_kernel(AttnArgs a) {
   v4f oacc[DT];
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) oacc[dt] = v4f{0.f, 0.f, 0.f, 0.f};
-  // software pipeline over this wave's key tiles kt = wave, wave + NW, ...:
-  // PD tiles are requested ahead of the one in the products, in PD + 1
-  // register buffers used in turn (the loop is unrolled so that no buffer is
-  // copied); every load is issued, rows past n reading as 0, so that the
-  // compiler counts them and each tile waits only for its own rows
-  constexpr int PD = 1;
-  float kbuf[PD + 1][KS], vbuf[PD + 1][4][DT];
-  auto load_tile = [&](int kt, float* kx, float (*vx)[DT]) {
-    buf_load<KS>(rk, ((kt * 16 + c) * D + g * KS) * ESZ, 0, kx, T{});
-    const uint32_t voff = ((kt * 16 + 4 * g) * D + DT * c) * ESZ;
+  if constexpr (sizeof(T) == 2) {
+    // bf16 inputs: both products on the bf16 matrix cores, exact for the bf16
+    // keys and values, with Q^c and P split into three bf16 parts each (an fp32
+    // value is exactly the sum of its three truncated parts), so that every
+    // logit and value keeps fp32 accuracy: three part products per 32 dims or
+    // per 32 keys.  The k index of a product over dims maps to the lane's own
+    // dims g KS + 8 m + j; over keys, k = 8 g + j is key 4 g + j of the
+    // block's first tile (j < 4) or key 4 g + j - 4 of its second, which is
+    // where the logit results put P.  (For fp32 inputs the same scheme needs
+    // six part products and the splits of K and V, and measured no faster than
+    // the fp32 matrix cores, which the fp32 branch below uses.)
+    constexpr int NC = KS / 8;              // 32-dim chunks
+    Split8 qs[NC];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) buf_load<DT>(rv, voff, i * D * ESZ, vx[i], T{});
-  };
-  auto step = [&](int kt, const float* kx, const float (*vx)[DT]) {
-    v4f acc = {0.f, 0.f, 0.f, 0.f};
+    for (int m = 0; m < NC; ++m) qs[m] = split8(&bq[8 * m]);
+    const int nkb = (n + 31) / 32;  // blocks of two key tiles; wave w takes blocks w, w + NW, ...
+    // every load is issued, rows past n reading as 0, so that the compiler
+    // counts them and each block waits only for its own rows
+    auto load_block = [&](int bk, float (*kx)[KS], float (*vx)[4][DT]) {
 #pragma unroll
-    for (int s = 0; s < KS; ++s) acc = mfma_f32_16x16x4(kx[s], bq[s], acc);
-    float o[4];
+      for (int t = 0; t < 2; ++t) {
+        const int kt = 2 * bk + t;
+        buf_load<KS>(rk, ((kt * 16 + c) * D + g * KS) * ESZ, 0, kx[t], T{});
+        const uint32_t voff = ((kt * 16 + 4 * g) * D + DT * c) * ESZ;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) o[i] = (kt * 16 + 4 * g + i < n) ? acc[i] * a.scale : -INFINITY;
-    // key kt * 16 is valid, so the tile maximum of every column is finite
-    const float tmax = cross_rows_max(fmaxf(fmaxf(o[0], o[1]), fmaxf(o[2], o[3])));
-    const float mnew = fmaxf(mrun, tmax);
-    const float alpha = __expf(mrun - mnew);  // 0 on the first tile
-    mrun = mnew;
-    float p[4];
+        for (int i = 0; i < 4; ++i) buf_load<DT>(rv, voff, i * D * ESZ, vx[t][i], T{});
+      }
+    };
+    auto step = [&](int bk, float (*kx)[KS], float (*vx)[4][DT]) {
+      float o[8];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) p[i] = __expf(o[i] - mnew);
-    zl = zl * alpha + ((p[0] + p[1]) + (p[2] + p[3]));
+      for (int t = 0; t < 2; ++t) {
+        v4f acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
+        for (int m = 0; m < NC; ++m) {
+          acc = mfma_split3(pack_bf16x8(&kx[t][8 * m]), qs[m], acc);
+        }
 #pragma unroll
-      for (int r = 0; r < 4; ++r) oacc[dt][r] *= alpha;
+        for (int i = 0; i < 4; ++i) o[4 * t + i] = ((2 * bk + t) * 16 + 4 * g + i < n) ? acc[i] * a.scale : -INFINITY;
+      }
+      // key 32 bk is valid, so the block maximum of every column is finite
+      float bmax = o[0];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+      for (int e = 1; e < 8; ++e) bmax = fmaxf(bmax, o[e]);
+      const float mnew = fmaxf(mrun, cross_rows_max(bmax));
+      const float alpha = __expf(mrun - mnew);  // 0 on the first block
+      mrun = mnew;
+      float p[8], psum = 0.0f;
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt) oacc[dt] = mfma_f32_16x16x4(vx[i][dt], p[i], oacc[dt]);
-  };
+      for (int e = 0; e < 8; ++e) {
+        p[e] = __expf(o[e] - mnew);
+        psum += p[e];
+      }
+      zl = zl * alpha + psum;
+      const Split8 ps = split8(p);
 #pragma unroll
-  for (int e = 0; e < PD; ++e) load_tile(wave + NW * e, kbuf[e], vbuf[e]);
-  for (int kt0 = wave; kt0 < nkt; kt0 += (PD + 1) * NW) {
+      for (int dt = 0; dt < DT; ++dt) {
+        float va8[8];
 #pragma unroll
-    for (int e = 0; e <= PD; ++e) {
-      const int kt = kt0 + NW * e;
-      // the buffer of the tile PD ahead is the one that the previous step freed
-      load_tile(kt + NW * PD, kbuf[(e + PD) % (PD + 1)], vbuf[(e + PD) % (PD + 1)]);
-      if (kt < nkt) step(kt, kbuf[e], vbuf[e]);
+        for (int j = 0; j < 4; ++j) {
+          va8[j] = vx[0][j][dt];
+          va8[4 + j] = vx[1][j][dt];
+        }
+        oacc[dt] = mfma_split3(pack_bf16x8(va8), ps, oacc[dt] * alpha);
+      }
+    };
+    for (int bk = wave; bk < nkb; bk += NW) {
+      float kx[2][KS], vx[2][4][DT];
+      load_block(bk, kx, vx);
+      step(bk, kx, vx);
+    }
+  } else {
+    // fp32 inputs: one key tile in registers, the next one requested before
+    // the current one goes to the fp32 matrix cores (two buffers used in turn,
+    // the loop unrolled so that no buffer is copied); every load is issued,
+    // rows past n reading as 0, so that the compiler counts them and each tile
+    // waits only for its own rows
+    float kbuf[2][KS], vbuf[2][4][DT];
+    auto load_tile = [&](int kt, float* kx, float (*vx)[DT]) {
+      buf_load<KS>(rk, ((kt * 16 + c) * D + g * KS) * ESZ, 0, kx, T{});
+      const uint32_t voff = ((kt * 16 + 4 * g) * D + DT * c) * ESZ;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) buf_load<DT>(rv, voff, i * D * ESZ, vx[i], T{});
+    };
+    auto step = [&](int kt, const float* kx, const float (*vx)[DT]) {
+      v4f acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < KS; ++s) acc = mfma_f32_16x16x4(kx[s], bq[s], acc);
+      float o[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) o[i] = (kt * 16 + 4 * g + i < n) ? acc[i] * a.scale : -INFINITY;
+      // key kt * 16 is valid, so the tile maximum of every column is finite
+      const float tmax = cross_rows_max(fmaxf(fmaxf(o[0], o[1]), fmaxf(o[2], o[3])));
+      const float mnew = fmaxf(mrun, tmax);
+      const float alpha = __expf(mrun - mnew);  // 0 on the first tile
+      mrun = mnew;
+      float p[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) p[i] = __expf(o[i] - mnew);
+      zl = zl * alpha + ((p[0] + p[1]) + (p[2] + p[3]));
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) oacc[dt][r] *= alpha;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) oacc[dt] = mfma_f32_16x16x4(vx[i][dt], p[i], oacc[dt]);
+    };
+    load_tile(wave, kbuf[0], vbuf[0]);
+    for (int kt0 = wave; kt0 < nkt; kt0 += 2 * NW) {
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const int kt = kt0 + NW * e;
+        // the buffer of the next tile is the one that the previous step freed
+        load_tile(kt + NW, kbuf[(e + 1) % 2], vbuf[(e + 1) % 2]);
+        if (kt < nkt) step(kt, kbuf[e], vbuf[e]);
+      }
     }
   }
   const float zc = cross_rows_sum(zl);

@@ -184,6 +184,61 @@ __device__ __forceinline__ uint64_t lanemask_lt() {
 // A and B pair their k values by (k-group, position in the register), so any
 // permutation of the reduction index applied to both operands is allowed.
 // ---------------------------------------------------------------------------
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+
+// bf16 16x16x32: lane l holds row (l % 16) of A and column (l % 16) of B with
+// the eight consecutive k of group (l / 16), two bf16 per word in k order
+// (the lower k in the low half); the result lane l, register r holds
+// [4 (l / 16) + r][l % 16].  Products are exact, sums in fp32.
+__device__ __forceinline__ v4f mfma_bf16_16x16x32(v4u a, v4u b, v4f c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(v8bf, a),
+                                                 __builtin_bit_cast(v8bf, b), c, 0, 0, 0);
+}
+// Exact split of an fp32 value into three bf16 values x = hi + mid + lo by
+// truncation (8 + 8 + 8 significant bits); the parts are returned as fp32 bit
+// patterns whose low halves are zero.
+__device__ __forceinline__ void split3(float x, uint32_t& h, uint32_t& m, uint32_t& l) {
+  const uint32_t u = __float_as_uint(x);
+  h = u & 0xffff0000u;
+  const float r1 = x - __uint_as_float(h);
+  m = __float_as_uint(r1) & 0xffff0000u;
+  const float r2 = r1 - __uint_as_float(m);
+  l = __float_as_uint(r2) & 0xffff0000u;
+}
+// Eight fp32 values split as above and packed as bf16 operands (k order).
+struct Split8 {
+  v4u h, m, l;
+};
+__device__ __forceinline__ Split8 split8(const float* x) {
+  Split8 s;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    uint32_t h0, m0, l0, h1, m1, l1;
+    split3(x[2 * e], h0, m0, l0);
+    split3(x[2 * e + 1], h1, m1, l1);
+    s.h[e] = (h0 >> 16) | h1;
+    s.m[e] = (m0 >> 16) | m1;
+    s.l[e] = (l0 >> 16) | l1;
+  }
+  return s;
+}
+// Eight values that are bf16 values already (widened to fp32), packed.
+__device__ __forceinline__ v4u pack_bf16x8(const float* x) {
+  v4u p;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) p[e] = (__float_as_uint(x[2 * e]) >> 16) | (__float_as_uint(x[2 * e + 1]) & 0xffff0000u);
+  return p;
+}
+// A.B with A exact in bf16 and B split: three products, exact up to the fp32
+// sums.
+__device__ __forceinline__ v4f mfma_split3(v4u a, const Split8& b, v4f c) {
+  c = mfma_bf16_16x16x32(a, b.h, c);
+  c = mfma_bf16_16x16x32(a, b.m, c);
+  c = mfma_bf16_16x16x32(a, b.l, c);
+  return c;
+}
+
 __device__ __forceinline__ v4f mfma_f32_16x16x4(float a, float b, v4f c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }

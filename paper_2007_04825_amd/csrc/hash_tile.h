@@ -32,13 +32,6 @@
 
 namespace ca {
 
-typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
-typedef uint32_t v4u __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ v4f mfma_bf16_16x16x32(v4u a, v4u b, v4f c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(v8bf, a),
-                                                 __builtin_bit_cast(v8bf, b), c, 0, 0, 0);
-}
 
 // A operands of the 64 plane rows (four 16-plane tiles) for D/32 k-chunks,
 // and, for the planes whose signs this lane receives (16 pt + 4 (lane / 16) +
@@ -157,14 +150,6 @@ struct QueryOps {
   v4u hi, mid, lo;
   float sq;
 };
-__device__ __forceinline__ void split3(float x, uint32_t& h, uint32_t& m, uint32_t& l) {
-  const uint32_t u = __float_as_uint(x);
-  h = u & 0xffff0000u;
-  const float r1 = x - __uint_as_float(h);
-  m = __float_as_uint(r1) & 0xffff0000u;
-  const float r2 = r1 - __uint_as_float(m);
-  l = __float_as_uint(r2) & 0xffff0000u;
-}
 __device__ __forceinline__ QueryOps query_ops(const uint4 (&w)[2]) {
   const float x[8] = {__uint_as_float(w[0].x), __uint_as_float(w[0].y), __uint_as_float(w[0].z),
                       __uint_as_float(w[0].w), __uint_as_float(w[1].x), __uint_as_float(w[1].y),
