@@ -250,6 +250,16 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
           make_rsrc(a.qc + (static_cast<size_t>(u) * C + j0) * D, static_cast<uint32_t>(min(16, C - j0)) * D * 4);
       buf_load<KS>(rq, (c * D + g * KS) * 4, 0, bq, float{});
     }
+    // bf16 inputs: exact keys, the rows split into three bf16 parts, three
+    // part products per 32 dims on the bf16 matrix cores (fp32-accurate
+    // logits; the k index maps to the lane's own dims g KS + 8 m + j)
+    constexpr bool BF = sizeof(T) == 2;
+    constexpr int NC = KS / 8;
+    Split8 qs[BF ? NC : 1];
+    if constexpr (BF) {
+#pragma unroll
+      for (int m = 0; m < NC; ++m) qs[m] = split8(&bq[8 * m]);
+    }
     float lmax = -INFINITY;
     float top[NT];
 #pragma unroll
@@ -271,8 +281,13 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
         const int kt = kt0 + NW * b;
         if (kt < nkt) {
           v4f acc = {0.f, 0.f, 0.f, 0.f};
+          if constexpr (BF) {
 #pragma unroll
-          for (int s = 0; s < KS; ++s) acc = mfma_f32_16x16x4(ka[b][s], bq[s], acc);
+            for (int m = 0; m < NC; ++m) acc = mfma_split3(pack_bf16x8(&ka[b][8 * m]), qs[m], acc);
+          } else {
+#pragma unroll
+            for (int s = 0; s < KS; ++s) acc = mfma_f32_16x16x4(ka[b][s], bq[s], acc);
+          }
           float o[4];
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
@@ -449,17 +464,56 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
             for (int dt = 0; dt < DT; ++dt) va[b][i][dt] = 0.0f;
           }
         }
+      if constexpr (sizeof(T) == 2) {
+        // bf16 values are exact; P splits into three bf16 parts; tiles b and
+        // b + 1 of the batch form one product over 32 keys (k = 8 g + j: key
+        // 4 g + j of tile b for j < 4, of tile b + 1 otherwise), a tile past
+        // the row contributing P = 0
+        static_assert(BT % 2 == 0, "tile pairs");
 #pragma unroll
-      for (int b = 0; b < BT; ++b) {
-        const int kt = kt0 + NW * b;
-        if (kt < nkt) {
-          const float4 s4 = *reinterpret_cast<const float4*>(&logits[c * kLStride + kt * 16 + 4 * g]);
-          const float p[4] = {__expf(s4.x - mc), __expf(s4.y - mc), __expf(s4.z - mc), __expf(s4.w - mc)};
-          psum += (p[0] + p[1]) + (p[2] + p[3]);
+        for (int b = 0; b < BT; b += 2) {
+          if (kt0 + NW * b >= nkt) break;
+          float p8[8];
 #pragma unroll
-          for (int i = 0; i < 4; ++i)
+          for (int h = 0; h < 2; ++h) {
+            const int kt = kt0 + NW * (b + h);
+            if (kt < nkt) {
+              const float4 s4 = *reinterpret_cast<const float4*>(&logits[c * kLStride + kt * 16 + 4 * g]);
+              p8[4 * h] = __expf(s4.x - mc);
+              p8[4 * h + 1] = __expf(s4.y - mc);
+              p8[4 * h + 2] = __expf(s4.z - mc);
+              p8[4 * h + 3] = __expf(s4.w - mc);
+            } else {
 #pragma unroll
-            for (int dt = 0; dt < DT; ++dt) oacc[dt] = mfma_f32_16x16x4(va[b][i][dt], p[i], oacc[dt]);
+              for (int i = 0; i < 4; ++i) p8[4 * h + i] = 0.0f;
+            }
+          }
+          psum += ((p8[0] + p8[1]) + (p8[2] + p8[3])) + ((p8[4] + p8[5]) + (p8[6] + p8[7]));
+          const Split8 ps = split8(p8);
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) {
+            float v8[8];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              v8[i] = va[b][i][dt];
+              v8[4 + i] = va[b + 1][i][dt];
+            }
+            oacc[dt] = mfma_split3(pack_bf16x8(v8), ps, oacc[dt]);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int b = 0; b < BT; ++b) {
+          const int kt = kt0 + NW * b;
+          if (kt < nkt) {
+            const float4 s4 = *reinterpret_cast<const float4*>(&logits[c * kLStride + kt * 16 + 4 * g]);
+            const float p[4] = {__expf(s4.x - mc), __expf(s4.y - mc), __expf(s4.z - mc), __expf(s4.w - mc)};
+            psum += (p[0] + p[1]) + (p[2] + p[3]);
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+              for (int dt = 0; dt < DT; ++dt) oacc[dt] = mfma_f32_16x16x4(va[b][i][dt], p[i], oacc[dt]);
+          }
         }
       }
     }
