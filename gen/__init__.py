@@ -159,6 +159,35 @@ def config_long(B=1, H=8, N=65536, d=64, C=200, n_bits=63, L=15, topk=64, seed_c
                     variants=("iclustered",))
 
 
+def config_random(seed: int) -> Workload:
+    """Seeded random shapes for broad parity checks: batch 1-3, heads 1-3,
+    N from 1 to 3000 (small and chunk-edge sizes favoured), d 32 or 64, fp32
+    or bf16, C 1-256, n_bits 1-63, L 1-12, k 1-128, ragged lengths (the first
+    sequence full, the others uniform in [0, N]); queries from a Gaussian
+    mixture of about C / 2 components (sigma 0.3), keys and values iid N(0, 1),
+    padded rows 0."""
+    r = np.random.default_rng([seed, 77])
+    B = int(r.integers(1, 4))
+    H = int(r.integers(1, 4))
+    N = int(r.choice([1, 2, 5, 16, 17, 63, 100, 257, 600, 1024, 1025, 2100, 3000]))
+    d = int(r.choice([32, 64]))
+    dtype = str(r.choice(["f32", "bf16"]))
+    C = int(r.choice([1, 3, 16, 17, 100, 256]))
+    n_bits = int(r.choice([1, 8, 31, 63]))
+    L = int(r.integers(1, 13))
+    topk = int(r.choice([1, 2, 16, 32, 33, 64, 128]))
+    lengths = r.integers(0, N + 1, size=B).astype(np.int32)
+    lengths[0] = N
+    q = _mixture(10, B, H, N, d, max(1, C // 2), 0.3, extra=seed)
+    k = rng(10, 1, seed).standard_normal((B, H, N, d))
+    v = rng(10, 2, seed).standard_normal((B, H, N, d))
+    mask = np.arange(N)[None, None, :, None] >= lengths[:, None, None, None]
+    q, k, v = (np.where(mask, 0.0, x) for x in (q, k, v))
+    return Workload("random%d_b%dh%dn%dd%d_%s" % (seed, B, H, N, d, dtype), _finish(q, dtype),
+                    _finish(k, dtype), _finish(v, dtype), lengths, hyperplanes(10, H, n_bits, d, seed),
+                    C, n_bits, L, topk, dtype)
+
+
 def make_config(cfg: int, **kw) -> Workload:
     """The five workloads: 1 tiny, 2 speech, 3 sweep (pass N=, dtype=), 4 encoder,
     5 long."""

@@ -207,12 +207,25 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
       return;
     }
   }
-  const int k0 = chunk * kChunk;
-  if (k0 >= n) return;
-  const int kn = min(kChunk, n - k0);
   const int C = a.C;
   const int j0 = tile * 16;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // single-chunk improved mode: a tile whose clusters are all empty exports
+  // what an empty cluster has (values 0, no top-k set, mass 0)
+  auto export_empty_tile = [&]() {
+    const size_t uj0 = static_cast<size_t>(u) * C + j0;
+    for (int x = tid; x < 16 * D; x += kTileThreads)
+      if (j0 + x / D < C) a.vcb[uj0 * D + x] = 0.0f;
+    for (int x = tid; x < 16 * a.topk; x += kTileThreads)
+      if (j0 + x / a.topk < C) a.topk_out[uj0 * a.topk + x] = -1;
+    if (tid < 16 && j0 + tid < C) a.mass[uj0 + tid] = 0.0f;
+  };
+  const int k0 = chunk * kChunk;
+  if (k0 >= n) {  // in a single-chunk mode: a sequence of length 0
+    if constexpr (FUSED && !OTOP) export_empty_tile();
+    return;
+  }
+  const int kn = min(kChunk, n - k0);
   const int c = lane & 15, g = lane >> 4;
   const T* ku = static_cast<const T*>(a.k) + (static_cast<size_t>(u) * a.N + k0) * D;
   const T* vu = static_cast<const T*>(a.v) + (static_cast<size_t>(u) * a.N + k0) * D;
@@ -228,7 +241,10 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
     const int32_t* ou = a.offsets + static_cast<size_t>(u) * (C + 1);
     if (tid < 17) moff[tid] = ou[min(j0 + tid, C)];
     __syncthreads();
-    if (moff[16] == moff[0]) return;  // every cluster of the tile is empty
+    if (moff[16] == moff[0]) {  // every cluster of the tile is empty
+      export_empty_tile();
+      return;
+    }
   } else {
     if (tid == 0) any_nonempty = 0;
     __syncthreads();
@@ -598,7 +614,12 @@ __global__ __launch_bounds__(kFlashThreads) void attn_flash_kernel(AttnArgs a) {
   const int32_t* ou = a.offsets + static_cast<size_t>(u) * (C + 1);
   if (tid < 17) moff[tid] = ou[min(j0 + tid, C)];
   __syncthreads();
-  if (moff[16] == moff[0] || n == 0) return;  // every cluster of the tile is empty
+  if (moff[16] == moff[0] || n == 0) {  // every cluster of the tile is empty: V^c = 0
+    const size_t uj0 = static_cast<size_t>(u) * C + j0;
+    for (int x = tid; x < 16 * D; x += kFlashThreads)
+      if (j0 + x / D < C) a.vcb[uj0 * D + x] = 0.0f;
+    return;
+  }
   const int m0 = moff[0], mn = moff[16] - m0;
   // the member lists are requested now and stored once the products are done
   constexpr int MPT = kChunk / kFlashThreads;

@@ -160,13 +160,19 @@ def check_end_to_end(w, topk, shared_qk=False):
     assert np.array_equal(got["sizes"], ref["sizes"]), "cluster sizes differ"
     np.testing.assert_allclose(got["centroids"], ref["qc"], rtol=0, atol=2e-6)
     skip_rows = np.zeros(vm.shape, bool)
+    skip_clusters = np.zeros(ref["sizes"].shape, bool)
     if topk:
         diff, bad = topk_mismatches(w, ref, got, topk)
         print("top-k near-tie differences: %d clusters" % len(diff))
         assert not bad, "top-k sets differ beyond near ties: %s" % bad[:5]
         for (b, h, j) in diff:
             skip_rows[b, h] |= ref["assign"][b, h] == j
+            skip_clusters[b, h, j] = True
         np.testing.assert_allclose(got["mass"], ref["mass"], rtol=0, atol=1e-5)
+    # the exported per-cluster values (V^c, or V^b for the improved variant);
+    # empty clusters export 0
+    verr = np.abs(got["values"] - ref["vcb"])[~skip_clusters].max()
+    assert verr <= tol(w), "cluster values differ: %.3g" % verr
     cmp = vm & ~skip_rows
     err = np.abs(got["out"] - ref["out"])[cmp].max()
     print("max abs error: %.3g (tolerance %.0e)" % (err, tol(w)))
