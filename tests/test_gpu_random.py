@@ -24,3 +24,15 @@ def test_random_shapes(seed):
     check_end_to_end(w, 0)
     check_end_to_end(w, w.topk)
     check_oracle_top(w, w.topk)
+
+
+@pytest.mark.parametrize("seed", SEEDS)
+def test_random_shapes_backward(seed):
+    """The backward pass of both variants on the same random shapes, against
+    the oracle's gradients for the GPU forward's partition and top-k sets."""
+    from test_gpu_backward import run_case
+    w = gen.config_random(seed)
+    print("\n[gpu case] backward %s C %d k %d lengths %s" % (w.name, w.C, w.topk, w.lengths.tolist()),
+          flush=True)
+    run_case(w, 0)
+    run_case(w, w.topk)
