@@ -48,3 +48,19 @@ def test_sweep_full_size(log2n, dtype, variant):
 def test_long_context_full_size():
     w = workload(("long",))
     check_end_to_end(w, w.topk)
+
+
+@pytest.mark.parametrize("variant", ["clustered", "iclustered"])
+@pytest.mark.parametrize("log2n", [9, 12])
+def test_time_benchmark_protocol_full_size(log2n, variant):
+    """The shapes of the time and memory benchmark (6 heads x 64, 2^17 tokens
+    per call: batch 256 at N = 512, 32 at N = 4096), which run the one-
+    workgroup K-means for many units, up to its largest n."""
+    N = 1 << log2n
+    key = ("fig4", N)
+    if key not in _W:
+        _W.clear()
+        gpu_util.clear_oracle_cache()
+        _W[key] = gen.config_sweep(N, dtype="f32", B=(1 << 17) // N, H=6, d=64)
+    w = _W[key]
+    check_end_to_end(w, w.topk if variant == "iclustered" else 0)
