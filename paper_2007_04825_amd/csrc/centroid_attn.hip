@@ -1079,8 +1079,16 @@ __global__ __launch_bounds__(256) void sparse_kernel(AttnArgs a) {
     for (int kt = 0; kt < NKT; ++kt) {
       sacc[kt] = v4f{0.f, 0.f, 0.f, 0.f};
       if (kt < nkt) {
+        if constexpr (sizeof(T) == 2) {
+          // bf16 inputs: the T rows of K and the member rows of Q are exact
+          // bf16, so one bf16 product per 32 dims gives the fp32-accurate logits
 #pragma unroll
-        for (int s = 0; s < KS; ++s) sacc[kt] = mfma_f32_16x16x4(kf[kt][s], bq[s], sacc[kt]);
+          for (int m = 0; m < KS / 8; ++m)
+            sacc[kt] = mfma_bf16_16x16x32(pack_bf16x8(&kf[kt][8 * m]), pack_bf16x8(&bq[8 * m]), sacc[kt]);
+        } else {
+#pragma unroll
+          for (int s = 0; s < KS; ++s) sacc[kt] = mfma_f32_16x16x4(kf[kt][s], bq[s], sacc[kt]);
+        }
       }
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -1104,14 +1112,40 @@ __global__ __launch_bounds__(256) void sparse_kernel(AttnArgs a) {
     v4f oacc[DT];
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) oacc[dt] = v4f{0.f, 0.f, 0.f, 0.f};
+    if constexpr (sizeof(T) == 2) {
+      // exact bf16 values, P split into three bf16 parts; slots of tiles kt and
+      // kt + 1 form one product over 32 (k = 8 g + j: slot 4 g + j of tile kt
+      // for j < 4, of tile kt + 1 otherwise); a missing tile contributes 0
 #pragma unroll
-    for (int kt = 0; kt < NKT; ++kt) {
-      if (kt < nkt) {
+      for (int kt = 0; kt < NKT; kt += 2) {
+        if (kt >= nkt) break;
+        float p8[8];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float pv = sacc[kt][i] * f;
+        for (int h = 0; h < 2; ++h)
 #pragma unroll
-          for (int dt = 0; dt < DT; ++dt) oacc[dt] = mfma_f32_16x16x4(vf[kt][i][dt], pv, oacc[dt]);
+          for (int i = 0; i < 4; ++i) p8[4 * h + i] = (kt + h < NKT && kt + h < nkt) ? sacc[min(kt + h, NKT - 1)][i] * f : 0.0f;
+        const Split8 ps = split8(p8);
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+          float v8[8];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            v8[i] = vf[kt][i][dt];
+            v8[4 + i] = kt + 1 < NKT ? vf[min(kt + 1, NKT - 1)][i][dt] : 0.0f;
+          }
+          oacc[dt] = mfma_split3(pack_bf16x8(v8), ps, oacc[dt]);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt) {
+        if (kt < nkt) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float pv = sacc[kt][i] * f;
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) oacc[dt] = mfma_f32_16x16x4(vf[kt][i][dt], pv, oacc[dt]);
+          }
         }
       }
     }
