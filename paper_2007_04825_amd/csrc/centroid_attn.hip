@@ -873,8 +873,10 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
       a.stats[uj * 2] = M;
       a.stats[uj * 2 + 1] = Z;
     }
-    // V^c = sum_chunks exp(m_c - M) acc_c / Z   (lane -> dimension)
+    // V^c = sum_chunks exp(m_c - M) acc_c / Z   (lane -> dimension; eight
+    // chunks' partials in flight)
     float acc = 0.0f;
+#pragma unroll 8
     for (int x = r; x < nch; x += RPS) acc += __expf(pmj[x] - M) * a.pacc[(uj * a.nchunk + x) * D + t];
     if (RPS == 2) acc += lane_xor32(acc);
     const float vc = acc / Z;

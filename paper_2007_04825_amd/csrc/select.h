@@ -128,6 +128,8 @@ __device__ int wave_topk_row(const float* row, int m, int kk, int* scratch, OutT
   const int lane = lane_id();
   float a1 = -INFINITY, a2 = -INFINITY;
   int have = 0;
+  // eight loads in flight per lane (the row may be in global memory)
+#pragma unroll 8
   for (int pos = lane; pos < m; pos += 64) {
     const float x = row[pos];
     a2 = fmaxf(a2, fminf(a1, x));
@@ -140,6 +142,7 @@ __device__ int wave_topk_row(const float* row, int m, int kk, int* scratch, OutT
                                     two, kk);
   float z = 0.0f;
   int c = 0;
+#pragma unroll 8
   for (int base = 0; base < m; base += 64) {
     const int pos = base + lane;
     const bool ok = pos < m;
