@@ -308,10 +308,10 @@ __device__ __forceinline__ uint32_t group_kth_key(const uint32_t* keys, int kk) 
   for (int bit = top; bit >= 0; --bit) {
     if (__ballot(!done) == 0ull) break;
     const uint32_t cand = t | (1u << bit);
-    int cnt = 0;
+    // the group's count from one ballot per key slot (no cross-lane chain)
+    int tot = 0;
 #pragma unroll
-    for (int e = 0; e < NK; ++e) cnt += keys[e] >= cand ? 1 : 0;
-    const int tot = grp_sum_i<GL>(cnt);
+    for (int e = 0; e < NK; ++e) tot += __popc(grp_field<GL>(__ballot(keys[e] >= cand)));
     if (!done && tot >= kk) {
       t = cand;
       done = tot == kk;
