@@ -619,7 +619,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the forward pass of each (sequence, head) is "
-              "independent and this build has no multi-GPU path (--gpus %d refused)" % args.gpus,
+              "independent and the library has no multi-GPU path (--gpus %d refused)" % args.gpus,
               file=sys.stderr)
         sys.exit(2)
     if args.copy_calibration:
