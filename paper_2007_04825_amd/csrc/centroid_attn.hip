@@ -957,7 +957,7 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
 // wave per (cluster j, chunk of up to kSparseChunk members), so that large
 // clusters spread over many waves: for every member i,
 //   out_i = m_j * sum_{l in T} softmax_T(q_i k_l / sqrt d)_l v_l + V^b_j.
-// The loads come in three dependent rounds: size, offset, m_j, V^b_j and T;
+// The loads come in three dependent steps: size, offset, m_j, V^b_j and T;
 // then the member indices with the K_T and V_T rows; then the member rows of
 // Q.  Member tiles after the first are requested one tile ahead.
 //   S^T = K_T Q^T : A = K_T rows (slot kt*16 + lane%16, dims g*KS..), B = Q^T
@@ -1005,7 +1005,7 @@ __global__ __launch_bounds__(256) void sparse_kernel(AttnArgs a) {
   if (j >= C) return;
   const size_t uj = static_cast<size_t>(u) * C + j;
 
-  // ---- round 1: the cluster's size, offset, m_j, V^b_j and T -----------------------
+  // ---- load step 1: the cluster's size, offset, m_j, V^b_j and T ------------------
   const int sz_all = a.sizes[uj];
   const int sz = min(kSparseChunk, sz_all - chunk * kSparseChunk);  // members of this item
   const int off = a.offsets[static_cast<size_t>(u) * (C + 1) + j] + chunk * kSparseChunk;
@@ -1029,7 +1029,7 @@ __global__ __launch_bounds__(256) void sparse_kernel(AttnArgs a) {
   wave_lds_sync();
   const int nkt = (kk + 15) >> 4;
 
-  // ---- round 2: member indices of the first two tiles, K_T and V_T -------------------
+  // ---- load step 2: member indices of the first two tiles, K_T and V_T --------------
   const int32_t* mem = a.members + static_cast<size_t>(u) * a.N + off;
   int row0 = c < sz ? mem[c] : -1;
   int row1 = 16 + c < sz ? mem[16 + c] : -1;
@@ -1064,7 +1064,7 @@ __global__ __launch_bounds__(256) void sparse_kernel(AttnArgs a) {
   }
   auto qoff = [&](int row) { return row >= 0 ? static_cast<uint32_t>(row) * D * ESZ + g * KS * ESZ : kNone; };
 
-  // ---- round 3: member rows of Q, one tile of 16 at a time -------------------------
+  // ---- load step 3: member rows of Q, one tile of 16 at a time --------------------
   float bq[KS];
   buf_load<KS>(rq, qoff(row0), 0, bq, T{});
   for (int mt = 0; mt < sz; mt += 16) {
