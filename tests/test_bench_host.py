@@ -1,0 +1,65 @@
+"""Host logic of the benchmark (no GPU): the one-GPU refusal, the algorithmic
+work behind the roofline entry (closed forms on a small workload), the
+committed HBM counter profile and the guard that withholds it once the kernel
+sources change, and the host thread count of the oracle baseline."""
+import json
+import os
+import subprocess
+import sys
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import bench  # noqa: E402
+import gen  # noqa: E402
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=300)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr and "--gpus 2" in r.stderr
+
+
+def test_stage_work_closed_forms():
+    w = gen.config_speech(B=2, H=3, N=40, d=32, lengths=np.array([40, 25], np.int32))
+    nsum = (40 + 25) * 3
+    flops, unit, bound, peak = bench.stage_work(w, "centroid_attn", 32)
+    assert (unit, bound) == ("TFLOP/s", "mfma") and peak == bench.PEAKS["fp32_mfma_TFLOPs"]
+    assert flops == 2 * (2 * w.C * nsum * 32)  # Q^c K^T and A^c V
+    ops, unit, bound, _ = bench.stage_work(w, "kmeans", 0)
+    assert unit == "TOP/s" and ops == 2 * 64 * w.L * nsum * w.C
+    byts, unit, bound, peak = bench.stage_work(w, "hash", 0)
+    assert (unit, bound) == ("GB/s", "hbm") and byts == nsum * 32 * 4 + nsum * 8
+    assert bench.stage_work(w, "output", 0)[0] == nsum * 32 * 4 + nsum * 4
+    assert bench.stage_work(w, "output", 32)[0] == 2 * nsum * 32 * 4 + 2 * 3 * 2 * w.C * 32 * 32 * 4
+    with pytest.raises(ValueError):
+        bench.stage_work(w, "nonsense", 0)
+
+
+def test_counter_profile_is_withheld_when_sources_change(monkeypatch):
+    path = os.path.join(ROOT, "profiles", "speech_b32h6n800_d32_f32_hbm_counters.json")
+    with open(path) as f:
+        prof = json.load(f)
+    key = "centroid_attn (iclustered)"
+    assert prof["kernels"][key]["hbm_bytes_per_launch"] > 0
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda: prof["source_sha256"])
+    assert bench.measured_traffic(key) == prof["kernels"][key]["hbm_bytes_per_launch"]
+    assert bench.measured_traffic("no such kernel") is None
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda: "0" * 64)
+    assert bench.measured_traffic(key) is None
+
+
+def test_kernel_source_hash_is_stable():
+    h0 = bench.kernel_source_hash()
+    assert len(h0) == 64 and h0 == bench.kernel_source_hash()
+
+
+def test_cpu_threads(monkeypatch):
+    monkeypatch.setenv("OMP_NUM_THREADS", "1")
+    assert bench.cpu_threads() == 1
+    monkeypatch.setenv("OMP_NUM_THREADS", "")
+    assert bench.cpu_threads() >= 1
