@@ -235,6 +235,34 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
   const __amdgpu_buffer_rsrc_t rk = make_rsrc(ku, static_cast<uint32_t>(kn) * D * ESZ);
   const __amdgpu_buffer_rsrc_t rv = make_rsrc(vu, static_cast<uint32_t>(kn) * D * ESZ);
 
+  // the rows of this tile and the first batch of key tiles do not depend on
+  // the cluster sizes: they are requested first, so that the latencies overlap
+  float bq[KS];
+  if constexpr (OTOP) {  // the query rows j0 .. j0 + 15 (rows past n read as 0)
+    const __amdgpu_buffer_rsrc_t rq =
+        make_rsrc(static_cast<const T*>(a.q) + (static_cast<size_t>(u) * a.N + j0) * D,
+                  static_cast<uint32_t>(min(16, n - j0)) * D * ESZ);
+    buf_load<KS>(rq, (c * D + g * KS) * ESZ, 0, bq, T{});
+  } else {
+    const __amdgpu_buffer_rsrc_t rq =
+        make_rsrc(a.qc + (static_cast<size_t>(u) * C + j0) * D, static_cast<uint32_t>(min(16, C - j0)) * D * 4);
+    buf_load<KS>(rq, (c * D + g * KS) * 4, 0, bq, float{});
+  }
+  float ka[BT][KS];
+  auto load_keys = [&](int kt0) {
+    const uint32_t voff = ((kt0 * 16 + c) * D + g * KS) * ESZ;
+#pragma unroll
+    for (int b = 0; b < BT; ++b) {
+      if (kt0 + NW * b < nkt) {  // whole tiles past the chunk are not requested
+        buf_load<KS>(rk, voff, NW * b * 16 * D * ESZ, ka[b], T{});
+      } else {
+#pragma unroll
+        for (int s = 0; s < KS; ++s) ka[b][s] = 0.0f;
+      }
+    }
+  };
+  load_keys(wave);
+
   // ---- sizes (fused: the member offsets of the 16 clusters) -----------------------
   if constexpr (OTOP) {
   } else if constexpr (FUSED) {
@@ -255,17 +283,6 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
 
   // ---- logits of this chunk, with the slice statistics -------------------------------
   {
-    float bq[KS];
-    if constexpr (OTOP) {  // the query rows j0 .. j0 + 15 (rows past n read as 0)
-      const __amdgpu_buffer_rsrc_t rq =
-          make_rsrc(static_cast<const T*>(a.q) + (static_cast<size_t>(u) * a.N + j0) * D,
-                    static_cast<uint32_t>(min(16, n - j0)) * D * ESZ);
-      buf_load<KS>(rq, (c * D + g * KS) * ESZ, 0, bq, T{});
-    } else {
-      const __amdgpu_buffer_rsrc_t rq =
-          make_rsrc(a.qc + (static_cast<size_t>(u) * C + j0) * D, static_cast<uint32_t>(min(16, C - j0)) * D * 4);
-      buf_load<KS>(rq, (c * D + g * KS) * 4, 0, bq, float{});
-    }
     // bf16 inputs: exact keys, the rows split into three bf16 parts, three
     // part products per 32 dims on the bf16 matrix cores (fp32-accurate
     // logits; the k index maps to the lane's own dims g KS + 8 m + j)
@@ -281,17 +298,7 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
 #pragma unroll
     for (int e = 0; e < NT; ++e) top[e] = -INFINITY;
     for (int kt0 = wave; kt0 < nkt; kt0 += NW * BT) {
-      float ka[BT][KS];
-      const uint32_t voff = ((kt0 * 16 + c) * D + g * KS) * ESZ;
-#pragma unroll
-      for (int b = 0; b < BT; ++b) {
-        if (kt0 + NW * b < nkt) {  // whole tiles past the chunk are not requested
-          buf_load<KS>(rk, voff, NW * b * 16 * D * ESZ, ka[b], T{});
-        } else {
-#pragma unroll
-          for (int s = 0; s < KS; ++s) ka[b][s] = 0.0f;
-        }
-      }
+      if (kt0 != wave) load_keys(kt0);  // the first batch is in flight already
 #pragma unroll
       for (int b = 0; b < BT; ++b) {
         const int kt = kt0 + NW * b;
@@ -611,6 +618,29 @@ __global__ __launch_bounds__(kFlashThreads) void attn_flash_kernel(AttnArgs a) {
   const int j0 = tile * 16;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int c = lane & 15, g = lane >> 4;
+  // the centroid rows and (fp32) the first key tile do not depend on the
+  // member offsets: they are requested first, so that both latencies overlap
+  const T* ku = static_cast<const T*>(a.k) + static_cast<size_t>(u) * a.N * D;
+  const T* vu = static_cast<const T*>(a.v) + static_cast<size_t>(u) * a.N * D;
+  const __amdgpu_buffer_rsrc_t rk = make_rsrc(ku, static_cast<uint32_t>(n) * D * ESZ);
+  const __amdgpu_buffer_rsrc_t rv = make_rsrc(vu, static_cast<uint32_t>(n) * D * ESZ);
+  const int nkt = (n + 15) / 16;
+  float bq[KS];
+  {
+    const __amdgpu_buffer_rsrc_t rq =
+        make_rsrc(a.qc + (static_cast<size_t>(u) * C + j0) * D, static_cast<uint32_t>(min(16, C - j0)) * D * 4);
+    buf_load<KS>(rq, (c * D + g * KS) * 4, 0, bq, float{});
+  }
+  // fp32 inputs: one key tile in registers, the next one requested before
+  // the current one goes to the fp32 matrix cores (two buffers used in turn)
+  float kbuf[2][KS], vbuf[2][4][DT];
+  auto load_tile = [&](int kt, float* kx, float (*vx)[DT]) {
+    buf_load<KS>(rk, ((kt * 16 + c) * D + g * KS) * ESZ, 0, kx, T{});
+    const uint32_t voff = ((kt * 16 + 4 * g) * D + DT * c) * ESZ;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) buf_load<DT>(rv, voff, i * D * ESZ, vx[i], T{});
+  };
+  if constexpr (sizeof(T) == 4) load_tile(wave, kbuf[0], vbuf[0]);
   const int32_t* ou = a.offsets + static_cast<size_t>(u) * (C + 1);
   if (tid < 17) moff[tid] = ou[min(j0 + tid, C)];
   __syncthreads();
@@ -631,17 +661,6 @@ __global__ __launch_bounds__(kFlashThreads) void attn_flash_kernel(AttnArgs a) {
       const int x = tid + kFlashThreads * e;
       mreg[e] = x < mn ? mg[x] : 0;
     }
-  }
-  const T* ku = static_cast<const T*>(a.k) + static_cast<size_t>(u) * a.N * D;
-  const T* vu = static_cast<const T*>(a.v) + static_cast<size_t>(u) * a.N * D;
-  const __amdgpu_buffer_rsrc_t rk = make_rsrc(ku, static_cast<uint32_t>(n) * D * ESZ);
-  const __amdgpu_buffer_rsrc_t rv = make_rsrc(vu, static_cast<uint32_t>(n) * D * ESZ);
-  const int nkt = (n + 15) / 16;
-  float bq[KS];
-  {
-    const __amdgpu_buffer_rsrc_t rq =
-        make_rsrc(a.qc + (static_cast<size_t>(u) * C + j0) * D, static_cast<uint32_t>(min(16, C - j0)) * D * 4);
-    buf_load<KS>(rq, (c * D + g * KS) * 4, 0, bq, float{});
   }
   float mrun = -INFINITY, zl = 0.0f;
   v4f oacc[DT];
@@ -719,18 +738,10 @@ __global__ __launch_bounds__(kFlashThreads) void attn_flash_kernel(AttnArgs a) {
       step(bk, kx, vx);
     }
   } else {
-    // fp32 inputs: one key tile in registers, the next one requested before
-    // the current one goes to the fp32 matrix cores (two buffers used in turn,
-    // the loop unrolled so that no buffer is copied); every load is issued,
-    // rows past n reading as 0, so that the compiler counts them and each tile
-    // waits only for its own rows
-    float kbuf[2][KS], vbuf[2][4][DT];
-    auto load_tile = [&](int kt, float* kx, float (*vx)[DT]) {
-      buf_load<KS>(rk, ((kt * 16 + c) * D + g * KS) * ESZ, 0, kx, T{});
-      const uint32_t voff = ((kt * 16 + 4 * g) * D + DT * c) * ESZ;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) buf_load<DT>(rv, voff, i * D * ESZ, vx[i], T{});
-    };
+    // fp32 inputs: the loop is unrolled so that no buffer is copied; every
+    // load is issued, rows past n reading as 0, so that the compiler counts
+    // them and each tile waits only for its own rows (the first tile was
+    // requested before the offsets)
     auto step = [&](int kt, const float* kx, const float (*vx)[DT]) {
       v4f acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -756,7 +767,6 @@ __global__ __launch_bounds__(kFlashThreads) void attn_flash_kernel(AttnArgs a) {
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) oacc[dt] = mfma_f32_16x16x4(vx[i][dt], p[i], oacc[dt]);
     };
-    load_tile(wave, kbuf[0], vbuf[0]);
     for (int kt0 = wave; kt0 < nkt; kt0 += 2 * NW) {
 #pragma unroll
       for (int e = 0; e < 2; ++e) {
