@@ -981,6 +981,7 @@ __global__ __launch_bounds__(256) void sparse_kernel(AttnArgs a) {
   constexpr uint32_t ESZ = sizeof(T);
   constexpr uint32_t kNone = 0x80000000u;  // past every buffer: loads read 0, stores are dropped
   __shared__ int tp[4][kCandCap];
+  __shared__ __align__(16) float vbs[4][D];  // V^b_j of each wave's cluster
   const int wi = xcd_work_item();  // item group fastest, then (batch, head)
   if (wi >= a.nsg * a.units) return;
   const int u = wi / a.nsg, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -1026,9 +1027,11 @@ __global__ __launch_bounds__(256) void sparse_kernel(AttnArgs a) {
     const int x = lane + 64 * e;
     tv[e] = x < a.topk ? a.topk_out[uj * a.topk + x] : -1;
   }
-  float vbf[4 * DT];
-  load_row<4 * DT>(a.vcb + uj * D + DT * 4 * g, vbf);
+  // V^b_j is the same for every member row: it waits in LDS, not in registers
+  float vb4[4];
+  if (lane < D / 4) load_row<4>(a.vcb + uj * D + 4 * lane, vb4);
   if (sz <= 0) return;
+  if (lane < D / 4) *reinterpret_cast<float4*>(&vbs[wave][4 * lane]) = make_float4(vb4[0], vb4[1], vb4[2], vb4[3]);
   // T: the leading non-negative entries (a caller-supplied set may be shorter)
   int kk = 0;
 #pragma unroll
@@ -1075,16 +1078,13 @@ __global__ __launch_bounds__(256) void sparse_kernel(AttnArgs a) {
   auto qoff = [&](int row) { return row >= 0 ? static_cast<uint32_t>(row) * D * ESZ + g * KS * ESZ : kNone; };
 
   // ---- load step 3: member rows of Q, one tile of 16 at a time --------------------
+  // (most items have one tile; a later tile's rows are requested when it starts)
   float bq[KS];
-  buf_load<KS>(rq, qoff(row0), 0, bq, T{});
   for (int mt = 0; mt < sz; mt += 16) {
     const bool more = mt + 16 < sz;
-    float nbq[KS];
+    buf_load<KS>(rq, qoff(row0), 0, bq, T{});
     int row2 = -1;
-    if (more) {
-      buf_load<KS>(rq, qoff(row1), 0, nbq, T{});
-      row2 = mt + 32 + c < sz ? mem[mt + 32 + c] : -1;
-    }
+    if (more) row2 = mt + 32 + c < sz ? mem[mt + 32 + c] : -1;
     v4f sacc[NKT];
     float mx = -INFINITY;
 #pragma unroll
@@ -1165,14 +1165,10 @@ __global__ __launch_bounds__(256) void sparse_kernel(AttnArgs a) {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt) o[i * DT + dt] = oacc[dt][i] + vbf[i * DT + dt];
+      for (int dt = 0; dt < DT; ++dt) o[i * DT + dt] = oacc[dt][i] + vbs[wave][DT * 4 * g + i * DT + dt];
     buf_store<4 * DT>(ro, row0 >= 0 ? static_cast<uint32_t>(row0) * D * ESZ + DT * 4 * g * ESZ : kNone, 0, o, T{});
     row0 = row1;
     row1 = row2;
-    if (more) {
-#pragma unroll
-      for (int s = 0; s < KS; ++s) bq[s] = nbq[s];
-    }
   }
 }
 
