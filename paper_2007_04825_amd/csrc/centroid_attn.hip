@@ -975,13 +975,14 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
 //                     B = P^T straight from the S^T result registers.
 // Lane (query c, group g) ends with dims DT*4g .. DT*4g + 4*DT - 1 of its row.
 // ---------------------------------------------------------------------------
-// d = 32 with k <= 32: the register budget of seven waves per SIMD (69
-// registers for fp32, no spills; measured faster than the six that the
-// unconstrained allocation allows)
-template <int D, int NKT>
-constexpr int kSparseMinWaves = (D == 32 && NKT <= 2) ? 7 : 1;
+// Register budgets that fit without spills and measured faster than the
+// unconstrained allocation: seven waves per SIMD for d = 32 with k <= 32 (69
+// registers in fp32, against six waves), six for bf16 d = 64 with k <= 32
+// (against five)
 template <int D, typename T, int NKT>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kSparseMinWaves<D, NKT>))) void sparse_kernel(AttnArgs a) {
+constexpr int kSparseMinWaves = (D == 32 && NKT <= 2) ? 7 : (D == 64 && NKT == 2 && sizeof(T) == 2) ? 6 : 1;
+template <int D, typename T, int NKT>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kSparseMinWaves<D, T, NKT>))) void sparse_kernel(AttnArgs a) {
   constexpr int KS = D / 4, DT = D / 16;
   constexpr uint32_t ESZ = sizeof(T);
   constexpr uint32_t kNone = 0x80000000u;  // past every buffer: loads read 0, stores are dropped
