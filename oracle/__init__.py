@@ -31,7 +31,7 @@ def build(force: bool = True) -> str:
     ):
         return _LIB
     tmp = _LIB + ".tmp%d" % os.getpid()
-    cmd = ["gcc", "-O2", "-std=c11", "-fno-fast-math", "-fopenmp", "-fPIC",
+    cmd = ["gcc", "-O3", "-std=c11", "-fno-fast-math", "-fopenmp", "-fPIC",
            "-shared", _SRC, "-o", tmp, "-lm"]
     subprocess.run(cmd, check=True)
     os.replace(tmp, _LIB)

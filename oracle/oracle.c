@@ -39,7 +39,13 @@
  *     part Vb_j, all of which depend on the centroid attention.
  *
  * Parity status: every function here is pinned by the CPU test-suite against
- * closed forms, brute force or special cases; none is marked unpinned.
+ * something other than itself (exact rational arithmetic, brute force,
+ * closed forms, special cases that reduce to textbook attention, finite
+ * differences); none is marked unpinned.  The projections are pinned to
+ * exact rational dot products within the fp64 summation bound and to the
+ * hash codes; exact attention to numpy's softmax attention, closed forms and
+ * its permutation symmetries.  The whole file also runs clean under
+ * AddressSanitizer and UndefinedBehaviorSanitizer (sanitize_check.c).
  */
 #include <math.h>
 #include <stdint.h>
@@ -302,9 +308,11 @@ void orc_iclustered_from_assign(const double* q, const double* k,
   double* s = (double*)malloc(sizeof(double) * (size_t)(n > 0 ? n : 1));
   double* a = (double*)malloc(sizeof(double) * (size_t)(n > 0 ? n : 1));
   char* in_t = (char*)malloc((size_t)(n > 0 ? n : 1));
-  int32_t* tj = (int32_t*)malloc(sizeof(int32_t) * (size_t)(ke > 0 ? ke : 1));
+  /* a caller-supplied set may hold up to topk entries */
+  const int tcap = topk > ke ? topk : (ke > 0 ? ke : 1);
+  int32_t* tj = (int32_t*)malloc(sizeof(int32_t) * (size_t)tcap);
   double* vb = (double*)malloc(sizeof(double) * (size_t)d);
-  double* w = (double*)malloc(sizeof(double) * (size_t)(ke > 0 ? ke : 1));
+  double* w = (double*)malloc(sizeof(double) * (size_t)tcap);
   orc_centroids(q, n, d, assign, C, qc, sizes);
   if (topk_out)
     for (int64_t x = 0; x < (int64_t)C * topk; ++x) topk_out[x] = -1;

@@ -350,3 +350,80 @@ def test_forward_masks_padding_and_matches_per_unit_path():
                     out, _, _ = oracle.clustered_from_assign(q[b, h, :n], w.k[b, h, :n],
                                                              w.v[b, h, :n], a, w.C)
                 np.testing.assert_array_equal(res["out"][b, h, :n], out)
+
+
+# --------------------------------------------------------------------------
+# Projection values (Section 3.2.2) and exact attention (Section 3.1, Eq. 1-2).
+# The projections are pinned to exact rational dot products within the error
+# bound of recursive fp64 summation (each product of two fp32 values is exact
+# in fp64), and their packed signs must be the hash codes; a wrong plane
+# index, a transposed operand or a wrong output layout fails.  Exact attention
+# is pinned to numpy's softmax attention, to closed forms (zero keys give the
+# mean value row, one key gives its value row) and to the permutation
+# symmetries of the definition.
+# --------------------------------------------------------------------------
+
+def gamma(m):
+    u = 2.0 ** -53
+    return m * u / (1 - m * u)
+
+
+@pytest.mark.parametrize("seed,n,d,nb,bf16_planes", [(0, 9, 4, 7, True), (1, 6, 32, 63, True),
+                                                     (2, 5, 64, 64, False), (3, 3, 8, 1, False)])
+def test_projections_match_exact_rational_dot_products(seed, n, d, nb, bf16_planes):
+    q, _, _ = gen.random_unit(20 + seed, n, d)
+    planes = np.random.default_rng(seed).standard_normal((nb, d)).astype(np.float32)
+    if bf16_planes:
+        planes = gen.round_bf16(planes)
+    proj = oracle.projections(q, planes)
+    assert proj.shape == (n, nb)
+    for i in range(n):
+        for b in range(nb):
+            terms = [Fraction(float(x)) * Fraction(float(y)) for x, y in zip(q[i], planes[b])]
+            exact = sum(terms)
+            bound = gamma(d - 1) * float(sum(abs(t) for t in terms))
+            assert abs(float(Fraction(float(proj[i, b])) - exact)) <= bound
+    packed = np.zeros(n, np.uint64)
+    for b in range(nb):
+        packed |= (proj[:, b] > 0).astype(np.uint64) << np.uint64(b)
+    assert np.array_equal(packed, oracle.hash_codes(q, planes))
+
+
+@pytest.mark.parametrize("n,d", [(1, 4), (13, 8), (70, 32), (33, 64)])
+def test_full_attention_equals_numpy_softmax_attention(n, d):
+    q, k, v = gen.random_unit(300 + n, n, d, scale=1.5)
+    out = oracle.full_attention(q, k, v)
+    ref, _ = exact_attention(q, k, v)
+    np.testing.assert_allclose(out, ref, rtol=0, atol=1e-12)
+    if n == 1:
+        np.testing.assert_array_equal(out, v.astype(np.float64))     # one key: its value row
+
+
+def test_full_attention_closed_forms_and_symmetries():
+    n, d = 24, 16
+    q, k, v = gen.random_unit(41, n, d)
+    # zero keys: uniform weights, every row is the mean value row
+    out0 = oracle.full_attention(q, np.zeros_like(k), v)
+    np.testing.assert_allclose(out0, np.broadcast_to(v.astype(np.float64).mean(0), (n, d)),
+                               rtol=0, atol=1e-14)
+    out = oracle.full_attention(q, k, v)
+    perm = np.random.default_rng(41).permutation(n)
+    # a joint permutation of keys and values leaves every row unchanged ...
+    np.testing.assert_allclose(oracle.full_attention(q, k[perm], v[perm]), out, rtol=0, atol=1e-13)
+    # ... and a permutation of the queries permutes the rows
+    np.testing.assert_allclose(oracle.full_attention(q[perm], k, v), out[perm], rtol=0, atol=1e-13)
+    # the 1/sqrt(d) scale: doubling q and halving k changes nothing
+    np.testing.assert_allclose(oracle.full_attention(2 * q, k / 2, v), out, rtol=0, atol=1e-13)
+    # singleton clusters of the clustered oracle are exact attention
+    sing, _, _ = oracle.clustered_from_assign(q, k, v, np.arange(n), n)
+    np.testing.assert_allclose(sing, out, rtol=0, atol=1e-12)
+
+
+def test_centroid_row_logits_and_softmax():
+    """Eq. (4) for one row: logits Q^c_j . K_l / sqrt(d) and their softmax."""
+    q, k, _ = gen.random_unit(51, 40, 32)
+    qc = q[:7].astype(np.float64).mean(0)
+    s, a = oracle.centroid_row(qc, k)
+    np.testing.assert_allclose(s, k.astype(np.float64) @ qc / np.sqrt(32), rtol=0, atol=1e-13)
+    np.testing.assert_allclose(a, softmax_rows(s[None])[0], rtol=0, atol=1e-15)
+    assert abs(a.sum() - 1.0) < 1e-14
