@@ -1,16 +1,19 @@
 """Benchmark of the clustered / improved-clustered attention forward pass.
 
-One step = one clustered forward and one improved-clustered forward over the
-whole batch of the speech-encoder-shaped workload (32 sequences x 6 heads,
-padded length 800 with lengths uniform in [400, 800], d = 32, fp32, C = 100,
-63-bit hashes, 10 Lloyd rounds, top-32 keys), i.e. every stage of both
-variants.  Inputs are seeded synthetic data already resident in HBM.
+Default line: one step = one clustered forward and one improved-clustered
+forward over the length-sweep workload at N = 32768 (batch 1, 8 heads, d 64,
+fp32, iid N(0, 1) queries, keys and values, C = 100, 63-bit hashes, 10 Lloyd
+rounds, top-32 keys), i.e. every stage of both variants on the largest
+single-GPU configuration that runs both of them.  --speech gives the same line
+on the speech-encoder-shaped workload (32 x 6 x 800, ragged lengths, d 32).
+Inputs are seeded synthetic data already resident in HBM.
 
 Prints one JSON line.  value = queries answered per second, counting each
 valid (sequence, head, position) once per variant.  The roofline entry times
-the dominant stage with HIP events recorded by the library around its kernels
-on the call's stream, in every eighth timed step; the cpu_baseline entry times
-the fp64 oracle on the host's cores on the same workload.
+the dominant kernel with HIP events recorded by the library around it on the
+call's stream, in every eighth timed step; "phases" gives every stage's
+achieved rate against its bound; the cpu_baseline entry times the fp64 oracle
+on the host's cores on the same workload.
 """
 from __future__ import annotations
 
@@ -80,32 +83,44 @@ class Hip:
 
 def stage_work(w, stage, variant_topk):
     """Algorithmic work of one launch of a stage over the whole batch:
-    returns (amount, unit, bound, peak) for the roofline entry."""
+    returns (amount, unit, bound, peak) for the roofline entry.  Per
+    (sequence, head) of valid length n, with C_eff = min(C, n):
+      hash: read Q, write the codes (n d s + 8 n bytes);
+      kmeans: L n C_eff Hamming distances, each a 64-entry int8 dot product
+        on the matrix cores (2 * 64 operations);
+      centroids: gather Q once, read the member list (n d s + 4 n bytes);
+      centroid attention (the tile kernel, or tile + merge): Q^c K^T and A^c V,
+        2 C_eff n d flops each;
+      output: clustered, write every row and read the assignment (n d s + 4 n);
+        improved, gather Q and the T rows of K and V (C_eff k rows each), write
+        every row."""
     H = w.q.shape[1]
     D = w.q.shape[3]
-    nsum = int(w.lengths.astype(np.int64).sum()) * H        # valid queries = valid keys
+    lens = w.lengths.astype(np.int64)
+    nsum = int(lens.sum()) * H                                   # valid queries = valid keys
+    cn = int((np.minimum(lens, w.C) * lens).sum()) * H          # sum over units of C_eff n
+    ceff = int(np.minimum(lens, w.C).sum()) * H                 # sum over units of C_eff
     s = 4 if w.dtype == "f32" else 2
-    if stage == "centroid_attn":
-        # Q^c K^T and A^c V: 2 * C * n * d flops each, per (sequence, head)
-        flops = 4.0 * w.C * nsum * D
-        return flops, "TFLOP/s", "mfma", PEAKS["fp32_mfma_TFLOPs"]
+    if stage in ("centroid_attn", "attn_tile"):
+        flops = 4.0 * cn * D
+        peak = PEAKS["fp32_mfma_TFLOPs"] if w.dtype == "f32" else PEAKS["bf16_mfma_TFLOPs"]
+        return flops, "TFLOP/s", "mfma", peak
     if stage == "kmeans":
-        # L rounds x n x C Hamming distances, each a 64-entry int8 dot product
-        ops = 2.0 * 64 * w.L * nsum * w.C
+        ops = 2.0 * 64 * w.L * cn
         return ops, "TOP/s", "mfma", PEAKS["int8_mfma_TOPs"]
     if stage == "hash":
-        byts = nsum * D * s + nsum * 8                          # read Q, write codes
+        byts = nsum * D * s + nsum * 8
         return byts, "GB/s", "hbm", PEAKS["hbm_GBps"]
     if stage == "output":
         if variant_topk:
-            # improved per-query part: gather Q, the T rows of K and V (C k rows
-            # each per sequence and head), scatter out
-            byts = 2 * nsum * D * s + 2 * H * w.q.shape[0] * w.C * variant_topk * D * s
+            kk = np.minimum(lens, variant_topk)
+            trow = int((np.minimum(lens, w.C) * kk).sum()) * H   # sum of C_eff k_eff
+            byts = 2 * nsum * D * s + 2 * trow * D * s
         else:
-            byts = nsum * D * s + nsum * 4                      # write out, read assign
+            byts = nsum * D * s + nsum * 4
         return byts, "GB/s", "hbm", PEAKS["hbm_GBps"]
     if stage == "centroids":
-        byts = nsum * D * s + nsum * 4
+        byts = nsum * D * s + nsum * 4 + ceff * D * 4
         return byts, "GB/s", "hbm", PEAKS["hbm_GBps"]
     raise ValueError(stage)
 
@@ -123,12 +138,12 @@ def kernel_source_hash():
     return h.hexdigest()
 
 
-def measured_traffic(kernel_key):
+def measured_traffic(kernel_key, profile="speech_b32h6n800_d32_f32"):
     """HBM bytes per launch of the given kernel from the committed counter
-    profile (FETCH_SIZE and WRITE_SIZE, each scaled by the same counter's
-    reading for a plain copy of known size), or None when there is no such
-    profile or the kernel sources changed after it was taken."""
-    path = os.path.join(ROOT, "profiles", "speech_b32h6n800_d32_f32_hbm_counters.json")
+    profile of the workload (FETCH_SIZE and WRITE_SIZE, each scaled by the same
+    counter's reading for a plain copy of known size), or None when there is no
+    such profile or the kernel sources changed after it was taken."""
+    path = os.path.join(ROOT, "profiles", profile + "_hbm_counters.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
@@ -151,9 +166,10 @@ def cpu_threads():
 
 def cpu_baseline(w, min_seconds=10.0, max_passes=1000):
     """Times the fp64 oracle (both variants) on the same workload for at
-    least min_seconds."""
+    least min_seconds.  The oracle runs the (sequence, head) units in
+    parallel, so it uses min(host threads, units) threads."""
     import oracle
-    threads = cpu_threads()
+    threads = min(cpu_threads(), w.q.shape[0] * w.q.shape[1])
     q = np.nan_to_num(w.q, nan=0.0)
     oracle.forward(q[:1], w.k[:1], w.v[:1], w.lengths[:1], w.planes, w.C, w.n_bits, w.L, w.topk,
                    num_threads=threads, exports=False)  # load / warm
@@ -168,6 +184,7 @@ def cpu_baseline(w, min_seconds=10.0, max_passes=1000):
             break
     queries = 2 * w.queries() * passes
     return {"value": queries / el, "unit": "queries/s", "cores": threads, "kind": "oracle",
+            "cpu": cpu_model(),
             "sample": "%d passes of the full workload, both variants (%.1f s)" % (passes, el)}
 
 
@@ -597,15 +614,209 @@ def copy_calibration(nbytes):
     print(json.dumps({"copy_calibration_bytes": nbytes}))
 
 
+def cpu_model():
+    """The host CPU's model name (from /proc/cpuinfo), or the platform string."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or platform.machine()
+
+
+def phase_entry(w, stage, variant_topk, us):
+    """Achieved rate of one stage launch (the whole batch) against its bound."""
+    amount, unit, bound, peak = stage_work(w, stage, variant_topk)
+    if us is None or us <= 0:
+        return None
+    achieved = amount / (us * 1e-6) / (1e9 if unit == "GB/s" else 1e12)
+    return {"us": round(us, 2), "achieved": round(achieved, 3), "unit": unit, "bound": bound,
+            "peak": peak, "frac": round(achieved / peak, 5)}
+
+
+HEADLINE = {
+    "workload": "length-sweep point: batch 1, heads 8, N 32768, d 64, fp32, iid N(0,1) Q/K/V, "
+                "C 100, B 63, L 10, k 32; clustered + i-clustered",
+    "profile": "sweep_b1h8n32768_d64_f32",
+}
+SPEECH = {
+    "workload": "speech-encoder layer: batch 32, heads 6, N 800 (lengths 400-800), d 32, fp32, "
+                "C 100, B 63, L 10, k 32; clustered + i-clustered",
+    "profile": "speech_b32h6n800_d32_f32",
+}
+
+
+def bench_forward(args, w, desc):
+    """One step = one clustered and one improved-clustered forward call over
+    the whole batch of workload w (inputs resident in HBM).  Prints the
+    headline JSON line: value = valid queries answered per second (each
+    variant counted), over exactly args.steps back-to-back steps between two
+    events; the roofline entry of the dominant kernel, timed with event pairs
+    that the library records around it on the call's stream in every eighth
+    timed step; every stage's achieved rate; the per-step median of separately
+    timed steps; and the fp64 oracle on the host's cores."""
+    import torch
+
+    import paper_2007_04825_amd as ca
+
+    B, H, N, D = w.q.shape
+    dt = ca.CA_F32 if w.dtype == "f32" else ca.CA_BF16
+    tdt = torch.float32 if w.dtype == "f32" else torch.bfloat16
+    dev = torch.device("cuda:0")
+    q, k, v = (torch.from_numpy(np.nan_to_num(x, nan=0.0)).to(dev).to(tdt) for x in (w.q, w.k, w.v))
+    planes = torch.from_numpy(w.planes).to(dev)
+    lengths = torch.from_numpy(w.lengths).to(dev)
+    ws = torch.empty(max(ca.workspace_bytes(B, H, N, D, dt, w.C, w.n_bits, w.topk),
+                         ca.workspace_bytes(B, H, N, D, dt, w.C, w.n_bits, 0)),
+                     dtype=torch.uint8, device=dev)
+    out_c = torch.empty_like(q)
+    out_i = torch.empty_like(q)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    hip = Hip()
+    lib = ca.library()
+
+    def call(topk):
+        if topk:
+            ca.iclustered_attention(q, k, v, planes, w.C, w.n_bits, w.L, topk, lengths=lengths,
+                                    out=out_i, workspace=ws)
+        else:
+            ca.clustered_attention(q, k, v, planes, w.C, w.n_bits, w.L, lengths=lengths,
+                                   out=out_c, workspace=ws)
+
+    def step():
+        call(0)
+        call(w.topk)
+
+    # per-stage times (one event pair per stage and variant, median of 5 calls)
+    stages = dict(ca.STAGES)
+    stages["attn_tile"] = ca.CA_KERNEL_ATTN_TILE
+
+    def stage_times(reps=5):
+        tot = {}
+        for name, sid in stages.items():
+            for topk in (0, w.topk):
+                ts = []
+                for _ in range(reps):
+                    e0, e1 = hip.event(), hip.event()
+                    assert lib.ca_time_next_stage(sid, e0, e1) == 0
+                    call(topk)
+                    ms = hip.elapsed_ms(e0, e1)
+                    hip.destroy(e0)
+                    hip.destroy(e1)
+                    if ms is None:
+                        break
+                    ts.append(ms)
+                if ts:
+                    tot[(name, topk)] = float(np.median(ts))
+        return tot
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    st = stage_times()
+    # the dominant kernel: the largest single-kernel stage (the K-means and
+    # centroid stages may hold several kernels, the centroid-attention stage
+    # the tile kernel and a merge)
+    single = [key for key in st if key[0] in ("hash", "attn_tile", "output")
+              or (key[0] == "kmeans" and args.stage == "kmeans")]
+    if args.stage == "auto":
+        name, var_topk = max(single, key=st.get)
+    else:
+        name = args.stage
+        var_topk = w.topk if st.get((name, w.topk), 0) >= st.get((name, 0), 0) else 0
+
+    # timed region: exactly args.steps steps between two events; the dominant
+    # kernel of the chosen variant is timed with its own event pair in every
+    # EV_EVERY-th step (an event record between two kernels costs the stream a
+    # few microseconds, which would otherwise be added to every step)
+    sid = stages[name]
+    EV_EVERY = 8
+    evs = [(hip.event(light=True), hip.event(light=True)) if i % EV_EVERY == 0 else None
+           for i in range(args.steps)]
+    t_start, t_stop = hip.event(), hip.event()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    hip.record(t_start, stream)
+    for i in range(args.steps):
+        if var_topk == 0 and evs[i] is not None:
+            assert lib.ca_time_next_stage(sid, evs[i][0], evs[i][1]) == 0
+        call(0)
+        if var_topk and evs[i] is not None:
+            assert lib.ca_time_next_stage(sid, evs[i][0], evs[i][1]) == 0
+        call(w.topk)
+    hip.record(t_stop, stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    total_ms = hip.elapsed_ms(t_start, t_stop)
+    timed = [e for e in evs if e is not None]
+    stage_ms = sum(hip.elapsed_ms(a, b) for a, b in timed) / len(timed)
+    ms_per_step = total_ms / args.steps
+    queries_per_step = 2 * w.queries()
+    value = queries_per_step / (ms_per_step * 1e-3)
+    # per-step and per-call medians from separately timed steps
+    med_step = _timed(hip, stream, step, 21)
+    med_c = _timed(hip, stream, lambda: call(0), 21)
+    med_i = _timed(hip, stream, lambda: call(w.topk), 21)
+
+    amount, unit, bound, peak = stage_work(w, name, var_topk)
+    achieved = amount / (stage_ms * 1e-3) / (1e12 if unit != "GB/s" else 1e9)
+    kernel_key = "%s (%s)" % (name, "iclustered" if var_topk else "clustered")
+    roof = {"bound": bound, "achieved": round(achieved, 3), "peak": peak, "unit": unit,
+            "frac": round(achieved / peak, 5),
+            "traffic": measured_traffic(kernel_key, desc["profile"]),
+            "kernel": kernel_key, "avg_launch_us": round(stage_ms * 1e3, 3)}
+    phases = {}
+    for (n_, t_), ms in sorted(st.items()):
+        if n_ == "centroid_attn":
+            continue  # the tile kernel is reported alone; the merge is the difference
+        e = phase_entry(w, n_, t_, ms * 1e3)
+        if e is not None:
+            phases["%s_%s" % (n_, "ic" if t_ else "c")] = e
+    for t_ in (0, w.topk):
+        if ("centroid_attn", t_) in st and ("attn_tile", t_) in st:
+            phases["attn_merge_%s" % ("ic" if t_ else "c")] = {
+                "us": round((st[("centroid_attn", t_)] - st[("attn_tile", t_)]) * 1e3, 2)}
+    cpu = None if args.no_cpu_baseline else cpu_baseline(w)
+    rec = {
+        "metric": "queries/sec/GPU of clustered & i-clustered attn fwd",
+        "value": round(value, 1),
+        "unit": "queries/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "median_ms_per_step": round(med_step, 5),
+        "wall_ms_per_step": round(wall / args.steps * 1e3, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": desc["workload"], "global_batch": B, "seq_len": N,
+                   "parallelism": "none"},
+        "per_call_median_ms": {"clustered": round(med_c, 5), "iclustered": round(med_i, 5)},
+        "phases": phases,
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(rec))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--stage", default="auto",
-                    choices=["auto", "hash", "kmeans", "centroids", "centroid_attn", "output"])
+                    choices=["auto", "hash", "kmeans", "centroids", "centroid_attn", "attn_tile",
+                             "output"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES")
+    ap.add_argument("--speech", action="store_true",
+                    help="the headline line on the speech-encoder workload (32 x 6 x 800, d 32)")
     ap.add_argument("--backward", action="store_true",
                     help="time the backward pass instead (its own JSON line)")
     ap.add_argument("--sweep", action="store_true",
@@ -641,134 +852,12 @@ def main():
         bench_oracle_top(args)
         return
 
-    import torch
-
     import gen
-    import paper_2007_04825_amd as ca
 
-    w = gen.make_config(2)
-    B, H, N, D = w.q.shape
-    dev = torch.device("cuda:0")
-    q, k, v = (torch.from_numpy(x).to(dev) for x in (w.q, w.k, w.v))
-    planes = torch.from_numpy(w.planes).to(dev)
-    lengths = torch.from_numpy(w.lengths).to(dev)
-    ws = torch.empty(max(ca.workspace_bytes(B, H, N, D, 0, w.C, w.n_bits, w.topk),
-                         ca.workspace_bytes(B, H, N, D, 0, w.C, w.n_bits, 0)),
-                     dtype=torch.uint8, device=dev)
-    out_c = torch.empty_like(q)
-    out_i = torch.empty_like(q)
-    stream = torch.cuda.current_stream(dev).cuda_stream
-    hip = Hip()
-
-    def step():
-        ca.clustered_attention(q, k, v, planes, w.C, w.n_bits, w.L, lengths=lengths, out=out_c,
-                               workspace=ws)
-        ca.iclustered_attention(q, k, v, planes, w.C, w.n_bits, w.L, w.topk, lengths=lengths,
-                                out=out_i, workspace=ws)
-
-    # per-stage times (one event pair per stage and variant) to find the dominant stage
-    def stage_times(reps=5):
-        tot = {}
-        for name, sid in ca.STAGES.items():
-            for topk in (0, w.topk):
-                acc = 0.0
-                present = True
-                for _ in range(reps):
-                    e0, e1 = hip.event(), hip.event()
-                    lib = ca.library()
-                    assert lib.ca_time_next_stage(sid, e0, e1) == 0
-                    if topk:
-                        ca.iclustered_attention(q, k, v, planes, w.C, w.n_bits, w.L, topk,
-                                                lengths=lengths, out=out_i, workspace=ws)
-                    else:
-                        ca.clustered_attention(q, k, v, planes, w.C, w.n_bits, w.L,
-                                               lengths=lengths, out=out_c, workspace=ws)
-                    ms = hip.elapsed_ms(e0, e1)
-                    hip.destroy(e0)
-                    hip.destroy(e1)
-                    if ms is None:
-                        present = False
-                        break
-                    acc += ms
-                if present:
-                    tot[(name, topk)] = acc / reps
-        return tot
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    st = stage_times()
-    if args.stage == "auto":
-        name, var_topk = max(st, key=st.get)
+    if args.speech:
+        bench_forward(args, gen.make_config(2), SPEECH)
     else:
-        name = args.stage
-        var_topk = w.topk if st[(name, w.topk)] >= st[(name, 0)] else 0
-
-    # timed region: K steps; the dominant stage of the chosen variant is timed
-    # with its own event pair in every EV_EVERY-th step (an event record
-    # between two kernels still costs the stream a few microseconds, which
-    # would otherwise be added to every step)
-    sid = ca.STAGES[name]
-    EV_EVERY = 8
-    evs = [(hip.event(light=True), hip.event(light=True)) if i % EV_EVERY == 0 else None
-           for i in range(args.steps)]
-    t_start, t_stop = hip.event(), hip.event()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    hip.record(t_start, stream)
-    lib = ca.library()
-    for i in range(args.steps):
-        if var_topk == 0 and evs[i] is not None:
-            assert lib.ca_time_next_stage(sid, evs[i][0], evs[i][1]) == 0
-        ca.clustered_attention(q, k, v, planes, w.C, w.n_bits, w.L, lengths=lengths, out=out_c,
-                               workspace=ws)
-        if var_topk and evs[i] is not None:
-            assert lib.ca_time_next_stage(sid, evs[i][0], evs[i][1]) == 0
-        ca.iclustered_attention(q, k, v, planes, w.C, w.n_bits, w.L, w.topk, lengths=lengths,
-                                out=out_i, workspace=ws)
-    hip.record(t_stop, stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    total_ms = hip.elapsed_ms(t_start, t_stop)
-    timed = [e for e in evs if e is not None]
-    stage_ms = sum(hip.elapsed_ms(a, b) for a, b in timed) / len(timed)
-    ms_per_step = total_ms / args.steps
-    queries_per_step = 2 * w.queries()
-    value = queries_per_step / (ms_per_step * 1e-3)
-
-    amount, unit, bound, peak = stage_work(w, name, var_topk)
-    achieved = amount / (stage_ms * 1e-3) / (1e12 if unit != "GB/s" else 1e9)
-    kernel_key = "%s (%s)" % (name, "iclustered" if var_topk else "clustered")
-    roof = {"bound": bound, "achieved": round(achieved, 3), "peak": peak, "unit": unit,
-            "frac": round(achieved / peak, 5), "traffic": measured_traffic(kernel_key),
-            "kernel": kernel_key,
-            "avg_launch_us": round(stage_ms * 1e3, 3)}
-    stages_us = {"%s_%s" % (n, "ic" if t else "c"): round(v * 1e3, 2) for (n, t), v in st.items()}
-    cpu = None if args.no_cpu_baseline else cpu_baseline(w)
-    rec = {
-        "metric": "queries/sec/GPU of clustered & i-clustered attn fwd",
-        "value": round(value, 1),
-        "unit": "queries/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 5),
-        "wall_ms_per_step": round(wall / args.steps * 1e3, 5),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "f32",
-        "data": "synthetic",
-        "config": {"workload": "speech-encoder layer: batch 32, heads 6, N 800 (lengths 400-800), "
-                               "d 32, fp32, C 100, B 63, L 10, k 32; clustered + i-clustered",
-                   "global_batch": B, "seq_len": N, "parallelism": "none"},
-        "per_variant_ms": {"stage_sum_clustered": round(sum(v for (n, t), v in st.items() if t == 0), 4),
-                           "stage_sum_iclustered": round(sum(v for (n, t), v in st.items() if t), 4)},
-        "stages_us": stages_us,
-        "roofline": roof,
-        "cpu_baseline": cpu,
-    }
-    print(json.dumps(rec))
+        bench_forward(args, gen.make_config(3, N=32768, dtype="f32"), HEADLINE)
 
 
 if __name__ == "__main__":

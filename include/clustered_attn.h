@@ -255,6 +255,9 @@ int ca_version(void);
  *   CA_KERNEL_OUTPUT         broadcast (Eq. 6) or the improved per-query part
  *   CA_KERNEL_BWD_CENTROID   (backward calls) the centroid part of the
  *                            gradient: dK, dV and the dQ^c partials
+ *   CA_KERNEL_ATTN_TILE      the centroid-attention kernel alone (Eqs. 4-5 on
+ *                            the matrix cores), without the merge of several
+ *                            key chunks that CA_KERNEL_CENTROID_ATTN includes
  */
 #define CA_KERNEL_HASH 1
 #define CA_KERNEL_KMEANS 2
@@ -262,6 +265,7 @@ int ca_version(void);
 #define CA_KERNEL_CENTROID_ATTN 4
 #define CA_KERNEL_OUTPUT 5
 #define CA_KERNEL_BWD_CENTROID 6
+#define CA_KERNEL_ATTN_TILE 7
 
 /*
  * Profiling hook for callers that time one stage with HIP events: in the

@@ -38,6 +38,7 @@ EXPORTED_SYMBOLS = ("ca_workspace_bytes", "clustered_attention_fwd", "iclustered
 CA_KERNEL_HASH, CA_KERNEL_KMEANS, CA_KERNEL_CENTROIDS, CA_KERNEL_CENTROID_ATTN, CA_KERNEL_OUTPUT = \
     1, 2, 3, 4, 5
 CA_KERNEL_BWD_CENTROID = 6
+CA_KERNEL_ATTN_TILE = 7
 STAGES = {"hash": 1, "kmeans": 2, "centroids": 3, "centroid_attn": 4, "output": 5}
 
 _HERE = os.path.dirname(os.path.abspath(__file__))

@@ -228,7 +228,10 @@ static int run_forward(const void* q, const void* k, const void* v, const int32_
     CA_TRY(mark(CA_KERNEL_CENTROIDS, false, s));
   }
   CA_TRY(mark(CA_KERNEL_CENTROID_ATTN, true, s));
-  CA_TRY(launch_centroid_attention(p, ws, improved && aux ? aux->topk_in : nullptr, s));
+  CA_TRY(mark(CA_KERNEL_ATTN_TILE, true, s));
+  CA_TRY(launch_centroid_attention(p, ws, improved && aux ? aux->topk_in : nullptr, 0, s));
+  CA_TRY(mark(CA_KERNEL_ATTN_TILE, false, s));
+  CA_TRY(launch_centroid_attention(p, ws, improved && aux ? aux->topk_in : nullptr, 1, s));
   CA_TRY(mark(CA_KERNEL_CENTROID_ATTN, false, s));
   CA_TRY(mark(CA_KERNEL_OUTPUT, true, s));
   if (improved) CA_TRY(launch_sparse(p, ws, s));
@@ -489,7 +492,7 @@ const char* ca_last_error(void) { return ca::g_last_error.c_str(); }
 int ca_version(void) { return 100; }
 
 int ca_time_next_stage(int stage, void* start_event, void* stop_event) {
-  if (stage < 0 || stage > CA_KERNEL_BWD_CENTROID || (stage != 0 && (!start_event || !stop_event)))
+  if (stage < 0 || stage > CA_KERNEL_ATTN_TILE || (stage != 0 && (!start_event || !stop_event)))
     return ca::fail(CA_ERR_INVALID_ARG, "invalid stage %d or null event", stage);
   ca::g_ev_kernel = stage;
   ca::g_ev_start = static_cast<hipEvent_t>(start_event);

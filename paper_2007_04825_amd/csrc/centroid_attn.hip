@@ -1234,26 +1234,33 @@ static AttnArgs make_args(const Problem& p, const Workspace& ws, const int32_t* 
 // Key tiles of the register-resident sparse routine (k <= 16 * NKT).
 static int sparse_tiles(int topk) { return topk <= 16 ? 1 : topk <= 32 ? 2 : topk <= 64 ? 4 : 8; }
 
+// part 0: the tile kernel (single chunk: the whole stage); part 1: the merge
+// of several chunks (nothing for a single chunk).
 template <int D, typename T>
 static hipError_t launch_attn_t(const Problem& p, const Workspace& ws, const int32_t* topk_in,
-                                hipStream_t s) {
+                                int part, hipStream_t s) {
   const AttnArgs a = make_args(p, ws, topk_in);
   const bool improved = p.topk > 0;
   const dim3 g1(xcd_grid(static_cast<long long>(a.nchunk) * a.ntile * a.units));
   const dim3 g2(xcd_grid(static_cast<long long>(a.ncg) * a.units));
   if (ws.nchunk == 1) {
+    if (part != 0) return hipSuccess;
     if (improved)
       hipLaunchKernelGGL((attn_tile_kernel<D, T, 1>), g1, dim3(kTileThreads), 0, s, a);
     else
       hipLaunchKernelGGL((attn_flash_kernel<D, T>), g1, dim3(kFlashThreads), 0, s, a);
     return hipGetLastError();
   }
-  if (improved) {
-    hipLaunchKernelGGL((attn_tile_kernel<D, T, 3>), g1, dim3(kTileThreads), 0, s, a);
-    hipLaunchKernelGGL((attn_merge_kernel<D, T, true>), g2, dim3(256), 0, s, a);
+  if (part == 0) {
+    if (improved)
+      hipLaunchKernelGGL((attn_tile_kernel<D, T, 3>), g1, dim3(kTileThreads), 0, s, a);
+    else
+      hipLaunchKernelGGL((attn_tile_kernel<D, T, 2>), g1, dim3(kTileThreads), 0, s, a);
   } else {
-    hipLaunchKernelGGL((attn_tile_kernel<D, T, 2>), g1, dim3(kTileThreads), 0, s, a);
-    hipLaunchKernelGGL((attn_merge_kernel<D, T, false>), g2, dim3(256), 0, s, a);
+    if (improved)
+      hipLaunchKernelGGL((attn_merge_kernel<D, T, true>), g2, dim3(256), 0, s, a);
+    else
+      hipLaunchKernelGGL((attn_merge_kernel<D, T, false>), g2, dim3(256), 0, s, a);
   }
   return hipGetLastError();
 }
@@ -1298,9 +1305,9 @@ hipError_t launch_oracle_top(const Problem& p, const Workspace& ws, hipStream_t 
 // Centroid attention: softmax statistics, values (and, clustered in one key
 // chunk, the output rows via Eq. (6)); improved: top-k, mass and rest part.
 hipError_t launch_centroid_attention(const Problem& p, const Workspace& ws, const int32_t* topk_in,
-                                     hipStream_t s) {
-  if (p.d == 32) return p.dtype == 0 ? launch_attn_t<32, float>(p, ws, topk_in, s) : launch_attn_t<32, bf16_t>(p, ws, topk_in, s);
-  return p.dtype == 0 ? launch_attn_t<64, float>(p, ws, topk_in, s) : launch_attn_t<64, bf16_t>(p, ws, topk_in, s);
+                                     int part, hipStream_t s) {
+  if (p.d == 32) return p.dtype == 0 ? launch_attn_t<32, float>(p, ws, topk_in, part, s) : launch_attn_t<32, bf16_t>(p, ws, topk_in, part, s);
+  return p.dtype == 0 ? launch_attn_t<64, float>(p, ws, topk_in, part, s) : launch_attn_t<64, bf16_t>(p, ws, topk_in, part, s);
 }
 
 // Improved values of every member query (Section 3.3).

@@ -81,8 +81,10 @@ hipError_t launch_centroids(const Problem& p, const Workspace& ws, hipStream_t s
 // Centroid attention: softmax statistics and values; clustered in one key
 // chunk also the output rows (otherwise launch_broadcast writes them);
 // improved: top-k, mass and rest part (launch_sparse then writes the rows).
+// part 0 launches the tile kernel, part 1 the merge of several key chunks
+// (nothing for one chunk).
 hipError_t launch_centroid_attention(const Problem& p, const Workspace& ws, const int32_t* topk_in,
-                                     hipStream_t s);
+                                     int part, hipStream_t s);
 hipError_t launch_sparse(const Problem& p, const Workspace& ws, hipStream_t s);
 hipError_t launch_broadcast(const Problem& p, const int32_t* assign, const Workspace& ws,
                             hipStream_t s);

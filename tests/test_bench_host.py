@@ -25,17 +25,24 @@ def test_more_than_one_gpu_is_refused():
 
 
 def test_stage_work_closed_forms():
-    w = gen.config_speech(B=2, H=3, N=40, d=32, lengths=np.array([40, 25], np.int32))
+    # C = 30 clusters: C_eff = 30 for the sequence of 40 and 25 for that of 25
+    w = gen.config_speech(B=2, H=3, N=40, d=32, C=30, lengths=np.array([40, 25], np.int32))
     nsum = (40 + 25) * 3
+    cn = (30 * 40 + 25 * 25) * 3           # sum over units of C_eff n
     flops, unit, bound, peak = bench.stage_work(w, "centroid_attn", 32)
     assert (unit, bound) == ("TFLOP/s", "mfma") and peak == bench.PEAKS["fp32_mfma_TFLOPs"]
-    assert flops == 2 * (2 * w.C * nsum * 32)  # Q^c K^T and A^c V
+    assert flops == 2 * (2 * cn * 32)      # Q^c K^T and A^c V
+    assert bench.stage_work(w, "attn_tile", 32)[0] == flops
     ops, unit, bound, _ = bench.stage_work(w, "kmeans", 0)
-    assert unit == "TOP/s" and ops == 2 * 64 * w.L * nsum * w.C
+    assert unit == "TOP/s" and ops == 2 * 64 * w.L * cn
     byts, unit, bound, peak = bench.stage_work(w, "hash", 0)
     assert (unit, bound) == ("GB/s", "hbm") and byts == nsum * 32 * 4 + nsum * 8
     assert bench.stage_work(w, "output", 0)[0] == nsum * 32 * 4 + nsum * 4
-    assert bench.stage_work(w, "output", 32)[0] == 2 * nsum * 32 * 4 + 2 * 3 * 2 * w.C * 32 * 32 * 4
+    # the T rows: C_eff k_eff = 30 * 32 and 25 * 25 per head
+    assert bench.stage_work(w, "output", 32)[0] == 2 * nsum * 32 * 4 + 2 * 3 * (30 * 32 + 25 * 25) * 32 * 4
+    assert bench.stage_work(w, "centroids", 0)[0] == nsum * 32 * 4 + nsum * 4 + 3 * (30 + 25) * 32 * 4
+    wb = gen.config_sweep(64, dtype="bf16", H=2, C=10)
+    assert bench.stage_work(wb, "attn_tile", 0)[3] == bench.PEAKS["bf16_mfma_TFLOPs"]
     with pytest.raises(ValueError):
         bench.stage_work(w, "nonsense", 0)
 
@@ -49,6 +56,7 @@ def test_counter_profile_is_withheld_when_sources_change(monkeypatch):
     monkeypatch.setattr(bench, "kernel_source_hash", lambda: prof["source_sha256"])
     assert bench.measured_traffic(key) == prof["kernels"][key]["hbm_bytes_per_launch"]
     assert bench.measured_traffic("no such kernel") is None
+    assert bench.measured_traffic(key, "no_such_workload") is None
     monkeypatch.setattr(bench, "kernel_source_hash", lambda: "0" * 64)
     assert bench.measured_traffic(key) is None
 
