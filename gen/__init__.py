@@ -188,6 +188,18 @@ def config_random(seed: int) -> Workload:
                     C, n_bits, L, topk, dtype)
 
 
+def with_dtype(w: Workload, dtype: str) -> Workload:
+    """The same workload stored as dtype: 'bf16' rounds Q, K and V to the
+    nearest bf16 values, 'f32' leaves them."""
+    import dataclasses
+    if dtype == w.dtype:
+        return w
+    if dtype != "bf16" or w.dtype != "f32":
+        raise ValueError("only fp32 -> bf16 is supported")
+    return dataclasses.replace(w, q=round_bf16(w.q), k=round_bf16(w.k), v=round_bf16(w.v),
+                               dtype="bf16", name=w.name.replace("_f32", "") + "_bf16")
+
+
 def make_config(cfg: int, **kw) -> Workload:
     """The five workloads: 1 tiny, 2 speech, 3 sweep (pass N=, dtype=), 4 encoder,
     5 long."""

@@ -67,6 +67,13 @@ def library():
     if not os.path.exists(lib_path):
         raise RuntimeError("libclustered_attn.so is not built; run "
                            "`python -c 'import __graft_entry__ as g; g.build()'`")
+    # torch ships its own HIP runtime: importing it first makes the library
+    # bind to the runtime that owns the caller's device memory and streams,
+    # whichever of the two the caller touches first
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     lib = ctypes.CDLL(lib_path)
     vp, i32, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
     lib.ca_workspace_bytes.argtypes = [i32] * 8
@@ -150,7 +157,8 @@ def time_next_stage(stage: int, start_event, stop_event):
 
 
 def set_kmeans_path(path: int):
-    """0 automatic, 1 one workgroup per unit, 2 one kernel pair per Lloyd round."""
+    """0 automatic, 1 one workgroup per unit, 2 one kernel pair per Lloyd round,
+    3 one cooperative launch for all rounds."""
     _check(library().ca_set_kmeans_path(int(path)))
 
 

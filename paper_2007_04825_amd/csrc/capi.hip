@@ -71,6 +71,14 @@ size_t carve_workspace(const Problem& p, void* base, Workspace* ws) {
   w.mass = static_cast<float*>(take(p.topk > 0 ? U * C * 4 : 0));
   w.vcb = static_cast<float*>(take(U * C * D * 4));
   w.stats = static_cast<float*>(take(U * C * 2 * 4));
+  w.ncoop = coop_max_blocks(p.n, p.units());
+  w.coop_q = 0;
+  const size_t NC = static_cast<size_t>(w.ncoop);
+  w.sync = static_cast<int32_t*>(take(U * kSyncInts * 4));
+  w.ctab = static_cast<uint64_t*>(take(2 * U * static_cast<size_t>(coop_table_stride(p.C)) * 8));
+  w.cbases = static_cast<int32_t*>(take(U * NC * C * 4));
+  w.clsizes = static_cast<int32_t*>(take(U * NC * C * 4));
+  w.qc_part = static_cast<double*>(take(U * C * NC * D * 8));
   if (ws) *ws = w;
   return off;
 }
@@ -200,13 +208,14 @@ static int run_forward(const void* q, const void* k, const void* v, const int32_
   } while (0)
 
   const uint64_t* codes_in = aux ? aux->codes_in : nullptr;
+  const int driver = kmeans_driver(p);
   if (assign_given) {
     CA_TRY(launch_load_assign(p, aux->assign_in, ws, s));
     CA_TRY(mark(CA_KERNEL_CENTROIDS, true, s));
     CA_TRY(launch_csr(p, ws.assign, ws, s));
     CA_TRY(launch_centroids(p, ws, s));
     CA_TRY(mark(CA_KERNEL_CENTROIDS, false, s));
-  } else if (kmeans_uses_lds(p)) {
+  } else if (driver == 1) {
     // one kernel: hashing, K-means, member lists and centroids
     CA_TRY(mark(CA_KERNEL_KMEANS, true, s));
     CA_TRY(launch_cluster_lds(p, codes_in, ws, s));
@@ -219,13 +228,24 @@ static int run_forward(const void* q, const void* k, const void* v, const int32_
       CA_TRY(launch_hash(p, ws, s));
       CA_TRY(mark(CA_KERNEL_HASH, false, s));
     }
-    CA_TRY(mark(CA_KERNEL_KMEANS, true, s));
-    CA_TRY(launch_kmeans(p, ws, s));
-    CA_TRY(mark(CA_KERNEL_KMEANS, false, s));
-    CA_TRY(mark(CA_KERNEL_CENTROIDS, true, s));
-    CA_TRY(launch_csr(p, ws.assign, ws, s));
-    CA_TRY(launch_centroids(p, ws, s));
-    CA_TRY(mark(CA_KERNEL_CENTROIDS, false, s));
+    if (driver == 3) {
+      // all rounds and the member lists in one cooperative launch
+      ws.coop_q = coop_block_queries(p, ws.ncoop);
+      CA_TRY(mark(CA_KERNEL_KMEANS, true, s));
+      CA_TRY(launch_kmeans_coop(p, ws, s));
+      CA_TRY(mark(CA_KERNEL_KMEANS, false, s));
+      CA_TRY(mark(CA_KERNEL_CENTROIDS, true, s));
+      CA_TRY(launch_coop_centroids(p, ws, s));
+      CA_TRY(mark(CA_KERNEL_CENTROIDS, false, s));
+    } else {
+      CA_TRY(mark(CA_KERNEL_KMEANS, true, s));
+      CA_TRY(launch_kmeans(p, ws, s));
+      CA_TRY(mark(CA_KERNEL_KMEANS, false, s));
+      CA_TRY(mark(CA_KERNEL_CENTROIDS, true, s));
+      CA_TRY(launch_csr(p, ws.assign, ws, s));
+      CA_TRY(launch_centroids(p, ws, s));
+      CA_TRY(mark(CA_KERNEL_CENTROIDS, false, s));
+    }
   }
   CA_TRY(mark(CA_KERNEL_CENTROID_ATTN, true, s));
   CA_TRY(mark(CA_KERNEL_ATTN_TILE, true, s));
@@ -237,7 +257,7 @@ static int run_forward(const void* q, const void* k, const void* v, const int32_
   if (improved) CA_TRY(launch_sparse(p, ws, s));
   if (!improved && ws.nchunk > 1) {
     CA_TRY(launch_broadcast(p, ws.assign, ws, s));  // also zeroes the padded rows
-  } else if (lengths && (assign_given || (codes_in && !kmeans_uses_lds(p)))) {
+  } else if (lengths && (assign_given || (codes_in && driver != 1))) {
     CA_TRY(launch_pad_zero(p, s));  // otherwise the hashing or clustering kernel zeroed them
   }
   CA_TRY(mark(CA_KERNEL_OUTPUT, false, s));
@@ -501,9 +521,10 @@ int ca_time_next_stage(int stage, void* start_event, void* stop_event) {
 }
 
 // Selects the K-means driver (0 automatic, 1 one workgroup per unit, 2 one
-// launch pair per round).  Exposed for tests that cover both drivers.
+// launch pair per round, 3 cooperative).  Exposed for tests that cover every
+// driver.
 int ca_set_kmeans_path(int path) {
-  if (path < 0 || path > 2) return ca::fail(CA_ERR_INVALID_ARG, "path must be 0, 1 or 2");
+  if (path < 0 || path > 3) return ca::fail(CA_ERR_INVALID_ARG, "path must be 0, 1, 2 or 3");
   ca::set_kmeans_path(path);
   return CA_OK;
 }

@@ -79,6 +79,64 @@ __global__ __launch_bounds__(256) void centroid_kernel(const T* __restrict__ q,
   dst[t] = static_cast<float>(acc / static_cast<double>(sz));
 }
 
+// Eq. (3) after the cooperative K-means, in two steps with all the chip's
+// workgroups.  Step 1: for every (unit, block of coop_q queries, cluster)
+// D lanes add the block's members of the cluster (consecutive in the member
+// list, ascending query order) in fp64, 32 rows in flight.  Step 2: the
+// blocks' sums are added in block order and divided by the cluster size.  The
+// association is fixed, so the result is deterministic.
+template <int D, typename T>
+__global__ __launch_bounds__(256) void centroid_part_kernel(const T* __restrict__ q,
+                                                            const int32_t* __restrict__ members,
+                                                            const int32_t* __restrict__ bases,
+                                                            const int32_t* __restrict__ lsizes,
+                                                            int N, int C, int nwg, long long nitems,
+                                                            double* __restrict__ qc_part) {
+  constexpr int GPW = 64 / D;  // items per wave
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const long long item = (static_cast<long long>(blockIdx.x) * 4 + wave) * GPW + lane / D;
+  const int t = lane % D;
+  if (item >= nitems) return;  // item = (u nwg + b) C + j, the layout of bases and lsizes
+  const int j = static_cast<int>(item % C);
+  const long long ub = item / C;
+  const int b = static_cast<int>(ub % nwg);
+  const int u = static_cast<int>(ub / nwg);
+  const int cnt = lsizes[item];
+  const int32_t* mem = members + static_cast<size_t>(u) * N + bases[item];
+  const T* qu = q + static_cast<size_t>(u) * N * D;
+  double acc = 0.0;
+  constexpr int RB = 32;
+  for (int m = 0; m < cnt; m += RB) {
+    int mi[RB];
+#pragma unroll
+    for (int e = 0; e < RB; ++e) mi[e] = mem[min(m + e, cnt - 1)];
+    float x[RB];
+#pragma unroll
+    for (int e = 0; e < RB; ++e) x[e] = to_f32(qu[static_cast<size_t>(mi[e]) * D + t]);
+#pragma unroll
+    for (int e = 0; e < RB; ++e)
+      if (m + e < cnt) acc += static_cast<double>(x[e]);
+  }
+  qc_part[((static_cast<size_t>(u) * C + j) * nwg + b) * D + t] = acc;
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void centroid_final_kernel(const double* __restrict__ qc_part,
+                                                             const int32_t* __restrict__ sizes,
+                                                             int C, int nwg, long long nitems,
+                                                             float* __restrict__ qc) {
+  constexpr int GPW = 64 / D;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const long long item = (static_cast<long long>(blockIdx.x) * 4 + wave) * GPW + lane / D;  // u C + j
+  const int t = lane % D;
+  if (item >= nitems) return;
+  const int sz = sizes[item];
+  const double* pp = qc_part + static_cast<size_t>(item) * nwg * D + t;
+  double acc = 0.0;
+  for (int b = 0; b < nwg; ++b) acc += pp[static_cast<size_t>(b) * D];
+  qc[static_cast<size_t>(item) * D + t] = sz > 0 ? static_cast<float>(acc / static_cast<double>(sz)) : 0.0f;
+}
+
 // ---------------------------------------------------------------------------
 // Small vector helpers for the DT-wide value loads.
 // ---------------------------------------------------------------------------
@@ -1188,6 +1246,28 @@ static hipError_t launch_centroids_t(const Problem& p, const Workspace& ws, hipS
                      dim3(256), 0, s,
                      static_cast<const T*>(p.q), ws.sizes, ws.offsets, ws.members, p.n, p.C, ws.qc);
   return hipGetLastError();
+}
+
+template <int D, typename T>
+static hipError_t launch_coop_centroids_t(const Problem& p, const Workspace& ws, hipStream_t s) {
+  constexpr int per_block = 4 * (64 / D);  // items per workgroup
+  const int nwg = (p.n + ws.coop_q - 1) / ws.coop_q;
+  const long long n1 = static_cast<long long>(p.units()) * nwg * p.C;
+  hipLaunchKernelGGL((centroid_part_kernel<D, T>), dim3(static_cast<unsigned>((n1 + per_block - 1) / per_block)),
+                     dim3(256), 0, s, static_cast<const T*>(p.q), ws.members, ws.cbases, ws.clsizes,
+                     p.n, p.C, nwg, n1, ws.qc_part);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const long long n2 = static_cast<long long>(p.units()) * p.C;
+  hipLaunchKernelGGL((centroid_final_kernel<D>), dim3(static_cast<unsigned>((n2 + per_block - 1) / per_block)),
+                     dim3(256), 0, s, ws.qc_part, ws.sizes, p.C, nwg, n2, ws.qc);
+  return hipGetLastError();
+}
+
+hipError_t launch_coop_centroids(const Problem& p, const Workspace& ws, hipStream_t s) {
+  if (p.d == 32)
+    return p.dtype == 0 ? launch_coop_centroids_t<32, float>(p, ws, s) : launch_coop_centroids_t<32, bf16_t>(p, ws, s);
+  return p.dtype == 0 ? launch_coop_centroids_t<64, float>(p, ws, s) : launch_coop_centroids_t<64, bf16_t>(p, ws, s);
 }
 
 hipError_t launch_centroids(const Problem& p, const Workspace& ws, hipStream_t s) {

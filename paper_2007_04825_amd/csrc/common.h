@@ -359,6 +359,16 @@ __device__ __forceinline__ void buf_store(__amdgpu_buffer_rsrc_t r, uint32_t vof
   }
 }
 
+// Zeroes the arrival counters (sync_ints ints) and both count tables
+// (2 tstride words) of unit u of the cooperative K-means with the threads of
+// workgroup blk of nblk, in the kernel that runs before it.
+__device__ __forceinline__ void coop_reset(int32_t* sync, int sync_ints, uint64_t* tab, int tstride,
+                                           int u, int blk, int nblk, int tid, int nthreads) {
+  if (blk == 0 && tid < sync_ints) sync[u * sync_ints + tid] = 0;
+  uint64_t* t0 = tab + static_cast<size_t>(u) * 2 * tstride;
+  for (int x = blk * nthreads + tid; x < 2 * tstride; x += nblk * nthreads) t0[x] = 0ull;
+}
+
 __device__ __forceinline__ uint32_t order_key(float f) {
   uint32_t u = __float_as_uint(f == 0.0f ? 0.0f : f);
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);

@@ -11,15 +11,20 @@ namespace ca {
 constexpr int kHashThreads = 256;
 constexpr int kHashQB = 256;  // queries per workgroup: four 16-query tiles per wave
 
-// Rows past the valid length get code 0 and, when out is given, a zero output row.
+// Rows past the valid length get code 0 and, when out is given, a zero output
+// row.  The workgroups of each unit also zero the unit's arrival counters and
+// first count table of the cooperative K-means, which runs next.
 template <int D, typename T>
 __global__ __launch_bounds__(kHashThreads) void hash_kernel(const T* __restrict__ q,
                                                             const float* __restrict__ planes,
                                                             const int32_t* __restrict__ lengths,
                                                             int heads, int N, int n_bits,
                                                             uint64_t* __restrict__ codes,
-                                                            T* __restrict__ out) {
+                                                            T* __restrict__ out,
+                                                            int32_t* __restrict__ sync,
+                                                            uint64_t* __restrict__ ctab, int tstride) {
   const int u = blockIdx.y;
+  coop_reset(sync, kSyncInts, ctab, tstride, u, blockIdx.x, gridDim.x, threadIdx.x, kHashThreads);
   const int b = u / heads, h = u % heads;
   const int n = unit_length(lengths, b, N);
   const int q0 = blockIdx.x * kHashQB;
@@ -58,12 +63,16 @@ __global__ __launch_bounds__(kHashThreads) void hash_kernel(const T* __restrict_
   }
 }
 
-// Copies caller-supplied codes, keeping bits below n_bits and zeroing padded rows.
+// Copies caller-supplied codes, keeping bits below n_bits and zeroing padded
+// rows; zeroes the cooperative K-means' counters and table as hash_kernel does.
 __global__ __launch_bounds__(256) void load_codes_kernel(const uint64_t* __restrict__ in,
                                                          const int32_t* __restrict__ lengths,
                                                          int heads, int N, int n_bits,
-                                                         uint64_t* __restrict__ codes) {
+                                                         uint64_t* __restrict__ codes,
+                                                         int32_t* __restrict__ sync,
+                                                         uint64_t* __restrict__ ctab, int tstride) {
   const int u = blockIdx.y;
+  coop_reset(sync, kSyncInts, ctab, tstride, u, blockIdx.x, gridDim.x, threadIdx.x, 256);
   const int n = unit_length(lengths, u / heads, N);
   const int i = blockIdx.x * 256 + threadIdx.x;
   if (i >= N) return;
@@ -77,7 +86,8 @@ static hipError_t launch_hash_t(const Problem& p, const Workspace& ws, hipStream
   dim3 grid((p.n + kHashQB - 1) / kHashQB, p.units());
   hipLaunchKernelGGL((hash_kernel<D, T>), grid, dim3(kHashThreads), 0, s,
                      static_cast<const T*>(p.q), p.planes, p.lengths, p.heads, p.n, p.n_bits,
-                     ws.codes, p.lengths ? static_cast<T*>(p.out) : nullptr);
+                     ws.codes, p.lengths ? static_cast<T*>(p.out) : nullptr, ws.sync, ws.ctab,
+                     coop_table_stride(p.C));
   return hipGetLastError();
 }
 
@@ -90,7 +100,7 @@ hipError_t launch_load_codes(const Problem& p, const uint64_t* codes_in, const W
                              hipStream_t s) {
   dim3 grid((p.n + 255) / 256, p.units());
   hipLaunchKernelGGL(load_codes_kernel, grid, dim3(256), 0, s, codes_in, p.lengths, p.heads, p.n,
-                     p.n_bits, ws.codes);
+                     p.n_bits, ws.codes, ws.sync, ws.ctab, coop_table_stride(p.C));
   return hipGetLastError();
 }
 

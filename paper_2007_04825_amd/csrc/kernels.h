@@ -27,6 +27,23 @@ constexpr int kKmLdsMaxN = 4096;
 constexpr int kKmBlockQ = 1024;
 // Queries per workgroup of the CSR build.
 constexpr int kCsrBlockQ = 256;
+// Queries per workgroup of the cooperative K-means (codes resident in LDS):
+// 1024 or 2048, the smaller one whose grid the device holds at once.
+constexpr int kCoopMinQ = 1024;
+constexpr int kCoopMaxQ = 2048;
+// Workgroups of the cooperative K-means that the workspace is sized for.
+constexpr int kCoopMaxWgs = 512;
+inline int coop_max_blocks(int n, int units) {
+  const int by_len = (n + kCoopMinQ - 1) / kCoopMinQ;
+  const int by_grid = units > 0 ? (kCoopMaxWgs / units > 0 ? kCoopMaxWgs / units : 1) : 1;
+  return by_len < by_grid ? by_len : by_grid;
+}
+// Ints per unit of the cooperative K-means' arrival word (64-bit, 8-byte
+// aligned); the kernel that runs before it (hashing, or the copy of given
+// codes) sets it and both count tables to zero.
+constexpr int kSyncInts = 4;
+// Words per unit of a count table of the cooperative K-means.
+int coop_table_stride(int C);
 
 // Device buffers carved from the caller's workspace.
 struct Workspace {
@@ -49,9 +66,16 @@ struct Workspace {
   float* mass;          // [U][C]
   float* vcb;           // [U][C][d]
   float* stats;         // [U][C][2] row maximum and normaliser of the centroid softmax
+  int32_t* sync;        // [U][kSyncInts] arrival counters of the cooperative K-means
+  uint64_t* ctab;       // [U][2][C * 33] running count tables of the cooperative K-means
+  int32_t* cbases;      // [U][ncoop][C] first member position of each (block, cluster)
+  int32_t* clsizes;     // [U][ncoop][C] members of each (block, cluster)
+  double* qc_part;      // [U][C][ncoop][d] per-block centroid sums (used: n / coop_q blocks)
   int nblk;             // ceil(N / kKmBlockQ)
   int ncsr;             // ceil(N / kCsrBlockQ)
   int nchunk;           // ceil(N / kChunk)
+  int ncoop;            // cooperative K-means blocks the workspace holds per unit
+  int coop_q;           // queries per cooperative block of this call (0: not used)
 };
 
 // Carves the workspace; returns the bytes needed (ws may be null to only size it).
@@ -63,7 +87,8 @@ size_t carve_otop_workspace(const Problem& p, void* base, Workspace* ws);
 // Oracle-top outputs and top-k sets (into ws.topk).
 hipError_t launch_oracle_top(const Problem& p, const Workspace& ws, hipStream_t s);
 
-// Hashing; also writes 0 to the output rows past each sequence's length.
+// Hashing; also writes 0 to the output rows past each sequence's length and
+// zeroes ws.sync.
 hipError_t launch_hash(const Problem& p, const Workspace& ws, hipStream_t s);
 hipError_t launch_load_codes(const Problem& p, const uint64_t* codes_in, const Workspace& ws,
                              hipStream_t s);
@@ -72,8 +97,22 @@ hipError_t launch_load_codes(const Problem& p, const uint64_t* codes_in, const W
 // the output rows past each sequence's length.
 hipError_t launch_cluster_lds(const Problem& p, const uint64_t* codes_in, const Workspace& ws,
                               hipStream_t s);
-// Multi-workgroup K-means on ws.codes: writes the assignments of valid rows.
+// Multi-workgroup K-means on ws.codes, one launch pair per round: writes the
+// assignments of valid rows.
 hipError_t launch_kmeans(const Problem& p, const Workspace& ws, hipStream_t s);
+// Cooperative K-means on ws.codes (ws.sync zero), all rounds in one launch:
+// assignments (-1 on padded rows), sizes, offsets, member lists and the
+// per-block member ranges that launch_coop_centroids reads.
+hipError_t launch_kmeans_coop(const Problem& p, const Workspace& ws, hipStream_t s);
+// Centroids (Eq. 3) after launch_kmeans_coop: per-block fp64 partial sums,
+// then added in block order.
+hipError_t launch_coop_centroids(const Problem& p, const Workspace& ws, hipStream_t s);
+// K-means driver for a problem: 1 one workgroup per unit, 2 one launch pair
+// per round, 3 cooperative.
+int kmeans_driver(const Problem& p);
+// Queries per block of the cooperative K-means for p with at most max_blocks
+// blocks per unit, or 0 when its grid does not fit on the device.
+int coop_block_queries(const Problem& p, int max_blocks);
 hipError_t launch_load_assign(const Problem& p, const int32_t* assign_in, const Workspace& ws,
                               hipStream_t s);
 hipError_t launch_csr(const Problem& p, const int32_t* assign, const Workspace& ws, hipStream_t s);
@@ -121,7 +160,8 @@ size_t carve_bwd_workspace(const BwdProblem& p, void* base, BwdWorkspace* ws);
 // ev_start / ev_stop (may be null) are recorded around bwd_tile_kernel.
 hipError_t launch_backward(const BwdProblem& p, hipStream_t s, hipEvent_t ev_start, hipEvent_t ev_stop);
 
-// Which K-means path runs: 0 automatic, 1 one workgroup per unit, 2 multi-workgroup.
+// Which K-means path runs: 0 automatic, 1 one workgroup per unit, 2 one
+// launch pair per round, 3 cooperative.
 void set_kmeans_path(int path);
 int kmeans_uses_lds(const Problem& p);
 

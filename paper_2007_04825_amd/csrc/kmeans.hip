@@ -204,6 +204,151 @@ constexpr int kKmThreads = 1024;
 constexpr int kKmWaves = kKmThreads / 64;
 static_assert(kKmLdsMaxN == kMaxQt * 16 * kKmWaves, "tile budget");
 
+// One assign step over the n queries of a workgroup of kKmWaves waves (codes,
+// assignments and counts in LDS): each query goes to the nearest centroid of
+// the operand table cop (nct tiles), and a query whose cluster changed moves
+// its bit-pair counts and its size from the old row to the new one (a first
+// assignment, old = -1, only adds).  Adds the number of moved queries to
+// *nchange.  bq0 / code0 are the operands and codes of each wave's first four
+// query tiles, built once.  Ends without a workgroup barrier.
+__device__ __forceinline__ void assign_round(int n, int nqt, int nct, int n_bits,
+                                             const v4i* cop, const uint64_t* codes,
+                                             int32_t* assign, uint32_t* cnt, int32_t* size,
+                                             int* nchange, const uint2* qlut, const OpMasks& qm,
+                                             const v4i* bq0, const uint64_t* code0, int lane,
+                                             int wave) {
+  const int g = lane >> 4, c = lane & 15;
+  for (int s0 = 0; s0 < kMaxQt; s0 += 4) {
+    const int left = (nqt - wave + kKmWaves - 1) / kKmWaves - s0;  // tiles of this wave not yet done
+    if (left <= 0) break;
+    v4i bq[4];
+    int best[4];
+    uint64_t mycode[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if (s0 == 0) {
+        mycode[e] = code0[e];
+        bq[e] = bq0[e];
+      } else {
+        const int qb = (wave + (s0 + e) * kKmWaves) * 16 + c;
+        mycode[e] = qb < n ? codes[qb] : 0ull;
+        bq[e] = query_operand_lut(mycode[e], g, qm, qlut);
+      }
+      best[e] = INT_MIN;
+    }
+    best_keys_n<false>(left < 4 ? left : 4, cop, nct, bq, best, lane);
+    // lane l now decides query (l % 16) of tile l / 16 of the group; the
+    // queries whose cluster changed move their bit counts
+    const int eq = lane >> 4;
+    const int bsel = eq == 0 ? best[0] : eq == 1 ? best[1] : eq == 2 ? best[2] : best[3];
+    const uint64_t code = eq == 0 ? mycode[0] : eq == 1 ? mycode[1] : eq == 2 ? mycode[2] : mycode[3];
+    const int qi = (wave + (s0 + eq) * kKmWaves) * 16 + c;
+    bool chg = false;
+    int j = 0, old = 0;
+    if (eq < left && qi < n) {
+      j = decode_cluster(bsel, n_bits);
+      old = assign[qi];
+      chg = j != old;
+      if (chg) assign[qi] = j;
+    }
+    const uint64_t cmask = __ballot(chg);
+    const int nchg = __popcll(cmask);
+    if (nchg > 32) {
+      // many (the first round): every changed lane moves its own 32 words,
+      // the word order rotated by lane so that the atomics spread over banks
+      if (chg) {
+        if (old >= 0) {
+          atomicSub(&size[old], 1);
+#pragma unroll 4
+          for (int s = 0; s < 32; ++s) {
+            const int w = (s + lane) & 31;
+            atomicSub(&cnt[old * kCntStride + w], pair_val(code, w));
+          }
+        }
+        atomicAdd(&size[j], 1);
+#pragma unroll 4
+        for (int s = 0; s < 32; ++s) {
+          const int w = (s + lane) & 31;
+          atomicAdd(&cnt[j * kCntStride + w], pair_val(code, w));
+        }
+      }
+    } else {
+      // few: one wave-wide atomic per changed query, lanes 0-31 taking its
+      // words out of the old row and lanes 32-63 adding them to the new one
+      uint64_t cm = cmask;
+      while (cm != 0ull) {
+        const int src = __ffsll(static_cast<unsigned long long>(cm)) - 1;
+        cm &= cm - 1;
+        const int row = lane < 32 ? __builtin_amdgcn_readlane(old, src) : __builtin_amdgcn_readlane(j, src);
+        const uint64_t cs =
+            (static_cast<uint64_t>(static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(code >> 32), src))) << 32) |
+            static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(code), src));
+        const int w = lane & 31;
+        const uint32_t pv = pair_val(cs, w);
+        if (row >= 0) {
+          atomicAdd(&cnt[row * kCntStride + w], lane < 32 ? 0u - pv : pv);
+          if (w == 0) atomicAdd(&size[row], lane < 32 ? -1 : 1);
+        }
+      }
+    }
+    if (lane == 0 && nchg > 0) atomicAdd(nchange, nchg);
+  }
+}
+
+// Order-preserving counting sort of the n queries of a workgroup of kKmWaves
+// waves by cluster: emit(pos, i) receives every query i (assign[i] in
+// [0, ce), LDS) at position off[assign[i]] + (earlier queries of that
+// cluster), so that each cluster's queries come out in ascending order.  Wave
+// w takes the contiguous query range [w per, (w + 1) per); within 64 queries,
+// the lanes of one cluster find each other with nine ballots on the bits of
+// the cluster index.  hist is LDS scratch of kKmWaves * kCmax ints, free at
+// entry.  Ends without a workgroup barrier.
+template <typename Emit>
+__device__ __forceinline__ void member_sort(int n, int ce, const int32_t* assign, const int32_t* off,
+                                            int32_t* hist, Emit emit, int tid, int lane, int wave) {
+  for (int x = tid; x < kKmWaves * kCmax; x += kKmThreads) hist[x] = 0;
+  const int per = (n + kKmWaves - 1) / kKmWaves;
+  const int q_begin = min(n, wave * per), q_end = min(n, q_begin + per);
+  auto same_cluster = [&](int a) {  // lanes whose a equals this lane's (a in [0, 511])
+    uint64_t eq = ~0ull;
+#pragma unroll
+    for (int b = 0; b < 9; ++b) {
+      const uint64_t m = __ballot((a >> b) & 1);
+      eq &= ((a >> b) & 1) ? m : ~m;
+    }
+    return eq;
+  };
+  __syncthreads();
+  for (int base = q_begin; base < q_end; base += 64) {
+    const int i = base + lane;
+    const int a = i < q_end ? assign[i] : 511;
+    const uint64_t eq = same_cluster(a);
+    if (a < kCmax && (eq & lanemask_lt()) == 0ull) hist[wave * kCmax + a] += __popcll(eq);
+  }
+  __syncthreads();
+  for (int j = tid; j < ce; j += kKmThreads) {  // per-wave bases
+    int run = off[j];
+    for (int w = 0; w < kKmWaves; ++w) {
+      const int x = hist[w * kCmax + j];
+      hist[w * kCmax + j] = run;
+      run += x;
+    }
+  }
+  __syncthreads();
+  for (int base = q_begin; base < q_end; base += 64) {
+    const int i = base + lane;
+    const int a = i < q_end ? assign[i] : 511;
+    const uint64_t eq = same_cluster(a);
+    if (a < kCmax) {
+      const int pos = hist[wave * kCmax + a] + __popcll(eq & lanemask_lt());
+      emit(pos, i);
+    }
+    wave_lds_sync();
+    if (a < kCmax && (eq & lanemask_lt()) == 0ull) hist[wave * kCmax + a] += __popcll(eq);
+    wave_lds_sync();
+  }
+}
+
 struct KmShared {
   uint64_t codes[kKmLdsMaxN];
   int32_t assign[kKmLdsMaxN];
@@ -328,81 +473,8 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
     // round's update, after every thread has read it in the previous round
     // assign (up to four query tiles share every centroid-operand load); the
     // queries whose cluster changed move their bit counts right away
-    for (int s0 = 0; s0 < kMaxQt; s0 += 4) {
-      const int left = (nqt - wave + kKmWaves - 1) / kKmWaves - s0;  // tiles of this wave not yet done
-      if (left <= 0) break;
-      v4i bq[4];
-      int best[4];
-      uint64_t mycode[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        if (s0 == 0) {
-          mycode[e] = code0[e];
-          bq[e] = bq0[e];
-        } else {
-          const int qb = (wave + (s0 + e) * kKmWaves) * 16 + c;
-          mycode[e] = qb < n ? sh.codes[qb] : 0ull;
-          bq[e] = query_operand_lut(mycode[e], g, qm, sh.qlut);
-        }
-        best[e] = INT_MIN;
-      }
-      best_keys_n<false>(left < 4 ? left : 4, sh.cop, nct, bq, best, lane);
-      // lane l now decides query (l % 16) of tile l / 16 of the group; the
-      // queries whose cluster changed move their bit counts
-      const int eq = lane >> 4;
-      const int bsel = eq == 0 ? best[0] : eq == 1 ? best[1] : eq == 2 ? best[2] : best[3];
-      const uint64_t code = eq == 0 ? mycode[0] : eq == 1 ? mycode[1] : eq == 2 ? mycode[2] : mycode[3];
-      const int qi = (wave + (s0 + eq) * kKmWaves) * 16 + c;
-      bool chg = false;
-      int j = 0, old = 0;
-      if (eq < left && qi < n) {
-        j = decode_cluster(bsel, n_bits);
-        old = sh.assign[qi];
-        chg = j != old;
-        if (chg) sh.assign[qi] = j;
-      }
-      const uint64_t cmask = __ballot(chg);
-      const int nchg = __popcll(cmask);
-      if (nchg > 32) {
-        // many (the first round): every changed lane moves its own 32 words,
-        // the word order rotated by lane so that the atomics spread over banks
-        if (chg) {
-          if (old >= 0) {
-            atomicSub(&sh.size[old], 1);
-#pragma unroll 4
-            for (int s = 0; s < 32; ++s) {
-              const int w = (s + lane) & 31;
-              atomicSub(&sh.cnt[old * kCntStride + w], pair_val(code, w));
-            }
-          }
-          atomicAdd(&sh.size[j], 1);
-#pragma unroll 4
-          for (int s = 0; s < 32; ++s) {
-            const int w = (s + lane) & 31;
-            atomicAdd(&sh.cnt[j * kCntStride + w], pair_val(code, w));
-          }
-        }
-      } else {
-        // few: one wave-wide atomic per changed query, lanes 0-31 taking its
-        // words out of the old row and lanes 32-63 adding them to the new one
-        uint64_t cm = cmask;
-        while (cm != 0ull) {
-          const int src = __ffsll(static_cast<unsigned long long>(cm)) - 1;
-          cm &= cm - 1;
-          const int row = lane < 32 ? __builtin_amdgcn_readlane(old, src) : __builtin_amdgcn_readlane(j, src);
-          const uint64_t cs =
-              (static_cast<uint64_t>(static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(code >> 32), src))) << 32) |
-              static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(code), src));
-          const int w = lane & 31;
-          const uint32_t pv = pair_val(cs, w);
-          if (row >= 0) {
-            atomicAdd(&sh.cnt[row * kCntStride + w], lane < 32 ? 0u - pv : pv);
-            if (w == 0) atomicAdd(&sh.size[row], lane < 32 ? -1 : 1);
-          }
-        }
-      }
-      if (lane == 0 && nchg > 0) atomicAdd(&sh.nchange[t & 1], nchg);
-    }
+    assign_round(n, nqt, nct, n_bits, sh.cop, sh.codes, sh.assign, sh.cnt, sh.size,
+                 &sh.nchange[t & 1], sh.qlut, qm, bq0, code0, lane, wave);
     __syncthreads();
     // no query moved: every later round would repeat this assignment
     if (sh.nchange[t & 1] == 0) break;
@@ -431,6 +503,7 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
 
   // ---- member lists, ascending query order per cluster -------------------------
   int32_t* off = reinterpret_cast<int32_t*>(sh.cnt);  // [kCmax + 1], the counts are dead
+  static_assert((kCmax + 8) + kKmWaves * kCmax <= kCmax * kCntStride, "member-list scratch");
   int32_t* mem = sh.scratch;
   if (wave == 0) {
     int sz4[4], local = 0;
@@ -449,52 +522,7 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
     if (lane == 63) off[kCmax] = run;
   }
   __syncthreads();
-  // counting sort that keeps query order: wave w takes the contiguous query
-  // range [w per, (w + 1) per); within 64 queries, the lanes of one cluster
-  // find each other with nine ballots on the bits of the cluster index
-  int32_t* hist = off + kCmax + 8;  // [kKmWaves][kCmax] per-wave counts, then bases
-  static_assert((kCmax + 8) + kKmWaves * kCmax <= kCmax * kCntStride, "member-list scratch");
-  for (int x = tid; x < kKmWaves * kCmax; x += kKmThreads) hist[x] = 0;
-  const int per = (n + kKmWaves - 1) / kKmWaves;
-  const int q_begin = min(n, wave * per), q_end = min(n, q_begin + per);
-  auto same_cluster = [&](int a) {  // lanes whose a equals this lane's (a in [0, 511])
-    uint64_t eq = ~0ull;
-#pragma unroll
-    for (int b = 0; b < 9; ++b) {
-      const uint64_t m = __ballot((a >> b) & 1);
-      eq &= ((a >> b) & 1) ? m : ~m;
-    }
-    return eq;
-  };
-  __syncthreads();
-  for (int base = q_begin; base < q_end; base += 64) {
-    const int i = base + lane;
-    const int a = i < q_end ? sh.assign[i] : 511;
-    const uint64_t eq = same_cluster(a);
-    if (a < kCmax && (eq & lanemask_lt()) == 0ull) hist[wave * kCmax + a] += __popcll(eq);
-  }
-  __syncthreads();
-  for (int j = tid; j < ce; j += kKmThreads) {  // per-wave bases
-    int run = off[j];
-    for (int w = 0; w < kKmWaves; ++w) {
-      const int x = hist[w * kCmax + j];
-      hist[w * kCmax + j] = run;
-      run += x;
-    }
-  }
-  __syncthreads();
-  for (int base = q_begin; base < q_end; base += 64) {
-    const int i = base + lane;
-    const int a = i < q_end ? sh.assign[i] : 511;
-    const uint64_t eq = same_cluster(a);
-    if (a < kCmax) {
-      const int pos = hist[wave * kCmax + a] + __popcll(eq & lanemask_lt());
-      mem[pos] = i;
-    }
-    wave_lds_sync();
-    if (a < kCmax && (eq & lanemask_lt()) == 0ull) hist[wave * kCmax + a] += __popcll(eq);
-    wave_lds_sync();
-  }
+  member_sort(n, ce, sh.assign, off, off + kCmax + 8, [&](int pos, int i) { mem[pos] = i; }, tid, lane, wave);
   __syncthreads();
   // ---- centroids, Eq. (3) ---------------------------------------------------------
   // D lanes (lane = dimension) per group; group g takes the sorted positions
@@ -583,6 +611,290 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
   for (int j = tid; j < C; j += kKmThreads) f.sizes[static_cast<size_t>(u) * C + j] = j < ce ? sh.size[j] : 0;
   for (int j = tid; j <= C; j += kKmThreads)
     f.offsets[static_cast<size_t>(u) * (C + 1) + j] = j < ce ? off[j] : n;
+}
+
+// ===========================================================================
+// Cooperative path: the workgroups of a unit run all L rounds in one launch.
+//
+// Workgroup b of unit u holds queries [b Q, (b + 1) Q) (Q = 1024 or 2048:
+// the smaller one whose grid the device holds at once) with their codes,
+// assignments and bit-pair counts resident in LDS, as the one-workgroup
+// kernel does.  The unit's counts live in two running-total tables of
+// 64-bit words (a cluster row has 32 words, each holding the two 32-bit
+// counts of one bit pair, and its size).  In round t a workgroup adds to
+// table t % 2 the change of its local counts since it last added to that
+// table (two rounds earlier), as signed 64-bit atomic adds of only the words
+// that changed, so that the table then holds the unit's counts of round t
+// (the two halves of a word stay exact: modular arithmetic, and each final
+// half is a true count).  It then waits at a per-unit arrival counter until
+// every workgroup of the unit has added its part; every workgroup reads the
+// whole table and forms the next centroids by the per-bit majority itself.
+// Integer sums, so nothing depends on the order of the atomics.  Table t % 2
+// is next changed in round t + 2, after the arrival of round t + 1, which
+// every reader of round t has passed.  The arrival counter is one 64-bit
+// word: each arrival adds 1 to its low half and, when some query of the
+// workgroup moved in that round, 1 to its high half, so the poll that sees
+// the last arrival also tells whether any query of the unit moved.  The
+// launch is cooperative, so all workgroups are resident
+// together and every wait ends; each wait is also bounded.  A round in which
+// no query of the unit moved ends the loop: every later round would repeat
+// it.  The final member lists come from the per-workgroup sizes of the last
+// round: cluster j's members of workgroup b follow those of workgroups
+// 0..b-1, so each cluster's members stay in ascending query order.
+// ===========================================================================
+constexpr int kSpinLimit = 1 << 22;   // polls of the arrival counter before giving up
+static_assert(kCoopMaxQ <= kKmLdsMaxN, "the shared assign step handles kKmLdsMaxN queries");
+constexpr int kTabBatch = 4;          // table words requested together per thread
+constexpr int kRowWords = 33;         // table words per cluster: 32 bit pairs and the size
+static_assert(kSyncInts >= 2, "one 64-bit arrival word");
+
+template <typename X>
+__device__ __forceinline__ X ld_agent(const X* p) {
+  return __hip_atomic_load(const_cast<X*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+template <typename X>
+__device__ __forceinline__ void st_agent(X* p, X v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// Waits until this wave's stores and atomics have been performed.
+__device__ __forceinline__ void wait_memory() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+struct CoopArgs {
+  const uint64_t* codes;   // [U][N]
+  const int32_t* lengths;
+  int heads, N, C, n_bits, L, nwg;
+  int tstride;             // words per unit of a count table: C * 33
+  int32_t* assign;         // [U][N]
+  int32_t* sizes;          // [U][C]
+  int32_t* offsets;        // [U][C+1]
+  int32_t* members;        // [U][N]
+  int32_t* bases;          // [U][nwg][C] first member position of (workgroup, cluster)
+  int32_t* lsizes;         // [U][nwg][C] members of (workgroup, cluster)
+  uint64_t* tab;           // [U][2][tstride] running count tables, zero at launch
+  int32_t* sync;           // [U][kSyncInts] arrival word (64-bit), zero at launch
+};
+
+template <int QW>
+struct CoopShared {
+  uint64_t codes[QW];
+  int32_t assign[QW];
+  uint32_t cnt[kCmax * kCntStride];
+  uint32_t pub[2][kCmax * kRowWords];  // local counts last added to each table
+  int32_t size[kCmax];
+  uint64_t cent[kCmax];
+  uint32_t ncent[2 * kCmax];  // next centroid codes, low and high words
+  v4i cop[kCmax / 16 * 64];
+  uint2 qlut[256];
+  int32_t tsize[kCmax];
+  int32_t pre[kCmax];
+  int32_t off[kCmax + 8];
+  int nchange;
+  int moved;  // some query of the unit moved in this round
+  int ok;
+};
+// the member sort's per-wave counts use the operand table, dead by then
+static_assert(sizeof(v4i) * (kCmax / 16 * 64) >= sizeof(int32_t) * kKmWaves * kCmax, "member-sort scratch");
+
+template <int QW>
+__global__ __launch_bounds__(kKmThreads) void kmeans_coop_kernel(CoopArgs a) {
+  __shared__ CoopShared<QW> sh;
+  const int u = blockIdx.y, b = blockIdx.x, nwg = a.nwg;
+  const int N = a.N, C = a.C, n_bits = a.n_bits;
+  const int n = unit_length(a.lengths, u / a.heads, N);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int q0 = b * QW;
+  const size_t row0 = static_cast<size_t>(u) * N;
+  for (int i = max(n, q0) + tid; i < min(N, q0 + QW); i += kKmThreads) a.assign[row0 + i] = -1;
+  if (n == 0) {  // the same in every workgroup of the unit: none of them waits
+    if (b == 0) {
+      for (int j = tid; j < C; j += kKmThreads) a.sizes[static_cast<size_t>(u) * C + j] = 0;
+      for (int j = tid; j <= C; j += kKmThreads) a.offsets[static_cast<size_t>(u) * (C + 1) + j] = 0;
+    }
+    return;
+  }
+  const int nq = max(0, min(QW, n - q0));
+  const int ce = C < n ? C : n;
+  const int nct = (ce + 15) / 16;
+  const int nqt = (nq + 15) / 16;
+  const int tstride = a.tstride;
+  const uint64_t* cu = a.codes + row0;
+  for (int i = tid; i < nq; i += kKmThreads) {
+    sh.codes[i] = cu[q0 + i];
+    sh.assign[i] = -1;
+  }
+  for (int x = tid; x < kCmax * kCntStride; x += kKmThreads) sh.cnt[x] = 0;
+  for (int j = tid; j < kCmax; j += kKmThreads) sh.size[j] = 0;
+  for (int x = tid; x < 2 * kCmax; x += kKmThreads) sh.ncent[x] = 0u;
+  for (int x = tid; x < 2 * kCmax * kRowWords; x += kKmThreads) (&sh.pub[0][0])[x] = 0u;
+  for (int j = tid; j < ce; j += kKmThreads) sh.cent[j] = cu[(static_cast<int64_t>(j) * n) / ce];
+  for (int v = tid; v < 256; v += kKmThreads) {
+    const uint32_t lo = 0xc0c0c0c0u ^ (spread4(v & 0xf) << 7);
+    const uint32_t hi = 0xc0c0c0c0u ^ (spread4(v >> 4) << 7);
+    sh.qlut[v] = make_uint2(lo, hi);
+  }
+  if (tid == 0) sh.nchange = 0;
+  const int g = lane >> 4, c = lane & 15;
+  const OpMasks qm = op_masks(g, n_bits);
+  __syncthreads();
+  build_centroid_operands(sh.cop, sh.cent, ce, nct, n_bits, tid, kKmThreads);
+  __syncthreads();
+  unsigned long long* arrive =
+      reinterpret_cast<unsigned long long*>(a.sync + static_cast<size_t>(u) * kSyncInts);
+  unsigned long long moved_before = 0;  // high half of the arrival word after the previous round
+  const size_t U = gridDim.y;
+  int32_t* lsz = a.lsizes + (static_cast<size_t>(u) * nwg + b) * C;
+  for (int t = 0; t < a.L; ++t) {
+    // the first four query tiles' operands, rebuilt each round (registers are
+    // scarcer here than in the one-workgroup kernel)
+    v4i bq0[4];
+    uint64_t code0[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int qb = (wave + e * kKmWaves) * 16 + c;
+      code0[e] = qb < nq ? sh.codes[qb] : 0ull;
+      bq0[e] = query_operand_lut(code0[e], g, qm, sh.qlut);
+    }
+    assign_round(nq, nqt, nct, n_bits, sh.cop, sh.codes, sh.assign, sh.cnt, sh.size, &sh.nchange,
+                 sh.qlut, qm, bq0, code0, lane, wave);
+    __syncthreads();
+    // add the change of this workgroup's counts since its last addition to
+    // table t % 2; keep the sizes for the member lists
+    uint64_t* tab = a.tab + (static_cast<size_t>(u) * 2 + (t & 1)) * tstride;
+    uint32_t* pub = sh.pub[t & 1];
+    for (int x = tid; x < ce * kRowWords; x += kKmThreads) {
+      const int j = x / kRowWords, w = x - kRowWords * j;
+      const uint32_t cur = w < 32 ? sh.cnt[j * kCntStride + w] : static_cast<uint32_t>(sh.size[j]);
+      const uint32_t old = pub[x];
+      if (cur != old) {
+        pub[x] = cur;
+        const long long dlo = static_cast<long long>(w < 32 ? (cur & 0xffffu) : cur) -
+                              static_cast<long long>(w < 32 ? (old & 0xffffu) : old);
+        const long long dhi = w < 32 ? static_cast<long long>(cur >> 16) - static_cast<long long>(old >> 16) : 0;
+        const unsigned long long dv = static_cast<unsigned long long>(dhi) * 0x100000000ull +
+                                      static_cast<unsigned long long>(dlo);
+        atomicAdd(reinterpret_cast<unsigned long long*>(&tab[x]), dv);
+      }
+    }
+    for (int j = tid; j < ce; j += kKmThreads) st_agent(&lsz[j], sh.size[j]);
+    // arrive once every wave's additions have been performed, then wait until
+    // every workgroup of the unit has arrived
+    wait_memory();
+    __syncthreads();
+    if (tid == 0) {
+      const unsigned long long add = 1ull + (sh.nchange > 0 ? 0x100000000ull : 0ull);
+      sh.nchange = 0;
+      __hip_atomic_fetch_add(arrive, add, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const unsigned long long target = static_cast<unsigned long long>(t + 1) * nwg;
+      unsigned long long seen = 0;
+      int spins = 0;
+      while (((seen = __hip_atomic_load(arrive, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) & 0xffffffffull) <
+                 target &&
+             spins < kSpinLimit) {
+        __builtin_amdgcn_s_sleep(1);
+        ++spins;
+      }
+      sh.ok = spins < kSpinLimit;
+      sh.moved = (seen >> 32) != moved_before;
+      moved_before = seen >> 32;
+    }
+    __syncthreads();
+    if (t + 1 == a.L || !sh.moved || !sh.ok) break;  // no query moved: later rounds repeat this one
+    // per-bit majority (tie -> 0) of the unit's non-empty clusters: the
+    // (cluster, pair word) items' words and the cluster sizes are requested
+    // together (kTabBatch words per thread in flight); each item sets its two
+    // bits once the sizes are in LDS
+    {
+      const int items = ce * 32;
+      for (int x0 = 0; x0 < items; x0 += kTabBatch * kKmThreads) {
+        uint64_t wv[kTabBatch];
+#pragma unroll
+        for (int e = 0; e < kTabBatch; ++e) {
+          const int x = x0 + tid + e * kKmThreads;
+          wv[e] = x < items ? ld_agent(&tab[(x >> 5) * kRowWords + (x & 31)]) : 0ull;
+        }
+        if (x0 == 0)
+          for (int j = tid; j < ce; j += kKmThreads) sh.tsize[j] = static_cast<int>(ld_agent(&tab[j * kRowWords + 32]));
+        __syncthreads();
+#pragma unroll
+        for (int e = 0; e < kTabBatch; ++e) {
+          const int x = x0 + tid + e * kKmThreads;
+          if (x < items) {
+            const int j = x >> 5, w = x & 31;
+            const long long tz = sh.tsize[j];
+            const uint32_t bits = static_cast<uint32_t>(2 * static_cast<long long>(wv[e] & 0xffffffffull) > tz) |
+                                  (static_cast<uint32_t>(2 * static_cast<long long>(wv[e] >> 32) > tz) << 1);
+            if (bits) atomicOr(&sh.ncent[2 * j + (w >> 4)], bits << (2 * (w & 15)));
+          }
+        }
+      }
+    }
+    __syncthreads();
+    for (int j = tid; j < ce; j += kKmThreads) {
+      if (sh.tsize[j] > 0)
+        sh.cent[j] = static_cast<uint64_t>(sh.ncent[2 * j]) | (static_cast<uint64_t>(sh.ncent[2 * j + 1]) << 32);
+      sh.ncent[2 * j] = sh.ncent[2 * j + 1] = 0u;
+    }
+    __syncthreads();
+    build_centroid_operands(sh.cop, sh.cent, ce, nct, n_bits, tid, kKmThreads);
+    __syncthreads();
+  }
+
+  // ---- member lists from the last round's per-workgroup sizes ------------------
+  // every (cluster, workgroup) size is read once, four per thread in flight:
+  // the cluster's total and the part of workgroups 0..b-1
+  for (int j = tid; j < ce; j += kKmThreads) sh.tsize[j] = sh.pre[j] = 0;
+  __syncthreads();
+  {
+    const int32_t* lsu = a.lsizes + static_cast<size_t>(u) * nwg * C;
+    constexpr int RB = 4;
+    for (int x0 = tid; x0 < ce * nwg; x0 += RB * kKmThreads) {
+      int v[RB];
+#pragma unroll
+      for (int e = 0; e < RB; ++e) {
+        const int x = x0 + e * kKmThreads;
+        v[e] = x < ce * nwg ? ld_agent(&lsu[static_cast<size_t>(x % nwg) * C + x / nwg]) : 0;
+      }
+#pragma unroll
+      for (int e = 0; e < RB; ++e) {
+        const int x = x0 + e * kKmThreads;
+        if (x < ce * nwg && v[e] != 0) {
+          atomicAdd(&sh.tsize[x / nwg], v[e]);
+          if (x % nwg < b) atomicAdd(&sh.pre[x / nwg], v[e]);
+        }
+      }
+    }
+  }
+  __syncthreads();
+  if (wave == 0) {  // exclusive scan of the unit's sizes: kCmax / 64 clusters per lane
+    constexpr int PL = kCmax / 64;
+    int sz[PL], local = 0;
+#pragma unroll
+    for (int e = 0; e < PL; ++e) {
+      const int j = PL * lane + e;
+      sz[e] = j < ce ? sh.tsize[j] : 0;
+      local += sz[e];
+    }
+    int run = wave_incl_scan(local) - local;
+#pragma unroll
+    for (int e = 0; e < PL; ++e) {
+      const int j = PL * lane + e;
+      if (b == 0) a.offsets[static_cast<size_t>(u) * (C + 1) + min(j, C)] = j < ce ? run : n;
+      sh.off[j] = run + (j < ce ? sh.pre[j] : 0);
+      run += sz[e];
+    }
+  }
+  __syncthreads();
+  int32_t* bs = a.bases + (static_cast<size_t>(u) * nwg + b) * C;
+  for (int j = tid; j < C; j += kKmThreads) {
+    if (b == 0) a.sizes[static_cast<size_t>(u) * C + j] = j < ce ? sh.tsize[j] : 0;
+    bs[j] = j < ce ? sh.off[j] : 0;
+    if (j >= ce) lsz[j] = 0;
+  }
+  if (b == 0 && tid == 0) a.offsets[static_cast<size_t>(u) * (C + 1) + C] = n;
+  int32_t* mg = a.members + row0;
+  member_sort(nq, ce, sh.assign, sh.off, reinterpret_cast<int32_t*>(sh.cop),
+              [&](int pos, int i) { mg[pos] = q0 + i; }, tid, lane, wave);
+  for (int i = tid; i < nq; i += kKmThreads) a.assign[row0 + q0 + i] = sh.assign[i];
 }
 
 // ===========================================================================
@@ -820,6 +1132,50 @@ __global__ __launch_bounds__(256) void load_assign_kernel(const int32_t* __restr
 static int g_kmeans_path = 0;
 void set_kmeans_path(int path) { g_kmeans_path = path; }
 
+// Workgroups of the cooperative K-means (QW queries each) that the current
+// device holds at once (its occupancy times the compute units), measured once
+// per device.
+template <int QW>
+static int coop_capacity() {
+  constexpr int kMaxDev = 64;
+  static int cap[kMaxDev] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDev) return 0;
+  if (cap[dev] == 0) {
+    int per_cu = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kmeans_coop_kernel<QW>, kKmThreads, 0) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
+      (void)hipGetLastError();
+      return 0;
+    }
+    cap[dev] = per_cu * cus > 0 ? per_cu * cus : -1;
+  }
+  return cap[dev] > 0 ? cap[dev] : 0;
+}
+
+int coop_block_queries(const Problem& p, int max_blocks) {
+  const long long U = p.units();
+  auto fits = [&](int qw, int cap) {
+    const long long nb = (p.n + qw - 1) / qw;
+    return nb <= max_blocks && nb * U <= cap;
+  };
+  if (fits(2048, coop_capacity<2048>())) return 2048;
+  if (fits(1024, coop_capacity<1024>())) return 1024;
+  return 0;
+}
+
+static bool coop_fits(const Problem& p) {
+  return coop_block_queries(p, coop_max_blocks(p.n, p.units())) > 0;
+}
+
+int kmeans_driver(const Problem& p) {
+  if (g_kmeans_path == 1 && p.n <= kKmLdsMaxN) return 1;
+  if (g_kmeans_path == 2) return 2;
+  if (g_kmeans_path == 3) return coop_fits(p) ? 3 : 2;
+  if (kmeans_uses_lds(p)) return 1;
+  return coop_fits(p) ? 3 : 2;
+}
+
 int kmeans_uses_lds(const Problem& p) {
   if (p.n > kKmLdsMaxN) return 0;
   if (g_kmeans_path == 1) return 1;
@@ -886,6 +1242,41 @@ hipError_t launch_cluster_lds(const Problem& p, const uint64_t* codes_in, const 
                         : launch_cluster_lds_t<32, bf16_t>(p, codes_in, ws, s);
   return p.dtype == 0 ? launch_cluster_lds_t<64, float>(p, codes_in, ws, s)
                       : launch_cluster_lds_t<64, bf16_t>(p, codes_in, ws, s);
+}
+
+int coop_table_stride(int C) { return C * kRowWords; }
+
+hipError_t launch_kmeans_coop(const Problem& p, const Workspace& ws, hipStream_t s) {
+  CoopArgs a;
+  a.codes = ws.codes;
+  a.lengths = p.lengths;
+  a.heads = p.heads;
+  a.N = p.n;
+  a.C = p.C;
+  a.n_bits = p.n_bits;
+  a.L = p.L;
+  a.nwg = (p.n + ws.coop_q - 1) / ws.coop_q;
+  a.tstride = coop_table_stride(p.C);
+  a.assign = ws.assign;
+  a.sizes = ws.sizes;
+  a.offsets = ws.offsets;
+  a.members = ws.members;
+  a.bases = ws.cbases;
+  a.lsizes = ws.clsizes;
+  a.tab = ws.ctab;
+  a.sync = ws.sync;
+  void* args[] = {&a};
+  const dim3 grid(a.nwg, p.units());
+  switch (ws.coop_q) {
+    case 1024:
+      return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(kmeans_coop_kernel<1024>), grid,
+                                        dim3(kKmThreads), args, 0, s);
+    case 2048:
+      return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(kmeans_coop_kernel<2048>), grid,
+                                        dim3(kKmThreads), args, 0, s);
+    default:
+      return hipErrorInvalidValue;
+  }
 }
 
 hipError_t launch_kmeans(const Problem& p, const Workspace& ws, hipStream_t s) {

@@ -9,6 +9,7 @@ the host cores), so the comparison is element by element, to the same bars as
 the smaller cases: codes, assignments and sizes exact, top-k sets up to near
 ties, outputs within 2e-5 (fp32) or 2e-2 (bf16).
 """
+import numpy as np
 import pytest
 
 import gen
@@ -48,6 +49,25 @@ def test_sweep_full_size(log2n, dtype, variant):
 def test_long_context_full_size():
     w = workload(("long",))
     check_end_to_end(w, w.topk)
+
+
+@pytest.mark.parametrize("key", [("long",), ("sweep", 32768, "f32")])
+def test_stage_isolated_full_size(key):
+    """The oracle's partition and top-k sets injected at the full sizes: every
+    mass, rest part and output row comparable, with no near-tie exemption."""
+    w = workload(key)
+    ref = gpu_util.run_oracle(w, w.topk)
+    N = w.q.shape[2]
+    assign_in = np.where(ref["assign"] < 0, 0, ref["assign"]).reshape(-1, N)
+    topk_in = ref["topk"].reshape(-1, w.C, w.topk)
+    got = gpu_util.run_gpu(w, w.topk, assign_in=assign_in, topk_in=topk_in)
+    vm = gpu_util.valid_mask(w)
+    assert np.array_equal(got["topk"], ref["topk"])
+    np.testing.assert_allclose(got["mass"], ref["mass"], rtol=0, atol=1e-5)
+    np.testing.assert_allclose(got["values"], ref["vcb"], rtol=0, atol=gpu_util.tol(w))
+    err = np.abs(got["out"] - ref["out"])[vm].max()
+    print("max abs error: %.3g" % err)
+    assert err <= gpu_util.tol(w)
 
 
 @pytest.mark.parametrize("variant", ["clustered", "iclustered"])

@@ -19,7 +19,8 @@ import pytest
 
 import gen
 import oracle
-from gpu_util import check_end_to_end, run_gpu, run_oracle, tol, topk_mismatches, valid_mask
+from gpu_util import (check_end_to_end, compare_outputs, run_gpu, run_oracle, tol,
+                      topk_mismatches, valid_mask)
 
 pytestmark = pytest.mark.gpu
 
@@ -79,19 +80,21 @@ def test_injected_codes_give_oracle_assignment(name):
 
 
 @pytest.mark.parametrize("name", ["tiny", "sweep2048_f32", "sweep4096_bf16"])
-def test_both_kmeans_drivers_agree(name):
+def test_every_kmeans_driver_agrees(name):
     import paper_2007_04825_amd as ca
     w = workload(name)
     res = []
     try:
-        for path in (1, 2):
+        for path in (1, 2, 3):
             ca.set_kmeans_path(path)
             res.append(run_gpu(w, w.topk))
     finally:
         ca.set_kmeans_path(0)
-    for key in ("codes", "assign", "sizes", "topk"):
-        assert np.array_equal(res[0][key], res[1][key]), key
-    assert np.array_equal(res[0]["out"], res[1]["out"])
+    for r in res[1:]:
+        for key in ("codes", "assign", "sizes", "topk"):
+            assert np.array_equal(res[0][key], r[key]), key
+        np.testing.assert_allclose(r["centroids"], res[0]["centroids"], rtol=0, atol=2e-6)
+        assert np.abs(r["out"] - res[0]["out"]).max() <= tol(w)
 
 
 def test_deterministic_bitwise():
@@ -169,17 +172,9 @@ def test_ragged_lengths_nan_padding(variant):
     topk = w.topk if variant == "iclustered" else 0
     ref = run_oracle(w, topk)
     got = run_gpu(w, topk)
-    vm = valid_mask(w)
     assert np.array_equal(got["assign"], ref["assign"])
     assert not np.isnan(got["out"]).any()
-    assert np.all(got["out"][~vm] == 0)
-    skip = np.zeros(vm.shape, bool)
-    if topk:
-        diff, bad = topk_mismatches(w, ref, got, topk)
-        assert not bad
-        for (b, h, j) in diff:
-            skip[b, h] |= ref["assign"][b, h] == j
-    assert np.abs(got["out"] - ref["out"])[vm & ~skip].max() <= 2e-5
+    compare_outputs(w, ref, got, topk)
 
 
 @pytest.mark.parametrize("C,n_bits,L,topk", [(1, 63, 3, 1), (16, 8, 1, 5), (17, 33, 2, 128),
@@ -189,25 +184,74 @@ def test_parameter_corners(C, n_bits, L, topk):
     w.lengths = np.array([700, 517], np.int32)
     ref = run_oracle(w, topk, key="corner%d_%d_%d_%d" % (C, n_bits, L, topk))
     got = run_gpu(w, topk)
-    vm = valid_mask(w)
     assert np.array_equal(got["codes"], ref["codes"])
     assert np.array_equal(got["assign"], ref["assign"])
-    diff, bad = topk_mismatches(w, ref, got, topk)
-    assert not bad
-    skip = np.zeros(vm.shape, bool)
-    for (b, h, j) in diff:
-        skip[b, h] |= ref["assign"][b, h] == j
-    assert np.abs(got["out"] - ref["out"])[vm & ~skip].max() <= 2e-5
+    compare_outputs(w, ref, got, topk)
+
+
+# Every K-means driver that applies to the length: 1 one workgroup per unit
+# (n <= 4096), 2 one launch pair per round, 3 cooperative (all rounds in one
+# launch); C = 256 with n above one key chunk (several-chunk attention and
+# merge) and above one cooperative block (4096 queries).
+BIG_C = [(2100, "f32", 128), (3000, "bf16", 100), (4500, "f32", 64), (9000, "bf16", 128)]
+
+
+@pytest.mark.parametrize("N,dtype,topk", BIG_C)
+@pytest.mark.parametrize("variant", ["clustered", "iclustered"])
+def test_many_clusters_every_driver(N, dtype, topk, variant):
+    import paper_2007_04825_amd as ca
+    w = gen.config_tiny(B=2, H=1, N=N, d=64, C=256, L=4, topk=topk)
+    w = gen.with_dtype(w, dtype)
+    w.lengths = np.array([N, N - 777], np.int32)
+    t = topk if variant == "iclustered" else 0
+    ref = run_oracle(w, t, key="bigc%d_%s_%d" % (N, dtype, topk))
+    paths = (1, 2, 3) if N <= 4096 else (2, 3)
+    results = []
+    try:
+        for path in paths:
+            ca.set_kmeans_path(path)
+            got = run_gpu(w, t)
+            print("driver %d" % path)
+            assert np.array_equal(got["codes"], ref["codes"])
+            assert np.array_equal(got["assign"], ref["assign"]), "driver %d" % path
+            assert np.array_equal(got["sizes"], ref["sizes"])
+            np.testing.assert_allclose(got["centroids"], ref["qc"], rtol=0, atol=2e-6)
+            compare_outputs(w, ref, got, t)
+            results.append(got)
+    finally:
+        ca.set_kmeans_path(0)
+    for r in results[1:]:
+        assert np.array_equal(r["assign"], results[0]["assign"])
 
 
 def test_invalid_arguments_enqueue_nothing():
+    """A rejected call (through the C ABI) returns its error code and leaves
+    the output untouched: nothing was enqueued, also seen after the stream has
+    drained."""
     import paper_2007_04825_amd as ca
     torch = pytest.importorskip("torch")
-    q = torch.zeros((1, 1, 64, 48), device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    q = torch.zeros((1, 1, 64, 48), device="cuda")             # d = 48: unsupported
     planes = torch.zeros((1, 63, 48), device="cuda")
-    with pytest.raises(ca.ClusteredAttnError) as e:
-        ca.clustered_attention(q, q, q, planes, 10)
-    assert e.value.code == ca.CA_ERR_UNSUPPORTED
+    out = torch.full((1, 1, 64, 48), 7.25, device="cuda")
+    ws = torch.empty(1 << 20, dtype=torch.uint8, device="cuda")
+    rc = ca.clustered_attention_fwd(q.data_ptr(), q.data_ptr(), q.data_ptr(), None, planes.data_ptr(),
+                                    1, 1, 64, 48, ca.CA_F32, 10, 63, 3, out.data_ptr(), ws.data_ptr(),
+                                    1 << 20, None, stream)
+    assert rc == ca.CA_ERR_UNSUPPORTED
+    q32 = torch.zeros((1, 1, 64, 32), device="cuda")
+    p32 = torch.zeros((1, 63, 32), device="cuda")
+    out32 = torch.full((1, 1, 64, 32), 7.25, device="cuda")
+    rc = ca.iclustered_attention_fwd(q32.data_ptr(), q32.data_ptr(), q32.data_ptr(), None,
+                                     p32.data_ptr(), 1, 1, 64, 32, ca.CA_F32, 10, 63, 3, 4,
+                                     out32.data_ptr(), ws.data_ptr(), 16, None, stream)
+    assert rc == ca.CA_ERR_WORKSPACE                        # 16 bytes: far too small
+    rc = ca.iclustered_attention_fwd(q32.data_ptr(), q32.data_ptr(), q32.data_ptr(), None,
+                                     p32.data_ptr(), 1, 1, 64, 32, ca.CA_F32, 0, 63, 3, 4,
+                                     out32.data_ptr(), ws.data_ptr(), 1 << 20, None, stream)
+    assert rc == ca.CA_ERR_INVALID_ARG                      # no clusters
+    torch.cuda.synchronize()
+    assert bool((out == 7.25).all()) and bool((out32 == 7.25).all())
 
 
 def near_orthogonal_queries(w, seed=0):
