@@ -179,6 +179,15 @@ __device__ __forceinline__ void store_vec(bf16_t* p, const float* s) {
 constexpr int kLStride = kChunk + 16;  // floats per LDS logit row (the four rows of a wave fall in distinct banks)
 static_assert(kLStride >= kChunk, "rows padded for the top-k sweep: 32 grp_block_len(kChunk) <= kChunk");
 constexpr int kCandCap = 128;
+// Whether fp32 inputs take the centroid products on the bf16 matrix cores
+// with both operands split in three (six part products, fp32 accuracy)
+// instead of the fp32 matrix cores.  The bf16 instruction does eight times
+// the work of v_mfma_f32_16x16x4f32 in half the cycles, but measured on the
+// length-sweep point N = 32768 the single-pass kernel ran no faster (it is
+// not bound by the matrix cores) and the tile kernel slower (the splits cost
+// registers: 169 instead of one workgroup's worth of occupancy), so fp32
+// keeps the fp32 matrix cores.
+constexpr bool kSplitF32 = false;
 constexpr int kSparseChunk = 64;  // members per work item of sparse_kernel
 constexpr int kTileWaves = 8;  // waves per centroid-tile workgroup
 constexpr int kTileThreads = 64 * kTileWaves;
@@ -195,6 +204,8 @@ struct AttnArgs {
   const int32_t* lengths;
   int heads, N, C, nchunk, topk;
   int ntile, ncg, units;  // 16-centroid tiles, 4-cluster groups, (batch, head) units
+  int pchunk;             // keys per chunk of the partial states that the merge combines
+  int npc;                // chunks of the partial single-pass kernel (nchunk is the state stride)
   int nsg;                // groups of four sparse_kernel work items per unit
   float scale;
   const int32_t* topk_in;
@@ -247,9 +258,11 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
   __shared__ int moff[17];
   __shared__ int any_nonempty;
 
-  const int wi = xcd_work_item();  // chunk fastest, then tile, then (batch, head)
+  // tile fastest, then chunk, then (batch, head): the tiles that read the same
+  // key chunk run together on one XCD and share its L2
+  const int wi = xcd_work_item();
   if (wi >= a.nchunk * a.ntile * a.units) return;
-  const int chunk = wi % a.nchunk, tile = (wi / a.nchunk) % a.ntile, u = wi / (a.nchunk * a.ntile);
+  const int tile = wi % a.ntile, chunk = (wi / a.ntile) % a.nchunk, u = wi / (a.nchunk * a.ntile);
   const int n = unit_length(a.lengths, u / a.heads, a.N);
   if constexpr (OTOP) {
     const int r0 = tile * 16;
@@ -344,7 +357,7 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
     // bf16 inputs: exact keys, the rows split into three bf16 parts, three
     // part products per 32 dims on the bf16 matrix cores (fp32-accurate
     // logits; the k index maps to the lane's own dims g KS + 8 m + j)
-    constexpr bool BF = sizeof(T) == 2;
+    constexpr bool BF = sizeof(T) == 2 || kSplitF32;
     constexpr int NC = KS / 8;
     Split8 qs[BF ? NC : 1];
     if constexpr (BF) {
@@ -364,7 +377,7 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
           v4f acc = {0.f, 0.f, 0.f, 0.f};
           if constexpr (BF) {
 #pragma unroll
-            for (int m = 0; m < NC; ++m) acc = mfma_split3(pack_bf16x8(&ka[b][8 * m]), qs[m], acc);
+            for (int m = 0; m < NC; ++m) acc = mfma_bf16x<T>(&ka[b][8 * m], qs[m], acc);
           } else {
 #pragma unroll
             for (int s = 0; s < KS; ++s) acc = mfma_f32_16x16x4(ka[b][s], bq[s], acc);
@@ -545,9 +558,9 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
             for (int dt = 0; dt < DT; ++dt) va[b][i][dt] = 0.0f;
           }
         }
-      if constexpr (sizeof(T) == 2) {
-        // bf16 values are exact; P splits into three bf16 parts; tiles b and
-        // b + 1 of the batch form one product over 32 keys (k = 8 g + j: key
+      if constexpr (sizeof(T) == 2 || kSplitF32) {
+        // bf16 values are exact, fp32 values split into three bf16 parts like
+        // P; tiles b and b + 1 of the batch form one product over 32 keys (k = 8 g + j: key
         // 4 g + j of tile b for j < 4, of tile b + 1 otherwise), a tile past
         // the row contributing P = 0
         static_assert(BT % 2 == 0, "tile pairs");
@@ -579,7 +592,7 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
               v8[i] = va[b][i][dt];
               v8[4 + i] = va[b + 1][i][dt];
             }
-            oacc[dt] = mfma_split3(pack_bf16x8(v8), ps, oacc[dt]);
+            oacc[dt] = mfma_bf16x<T>(v8, ps, oacc[dt]);
           }
         }
       } else {
@@ -654,11 +667,16 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
 // exp(m_old - m_new) when the maximum grows.  The waves' (m, z, O) are merged
 // in LDS (log-sum-exp), which gives V^c_j and the softmax statistics; then
 // every member row receives V^c_j (Eq. 6).
+//
+// PARTIAL: the same pass over one chunk of kFlashChunk keys per workgroup
+// (several chunks of a long sequence), writing the chunk's (m, z,
+// unnormalised values) for attn_merge_kernel instead of the member rows.
 // ---------------------------------------------------------------------------
 constexpr int kFlashWaves = 8;
 constexpr int kFlashThreads = 64 * kFlashWaves;
+constexpr int kFlashChunk = 2048;  // keys per workgroup of the partial pass
 
-template <int D, typename T>
+template <int D, typename T, bool PARTIAL>
 __global__ __launch_bounds__(kFlashThreads) void attn_flash_kernel(AttnArgs a) {
   constexpr int KS = D / 4, DT = D / 16, NW = kFlashWaves;
   constexpr uint32_t ESZ = sizeof(T);
@@ -666,20 +684,26 @@ __global__ __launch_bounds__(kFlashThreads) void attn_flash_kernel(AttnArgs a) {
   __shared__ float wm[NW][16], wz[NW][16];
   __shared__ __align__(16) float vhat[16][D];
   __shared__ int moff[17];
-  __shared__ int mlist[kChunk];
+  __shared__ int mlist[PARTIAL ? 1 : kChunk];
 
-  const int wi = xcd_work_item();  // tile fastest, then (batch, head)
-  if (wi >= a.ntile * a.units) return;
-  const int tile = wi % a.ntile, u = wi / a.ntile;
-  const int n = unit_length(a.lengths, u / a.heads, a.N);
+  // tile fastest, (then chunk,) then (batch, head): the tiles that read the
+  // same keys run together on one XCD and share its L2
+  const int wi = xcd_work_item();
+  const int nfc = PARTIAL ? a.npc : 1;
+  if (wi >= nfc * a.ntile * a.units) return;
+  const int tile = wi % a.ntile, chunk = (wi / a.ntile) % nfc, u = wi / (nfc * a.ntile);
+  const int nu = unit_length(a.lengths, u / a.heads, a.N);
+  const int k0 = PARTIAL ? chunk * kFlashChunk : 0;
+  if (PARTIAL && k0 >= nu) return;  // a chunk past the sequence: the merge does not read it
+  const int n = PARTIAL ? min(kFlashChunk, nu - k0) : nu;  // keys of this workgroup
   const int C = a.C;
   const int j0 = tile * 16;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int c = lane & 15, g = lane >> 4;
   // the centroid rows and (fp32) the first key tile do not depend on the
   // member offsets: they are requested first, so that both latencies overlap
-  const T* ku = static_cast<const T*>(a.k) + static_cast<size_t>(u) * a.N * D;
-  const T* vu = static_cast<const T*>(a.v) + static_cast<size_t>(u) * a.N * D;
+  const T* ku = static_cast<const T*>(a.k) + (static_cast<size_t>(u) * a.N + k0) * D;
+  const T* vu = static_cast<const T*>(a.v) + (static_cast<size_t>(u) * a.N + k0) * D;
   const __amdgpu_buffer_rsrc_t rk = make_rsrc(ku, static_cast<uint32_t>(n) * D * ESZ);
   const __amdgpu_buffer_rsrc_t rv = make_rsrc(vu, static_cast<uint32_t>(n) * D * ESZ);
   const int nkt = (n + 15) / 16;
@@ -698,11 +722,12 @@ __global__ __launch_bounds__(kFlashThreads) void attn_flash_kernel(AttnArgs a) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) buf_load<DT>(rv, voff, i * D * ESZ, vx[i], T{});
   };
-  if constexpr (sizeof(T) == 4) load_tile(wave, kbuf[0], vbuf[0]);
+  if constexpr (sizeof(T) == 4 && !kSplitF32) load_tile(wave, kbuf[0], vbuf[0]);
   const int32_t* ou = a.offsets + static_cast<size_t>(u) * (C + 1);
   if (tid < 17) moff[tid] = ou[min(j0 + tid, C)];
   __syncthreads();
   if (moff[16] == moff[0] || n == 0) {  // every cluster of the tile is empty: V^c = 0
+    if constexpr (PARTIAL) return;       // (the merge writes it)
     const size_t uj0 = static_cast<size_t>(u) * C + j0;
     for (int x = tid; x < 16 * D; x += kFlashThreads)
       if (j0 + x / D < C) a.vcb[uj0 * D + x] = 0.0f;
@@ -710,9 +735,9 @@ __global__ __launch_bounds__(kFlashThreads) void attn_flash_kernel(AttnArgs a) {
   }
   const int m0 = moff[0], mn = moff[16] - m0;
   // the member lists are requested now and stored once the products are done
-  constexpr int MPT = kChunk / kFlashThreads;
+  constexpr int MPT = PARTIAL ? 1 : kChunk / kFlashThreads;
   int mreg[MPT];
-  {
+  if constexpr (!PARTIAL) {
     const int32_t* mg = a.members + static_cast<size_t>(u) * a.N + m0;
 #pragma unroll
     for (int e = 0; e < MPT; ++e) {
@@ -724,17 +749,16 @@ __global__ __launch_bounds__(kFlashThreads) void attn_flash_kernel(AttnArgs a) {
   v4f oacc[DT];
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) oacc[dt] = v4f{0.f, 0.f, 0.f, 0.f};
-  if constexpr (sizeof(T) == 2) {
-    // bf16 inputs: both products on the bf16 matrix cores, exact for the bf16
-    // keys and values, with Q^c and P split into three bf16 parts each (an fp32
-    // value is exactly the sum of its three truncated parts), so that every
-    // logit and value keeps fp32 accuracy: three part products per 32 dims or
-    // per 32 keys.  The k index of a product over dims maps to the lane's own
-    // dims g KS + 8 m + j; over keys, k = 8 g + j is key 4 g + j of the
-    // block's first tile (j < 4) or key 4 g + j - 4 of its second, which is
-    // where the logit results put P.  (For fp32 inputs the same scheme needs
-    // six part products and the splits of K and V, and measured no faster than
-    // the fp32 matrix cores, which the fp32 branch below uses.)
+  if constexpr (sizeof(T) == 2 || kSplitF32) {
+    // Both products on the bf16 matrix cores, with Q^c and P split into three
+    // bf16 parts each (an fp32 value is exactly the sum of its three truncated
+    // parts), so that every logit and value keeps fp32 accuracy: bf16 keys and
+    // values are exact (three part products per 32 dims or per 32 keys), fp32
+    // keys and values are split too (six part products, mfma_split6).  The k
+    // index of a product over dims maps to the lane's own dims g KS + 8 m + j;
+    // over keys, k = 8 g + j is key 4 g + j of the block's first tile (j < 4)
+    // or key 4 g + j - 4 of its second, which is where the logit results put
+    // P.
     constexpr int NC = KS / 8;              // 32-dim chunks
     Split8 qs[NC];
 #pragma unroll
@@ -759,7 +783,7 @@ __global__ __launch_bounds__(kFlashThreads) void attn_flash_kernel(AttnArgs a) {
         v4f acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int m = 0; m < NC; ++m) {
-          acc = mfma_split3(pack_bf16x8(&kx[t][8 * m]), qs[m], acc);
+          acc = mfma_bf16x<T>(&kx[t][8 * m], qs[m], acc);
         }
 #pragma unroll
         for (int i = 0; i < 4; ++i) o[4 * t + i] = ((2 * bk + t) * 16 + 4 * g + i < n) ? acc[i] * a.scale : -INFINITY;
@@ -787,7 +811,7 @@ __global__ __launch_bounds__(kFlashThreads) void attn_flash_kernel(AttnArgs a) {
           va8[j] = vx[0][j][dt];
           va8[4 + j] = vx[1][j][dt];
         }
-        oacc[dt] = mfma_split3(pack_bf16x8(va8), ps, oacc[dt] * alpha);
+        oacc[dt] = mfma_bf16x<T>(va8, ps, oacc[dt] * alpha);
       }
     };
     for (int bk = wave; bk < nkb; bk += NW) {
@@ -796,7 +820,8 @@ __global__ __launch_bounds__(kFlashThreads) void attn_flash_kernel(AttnArgs a) {
       step(bk, kx, vx);
     }
   } else {
-    // fp32 inputs: the loop is unrolled so that no buffer is copied; every
+    // fp32 inputs on the fp32 matrix cores (kSplitF32 false): the loop is
+    // unrolled so that no buffer is copied; every
     // load is issued, rows past n reading as 0, so that the compiler counts
     // them and each tile waits only for its own rows (the first tile was
     // requested before the offsets)
@@ -844,10 +869,12 @@ __global__ __launch_bounds__(kFlashThreads) void attn_flash_kernel(AttnArgs a) {
   for (int r = 0; r < 4; ++r)
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) red[wave][c][DT * (4 * g + r) + dt] = oacc[dt][r];
+  if constexpr (!PARTIAL) {
 #pragma unroll
-  for (int e = 0; e < MPT; ++e) {
-    const int x = tid + kFlashThreads * e;
-    if (x < mn) mlist[x] = mreg[e];
+    for (int e = 0; e < MPT; ++e) {
+      const int x = tid + kFlashThreads * e;
+      if (x < mn) mlist[x] = mreg[e];
+    }
   }
   __syncthreads();
   for (int x = tid; x < 16 * D; x += kFlashThreads) {
@@ -864,6 +891,15 @@ __global__ __launch_bounds__(kFlashThreads) void attn_flash_kernel(AttnArgs a) {
     }
     if (j0 + cc >= C) continue;
     const size_t ujc = static_cast<size_t>(u) * C + j0 + cc;
+    if constexpr (PARTIAL) {  // the chunk's state, relative to its maximum M
+      const size_t pj = ujc * a.nchunk + chunk;
+      a.pacc[pj * D + dim] = O;
+      if (dim == 0) {
+        a.pm[pj] = M;
+        a.pz[pj] = Z;
+      }
+      continue;
+    }
     const bool nonempty = moff[cc + 1] > moff[cc];
     const float val = nonempty ? O / Z : 0.0f;
     vhat[cc][dim] = val;
@@ -873,6 +909,7 @@ __global__ __launch_bounds__(kFlashThreads) void attn_flash_kernel(AttnArgs a) {
       a.stats[ujc * 2 + 1] = Z;
     }
   }
+  if constexpr (PARTIAL) return;
   __syncthreads();
   // Eq. (6): each member row receives V^c_j; a lane writes 4 dims of a row
   T* out = static_cast<T*>(a.out) + static_cast<size_t>(u) * a.N * D;
@@ -926,7 +963,7 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
     }
     return;
   }
-  const int nch = (n + kChunk - 1) / kChunk;
+  const int nch = (n + a.pchunk - 1) / a.pchunk;
   constexpr int RPS = 64 / D;
   const int t = lane % D, r = lane / D;
   float M = -INFINITY, Z = 0.0f;
@@ -1292,6 +1329,8 @@ static AttnArgs make_args(const Problem& p, const Workspace& ws, const int32_t* 
   a.nchunk = ws.nchunk;
   a.ntile = (p.C + 15) / 16;
   a.ncg = (p.C + 3) / 4;
+  a.pchunk = kChunk;
+  a.npc = 1;
   // at most C + n / kSparseChunk (cluster, member chunk) items per unit
   a.nsg = (p.C + (p.n + kSparseChunk - 1) / kSparseChunk + 3) / 4;
   a.units = p.units();
@@ -1315,33 +1354,40 @@ static AttnArgs make_args(const Problem& p, const Workspace& ws, const int32_t* 
 static int sparse_tiles(int topk) { return topk <= 16 ? 1 : topk <= 32 ? 2 : topk <= 64 ? 4 : 8; }
 
 // part 0: the tile kernel (single chunk: the whole stage); part 1: the merge
-// of several chunks (nothing for a single chunk).
+// of several chunks (nothing for a single chunk).  The clustered variant
+// takes every chunk in the single-pass kernel, kFlashChunk keys per
+// workgroup.
 template <int D, typename T>
 static hipError_t launch_attn_t(const Problem& p, const Workspace& ws, const int32_t* topk_in,
                                 int part, hipStream_t s) {
-  const AttnArgs a = make_args(p, ws, topk_in);
+  AttnArgs a = make_args(p, ws, topk_in);
   const bool improved = p.topk > 0;
-  const dim3 g1(xcd_grid(static_cast<long long>(a.nchunk) * a.ntile * a.units));
   const dim3 g2(xcd_grid(static_cast<long long>(a.ncg) * a.units));
   if (ws.nchunk == 1) {
     if (part != 0) return hipSuccess;
+    const dim3 g1(xcd_grid(static_cast<long long>(a.ntile) * a.units));
     if (improved)
       hipLaunchKernelGGL((attn_tile_kernel<D, T, 1>), g1, dim3(kTileThreads), 0, s, a);
     else
-      hipLaunchKernelGGL((attn_flash_kernel<D, T>), g1, dim3(kFlashThreads), 0, s, a);
+      hipLaunchKernelGGL((attn_flash_kernel<D, T, false>), g1, dim3(kFlashThreads), 0, s, a);
     return hipGetLastError();
   }
-  if (part == 0) {
-    if (improved)
-      hipLaunchKernelGGL((attn_tile_kernel<D, T, 3>), g1, dim3(kTileThreads), 0, s, a);
-    else
-      hipLaunchKernelGGL((attn_tile_kernel<D, T, 2>), g1, dim3(kTileThreads), 0, s, a);
-  } else {
-    if (improved)
-      hipLaunchKernelGGL((attn_merge_kernel<D, T, true>), g2, dim3(256), 0, s, a);
-    else
+  if (!improved) {
+    a.pchunk = kFlashChunk;  // the states keep the stride ws.nchunk
+    a.npc = (p.n + kFlashChunk - 1) / kFlashChunk;
+    if (part == 0) {
+      const dim3 g1(xcd_grid(static_cast<long long>(a.npc) * a.ntile * a.units));
+      hipLaunchKernelGGL((attn_flash_kernel<D, T, true>), g1, dim3(kFlashThreads), 0, s, a);
+    } else {
       hipLaunchKernelGGL((attn_merge_kernel<D, T, false>), g2, dim3(256), 0, s, a);
+    }
+    return hipGetLastError();
   }
+  const dim3 g1(xcd_grid(static_cast<long long>(a.nchunk) * a.ntile * a.units));
+  if (part == 0)
+    hipLaunchKernelGGL((attn_tile_kernel<D, T, 3>), g1, dim3(kTileThreads), 0, s, a);
+  else
+    hipLaunchKernelGGL((attn_merge_kernel<D, T, true>), g2, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

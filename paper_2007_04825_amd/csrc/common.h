@@ -239,6 +239,32 @@ __device__ __forceinline__ v4f mfma_split3(v4u a, const Split8& b, v4f c) {
   return c;
 }
 
+// A.B with both operands fp32, each split exactly into three bf16 parts
+// (x = hi + mid + lo): the six part products of relative size 2^-16 and
+// above, smallest first.  The three left out are below 2^-24 |a_k b_k| each,
+// so the result matches an fp32 product sum to within a few units of 2^-24
+// (products exact, sums in fp32), on the bf16 matrix cores.
+__device__ __forceinline__ v4f mfma_split6(const Split8& a, const Split8& b, v4f c) {
+  c = mfma_bf16_16x16x32(a.l, b.h, c);
+  c = mfma_bf16_16x16x32(a.m, b.m, c);
+  c = mfma_bf16_16x16x32(a.h, b.l, c);
+  c = mfma_bf16_16x16x32(a.m, b.h, c);
+  c = mfma_bf16_16x16x32(a.h, b.m, c);
+  c = mfma_bf16_16x16x32(a.h, b.h, c);
+  return c;
+}
+// Eight values of the element type T (widened to fp32) times a split B on
+// the bf16 matrix cores: bf16 values are exact as one operand (three
+// products), fp32 values are split as well (six products).
+template <typename T>
+__device__ __forceinline__ v4f mfma_bf16x(const float* x8, const Split8& b, v4f c) {
+  if constexpr (sizeof(T) == 2) {
+    return mfma_split3(pack_bf16x8(x8), b, c);
+  } else {
+    return mfma_split6(split8(x8), b, c);
+  }
+}
+
 __device__ __forceinline__ v4f mfma_f32_16x16x4(float a, float b, v4f c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }

@@ -616,8 +616,8 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
 // ===========================================================================
 // Cooperative path: the workgroups of a unit run all L rounds in one launch.
 //
-// Workgroup b of unit u holds queries [b Q, (b + 1) Q) (Q = 1024 or 2048:
-// the smaller one whose grid the device holds at once) with their codes,
+// Workgroup b of unit u holds queries [b Q, (b + 1) Q) (Q = 2048, or 1024
+// when that grid does not fit on the device at once) with their codes,
 // assignments and bit-pair counts resident in LDS, as the one-workgroup
 // kernel does.  The unit's counts live in two running-total tables of
 // 64-bit words (a cluster row has 32 words, each holding the two 32-bit
@@ -634,8 +634,14 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
 // every reader of round t has passed.  The arrival counter is one 64-bit
 // word: each arrival adds 1 to its low half and, when some query of the
 // workgroup moved in that round, 1 to its high half, so the poll that sees
-// the last arrival also tells whether any query of the unit moved.  The
-// launch is cooperative, so all workgroups are resident
+// the last arrival also tells whether any query of the unit moved.  Every
+// value that crosses workgroups travels through device-scope atomics or
+// stores, each wave waits until its own have been performed before the
+// workgroup barrier that precedes the arrival, and the waiting side reads
+// with device-scope loads issued after it has seen every arrival; so the
+// arrival itself needs no cache write-back or invalidation (which cost each
+// round several microseconds when measured).  The launch is cooperative, so
+// all workgroups are resident
 // together and every wait ends; each wait is also bounded.  A round in which
 // no query of the unit moved ends the loop: every later round would repeat
 // it.  The final member lists come from the per-workgroup sizes of the last
