@@ -711,10 +711,17 @@ __global__ __launch_bounds__(kKmThreads) void kmeans_coop_kernel(CoopArgs a) {
   const int q0 = b * QW;
   const size_t row0 = static_cast<size_t>(u) * N;
   for (int i = max(n, q0) + tid; i < min(N, q0 + QW); i += kKmThreads) a.assign[row0 + i] = -1;
+  int32_t* lsz = a.lsizes + (static_cast<size_t>(u) * nwg + b) * C;
+  int32_t* bs = a.bases + (static_cast<size_t>(u) * nwg + b) * C;
   if (n == 0) {  // the same in every workgroup of the unit: none of them waits
     if (b == 0) {
       for (int j = tid; j < C; j += kKmThreads) a.sizes[static_cast<size_t>(u) * C + j] = 0;
       for (int j = tid; j <= C; j += kKmThreads) a.offsets[static_cast<size_t>(u) * (C + 1) + j] = 0;
+    }
+    // every block's member ranges are empty (the centroid kernels read them all)
+    for (int j = tid; j < C; j += kKmThreads) {
+      lsz[j] = 0;
+      bs[j] = 0;
     }
     return;
   }
@@ -748,7 +755,6 @@ __global__ __launch_bounds__(kKmThreads) void kmeans_coop_kernel(CoopArgs a) {
       reinterpret_cast<unsigned long long*>(a.sync + static_cast<size_t>(u) * kSyncInts);
   unsigned long long moved_before = 0;  // high half of the arrival word after the previous round
   const size_t U = gridDim.y;
-  int32_t* lsz = a.lsizes + (static_cast<size_t>(u) * nwg + b) * C;
   for (int t = 0; t < a.L; ++t) {
     // the first four query tiles' operands, rebuilt each round (registers are
     // scarcer here than in the one-workgroup kernel)
@@ -890,7 +896,6 @@ __global__ __launch_bounds__(kKmThreads) void kmeans_coop_kernel(CoopArgs a) {
     }
   }
   __syncthreads();
-  int32_t* bs = a.bases + (static_cast<size_t>(u) * nwg + b) * C;
   for (int j = tid; j < C; j += kKmThreads) {
     if (b == 0) a.sizes[static_cast<size_t>(u) * C + j] = j < ce ? sh.tsize[j] : 0;
     bs[j] = j < ce ? sh.off[j] : 0;

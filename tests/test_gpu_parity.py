@@ -224,6 +224,29 @@ def test_many_clusters_every_driver(N, dtype, topk, variant):
         assert np.array_equal(r["assign"], results[0]["assign"])
 
 
+@pytest.mark.parametrize("variant", ["clustered", "iclustered"])
+def test_block_kmeans_ragged_and_empty(variant):
+    """The several-block K-means drivers with empty, one-row, one-block and
+    block-edge sequences in one batch (every block of an empty sequence must
+    still describe empty member ranges)."""
+    import paper_2007_04825_amd as ca
+    w = gen.config_tiny(B=5, H=1, N=5000, d=32, C=100, L=4, topk=32)
+    w.lengths = np.array([5000, 0, 1, 2049, 4097], np.int32)
+    t = w.topk if variant == "iclustered" else 0
+    ref = run_oracle(w, t, key="blockragged")
+    try:
+        for path in (2, 3):
+            ca.set_kmeans_path(path)
+            print("driver %d" % path, flush=True)
+            got = run_gpu(w, t)
+            assert np.array_equal(got["assign"], ref["assign"]), "driver %d" % path
+            assert np.array_equal(got["sizes"], ref["sizes"])
+            np.testing.assert_allclose(got["centroids"], ref["qc"], rtol=0, atol=2e-6)
+            compare_outputs(w, ref, got, t)
+    finally:
+        ca.set_kmeans_path(0)
+
+
 def test_invalid_arguments_enqueue_nothing():
     """A rejected call (through the C ABI) returns its error code and leaves
     the output untouched: nothing was enqueued, also seen after the stream has
