@@ -239,6 +239,31 @@ int oracle_top_attention_fwd(const void* q, const void* k, const void* v,
                              int d, int dtype, int topk, void* out, int32_t* topk_out,
                              void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the
+ * improved clustered attention forward of iclustered_attention_fwd, with the
+ * same arguments and results but no workspace argument.  Its scratch is a
+ * device array of CA_NOALLOC_SCRATCH_BYTES bytes inside the library, one per
+ * GPU, held until the process ends; the call allocates nothing (no hipMalloc,
+ * no hipFree, no allocating library routine).  Sizes whose workspace
+ * (ca_workspace_bytes with the same arguments) exceeds that maximum are
+ * rejected with CA_ERR_UNSUPPORTED before anything is enqueued.  Every call
+ * on one GPU uses that GPU's single array, which keeps the last call's
+ * contents (nothing in it needs to start at zero): calls that overlap on one
+ * GPU, on different streams or threads, race and give wrong results; calls
+ * on one stream are ordered and safe.  As with the workspace of the other
+ * entry point, the array then holds the call's forward state, but no
+ * backward entry point can be pointed at it.
+ */
+#define CA_NOALLOC_SCRATCH_BYTES (64u * 1024u * 1024u)
+int iclustered_attention_fwd_noalloc(const void* q, const void* k, const void* v,
+                                     const int32_t* lengths, const float* planes,
+                                     int batch, int heads, int n, int d, int dtype,
+                                     int n_clusters, int n_bits, int lloyd_iters,
+                                     int topk, void* out, const ca_aux* aux,
+                                     void* stream);
+
 /* Message describing the last non-zero status returned on this thread. */
 const char* ca_last_error(void);
 

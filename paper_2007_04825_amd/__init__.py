@@ -20,6 +20,7 @@ __all__ = [
     "backward_workspace_bytes", "clustered_attention_bwd", "iclustered_attention_bwd",
     "clustered_attention_backward", "iclustered_attention_backward",
     "oracle_top_workspace_bytes", "oracle_top_attention_fwd", "oracle_top_attention",
+    "iclustered_attention_fwd_noalloc", "NOALLOC_SCRATCH_BYTES",
 ]
 
 CA_OK = 0
@@ -34,7 +35,10 @@ EXPORTED_SYMBOLS = ("ca_workspace_bytes", "clustered_attention_fwd", "iclustered
                     "ca_last_error", "ca_version", "ca_set_kmeans_path", "ca_time_next_stage",
                     "ca_backward_workspace_bytes", "clustered_attention_bwd",
                     "iclustered_attention_bwd", "ca_oracle_top_workspace_bytes",
-                    "oracle_top_attention_fwd")
+                    "oracle_top_attention_fwd", "iclustered_attention_fwd_noalloc")
+# bytes of the allocation-free entry point's device scratch (the header's
+# CA_NOALLOC_SCRATCH_BYTES)
+NOALLOC_SCRATCH_BYTES = 64 * 1024 * 1024
 CA_KERNEL_HASH, CA_KERNEL_KMEANS, CA_KERNEL_CENTROIDS, CA_KERNEL_CENTROID_ATTN, CA_KERNEL_OUTPUT = \
     1, 2, 3, 4, 5
 CA_KERNEL_BWD_CENTROID = 6
@@ -83,6 +87,8 @@ def library():
     lib.clustered_attention_fwd.restype = i32
     lib.iclustered_attention_fwd.argtypes = common + [i32, vp, vp, sz, ctypes.POINTER(Aux), vp]
     lib.iclustered_attention_fwd.restype = i32
+    lib.iclustered_attention_fwd_noalloc.argtypes = common + [i32, vp, ctypes.POINTER(Aux), vp]
+    lib.iclustered_attention_fwd_noalloc.restype = i32
     lib.ca_last_error.argtypes = []
     lib.ca_last_error.restype = ctypes.c_char_p
     lib.ca_version.restype = i32
@@ -179,6 +185,17 @@ def iclustered_attention_fwd(q, k, v, lengths, planes, batch, heads, n, d, dtype
         q, k, v, lengths, planes, batch, heads, n, d, dtype, n_clusters, n_bits, lloyd_iters,
         topk, out, workspace, workspace_nbytes, ctypes.byref(aux) if aux is not None else None,
         stream)
+
+
+def iclustered_attention_fwd_noalloc(q, k, v, lengths, planes, batch, heads, n, d, dtype,
+                                     n_clusters, n_bits, lloyd_iters, topk, out, aux=None,
+                                     stream=None):
+    """Raw call of the allocation-free entry point (the library's own device
+    scratch instead of a workspace) with integer device addresses; returns the
+    status code."""
+    return library().iclustered_attention_fwd_noalloc(
+        q, k, v, lengths, planes, batch, heads, n, d, dtype, n_clusters, n_bits, lloyd_iters,
+        topk, out, ctypes.byref(aux) if aux is not None else None, stream)
 
 
 # ---------------------------------------------------------------------------

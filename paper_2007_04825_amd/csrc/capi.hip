@@ -5,6 +5,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <mutex>
 #include <string>
 
 #include "../../include/clustered_attn.h"
@@ -385,6 +386,40 @@ static int run_backward(const void* q, const void* k, const void* v, const int32
   return CA_OK;
 }
 
+// Device-resident scratch of the allocation-free entry point: one array per
+// GPU that the library runs on, held until the process ends, shared by every
+// call on that GPU.  Host code never uses the array's name as an address: its
+// device address comes from hipGetSymbolAddress once per device.
+constexpr size_t kScratchBytes = static_cast<size_t>(CA_NOALLOC_SCRATCH_BYTES);
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+constexpr int kMaxDevices = 64;
+static void* g_scratch_ptr[kMaxDevices] = {nullptr};
+static std::mutex g_scratch_mutex;
+
+// The current device's scratch address, looked up on its first use (with that
+// device current); null with the error recorded if the lookup fails.
+static void* scratch_address(int* rc) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    *rc = fail(CA_ERR_HIP, "hipGetDevice failed or device index out of range: %s", hipGetErrorString(e));
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || ptr == nullptr) {
+      *rc = fail(CA_ERR_HIP, "hipGetSymbolAddress(scratch) failed on device %d: %s", dev,
+                 hipGetErrorString(e));
+      return nullptr;
+    }
+    g_scratch_ptr[dev] = ptr;
+  }
+  *rc = CA_OK;
+  return g_scratch_ptr[dev];
+}
+
 }  // namespace ca
 
 extern "C" {
@@ -430,6 +465,32 @@ int iclustered_attention_fwd(const void* q, const void* k, const void* v, const 
     if (topk < 1) return ca::fail(CA_ERR_INVALID_ARG, "topk must be >= 1 (got %d)", topk);
     return ca::run_forward(q, k, v, lengths, planes, batch, heads, n, d, dtype, n_clusters,
                            n_bits, lloyd_iters, topk, out, workspace, workspace_bytes, aux, stream);
+  } catch (...) {
+    return ca::fail(CA_ERR_HIP, "unexpected C++ exception");
+  }
+}
+
+int iclustered_attention_fwd_noalloc(const void* q, const void* k, const void* v,
+                                     const int32_t* lengths, const float* planes, int batch,
+                                     int heads, int n, int d, int dtype, int n_clusters,
+                                     int n_bits, int lloyd_iters, int topk, void* out,
+                                     const ca_aux* aux, void* stream) {
+  try {
+    if (topk < 1) return ca::fail(CA_ERR_INVALID_ARG, "topk must be >= 1 (got %d)", topk);
+    // sizes first, so that a rejected call touches no device state
+    const size_t need = ca_workspace_bytes(batch, heads, n, d, dtype, n_clusters, n_bits, topk);
+    if (need == 0)
+      return ca::run_forward(q, k, v, lengths, planes, batch, heads, n, d, dtype, n_clusters,
+                             n_bits, lloyd_iters, topk, out, nullptr, 0, aux, stream);
+    if (need > ca::kScratchBytes)
+      return ca::fail(CA_ERR_UNSUPPORTED,
+                      "these sizes need %zu bytes of scratch; the allocation-free entry point holds %zu",
+                      need, ca::kScratchBytes);
+    int rc = CA_OK;
+    void* ws = ca::scratch_address(&rc);
+    if (ws == nullptr) return rc;
+    return ca::run_forward(q, k, v, lengths, planes, batch, heads, n, d, dtype, n_clusters, n_bits,
+                           lloyd_iters, topk, out, ws, ca::kScratchBytes, aux, stream);
   } catch (...) {
     return ca::fail(CA_ERR_HIP, "unexpected C++ exception");
   }
