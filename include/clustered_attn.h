@@ -38,7 +38,7 @@
  *   returns a message for the calling thread.  No C++ exception crosses this
  *   interface.
  *
- * Supported sizes: d in {32, 64}; 1 <= n_bits <= 63; 1 <= C <= 256;
+ * Supported sizes: d in {32, 64}; 1 <= n_bits <= 64; 1 <= C <= 256;
  * 1 <= L <= 1000; 1 <= k <= 128; 1 <= n <= 1048576; 1 <= batch*heads <= 65535
  * and batch*heads*n < 2^31.
  *

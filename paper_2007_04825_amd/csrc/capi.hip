@@ -147,7 +147,7 @@ static int check_sizes(int batch, int heads, int n, int d, int dtype, int C, int
   if (L < 1) return fail(CA_ERR_INVALID_ARG, "lloyd_iters must be >= 1 (got %d)", L);
   if (improved && topk < 1) return fail(CA_ERR_INVALID_ARG, "topk must be >= 1 (got %d)", topk);
   if (d != 32 && d != 64) return fail(CA_ERR_UNSUPPORTED, "d must be 32 or 64 (got %d)", d);
-  if (n_bits > 63) return fail(CA_ERR_UNSUPPORTED, "n_bits must be <= 63 (got %d)", n_bits);
+  if (n_bits > 64) return fail(CA_ERR_UNSUPPORTED, "n_bits must be <= 64 (got %d)", n_bits);
   if (C > 256) return fail(CA_ERR_UNSUPPORTED, "n_clusters must be <= 256 (got %d)", C);
   if (L > 1000) return fail(CA_ERR_UNSUPPORTED, "lloyd_iters must be <= 1000 (got %d)", L);
   if (improved && topk > 128) return fail(CA_ERR_UNSUPPORTED, "topk must be <= 128 (got %d)", topk);

@@ -2,15 +2,16 @@
 // cluster-sorted member lists (CSR) that the later stages read.
 //
 // Assign step on the int8 matrix cores.  A code h is expanded to a 64-entry
-// int8 vector: bit b (b < n_bits) becomes +64 / -64 for a query and +2 / -2
-// for a centroid, positions n_bits..62 are 0, and position 63 (never a hash
-// bit, n_bits <= 63) carries 1 for a query and 127 - j for centroid j.  One
-// v_mfma_i32_16x16x64_i8 then yields, for 16 centroids x 16 queries,
-//     key = 128 * (n_bits - 2 * ham(h, c_j)) + 127 - j,
+// int8 vector: bit b (b < n_bits) becomes +64 / -64 for a query and +16 / -16
+// for a centroid, positions n_bits..63 are 0.  One v_mfma_i32_16x16x64_i8,
+// its accumulator starting at kTie - j for centroid j, then yields for 16
+// centroids x 16 queries
+//     key = 1024 * (n_bits - 2 * ham(h, c_j)) + kTie - j      (kTie = 1023),
 // so the largest key is the nearest centroid with ties resolved to the
-// smallest index, exactly; the argmin costs one integer max per distance.
-// Centroid slots past C_eff in the last 16-wide tile repeat centroid 0 with
-// tie byte -128 (index 255), so they can never win against centroid 0.
+// smallest index, exactly (the tie term spans 1024 values, the distance term
+// steps by 2048); the argmin costs one integer max per distance, and all 64
+// code bits are usable.  Centroid slots past C_eff in the last 16-wide tile
+// start from a large negative accumulator, so they never win.
 //
 // Update step.  Member bit counts live in LDS as 16-bit pairs (dword w holds
 // the counts of bits 2w and 2w+1); a lane adds its query's 32 pairs with LDS
@@ -64,7 +65,10 @@ __device__ __forceinline__ OpMasks op_masks(int g, int n_bits) {
   return m;
 }
 
-// Bits 16g..16g+15 of a query code as 16 int8: +64 / -64, 0 past n_bits, 1 at slot 63.
+constexpr int kTie = 1023;               // tie term of cluster 0; cluster j adds kTie - j
+constexpr int kTieNone = -(1 << 30);     // accumulator start of slots past C_eff
+
+// Bits 16g..16g+15 of a query code as 16 int8: +64 / -64, 0 past n_bits.
 __device__ __forceinline__ v4i query_operand(uint64_t code, int g, const OpMasks& m) {
   const uint32_t x = static_cast<uint32_t>(code >> (16 * g)) & 0xffffu;
   v4i r;
@@ -73,24 +77,33 @@ __device__ __forceinline__ v4i query_operand(uint64_t code, int g, const OpMasks
     const uint32_t s = spread4((x >> (4 * q)) & 0xfu);
     r[q] = static_cast<int>((0xc0c0c0c0u ^ (s << 7)) & m.keep[q]);
   }
-  if (g == 3) r[3] |= 0x01000000;
   return r;
 }
 
-// 16 code bits x (bits 16g..16g+15 of centroid j) as 16 int8: +2 / -2, 0 past
-// n_bits, 127 - j at slot 63.
-__device__ __forceinline__ v4i centroid_operand16(uint32_t x, int g, const OpMasks& m, int j) {
+// 16 code bits x (bits 16g..16g+15 of a centroid) as 16 int8: +16 / -16, 0
+// past n_bits.
+__device__ __forceinline__ v4i centroid_operand16(uint32_t x, const OpMasks& m) {
   v4i r;
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const uint32_t s = spread4((x >> (4 * q)) & 0xfu);
-    r[q] = static_cast<int>((0xfefefefeu ^ (s * 0xfcu)) & m.keep[q]);
+    r[q] = static_cast<int>((0xf0f0f0f0u ^ (s * 0xe0u)) & m.keep[q]);
   }
-  if (g == 3) r[3] |= static_cast<int>(static_cast<uint32_t>(static_cast<uint8_t>(127 - j)) << 24);
   return r;
 }
-__device__ __forceinline__ v4i centroid_operand(uint64_t code, int g, const OpMasks& m, int j) {
-  return centroid_operand16(static_cast<uint32_t>(code >> (16 * g)) & 0xffffu, g, m, j);
+__device__ __forceinline__ v4i centroid_operand(uint64_t code, int g, const OpMasks& m) {
+  return centroid_operand16(static_cast<uint32_t>(code >> (16 * g)) & 0xffffu, m);
+}
+// Accumulator start of centroid tile ct for this lane's four result rows
+// (centroids 16 ct + 4 (lane / 16) + r): the tie term, or kTieNone past C_eff.
+__device__ __forceinline__ v4i tie_init(int ct, int ce, int lane) {
+  v4i r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int j = ct * 16 + 4 * (lane >> 4) + i;
+    r[i] = j < ce ? kTie - j : kTieNone;
+  }
+  return r;
 }
 
 // Same as query_operand, from a table mapping 8 code bits to 8 int8 entries.
@@ -103,32 +116,18 @@ __device__ __forceinline__ v4i query_operand_lut(uint64_t code, int g, const OpM
   r[1] = static_cast<int>(lo.y & m.keep[1]);
   r[2] = static_cast<int>(hi.x & m.keep[2]);
   r[3] = static_cast<int>(hi.y & m.keep[3]);
-  if (g == 3) r[3] |= 0x01000000;
   return r;
 }
 
 // Cluster index from the best key.
 __device__ __forceinline__ int decode_cluster(int best, int n_bits) {
-  return (128 * n_bits + 127 - best) & 255;
+  return (1024 * n_bits + kTie - best) & 2047;
 }
 
 // Bit-pair w of a code as two 16-bit counters.
 __device__ __forceinline__ uint32_t pair_val(uint64_t code, int w) {
   const uint32_t x = static_cast<uint32_t>(code >> (2 * w));
   return (x & 1u) | ((x & 2u) << 15);
-}
-
-// Best key over the centroid tiles for one 16-query tile (B operand bq).
-// cop[ct * 64 + lane] holds the A operand of centroid tile ct.
-__device__ __forceinline__ int best_key(const v4i* cop, int nct, v4i bq, int lane) {
-  int best = INT_MIN;
-  const v4i zero = {0, 0, 0, 0};
-  for (int ct = 0; ct < nct; ++ct) {
-    const v4i d = mfma_i8_16x16x64(cop[ct * 64 + lane], bq, zero);
-    best = max(best, max(max(d[0], d[1]), max(d[2], d[3])));
-  }
-  best = cross_rows_max(best);
-  return best;
 }
 
 // Best keys of NG 16-query tiles at once: one centroid-operand load feeds NG
@@ -138,12 +137,14 @@ __device__ __forceinline__ int best_key(const v4i* cop, int nct, v4i bq, int lan
 // with a repeat, which saves its products but (measured) slows the
 // one-workgroup-per-unit kernel, whose schedule favours the branch-free form.
 template <int NG, bool EXACT_TAIL>
-__device__ __forceinline__ void best_keys(const v4i* cop, int nct, const v4i* bq, int* best, int lane) {
-  const v4i zero = {0, 0, 0, 0};
+__device__ __forceinline__ void best_keys(const v4i* cop, int nct, int ce, const v4i* bq, int* best, int lane) {
   for (int ct0 = 0; ct0 < nct; ct0 += 4) {
-    v4i a[4];
+    v4i a[4], z[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) a[q] = cop[min(ct0 + q, nct - 1) * 64 + lane];
+    for (int q = 0; q < 4; ++q) {
+      a[q] = cop[min(ct0 + q, nct - 1) * 64 + lane];
+      z[q] = tie_init(min(ct0 + q, nct - 1), ce, lane);
+    }
 #pragma unroll
     for (int q0 = 0; q0 < 4; q0 += 2) {  // two tiles' products in flight at a time
       if constexpr (EXACT_TAIL) {
@@ -152,7 +153,7 @@ __device__ __forceinline__ void best_keys(const v4i* cop, int nct, const v4i* bq
         if (rem == 1) {
           v4i d1[NG];
 #pragma unroll
-          for (int e = 0; e < NG; ++e) d1[e] = mfma_i8_16x16x64(a[q0], bq[e], zero);
+          for (int e = 0; e < NG; ++e) d1[e] = mfma_i8_16x16x64(a[q0], bq[e], z[q0]);
 #pragma unroll
           for (int e = 0; e < NG; ++e) best[e] = max(best[e], max(max(d1[e][0], d1[e][1]), max(d1[e][2], d1[e][3])));
           break;
@@ -162,7 +163,7 @@ __device__ __forceinline__ void best_keys(const v4i* cop, int nct, const v4i* bq
 #pragma unroll
       for (int q = 0; q < 2; ++q)
 #pragma unroll
-        for (int e = 0; e < NG; ++e) d[q][e] = mfma_i8_16x16x64(a[q0 + q], bq[e], zero);
+        for (int e = 0; e < NG; ++e) d[q][e] = mfma_i8_16x16x64(a[q0 + q], bq[e], z[q0 + q]);
 #pragma unroll
       for (int q = 0; q < 2; ++q)
 #pragma unroll
@@ -176,13 +177,13 @@ __device__ __forceinline__ void best_keys(const v4i* cop, int nct, const v4i* bq
   }
 }
 template <bool EXACT_TAIL>
-__device__ __forceinline__ void best_keys_n(int ng, const v4i* cop, int nct, const v4i* bq,
+__device__ __forceinline__ void best_keys_n(int ng, const v4i* cop, int nct, int ce, const v4i* bq,
                                             int* best, int lane) {
   switch (ng) {
-    case 1: best_keys<1, EXACT_TAIL>(cop, nct, bq, best, lane); break;
-    case 2: best_keys<2, EXACT_TAIL>(cop, nct, bq, best, lane); break;
-    case 3: best_keys<3, EXACT_TAIL>(cop, nct, bq, best, lane); break;
-    default: best_keys<4, EXACT_TAIL>(cop, nct, bq, best, lane); break;
+    case 1: best_keys<1, EXACT_TAIL>(cop, nct, ce, bq, best, lane); break;
+    case 2: best_keys<2, EXACT_TAIL>(cop, nct, ce, bq, best, lane); break;
+    case 3: best_keys<3, EXACT_TAIL>(cop, nct, ce, bq, best, lane); break;
+    default: best_keys<4, EXACT_TAIL>(cop, nct, ce, bq, best, lane); break;
   }
 }
 
@@ -193,7 +194,7 @@ __device__ __forceinline__ void build_centroid_operands(v4i* cop, const uint64_t
     const int ct = e >> 6, ln = e & 63;
     const int j = ct * 16 + (ln & 15), g = ln >> 4;
     const OpMasks m = op_masks(g, n_bits);
-    cop[e] = j < ce ? centroid_operand(cent[j], g, m, j) : centroid_operand(cent[0], g, m, 255);
+    cop[e] = centroid_operand(cent[j < ce ? j : 0], g, m);
   }
 }
 
@@ -206,12 +207,12 @@ static_assert(kKmLdsMaxN == kMaxQt * 16 * kKmWaves, "tile budget");
 
 // One assign step over the n queries of a workgroup of kKmWaves waves (codes,
 // assignments and counts in LDS): each query goes to the nearest centroid of
-// the operand table cop (nct tiles), and a query whose cluster changed moves
+// the operand table cop (nct tiles, ce centroids), and a query whose cluster changed moves
 // its bit-pair counts and its size from the old row to the new one (a first
 // assignment, old = -1, only adds).  Adds the number of moved queries to
 // *nchange.  bq0 / code0 are the operands and codes of each wave's first four
 // query tiles, built once.  Ends without a workgroup barrier.
-__device__ __forceinline__ void assign_round(int n, int nqt, int nct, int n_bits,
+__device__ __forceinline__ void assign_round(int n, int nqt, int nct, int ce, int n_bits,
                                              const v4i* cop, const uint64_t* codes,
                                              int32_t* assign, uint32_t* cnt, int32_t* size,
                                              int* nchange, const uint2* qlut, const OpMasks& qm,
@@ -236,7 +237,7 @@ __device__ __forceinline__ void assign_round(int n, int nqt, int nct, int n_bits
       }
       best[e] = INT_MIN;
     }
-    best_keys_n<false>(left < 4 ? left : 4, cop, nct, bq, best, lane);
+    best_keys_n<false>(left < 4 ? left : 4, cop, nct, ce, bq, best, lane);
     // lane l now decides query (l % 16) of tile l / 16 of the group; the
     // queries whose cluster changed move their bit counts
     const int eq = lane >> 4;
@@ -409,7 +410,7 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
 
   // ---- codes -----------------------------------------------------------------
   if (f.codes_in != nullptr) {
-    const uint64_t mask = (1ull << n_bits) - 1;  // n_bits <= 63
+    const uint64_t mask = n_bits >= 64 ? ~0ull : (1ull << n_bits) - 1;
     for (int i = tid; i < n; i += kKmThreads) {
       const uint64_t x = f.codes_in[row0 + i] & mask;
       sh.codes[i] = x;
@@ -473,7 +474,7 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
     // round's update, after every thread has read it in the previous round
     // assign (up to four query tiles share every centroid-operand load); the
     // queries whose cluster changed move their bit counts right away
-    assign_round(n, nqt, nct, n_bits, sh.cop, sh.codes, sh.assign, sh.cnt, sh.size,
+    assign_round(n, nqt, nct, ce, n_bits, sh.cop, sh.codes, sh.assign, sh.cnt, sh.size,
                  &sh.nchange[t & 1], sh.qlut, qm, bq0, code0, lane, wave);
     __syncthreads();
     // no query moved: every later round would repeat this assignment
@@ -482,7 +483,7 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
     if (tid == 0) sh.nchange[(t + 1) & 1] = 0;
     // majority update fused with the operand rebuild: thread (tile, lane)
     // forms the 16 bits of k-group g of centroid j (slots past C_eff copy
-    // centroid 0 with tie byte 255); an empty cluster keeps its operands
+    // centroid 0; they never win); an empty cluster keeps its operands
     for (int e = tid; e < nct * 64; e += kKmThreads) {
       const int j = (e >> 6) * 16 + c;  // e & 63 == lane because the stride is a multiple of 64
       const int src = j < ce ? j : 0;
@@ -496,7 +497,7 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
         bits16 |= static_cast<uint32_t>(2 * static_cast<int>(dw & 0xffffu) > sz) << (2 * w);
         bits16 |= static_cast<uint32_t>(2 * static_cast<int>(dw >> 16) > sz) << (2 * w + 1);
       }
-      sh.cop[e] = centroid_operand16(bits16, g, qm, j < ce ? j : 255);
+      sh.cop[e] = centroid_operand16(bits16, qm);
     }
     __syncthreads();
   }
@@ -766,7 +767,7 @@ __global__ __launch_bounds__(kKmThreads) void kmeans_coop_kernel(CoopArgs a) {
       code0[e] = qb < nq ? sh.codes[qb] : 0ull;
       bq0[e] = query_operand_lut(code0[e], g, qm, sh.qlut);
     }
-    assign_round(nq, nqt, nct, n_bits, sh.cop, sh.codes, sh.assign, sh.cnt, sh.size, &sh.nchange,
+    assign_round(nq, nqt, nct, ce, n_bits, sh.cop, sh.codes, sh.assign, sh.cnt, sh.size, &sh.nchange,
                  sh.qlut, qm, bq0, code0, lane, wave);
     __syncthreads();
     // add the change of this workgroup's counts since its last addition to
@@ -960,7 +961,7 @@ __global__ __launch_bounds__(kKbThreads) void kmeans_assign_kernel(
       bq[e] = query_operand(qi < nq ? lcodes[qi] : 0ull, g, qm);
       best[e] = INT_MIN;
     }
-    best_keys_n<true>(left < 4 ? left : 4, cop, nct, bq, best, lane);
+    best_keys_n<true>(left < 4 ? left : 4, cop, nct, ce, bq, best, lane);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int qo = (wave + (s0 + e) * kKbWaves) * 16 + lane;

@@ -38,7 +38,7 @@ def test_workspace_bytes():
     assert 0 < big < 2 ** 30
     for bad in [(0, 1, 100, 32, 0, 10, 63, 0), (1, 1, 100, 48, 0, 10, 63, 0),
                 (1, 1, 100, 32, 2, 10, 63, 0), (1, 1, 100, 32, 0, 257, 63, 0),
-                (1, 1, 100, 32, 0, 10, 64, 0), (1, 1, 100, 32, 0, 10, 63, 129),
+                (1, 1, 100, 32, 0, 10, 65, 0), (1, 1, 100, 32, 0, 10, 63, 129),
                 (1, 1, 2 ** 20 + 1, 32, 0, 10, 63, 0)]:
         assert ca.workspace_bytes(*bad) == 0, bad
 
@@ -50,7 +50,7 @@ def test_workspace_bytes():
     (dict(C=0), ca.CA_ERR_INVALID_ARG),
     (dict(C=300), ca.CA_ERR_UNSUPPORTED),
     (dict(n_bits=0), ca.CA_ERR_INVALID_ARG),
-    (dict(n_bits=64), ca.CA_ERR_UNSUPPORTED),
+    (dict(n_bits=65), ca.CA_ERR_UNSUPPORTED),
     (dict(L=0), ca.CA_ERR_INVALID_ARG),
     (dict(topk=0), ca.CA_ERR_INVALID_ARG),
     (dict(topk=200), ca.CA_ERR_UNSUPPORTED),

@@ -225,6 +225,29 @@ def test_many_clusters_every_driver(N, dtype, topk, variant):
 
 
 @pytest.mark.parametrize("variant", ["clustered", "iclustered"])
+def test_full_width_codes_every_driver(variant):
+    """64-bit hash codes (every bit of the word a plane) on every K-means
+    driver: codes, assignments, sizes and outputs against the oracle."""
+    import paper_2007_04825_amd as ca
+    w = gen.config_tiny(B=2, H=2, N=3000, d=64, C=100, n_bits=64, L=5, topk=32)
+    w.lengths = np.array([3000, 1999], np.int32)
+    t = w.topk if variant == "iclustered" else 0
+    ref = run_oracle(w, t, key="fullwidth64")
+    assert np.any(ref["codes"] >> np.uint64(63))      # bit 63 is in use
+    try:
+        for path in (1, 2, 3):
+            ca.set_kmeans_path(path)
+            print("driver %d" % path, flush=True)
+            got = run_gpu(w, t)
+            assert np.array_equal(got["codes"], ref["codes"])
+            assert np.array_equal(got["assign"], ref["assign"]), "driver %d" % path
+            assert np.array_equal(got["sizes"], ref["sizes"])
+            compare_outputs(w, ref, got, t)
+    finally:
+        ca.set_kmeans_path(0)
+
+
+@pytest.mark.parametrize("variant", ["clustered", "iclustered"])
 def test_block_kmeans_ragged_and_empty(variant):
     """The several-block K-means drivers with empty, one-row, one-block and
     block-edge sequences in one batch (every block of an empty sequence must
