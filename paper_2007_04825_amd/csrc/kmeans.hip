@@ -139,12 +139,9 @@ __device__ __forceinline__ uint32_t pair_val(uint64_t code, int w) {
 template <int NG, bool EXACT_TAIL>
 __device__ __forceinline__ void best_keys(const v4i* cop, int nct, int ce, const v4i* bq, int* best, int lane) {
   for (int ct0 = 0; ct0 < nct; ct0 += 4) {
-    v4i a[4], z[4];
+    v4i a[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      a[q] = cop[min(ct0 + q, nct - 1) * 64 + lane];
-      z[q] = tie_init(min(ct0 + q, nct - 1), ce, lane);
-    }
+    for (int q = 0; q < 4; ++q) a[q] = cop[min(ct0 + q, nct - 1) * 64 + lane];
 #pragma unroll
     for (int q0 = 0; q0 < 4; q0 += 2) {  // two tiles' products in flight at a time
       if constexpr (EXACT_TAIL) {
@@ -152,8 +149,9 @@ __device__ __forceinline__ void best_keys(const v4i* cop, int nct, int ce, const
         if (rem <= 0) break;
         if (rem == 1) {
           v4i d1[NG];
+          const v4i z = tie_init(min(ct0 + q0, nct - 1), ce, lane);
 #pragma unroll
-          for (int e = 0; e < NG; ++e) d1[e] = mfma_i8_16x16x64(a[q0], bq[e], z[q0]);
+          for (int e = 0; e < NG; ++e) d1[e] = mfma_i8_16x16x64(a[q0], bq[e], z);
 #pragma unroll
           for (int e = 0; e < NG; ++e) best[e] = max(best[e], max(max(d1[e][0], d1[e][1]), max(d1[e][2], d1[e][3])));
           break;
@@ -161,9 +159,12 @@ __device__ __forceinline__ void best_keys(const v4i* cop, int nct, int ce, const
       }
       v4i d[2][NG];
 #pragma unroll
-      for (int q = 0; q < 2; ++q)
+      for (int q = 0; q < 2; ++q) {
+        // accumulator start of this centroid tile, made just before its products
+        const v4i z = tie_init(min(ct0 + q0 + q, nct - 1), ce, lane);
 #pragma unroll
-        for (int e = 0; e < NG; ++e) d[q][e] = mfma_i8_16x16x64(a[q0 + q], bq[e], z[q0 + q]);
+        for (int e = 0; e < NG; ++e) d[q][e] = mfma_i8_16x16x64(a[q0 + q], bq[e], z);
+      }
 #pragma unroll
       for (int q = 0; q < 2; ++q)
 #pragma unroll
@@ -210,8 +211,9 @@ static_assert(kKmLdsMaxN == kMaxQt * 16 * kKmWaves, "tile budget");
 // the operand table cop (nct tiles, ce centroids), and a query whose cluster changed moves
 // its bit-pair counts and its size from the old row to the new one (a first
 // assignment, old = -1, only adds).  Adds the number of moved queries to
-// *nchange.  bq0 / code0 are the operands and codes of each wave's first four
-// query tiles, built once.  Ends without a workgroup barrier.
+// *nchange.  bq0 / code0, when not null, are the operands and codes of each
+// wave's first four query tiles, built once by the caller (otherwise every
+// tile's operands come from the LDS codes).  Ends without a workgroup barrier.
 __device__ __forceinline__ void assign_round(int n, int nqt, int nct, int ce, int n_bits,
                                              const v4i* cop, const uint64_t* codes,
                                              int32_t* assign, uint32_t* cnt, int32_t* size,
@@ -227,7 +229,7 @@ __device__ __forceinline__ void assign_round(int n, int nqt, int nct, int ce, in
     uint64_t mycode[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      if (s0 == 0) {
+      if (s0 == 0 && bq0 != nullptr) {
         mycode[e] = code0[e];
         bq[e] = bq0[e];
       } else {
@@ -757,18 +759,11 @@ __global__ __launch_bounds__(kKmThreads) void kmeans_coop_kernel(CoopArgs a) {
   unsigned long long moved_before = 0;  // high half of the arrival word after the previous round
   const size_t U = gridDim.y;
   for (int t = 0; t < a.L; ++t) {
-    // the first four query tiles' operands, rebuilt each round (registers are
-    // scarcer here than in the one-workgroup kernel)
-    v4i bq0[4];
-    uint64_t code0[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int qb = (wave + e * kKmWaves) * 16 + c;
-      code0[e] = qb < nq ? sh.codes[qb] : 0ull;
-      bq0[e] = query_operand_lut(code0[e], g, qm, sh.qlut);
-    }
+    // every query tile's operands come from the LDS codes (cached operands
+    // would stay live across the assign step and, with two tile groups per
+    // wave, push it into spilled registers)
     assign_round(nq, nqt, nct, ce, n_bits, sh.cop, sh.codes, sh.assign, sh.cnt, sh.size, &sh.nchange,
-                 sh.qlut, qm, bq0, code0, lane, wave);
+                 sh.qlut, qm, nullptr, nullptr, lane, wave);
     __syncthreads();
     // add the change of this workgroup's counts since its last addition to
     // table t % 2; keep the sizes for the member lists
