@@ -3,15 +3,17 @@
 //
 // Assign step on the int8 matrix cores.  A code h is expanded to a 64-entry
 // int8 vector: bit b (b < n_bits) becomes +64 / -64 for a query and +16 / -16
-// for a centroid, positions n_bits..63 are 0.  One v_mfma_i32_16x16x64_i8,
-// its accumulator starting at kTie - j for centroid j, then yields for 16
-// centroids x 16 queries
+// for a centroid, positions n_bits..63 are 0.  One v_mfma_i32_16x16x64_i8
+// over the 16 centroids j = 16 t + r of tile t, its accumulator starting at
+// kTie - r, gives per query 1024 * (n_bits - 2 * ham) + kTie - r, and taking
+// 16 t off the tile's maximum gives
 //     key = 1024 * (n_bits - 2 * ham(h, c_j)) + kTie - j      (kTie = 1023),
 // so the largest key is the nearest centroid with ties resolved to the
 // smallest index, exactly (the tie term spans 1024 values, the distance term
-// steps by 2048); the argmin costs one integer max per distance, and all 64
-// code bits are usable.  Centroid slots past C_eff in the last 16-wide tile
-// start from a large negative accumulator, so they never win.
+// steps by 2048); all 64 code bits are usable, the accumulator start is the
+// same for every tile, and the argmin costs one integer max per distance plus
+// one subtraction per tile and query.  Centroid slots past C_eff in the last
+// tile hold centroid 0 again: same distance, larger index, so they never win.
 //
 // Update step.  Member bit counts live in LDS as 16-bit pairs (dword w holds
 // the counts of bits 2w and 2w+1); a lane adds its query's 32 pairs with LDS
@@ -65,8 +67,7 @@ __device__ __forceinline__ OpMasks op_masks(int g, int n_bits) {
   return m;
 }
 
-constexpr int kTie = 1023;               // tie term of cluster 0; cluster j adds kTie - j
-constexpr int kTieNone = -(1 << 30);     // accumulator start of slots past C_eff
+constexpr int kTie = 1023;  // tie term of cluster 0; cluster j has kTie - j
 
 // Bits 16g..16g+15 of a query code as 16 int8: +64 / -64, 0 past n_bits.
 __device__ __forceinline__ v4i query_operand(uint64_t code, int g, const OpMasks& m) {
@@ -94,16 +95,17 @@ __device__ __forceinline__ v4i centroid_operand16(uint32_t x, const OpMasks& m) 
 __device__ __forceinline__ v4i centroid_operand(uint64_t code, int g, const OpMasks& m) {
   return centroid_operand16(static_cast<uint32_t>(code >> (16 * g)) & 0xffffu, m);
 }
-// Accumulator start of centroid tile ct for this lane's four result rows
-// (centroids 16 ct + 4 (lane / 16) + r): the tie term, or kTieNone past C_eff.
-__device__ __forceinline__ v4i tie_init(int ct, int ce, int lane) {
+// Accumulator start for this lane's four result rows, centroids
+// 4 (lane / 16) + i of every tile: the in-tile part of the tie term.
+__device__ __forceinline__ v4i tie_start(int lane) {
   v4i r;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int j = ct * 16 + 4 * (lane >> 4) + i;
-    r[i] = j < ce ? kTie - j : kTieNone;
-  }
+  for (int i = 0; i < 4; ++i) r[i] = kTie - (4 * (lane >> 4) + i);
   return r;
+}
+// The tile's part of the key taken off the lane's four results, and their maximum.
+__device__ __forceinline__ int tile_key(const v4i& d, int ct) {
+  return max(max(d[0], d[1]), max(d[2], d[3])) - 16 * ct;
 }
 
 // Same as query_operand, from a table mapping 8 code bits to 8 int8 entries.
@@ -137,7 +139,8 @@ __device__ __forceinline__ uint32_t pair_val(uint64_t code, int w) {
 // with a repeat, which saves its products but (measured) slows the
 // one-workgroup-per-unit kernel, whose schedule favours the branch-free form.
 template <int NG, bool EXACT_TAIL>
-__device__ __forceinline__ void best_keys(const v4i* cop, int nct, int ce, const v4i* bq, int* best, int lane) {
+__device__ __forceinline__ void best_keys(const v4i* cop, int nct, const v4i* bq, int* best, int lane) {
+  const v4i z = tie_start(lane);
   for (int ct0 = 0; ct0 < nct; ct0 += 4) {
     v4i a[4];
 #pragma unroll
@@ -149,27 +152,22 @@ __device__ __forceinline__ void best_keys(const v4i* cop, int nct, int ce, const
         if (rem <= 0) break;
         if (rem == 1) {
           v4i d1[NG];
-          const v4i z = tie_init(min(ct0 + q0, nct - 1), ce, lane);
 #pragma unroll
           for (int e = 0; e < NG; ++e) d1[e] = mfma_i8_16x16x64(a[q0], bq[e], z);
 #pragma unroll
-          for (int e = 0; e < NG; ++e) best[e] = max(best[e], max(max(d1[e][0], d1[e][1]), max(d1[e][2], d1[e][3])));
+          for (int e = 0; e < NG; ++e) best[e] = max(best[e], tile_key(d1[e], ct0 + q0));
           break;
         }
       }
       v4i d[2][NG];
 #pragma unroll
-      for (int q = 0; q < 2; ++q) {
-        // accumulator start of this centroid tile, made just before its products
-        const v4i z = tie_init(min(ct0 + q0 + q, nct - 1), ce, lane);
-#pragma unroll
-        for (int e = 0; e < NG; ++e) d[q][e] = mfma_i8_16x16x64(a[q0 + q], bq[e], z);
-      }
-#pragma unroll
       for (int q = 0; q < 2; ++q)
 #pragma unroll
-        for (int e = 0; e < NG; ++e)
-          best[e] = max(best[e], max(max(d[q][e][0], d[q][e][1]), max(d[q][e][2], d[q][e][3])));
+        for (int e = 0; e < NG; ++e) d[q][e] = mfma_i8_16x16x64(a[q0 + q], bq[e], z);
+#pragma unroll
+      for (int e = 0; e < NG; ++e)
+        best[e] = max(best[e], max(tile_key(d[0][e], min(ct0 + q0, nct - 1)),
+                                   tile_key(d[1][e], min(ct0 + q0 + 1, nct - 1))));
     }
   }
 #pragma unroll
@@ -178,17 +176,18 @@ __device__ __forceinline__ void best_keys(const v4i* cop, int nct, int ce, const
   }
 }
 template <bool EXACT_TAIL>
-__device__ __forceinline__ void best_keys_n(int ng, const v4i* cop, int nct, int ce, const v4i* bq,
+__device__ __forceinline__ void best_keys_n(int ng, const v4i* cop, int nct, const v4i* bq,
                                             int* best, int lane) {
   switch (ng) {
-    case 1: best_keys<1, EXACT_TAIL>(cop, nct, ce, bq, best, lane); break;
-    case 2: best_keys<2, EXACT_TAIL>(cop, nct, ce, bq, best, lane); break;
-    case 3: best_keys<3, EXACT_TAIL>(cop, nct, ce, bq, best, lane); break;
-    default: best_keys<4, EXACT_TAIL>(cop, nct, ce, bq, best, lane); break;
+    case 1: best_keys<1, EXACT_TAIL>(cop, nct, bq, best, lane); break;
+    case 2: best_keys<2, EXACT_TAIL>(cop, nct, bq, best, lane); break;
+    case 3: best_keys<3, EXACT_TAIL>(cop, nct, bq, best, lane); break;
+    default: best_keys<4, EXACT_TAIL>(cop, nct, bq, best, lane); break;
   }
 }
 
-// Fills the centroid operands of nct tiles (entries e = ct * 64 + lane).
+// Fills the centroid operands of nct tiles (entries e = ct * 64 + lane); the
+// slots past ce hold centroid 0, whose own slot always beats them.
 __device__ __forceinline__ void build_centroid_operands(v4i* cop, const uint64_t* cent, int ce,
                                                         int nct, int n_bits, int tid, int nthreads) {
   for (int e = tid; e < nct * 64; e += nthreads) {
@@ -239,7 +238,7 @@ __device__ __forceinline__ void assign_round(int n, int nqt, int nct, int ce, in
       }
       best[e] = INT_MIN;
     }
-    best_keys_n<false>(left < 4 ? left : 4, cop, nct, ce, bq, best, lane);
+    best_keys_n<false>(left < 4 ? left : 4, cop, nct, bq, best, lane);
     // lane l now decides query (l % 16) of tile l / 16 of the group; the
     // queries whose cluster changed move their bit counts
     const int eq = lane >> 4;
@@ -653,7 +652,7 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
 // ===========================================================================
 constexpr int kSpinLimit = 1 << 22;   // polls of the arrival counter before giving up
 static_assert(kCoopMaxQ <= kKmLdsMaxN, "the shared assign step handles kKmLdsMaxN queries");
-constexpr int kTabBatch = 4;          // table words requested together per thread
+constexpr int kTabBatch = 8;          // table words requested together per thread
 constexpr int kRowWords = 33;         // table words per cluster: 32 bit pairs and the size
 static_assert(kSyncInts >= 2, "one 64-bit arrival word");
 
@@ -749,15 +748,13 @@ __global__ __launch_bounds__(kKmThreads) void kmeans_coop_kernel(CoopArgs a) {
     sh.qlut[v] = make_uint2(lo, hi);
   }
   if (tid == 0) sh.nchange = 0;
-  const int g = lane >> 4, c = lane & 15;
-  const OpMasks qm = op_masks(g, n_bits);
+  const OpMasks qm = op_masks(lane >> 4, n_bits);
   __syncthreads();
   build_centroid_operands(sh.cop, sh.cent, ce, nct, n_bits, tid, kKmThreads);
   __syncthreads();
   unsigned long long* arrive =
       reinterpret_cast<unsigned long long*>(a.sync + static_cast<size_t>(u) * kSyncInts);
   unsigned long long moved_before = 0;  // high half of the arrival word after the previous round
-  const size_t U = gridDim.y;
   for (int t = 0; t < a.L; ++t) {
     // every query tile's operands come from the LDS codes (cached operands
     // would stay live across the assign step and, with two tile groups per
@@ -956,7 +953,7 @@ __global__ __launch_bounds__(kKbThreads) void kmeans_assign_kernel(
       bq[e] = query_operand(qi < nq ? lcodes[qi] : 0ull, g, qm);
       best[e] = INT_MIN;
     }
-    best_keys_n<true>(left < 4 ? left : 4, cop, nct, ce, bq, best, lane);
+    best_keys_n<true>(left < 4 ? left : 4, cop, nct, bq, best, lane);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int qo = (wave + (s0 + e) * kKbWaves) * 16 + lane;
