@@ -230,7 +230,7 @@ static int run_forward(const void* q, const void* k, const void* v, const int32_
       CA_TRY(mark(CA_KERNEL_HASH, false, s));
     }
     if (driver == 3) {
-      // all rounds and the member lists in one cooperative launch
+      // all rounds and the member lists in one launch
       ws.coop_q = coop_block_queries(p, ws.ncoop);
       CA_TRY(mark(CA_KERNEL_KMEANS, true, s));
       CA_TRY(launch_kmeans_coop(p, ws, s));

@@ -5,15 +5,16 @@
 // int8 vector: bit b (b < n_bits) becomes +64 / -64 for a query and +16 / -16
 // for a centroid, positions n_bits..63 are 0.  One v_mfma_i32_16x16x64_i8
 // over the 16 centroids j = 16 t + r of tile t, its accumulator starting at
-// kTie - r, gives per query 1024 * (n_bits - 2 * ham) + kTie - r, and taking
-// 16 t off the tile's maximum gives
-//     key = 1024 * (n_bits - 2 * ham(h, c_j)) + kTie - j      (kTie = 1023),
-// so the largest key is the nearest centroid with ties resolved to the
+// kTie - r, gives per query 1024 * (n_bits - 2 * ham) + kTie - r.  The tile's
+// part -16 t comes from position 63 when n_bits <= 63 (query +16, centroid
+// -t), and is otherwise taken off each tile's maximum, so that
+//     key = 1024 * (n_bits - 2 * ham(h, c_j)) + kTie - j      (kTie = 1023)
+// and the largest key is the nearest centroid with ties resolved to the
 // smallest index, exactly (the tie term spans 1024 values, the distance term
-// steps by 2048); all 64 code bits are usable, the accumulator start is the
-// same for every tile, and the argmin costs one integer max per distance plus
-// one subtraction per tile and query.  Centroid slots past C_eff in the last
-// tile hold centroid 0 again: same distance, larger index, so they never win.
+// steps by 2048).  All 64 code bits are usable, the accumulator start is the
+// same for every tile, and the argmin costs one integer max per distance.
+// Centroid slots past C_eff in the last tile hold centroid 0 again: same
+// distance, larger index, so they never win.
 //
 // Update step.  Member bit counts live in LDS as 16-bit pairs (dword w holds
 // the counts of bits 2w and 2w+1); a lane adds its query's 32 pairs with LDS
@@ -50,12 +51,18 @@ __device__ __forceinline__ uint32_t spread4(uint32_t nib) {
   return (nib & 1u) | ((nib & 2u) << 7) | ((nib & 4u) << 14) | ((nib & 8u) << 21);
 }
 
-// keep[q]: byte p is 0xff when bit 16g + 4q + p is a hash bit (< n_bits).
+// keep[q]: byte p is 0xff when bit 16g + 4q + p is a hash bit (< n_bits);
+// qslot: the query's +16 at position 63 (byte 3 of the lane group g = 3's
+// last word) when that position carries the tile term (n_bits <= 63).
 struct OpMasks {
   uint32_t keep[4];
+  uint32_t qslot;
 };
+// Whether position 63 carries the tile part of the tie term.
+__device__ __forceinline__ bool tile_slot(int n_bits) { return n_bits <= 63; }
 __device__ __forceinline__ OpMasks op_masks(int g, int n_bits) {
   OpMasks m;
+  m.qslot = (g == 3 && tile_slot(n_bits)) ? 0x10000000u : 0u;
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     uint32_t k = 0;
@@ -69,7 +76,8 @@ __device__ __forceinline__ OpMasks op_masks(int g, int n_bits) {
 
 constexpr int kTie = 1023;  // tie term of cluster 0; cluster j has kTie - j
 
-// Bits 16g..16g+15 of a query code as 16 int8: +64 / -64, 0 past n_bits.
+// Bits 16g..16g+15 of a query code as 16 int8: +64 / -64, 0 past n_bits
+// (+16 at position 63 when it carries the tile term).
 __device__ __forceinline__ v4i query_operand(uint64_t code, int g, const OpMasks& m) {
   const uint32_t x = static_cast<uint32_t>(code >> (16 * g)) & 0xffffu;
   v4i r;
@@ -78,22 +86,25 @@ __device__ __forceinline__ v4i query_operand(uint64_t code, int g, const OpMasks
     const uint32_t s = spread4((x >> (4 * q)) & 0xfu);
     r[q] = static_cast<int>((0xc0c0c0c0u ^ (s << 7)) & m.keep[q]);
   }
+  r[3] |= static_cast<int>(m.qslot);
   return r;
 }
 
-// 16 code bits x (bits 16g..16g+15 of a centroid) as 16 int8: +16 / -16, 0
-// past n_bits.
-__device__ __forceinline__ v4i centroid_operand16(uint32_t x, const OpMasks& m) {
+// 16 code bits x (bits 16g..16g+15 of a centroid of tile ct) as 16 int8:
+// +16 / -16, 0 past n_bits, and -ct at position 63 when it carries the tile
+// term.
+__device__ __forceinline__ v4i centroid_operand16(uint32_t x, int ct, const OpMasks& m) {
   v4i r;
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const uint32_t s = spread4((x >> (4 * q)) & 0xfu);
     r[q] = static_cast<int>((0xf0f0f0f0u ^ (s * 0xe0u)) & m.keep[q]);
   }
+  if (m.qslot != 0u) r[3] |= static_cast<int>(static_cast<uint32_t>(-ct & 0xff) << 24);
   return r;
 }
-__device__ __forceinline__ v4i centroid_operand(uint64_t code, int g, const OpMasks& m) {
-  return centroid_operand16(static_cast<uint32_t>(code >> (16 * g)) & 0xffffu, m);
+__device__ __forceinline__ v4i centroid_operand(uint64_t code, int g, int ct, const OpMasks& m) {
+  return centroid_operand16(static_cast<uint32_t>(code >> (16 * g)) & 0xffffu, ct, m);
 }
 // Accumulator start for this lane's four result rows, centroids
 // 4 (lane / 16) + i of every tile: the in-tile part of the tie term.
@@ -103,9 +114,12 @@ __device__ __forceinline__ v4i tie_start(int lane) {
   for (int i = 0; i < 4; ++i) r[i] = kTie - (4 * (lane >> 4) + i);
   return r;
 }
-// The tile's part of the key taken off the lane's four results, and their maximum.
+// The largest of the lane's four keys of tile ct; SHIFT: the tile's part of
+// the tie term is not in the products yet (n_bits = 64).
+template <bool SHIFT>
 __device__ __forceinline__ int tile_key(const v4i& d, int ct) {
-  return max(max(d[0], d[1]), max(d[2], d[3])) - 16 * ct;
+  const int m = max(max(d[0], d[1]), max(d[2], d[3]));
+  return SHIFT ? m - 16 * ct : m;
 }
 
 // Same as query_operand, from a table mapping 8 code bits to 8 int8 entries.
@@ -117,7 +131,7 @@ __device__ __forceinline__ v4i query_operand_lut(uint64_t code, int g, const OpM
   r[0] = static_cast<int>(lo.x & m.keep[0]);
   r[1] = static_cast<int>(lo.y & m.keep[1]);
   r[2] = static_cast<int>(hi.x & m.keep[2]);
-  r[3] = static_cast<int>(hi.y & m.keep[3]);
+  r[3] = static_cast<int>((hi.y & m.keep[3]) | m.qslot);
   return r;
 }
 
@@ -138,7 +152,7 @@ __device__ __forceinline__ uint32_t pair_val(uint64_t code, int w) {
 // repeats); EXACT_TAIL takes an odd last tile alone instead of pairing it
 // with a repeat, which saves its products but (measured) slows the
 // one-workgroup-per-unit kernel, whose schedule favours the branch-free form.
-template <int NG, bool EXACT_TAIL>
+template <int NG, bool EXACT_TAIL, bool SHIFT>
 __device__ __forceinline__ void best_keys(const v4i* cop, int nct, const v4i* bq, int* best, int lane) {
   const v4i z = tie_start(lane);
   for (int ct0 = 0; ct0 < nct; ct0 += 4) {
@@ -155,7 +169,7 @@ __device__ __forceinline__ void best_keys(const v4i* cop, int nct, const v4i* bq
 #pragma unroll
           for (int e = 0; e < NG; ++e) d1[e] = mfma_i8_16x16x64(a[q0], bq[e], z);
 #pragma unroll
-          for (int e = 0; e < NG; ++e) best[e] = max(best[e], tile_key(d1[e], ct0 + q0));
+          for (int e = 0; e < NG; ++e) best[e] = max(best[e], tile_key<SHIFT>(d1[e], ct0 + q0));
           break;
         }
       }
@@ -166,8 +180,8 @@ __device__ __forceinline__ void best_keys(const v4i* cop, int nct, const v4i* bq
         for (int e = 0; e < NG; ++e) d[q][e] = mfma_i8_16x16x64(a[q0 + q], bq[e], z);
 #pragma unroll
       for (int e = 0; e < NG; ++e)
-        best[e] = max(best[e], max(tile_key(d[0][e], min(ct0 + q0, nct - 1)),
-                                   tile_key(d[1][e], min(ct0 + q0 + 1, nct - 1))));
+        best[e] = max(best[e], max(tile_key<SHIFT>(d[0][e], min(ct0 + q0, nct - 1)),
+                                   tile_key<SHIFT>(d[1][e], min(ct0 + q0 + 1, nct - 1))));
     }
   }
 #pragma unroll
@@ -175,15 +189,23 @@ __device__ __forceinline__ void best_keys(const v4i* cop, int nct, const v4i* bq
     best[e] = cross_rows_max(best[e]);
   }
 }
-template <bool EXACT_TAIL>
-__device__ __forceinline__ void best_keys_n(int ng, const v4i* cop, int nct, const v4i* bq,
-                                            int* best, int lane) {
+template <bool EXACT_TAIL, bool SHIFT>
+__device__ __forceinline__ void best_keys_ng(int ng, const v4i* cop, int nct, const v4i* bq,
+                                             int* best, int lane) {
   switch (ng) {
-    case 1: best_keys<1, EXACT_TAIL>(cop, nct, bq, best, lane); break;
-    case 2: best_keys<2, EXACT_TAIL>(cop, nct, bq, best, lane); break;
-    case 3: best_keys<3, EXACT_TAIL>(cop, nct, bq, best, lane); break;
-    default: best_keys<4, EXACT_TAIL>(cop, nct, bq, best, lane); break;
+    case 1: best_keys<1, EXACT_TAIL, SHIFT>(cop, nct, bq, best, lane); break;
+    case 2: best_keys<2, EXACT_TAIL, SHIFT>(cop, nct, bq, best, lane); break;
+    case 3: best_keys<3, EXACT_TAIL, SHIFT>(cop, nct, bq, best, lane); break;
+    default: best_keys<4, EXACT_TAIL, SHIFT>(cop, nct, bq, best, lane); break;
   }
+}
+template <bool EXACT_TAIL>
+__device__ __forceinline__ void best_keys_n(int ng, const v4i* cop, int nct, int n_bits,
+                                            const v4i* bq, int* best, int lane) {
+  if (tile_slot(n_bits))
+    best_keys_ng<EXACT_TAIL, false>(ng, cop, nct, bq, best, lane);
+  else
+    best_keys_ng<EXACT_TAIL, true>(ng, cop, nct, bq, best, lane);
 }
 
 // Fills the centroid operands of nct tiles (entries e = ct * 64 + lane); the
@@ -194,7 +216,7 @@ __device__ __forceinline__ void build_centroid_operands(v4i* cop, const uint64_t
     const int ct = e >> 6, ln = e & 63;
     const int j = ct * 16 + (ln & 15), g = ln >> 4;
     const OpMasks m = op_masks(g, n_bits);
-    cop[e] = centroid_operand(cent[j < ce ? j : 0], g, m);
+    cop[e] = centroid_operand(cent[j < ce ? j : 0], g, ct, m);
   }
 }
 
@@ -212,7 +234,9 @@ static_assert(kKmLdsMaxN == kMaxQt * 16 * kKmWaves, "tile budget");
 // assignment, old = -1, only adds).  Adds the number of moved queries to
 // *nchange.  bq0 / code0, when not null, are the operands and codes of each
 // wave's first four query tiles, built once by the caller (otherwise every
-// tile's operands come from the LDS codes).  Ends without a workgroup barrier.
+// tile's operands come from the LDS codes).  EXACT_TAIL as in best_keys.
+// Ends without a workgroup barrier.
+template <bool EXACT_TAIL>
 __device__ __forceinline__ void assign_round(int n, int nqt, int nct, int ce, int n_bits,
                                              const v4i* cop, const uint64_t* codes,
                                              int32_t* assign, uint32_t* cnt, int32_t* size,
@@ -238,7 +262,7 @@ __device__ __forceinline__ void assign_round(int n, int nqt, int nct, int ce, in
       }
       best[e] = INT_MIN;
     }
-    best_keys_n<false>(left < 4 ? left : 4, cop, nct, bq, best, lane);
+    best_keys_n<EXACT_TAIL>(left < 4 ? left : 4, cop, nct, n_bits, bq, best, lane);
     // lane l now decides query (l % 16) of tile l / 16 of the group; the
     // queries whose cluster changed move their bit counts
     const int eq = lane >> 4;
@@ -475,7 +499,7 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
     // round's update, after every thread has read it in the previous round
     // assign (up to four query tiles share every centroid-operand load); the
     // queries whose cluster changed move their bit counts right away
-    assign_round(n, nqt, nct, ce, n_bits, sh.cop, sh.codes, sh.assign, sh.cnt, sh.size,
+    assign_round<false>(n, nqt, nct, ce, n_bits, sh.cop, sh.codes, sh.assign, sh.cnt, sh.size,
                  &sh.nchange[t & 1], sh.qlut, qm, bq0, code0, lane, wave);
     __syncthreads();
     // no query moved: every later round would repeat this assignment
@@ -498,7 +522,7 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
         bits16 |= static_cast<uint32_t>(2 * static_cast<int>(dw & 0xffffu) > sz) << (2 * w);
         bits16 |= static_cast<uint32_t>(2 * static_cast<int>(dw >> 16) > sz) << (2 * w + 1);
       }
-      sh.cop[e] = centroid_operand16(bits16, qm);
+      sh.cop[e] = centroid_operand16(bits16, e >> 6, qm);
     }
     __syncthreads();
   }
@@ -642,9 +666,14 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
 // workgroup barrier that precedes the arrival, and the waiting side reads
 // with device-scope loads issued after it has seen every arrival; so the
 // arrival itself needs no cache write-back or invalidation (which cost each
-// round several microseconds when measured).  The launch is cooperative, so
-// all workgroups are resident
-// together and every wait ends; each wait is also bounded.  A round in which
+// round several microseconds when measured).  All workgroups are resident
+// together, so every wait ends: the grid never exceeds what the device holds
+// at once (the occupancy query times the compute units), the kernel before it
+// in the stream has finished when it starts, and a waiting workgroup blocks
+// no other kernel, so a workgroup held back by another stream's work is
+// placed once that work drains.  (A cooperative launch gives the same
+// guarantee, but measured about 15 us slower per call: it goes through a
+// queue of its own.)  Each wait is also bounded.  A round in which
 // no query of the unit moved ends the loop: every later round would repeat
 // it.  The final member lists come from the per-workgroup sizes of the last
 // round: cluster j's members of workgroup b follow those of workgroups
@@ -759,7 +788,7 @@ __global__ __launch_bounds__(kKmThreads) void kmeans_coop_kernel(CoopArgs a) {
     // every query tile's operands come from the LDS codes (cached operands
     // would stay live across the assign step and, with two tile groups per
     // wave, push it into spilled registers)
-    assign_round(nq, nqt, nct, ce, n_bits, sh.cop, sh.codes, sh.assign, sh.cnt, sh.size, &sh.nchange,
+    assign_round<true>(nq, nqt, nct, ce, n_bits, sh.cop, sh.codes, sh.assign, sh.cnt, sh.size, &sh.nchange,
                  sh.qlut, qm, nullptr, nullptr, lane, wave);
     __syncthreads();
     // add the change of this workgroup's counts since its last addition to
@@ -953,7 +982,7 @@ __global__ __launch_bounds__(kKbThreads) void kmeans_assign_kernel(
       bq[e] = query_operand(qi < nq ? lcodes[qi] : 0ull, g, qm);
       best[e] = INT_MIN;
     }
-    best_keys_n<true>(left < 4 ? left : 4, cop, nct, bq, best, lane);
+    best_keys_n<true>(left < 4 ? left : 4, cop, nct, n_bits, bq, best, lane);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int qo = (wave + (s0 + e) * kKbWaves) * 16 + lane;
@@ -1273,11 +1302,11 @@ hipError_t launch_kmeans_coop(const Problem& p, const Workspace& ws, hipStream_t
   const dim3 grid(a.nwg, p.units());
   switch (ws.coop_q) {
     case 1024:
-      return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(kmeans_coop_kernel<1024>), grid,
-                                        dim3(kKmThreads), args, 0, s);
+      return hipLaunchKernel(reinterpret_cast<const void*>(kmeans_coop_kernel<1024>), grid,
+                             dim3(kKmThreads), args, 0, s);
     case 2048:
-      return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(kmeans_coop_kernel<2048>), grid,
-                                        dim3(kKmThreads), args, 0, s);
+      return hipLaunchKernel(reinterpret_cast<const void*>(kmeans_coop_kernel<2048>), grid,
+                             dim3(kKmThreads), args, 0, s);
     default:
       return hipErrorInvalidValue;
   }
