@@ -711,6 +711,18 @@ struct CoopArgs {
   int32_t* sync;           // [U][kSyncInts] arrival word (64-bit), zero at launch
 };
 
+// The 64-bit word whose even bits are e and odd bits are o.
+__device__ __forceinline__ uint64_t interleave_bits(uint32_t e, uint32_t o) {
+  auto spread = [](uint64_t v) {  // bit i to bit 2i
+    v = (v | (v << 16)) & 0x0000ffff0000ffffull;
+    v = (v | (v << 8)) & 0x00ff00ff00ff00ffull;
+    v = (v | (v << 4)) & 0x0f0f0f0f0f0f0f0full;
+    v = (v | (v << 2)) & 0x3333333333333333ull;
+    return (v | (v << 1)) & 0x5555555555555555ull;
+  };
+  return spread(e) | (spread(o) << 1);
+}
+
 template <int QW>
 struct CoopShared {
   uint64_t codes[QW];
@@ -719,7 +731,6 @@ struct CoopShared {
   uint32_t pub[2][kCmax * kRowWords];  // local counts last added to each table
   int32_t size[kCmax];
   uint64_t cent[kCmax];
-  uint32_t ncent[2 * kCmax];  // next centroid codes, low and high words
   v4i cop[kCmax / 16 * 64];
   uint2 qlut[256];
   int32_t tsize[kCmax];
@@ -768,7 +779,6 @@ __global__ __launch_bounds__(kKmThreads) void kmeans_coop_kernel(CoopArgs a) {
   }
   for (int x = tid; x < kCmax * kCntStride; x += kKmThreads) sh.cnt[x] = 0;
   for (int j = tid; j < kCmax; j += kKmThreads) sh.size[j] = 0;
-  for (int x = tid; x < 2 * kCmax; x += kKmThreads) sh.ncent[x] = 0u;
   for (int x = tid; x < 2 * kCmax * kRowWords; x += kKmThreads) (&sh.pub[0][0])[x] = 0u;
   for (int j = tid; j < ce; j += kKmThreads) sh.cent[j] = cu[(static_cast<int64_t>(j) * n) / ce];
   for (int v = tid; v < 256; v += kKmThreads) {
@@ -833,40 +843,45 @@ __global__ __launch_bounds__(kKmThreads) void kmeans_coop_kernel(CoopArgs a) {
     }
     __syncthreads();
     if (t + 1 == a.L || !sh.moved || !sh.ok) break;  // no query moved: later rounds repeat this one
-    // per-bit majority (tie -> 0) of the unit's non-empty clusters: the
-    // (cluster, pair word) items' words and the cluster sizes are requested
-    // together (kTabBatch words per thread in flight); each item sets its two
-    // bits once the sizes are in LDS
+    // per-bit majority (tie -> 0) of the unit's non-empty clusters: item x
+    // is pair word x % 32 of cluster x / 32 (kTabBatch words per thread in
+    // flight, and lane 2e + h < 2 kTabBatch of a wave fetches the size of the
+    // cluster of its half h in batch e); the 64 items of a wave are two whole
+    // clusters, so two ballots give each cluster's even and odd bits, which
+    // one lane per cluster interleaves into the new code
+    static_assert(2 * kTabBatch <= 64, "one size per lane");
     {
       const int items = ce * 32;
+      // the item index made opaque in every round, so that the loads'
+      // addresses are formed here rather than kept in registers across rounds
+      int tidr = tid;
+      asm volatile("" : "+v"(tidr));
       for (int x0 = 0; x0 < items; x0 += kTabBatch * kKmThreads) {
         uint64_t wv[kTabBatch];
 #pragma unroll
         for (int e = 0; e < kTabBatch; ++e) {
-          const int x = x0 + tid + e * kKmThreads;
+          const int x = x0 + tidr + e * kKmThreads;
           wv[e] = x < items ? ld_agent(&tab[(x >> 5) * kRowWords + (x & 31)]) : 0ull;
         }
-        if (x0 == 0)
-          for (int j = tid; j < ce; j += kKmThreads) sh.tsize[j] = static_cast<int>(ld_agent(&tab[j * kRowWords + 32]));
-        __syncthreads();
+        // a size is a true count (at most n), so the low half of its word is it
+        int32_t szl = 0;
+        if (lane < 2 * kTabBatch) {
+          const int xs = x0 + wave * 64 + (lane & 1) * 32 + (lane >> 1) * kKmThreads;
+          if (xs < items) szl = ld_agent(reinterpret_cast<const int32_t*>(&tab[(xs >> 5) * kRowWords + 32]));
+        }
 #pragma unroll
         for (int e = 0; e < kTabBatch; ++e) {
           const int x = x0 + tid + e * kKmThreads;
-          if (x < items) {
-            const int j = x >> 5, w = x & 31;
-            const long long tz = sh.tsize[j];
-            const uint32_t bits = static_cast<uint32_t>(2 * static_cast<long long>(wv[e] & 0xffffffffull) > tz) |
-                                  (static_cast<uint32_t>(2 * static_cast<long long>(wv[e] >> 32) > tz) << 1);
-            if (bits) atomicOr(&sh.ncent[2 * j + (w >> 4)], bits << (2 * (w & 15)));
+          const bool in = x < items;
+          const int tz = lane < 32 ? __builtin_amdgcn_readlane(szl, 2 * e) : __builtin_amdgcn_readlane(szl, 2 * e + 1);
+          const uint64_t even = __ballot(in && 2 * static_cast<long long>(wv[e] & 0xffffffffull) > tz);
+          const uint64_t odd = __ballot(in && 2 * static_cast<long long>(wv[e] >> 32) > tz);
+          if (in && (lane & 31) == 0 && tz > 0) {
+            const int sh32 = lane & 32;  // this cluster's half of the ballots
+            sh.cent[x >> 5] = interleave_bits(static_cast<uint32_t>(even >> sh32), static_cast<uint32_t>(odd >> sh32));
           }
         }
       }
-    }
-    __syncthreads();
-    for (int j = tid; j < ce; j += kKmThreads) {
-      if (sh.tsize[j] > 0)
-        sh.cent[j] = static_cast<uint64_t>(sh.ncent[2 * j]) | (static_cast<uint64_t>(sh.ncent[2 * j + 1]) << 32);
-      sh.ncent[2 * j] = sh.ncent[2 * j + 1] = 0u;
     }
     __syncthreads();
     build_centroid_operands(sh.cop, sh.cent, ce, nct, n_bits, tid, kKmThreads);
