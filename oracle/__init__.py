@@ -51,6 +51,8 @@ def _load():
     i64, i32 = ctypes.c_int64, ctypes.c_int
     lib.orc_full_attention.argtypes = [dp, dp, dp, i64, i32, dp]
     lib.orc_hash.argtypes = [dp, i64, i32, dp, i32, u64p]
+    lib.orc_philox4x64_10.argtypes = [u64p, u64p, u64p]
+    lib.orc_planes.argtypes = [ctypes.c_uint64, i32, i32, i32, dp]
     lib.orc_projections.argtypes = [dp, i64, i32, dp, i32, dp]
     lib.orc_kmeans.argtypes = [u64p, i64, i32, i32, i32p, u64p, i64p]
     lib.orc_centroids.argtypes = [dp, i64, i32, i32p, i32, dp, i64p]
@@ -95,6 +97,24 @@ def full_attention(q, k, v):
     out = np.zeros((n, d), np.float64)
     _load().orc_full_attention(_ptr(q, ctypes.c_double), _ptr(k, ctypes.c_double),
                                _ptr(v, ctypes.c_double), n, d, _ptr(out, ctypes.c_double))
+    return out
+
+
+def philox4x64_10(counter, key):
+    """The generator's four output words for a 4-word counter and a 2-word key."""
+    ctr = np.ascontiguousarray(np.asarray(counter, dtype=np.uint64).reshape(4))
+    k = np.ascontiguousarray(np.asarray(key, dtype=np.uint64).reshape(2))
+    out = np.zeros(4, np.uint64)
+    _load().orc_philox4x64_10(_ptr(ctr, ctypes.c_uint64), _ptr(k, ctypes.c_uint64),
+                              _ptr(out, ctypes.c_uint64))
+    return out
+
+
+def planes_from_seed(seed, heads, n_bits, d):
+    """Hash planes [heads, n_bits, d] drawn from a seed (fp32 values held in fp64)."""
+    out = np.zeros((heads, n_bits, d), np.float64)
+    _load().orc_planes(int(seed) & 0xffffffffffffffff, heads, n_bits, d,
+                       _ptr(out, ctypes.c_double))
     return out
 
 

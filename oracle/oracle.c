@@ -44,7 +44,9 @@
  * differences); none is marked unpinned.  The projections are pinned to
  * exact rational dot products within the fp64 summation bound and to the
  * hash codes; exact attention to numpy's softmax attention, closed forms and
- * its permutation symmetries.  The whole file also runs clean under
+ * its permutation symmetries; the seeded planes' generator to numpy's own
+ * Philox4x64-10 word for word, and their deviates to the Box-Muller polar
+ * identities and the normal distribution.  The whole file also runs clean under
  * AddressSanitizer and UndefinedBehaviorSanitizer (sanitize_check.c).
  */
 #include <math.h>
@@ -84,6 +86,64 @@ void orc_full_attention(const double* q, const double* k, const double* v,
     }
   }
   free(s);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Section 3.2.2 draws the hyperplanes of the hash at random.  When a caller */
+/* gives none they come from a seed, through the counter-based generator     */
+/* Philox4x64-10 of Salmon, Moraes, Dror and Shaw ("Parallel random numbers: */
+/* as easy as 1, 2, 3", SC 2011): ten rounds; a round takes the 128-bit      */
+/* products of words 0 and 2 with two fixed multipliers and mixes their      */
+/* halves with words 1 and 3 and the key, and the key is advanced by two     */
+/* Weyl increments before the next round.                                    */
+/* ------------------------------------------------------------------------ */
+void orc_philox4x64_10(const uint64_t ctr[4], const uint64_t key[2], uint64_t out[4]) {
+  const uint64_t mult0 = 0xD2E7470EE14C6C93ull, mult1 = 0xCA5A826395121157ull;
+  const uint64_t weyl0 = 0x9E3779B97F4A7C15ull, weyl1 = 0xBB67AE8584CAA73Bull;
+  uint64_t x0 = ctr[0], x1 = ctr[1], x2 = ctr[2], x3 = ctr[3];
+  uint64_t k0 = key[0], k1 = key[1];
+  for (int round = 0; round < 10; ++round) {
+    const unsigned __int128 p0 = (unsigned __int128)mult0 * x0;
+    const unsigned __int128 p1 = (unsigned __int128)mult1 * x2;
+    const uint64_t hi0 = (uint64_t)(p0 >> 64), lo0 = (uint64_t)p0;
+    const uint64_t hi1 = (uint64_t)(p1 >> 64), lo1 = (uint64_t)p1;
+    x0 = hi1 ^ x1 ^ k0;
+    x1 = lo1;
+    x2 = hi0 ^ x3 ^ k1;
+    x3 = lo0;
+    k0 += weyl0;
+    k1 += weyl1;
+  }
+  out[0] = x0;
+  out[1] = x1;
+  out[2] = x2;
+  out[3] = x3;
+}
+
+/* Standard normal planes[h][b][t] (flat index i over [heads][n_bits][d])   */
+/* from a seed: the generator's block for counter (i / 4, 0, 0, 0) and key   */
+/* (seed, 0) holds two pairs of words; pair p = (i % 4) / 2 gives           */
+/* u1 = ((w_2p >> 11) + 1) 2^-53 in (0, 1] and u2 = (w_2p+1 >> 11) 2^-53 in */
+/* [0, 1), and the Box-Muller transform (Box and Muller 1958) gives the two */
+/* deviates r cos(phi) (even i) and r sin(phi) (odd i) with                  */
+/* r = sqrt(-2 ln u1), phi = 2 pi u2, evaluated in fp64.  Planes are kept as */
+/* fp32 values, so each deviate is rounded to fp32.                          */
+void orc_planes(uint64_t seed, int heads, int n_bits, int d, double* planes) {
+  const int64_t count = (int64_t)heads * n_bits * d;
+  const double two_pi = 6.283185307179586476925286766559;
+  for (int64_t i = 0; i < count; ++i) {
+    const uint64_t ctr[4] = {(uint64_t)(i / 4), 0, 0, 0};
+    const uint64_t key[2] = {seed, 0};
+    uint64_t w[4];
+    orc_philox4x64_10(ctr, key, w);
+    const int p = (int)((i % 4) / 2);
+    const double u1 = (double)((w[2 * p] >> 11) + 1) * 0x1.0p-53;
+    const double u2 = (double)(w[2 * p + 1] >> 11) * 0x1.0p-53;
+    const double r = sqrt(-2.0 * log(u1));
+    const double phi = two_pi * u2;
+    const double z = (i % 2 == 0) ? r * cos(phi) : r * sin(phi);
+    planes[i] = (double)(float)z;
+  }
 }
 
 /* ------------------------------------------------------------------------ */

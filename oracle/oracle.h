@@ -5,6 +5,8 @@
 
 void orc_full_attention(const double* q, const double* k, const double* v,
                         int64_t n, int d, double* out);
+void orc_philox4x64_10(const uint64_t ctr[4], const uint64_t key[2], uint64_t out[4]);
+void orc_planes(uint64_t seed, int heads, int n_bits, int d, double* planes);
 void orc_hash(const double* q, int64_t n, int d, const double* planes,
               int n_bits, uint64_t* codes);
 void orc_projections(const double* q, int64_t n, int d, const double* planes,

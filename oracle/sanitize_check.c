@@ -7,7 +7,8 @@
  * sequences (lengths 0, 1, a ragged one and the full length), C larger than
  * a sequence, k larger than a sequence, a caller-supplied top-k set that is
  * shorter than k (-1 terminated), n_bits = 64, and both backward variants
- * fed with the forward pass's own partition and top-k sets.  The values are
+ * fed with the forward pass's own partition and top-k sets, and the seeded
+ * plane generator.  The values are
  * irrelevant here: the sanitizers check the memory accesses and the integer
  * arithmetic.  Exit status 0 and the line "sanitize ok" mean that no check
  * fired (the build aborts on the first report).
@@ -135,9 +136,22 @@ static int run_unit(int64_t n, int d, int C, int n_bits, int L, int topk) {
   return 0;
 }
 
+/* The seeded planes, including a count that is not a multiple of a block. */
+static int run_planes(void) {
+  double* p = (double*)malloc(sizeof(double) * 3 * 7 * 5);
+  orc_planes(0xffffffffffffffffull, 3, 7, 5, p);
+  const uint64_t ctr[4] = {~0ull, ~0ull, ~0ull, ~0ull}, key[2] = {~0ull, 1};
+  uint64_t w[4];
+  orc_philox4x64_10(ctr, key, w);
+  int ok = 1;
+  for (int i = 0; i < 3 * 7 * 5; ++i) ok &= isfinite(p[i]) ? 1 : 0;
+  free(p);
+  return ok ? 0 : 1;
+}
+
 int main(void) {
   const int32_t lengths[4] = {37, 0, 1, 64};
-  int rc = 0;
+  int rc = run_planes();
   rc |= run_case(4, 2, 64, 8, 9, 63, 4, 5, lengths, 2);    /* ragged, C and k above some lengths */
   rc |= run_case(4, 1, 64, 4, 80, 64, 2, 100, lengths, 1); /* C > N, k > N, n_bits = 64 */
   rc |= run_case(1, 3, 17, 16, 1, 1, 1, 1, NULL, 3);       /* C = 1, B = 1, L = 1, k = 1 */
