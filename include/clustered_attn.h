@@ -14,10 +14,19 @@
  *   clamped to [0, n] on the device.  Keys past the length get no attention,
  *   queries past it are not hashed or clustered, and their output rows are
  *   written as 0.
- * - planes is a DEVICE pointer to fp32[heads][n_bits][d]: the random
- *   hyperplanes of the sign-random-projection hash (Section 3.2.2), drawn by
- *   the caller (the library draws no random numbers).  Any fp32 values work;
- *   the projections are evaluated in fp64, where each product is exact.
+ * - planes is NULL or a DEVICE pointer to fp32[heads][n_bits][d]: the random
+ *   hyperplanes of the sign-random-projection hash (Section 3.2.2).  Any fp32
+ *   values work; the projections are evaluated in fp64, where each product
+ *   is exact.  When planes is NULL the library draws them from `seed` into
+ *   the workspace: entry i of the flat [heads][n_bits][d] order is a
+ *   standard normal deviate from block i / 4 of the counter-based generator
+ *   Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC 2011; counter
+ *   (i / 4, 0, 0, 0), key (seed, 0)), whose words (2p, 2p + 1),
+ *   p = (i mod 4) / 2, give u1 = ((w >> 11) + 1) 2^-53 and u2 = (w >> 11)
+ *   2^-53 and, by the Box-Muller transform in fp64, the deviates
+ *   sqrt(-2 ln u1) cos(2 pi u2) (even i) and sqrt(-2 ln u1) sin(2 pi u2)
+ *   (odd i), rounded to fp32.  The same seed gives the same planes for
+ *   every call and sequence length; `seed` is ignored when planes is given.
  * - C = n_clusters, B = n_bits, L = lloyd_iters, k = topk are the method's
  *   hyper-parameters (Sections 3.2.2 and 3.3).  Per unit the library uses
  *   C_eff = min(C, length) clusters and k_eff = min(k, length) keys.
@@ -90,6 +99,8 @@ extern "C" {
  *                             for the improved variant the part of A^c V
  *                             over the keys outside T_j (supplementary
  *                             decomposition of the improved values).
+ *   planes_out  float[heads][n_bits][d] the hash planes used: the caller's,
+ *                             or those drawn from the seed.
  */
 typedef struct ca_aux {
   const uint64_t* codes_in;
@@ -102,12 +113,14 @@ typedef struct ca_aux {
   int32_t* topk_out;
   float* mass_out;
   float* values_out;
+  float* planes_out;
 } ca_aux;
 
 /*
  * Bytes of workspace that clustered_attention_fwd (topk = 0) or
- * iclustered_attention_fwd (topk >= 1) needs for these sizes.  Returns 0 if
- * the sizes are invalid or unsupported.
+ * iclustered_attention_fwd (topk >= 1) needs for these sizes (n_bits sizes
+ * the room for planes drawn from a seed).  Returns 0 if the sizes are
+ * invalid or unsupported.
  */
 size_t ca_workspace_bytes(int batch, int heads, int n, int d, int dtype,
                           int n_clusters, int n_bits, int topk);
@@ -129,8 +142,9 @@ int clustered_attention_fwd(const void* q, const void* k, const void* v,
                             const int32_t* lengths, const float* planes,
                             int batch, int heads, int n, int d, int dtype,
                             int n_clusters, int n_bits, int lloyd_iters,
-                            void* out, void* workspace, size_t workspace_bytes,
-                            const ca_aux* aux, void* stream);
+                            uint64_t seed, void* out, void* workspace,
+                            size_t workspace_bytes, const ca_aux* aux,
+                            void* stream);
 
 /*
  * Improved clustered attention (Section 3.3, Eq. 11), steps 1-4 as above and
@@ -146,9 +160,9 @@ int iclustered_attention_fwd(const void* q, const void* k, const void* v,
                              const int32_t* lengths, const float* planes,
                              int batch, int heads, int n, int d, int dtype,
                              int n_clusters, int n_bits, int lloyd_iters,
-                             int topk, void* out, void* workspace,
-                             size_t workspace_bytes, const ca_aux* aux,
-                             void* stream);
+                             uint64_t seed, int topk, void* out,
+                             void* workspace, size_t workspace_bytes,
+                             const ca_aux* aux, void* stream);
 
 /*
  * Backward pass.  The paper trains through the operator (Section 4) without
@@ -261,8 +275,8 @@ int iclustered_attention_fwd_noalloc(const void* q, const void* k, const void* v
                                      const int32_t* lengths, const float* planes,
                                      int batch, int heads, int n, int d, int dtype,
                                      int n_clusters, int n_bits, int lloyd_iters,
-                                     int topk, void* out, const ca_aux* aux,
-                                     void* stream);
+                                     uint64_t seed, int topk, void* out,
+                                     const ca_aux* aux, void* stream);
 
 /* Message describing the last non-zero status returned on this thread. */
 const char* ca_last_error(void);

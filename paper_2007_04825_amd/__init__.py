@@ -60,7 +60,7 @@ class Aux(ctypes.Structure):
     """Mirror of ``ca_aux`` (all device pointers, 0 = unused)."""
     _fields_ = [(name, ctypes.c_void_p) for name in (
         "codes_in", "assign_in", "topk_in", "codes_out", "assign_out", "sizes_out",
-        "centroids_out", "topk_out", "mass_out", "values_out")]
+        "centroids_out", "topk_out", "mass_out", "values_out", "planes_out")]
 
 
 def library():
@@ -79,15 +79,15 @@ def library():
     except ImportError:
         pass
     lib = ctypes.CDLL(lib_path)
-    vp, i32, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
+    vp, i32, sz, u64 = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t, ctypes.c_uint64
     lib.ca_workspace_bytes.argtypes = [i32] * 8
     lib.ca_workspace_bytes.restype = sz
     common = [vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, i32]
-    lib.clustered_attention_fwd.argtypes = common + [vp, vp, sz, ctypes.POINTER(Aux), vp]
+    lib.clustered_attention_fwd.argtypes = common + [u64, vp, vp, sz, ctypes.POINTER(Aux), vp]
     lib.clustered_attention_fwd.restype = i32
-    lib.iclustered_attention_fwd.argtypes = common + [i32, vp, vp, sz, ctypes.POINTER(Aux), vp]
+    lib.iclustered_attention_fwd.argtypes = common + [u64, i32, vp, vp, sz, ctypes.POINTER(Aux), vp]
     lib.iclustered_attention_fwd.restype = i32
-    lib.iclustered_attention_fwd_noalloc.argtypes = common + [i32, vp, ctypes.POINTER(Aux), vp]
+    lib.iclustered_attention_fwd_noalloc.argtypes = common + [u64, i32, vp, ctypes.POINTER(Aux), vp]
     lib.iclustered_attention_fwd_noalloc.restype = i32
     lib.ca_last_error.argtypes = []
     lib.ca_last_error.restype = ctypes.c_char_p
@@ -168,34 +168,41 @@ def set_kmeans_path(path: int):
     _check(library().ca_set_kmeans_path(int(path)))
 
 
+def _seed(seed) -> int:
+    return int(seed) & 0xFFFFFFFFFFFFFFFF
+
+
 def clustered_attention_fwd(q, k, v, lengths, planes, batch, heads, n, d, dtype, n_clusters,
-                            n_bits, lloyd_iters, out, workspace, workspace_nbytes, aux=None,
+                            n_bits, lloyd_iters, seed, out, workspace, workspace_nbytes, aux=None,
                             stream=None):
-    """Raw call with integer device addresses; returns the status code."""
+    """Raw call with integer device addresses (planes None: drawn from seed);
+    returns the status code."""
     return library().clustered_attention_fwd(
         q, k, v, lengths, planes, batch, heads, n, d, dtype, n_clusters, n_bits, lloyd_iters,
-        out, workspace, workspace_nbytes, ctypes.byref(aux) if aux is not None else None, stream)
+        _seed(seed), out, workspace, workspace_nbytes,
+        ctypes.byref(aux) if aux is not None else None, stream)
 
 
 def iclustered_attention_fwd(q, k, v, lengths, planes, batch, heads, n, d, dtype, n_clusters,
-                             n_bits, lloyd_iters, topk, out, workspace, workspace_nbytes,
+                             n_bits, lloyd_iters, seed, topk, out, workspace, workspace_nbytes,
                              aux=None, stream=None):
-    """Raw call with integer device addresses; returns the status code."""
+    """Raw call with integer device addresses (planes None: drawn from seed);
+    returns the status code."""
     return library().iclustered_attention_fwd(
         q, k, v, lengths, planes, batch, heads, n, d, dtype, n_clusters, n_bits, lloyd_iters,
-        topk, out, workspace, workspace_nbytes, ctypes.byref(aux) if aux is not None else None,
-        stream)
+        _seed(seed), topk, out, workspace, workspace_nbytes,
+        ctypes.byref(aux) if aux is not None else None, stream)
 
 
 def iclustered_attention_fwd_noalloc(q, k, v, lengths, planes, batch, heads, n, d, dtype,
-                                     n_clusters, n_bits, lloyd_iters, topk, out, aux=None,
+                                     n_clusters, n_bits, lloyd_iters, seed, topk, out, aux=None,
                                      stream=None):
     """Raw call of the allocation-free entry point (the library's own device
     scratch instead of a workspace) with integer device addresses; returns the
     status code."""
     return library().iclustered_attention_fwd_noalloc(
         q, k, v, lengths, planes, batch, heads, n, d, dtype, n_clusters, n_bits, lloyd_iters,
-        topk, out, ctypes.byref(aux) if aux is not None else None, stream)
+        _seed(seed), topk, out, ctypes.byref(aux) if aux is not None else None, stream)
 
 
 # ---------------------------------------------------------------------------
@@ -257,37 +264,41 @@ def _workspace(nbytes, device, workspace):
     return torch.empty(max(nbytes, 1), dtype=torch.uint8, device=device)
 
 
-def clustered_attention(q, k, v, planes, n_clusters=100, n_bits=63, lloyd_iters=10,
-                        lengths=None, out=None, workspace=None, aux: Optional[Aux] = None):
-    """Clustered attention forward (Section 3.2) on torch device tensors."""
+def clustered_attention(q, k, v, planes=None, n_clusters=100, n_bits=63, lloyd_iters=10,
+                        lengths=None, out=None, workspace=None, aux: Optional[Aux] = None,
+                        seed=0):
+    """Clustered attention forward (Section 3.2) on torch device tensors;
+    planes None: the library draws them from seed."""
     torch = _torch()
     B, H, N, D = _prepare(q, k, v, planes, lengths)
     dt = _dtype_code(q)
     need = workspace_bytes(B, H, N, D, dt, n_clusters, n_bits, 0)
     if need == 0:
         _check(library().clustered_attention_fwd(None, None, None, None, None, B, H, N, D, dt,
-                                                 n_clusters, n_bits, lloyd_iters, None, None, 0,
-                                                 None, None))
+                                                 n_clusters, n_bits, lloyd_iters, 0, None, None,
+                                                 0, None, None))
     ws = _workspace(need, q.device, workspace)
     if out is None:
         out = torch.empty_like(q)
     stream = torch.cuda.current_stream(q.device).cuda_stream
     _check(clustered_attention_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), _ptr(lengths),
                                    _ptr(planes), B, H, N, D, dt, n_clusters, n_bits, lloyd_iters,
-                                   out.data_ptr(), ws.data_ptr(), need, aux, stream))
+                                   seed, out.data_ptr(), ws.data_ptr(), need, aux, stream))
     return out
 
 
-def iclustered_attention(q, k, v, planes, n_clusters=100, n_bits=63, lloyd_iters=10, topk=32,
-                         lengths=None, out=None, workspace=None, aux: Optional[Aux] = None):
-    """Improved clustered attention forward (Section 3.3) on torch device tensors."""
+def iclustered_attention(q, k, v, planes=None, n_clusters=100, n_bits=63, lloyd_iters=10, topk=32,
+                         lengths=None, out=None, workspace=None, aux: Optional[Aux] = None,
+                         seed=0):
+    """Improved clustered attention forward (Section 3.3) on torch device
+    tensors; planes None: the library draws them from seed."""
     torch = _torch()
     B, H, N, D = _prepare(q, k, v, planes, lengths)
     dt = _dtype_code(q)
     need = workspace_bytes(B, H, N, D, dt, n_clusters, n_bits, topk)
     if need == 0:
         _check(library().iclustered_attention_fwd(None, None, None, None, None, B, H, N, D, dt,
-                                                  n_clusters, n_bits, lloyd_iters, topk, None,
+                                                  n_clusters, n_bits, lloyd_iters, 0, topk, None,
                                                   None, 0, None, None))
     ws = _workspace(need, q.device, workspace)
     if out is None:
@@ -295,7 +306,7 @@ def iclustered_attention(q, k, v, planes, n_clusters=100, n_bits=63, lloyd_iters
     stream = torch.cuda.current_stream(q.device).cuda_stream
     _check(iclustered_attention_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), _ptr(lengths),
                                     _ptr(planes), B, H, N, D, dt, n_clusters, n_bits, lloyd_iters,
-                                    topk, out.data_ptr(), ws.data_ptr(), need, aux, stream))
+                                    seed, topk, out.data_ptr(), ws.data_ptr(), need, aux, stream))
     return out
 
 

@@ -80,6 +80,7 @@ size_t carve_workspace(const Problem& p, void* base, Workspace* ws) {
   w.cbases = static_cast<int32_t*>(take(U * NC * C * 4));
   w.clsizes = static_cast<int32_t*>(take(U * NC * C * 4));
   w.qc_part = static_cast<double*>(take(U * C * NC * D * 8));
+  w.planes = static_cast<float*>(take(static_cast<size_t>(p.heads) * p.n_bits * D * 4));
   if (ws) *ws = w;
   return off;
 }
@@ -161,7 +162,7 @@ static int check_sizes(int batch, int heads, int n, int d, int dtype, int C, int
 
 static int run_forward(const void* q, const void* k, const void* v, const int32_t* lengths,
                        const float* planes, int batch, int heads, int n, int d, int dtype, int C,
-                       int n_bits, int L, int topk, void* out, void* workspace,
+                       int n_bits, int L, uint64_t seed, int topk, void* out, void* workspace,
                        size_t workspace_bytes, const ca_aux* aux, void* stream) {
   const bool improved = topk > 0;
   int rc = check_sizes(batch, heads, n, d, dtype, C, n_bits, L, topk, improved);
@@ -169,8 +170,6 @@ static int run_forward(const void* q, const void* k, const void* v, const int32_
   const bool assign_given = aux && aux->assign_in;
   if (!q || !k || !v || !out)
     return fail(CA_ERR_INVALID_ARG, "q, k, v and out must not be NULL");
-  if (!planes && !assign_given && !(aux && aux->codes_in))
-    return fail(CA_ERR_INVALID_ARG, "planes must not be NULL");
   Problem p;
   p.batch = batch;
   p.heads = heads;
@@ -210,6 +209,10 @@ static int run_forward(const void* q, const void* k, const void* v, const int32_
 
   const uint64_t* codes_in = aux ? aux->codes_in : nullptr;
   const int driver = kmeans_driver(p);
+  if (!planes) {  // drawn from the seed before anything hashes (outside the timed stages)
+    CA_TRY(launch_planes(p, seed, ws.planes, s));
+    p.planes = ws.planes;
+  }
   if (assign_given) {
     CA_TRY(launch_load_assign(p, aux->assign_in, ws, s));
     CA_TRY(mark(CA_KERNEL_CENTROIDS, true, s));
@@ -278,6 +281,7 @@ static int run_forward(const void* q, const void* k, const void* v, const int32_
       CA_TRY(copy(aux->topk_out, ws.topk, U * C * topk * 4));
       CA_TRY(copy(aux->mass_out, ws.mass, U * C * 4));
     }
+    CA_TRY(copy(aux->planes_out, p.planes, static_cast<size_t>(heads) * n_bits * d * 4));
   }
 #undef CA_TRY
   return CA_OK;
@@ -445,12 +449,13 @@ size_t ca_workspace_bytes(int batch, int heads, int n, int d, int dtype, int n_c
 
 int clustered_attention_fwd(const void* q, const void* k, const void* v, const int32_t* lengths,
                             const float* planes, int batch, int heads, int n, int d, int dtype,
-                            int n_clusters, int n_bits, int lloyd_iters, void* out,
+                            int n_clusters, int n_bits, int lloyd_iters, uint64_t seed, void* out,
                             void* workspace, size_t workspace_bytes, const ca_aux* aux,
                             void* stream) {
   try {
     return ca::run_forward(q, k, v, lengths, planes, batch, heads, n, d, dtype, n_clusters,
-                           n_bits, lloyd_iters, 0, out, workspace, workspace_bytes, aux, stream);
+                           n_bits, lloyd_iters, seed, 0, out, workspace, workspace_bytes, aux,
+                           stream);
   } catch (...) {
     return ca::fail(CA_ERR_HIP, "unexpected C++ exception");
   }
@@ -458,13 +463,14 @@ int clustered_attention_fwd(const void* q, const void* k, const void* v, const i
 
 int iclustered_attention_fwd(const void* q, const void* k, const void* v, const int32_t* lengths,
                              const float* planes, int batch, int heads, int n, int d, int dtype,
-                             int n_clusters, int n_bits, int lloyd_iters, int topk, void* out,
-                             void* workspace, size_t workspace_bytes, const ca_aux* aux,
-                             void* stream) {
+                             int n_clusters, int n_bits, int lloyd_iters, uint64_t seed, int topk,
+                             void* out, void* workspace, size_t workspace_bytes,
+                             const ca_aux* aux, void* stream) {
   try {
     if (topk < 1) return ca::fail(CA_ERR_INVALID_ARG, "topk must be >= 1 (got %d)", topk);
     return ca::run_forward(q, k, v, lengths, planes, batch, heads, n, d, dtype, n_clusters,
-                           n_bits, lloyd_iters, topk, out, workspace, workspace_bytes, aux, stream);
+                           n_bits, lloyd_iters, seed, topk, out, workspace, workspace_bytes, aux,
+                           stream);
   } catch (...) {
     return ca::fail(CA_ERR_HIP, "unexpected C++ exception");
   }
@@ -473,15 +479,15 @@ int iclustered_attention_fwd(const void* q, const void* k, const void* v, const 
 int iclustered_attention_fwd_noalloc(const void* q, const void* k, const void* v,
                                      const int32_t* lengths, const float* planes, int batch,
                                      int heads, int n, int d, int dtype, int n_clusters,
-                                     int n_bits, int lloyd_iters, int topk, void* out,
-                                     const ca_aux* aux, void* stream) {
+                                     int n_bits, int lloyd_iters, uint64_t seed, int topk,
+                                     void* out, const ca_aux* aux, void* stream) {
   try {
     if (topk < 1) return ca::fail(CA_ERR_INVALID_ARG, "topk must be >= 1 (got %d)", topk);
     // sizes first, so that a rejected call touches no device state
     const size_t need = ca_workspace_bytes(batch, heads, n, d, dtype, n_clusters, n_bits, topk);
     if (need == 0)
       return ca::run_forward(q, k, v, lengths, planes, batch, heads, n, d, dtype, n_clusters,
-                             n_bits, lloyd_iters, topk, out, nullptr, 0, aux, stream);
+                             n_bits, lloyd_iters, seed, topk, out, nullptr, 0, aux, stream);
     if (need > ca::kScratchBytes)
       return ca::fail(CA_ERR_UNSUPPORTED,
                       "these sizes need %zu bytes of scratch; the allocation-free entry point holds %zu",
@@ -490,7 +496,7 @@ int iclustered_attention_fwd_noalloc(const void* q, const void* k, const void* v
     void* ws = ca::scratch_address(&rc);
     if (ws == nullptr) return rc;
     return ca::run_forward(q, k, v, lengths, planes, batch, heads, n, d, dtype, n_clusters, n_bits,
-                           lloyd_iters, topk, out, ws, ca::kScratchBytes, aux, stream);
+                           lloyd_iters, seed, topk, out, ws, ca::kScratchBytes, aux, stream);
   } catch (...) {
     return ca::fail(CA_ERR_HIP, "unexpected C++ exception");
   }
@@ -570,7 +576,7 @@ int oracle_top_attention_fwd(const void* q, const void* k, const void* v, const 
 
 const char* ca_last_error(void) { return ca::g_last_error.c_str(); }
 
-int ca_version(void) { return 100; }
+int ca_version(void) { return 200; }
 
 int ca_time_next_stage(int stage, void* start_event, void* stop_event) {
   if (stage < 0 || stage > CA_KERNEL_ATTN_TILE || (stage != 0 && (!start_event || !stop_event)))

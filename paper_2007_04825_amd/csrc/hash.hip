@@ -81,6 +81,57 @@ __global__ __launch_bounds__(256) void load_codes_kernel(const uint64_t* __restr
   codes[x] = i < n ? (in[x] & mask) : 0ull;
 }
 
+// Hyperplanes drawn on the device when the caller gives none (Section 3.2.2
+// draws them at random).  Thread t makes entries 4t .. 4t + 3 of the flat
+// planes[heads][n_bits][d] from one block of the counter-based generator
+// Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC 2011), counter (t, 0, 0, 0)
+// and key (seed, 0): its words (0, 1) and (2, 3) are two pairs of uniforms
+// u1 = ((w >> 11) + 1) 2^-53 in (0, 1], u2 = (w >> 11) 2^-53 in [0, 1), and
+// the Box-Muller transform (Box and Muller 1958) turns a pair into the two
+// standard normal deviates sqrt(-2 ln u1) (cos, sin)(2 pi u2), evaluated in
+// fp64 and stored as fp32.
+constexpr uint64_t kPhiloxMul0 = 0xD2E7470EE14C6C93ull;
+constexpr uint64_t kPhiloxMul1 = 0xCA5A826395121157ull;
+constexpr uint64_t kPhiloxInc0 = 0x9E3779B97F4A7C15ull;  // key increments between rounds
+constexpr uint64_t kPhiloxInc1 = 0xBB67AE8584CAA73Bull;
+
+__global__ __launch_bounds__(256) void planes_kernel(uint64_t seed, int count,
+                                                     float* __restrict__ planes) {
+  const int t = blockIdx.x * 256 + threadIdx.x;
+  if (4 * static_cast<long long>(t) >= count) return;
+  uint64_t w0 = static_cast<uint64_t>(t), w1 = 0, w2 = 0, w3 = 0;
+  uint64_t ka = seed, kb = 0;
+#pragma unroll
+  for (int round = 0; round < 10; ++round) {
+    const uint64_t hi0 = __umul64hi(kPhiloxMul0, w0), lo0 = kPhiloxMul0 * w0;
+    const uint64_t hi1 = __umul64hi(kPhiloxMul1, w2), lo1 = kPhiloxMul1 * w2;
+    w0 = hi1 ^ w1 ^ ka;
+    w1 = lo1;
+    w2 = hi0 ^ w3 ^ kb;
+    w3 = lo0;
+    ka += kPhiloxInc0;
+    kb += kPhiloxInc1;
+  }
+  const uint64_t words[4] = {w0, w1, w2, w3};
+#pragma unroll
+  for (int pair = 0; pair < 2; ++pair) {
+    const double u1 = static_cast<double>((words[2 * pair] >> 11) + 1) * 0x1.0p-53;
+    const double u2 = static_cast<double>(words[2 * pair + 1] >> 11) * 0x1.0p-53;
+    const double r = sqrt(-2.0 * log(u1));
+    const double angle = 6.283185307179586476925286766559 * u2;
+    const int i = 4 * t + 2 * pair;
+    if (i < count) planes[i] = static_cast<float>(r * cos(angle));
+    if (i + 1 < count) planes[i + 1] = static_cast<float>(r * sin(angle));
+  }
+}
+
+hipError_t launch_planes(const Problem& p, uint64_t seed, float* planes, hipStream_t s) {
+  const int count = p.heads * p.n_bits * p.d;
+  const int threads = (count + 3) / 4;
+  hipLaunchKernelGGL(planes_kernel, dim3((threads + 255) / 256), dim3(256), 0, s, seed, count, planes);
+  return hipGetLastError();
+}
+
 template <int D, typename T>
 static hipError_t launch_hash_t(const Problem& p, const Workspace& ws, hipStream_t s) {
   dim3 grid((p.n + kHashQB - 1) / kHashQB, p.units());

@@ -71,6 +71,7 @@ struct Workspace {
   int32_t* cbases;      // [U][ncoop][C] first member position of each (block, cluster)
   int32_t* clsizes;     // [U][ncoop][C] members of each (block, cluster)
   double* qc_part;      // [U][C][ncoop][d] per-block centroid sums (used: n / coop_q blocks)
+  float* planes;        // [heads][n_bits][d] hash planes drawn from the seed (caller gave none)
   int nblk;             // ceil(N / kKmBlockQ)
   int ncsr;             // ceil(N / kCsrBlockQ)
   int nchunk;           // ceil(N / kChunk)
@@ -87,6 +88,8 @@ size_t carve_otop_workspace(const Problem& p, void* base, Workspace* ws);
 // Oracle-top outputs and top-k sets (into ws.topk).
 hipError_t launch_oracle_top(const Problem& p, const Workspace& ws, hipStream_t s);
 
+// Hash planes [heads][n_bits][d] drawn from seed (when the caller gives none).
+hipError_t launch_planes(const Problem& p, uint64_t seed, float* planes, hipStream_t s);
 // Hashing; also writes 0 to the output rows past each sequence's length and
 // zeroes ws.sync.
 hipError_t launch_hash(const Problem& p, const Workspace& ws, hipStream_t s);

@@ -21,10 +21,11 @@ def to_dev(x, dtype):
 
 
 def run_gpu(w, topk, codes_in=None, assign_in=None, topk_in=None, lengths=True, C=None, L=None,
-            q=None, shared_qk=False):
+            q=None, shared_qk=False, seed=None):
     """Runs the library on workload w.  topk = 0 -> clustered variant;
-    shared_qk passes the query buffer as the keys too.  Returns a dict of
-    numpy arrays (out as float64)."""
+    shared_qk passes the query buffer as the keys too; seed: no planes are
+    passed, the library draws them from the seed (exported as "planes").
+    Returns a dict of numpy arrays (out as float64)."""
     import paper_2007_04825_amd as ca
     torch = torch_mod()
     C = w.C if C is None else C
@@ -33,11 +34,12 @@ def run_gpu(w, topk, codes_in=None, assign_in=None, topk_in=None, lengths=True, 
     B, H, N, D = qn.shape
     qd, vd = to_dev(qn, w.dtype), to_dev(w.v, w.dtype)
     kd = qd if shared_qk else to_dev(w.k, w.dtype)
-    planes = torch.from_numpy(np.ascontiguousarray(w.planes)).cuda()
+    planes = None if seed is not None else torch.from_numpy(np.ascontiguousarray(w.planes)).cuda()
     lens = torch.from_numpy(w.lengths.astype(np.int32)).cuda() if lengths else None
     U = B * H
     kk = max(topk, 1)
     ex = dict(
+        planes_out=torch.zeros(w.planes.shape, dtype=torch.float32, device="cuda"),
         codes_out=torch.zeros((U, N), dtype=torch.int64, device="cuda"),
         assign_out=torch.zeros((U, N), dtype=torch.int32, device="cuda"),
         sizes_out=torch.zeros((U, C), dtype=torch.int32, device="cuda"),
@@ -54,10 +56,13 @@ def run_gpu(w, topk, codes_in=None, assign_in=None, topk_in=None, lengths=True, 
     if topk_in is not None:
         inj["topk_in"] = torch.from_numpy(np.ascontiguousarray(topk_in, dtype=np.int32)).cuda()
     aux = ca.make_aux(**ex, **inj)
+    sd = 0 if seed is None else seed
     if topk > 0:
-        out = ca.iclustered_attention(qd, kd, vd, planes, C, w.n_bits, L, topk, lengths=lens, aux=aux)
+        out = ca.iclustered_attention(qd, kd, vd, planes, C, w.n_bits, L, topk, lengths=lens, aux=aux,
+                                      seed=sd)
     else:
-        out = ca.clustered_attention(qd, kd, vd, planes, C, w.n_bits, L, lengths=lens, aux=aux)
+        out = ca.clustered_attention(qd, kd, vd, planes, C, w.n_bits, L, lengths=lens, aux=aux,
+                                     seed=sd)
     torch.cuda.synchronize()
     res = {k.replace("_out", ""): v.cpu().numpy() for k, v in ex.items()}
     res["codes"] = res["codes"].view(np.uint64).reshape(B, H, N)

@@ -27,7 +27,7 @@ def test_library_exports_every_declared_symbol():
     lib = ca.library()
     for name in declared_functions():
         assert hasattr(lib, name), name
-    assert lib.ca_version() == 100
+    assert lib.ca_version() == 200
 
 
 def test_workspace_bytes():
@@ -36,6 +36,10 @@ def test_workspace_bytes():
     assert ca.workspace_bytes(1, 1, 100, 32, ca.CA_F32, 10, 63, 8) > small
     big = ca.workspace_bytes(1, 8, 65536, 64, ca.CA_BF16, 200, 63, 64)
     assert 0 < big < 2 ** 30
+    # n_bits sizes the room for planes drawn from a seed, [heads][n_bits][d] fp32
+    grow = (ca.workspace_bytes(1, 8, 1000, 64, ca.CA_F32, 10, 64, 0)
+            - ca.workspace_bytes(1, 8, 1000, 64, ca.CA_F32, 10, 1, 0))
+    assert grow == 8 * 64 * 64 * 4 - 8 * 1 * 64 * 4
     for bad in [(0, 1, 100, 32, 0, 10, 63, 0), (1, 1, 100, 48, 0, 10, 63, 0),
                 (1, 1, 100, 32, 2, 10, 63, 0), (1, 1, 100, 32, 0, 257, 63, 0),
                 (1, 1, 100, 32, 0, 10, 65, 0), (1, 1, 100, 32, 0, 10, 63, 129),
@@ -55,7 +59,8 @@ def test_workspace_bytes():
     (dict(topk=0), ca.CA_ERR_INVALID_ARG),
     (dict(topk=200), ca.CA_ERR_UNSUPPORTED),
     (dict(q=None), ca.CA_ERR_INVALID_ARG),
-    (dict(planes=None), ca.CA_ERR_INVALID_ARG),
+    (dict(out=None), ca.CA_ERR_INVALID_ARG),
+    (dict(planes=None, n_bits=65), ca.CA_ERR_UNSUPPORTED),  # planes drawn from the seed
     (dict(ws=None), ca.CA_ERR_WORKSPACE),
     (dict(ws_bytes=16), ca.CA_ERR_WORKSPACE),
     (dict(ws=0x1001), ca.CA_ERR_WORKSPACE),
@@ -68,13 +73,13 @@ def test_invalid_arguments_rejected_on_host(args, code):
     p.update(args)
     rc = ca.iclustered_attention_fwd(p["q"], p["k"], p["v"], p["lengths"], p["planes"], p["batch"],
                                      p["heads"], p["n"], p["d"], p["dtype"], p["C"], p["n_bits"],
-                                     p["L"], p["topk"], p["out"], p["ws"], p["ws_bytes"])
+                                     p["L"], 7, p["topk"], p["out"], p["ws"], p["ws_bytes"])
     assert rc == code
     assert len(ca.library().ca_last_error()) > 0
     if "topk" not in args:
         rc = ca.clustered_attention_fwd(p["q"], p["k"], p["v"], p["lengths"], p["planes"],
                                         p["batch"], p["heads"], p["n"], p["d"], p["dtype"], p["C"],
-                                        p["n_bits"], p["L"], p["out"], p["ws"], p["ws_bytes"])
+                                        p["n_bits"], p["L"], 7, p["out"], p["ws"], p["ws_bytes"])
         assert rc == code
 
 

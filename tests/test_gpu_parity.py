@@ -247,6 +247,45 @@ def test_full_width_codes_every_driver(variant):
         ca.set_kmeans_path(0)
 
 
+SEEDED = {
+    "tiny": lambda: gen.config_tiny(B=1, H=4, N=1024, d=64, C=100, L=10, topk=32),
+    "bits64-d32-bf16": lambda: gen.with_dtype(
+        gen.config_tiny(B=2, H=3, N=3000, d=32, C=60, n_bits=64, L=5, topk=16), "bf16"),
+}
+
+
+@pytest.mark.parametrize("case", list(SEEDED))
+@pytest.mark.parametrize("variant", ["clustered", "iclustered"])
+def test_planes_drawn_from_seed(case, variant):
+    """No planes given: the library draws them from a seed (Section 3.2.2
+    draws them at random).  The drawn planes equal the oracle's draw from
+    the same seed (the two sides' fp64 log, cos and sin may differ in the
+    last place, so one fp32 ulp is allowed, and nearly every entry must match
+    exactly); they are the same on every call and differ for another seed;
+    the forward with them is bitwise the forward given those planes, which
+    matches the oracle."""
+    w = SEEDED[case]()
+    H, nb, D = w.planes.shape
+    seed = 0x2007048250
+    want = oracle.planes_from_seed(seed, H, nb, D).astype(np.float32)
+    t = w.topk if variant == "iclustered" else 0
+    got = run_gpu(w, t, seed=seed)
+    gp = got["planes"]
+    ulps = np.abs(gp.view(np.int32).astype(np.int64) - want.view(np.int32).astype(np.int64))
+    print("plane entries one ulp off the oracle's: %d of %d" % (int((ulps != 0).sum()), ulps.size))
+    assert ulps.max() <= 1 and (ulps == 0).mean() >= 0.999
+    again = run_gpu(w, t, seed=seed)
+    assert np.array_equal(again["planes"], gp) and np.array_equal(again["out"], got["out"])
+    other = run_gpu(w, t, seed=seed + 1)
+    assert np.mean(other["planes"] == gp) < 0.01
+    w.planes = gp
+    w.name = "%s-seeded-%s" % (w.name, case)
+    given = run_gpu(w, t)
+    for key in ("codes", "assign", "out", "values"):
+        assert np.array_equal(given[key], got[key]), key
+    check_end_to_end(w, t)
+
+
 @pytest.mark.parametrize("variant", ["clustered", "iclustered"])
 def test_block_kmeans_ragged_and_empty(variant):
     """The several-block K-means drivers with empty, one-row, one-block and
@@ -282,18 +321,18 @@ def test_invalid_arguments_enqueue_nothing():
     out = torch.full((1, 1, 64, 48), 7.25, device="cuda")
     ws = torch.empty(1 << 20, dtype=torch.uint8, device="cuda")
     rc = ca.clustered_attention_fwd(q.data_ptr(), q.data_ptr(), q.data_ptr(), None, planes.data_ptr(),
-                                    1, 1, 64, 48, ca.CA_F32, 10, 63, 3, out.data_ptr(), ws.data_ptr(),
+                                    1, 1, 64, 48, ca.CA_F32, 10, 63, 3, 0, out.data_ptr(), ws.data_ptr(),
                                     1 << 20, None, stream)
     assert rc == ca.CA_ERR_UNSUPPORTED
     q32 = torch.zeros((1, 1, 64, 32), device="cuda")
     p32 = torch.zeros((1, 63, 32), device="cuda")
     out32 = torch.full((1, 1, 64, 32), 7.25, device="cuda")
     rc = ca.iclustered_attention_fwd(q32.data_ptr(), q32.data_ptr(), q32.data_ptr(), None,
-                                     p32.data_ptr(), 1, 1, 64, 32, ca.CA_F32, 10, 63, 3, 4,
+                                     p32.data_ptr(), 1, 1, 64, 32, ca.CA_F32, 10, 63, 3, 0, 4,
                                      out32.data_ptr(), ws.data_ptr(), 16, None, stream)
     assert rc == ca.CA_ERR_WORKSPACE                        # 16 bytes: far too small
     rc = ca.iclustered_attention_fwd(q32.data_ptr(), q32.data_ptr(), q32.data_ptr(), None,
-                                     p32.data_ptr(), 1, 1, 64, 32, ca.CA_F32, 0, 63, 3, 4,
+                                     p32.data_ptr(), 1, 1, 64, 32, ca.CA_F32, 0, 63, 3, 0, 4,
                                      out32.data_ptr(), ws.data_ptr(), 1 << 20, None, stream)
     assert rc == ca.CA_ERR_INVALID_ARG                      # no clusters
     torch.cuda.synchronize()

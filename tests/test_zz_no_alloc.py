@@ -37,13 +37,13 @@ def _run(w, noalloc):
     if noalloc:
         rc = ca.iclustered_attention_fwd_noalloc(q.data_ptr(), k.data_ptr(), v.data_ptr(),
                                                  lens.data_ptr(), planes.data_ptr(), B, H, N, D,
-                                                 dt, w.C, w.n_bits, w.L, w.topk, out.data_ptr(),
-                                                 aux, stream)
+                                                 dt, w.C, w.n_bits, w.L, 0, w.topk,
+                                                 out.data_ptr(), aux, stream)
     else:
         need = ca.workspace_bytes(B, H, N, D, dt, w.C, w.n_bits, w.topk)
         ws = torch.empty(need, dtype=torch.uint8, device="cuda")
         rc = ca.iclustered_attention_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), lens.data_ptr(),
-                                         planes.data_ptr(), B, H, N, D, dt, w.C, w.n_bits, w.L,
+                                         planes.data_ptr(), B, H, N, D, dt, w.C, w.n_bits, w.L, 0,
                                          w.topk, out.data_ptr(), ws.data_ptr(), need, aux, stream)
     assert rc == ca.CA_OK, ca.library().ca_last_error()
     torch.cuda.synchronize()
@@ -77,7 +77,7 @@ def test_noalloc_rejects_sizes_beyond_its_scratch():
     out = torch.full_like(q, 5.0)
     rc = ca.iclustered_attention_fwd_noalloc(q.data_ptr(), q.data_ptr(), q.data_ptr(), None,
                                              planes.data_ptr(), B, H, N, D, ca.CA_BF16, C, 63, 15,
-                                             topk, out.data_ptr(), None,
+                                             0, topk, out.data_ptr(), None,
                                              torch.cuda.current_stream().cuda_stream)
     assert rc == ca.CA_ERR_UNSUPPORTED
     assert b"scratch" in ca.library().ca_last_error()
