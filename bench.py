@@ -506,7 +506,7 @@ def bench_long(args):
     ms = _timed(hip, stream, fwd, max(3, args.steps // 20))
     stages = {}
     lib = ca.library()
-    for name, sid in ca.STAGES.items():
+    for name, sid in dict(ca.STAGES, attn_tile=ca.CA_KERNEL_ATTN_TILE).items():
         ts = []
         for _ in range(3):
             e0, e1 = hip.event(), hip.event()
@@ -525,7 +525,10 @@ def bench_long(args):
                       "ms_per_call": round(ms, 4), "dtype": "bf16", "data": "synthetic",
                       "config": {"workload": "long-context stress: batch 1, heads 8, N 65536, d 64, bf16, "
                                              "C 200, B 63, L 15, k 64; i-clustered"},
-                      "stages_us": stages}), flush=True)
+                      "stages_us": stages,
+                      "phases": {name: phase_entry(w, name, w.topk, us, LONG_PROFILE)
+                                 for name, us in stages.items() if name != "centroid_attn"}}),
+          flush=True)
 
 
 def bench_oracle_top(args):
@@ -627,14 +630,18 @@ def cpu_model():
     return platform.processor() or platform.machine()
 
 
-def phase_entry(w, stage, variant_topk, us):
-    """Achieved rate of one stage launch (the whole batch) against its bound."""
+def phase_entry(w, stage, variant_topk, us, profile=None):
+    """Achieved rate of one stage launch (the whole batch) against its bound,
+    and the stage's HBM bytes per launch from the workload's committed counter
+    profile (null without one, or once the kernels have changed)."""
     amount, unit, bound, peak = stage_work(w, stage, variant_topk)
     if us is None or us <= 0:
         return None
     achieved = amount / (us * 1e-6) / (1e9 if unit == "GB/s" else 1e12)
+    key = "%s (%s)" % (stage, "iclustered" if variant_topk else "clustered")
     return {"us": round(us, 2), "achieved": round(achieved, 3), "unit": unit, "bound": bound,
-            "peak": peak, "frac": round(achieved / peak, 5)}
+            "peak": peak, "frac": round(achieved / peak, 5),
+            "traffic": measured_traffic(key, profile) if profile else None}
 
 
 HEADLINE = {
@@ -642,6 +649,7 @@ HEADLINE = {
                 "C 100, B 63, L 10, k 32; clustered + i-clustered",
     "profile": "sweep_b1h8n32768_d64_f32",
 }
+LONG_PROFILE = "long_b1h8n65536_d64_bf16"
 SPEECH = {
     "workload": "speech-encoder layer: batch 32, heads 6, N 800 (lengths 400-800), d 32, fp32, "
                 "C 100, B 63, L 10, k 32; clustered + i-clustered",
@@ -772,7 +780,7 @@ def bench_forward(args, w, desc):
     for (n_, t_), ms in sorted(st.items()):
         if n_ == "centroid_attn":
             continue  # the tile kernel is reported alone; the merge is the difference
-        e = phase_entry(w, n_, t_, ms * 1e3)
+        e = phase_entry(w, n_, t_, ms * 1e3, desc["profile"])
         if e is not None:
             phases["%s_%s" % (n_, "ic" if t_ else "c")] = e
     for t_ in (0, w.topk):
