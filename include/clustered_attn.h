@@ -217,7 +217,11 @@ int clustered_attention_bwd(const void* q, const void* k, const void* v,
  *                  dK and dQ as for the clustered variant.
  * workspace must be that of the last iclustered_attention_fwd call with the
  * same inputs, n_clusters and topk; other arguments as for
- * clustered_attention_bwd.
+ * clustered_attention_bwd.  The top-k parts of dK_l and dV_l are summed over
+ * the sets that hold key l as 64-bit fixed-point integers (units of 2^-32),
+ * which makes the result independent of their order; a term above 2^22 in
+ * magnitude, or one that is not finite, cannot be held, and the dK or dV
+ * entry it belongs to is then written as NaN.
  */
 int iclustered_attention_bwd(const void* q, const void* k, const void* v,
                              const int32_t* lengths, int batch, int heads, int n,

@@ -687,11 +687,14 @@ __global__ __launch_bounds__(1024) void bwd_index_kernel(BwdArgs a) {
 // order of the entries does not matter and the result is deterministic),
 // then rounds the sum once into fp32.  A term is converted exactly when
 // |x| >= 2^-8 (x * 2^32 is then an integer in fp32) and to the nearest unit
-// otherwise; terms are clamped to |x| <= 2^22 so that no sum of at most 256
-// of them leaves the int64 range.
-__device__ __forceinline__ long long to_fixed32(float x) {
-  x = fminf(fmaxf(x, -4194304.0f), 4194304.0f);
-  return __float2ll_rn(x * 4294967296.0f);
+// otherwise.  Terms up to |x| = 2^22 are held, so no sum of at most 256 of
+// them leaves the int64 range; a larger or non-finite term is not added but
+// sets `bad`, and the entry it belongs to is written as NaN, so that the
+// caller sees it instead of a silently altered sum.
+__device__ __forceinline__ long long to_fixed32(float x, bool& bad) {
+  const bool ok = fabsf(x) <= 4194304.0f;  // false for NaN as well
+  bad = bad || !ok;
+  return ok ? __float2ll_rn(x * 4294967296.0f) : 0ll;
 }
 template <int D>
 __global__ __launch_bounds__(256) void bwd_index_gather_kernel(BwdArgs a) {
@@ -710,6 +713,7 @@ __global__ __launch_bounds__(256) void bwd_index_gather_kernel(BwdArgs a) {
   const float4* pk = reinterpret_cast<const float4*>(a.part_k) + first * Q4 + part;
   const float4* pv = reinterpret_cast<const float4*>(a.part_v) + first * Q4 + part;
   long long ak[4] = {0, 0, 0, 0}, av[4] = {0, 0, 0, 0};
+  bool bk[4] = {false, false, false, false}, bv[4] = {false, false, false, false};
   constexpr int B = 4;  // entries in flight (consecutive rows)
   for (int t0 = 0; t0 < cnt; t0 += B) {
     float4 k4[B], v4[B];
@@ -721,24 +725,27 @@ __global__ __launch_bounds__(256) void bwd_index_gather_kernel(BwdArgs a) {
     }
 #pragma unroll
     for (int t = 0; t < B; ++t) {
-      ak[0] += to_fixed32(k4[t].x); ak[1] += to_fixed32(k4[t].y);
-      ak[2] += to_fixed32(k4[t].z); ak[3] += to_fixed32(k4[t].w);
-      av[0] += to_fixed32(v4[t].x); av[1] += to_fixed32(v4[t].y);
-      av[2] += to_fixed32(v4[t].z); av[3] += to_fixed32(v4[t].w);
+      ak[0] += to_fixed32(k4[t].x, bk[0]); ak[1] += to_fixed32(k4[t].y, bk[1]);
+      ak[2] += to_fixed32(k4[t].z, bk[2]); ak[3] += to_fixed32(k4[t].w, bk[3]);
+      av[0] += to_fixed32(v4[t].x, bv[0]); av[1] += to_fixed32(v4[t].y, bv[1]);
+      av[2] += to_fixed32(v4[t].z, bv[2]); av[3] += to_fixed32(v4[t].w, bv[3]);
     }
   }
   constexpr double kUnit = 1.0 / 4294967296.0;
   float4* dk4 = reinterpret_cast<float4*>(a.dk) + ul * Q4 + part;
   float4* dv4 = reinterpret_cast<float4*>(a.dv) + ul * Q4 + part;
   float4 sk = *dk4, sv = *dv4;
-  sk.x = static_cast<float>(static_cast<double>(sk.x) + static_cast<double>(ak[0]) * kUnit);
-  sk.y = static_cast<float>(static_cast<double>(sk.y) + static_cast<double>(ak[1]) * kUnit);
-  sk.z = static_cast<float>(static_cast<double>(sk.z) + static_cast<double>(ak[2]) * kUnit);
-  sk.w = static_cast<float>(static_cast<double>(sk.w) + static_cast<double>(ak[3]) * kUnit);
-  sv.x = static_cast<float>(static_cast<double>(sv.x) + static_cast<double>(av[0]) * kUnit);
-  sv.y = static_cast<float>(static_cast<double>(sv.y) + static_cast<double>(av[1]) * kUnit);
-  sv.z = static_cast<float>(static_cast<double>(sv.z) + static_cast<double>(av[2]) * kUnit);
-  sv.w = static_cast<float>(static_cast<double>(sv.w) + static_cast<double>(av[3]) * kUnit);
+  auto add = [&](float base, long long sum, bool bad) {
+    return bad ? __builtin_nanf("") : static_cast<float>(static_cast<double>(base) + static_cast<double>(sum) * kUnit);
+  };
+  sk.x = add(sk.x, ak[0], bk[0]);
+  sk.y = add(sk.y, ak[1], bk[1]);
+  sk.z = add(sk.z, ak[2], bk[2]);
+  sk.w = add(sk.w, ak[3], bk[3]);
+  sv.x = add(sv.x, av[0], bv[0]);
+  sv.y = add(sv.y, av[1], bv[1]);
+  sv.z = add(sv.z, av[2], bv[2]);
+  sv.w = add(sv.w, av[3], bv[3]);
   *dk4 = sk;
   *dv4 = sv;
 }

@@ -101,3 +101,26 @@ def test_backward_singletons_equal_exact_attention_gradient(topk):
         for x, r in zip(grads[0], (tq.grad, tk.grad, tv.grad)):
             r = r.numpy()
             assert np.abs(x[0, h] - r).max() <= REL * max(1.0, np.abs(r).max())
+
+
+def test_backward_flags_terms_beyond_the_fixed_point_range():
+    """The top-k parts of dK and dV are summed as 64-bit fixed-point integers
+    that hold terms up to 2^22 in magnitude.  An output gradient scaled far
+    beyond that must mark the affected entries as NaN (not clamp them), and
+    only entries of keys that some top-k set holds; dQ stays finite."""
+    w = gen.config_tiny(B=1, H=2, N=512, d=32, C=20, L=4, topk=8)
+    dout = gen.output_gradient(w) * np.float32(1e9)
+    grads, fwd = run_gpu_backward(w, w.topk, dout)
+    dq, dk, dv = grads[0]
+    assert np.isfinite(dq).all()
+    B, H, N, _ = w.q.shape
+    held = np.zeros((B, H, N), bool)
+    for b in range(B):
+        for h in range(H):
+            t = fwd["topk"][b, h].reshape(-1)
+            held[b, h, t[t >= 0]] = True
+    flagged = np.isnan(dk).any(axis=-1) | np.isnan(dv).any(axis=-1)
+    print("flagged keys: %d of %d held by a top-k set" % (int(flagged.sum()), int(held.sum())))
+    assert flagged.any()
+    assert not (flagged & ~held).any()
+    assert np.isfinite(dk[~held]).all() and np.isfinite(dv[~held]).all()
