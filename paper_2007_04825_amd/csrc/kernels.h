@@ -38,9 +38,9 @@ inline int coop_max_blocks(int n, int units) {
   const int by_grid = units > 0 ? (kCoopMaxWgs / units > 0 ? kCoopMaxWgs / units : 1) : 1;
   return by_len < by_grid ? by_len : by_grid;
 }
-// Ints per unit of the cooperative K-means' arrival word (64-bit, 8-byte
-// aligned); the kernel that runs before it (hashing, or the copy of given
-// codes) sets it and both count tables to zero.
+// Ints per unit of the cooperative K-means' two arrival words (64-bit each,
+// 8-byte aligned); the kernel that runs before it (hashing, or the copy of
+// given codes) sets them and both count tables to zero.
 constexpr int kSyncInts = 4;
 // Words per unit of a count table of the cooperative K-means.
 int coop_table_stride(int C);

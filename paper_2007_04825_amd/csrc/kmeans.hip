@@ -657,10 +657,17 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
 // whole table and forms the next centroids by the per-bit majority itself.
 // Integer sums, so nothing depends on the order of the atomics.  Table t % 2
 // is next changed in round t + 2, after the arrival of round t + 1, which
-// every reader of round t has passed.  The arrival counter is one 64-bit
-// word: each arrival adds 1 to its low half and, when some query of the
-// workgroup moved in that round, 1 to its high half, so the poll that sees
-// the last arrival also tells whether any query of the unit moved.  Every
+// every reader of round t has passed.  Arrivals go to one of two 64-bit
+// words, word t % 2: each adds 1 to its low half and, when some query of the
+// workgroup moved in that round, 1 to its high half.  A workgroup arrives in
+// round t + 2 only after every workgroup has arrived in round t + 1, so when
+// the low half of word t % 2 shows every arrival of rounds t, t - 2, ..., the
+// word holds exactly those rounds' arrivals, however late the poll comes;
+// its high half, against the value seen two rounds earlier, tells whether
+// any query of the unit moved in round t, the same answer for every
+// workgroup.  (With one word for all rounds, a poll delayed past other
+// workgroups' next arrival would count their next-round moves in this round
+// and could end the loop one round early in that workgroup alone.)  Every
 // value that crosses workgroups travels through device-scope atomics or
 // stores, each wave waits until its own have been performed before the
 // workgroup barrier that precedes the arrival, and the waiting side reads
@@ -683,7 +690,7 @@ constexpr int kSpinLimit = 1 << 22;   // polls of the arrival counter before giv
 static_assert(kCoopMaxQ <= kKmLdsMaxN, "the shared assign step handles kKmLdsMaxN queries");
 constexpr int kTabBatch = 8;          // table words requested together per thread
 constexpr int kRowWords = 33;         // table words per cluster: 32 bit pairs and the size
-static_assert(kSyncInts >= 2, "one 64-bit arrival word");
+static_assert(kSyncInts >= 4, "two 64-bit arrival words");
 
 template <typename X>
 __device__ __forceinline__ X ld_agent(const X* p) {
@@ -708,7 +715,7 @@ struct CoopArgs {
   int32_t* bases;          // [U][nwg][C] first member position of (workgroup, cluster)
   int32_t* lsizes;         // [U][nwg][C] members of (workgroup, cluster)
   uint64_t* tab;           // [U][2][tstride] running count tables, zero at launch
-  int32_t* sync;           // [U][kSyncInts] arrival word (64-bit), zero at launch
+  int32_t* sync;           // [U][kSyncInts] two 64-bit arrival words, zero at launch
 };
 
 // The 64-bit word whose even bits are e and odd bits are o.
@@ -793,7 +800,7 @@ __global__ __launch_bounds__(kKmThreads) void kmeans_coop_kernel(CoopArgs a) {
   __syncthreads();
   unsigned long long* arrive =
       reinterpret_cast<unsigned long long*>(a.sync + static_cast<size_t>(u) * kSyncInts);
-  unsigned long long moved_before = 0;  // high half of the arrival word after the previous round
+  unsigned long long moved_seen[2] = {0, 0};  // high half of each arrival word when last seen
   for (int t = 0; t < a.L; ++t) {
     // every query tile's operands come from the LDS codes (cached operands
     // would stay live across the assign step and, with two tile groups per
@@ -827,19 +834,26 @@ __global__ __launch_bounds__(kKmThreads) void kmeans_coop_kernel(CoopArgs a) {
     if (tid == 0) {
       const unsigned long long add = 1ull + (sh.nchange > 0 ? 0x100000000ull : 0ull);
       sh.nchange = 0;
-      __hip_atomic_fetch_add(arrive, add, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      const unsigned long long target = static_cast<unsigned long long>(t + 1) * nwg;
+      unsigned long long* word = arrive + (t & 1);
+      __hip_atomic_fetch_add(word, add, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      // every arrival of rounds t, t - 2, ... (t / 2 + 1 per workgroup)
+      const unsigned long long target = static_cast<unsigned long long>(t / 2 + 1) * nwg;
       unsigned long long seen = 0;
       int spins = 0;
-      while (((seen = __hip_atomic_load(arrive, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) & 0xffffffffull) <
+      while (((seen = __hip_atomic_load(word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) & 0xffffffffull) <
                  target &&
              spins < kSpinLimit) {
         __builtin_amdgcn_s_sleep(1);
         ++spins;
       }
       sh.ok = spins < kSpinLimit;
-      sh.moved = (seen >> 32) != moved_before;
-      moved_before = seen >> 32;
+      const unsigned long long moves = seen >> 32;
+      const unsigned long long before = (t & 1) ? moved_seen[1] : moved_seen[0];
+      sh.moved = moves != before;
+      if (t & 1)
+        moved_seen[1] = moves;
+      else
+        moved_seen[0] = moves;
     }
     __syncthreads();
     if (t + 1 == a.L || !sh.moved || !sh.ok) break;  // no query moved: later rounds repeat this one
