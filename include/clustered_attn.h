@@ -325,9 +325,12 @@ int ca_time_next_stage(int stage, void* start_event, void* stop_event);
  * Chooses the K-means driver for later calls in this process: 0 automatic
  * (default), 1 one workgroup per unit (used only when n <= 4096), 2 one
  * kernel pair per Lloyd round, 3 one cooperative launch for all rounds (used
- * only when all its workgroups fit on the device at once, otherwise 2).  All
- * give identical partitions; the switch exists so that tests cover every
- * driver and benchmarks can compare them.  Returns CA_OK or
+ * only when all its workgroups fit on the device at once, otherwise 2), whose
+ * workgroups also form the per-workgroup centroid sums when its grid covers
+ * every compute unit; 4 and 5 are 3 with those sums always formed by the
+ * K-means kernel (4) or always by a separate kernel (5).  All give identical
+ * partitions and centroids within fp32 rounding; the switch exists so that
+ * tests cover every driver and benchmarks can compare them.  Returns CA_OK or
  * CA_ERR_INVALID_ARG.
  */
 int ca_set_kmeans_path(int path);

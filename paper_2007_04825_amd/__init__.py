@@ -164,7 +164,8 @@ def time_next_stage(stage: int, start_event, stop_event):
 
 def set_kmeans_path(path: int):
     """0 automatic, 1 one workgroup per unit, 2 one kernel pair per Lloyd round,
-    3 one cooperative launch for all rounds."""
+    3 one cooperative launch for all rounds; 4 and 5 as 3 with the centroid
+    sums formed by the K-means kernel (4) or by a separate kernel (5)."""
     _check(library().ca_set_kmeans_path(int(path)))
 
 

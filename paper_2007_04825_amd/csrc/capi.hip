@@ -74,6 +74,7 @@ size_t carve_workspace(const Problem& p, void* base, Workspace* ws) {
   w.stats = static_cast<float*>(take(U * C * 2 * 4));
   w.ncoop = coop_max_blocks(p.n, p.units());
   w.coop_q = 0;
+  w.coop_sums = 0;
   const size_t NC = static_cast<size_t>(w.ncoop);
   w.sync = static_cast<int32_t*>(take(U * kSyncInts * 4));
   w.ctab = static_cast<uint64_t*>(take(2 * U * static_cast<size_t>(coop_table_stride(p.C)) * 8));
@@ -235,6 +236,7 @@ static int run_forward(const void* q, const void* k, const void* v, const int32_
     if (driver == 3) {
       // all rounds and the member lists in one launch
       ws.coop_q = coop_block_queries(p, ws.ncoop);
+      ws.coop_sums = coop_fused_sums(p, ws.coop_q);
       CA_TRY(mark(CA_KERNEL_KMEANS, true, s));
       CA_TRY(launch_kmeans_coop(p, ws, s));
       CA_TRY(mark(CA_KERNEL_KMEANS, false, s));
@@ -588,10 +590,11 @@ int ca_time_next_stage(int stage, void* start_event, void* stop_event) {
 }
 
 // Selects the K-means driver (0 automatic, 1 one workgroup per unit, 2 one
-// launch pair per round, 3 cooperative).  Exposed for tests that cover every
-// driver.
+// launch pair per round, 3 cooperative; 4 and 5 cooperative with the centroid
+// sums formed by the K-means kernel or by a separate kernel).  Exposed for
+// tests that cover every driver.
 int ca_set_kmeans_path(int path) {
-  if (path < 0 || path > 3) return ca::fail(CA_ERR_INVALID_ARG, "path must be 0, 1, 2 or 3");
+  if (path < 0 || path > 5) return ca::fail(CA_ERR_INVALID_ARG, "path must be 0 to 5");
   ca::set_kmeans_path(path);
   return CA_OK;
 }

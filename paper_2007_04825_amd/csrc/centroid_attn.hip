@@ -79,11 +79,12 @@ __global__ __launch_bounds__(256) void centroid_kernel(const T* __restrict__ q,
   dst[t] = static_cast<float>(acc / static_cast<double>(sz));
 }
 
-// Eq. (3) after the cooperative K-means, in two steps with all the chip's
-// workgroups.  Step 1: for every (unit, block of coop_q queries, cluster)
-// D lanes add the block's members of the cluster (consecutive in the member
-// list, ascending query order) in fp64, 32 rows in flight.  Step 2: the
-// blocks' sums are added in block order and divided by the cluster size.  The
+// Eq. (3) after the cooperative K-means, in two steps.  Step 1 (unless the
+// K-means kernel formed these sums itself): for every (unit, block of coop_q
+// queries, cluster) D lanes add the block's members of the cluster
+// (consecutive in the member list, ascending query order) in fp64, 32 rows in
+// flight.  Step 2: the blocks' sums are added in block order and divided by
+// the cluster size.  The
 // association is fixed, so the result is deterministic.
 template <int D, typename T>
 __global__ __launch_bounds__(256) void centroid_part_kernel(const T* __restrict__ q,
@@ -1289,12 +1290,14 @@ template <int D, typename T>
 static hipError_t launch_coop_centroids_t(const Problem& p, const Workspace& ws, hipStream_t s) {
   constexpr int per_block = 4 * (64 / D);  // items per workgroup
   const int nwg = (p.n + ws.coop_q - 1) / ws.coop_q;
-  const long long n1 = static_cast<long long>(p.units()) * nwg * p.C;
-  hipLaunchKernelGGL((centroid_part_kernel<D, T>), dim3(static_cast<unsigned>((n1 + per_block - 1) / per_block)),
-                     dim3(256), 0, s, static_cast<const T*>(p.q), ws.members, ws.cbases, ws.clsizes,
-                     p.n, p.C, nwg, n1, ws.qc_part);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  if (!ws.coop_sums) {
+    const long long n1 = static_cast<long long>(p.units()) * nwg * p.C;
+    hipLaunchKernelGGL((centroid_part_kernel<D, T>), dim3(static_cast<unsigned>((n1 + per_block - 1) / per_block)),
+                       dim3(256), 0, s, static_cast<const T*>(p.q), ws.members, ws.cbases, ws.clsizes,
+                       p.n, p.C, nwg, n1, ws.qc_part);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   const long long n2 = static_cast<long long>(p.units()) * p.C;
   hipLaunchKernelGGL((centroid_final_kernel<D>), dim3(static_cast<unsigned>((n2 + per_block - 1) / per_block)),
                      dim3(256), 0, s, ws.qc_part, ws.sizes, p.C, nwg, n2, ws.qc);

@@ -77,6 +77,7 @@ struct Workspace {
   int nchunk;           // ceil(N / kChunk)
   int ncoop;            // cooperative K-means blocks the workspace holds per unit
   int coop_q;           // queries per cooperative block of this call (0: not used)
+  int coop_sums;        // 1: the cooperative K-means forms the blocks' centroid sums itself
 };
 
 // Carves the workspace; returns the bytes needed (ws may be null to only size it).
@@ -104,12 +105,16 @@ hipError_t launch_cluster_lds(const Problem& p, const uint64_t* codes_in, const 
 // assignments of valid rows.
 hipError_t launch_kmeans(const Problem& p, const Workspace& ws, hipStream_t s);
 // Cooperative K-means on ws.codes (ws.sync zero), all rounds in one launch:
-// assignments (-1 on padded rows), sizes, offsets, member lists and the
-// per-block member ranges that launch_coop_centroids reads.
+// assignments (-1 on padded rows), sizes, offsets, member lists and either
+// each block's fp64 centroid sums (ws.coop_sums) or the per-block member
+// ranges from which launch_coop_centroids forms them.
 hipError_t launch_kmeans_coop(const Problem& p, const Workspace& ws, hipStream_t s);
-// Centroids (Eq. 3) after launch_kmeans_coop: per-block fp64 partial sums,
-// then added in block order.
+// Centroids (Eq. 3) after launch_kmeans_coop: per-block fp64 partial sums
+// (unless the K-means formed them), then added in block order.
 hipError_t launch_coop_centroids(const Problem& p, const Workspace& ws, hipStream_t s);
+// Whether the cooperative K-means with coop_q queries per block should form
+// the centroid sums itself: its grid covers every compute unit.
+int coop_fused_sums(const Problem& p, int coop_q);
 // K-means driver for a problem: 1 one workgroup per unit, 2 one launch pair
 // per round, 3 cooperative.
 int kmeans_driver(const Problem& p);
@@ -164,7 +169,8 @@ size_t carve_bwd_workspace(const BwdProblem& p, void* base, BwdWorkspace* ws);
 hipError_t launch_backward(const BwdProblem& p, hipStream_t s, hipEvent_t ev_start, hipEvent_t ev_stop);
 
 // Which K-means path runs: 0 automatic, 1 one workgroup per unit, 2 one
-// launch pair per round, 3 cooperative.
+// launch pair per round, 3 cooperative (4 / 5: with the centroid sums always
+// in the K-means kernel / always in a separate kernel).
 void set_kmeans_path(int path);
 int kmeans_uses_lds(const Problem& p);
 

@@ -684,7 +684,12 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
 // no query of the unit moved ends the loop: every later round would repeat
 // it.  The final member lists come from the per-workgroup sizes of the last
 // round: cluster j's members of workgroup b follow those of workgroups
-// 0..b-1, so each cluster's members stay in ascending query order.
+// 0..b-1, so each cluster's members stay in ascending query order.  When the
+// grid covers every compute unit, each workgroup then adds its own members'
+// rows of Q per cluster (coop_centroid_sums), so that the centroid step only
+// adds the workgroups' sums; otherwise (a grid on part of the chip streams Q
+// more slowly than a kernel on all of it) centroid_part_kernel forms them
+// from the member ranges (bases, lsizes) written here.
 // ===========================================================================
 constexpr int kSpinLimit = 1 << 22;   // polls of the arrival counter before giving up
 static_assert(kCoopMaxQ <= kKmLdsMaxN, "the shared assign step handles kKmLdsMaxN queries");
@@ -716,7 +721,94 @@ struct CoopArgs {
   int32_t* lsizes;         // [U][nwg][C] members of (workgroup, cluster)
   uint64_t* tab;           // [U][2][tstride] running count tables, zero at launch
   int32_t* sync;           // [U][kSyncInts] two 64-bit arrival words, zero at launch
+  int sums;                // 1: also form the per-workgroup centroid sums
+  const void* q;           // [U][N][d] queries, for the centroid sums
+  int d, dtype;
+  double* qc_part;         // [U][C][nwg][d] per-workgroup centroid sums
 };
+
+// Centroid sums (Eq. 3) of one workgroup of the one-launch K-means: for every
+// cluster j, the fp64 sum of this workgroup's member rows of Q in ascending
+// query order goes to part[(j nwg + b) d + t]; centroid_final_kernel adds the
+// workgroups' sums in workgroup order and divides by the cluster size.
+// Groups of D lanes (lane = dimension) take contiguous ranges of the local
+// member list lmem (cluster j at positions lofs[j] .. lofs[j + 1] - 1), all of
+// a range's rows requested 32 at a time and added in order; a cluster cut by
+// range ends leaves partial sums in LDS (slot 0: the piece at the start of a
+// range, slot 1: the piece at its end), which the group holding its first
+// member adds up in range order after a barrier.  The association is fixed,
+// so the result is deterministic.
+template <int D, typename T>
+__device__ __forceinline__ void coop_centroid_sums(const T* __restrict__ rows, const int32_t* lmem,
+                                                   const int32_t* lofs, const int32_t* lassign,
+                                                   const int32_t* lsize, int nq, int ce, int C,
+                                                   double* cut, double* part, int nwg, int b,
+                                                   int tid, int lane, int wave) {
+  constexpr int GPW = 64 / D;        // groups per wave
+  constexpr int G = kKmWaves * GPW;  // groups per workgroup
+  constexpr int RB = 32;             // rows in flight per lane
+  const int t = lane % D, grp = wave * GPW + lane / D;
+  const int per = (nq + G - 1) / G;
+  const int p0 = min(nq, grp * per), p1 = min(nq, p0 + per);
+  auto slot = [&](int j) -> double& { return part[(static_cast<size_t>(j) * nwg + b) * D + t]; };
+  int j = 0, start = 0, end = 0;
+  if (p0 < p1) {  // cluster of position p0
+    j = lassign[lmem[p0]];
+    start = lofs[j];
+    end = lofs[j + 1];
+  }
+  int s1j = -1, s1end = 0;  // the cluster cut at the end of the range
+  double acc = 0.0;
+  for (int b0 = p0; b0 < p1; b0 += RB) {
+    // positions past the range repeat its last row (straight-line loads)
+    int mi[RB];
+#pragma unroll
+    for (int e = 0; e < RB; ++e) mi[e] = lmem[min(b0 + e, p1 - 1)];
+    float x[RB];
+#pragma unroll
+    for (int e = 0; e < RB; ++e) x[e] = to_f32(rows[static_cast<size_t>(mi[e]) * D + t]);
+#pragma unroll
+    for (int e = 0; e < RB; ++e) {
+      const int p = b0 + e;
+      if (p >= p1) continue;
+      acc += static_cast<double>(x[e]);
+      if (p + 1 == end) {  // cluster j ends here
+        if (start >= p0)
+          slot(j) = acc;
+        else
+          cut[(grp * 2 + 0) * D + t] = acc;
+        acc = 0.0;
+        if (p + 1 < p1) {  // next non-empty cluster, starting at p + 1
+          do {
+            ++j;
+            end = lofs[j + 1];
+          } while (end == p + 1);
+          start = p + 1;
+        }
+      } else if (p + 1 == p1) {  // the range ends inside cluster j
+        if (start < p0) {
+          cut[(grp * 2 + 0) * D + t] = acc;
+        } else {
+          cut[(grp * 2 + 1) * D + t] = acc;
+          s1j = j;
+          s1end = end;
+        }
+      }
+    }
+  }
+  // clusters with no member in this workgroup, and slots past C_eff
+  for (int x = tid; x < C * D; x += kKmThreads) {
+    const int jj = x / D;
+    if (jj >= ce || lsize[jj] == 0) part[(static_cast<size_t>(jj) * nwg + b) * D + x % D] = 0.0;
+  }
+  __syncthreads();
+  if (s1j >= 0) {
+    double sum = cut[(grp * 2 + 1) * D + t];
+    const int g_last = (s1end - 1) / per;
+    for (int gg = grp + 1; gg <= g_last; ++gg) sum += cut[(gg * 2 + 0) * D + t];
+    slot(s1j) = sum;
+  }
+}
 
 // The 64-bit word whose even bits are e and odd bits are o.
 __device__ __forceinline__ uint64_t interleave_bits(uint32_t e, uint32_t o) {
@@ -767,10 +859,17 @@ __global__ __launch_bounds__(kKmThreads) void kmeans_coop_kernel(CoopArgs a) {
       for (int j = tid; j < C; j += kKmThreads) a.sizes[static_cast<size_t>(u) * C + j] = 0;
       for (int j = tid; j <= C; j += kKmThreads) a.offsets[static_cast<size_t>(u) * (C + 1) + j] = 0;
     }
-    // every block's member ranges are empty (the centroid kernels read them all)
-    for (int j = tid; j < C; j += kKmThreads) {
-      lsz[j] = 0;
-      bs[j] = 0;
+    // every block's member ranges, or its centroid sums, are empty (the
+    // centroid kernels read them all)
+    if (a.sums) {
+      double* part = a.qc_part + static_cast<size_t>(u) * C * nwg * a.d;
+      for (int x = tid; x < C * a.d; x += kKmThreads)
+        part[(static_cast<size_t>(x / a.d) * nwg + b) * a.d + x % a.d] = 0.0;
+    } else {
+      for (int j = tid; j < C; j += kKmThreads) {
+        lsz[j] = 0;
+        bs[j] = 0;
+      }
     }
     return;
   }
@@ -928,8 +1027,29 @@ __global__ __launch_bounds__(kKmThreads) void kmeans_coop_kernel(CoopArgs a) {
     }
   }
   __syncthreads();
-  if (wave == 0) {  // exclusive scan of the unit's sizes: kCmax / 64 clusters per lane
+  // dead after the rounds: the local member list and its offsets (in the count
+  // rows) and the cut sums of the centroid step (in the published counts)
+  int32_t* lmem = reinterpret_cast<int32_t*>(sh.cnt);
+  int32_t* lofs = lmem + QW;  // [kCmax + 1]
+  double* cut = reinterpret_cast<double*>(&sh.pub[0][0]);
+  static_assert(sizeof(sh.cnt) >= sizeof(int32_t) * (QW + kCmax + 1), "local member list");
+  static_assert(sizeof(sh.pub) >= sizeof(double) * 2 * kKmThreads, "centroid cut sums");
+  if (wave == 0) {  // exclusive scans of the unit's and this workgroup's sizes: kCmax / 64 clusters per lane
     constexpr int PL = kCmax / 64;
+    int lsz4[PL], llocal = 0;
+#pragma unroll
+    for (int e = 0; e < PL; ++e) {
+      const int j = PL * lane + e;
+      lsz4[e] = j < ce ? sh.size[j] : 0;
+      llocal += lsz4[e];
+    }
+    int lrun = wave_incl_scan(llocal) - llocal;
+#pragma unroll
+    for (int e = 0; e < PL; ++e) {
+      lofs[PL * lane + e] = lrun;
+      lrun += lsz4[e];
+    }
+    if (lane == 63) lofs[kCmax] = lrun;
     int sz[PL], local = 0;
 #pragma unroll
     for (int e = 0; e < PL; ++e) {
@@ -949,13 +1069,46 @@ __global__ __launch_bounds__(kKmThreads) void kmeans_coop_kernel(CoopArgs a) {
   __syncthreads();
   for (int j = tid; j < C; j += kKmThreads) {
     if (b == 0) a.sizes[static_cast<size_t>(u) * C + j] = j < ce ? sh.tsize[j] : 0;
-    bs[j] = j < ce ? sh.off[j] : 0;
-    if (j >= ce) lsz[j] = 0;
+    if (!a.sums) {  // the member ranges that centroid_part_kernel reads
+      bs[j] = j < ce ? sh.off[j] : 0;
+      if (j >= ce) lsz[j] = 0;
+    }
   }
   if (b == 0 && tid == 0) a.offsets[static_cast<size_t>(u) * (C + 1) + C] = n;
   int32_t* mg = a.members + row0;
   member_sort(nq, ce, sh.assign, sh.off, reinterpret_cast<int32_t*>(sh.cop),
-              [&](int pos, int i) { mg[pos] = q0 + i; }, tid, lane, wave);
+              [&](int pos, int i) {
+                mg[pos] = q0 + i;
+                if (a.sums) {
+                  const int j = sh.assign[i];
+                  lmem[lofs[j] + pos - sh.off[j]] = i;
+                }
+              },
+              tid, lane, wave);
+  if (!a.sums) {
+    for (int i = tid; i < nq; i += kKmThreads) a.assign[row0 + q0 + i] = sh.assign[i];
+    return;  // uniform over the workgroup
+  }
+  __syncthreads();
+  double* part = a.qc_part + static_cast<size_t>(u) * C * nwg * a.d;
+  const size_t rbase = (row0 + q0) * static_cast<size_t>(a.d);
+  if (a.d == 64) {
+    if (a.dtype == 0)
+      coop_centroid_sums<64>(static_cast<const float*>(a.q) + rbase, lmem, lofs, sh.assign, sh.size, nq, ce, C,
+                             cut, part, nwg, b, tid, lane, wave);
+    else
+      coop_centroid_sums<64>(static_cast<const bf16_t*>(a.q) + rbase, lmem, lofs, sh.assign, sh.size, nq, ce,
+                             C, cut, part, nwg, b, tid, lane, wave);
+  } else {
+    if (a.dtype == 0)
+      coop_centroid_sums<32>(static_cast<const float*>(a.q) + rbase, lmem, lofs, sh.assign, sh.size, nq, ce, C,
+                             cut, part, nwg, b, tid, lane, wave);
+    else
+      coop_centroid_sums<32>(static_cast<const bf16_t*>(a.q) + rbase, lmem, lofs, sh.assign, sh.size, nq, ce,
+                             C, cut, part, nwg, b, tid, lane, wave);
+  }
+  // the assignment, written last so that the row loads above do not wait
+  // behind these stores
   for (int i = tid; i < nq; i += kKmThreads) a.assign[row0 + q0 + i] = sh.assign[i];
 }
 
@@ -1215,6 +1368,25 @@ static int coop_capacity() {
   return cap[dev] > 0 ? cap[dev] : 0;
 }
 
+int coop_fused_sums(const Problem& p, int coop_q) {
+  if (coop_q <= 0 || g_kmeans_path == 5) return 0;
+  if (g_kmeans_path == 4) return 1;
+  constexpr int kMaxDev = 64;
+  static int cus[kMaxDev] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDev) return 0;
+  if (cus[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
+      (void)hipGetLastError();
+      return 0;
+    }
+    cus[dev] = n > 0 ? n : -1;
+  }
+  const long long wgs = static_cast<long long>(p.units()) * ((p.n + coop_q - 1) / coop_q);
+  return cus[dev] > 0 && wgs >= cus[dev] ? 1 : 0;
+}
+
 int coop_block_queries(const Problem& p, int max_blocks) {
   const long long U = p.units();
   auto fits = [&](int qw, int cap) {
@@ -1233,7 +1405,7 @@ static bool coop_fits(const Problem& p) {
 int kmeans_driver(const Problem& p) {
   if (g_kmeans_path == 1 && p.n <= kKmLdsMaxN) return 1;
   if (g_kmeans_path == 2) return 2;
-  if (g_kmeans_path == 3) return coop_fits(p) ? 3 : 2;
+  if (g_kmeans_path >= 3) return coop_fits(p) ? 3 : 2;
   if (kmeans_uses_lds(p)) return 1;
   return coop_fits(p) ? 3 : 2;
 }
@@ -1323,10 +1495,15 @@ hipError_t launch_kmeans_coop(const Problem& p, const Workspace& ws, hipStream_t
   a.sizes = ws.sizes;
   a.offsets = ws.offsets;
   a.members = ws.members;
-  a.bases = ws.cbases;
   a.lsizes = ws.clsizes;
   a.tab = ws.ctab;
   a.sync = ws.sync;
+  a.bases = ws.cbases;
+  a.sums = ws.coop_sums;
+  a.q = p.q;
+  a.d = p.d;
+  a.dtype = p.dtype;
+  a.qc_part = ws.qc_part;
   void* args[] = {&a};
   const dim3 grid(a.nwg, p.units());
   switch (ws.coop_q) {

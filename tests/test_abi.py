@@ -85,9 +85,9 @@ def test_invalid_arguments_rejected_on_host(args, code):
 
 def test_kmeans_path_switch_validation():
     lib = ca.library()
-    assert lib.ca_set_kmeans_path(4) == ca.CA_ERR_INVALID_ARG
+    assert lib.ca_set_kmeans_path(6) == ca.CA_ERR_INVALID_ARG
     assert lib.ca_set_kmeans_path(-1) == ca.CA_ERR_INVALID_ARG
-    for path in (3, 2, 1, 0):
+    for path in (5, 4, 3, 2, 1, 0):
         assert lib.ca_set_kmeans_path(path) == ca.CA_OK
 
 

@@ -85,7 +85,7 @@ def test_every_kmeans_driver_agrees(name):
     w = workload(name)
     res = []
     try:
-        for path in (1, 2, 3):
+        for path in (1, 2, 4, 5):
             ca.set_kmeans_path(path)
             res.append(run_gpu(w, w.topk))
     finally:
@@ -205,7 +205,7 @@ def test_many_clusters_every_driver(N, dtype, topk, variant):
     w.lengths = np.array([N, N - 777], np.int32)
     t = topk if variant == "iclustered" else 0
     ref = run_oracle(w, t, key="bigc%d_%s_%d" % (N, dtype, topk))
-    paths = (1, 2, 3) if N <= 4096 else (2, 3)
+    paths = (1, 2, 4, 5) if N <= 4096 else (2, 4, 5)
     results = []
     try:
         for path in paths:
@@ -235,7 +235,7 @@ def test_full_width_codes_every_driver(variant):
     ref = run_oracle(w, t, key="fullwidth64")
     assert np.any(ref["codes"] >> np.uint64(63))      # bit 63 is in use
     try:
-        for path in (1, 2, 3):
+        for path in (1, 2, 4, 5):
             ca.set_kmeans_path(path)
             print("driver %d" % path, flush=True)
             got = run_gpu(w, t)
@@ -290,14 +290,15 @@ def test_planes_drawn_from_seed(case, variant):
 def test_block_kmeans_ragged_and_empty(variant):
     """The several-block K-means drivers with empty, one-row, one-block and
     block-edge sequences in one batch (every block of an empty sequence must
-    still describe empty member ranges)."""
+    still describe empty member ranges, or empty centroid sums when the
+    K-means kernel forms them)."""
     import paper_2007_04825_amd as ca
     w = gen.config_tiny(B=5, H=1, N=5000, d=32, C=100, L=4, topk=32)
     w.lengths = np.array([5000, 0, 1, 2049, 4097], np.int32)
     t = w.topk if variant == "iclustered" else 0
     ref = run_oracle(w, t, key="blockragged")
     try:
-        for path in (2, 3):
+        for path in (2, 4, 5):
             ca.set_kmeans_path(path)
             print("driver %d" % path, flush=True)
             got = run_gpu(w, t)
