@@ -475,10 +475,13 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
           if (g2 == gg) cnt = cg;
         }
       }
-      // sum over T of exp(s - max) (the numerator of the mass)
+      // sum over T of exp(s - max) (the numerator of the mass; a chunk of
+      // several leaves it to the merge)
       float tsum = 0.0f;
-      for (int x = c32; x < cnt; x += GL) tsum += __expf(row[cand[x]] - mx);
-      tsum = grp_sum<GL>(tsum);
+      if constexpr (FUSED) {
+        for (int x = c32; x < cnt; x += GL) tsum += __expf(row[cand[x]] - mx);
+        tsum = grp_sum<GL>(tsum);
+      }
       if constexpr (OTOP && FUSED) {
         // out_j = sum_{l in T} exp(s_l - m) v_l / sum_{l in T} exp(s_l - m), the
         // row maximum m being in T; lane c32 takes dims c32 (and c32 + 32),
