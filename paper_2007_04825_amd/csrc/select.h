@@ -109,8 +109,8 @@ __device__ __forceinline__ uint32_t wave_kth_key(uint32_t k1, uint32_t k2, bool 
 // chosen positions in ascending order to out[] and returns their number (kk);
 // also returns the row maximum and z = sum_pos exp(row[pos] - max).
 //
-// Each lane keeps the largest (and, for kk > 64, the second largest) value of
-// its strided slice.  The kk-th largest of those values is a threshold tau
+// Each lane keeps the largest and the second largest value of its strided
+// slice.  The kk-th largest of those values is a threshold tau
 // that at least kk entries reach, so every entry of the top-kk set is >= tau.
 // One more sweep collects the entries >= tau in position order (usually
 // little more than kk of them); the exact kk-th value among them is found by
@@ -137,7 +137,10 @@ __device__ int wave_topk_row(const float* row, int m, int kk, int* scratch, OutT
     ++have;
   }
   const float mx = wave_max(a1);
-  const bool two = kk > 64;
+  // the threshold from both kept values of every lane whenever a lane saw two:
+  // the kk-th largest of up to 128 values lets fewer entries through than the
+  // kk-th of the 64 lane maxima (long rows fell back to the radix selection)
+  const bool two = kk > 64 || m > 64;
   const uint32_t tau = wave_kth_key(have > 0 ? order_key(a1) : 0u, have > 1 ? order_key(a2) : 0u,
                                     two, kk);
   float z = 0.0f;
