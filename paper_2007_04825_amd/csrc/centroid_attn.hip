@@ -177,8 +177,12 @@ __device__ __forceinline__ void store_vec(bf16_t* p, const float* s) {
 // ---------------------------------------------------------------------------
 // Centroid attention tile kernel.
 // ---------------------------------------------------------------------------
-constexpr int kLStride = kChunk + 16;  // floats per LDS logit row (the four rows of a wave fall in distinct banks)
+// Floats per LDS logit row: a stride of 4 mod 64 puts the float4 accesses of
+// the 16 rows (lane c = row, lane group g = keys 4g..4g+3 of a tile) in
+// distinct banks.
+constexpr int kLStride = kChunk + 4;
 static_assert(kLStride >= kChunk, "rows padded for the top-k sweep: 32 grp_block_len(kChunk) <= kChunk");
+constexpr int kRedPad = 4;  // floats of padding per row of the cross-wave reduction
 constexpr int kCandCap = 128;
 // Whether fp32 inputs take the centroid products on the bf16 matrix cores
 // with both operands split in three (six part products, fp32 accuracy)
@@ -253,8 +257,10 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
   __shared__ float rowm[16], rowmass[16], rowtop[16];
   __shared__ int tcnt[16];
   __shared__ float zpart[NW][16];                              // per-wave sums of P per row
-  __shared__ float smax[16][NS];                               // [row][slice] maxima
-  __shared__ __align__(16) float stop[IMPROVED ? 16 : 1][NS][NT];  // [row][slice] kept logits
+  // [row][slice] maxima and kept logits, one slice of padding per row so that
+  // the slices' stores fall in distinct banks
+  __shared__ float smax[16][NS + 1];
+  __shared__ __align__(16) float stop[IMPROVED ? 16 : 1][NS + 1][NT];
   __shared__ uint16_t tpos16[IMPROVED ? 16 : 1][kCandCap];     // top-k candidates, then T
   __shared__ int moff[17];
   __shared__ int any_nonempty;
@@ -463,6 +469,7 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
         // rows whose threshold let too many entries through (many ties): the
         // whole wave selects them one after the other; its scratch is the
         // slice area of its own two rows, consumed by now
+        static_assert(!IMPROVED || 2 * (NS + 1) * NT >= 2 * kCandCap, "two rows' slices hold the wave's scratch");
         const uint64_t over = __ballot(cnt < 0);
         for (int gg = 0; gg < 2; ++gg) {
           if (((over >> (32 * gg)) & 1ull) == 0ull) continue;
@@ -619,19 +626,26 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
   psum = cross_rows_sum(psum);
   if (g == 0) zpart[wave][c] = psum;
   __syncthreads();  // logits are dead from here on: reuse them
-  float* red = logits;  // [NW waves][16 centroids][D]
-  static_assert(NW * 16 * D <= 16 * kLStride, "logit area reuse");
+  // [NW waves][16 centroids][D + kRedPad]: each lane stores its DT
+  // consecutive dimensions of a row at once, the padded rows in distinct banks
+  constexpr int RS = D + kRedPad;
+  float* red = logits;
+  static_assert(NW * 16 * RS <= 16 * kLStride, "logit area reuse");
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) red[(wave * 16 + c) * D + DT * (4 * g + i) + dt] = oacc[dt][i];
+  for (int i = 0; i < 4; ++i) {
+    float* dst = &red[(wave * 16 + c) * RS + DT * (4 * g + i)];
+    if constexpr (DT == 4)
+      *reinterpret_cast<float4*>(dst) = make_float4(oacc[0][i], oacc[1][i], oacc[2][i], oacc[3][i]);
+    else
+      *reinterpret_cast<float2*>(dst) = make_float2(oacc[0][i], oacc[1][i]);
+  }
   __syncthreads();
   for (int x = tid; x < 16 * D; x += kTileThreads) {
     const int cc = x / D, dim = x % D;
     float sum = 0.0f, z = 0.0f;
 #pragma unroll
     for (int w = 0; w < NW; ++w) {
-      sum += red[(w * 16 + cc) * D + dim];
+      sum += red[(w * 16 + cc) * RS + dim];
       z += zpart[w][cc];
     }
     if constexpr (IMPROVED && FUSED) z += rowtop[cc];
