@@ -46,7 +46,7 @@ __global__ __launch_bounds__(kHashThreads) __attribute__((amdgpu_waves_per_eu(4)
   }
   const int nq = min(kHashQB, n - q0);
   if (nq <= 0) return;  // uniform over the workgroup
-  __shared__ __align__(16) float sp[64 * D];
+  __shared__ __align__(16) float sp[64 * kPlaneRow<D>];
   const float* ph = planes + static_cast<size_t>(h) * n_bits * D;
   stage_planes<D>(ph, n_bits, sp, tid, kHashThreads);
   __syncthreads();

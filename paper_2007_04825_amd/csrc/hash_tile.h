@@ -44,21 +44,27 @@ struct PlaneOps {
   bool norms_ok;  // every plane norm within the range of the fp32 test
 };
 
-// Copies the n_bits planes of one head [n_bits][D] into sp[64][D] (LDS; rows
-// past n_bits are zero) with the threads of the workgroup, so that the waves
-// read their operands from LDS instead of all fetching the same few kilobytes
-// from L2.  The caller synchronises the workgroup before sp is read.
+// Floats per staged plane row: a stride of 4 mod 64 puts the rows that the
+// sixteen lanes of a lane group read together in distinct LDS banks.
+template <int D>
+constexpr int kPlaneRow = D + 4;
+
+// Copies the n_bits planes of one head [n_bits][D] into sp[64][kPlaneRow<D>]
+// (LDS; rows past n_bits are zero) with the threads of the workgroup, so that
+// the waves read their operands from LDS instead of all fetching the same few
+// kilobytes from L2.  The caller synchronises the workgroup before sp is read.
 template <int D>
 __device__ __forceinline__ void stage_planes(const float* __restrict__ ph, int n_bits, float* sp,
                                              int tid, int nthreads) {
   for (int x = tid; x < 64 * D / 4; x += nthreads) {
     float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
     if (x * 4 < n_bits * D) v = *reinterpret_cast<const float4*>(ph + x * 4);
-    *reinterpret_cast<float4*>(sp + x * 4) = v;
+    const int row = x / (D / 4), col = 4 * (x % (D / 4));
+    *reinterpret_cast<float4*>(sp + row * kPlaneRow<D> + col) = v;
   }
 }
 
-// Builds this lane's plane operands from the staged planes sp[64][D].  The
+// Builds this lane's plane operands from the staged planes sp[64][kPlaneRow<D>].  The
 // lanes of a wave read every plane value between them; returns true (in every
 // lane) if one of them is not a bf16 value.
 template <int D>
@@ -73,7 +79,7 @@ __device__ __forceinline__ bool load_plane_ops(const float* sp, int n_bits, int 
       const int plane = pt * 16 + c;
       v4u w = {0u, 0u, 0u, 0u};
       if (plane < n_bits) {
-        const float* pr = sp + plane * D + kc * 32 + 8 * g;
+        const float* pr = sp + plane * kPlaneRow<D> + kc * 32 + 8 * g;
         const float4 x0 = *reinterpret_cast<const float4*>(pr);
         const float4 x1 = *reinterpret_cast<const float4*>(pr + 4);
         const uint32_t u[8] = {__float_as_uint(x0.x), __float_as_uint(x0.y), __float_as_uint(x0.z),
@@ -230,7 +236,7 @@ __device__ uint64_t hash_tile(const T* __restrict__ qu, const TileRaw<D, T>& raw
       const int k = __ffs(m) - 1;
       m &= m - 1;
       const double p = exact_projection<D, T>(qu + static_cast<size_t>(row0 + c) * D,
-                                              sp + ((k >> 2) * 16 + 4 * g + (k & 3)) * D);
+                                              sp + ((k >> 2) * 16 + 4 * g + (k & 3)) * kPlaneRow<D>);
       pos = p > 0.0 ? (pos | (1u << k)) : (pos & ~(1u << k));
     }
   }

@@ -442,9 +442,12 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
       f.codes[row0 + i] = x;
     }
   } else {
-    // the planes are staged in the scratch area (free until the member lists)
-    static_assert(sizeof(sh.scratch) >= 64 * D * sizeof(float), "plane staging");
-    float* sp = reinterpret_cast<float*>(sh.scratch);
+    // the planes are staged in the assignment and scratch areas (adjacent,
+    // both unused until the hashing ends)
+    static_assert(offsetof(KmShared, scratch) == offsetof(KmShared, assign) + sizeof(sh.assign) &&
+                      sizeof(sh.assign) + sizeof(sh.scratch) >= 64 * kPlaneRow<D> * sizeof(float),
+                  "plane staging");
+    float* sp = reinterpret_cast<float*>(sh.assign);
     const float* ph = f.planes + static_cast<size_t>(u % f.heads) * n_bits * D;
     stage_planes<D>(ph, n_bits, sp, tid, kKmThreads);
     __syncthreads();
@@ -462,6 +465,7 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
         f.codes[row0 + r0 + lane] = code;
       }
     }
+    __syncthreads();  // every wave is done with the staged planes
   }
   for (int i = tid; i < n; i += kKmThreads) sh.assign[i] = -1;
   for (int x = tid; x < kCmax * kCntStride; x += kKmThreads) sh.cnt[x] = 0;
