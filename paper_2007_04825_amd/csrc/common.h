@@ -11,6 +11,13 @@ typedef double v4d __attribute__((ext_vector_type(4)));
 
 constexpr int kWave = 64;
 
+// Makes the LDS writes of this wave visible to its other lanes.
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 // ---------------------------------------------------------------------------
 // Element types.  bf16 is carried as raw uint16_t storage.
 // ---------------------------------------------------------------------------

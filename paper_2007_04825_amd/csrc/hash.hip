@@ -47,11 +47,13 @@ __global__ __launch_bounds__(kHashThreads) __attribute__((amdgpu_waves_per_eu(4)
   const int nq = min(kHashQB, n - q0);
   if (nq <= 0) return;  // uniform over the workgroup
   __shared__ __align__(16) float sp[64 * kPlaneRow<D>];
+  __shared__ __align__(16) float stash[kHashThreads / 64][16 * kPlaneRow<D>];  // per-wave query tile
+  __shared__ __align__(16) float sthr[kHashThreads / 64][64];                   // per-wave plane thresholds
   const float* ph = planes + static_cast<size_t>(h) * n_bits * D;
   stage_planes<D>(ph, n_bits, sp, tid, kHashThreads);
   __syncthreads();
   PlaneOps<D> P;
-  const bool exact_all = load_plane_ops<D>(sp, n_bits, lane, P);
+  const bool exact_all = load_plane_ops<D>(sp, n_bits, lane, P, sthr[wave]);
   const T* qu = q + static_cast<size_t>(u) * N * D;
   const int ntile = (nq + 15) / 16;
   constexpr int kStep = kHashThreads / 64;
@@ -61,7 +63,7 @@ __global__ __launch_bounds__(kHashThreads) __attribute__((amdgpu_waves_per_eu(4)
     const TileRaw<D, T> cur = nxt;
     const int t2 = tile + kStep;
     if (t2 < ntile) nxt = load_tile<D, T>(qu, q0 + t2 * 16, min(16, n - q0 - t2 * 16), lane);
-    const uint64_t code = hash_tile<D, T>(qu, cur, r0, min(16, n - r0), sp, n_bits, P, exact_all, lane);
+    const uint64_t code = hash_tile<D, T>(qu, cur, r0, min(16, n - r0), sp, n_bits, P, exact_all, lane, stash[wave]);
     if (lane < 16 && r0 + lane < n) cu[r0 + lane] = code;
   }
 }

@@ -7,17 +7,20 @@
 //
 // Fast path.  The planes are bf16 values (the hash draws them that way), and an
 // fp32 query value splits exactly into three bf16 parts x = hi + mid + lo
-// (truncation: 8 + 8 + 8 significant bits).  v_mfma_f32_16x16x32_bf16 forms
-// the products exactly and accumulates in fp32, so the result S obeys
-//     |S - Q . P| <= 3d * 2^-24 * (1 + 2^-6) * sum_t |Q_t P_t|
-//                <= 2^-16.3 * |Q| |P|            (d <= 64, Cauchy-Schwarz),
-// and a bf16 part flushed as a denormal adds at most 2^-16 * |Q| |P| more.
-// Every sign with |S| > 2^-14 * |Q| |P| is therefore the exact sign; the
-// projections inside that band (about 1e-4 of them for Gaussian data) are
-// recomputed by their lane as the sequential fp64 fma chain, which reproduces
-// the definition bit for bit.  Norms too small or too large for the fp32 test
-// send the projection to the fp64 chain as well.  bf16 queries need only the
-// hi part.
+// (truncation: 8 + 8 + 8 significant bits); a bf16 query value is its own hi
+// part.  v_mfma_f32_16x16x32_bf16 forms the products exactly and accumulates
+// them in fp32, so the result S of m = 3d (fp32) or m = d (bf16) exact terms
+// obeys, with unit roundoff u = 2^-24 (2^-23 if the accumulation truncated),
+//     |S - Q . P| <= m u (1 + 2^-7) sum_t |Q_t P_t| <= m u (1 + 2^-7) |Q| |P|
+// by Cauchy-Schwarz: at most 2^-16.4 |Q| |P| (fp32, d <= 64; 2^-15.4 under
+// truncation) and 2^-18 |Q| |P| (bf16; 2^-17 under truncation).  Parts and
+// products below the fp32 normal range, flushed to zero, change S by less
+// than 2^-120 |P|, negligible once |Q|^2 >= 2^-45 (checked).  Every sign with
+// |S| above the band, 2^-14 |Q| |P| (fp32) or 2^-16 |Q| |P| (bf16), is
+// therefore the exact sign; the projections inside it (about 4e-4 and 1e-4 of
+// them for Gaussian data) are recomputed by their lane as the sequential fp64
+// fma chain, which reproduces the definition bit for bit.  Norms too small or
+// too large for the fp32 test send the projection to the fp64 chain as well.
 //
 // Planes that are not bf16 values make every projection take the fp64 chain
 // (correct, slower).
@@ -33,13 +36,15 @@
 namespace ca {
 
 
-// A operands of the 64 plane rows (four 16-plane tiles) for D/32 k-chunks,
-// and, for the planes whose signs this lane receives (16 pt + 4 (lane / 16) +
-// r), 2^-28 |P|^2 and whether they exist (bit 4 pt + r).
+// A operands of the 64 plane rows (four 16-plane tiles) for D/32 k-chunks;
+// thr: |P_b|^2 for b = 0..63 in LDS (read per tile, so that the
+// sixteen values a lane needs do not occupy registers across the tile loop);
+// valid: for the planes whose signs this lane receives (16 pt + 4 (lane /
+// 16) + r), whether they exist (bit 4 pt + r).
 template <int D>
 struct PlaneOps {
   v4u b[D / 32][4];
-  float thr[4][4];
+  const float* thr;
   uint32_t valid;
   bool norms_ok;  // every plane norm within the range of the fp32 test
 };
@@ -66,9 +71,11 @@ __device__ __forceinline__ void stage_planes(const float* __restrict__ ph, int n
 
 // Builds this lane's plane operands from the staged planes sp[64][kPlaneRow<D>].  The
 // lanes of a wave read every plane value between them; returns true (in every
-// lane) if one of them is not a bf16 value.
+// lane) if one of them is not a bf16 value.  thr: 64 floats of LDS private to
+// the wave, which receive the plane thresholds.
 template <int D>
-__device__ __forceinline__ bool load_plane_ops(const float* sp, int n_bits, int lane, PlaneOps<D>& P) {
+__device__ __forceinline__ bool load_plane_ops(const float* sp, int n_bits, int lane, PlaneOps<D>& P,
+                                               float* thr) {
   const int c = lane & 15, g = lane >> 4;
   uint32_t low = 0;
   float sq[4] = {0.f, 0.f, 0.f, 0.f};
@@ -101,13 +108,13 @@ __device__ __forceinline__ bool load_plane_ops(const float* sp, int n_bits, int 
   for (int pt = 0; pt < 4; ++pt) {
     const float n2 = cross_rows_sum(sq[pt]);  // |P|^2 of plane 16 pt + lane % 16
     if (pt * 16 + c < n_bits) ok = ok && n2 >= 0x1p-45f && n2 < 0x1p+50f;
+    if (g == 0) thr[pt * 16 + c] = n2;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int src = 4 * g + r;  // lane holding plane 16 pt + 4 g + r
-      P.thr[pt][r] = 0x1p-28f * __shfl(n2, src);
-      if (pt * 16 + src < n_bits) P.valid |= 1u << (4 * pt + r);
-    }
+    for (int r = 0; r < 4; ++r)
+      if (pt * 16 + 4 * g + r < n_bits) P.valid |= 1u << (4 * pt + r);
   }
+  wave_lds_sync();
+  P.thr = thr;
   P.norms_ok = __ballot(!ok) == 0ull;
   return __ballot(low != 0u) != 0ull;
 }
@@ -148,6 +155,28 @@ __device__ __forceinline__ TileRaw<D, T> load_tile(const T* __restrict__ qu, int
     for (int h = 0; h < static_cast<int>(sizeof(T)) / 2; ++h)
       r.w[kc][h] = c < nq ? p[kc * (32 * static_cast<int>(sizeof(T)) / 16) + h] : make_uint4(0u, 0u, 0u, 0u);
   return r;
+}
+
+// Writes this lane's part of a loaded tile to stash[16][kPlaneRow<D>] as fp32
+// (row lane % 16), so that the exact fallback reads the query rows from LDS
+// instead of fetching them again from HBM.
+template <int D, typename T>
+__device__ __forceinline__ void stash_tile(const TileRaw<D, T>& raw, float* stash, int lane) {
+  const int c = lane & 15, g = lane >> 4;
+#pragma unroll
+  for (int kc = 0; kc < D / 32; ++kc) {
+    float* dst = stash + c * kPlaneRow<D> + kc * 32 + 8 * g;
+    if constexpr (sizeof(T) == 4) {
+      *reinterpret_cast<uint4*>(dst) = raw.w[kc][0];
+      *reinterpret_cast<uint4*>(dst + 4) = raw.w[kc][1];
+    } else {
+      const uint4 w = raw.w[kc][0];
+      *reinterpret_cast<float4*>(dst) = make_float4(__uint_as_float(w.x << 16), __uint_as_float(w.x & 0xffff0000u),
+                                                    __uint_as_float(w.y << 16), __uint_as_float(w.y & 0xffff0000u));
+      *reinterpret_cast<float4*>(dst + 4) = make_float4(__uint_as_float(w.z << 16), __uint_as_float(w.z & 0xffff0000u),
+                                                        __uint_as_float(w.w << 16), __uint_as_float(w.w & 0xffff0000u));
+    }
+  }
 }
 
 // Query operands of one k-chunk: hi / mid / lo parts, and the sum of squares
@@ -191,11 +220,12 @@ __device__ __forceinline__ QueryOps query_ops(const uint4 (&w)[1]) {
 // Code of query row0 + (lane % 16) (every lane of that column returns it).
 // qu: the unit's query rows; raw: this tile as loaded by load_tile; nq: valid
 // rows from row0 (>= 1); sp: the staged planes; exact_all: planes are not
-// bf16 values.
+// bf16 values; stash: 16 kPlaneRow<D> floats of LDS private to the wave, or
+// null (the fallback then reads the query rows from qu).
 template <int D, typename T>
 __device__ uint64_t hash_tile(const T* __restrict__ qu, const TileRaw<D, T>& raw, int row0, int nq,
                               const float* sp, int n_bits, const PlaneOps<D>& P,
-                              bool exact_all, int lane) {
+                              bool exact_all, int lane, float* stash) {
   const int c = lane & 15, g = lane >> 4;
   v4f s[4];
 #pragma unroll
@@ -217,13 +247,19 @@ __device__ uint64_t hash_tile(const T* __restrict__ qu, const TileRaw<D, T>& raw
     }
   }
   qsq = cross_rows_sum(qsq);  // |Q|^2 of query c in all four lanes of column c
+  // the square of the band's relative width (a power of two: exact)
+  constexpr float kBand2 = sizeof(T) == 4 ? 0x1p-28f : 0x1p-32f;
+  const float qband = kBand2 * qsq;
   // signs and certainties as lane bit masks, bit 4 pt + r = plane 16 pt + 4 g + r
+  v4f thr[4];
+#pragma unroll
+  for (int pt = 0; pt < 4; ++pt) thr[pt] = *reinterpret_cast<const v4f*>(P.thr + 16 * pt + 4 * g);
   uint32_t pos = 0u, sure = 0u;
 #pragma unroll
   for (int k = 15; k >= 0; --k) {
     const float sv = s[k >> 2][k & 3];
     pos = (pos << 1) | (sv > 0.0f ? 1u : 0u);
-    sure = (sure << 1) | (sv * sv > qsq * P.thr[k >> 2][k & 3] ? 1u : 0u);
+    sure = (sure << 1) | (sv * sv > qband * thr[k >> 2][k & 3] ? 1u : 0u);
   }
   const uint32_t valid = c < nq ? P.valid : 0u;
   const bool fast = !exact_all && P.norms_ok && qsq >= 0x1p-45f && qsq < 0x1p+50f;
@@ -231,14 +267,21 @@ __device__ uint64_t hash_tile(const T* __restrict__ qu, const TileRaw<D, T>& raw
   pos &= valid;
   // projections inside the band: the fp64 chain (rare, divergent)
   if (__ballot(unc != 0u) != 0ull) {
+    if (stash != nullptr) {
+      stash_tile<D, T>(raw, stash, lane);
+      wave_lds_sync();
+    }
     uint32_t m = unc;
     while (m != 0u) {
       const int k = __ffs(m) - 1;
       m &= m - 1;
-      const double p = exact_projection<D, T>(qu + static_cast<size_t>(row0 + c) * D,
-                                              sp + ((k >> 2) * 16 + 4 * g + (k & 3)) * kPlaneRow<D>);
+      const float* pr = sp + ((k >> 2) * 16 + 4 * g + (k & 3)) * kPlaneRow<D>;
+      const double p = stash != nullptr
+                           ? exact_projection<D, float>(stash + c * kPlaneRow<D>, pr)
+                           : exact_projection<D, T>(qu + static_cast<size_t>(row0 + c) * D, pr);
       pos = p > 0.0 ? (pos | (1u << k)) : (pos & ~(1u << k));
     }
+    if (stash != nullptr) wave_lds_sync();  // read before the next tile's stash
   }
   // this lane's 16 bits in place, then OR over the four lanes of the column
   uint32_t lo = ((pos & 0xfu) | ((pos & 0xf0u) << 12)) << (4 * g);

@@ -442,24 +442,26 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
       f.codes[row0 + i] = x;
     }
   } else {
-    // the planes are staged in the assignment and scratch areas (adjacent,
-    // both unused until the hashing ends)
+    // the planes and the waves' plane thresholds are staged in the assignment
+    // and scratch areas (adjacent, both unused until the hashing ends)
     static_assert(offsetof(KmShared, scratch) == offsetof(KmShared, assign) + sizeof(sh.assign) &&
-                      sizeof(sh.assign) + sizeof(sh.scratch) >= 64 * kPlaneRow<D> * sizeof(float),
+                      sizeof(sh.assign) + sizeof(sh.scratch) >=
+                          (64 * kPlaneRow<D> + 64 * kKmWaves) * sizeof(float),
                   "plane staging");
     float* sp = reinterpret_cast<float*>(sh.assign);
+    float* sthr = sp + 64 * kPlaneRow<D> + 64 * wave;
     const float* ph = f.planes + static_cast<size_t>(u % f.heads) * n_bits * D;
     stage_planes<D>(ph, n_bits, sp, tid, kKmThreads);
     __syncthreads();
     PlaneOps<D> P;
-    const bool exact_all = load_plane_ops<D>(sp, n_bits, lane, P);
+    const bool exact_all = load_plane_ops<D>(sp, n_bits, lane, P, sthr);
     TileRaw<D, T> nxt = load_tile<D, T>(qu, wave * 16, wave < nqt ? min(16, n - wave * 16) : 0, lane);
     for (int tile = wave; tile < nqt; tile += kKmWaves) {
       const int r0 = tile * 16;
       const TileRaw<D, T> cur = nxt;
       const int t2 = tile + kKmWaves;
       if (t2 < nqt) nxt = load_tile<D, T>(qu, t2 * 16, min(16, n - t2 * 16), lane);
-      const uint64_t code = hash_tile<D, T>(qu, cur, r0, min(16, n - r0), sp, n_bits, P, exact_all, lane);
+      const uint64_t code = hash_tile<D, T>(qu, cur, r0, min(16, n - r0), sp, n_bits, P, exact_all, lane, nullptr);
       if (lane < 16 && r0 + lane < n) {
         sh.codes[r0 + lane] = code;
         f.codes[row0 + r0 + lane] = code;

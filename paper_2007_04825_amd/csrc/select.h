@@ -4,13 +4,6 @@
 
 namespace ca {
 
-// Makes the LDS writes of this wave visible to its other lanes.
-__device__ __forceinline__ void wave_lds_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
 // Selects the kk positions of [0, m) with the largest keys, where
 // key(pos) = order_key(value) for a valid position and 0 for an invalid one;
 // among equal keys the smaller positions win.  Writes the chosen positions in

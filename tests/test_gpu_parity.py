@@ -359,7 +359,10 @@ def near_orthogonal_queries(w, seed=0):
 
 
 def in_band_count(w):
-    """Projections the kernels must recompute in fp64: |p| <= 2^-14 |q| |P|."""
+    """Projections the kernels must recompute in fp64: |p| <= 2^-14 |q| |P|
+    for fp32 queries, 2^-16 |q| |P| for bf16 ones (a single exact product per
+    dimension leaves a narrower rounding band)."""
+    band = 2.0 ** -14 if w.dtype == "f32" else 2.0 ** -16
     cnt = 0
     B, H = w.q.shape[:2]
     for b in range(B):
@@ -368,7 +371,7 @@ def in_band_count(w):
             qq = w.q[b, h, :n].astype(np.float64)
             pp = w.planes[h].astype(np.float64)
             pr = qq @ pp.T
-            lim = 2.0 ** -14 * np.linalg.norm(qq, axis=1)[:, None] * np.linalg.norm(pp, axis=1)[None]
+            lim = band * np.linalg.norm(qq, axis=1)[:, None] * np.linalg.norm(pp, axis=1)[None]
             cnt += int(np.sum(np.abs(pr) <= lim))
     return cnt
 
@@ -396,7 +399,7 @@ def test_hash_exact_inside_rounding_band(path, dtype, d):
     w = dataclasses.replace(base, q=near_orthogonal_queries(base), name=base.name + "_orth")
     nb = in_band_count(w)
     print("projections inside the band: %d" % nb)
-    assert nb > 100
+    assert nb > 50
     ref = oracle_codes(w)
     try:
         ca.set_kmeans_path(path)
