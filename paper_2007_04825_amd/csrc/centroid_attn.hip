@@ -326,11 +326,15 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
         make_rsrc(a.qc + (static_cast<size_t>(u) * C + j0) * D, static_cast<uint32_t>(min(16, C - j0)) * D * 4);
     buf_load<KS>(rq, (c * D + g * KS) * 4, 0, bq, float{});
   }
-  float ka[BT][KS];
-  auto load_keys = [&](int kt0) {
+  // key and value tiles come in batches of HB tiles (kt0, kt0 + NW, ...), two
+  // batches in flight: the next one is requested before the current one is used
+  constexpr int HB = BT / 2;
+  static_assert(HB % 2 == 0, "tile pairs");
+  float ka0[HB][KS], ka1[HB][KS];
+  auto load_keys = [&](int kt0, float (&ka)[HB][KS]) {
     const uint32_t voff = ((kt0 * 16 + c) * D + g * KS) * ESZ;
 #pragma unroll
-    for (int b = 0; b < BT; ++b) {
+    for (int b = 0; b < HB; ++b) {
       if (kt0 + NW * b < nkt) {  // whole tiles past the chunk are not requested
         buf_load<KS>(rk, voff, NW * b * 16 * D * ESZ, ka[b], T{});
       } else {
@@ -339,7 +343,7 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
       }
     }
   };
-  load_keys(wave);
+  load_keys(wave, ka0);
 
   // ---- sizes (fused: the member offsets of the 16 clusters) -----------------------
   if constexpr (OTOP) {
@@ -375,10 +379,9 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
     float top[NT];
 #pragma unroll
     for (int e = 0; e < NT; ++e) top[e] = -INFINITY;
-    for (int kt0 = wave; kt0 < nkt; kt0 += NW * BT) {
-      if (kt0 != wave) load_keys(kt0);  // the first batch is in flight already
+    auto key_batch = [&](int kt0, const float (&ka)[HB][KS]) {
 #pragma unroll
-      for (int b = 0; b < BT; ++b) {
+      for (int b = 0; b < HB; ++b) {
         const int kt = kt0 + NW * b;
         if (kt < nkt) {
           v4f acc = {0.f, 0.f, 0.f, 0.f};
@@ -407,6 +410,15 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
           *reinterpret_cast<float4*>(&logits[c * kLStride + kt * 16 + 4 * g]) = make_float4(o[0], o[1], o[2], o[3]);
         }
       }
+    };
+    // the first batch is in flight already
+    for (int kt0 = wave; kt0 < nkt; kt0 += 2 * NW * HB) {
+      const int kt1 = kt0 + NW * HB;
+      if (kt1 < nkt) load_keys(kt1, ka1);
+      key_batch(kt0, ka0);
+      if (kt1 >= nkt) break;
+      if (kt1 + NW * HB < nkt) load_keys(kt1 + NW * HB, ka0);
+      key_batch(kt1, ka1);
     }
     // slice (wave, g) of row c
     smax[c][wave * 4 + g] = lmax;
@@ -555,11 +567,11 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
   float psum = 0.0f;
   {
     const float mc = rowm[c];
-    for (int kt0 = wave; kt0 < nkt; kt0 += NW * BT) {
-      float va[BT][4][DT];
+    float va0[HB][4][DT], va1[HB][4][DT];
+    auto load_vals = [&](int kt0, float (&va)[HB][4][DT]) {
       const uint32_t voff = ((kt0 * 16 + 4 * g) * D + DT * c) * ESZ;
 #pragma unroll
-      for (int b = 0; b < BT; ++b)
+      for (int b = 0; b < HB; ++b)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           if (kt0 + NW * b < nkt) {
@@ -569,14 +581,15 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
             for (int dt = 0; dt < DT; ++dt) va[b][i][dt] = 0.0f;
           }
         }
+    };
+    auto value_batch = [&](int kt0, const float (&va)[HB][4][DT]) {
       if constexpr (sizeof(T) == 2 || kSplitF32) {
         // bf16 values are exact, fp32 values split into three bf16 parts like
         // P; tiles b and b + 1 of the batch form one product over 32 keys (k = 8 g + j: key
         // 4 g + j of tile b for j < 4, of tile b + 1 otherwise), a tile past
         // the row contributing P = 0
-        static_assert(BT % 2 == 0, "tile pairs");
 #pragma unroll
-        for (int b = 0; b < BT; b += 2) {
+        for (int b = 0; b < HB; b += 2) {
           if (kt0 + NW * b >= nkt) break;
           float p8[8];
 #pragma unroll
@@ -608,7 +621,7 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
         }
       } else {
 #pragma unroll
-        for (int b = 0; b < BT; ++b) {
+        for (int b = 0; b < HB; ++b) {
           const int kt = kt0 + NW * b;
           if (kt < nkt) {
             const float4 s4 = *reinterpret_cast<const float4*>(&logits[c * kLStride + kt * 16 + 4 * g]);
@@ -621,6 +634,15 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
           }
         }
       }
+    };
+    if (wave < nkt) load_vals(wave, va0);
+    for (int kt0 = wave; kt0 < nkt; kt0 += 2 * NW * HB) {
+      const int kt1 = kt0 + NW * HB;
+      if (kt1 < nkt) load_vals(kt1, va1);
+      value_batch(kt0, va0);
+      if (kt1 >= nkt) break;
+      if (kt1 + NW * HB < nkt) load_vals(kt1 + NW * HB, va0);
+      value_batch(kt1, va1);
     }
   }
   psum = cross_rows_sum(psum);
