@@ -584,8 +584,8 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
     };
     auto value_batch = [&](int kt0, const float (&va)[HB][4][DT]) {
       if constexpr (sizeof(T) == 2 || kSplitF32) {
-        // bf16 values are exact, fp32 values split into three bf16 parts like
-        // P; tiles b and b + 1 of the batch form one product over 32 keys (k = 8 g + j: key
+        // bf16 values are exact and P keeps two bf16 parts (mfma_weights);
+        // tiles b and b + 1 of the batch form one product over 32 keys (k = 8 g + j: key
         // 4 g + j of tile b for j < 4, of tile b + 1 otherwise), a tile past
         // the row contributing P = 0
 #pragma unroll
@@ -616,7 +616,7 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
               v8[i] = va[b][i][dt];
               v8[4 + i] = va[b + 1][i][dt];
             }
-            oacc[dt] = mfma_bf16x<T>(v8, ps, oacc[dt]);
+            oacc[dt] = mfma_weights<T>(v8, ps, oacc[dt]);
           }
         }
       } else {
@@ -790,11 +790,12 @@ __global__ __launch_bounds__(kFlashThreads) void attn_flash_kernel(AttnArgs a) {
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) oacc[dt] = v4f{0.f, 0.f, 0.f, 0.f};
   if constexpr (sizeof(T) == 2 || kSplitF32) {
-    // Both products on the bf16 matrix cores, with Q^c and P split into three
-    // bf16 parts each (an fp32 value is exactly the sum of its three truncated
-    // parts), so that every logit and value keeps fp32 accuracy: bf16 keys and
-    // values are exact (three part products per 32 dims or per 32 keys), fp32
-    // keys and values are split too (six part products, mfma_split6).  The k
+    // Both products on the bf16 matrix cores.  Q^c is split into three bf16
+    // parts (an fp32 value is exactly the sum of its three truncated parts), so
+    // that every logit keeps fp32 accuracy: bf16 keys are exact (three part
+    // products per 32 dims); P keeps two parts against the exact bf16 values
+    // (mfma_weights, each weight short by under 2^-15 of itself); fp32 keys
+    // and values are split too (six part products, mfma_split6).  The k
     // index of a product over dims maps to the lane's own dims g KS + 8 m + j;
     // over keys, k = 8 g + j is key 4 g + j of the block's first tile (j < 4)
     // or key 4 g + j - 4 of its second, which is where the logit results put
@@ -851,7 +852,7 @@ __global__ __launch_bounds__(kFlashThreads) void attn_flash_kernel(AttnArgs a) {
           va8[j] = vx[0][j][dt];
           va8[4 + j] = vx[1][j][dt];
         }
-        oacc[dt] = mfma_bf16x<T>(va8, ps, oacc[dt] * alpha);
+        oacc[dt] = mfma_weights<T>(va8, ps, oacc[dt] * alpha);
       }
     };
     for (int bk = wave; bk < nkb; bk += NW) {
@@ -1266,7 +1267,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kSparseMinW
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) oacc[dt] = v4f{0.f, 0.f, 0.f, 0.f};
     if constexpr (sizeof(T) == 2) {
-      // exact bf16 values, P split into three bf16 parts; slots of tiles kt and
+      // exact bf16 values, P in two bf16 parts (mfma_weights); slots of tiles kt and
       // kt + 1 form one product over 32 (k = 8 g + j: slot 4 g + j of tile kt
       // for j < 4, of tile kt + 1 otherwise); a missing tile contributes 0
 #pragma unroll
@@ -1286,7 +1287,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kSparseMinW
             v8[i] = vf[kt][i][dt];
             v8[4 + i] = kt + 1 < NKT ? vf[min(kt + 1, NKT - 1)][i][dt] : 0.0f;
           }
-          oacc[dt] = mfma_split3(pack_bf16x8(v8), ps, oacc[dt]);
+          oacc[dt] = mfma_weights<bf16_t>(v8, ps, oacc[dt]);
         }
       }
     } else {

@@ -260,6 +260,21 @@ __device__ __forceinline__ v4f mfma_split6(const Split8& a, const Split8& b, v4f
   c = mfma_bf16_16x16x32(a.h, b.h, c);
   return c;
 }
+// Softmax weights P in (0, 1] times bf16 values: P keeps its hi and mid parts
+// (16 significant bits, each weight short by less than 2^-15 of itself), two
+// products; far below the bf16 rounding of the outputs, and the normalisers
+// are summed from the unsplit weights.  fp32 values take the six products of
+// mfma_split6.
+template <typename T>
+__device__ __forceinline__ v4f mfma_weights(const float* x8, const Split8& p, v4f c) {
+  if constexpr (sizeof(T) == 2) {
+    const v4u a = pack_bf16x8(x8);
+    c = mfma_bf16_16x16x32(a, p.m, c);
+    return mfma_bf16_16x16x32(a, p.h, c);
+  } else {
+    return mfma_split6(split8(x8), p, c);
+  }
+}
 // Eight values of the element type T (widened to fp32) times a split B on
 // the bf16 matrix cores: bf16 values are exact as one operand (three
 // products), fp32 values are split as well (six products).
