@@ -133,8 +133,17 @@ __global__ __launch_bounds__(256) void centroid_final_kernel(const double* __res
   if (item >= nitems) return;
   const int sz = sizes[item];
   const double* pp = qc_part + static_cast<size_t>(item) * nwg * D + t;
+  // the parts in block order, eight loads in flight ahead of the additions
   double acc = 0.0;
-  for (int b = 0; b < nwg; ++b) acc += pp[static_cast<size_t>(b) * D];
+  int b = 0;
+  for (; b + 8 <= nwg; b += 8) {
+    double x[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x[e] = pp[static_cast<size_t>(b + e) * D];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc += x[e];
+  }
+  for (; b < nwg; ++b) acc += pp[static_cast<size_t>(b) * D];
   qc[static_cast<size_t>(item) * D + t] = sz > 0 ? static_cast<float>(acc / static_cast<double>(sz)) : 0.0f;
 }
 
