@@ -47,18 +47,23 @@ def test_stage_work_closed_forms():
         bench.stage_work(w, "nonsense", 0)
 
 
-def test_counter_profile_is_withheld_when_sources_change(monkeypatch):
-    path = os.path.join(ROOT, "profiles", "speech_b32h6n800_d32_f32_hbm_counters.json")
+@pytest.mark.parametrize("profile", ["speech_b32h6n800_d32_f32", "sweep_b1h8n32768_d64_f32",
+                                     "long_b1h8n65536_d64_bf16"])
+def test_counter_profile_is_withheld_when_sources_change(monkeypatch, profile):
+    """Each committed counter profile holds the key of the bench line's
+    roofline kernel (the i-clustered tile kernel), and the bench reports it
+    only while the kernel sources hash to the recorded value."""
+    path = os.path.join(ROOT, "profiles", profile + "_hbm_counters.json")
     with open(path) as f:
         prof = json.load(f)
-    key = "centroid_attn (iclustered)"
+    key = "attn_tile (iclustered)"
     assert prof["kernels"][key]["hbm_bytes_per_launch"] > 0
     monkeypatch.setattr(bench, "kernel_source_hash", lambda: prof["source_sha256"])
-    assert bench.measured_traffic(key) == prof["kernels"][key]["hbm_bytes_per_launch"]
-    assert bench.measured_traffic("no such kernel") is None
+    assert bench.measured_traffic(key, profile) == prof["kernels"][key]["hbm_bytes_per_launch"]
+    assert bench.measured_traffic("no such kernel", profile) is None
     assert bench.measured_traffic(key, "no_such_workload") is None
     monkeypatch.setattr(bench, "kernel_source_hash", lambda: "0" * 64)
-    assert bench.measured_traffic(key) is None
+    assert bench.measured_traffic(key, profile) is None
 
 
 def test_kernel_source_hash_is_stable():
