@@ -10,10 +10,14 @@ Inputs are seeded synthetic data already resident in HBM.
 
 Prints one JSON line.  value = queries answered per second, counting each
 valid (sequence, head, position) once per variant.  The roofline entry times
-the dominant kernel with HIP events recorded by the library around it on the
-call's stream, in every eighth timed step; "phases" gives every stage's
-achieved rate against its bound; the cpu_baseline entry times the fp64 oracle
-on the host's cores on the same workload.
+the largest kernel among the hash, centroid-attention and output stages (the
+centroid GEMMs of the improved call on the default workload) with HIP events
+recorded by the library around it on the call's stream, in every eighth timed
+step; the K-means stage, whose time is set by its dependent rounds rather
+than by a roofline, is left to "phases" unless --stage kmeans asks for it.
+"phases" gives every stage's achieved rate against its bound; the
+cpu_baseline entry times the fp64 oracle on the host's cores on the same
+workload.
 """
 from __future__ import annotations
 
@@ -662,7 +666,8 @@ def bench_forward(args, w, desc):
     the whole batch of workload w (inputs resident in HBM).  Prints the
     headline JSON line: value = valid queries answered per second (each
     variant counted), over exactly args.steps back-to-back steps between two
-    events; the roofline entry of the dominant kernel, timed with event pairs
+    events; the roofline entry of the largest hash, tile or output kernel
+    (the K-means with --stage kmeans), timed with event pairs
     that the library records around it on the call's stream in every eighth
     timed step; every stage's achieved rate; the per-step median of separately
     timed steps; and the fp64 oracle on the host's cores."""
@@ -725,9 +730,10 @@ def bench_forward(args, w, desc):
         step()
     torch.cuda.synchronize()
     st = stage_times()
-    # the dominant kernel: the largest single-kernel stage (the K-means and
-    # centroid stages may hold several kernels, the centroid-attention stage
-    # the tile kernel and a merge)
+    # the roofline kernel: the largest of the single-kernel hash, tile and
+    # output stages (the centroid stage may hold two kernels and the
+    # centroid-attention stage a tile kernel and a merge; the K-means, bound
+    # by its dependent rounds, only when asked for)
     single = [key for key in st if key[0] in ("hash", "attn_tile", "output")
               or (key[0] == "kmeans" and args.stage == "kmeans")]
     if args.stage == "auto":
