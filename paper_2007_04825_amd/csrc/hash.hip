@@ -50,15 +50,23 @@ __global__ __launch_bounds__(kHashThreads) __attribute__((amdgpu_waves_per_eu(4)
   __shared__ __align__(16) float stash[kHashThreads / 64][16 * kPlaneRow<D>];  // per-wave query tile
   __shared__ __align__(16) float sthr[kHashThreads / 64][64];                   // per-wave plane thresholds
   const float* ph = planes + static_cast<size_t>(h) * n_bits * D;
-  stage_planes<D>(ph, n_bits, sp, tid, kHashThreads);
-  __syncthreads();
-  PlaneOps<D> P;
-  const bool exact_all = load_plane_ops<D>(sp, n_bits, lane, P, sthr[wave]);
   const T* qu = q + static_cast<size_t>(u) * N * D;
   const int ntile = (nq + 15) / 16;
   constexpr int kStep = kHashThreads / 64;
-  TileRaw<D, T> nxt = load_tile<D, T>(qu, q0 + wave * 16, wave < ntile ? min(16, n - q0 - wave * 16) : 0, lane);
-  for (int tile = wave; tile < ntile; tile += kStep) {
+  // planes requested, then the first query tile, which stays in flight while
+  // the planes go to LDS
+  // (the scheduling barriers keep that order of the loads)
+  PlaneStage<D, kHashThreads> stage;
+  fetch_planes<D, kHashThreads>(ph, n_bits, stage, tid);
+  __builtin_amdgcn_sched_barrier(0);
+  const int wu = __builtin_amdgcn_readfirstlane(wave);  // uniform: the tile's buffer resource in scalars
+  TileRaw<D, T> nxt = load_tile<D, T>(qu, q0 + wu * 16, wu < ntile ? min(16, n - q0 - wu * 16) : 0, lane);
+  __builtin_amdgcn_sched_barrier(0);
+  store_planes<D, kHashThreads>(stage, sp, tid);
+  __syncthreads();
+  PlaneOps<D> P;
+  const bool exact_all = load_plane_ops<D>(sp, n_bits, lane, P, sthr[wave]);
+  for (int tile = wu; tile < ntile; tile += kStep) {
     const int r0 = q0 + tile * 16;
     const TileRaw<D, T> cur = nxt;
     const int t2 = tile + kStep;

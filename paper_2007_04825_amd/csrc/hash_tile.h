@@ -54,18 +54,44 @@ struct PlaneOps {
 template <int D>
 constexpr int kPlaneRow = D + 4;
 
-// Copies the n_bits planes of one head [n_bits][D] into sp[64][kPlaneRow<D>]
-// (LDS; rows past n_bits are zero) with the threads of the workgroup, so that
-// the waves read their operands from LDS instead of all fetching the same few
-// kilobytes from L2.  The caller synchronises the workgroup before sp is read.
-template <int D>
-__device__ __forceinline__ void stage_planes(const float* __restrict__ ph, int n_bits, float* sp,
-                                             int tid, int nthreads) {
-  for (int x = tid; x < 64 * D / 4; x += nthreads) {
-    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (x * 4 < n_bits * D) v = *reinterpret_cast<const float4*>(ph + x * 4);
-    const int row = x / (D / 4), col = 4 * (x % (D / 4));
-    *reinterpret_cast<float4*>(sp + row * kPlaneRow<D> + col) = v;
+// The n_bits planes of one head [n_bits][D] are copied into
+// sp[64][kPlaneRow<D>] (LDS; rows past n_bits are zero) by the NT threads of
+// the workgroup, so that the waves read their operands from LDS instead of
+// all fetching the same few kilobytes from L2.  The copy is split in two:
+// fetch_planes requests this thread's part, store_planes writes it to LDS.
+// Loads issued in between (the first query tile) stay in flight while the
+// stores wait for the planes alone.  The caller synchronises the workgroup
+// before sp is read.
+template <int D, int NT>
+struct PlaneStage {
+  static constexpr int kPer = (64 * D / 4 + NT - 1) / NT;  // float4 per thread
+  float4 v[kPer];
+};
+template <int D, int NT>
+__device__ __forceinline__ void fetch_planes(const float* __restrict__ ph, int n_bits,
+                                             PlaneStage<D, NT>& st, int tid) {
+  // through a buffer resource: every load is issued without a branch (so
+  // that the compiler counts them), positions past the planes reading 0
+  const __amdgpu_buffer_rsrc_t rp = make_rsrc(ph, static_cast<uint32_t>(n_bits) * D * 4);
+#pragma unroll
+  for (int i = 0; i < PlaneStage<D, NT>::kPer; ++i) {
+    const int x = tid + i * NT;
+    const auto t = __builtin_amdgcn_raw_buffer_load_b128(rp, static_cast<uint32_t>(x) * 16, 0, 0);
+    st.v[i] = make_float4(__uint_as_float(t[0]), __uint_as_float(t[1]), __uint_as_float(t[2]), __uint_as_float(t[3]));
+  }
+}
+template <int D, int NT>
+__device__ __forceinline__ void store_planes(const PlaneStage<D, NT>& st, float* sp, int tid) {
+  // with NT * kPer = 64 D / 4 every thread stores all of its parts (no branch
+  // for the compiler to sink the loads into)
+  constexpr bool kExact = NT * PlaneStage<D, NT>::kPer == 64 * D / 4;
+#pragma unroll
+  for (int i = 0; i < PlaneStage<D, NT>::kPer; ++i) {
+    const int x = tid + i * NT;
+    if (kExact || x < 64 * D / 4) {
+      const int row = x / (D / 4), col = 4 * (x % (D / 4));
+      *reinterpret_cast<float4*>(sp + row * kPlaneRow<D> + col) = st.v[i];
+    }
   }
 }
 
@@ -138,7 +164,10 @@ __device__ __forceinline__ double exact_projection(const T* __restrict__ qr, con
 
 // Raw query values of one tile as this lane loads them: row row0 + lane % 16,
 // dimensions kc * 32 + 8 (lane / 16) .. + 7 for each k-chunk kc (the next tile
-// is requested while the current one is on the matrix cores).
+// is requested while the current one is on the matrix cores).  The loads go
+// through a buffer resource over the nq valid rows: every load is issued
+// without a branch (so that the compiler counts the loads in flight), and
+// rows past nq read 0.
 template <int D, typename T>
 struct TileRaw {
   uint4 w[D / 32][sizeof(T) / 2];  // 8 values: two uint4 of fp32, or one of bf16
@@ -147,13 +176,18 @@ template <int D, typename T>
 __device__ __forceinline__ TileRaw<D, T> load_tile(const T* __restrict__ qu, int row0, int nq,
                                                    int lane) {
   const int c = lane & 15, g = lane >> 4;
+  constexpr uint32_t ESZ = sizeof(T);
+  const __amdgpu_buffer_rsrc_t rq =
+      make_rsrc(qu + static_cast<size_t>(nq > 0 ? row0 : 0) * D, static_cast<uint32_t>(nq > 0 ? nq : 0) * D * ESZ);
   TileRaw<D, T> r;
-  const uint4* p = reinterpret_cast<const uint4*>(qu + static_cast<size_t>(row0 + c) * D + 8 * g);
 #pragma unroll
   for (int kc = 0; kc < D / 32; ++kc)
 #pragma unroll
-    for (int h = 0; h < static_cast<int>(sizeof(T)) / 2; ++h)
-      r.w[kc][h] = c < nq ? p[kc * (32 * static_cast<int>(sizeof(T)) / 16) + h] : make_uint4(0u, 0u, 0u, 0u);
+    for (int h = 0; h < static_cast<int>(ESZ) / 2; ++h) {
+      const uint32_t voff = (static_cast<uint32_t>(c) * D + 8 * g + 32 * kc) * ESZ + 16 * h;
+      const auto t = __builtin_amdgcn_raw_buffer_load_b128(rq, voff, 0, 0);
+      r.w[kc][h] = make_uint4(t[0], t[1], t[2], t[3]);
+    }
   return r;
 }
 

@@ -451,12 +451,20 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
     float* sp = reinterpret_cast<float*>(sh.assign);
     float* sthr = sp + 64 * kPlaneRow<D> + 64 * wave;
     const float* ph = f.planes + static_cast<size_t>(u % f.heads) * n_bits * D;
-    stage_planes<D>(ph, n_bits, sp, tid, kKmThreads);
+    // planes requested, then the first query tile, which stays in flight
+    // while the planes go to LDS
+    // (the scheduling barriers keep that order of the loads)
+    PlaneStage<D, kKmThreads> stage;
+    fetch_planes<D, kKmThreads>(ph, n_bits, stage, tid);
+    __builtin_amdgcn_sched_barrier(0);
+    const int wu = __builtin_amdgcn_readfirstlane(wave);  // uniform: the tile's buffer resource in scalars
+    TileRaw<D, T> nxt = load_tile<D, T>(qu, wu * 16, wu < nqt ? min(16, n - wu * 16) : 0, lane);
+    __builtin_amdgcn_sched_barrier(0);
+    store_planes<D, kKmThreads>(stage, sp, tid);
     __syncthreads();
     PlaneOps<D> P;
     const bool exact_all = load_plane_ops<D>(sp, n_bits, lane, P, sthr);
-    TileRaw<D, T> nxt = load_tile<D, T>(qu, wave * 16, wave < nqt ? min(16, n - wave * 16) : 0, lane);
-    for (int tile = wave; tile < nqt; tile += kKmWaves) {
+    for (int tile = wu; tile < nqt; tile += kKmWaves) {
       const int r0 = tile * 16;
       const TileRaw<D, T> cur = nxt;
       const int t2 = tile + kKmWaves;
