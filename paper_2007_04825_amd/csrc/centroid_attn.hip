@@ -336,21 +336,18 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
     buf_load<KS>(rq, (c * D + g * KS) * 4, 0, bq, float{});
   }
   // key and value tiles come in batches of HB tiles (kt0, kt0 + NW, ...), two
-  // batches in flight: the next one is requested before the current one is used
+  // batches in flight: the next one is requested before the current one is
+  // used.  Every load is issued without a branch (tiles past the chunk read 0
+  // through the buffer resource and cost no memory traffic), so that the
+  // compiler knows how many loads are in flight and waits for the current
+  // batch alone.
   constexpr int HB = BT / 2;
   static_assert(HB % 2 == 0, "tile pairs");
   float ka0[HB][KS], ka1[HB][KS];
   auto load_keys = [&](int kt0, float (&ka)[HB][KS]) {
     const uint32_t voff = ((kt0 * 16 + c) * D + g * KS) * ESZ;
 #pragma unroll
-    for (int b = 0; b < HB; ++b) {
-      if (kt0 + NW * b < nkt) {  // whole tiles past the chunk are not requested
-        buf_load<KS>(rk, voff, NW * b * 16 * D * ESZ, ka[b], T{});
-      } else {
-#pragma unroll
-        for (int s = 0; s < KS; ++s) ka[b][s] = 0.0f;
-      }
-    }
+    for (int b = 0; b < HB; ++b) buf_load<KS>(rk, voff, NW * b * 16 * D * ESZ, ka[b], T{});
   };
   load_keys(wave, ka0);
 
@@ -423,10 +420,10 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
     // the first batch is in flight already
     for (int kt0 = wave; kt0 < nkt; kt0 += 2 * NW * HB) {
       const int kt1 = kt0 + NW * HB;
-      if (kt1 < nkt) load_keys(kt1, ka1);
+      load_keys(kt1, ka1);
       key_batch(kt0, ka0);
       if (kt1 >= nkt) break;
-      if (kt1 + NW * HB < nkt) load_keys(kt1 + NW * HB, ka0);
+      load_keys(kt1 + NW * HB, ka0);
       key_batch(kt1, ka1);
     }
     // slice (wave, g) of row c
@@ -582,14 +579,7 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
 #pragma unroll
       for (int b = 0; b < HB; ++b)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          if (kt0 + NW * b < nkt) {
-            buf_load<DT>(rv, voff, (NW * b * 16 + i) * D * ESZ, va[b][i], T{});
-          } else {
-#pragma unroll
-            for (int dt = 0; dt < DT; ++dt) va[b][i][dt] = 0.0f;
-          }
-        }
+        for (int i = 0; i < 4; ++i) buf_load<DT>(rv, voff, (NW * b * 16 + i) * D * ESZ, va[b][i], T{});
     };
     auto value_batch = [&](int kt0, const float (&va)[HB][4][DT]) {
       if constexpr (sizeof(T) == 2 || kSplitF32) {
@@ -644,13 +634,13 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
         }
       }
     };
-    if (wave < nkt) load_vals(wave, va0);
+    load_vals(wave, va0);
     for (int kt0 = wave; kt0 < nkt; kt0 += 2 * NW * HB) {
       const int kt1 = kt0 + NW * HB;
-      if (kt1 < nkt) load_vals(kt1, va1);
+      load_vals(kt1, va1);
       value_batch(kt0, va0);
       if (kt1 >= nkt) break;
-      if (kt1 + NW * HB < nkt) load_vals(kt1 + NW * HB, va0);
+      load_vals(kt1 + NW * HB, va0);
       value_batch(kt1, va1);
     }
   }
