@@ -343,6 +343,10 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
   // batch alone.
   constexpr int HB = BT / 2;
   static_assert(HB % 2 == 0, "tile pairs");
+  // batches of a wave over a whole chunk: the loops below run this many,
+  // unrolled into straight-line code, tiles past the chunk computing nothing
+  constexpr int NB = kChunk / 16 / NW / HB;
+  static_assert(NB % 2 == 0 && NB * HB * NW * 16 == kChunk, "batch pairs cover the chunk");
   float ka0[HB][KS], ka1[HB][KS];
   auto load_keys = [&](int kt0, float (&ka)[HB][KS]) {
     const uint32_t voff = ((kt0 * 16 + c) * D + g * KS) * ESZ;
@@ -418,12 +422,12 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
       }
     };
     // the first batch is in flight already
-    for (int kt0 = wave; kt0 < nkt; kt0 += 2 * NW * HB) {
-      const int kt1 = kt0 + NW * HB;
+#pragma unroll
+    for (int bb = 0; bb < NB; bb += 2) {
+      const int kt0 = wave + bb * NW * HB, kt1 = kt0 + NW * HB;
       load_keys(kt1, ka1);
       key_batch(kt0, ka0);
-      if (kt1 >= nkt) break;
-      load_keys(kt1 + NW * HB, ka0);
+      if (bb + 2 < NB) load_keys(kt1 + NW * HB, ka0);
       key_batch(kt1, ka1);
     }
     // slice (wave, g) of row c
@@ -635,12 +639,12 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
       }
     };
     load_vals(wave, va0);
-    for (int kt0 = wave; kt0 < nkt; kt0 += 2 * NW * HB) {
-      const int kt1 = kt0 + NW * HB;
+#pragma unroll
+    for (int bb = 0; bb < NB; bb += 2) {
+      const int kt0 = wave + bb * NW * HB, kt1 = kt0 + NW * HB;
       load_vals(kt1, va1);
       value_batch(kt0, va0);
-      if (kt1 >= nkt) break;
-      load_vals(kt1 + NW * HB, va0);
+      if (bb + 2 < NB) load_vals(kt1 + NW * HB, va0);
       value_batch(kt1, va1);
     }
   }
