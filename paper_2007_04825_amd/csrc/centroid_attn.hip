@@ -1116,10 +1116,15 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
 // ---------------------------------------------------------------------------
 // Register budgets that fit without spills and measured faster than the
 // unconstrained allocation: seven waves per SIMD for d = 32 with k <= 32 (69
-// registers in fp32, against six waves), six for bf16 d = 64 with k <= 32
-// (against five)
+// registers in fp32, against six waves), five for bf16 d = 64 with k <= 32
+// (the next member tile's rows take registers of their own)
 template <int D, typename T, int NKT>
-constexpr int kSparseMinWaves = (D == 32 && NKT <= 2) ? 7 : (D == 64 && NKT == 2 && sizeof(T) == 2) ? 6 : 1;
+constexpr int kSparseMinWaves = (D == 32 && NKT <= 2) ? 7 : (D == 64 && NKT == 2 && sizeof(T) == 2) ? 5 : 1;
+// d = 64: the next member tile's query rows are requested before the current
+// tile goes through the products (d = 32 measured faster with the seven waves
+// per SIMD that the registers of a second tile would cost)
+template <int D>
+constexpr bool kSparsePrefetch = D == 64;
 template <int D, typename T, int NKT>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kSparseMinWaves<D, T, NKT>))) void sparse_kernel(AttnArgs a) {
   constexpr int KS = D / 4, DT = D / 16;
@@ -1223,13 +1228,24 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kSparseMinW
   auto qoff = [&](int row) { return row >= 0 ? static_cast<uint32_t>(row) * D * ESZ + g * KS * ESZ : kNone; };
 
   // ---- load step 3: member rows of Q, one tile of 16 at a time --------------------
-  // (most items have one tile; a later tile's rows are requested when it starts)
+  // The member indices two tiles ahead are requested first and (d = 64) the
+  // next tile's rows before the current tile goes through the products; every
+  // load is issued without a branch (past the item's members they read 0
+  // through their buffer resources), so that each waits for itself alone.
+  const __amdgpu_buffer_rsrc_t rm = make_rsrc(mem, static_cast<uint32_t>(sz) * 4);
+  constexpr bool PF = kSparsePrefetch<D>;
   float bq[KS];
+  if constexpr (PF) buf_load<KS>(rq, qoff(row0), 0, bq, T{});
   for (int mt = 0; mt < sz; mt += 16) {
     const bool more = mt + 16 < sz;
-    buf_load<KS>(rq, qoff(row0), 0, bq, T{});
-    int row2 = -1;
-    if (more) row2 = mt + 32 + c < sz ? mem[mt + 32 + c] : -1;
+    float bqn[PF ? KS : 1];
+    if constexpr (PF)
+      buf_load<KS>(rq, qoff(more ? row1 : -1), 0, bqn, T{});
+    else
+      buf_load<KS>(rq, qoff(row0), 0, bq, T{});
+    const int m2 = mt + 32 + c;
+    const int r2 = static_cast<int>(__builtin_amdgcn_raw_buffer_load_b32(rm, static_cast<uint32_t>(m2) * 4, 0, 0));
+    const int row2 = m2 < sz ? r2 : -1;
     v4f sacc[NKT];
     float mx = -INFINITY;
 #pragma unroll
@@ -1314,6 +1330,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kSparseMinW
     buf_store<4 * DT>(ro, row0 >= 0 ? static_cast<uint32_t>(row0) * D * ESZ + DT * 4 * g * ESZ : kNone, 0, o, T{});
     row0 = row1;
     row1 = row2;
+    if constexpr (PF) {
+#pragma unroll
+      for (int s = 0; s < KS; ++s) bq[s] = bqn[s];
+    }
   }
 }
 
