@@ -322,8 +322,17 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
   const __amdgpu_buffer_rsrc_t rk = make_rsrc(ku, static_cast<uint32_t>(kn) * D * ESZ);
   const __amdgpu_buffer_rsrc_t rv = make_rsrc(vu, static_cast<uint32_t>(kn) * D * ESZ);
 
-  // the rows of this tile and the first batch of key tiles do not depend on
-  // the cluster sizes: they are requested first, so that the latencies overlap
+  // the tile's cluster sizes (or member offsets) are requested first, by
+  // every thread and without a branch, so that waiting for them leaves the
+  // rows of this tile and the first batch of key tiles, requested next, in
+  // flight
+  int pre = 0;
+  if constexpr (OTOP) {
+  } else if constexpr (FUSED) {
+    pre = a.offsets[static_cast<size_t>(u) * (C + 1) + min(j0 + min(tid, 16), C)];
+  } else {
+    pre = a.sizes[static_cast<size_t>(u) * C + min(j0 + (tid & 15), C - 1)];
+  }
   float bq[KS];
   if constexpr (OTOP) {  // the query rows j0 .. j0 + 15 (rows past n read as 0)
     const __amdgpu_buffer_rsrc_t rq =
@@ -358,8 +367,7 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
   // ---- sizes (fused: the member offsets of the 16 clusters) -----------------------
   if constexpr (OTOP) {
   } else if constexpr (FUSED) {
-    const int32_t* ou = a.offsets + static_cast<size_t>(u) * (C + 1);
-    if (tid < 17) moff[tid] = ou[min(j0 + tid, C)];
+    if (tid < 17) moff[tid] = pre;
     __syncthreads();
     if (moff[16] == moff[0]) {  // every cluster of the tile is empty
       export_empty_tile();
@@ -368,7 +376,7 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
   } else {
     if (tid == 0) any_nonempty = 0;
     __syncthreads();
-    if (tid < 16 && j0 + tid < C && a.sizes[static_cast<size_t>(u) * C + j0 + tid] > 0) any_nonempty = 1;
+    if (tid < 16 && j0 + tid < C && pre > 0) any_nonempty = 1;
     __syncthreads();
     if (!any_nonempty) return;
   }

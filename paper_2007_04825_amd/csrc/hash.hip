@@ -70,7 +70,9 @@ __global__ __launch_bounds__(kHashThreads) __attribute__((amdgpu_waves_per_eu(4)
     const int r0 = q0 + tile * 16;
     const TileRaw<D, T> cur = nxt;
     const int t2 = tile + kStep;
-    if (t2 < ntile) nxt = load_tile<D, T>(qu, q0 + t2 * 16, min(16, n - q0 - t2 * 16), lane);
+    // issued in every iteration (past the last tile it reads nothing), so that
+    // the wait for this tile does not take the next one's loads with it
+    nxt = load_tile<D, T>(qu, q0 + t2 * 16, t2 < ntile ? min(16, n - q0 - t2 * 16) : 0, lane);
     const uint64_t code = hash_tile<D, T>(qu, cur, r0, min(16, n - r0), sp, n_bits, P, exact_all, lane, stash[wave]);
     if (lane < 16 && r0 + lane < n) cu[r0 + lane] = code;
   }

@@ -468,7 +468,8 @@ __global__ __launch_bounds__(kKmThreads) void cluster_lds_kernel(FrontArgs f) {
       const int r0 = tile * 16;
       const TileRaw<D, T> cur = nxt;
       const int t2 = tile + kKmWaves;
-      if (t2 < nqt) nxt = load_tile<D, T>(qu, t2 * 16, min(16, n - t2 * 16), lane);
+      // issued in every iteration (past the last tile it reads nothing)
+      nxt = load_tile<D, T>(qu, t2 * 16, t2 < nqt ? min(16, n - t2 * 16) : 0, lane);
       const uint64_t code = hash_tile<D, T>(qu, cur, r0, min(16, n - r0), sp, n_bits, P, exact_all, lane, nullptr);
       if (lane < 16 && r0 + lane < n) {
         sh.codes[r0 + lane] = code;
