@@ -85,7 +85,22 @@ class Hip:
         self.lib.hipEventDestroy(ev)
 
 
-def stage_work(w, stage, variant_topk):
+COMPUTE_UNITS = 256  # MI355X; bench_forward reads the device's own count
+
+
+def fused_centroid_sums(w, compute_units=None):
+    """Whether the library forms the per-workgroup centroid sums inside the
+    one-launch K-means: sequences longer than 4096 (the several-workgroup
+    driver, 2048 queries per workgroup) whose grid covers every compute
+    unit.  The centroid stage then only adds the workgroups' parts."""
+    B, H, N, _ = w.q.shape
+    if N <= 4096:
+        return False
+    nwg = (N + 2047) // 2048
+    return B * H * nwg >= (compute_units or COMPUTE_UNITS)
+
+
+def stage_work(w, stage, variant_topk, compute_units=None):
     """Algorithmic work of one launch of a stage over the whole batch:
     returns (amount, unit, bound, peak) for the roofline entry.  Per
     (sequence, head) of valid length n, with C_eff = min(C, n):
@@ -93,6 +108,8 @@ def stage_work(w, stage, variant_topk):
       kmeans: L n C_eff Hamming distances, each a 64-entry int8 dot product
         on the matrix cores (2 * 64 operations);
       centroids: gather Q once, read the member list (n d s + 4 n bytes);
+        when the K-means kernel gathers Q itself (fused_centroid_sums), read
+        the workgroups' fp64 parts (C W d 8 bytes, W workgroups) instead;
       centroid attention (the tile kernel, or tile + merge): Q^c K^T and A^c V,
         2 C_eff n d flops each;
       output: clustered, write every row and read the assignment (n d s + 4 n);
@@ -124,7 +141,12 @@ def stage_work(w, stage, variant_topk):
             byts = nsum * D * s + nsum * 4
         return byts, "GB/s", "hbm", PEAKS["hbm_GBps"]
     if stage == "centroids":
-        byts = nsum * D * s + nsum * 4 + ceff * D * 4
+        if fused_centroid_sums(w, compute_units):
+            units = w.q.shape[0] * H
+            nwg = (w.q.shape[2] + 2047) // 2048
+            byts = units * w.C * nwg * D * 8 + ceff * D * 4 + units * w.C * 4
+        else:
+            byts = nsum * D * s + nsum * 4 + ceff * D * 4
         return byts, "GB/s", "hbm", PEAKS["hbm_GBps"]
     raise ValueError(stage)
 
@@ -494,6 +516,8 @@ def bench_long(args):
     import paper_2007_04825_amd as ca
 
     dev = torch.device("cuda:0")
+    global COMPUTE_UNITS
+    COMPUTE_UNITS = torch.cuda.get_device_properties(dev).multi_processor_count
     hip = Hip()
     stream = torch.cuda.current_stream(dev).cuda_stream
     w = gen.config_long()
@@ -679,6 +703,8 @@ def bench_forward(args, w, desc):
     dt = ca.CA_F32 if w.dtype == "f32" else ca.CA_BF16
     tdt = torch.float32 if w.dtype == "f32" else torch.bfloat16
     dev = torch.device("cuda:0")
+    global COMPUTE_UNITS
+    COMPUTE_UNITS = torch.cuda.get_device_properties(dev).multi_processor_count
     q, k, v = (torch.from_numpy(np.nan_to_num(x, nan=0.0)).to(dev).to(tdt) for x in (w.q, w.k, w.v))
     planes = torch.from_numpy(w.planes).to(dev)
     lengths = torch.from_numpy(w.lengths).to(dev)

@@ -76,3 +76,19 @@ def test_cpu_threads(monkeypatch):
     assert bench.cpu_threads() == 1
     monkeypatch.setenv("OMP_NUM_THREADS", "")
     assert bench.cpu_threads() >= 1
+
+
+def test_centroid_stage_priced_by_its_own_reads_when_fused():
+    """With the centroid sums formed inside the one-launch K-means (grids that
+    cover every compute unit), the centroid stage reads only the workgroups'
+    fp64 parts, and its algorithmic bytes say so."""
+    import gen
+    wl = gen.config_long()
+    ws = gen.make_config(3, N=32768, dtype="f32")
+    assert bench.fused_centroid_sums(wl, 256) and not bench.fused_centroid_sums(ws, 256)
+    B, H, N, D = wl.q.shape
+    nwg = (N + 2047) // 2048
+    want = B * H * wl.C * nwg * D * 8 + B * H * wl.C * D * 4 + B * H * wl.C * 4
+    assert bench.stage_work(wl, "centroids", wl.topk, 256)[0] == want
+    B, H, N, D = ws.q.shape
+    assert bench.stage_work(ws, "centroids", ws.topk, 256)[0] == B * H * N * (D * 4 + 4) + B * H * ws.C * D * 4
