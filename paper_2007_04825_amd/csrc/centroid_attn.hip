@@ -317,6 +317,8 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
   const T* ku = static_cast<const T*>(a.k) + (static_cast<size_t>(u) * a.N + k0) * D;
   const T* vu = static_cast<const T*>(a.v) + (static_cast<size_t>(u) * a.N + k0) * D;
   const int nkt = (kn + 15) / 16;
+  // batches of this wave that hold tiles of the chunk (0 when it has none)
+  const int nbw = (nkt - wave + NW * (BT / 2) - 1) / (NW * (BT / 2));
   // the chunk's keys and values as buffers: rows past kn read as 0
   constexpr uint32_t ESZ = sizeof(T);
   const __amdgpu_buffer_rsrc_t rk = make_rsrc(ku, static_cast<uint32_t>(kn) * D * ESZ);
@@ -352,10 +354,12 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
   // batch alone.
   constexpr int HB = BT / 2;
   static_assert(HB % 2 == 0, "tile pairs");
-  // batches of a wave over a whole chunk: the loops below run this many,
-  // unrolled into straight-line code, tiles past the chunk computing nothing
+  // batches of a wave over a whole chunk; the loops below run as straight-line
+  // code over the number of batches that hold the wave's tiles (nbw, one
+  // instance per count), tiles past the chunk in the last batch computing
+  // nothing
   constexpr int NB = kChunk / 16 / NW / HB;
-  static_assert(NB % 2 == 0 && NB * HB * NW * 16 == kChunk, "batch pairs cover the chunk");
+  static_assert(NB * HB * NW * 16 == kChunk, "batches cover the chunk");
   float ka0[HB][KS], ka1[HB][KS];
   auto load_keys = [&](int kt0, float (&ka)[HB][KS]) {
     const uint32_t voff = ((kt0 * 16 + c) * D + g * KS) * ESZ;
@@ -430,14 +434,17 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
       }
     };
     // the first batch is in flight already
+    with_count<NB>(nbw, [&](auto nbc) {
+      constexpr int NBX = decltype(nbc)::value;
 #pragma unroll
-    for (int bb = 0; bb < NB; bb += 2) {
-      const int kt0 = wave + bb * NW * HB, kt1 = kt0 + NW * HB;
-      load_keys(kt1, ka1);
-      key_batch(kt0, ka0);
-      if (bb + 2 < NB) load_keys(kt1 + NW * HB, ka0);
-      key_batch(kt1, ka1);
-    }
+      for (int bb = 0; bb < NBX; bb += 2) {
+        const int kt0 = wave + bb * NW * HB, kt1 = kt0 + NW * HB;
+        if (bb + 1 < NBX) load_keys(kt1, ka1);
+        key_batch(kt0, ka0);
+        if (bb + 2 < NBX) load_keys(kt1 + NW * HB, ka0);
+        if (bb + 1 < NBX) key_batch(kt1, ka1);
+      }
+    });
     // slice (wave, g) of row c
     smax[c][wave * 4 + g] = lmax;
     if constexpr (IMPROVED) {
@@ -646,15 +653,18 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
         }
       }
     };
-    load_vals(wave, va0);
+    with_count<NB>(nbw, [&](auto nbc) {
+      constexpr int NBX = decltype(nbc)::value;
+      load_vals(wave, va0);
 #pragma unroll
-    for (int bb = 0; bb < NB; bb += 2) {
-      const int kt0 = wave + bb * NW * HB, kt1 = kt0 + NW * HB;
-      load_vals(kt1, va1);
-      value_batch(kt0, va0);
-      if (bb + 2 < NB) load_vals(kt1 + NW * HB, va0);
-      value_batch(kt1, va1);
-    }
+      for (int bb = 0; bb < NBX; bb += 2) {
+        const int kt0 = wave + bb * NW * HB, kt1 = kt0 + NW * HB;
+        if (bb + 1 < NBX) load_vals(kt1, va1);
+        value_batch(kt0, va0);
+        if (bb + 2 < NBX) load_vals(kt1 + NW * HB, va0);
+        if (bb + 1 < NBX) value_batch(kt1, va1);
+      }
+    });
   }
   psum = cross_rows_sum(psum);
   if (g == 0) zpart[wave][c] = psum;

@@ -18,6 +18,24 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Compile-time count for with_count.
+template <int M> struct Count {
+  static constexpr int value = M;
+};
+
+// Calls f(Count<min(n, M)>{}) when n > 0: code that is straight-line over a
+// count known at compile time (so that every load in it is unconditional and
+// each wait counts exactly the loads still in flight) is instantiated for
+// every count from 1 to M and entered for the one that n asks for.
+template <int M, class F> __device__ __forceinline__ void with_count(int n, F&& f) {
+  if constexpr (M > 0) {
+    if (n >= M)
+      f(Count<M>{});
+    else
+      with_count<M - 1>(n, f);
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Element types.  bf16 is carried as raw uint16_t storage.
 // ---------------------------------------------------------------------------

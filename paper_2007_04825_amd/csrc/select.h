@@ -337,22 +337,31 @@ __device__ int group_select(const float* row, int m, int kk, uint32_t tau, uint1
   const int L = grp_block_len<GL>(m);
   const int base = c * L;
   const float tf = key_threshold(tau);
-  // an odd block length puts the group's reads in distinct banks; a block of
-  // 32 (a full row of 32 GL entries) would put them all in one, so there each
-  // lane starts its sweep at offset c of its block and wraps around
-  const int rot = (L & 1) ? 0 : c % L;
   uint32_t hits = 0u;  // bit i: position base + i reaches tau
-  for (int i0 = 0; i0 < L; i0 += 8) {
-    float x[8];
-    int at[8];
+  if (L == 32) {
+    // a block of 32 (a full row of 32 GL entries) would put the group's reads
+    // in one bank: each lane starts its sweep at offset c of its block and
+    // wraps around, collecting the bits in that rotated order
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int i = i0 + e + rot;
-      at[e] = i >= L ? i - L : i;
-      x[e] = i0 + e < L ? row[base + at[e]] : -INFINITY;
+    for (int i0 = 0; i0 < 32; i0 += 8) {
+      float x[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[e] = row[base + ((i0 + e + c) & 31)];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) hits |= x[e] >= tf ? (1u << (i0 + e)) : 0u;
     }
+    hits = __builtin_rotateleft32(hits, static_cast<uint32_t>(c));
+  } else {
+    // an odd block length puts the group's reads in distinct banks
+    for (int i0 = 0; i0 < L; i0 += 8) {
+      float x[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) hits |= x[e] >= tf ? (1u << at[e]) : 0u;
+      for (int e = 0; e < 8; ++e) x[e] = i0 + e < L ? row[base + i0 + e] : -INFINITY;
+      uint32_t h8 = 0u;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) h8 |= x[e] >= tf ? (1u << e) : 0u;
+      hits |= h8 << i0;
+    }
   }
   const int mine = __popc(hits);
   const int cnt = grp_sum_i<GL>(mine);
