@@ -271,7 +271,7 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
   __shared__ float smax[16][NS + 1];
   __shared__ __align__(16) float stop[IMPROVED ? 16 : 1][NS + 1][NT];
   __shared__ uint16_t tpos16[IMPROVED ? 16 : 1][kCandCap];     // top-k candidates, then T
-  __shared__ int moff[17];
+  __shared__ int moff[17];  // the tile's member offsets (fused modes) or sizes
   __shared__ int any_nonempty;
 
   // tile fastest, then chunk, then (batch, head): the tiles that read the same
@@ -381,6 +381,7 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
     if (tid == 0) any_nonempty = 0;
     __syncthreads();
     if (tid < 16 && j0 + tid < C && pre > 0) any_nonempty = 1;
+    if (tid < 16) moff[tid] = pre;  // the sizes, for the row phase
     __syncthreads();
     if (!any_nonempty) return;
   }
@@ -472,7 +473,7 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
     if constexpr (IMPROVED) {
       const int kk = min(a.topk, kn);
       const size_t uj = static_cast<size_t>(u) * C + (j < C ? j : 0);
-      const int jsize = OTOP ? (j < n ? 1 : 0) : j >= C ? 0 : FUSED ? moff[r + 1] - moff[r] : a.sizes[uj];
+      const int jsize = OTOP ? (j < n ? 1 : 0) : j >= C ? 0 : FUSED ? moff[r + 1] - moff[r] : moff[r];
       uint16_t* cand = tpos16[r];
       int cnt;
       if (FUSED && !OTOP && a.topk_in != nullptr) {
