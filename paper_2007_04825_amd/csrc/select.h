@@ -229,6 +229,22 @@ template <int GL> __device__ __forceinline__ float grp_max(float x) {
   if constexpr (GL == 32) x = fmaxf(x, lane_xor16(x));
   return x;
 }
+template <int GL> __device__ __forceinline__ uint32_t grp_min_u(uint32_t x) {
+  x = min(x, static_cast<uint32_t>(dpp_i<0xB1>(static_cast<int>(x))));
+  x = min(x, static_cast<uint32_t>(dpp_i<0x4E>(static_cast<int>(x))));
+  x = min(x, static_cast<uint32_t>(dpp_i<0x141>(static_cast<int>(x))));
+  x = min(x, static_cast<uint32_t>(dpp_i<0x140>(static_cast<int>(x))));
+  if constexpr (GL == 32) x = min(x, lane_xor16_u(x));
+  return x;
+}
+template <int GL> __device__ __forceinline__ int grp_max_i(int x) {
+  x = max(x, dpp_i<0xB1>(x));
+  x = max(x, dpp_i<0x4E>(x));
+  x = max(x, dpp_i<0x141>(x));
+  x = max(x, dpp_i<0x140>(x));
+  if constexpr (GL == 32) x = max(x, lane_xor16(x));
+  return x;
+}
 template <int GL> __device__ __forceinline__ uint32_t grp_and(uint32_t x) {
   x = row16_and(x);
   if constexpr (GL == 32) x &= lane_xor16_u(x);
@@ -383,6 +399,44 @@ __device__ int group_select(const float* row, int m, int kk, uint32_t tau, uint1
   }
 #pragma unroll
   for (int e = 0; e < PER; ++e) ck[e] = c + GL * e < cnt ? order_key(row[pos[e]]) : 0u;
+  // A few entries past the top kk (the usual case: the threshold misses only
+  // the entries of slices that hold more top entries than they keep) are
+  // dropped one at a time, each the last candidate in (key descending,
+  // position ascending) order: the smallest key, the last position among
+  // equal ones.  That leaves the same kk entries as the search below, in far
+  // fewer steps.
+  constexpr int kDropMax = 8;
+  const int extra = cnt - kk;  // the same in every lane of the group
+  if (__ballot(extra > kDropMax) == 0ull) {
+    bool live[PER];
+#pragma unroll
+    for (int e = 0; e < PER; ++e) live[e] = c + GL * e < cnt;
+    for (int it = 0; it < kDropMax; ++it) {
+      if (__ballot(it < extra) == 0ull) break;
+      uint32_t m = 0xffffffffu;
+#pragma unroll
+      for (int e = 0; e < PER; ++e) m = live[e] && ck[e] < m ? ck[e] : m;
+      m = grp_min_u<GL>(m);
+      int last = -1;
+#pragma unroll
+      for (int e = 0; e < PER; ++e) last = live[e] && ck[e] == m ? c + GL * e : last;
+      last = grp_max_i<GL>(last);
+      if (it < extra) {
+#pragma unroll
+        for (int e = 0; e < PER; ++e) live[e] = live[e] && c + GL * e != last;
+      }
+    }
+    wave_lds_sync();
+    int written = 0;
+#pragma unroll
+    for (int e = 0; e < PER; ++e) {
+      const uint32_t sf = grp_field<GL>(__ballot(live[e]));
+      if (live[e]) cand[written + __popc(sf & lt)] = static_cast<uint16_t>(pos[e]);
+      written += __popc(sf);
+    }
+    wave_lds_sync();
+    return written;
+  }
   const uint32_t kth = group_kth_key<PER, GL>(ck, kk);
   int gt = 0;
 #pragma unroll
