@@ -893,6 +893,9 @@ __global__ __launch_bounds__(kKmThreads) void kmeans_coop_kernel(CoopArgs a) {
   const int nct = (ce + 15) / 16;
   const int nqt = (nq + 15) / 16;
   const int tstride = a.tstride;
+  // counts of a unit below 65536 fit the 16-bit halves of a 32-bit table
+  // word: half the table's bytes for every workgroup to read each round
+  const bool narrow = n < 65536;
   const uint64_t* cu = a.codes + row0;
   for (int i = tid; i < nq; i += kKmThreads) {
     sh.codes[i] = cu[q0 + i];
@@ -925,12 +928,19 @@ __global__ __launch_bounds__(kKmThreads) void kmeans_coop_kernel(CoopArgs a) {
     // add the change of this workgroup's counts since its last addition to
     // table t % 2; keep the sizes for the member lists
     uint64_t* tab = a.tab + (static_cast<size_t>(u) * 2 + (t & 1)) * tstride;
+    uint32_t* tab32 = reinterpret_cast<uint32_t*>(tab);
     uint32_t* pub = sh.pub[t & 1];
     for (int x = tid; x < ce * kRowWords; x += kKmThreads) {
       const int j = x / kRowWords, w = x - kRowWords * j;
       const uint32_t cur = w < 32 ? sh.cnt[j * kCntStride + w] : static_cast<uint32_t>(sh.size[j]);
       const uint32_t old = pub[x];
-      if (cur != old) {
+      if (cur != old && narrow) {
+        // 32-bit words: the two 16-bit counts (or the size) change by the
+        // difference of the packed words, modulo 2^32; once every workgroup
+        // has added, the word holds the unit's counts, each below 65536
+        pub[x] = cur;
+        atomicAdd(&tab32[x], cur - old);
+      } else if (cur != old) {
         pub[x] = cur;
         const long long dlo = static_cast<long long>(w < 32 ? (cur & 0xffffu) : cur) -
                               static_cast<long long>(w < 32 ? (old & 0xffffu) : old);
@@ -986,16 +996,29 @@ __global__ __launch_bounds__(kKmThreads) void kmeans_coop_kernel(CoopArgs a) {
       asm volatile("" : "+v"(tidr));
       for (int x0 = 0; x0 < items; x0 += kTabBatch * kKmThreads) {
         uint64_t wv[kTabBatch];
-#pragma unroll
-        for (int e = 0; e < kTabBatch; ++e) {
-          const int x = x0 + tidr + e * kKmThreads;
-          wv[e] = x < items ? ld_agent(&tab[(x >> 5) * kRowWords + (x & 31)]) : 0ull;
-        }
-        // a size is a true count (at most n), so the low half of its word is it
         int32_t szl = 0;
-        if (lane < 2 * kTabBatch) {
-          const int xs = x0 + wave * 64 + (lane & 1) * 32 + (lane >> 1) * kKmThreads;
-          if (xs < items) szl = ld_agent(reinterpret_cast<const int32_t*>(&tab[(xs >> 5) * kRowWords + 32]));
+        if (narrow) {  // the 16-bit counts of bits 2w and 2w + 1 as the halves of a 64-bit value
+#pragma unroll
+          for (int e = 0; e < kTabBatch; ++e) {
+            const int x = x0 + tidr + e * kKmThreads;
+            const uint32_t v = x < items ? ld_agent(&tab32[(x >> 5) * kRowWords + (x & 31)]) : 0u;
+            wv[e] = (v & 0xffffu) | (static_cast<uint64_t>(v >> 16) << 32);
+          }
+          if (lane < 2 * kTabBatch) {
+            const int xs = x0 + wave * 64 + (lane & 1) * 32 + (lane >> 1) * kKmThreads;
+            if (xs < items) szl = ld_agent(reinterpret_cast<const int32_t*>(&tab32[(xs >> 5) * kRowWords + 32]));
+          }
+        } else {
+#pragma unroll
+          for (int e = 0; e < kTabBatch; ++e) {
+            const int x = x0 + tidr + e * kKmThreads;
+            wv[e] = x < items ? ld_agent(&tab[(x >> 5) * kRowWords + (x & 31)]) : 0ull;
+          }
+          // a size is a true count (at most n), so the low half of its word is it
+          if (lane < 2 * kTabBatch) {
+            const int xs = x0 + wave * 64 + (lane & 1) * 32 + (lane >> 1) * kKmThreads;
+            if (xs < items) szl = ld_agent(reinterpret_cast<const int32_t*>(&tab[(xs >> 5) * kRowWords + 32]));
+          }
         }
 #pragma unroll
         for (int e = 0; e < kTabBatch; ++e) {
