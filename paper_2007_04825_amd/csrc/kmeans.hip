@@ -857,7 +857,10 @@ struct CoopShared {
 // the member sort's per-wave counts use the operand table, dead by then
 static_assert(sizeof(v4i) * (kCmax / 16 * 64) >= sizeof(int32_t) * kKmWaves * kCmax, "member-sort scratch");
 
-template <int QW>
+// LF: the grid may hold units of exactly 65536 queries, whose narrow table
+// leaves the first query out (a separate instance, so that shorter
+// sequences run code without that path).
+template <int QW, bool LF>
 __global__ __launch_bounds__(kKmThreads) void kmeans_coop_kernel(CoopArgs a) {
   __shared__ CoopShared<QW> sh;
   const int u = blockIdx.y, b = blockIdx.x, nwg = a.nwg;
@@ -893,9 +896,13 @@ __global__ __launch_bounds__(kKmThreads) void kmeans_coop_kernel(CoopArgs a) {
   const int nct = (ce + 15) / 16;
   const int nqt = (nq + 15) / 16;
   const int tstride = a.tstride;
-  // counts of a unit below 65536 fit the 16-bit halves of a 32-bit table
-  // word: half the table's bytes for every workgroup to read each round
-  const bool narrow = n < 65536;
+  // narrow table: 32-bit words of two 16-bit counts, half the bytes for
+  // every workgroup to read each round.  For exactly 65536 queries the
+  // unit's first query (held by workgroup 0) is left out of it, so that no
+  // count exceeds 65535; workgroup 0 then publishes that query's cluster
+  // after the table, and every reader adds the query back.
+  const bool narrow = n < 65536 || (LF && n == 65536);
+  const bool leave_first = LF && n == 65536;
   const uint64_t* cu = a.codes + row0;
   for (int i = tid; i < nq; i += kKmThreads) {
     sh.codes[i] = cu[q0 + i];
@@ -932,7 +939,8 @@ __global__ __launch_bounds__(kKmThreads) void kmeans_coop_kernel(CoopArgs a) {
     uint32_t* pub = sh.pub[t & 1];
     for (int x = tid; x < ce * kRowWords; x += kKmThreads) {
       const int j = x / kRowWords, w = x - kRowWords * j;
-      const uint32_t cur = w < 32 ? sh.cnt[j * kCntStride + w] : static_cast<uint32_t>(sh.size[j]);
+      uint32_t cur = w < 32 ? sh.cnt[j * kCntStride + w] : static_cast<uint32_t>(sh.size[j]);
+      if (leave_first && b == 0 && j == sh.assign[0]) cur -= w < 32 ? pair_val(sh.codes[0], w) : 1u;
       const uint32_t old = pub[x];
       if (cur != old && narrow) {
         // 32-bit words: the two 16-bit counts (or the size) change by the
@@ -951,6 +959,7 @@ __global__ __launch_bounds__(kKmThreads) void kmeans_coop_kernel(CoopArgs a) {
       }
     }
     for (int j = tid; j < ce; j += kKmThreads) st_agent(&lsz[j], sh.size[j]);
+    if (leave_first && b == 0 && tid == 0) st_agent(reinterpret_cast<int32_t*>(&tab32[ce * kRowWords]), sh.assign[0]);
     // arrive once every wave's additions have been performed, then wait until
     // every workgroup of the unit has arrived
     wait_memory();
@@ -997,7 +1006,7 @@ __global__ __launch_bounds__(kKmThreads) void kmeans_coop_kernel(CoopArgs a) {
       for (int x0 = 0; x0 < items; x0 += kTabBatch * kKmThreads) {
         uint64_t wv[kTabBatch];
         int32_t szl = 0;
-        if (narrow) {  // the 16-bit counts of bits 2w and 2w + 1 as the halves of a 64-bit value
+        if (narrow && !leave_first) {  // the 16-bit counts of bits 2w and 2w + 1 as the halves of a 64-bit value
 #pragma unroll
           for (int e = 0; e < kTabBatch; ++e) {
             const int x = x0 + tidr + e * kKmThreads;
@@ -1007,6 +1016,26 @@ __global__ __launch_bounds__(kKmThreads) void kmeans_coop_kernel(CoopArgs a) {
           if (lane < 2 * kTabBatch) {
             const int xs = x0 + wave * 64 + (lane & 1) * 32 + (lane >> 1) * kKmThreads;
             if (xs < items) szl = ld_agent(reinterpret_cast<const int32_t*>(&tab32[(xs >> 5) * kRowWords + 32]));
+          }
+        } else if (narrow) {  // the same, the first query added back to its cluster jf
+          const int jf = ld_agent(reinterpret_cast<const int32_t*>(&tab32[ce * kRowWords]));
+          const uint64_t cf = a.codes[row0];
+          uint32_t v[kTabBatch];
+#pragma unroll
+          for (int e = 0; e < kTabBatch; ++e) {
+            const int x = x0 + tidr + e * kKmThreads;
+            v[e] = x < items ? ld_agent(&tab32[(x >> 5) * kRowWords + (x & 31)]) : 0u;
+          }
+          if (lane < 2 * kTabBatch) {
+            const int xs = x0 + wave * 64 + (lane & 1) * 32 + (lane >> 1) * kKmThreads;
+            if (xs < items) szl = ld_agent(reinterpret_cast<const int32_t*>(&tab32[(xs >> 5) * kRowWords + 32])) +
+                                  ((xs >> 5) == jf ? 1 : 0);
+          }
+#pragma unroll
+          for (int e = 0; e < kTabBatch; ++e) {
+            const int x = x0 + tidr + e * kKmThreads;
+            const uint32_t f = (x >> 5) == jf ? pair_val(cf, x & 31) : 0u;
+            wv[e] = ((v[e] & 0xffffu) + (f & 0xffffu)) | (static_cast<uint64_t>((v[e] >> 16) + (f >> 16)) << 32);
           }
         } else {
 #pragma unroll
@@ -1388,15 +1417,15 @@ void set_kmeans_path(int path) { g_kmeans_path = path; }
 // Workgroups of the cooperative K-means (QW queries each) that the current
 // device holds at once (its occupancy times the compute units), measured once
 // per device.
-template <int QW>
-static int coop_capacity() {
+template <int QW, bool LF>
+static int coop_capacity_of() {
   constexpr int kMaxDev = 64;
   static int cap[kMaxDev] = {0};
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDev) return 0;
   if (cap[dev] == 0) {
     int per_cu = 0, cus = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kmeans_coop_kernel<QW>, kKmThreads, 0) != hipSuccess ||
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kmeans_coop_kernel<QW, LF>, kKmThreads, 0) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
       (void)hipGetLastError();
       return 0;
@@ -1404,6 +1433,11 @@ static int coop_capacity() {
     cap[dev] = per_cu * cus > 0 ? per_cu * cus : -1;
   }
   return cap[dev] > 0 ? cap[dev] : 0;
+}
+// Workgroups that both instances of a query-block size can hold at once.
+template <int QW>
+static int coop_capacity() {
+  return min(coop_capacity_of<QW, false>(), coop_capacity_of<QW, true>());
 }
 
 int coop_fused_sums(const Problem& p, int coop_q) {
@@ -1544,16 +1578,21 @@ hipError_t launch_kmeans_coop(const Problem& p, const Workspace& ws, hipStream_t
   a.qc_part = ws.qc_part;
   void* args[] = {&a};
   const dim3 grid(a.nwg, p.units());
+  const bool lf = p.n >= 65536;  // some unit may hold exactly 65536 queries
+  const void* fn = nullptr;
   switch (ws.coop_q) {
     case 1024:
-      return hipLaunchKernel(reinterpret_cast<const void*>(kmeans_coop_kernel<1024>), grid,
-                             dim3(kKmThreads), args, 0, s);
+      fn = lf ? reinterpret_cast<const void*>(kmeans_coop_kernel<1024, true>)
+              : reinterpret_cast<const void*>(kmeans_coop_kernel<1024, false>);
+      break;
     case 2048:
-      return hipLaunchKernel(reinterpret_cast<const void*>(kmeans_coop_kernel<2048>), grid,
-                             dim3(kKmThreads), args, 0, s);
+      fn = lf ? reinterpret_cast<const void*>(kmeans_coop_kernel<2048, true>)
+              : reinterpret_cast<const void*>(kmeans_coop_kernel<2048, false>);
+      break;
     default:
       return hipErrorInvalidValue;
   }
+  return hipLaunchKernel(fn, grid, dim3(kKmThreads), args, 0, s);
 }
 
 hipError_t launch_kmeans(const Problem& p, const Workspace& ws, hipStream_t s) {

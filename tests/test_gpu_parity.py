@@ -224,6 +224,34 @@ def test_many_clusters_every_driver(N, dtype, topk, variant):
         assert np.array_equal(r["assign"], results[0]["assign"])
 
 
+def test_coop_kmeans_unit_of_65536_queries():
+    """Units of exactly 65536 queries, where one cluster may hold every query
+    and a bit count reach 65536: the one-launch K-means' table of 16-bit
+    counts leaves the unit's first query out and adds it back on reading.
+    Head 0 holds mixture queries, head 1 one row repeated 65536 times (one
+    cluster of every query, each set bit counted 65536 times).  Codes,
+    assignments, sizes and centroids against the oracle on both one-launch
+    forms and the per-round kernels."""
+    import paper_2007_04825_amd as ca
+    w = gen.config_tiny(B=1, H=2, N=65536, d=32, C=16, L=4, topk=32)
+    q = w.q.copy()
+    q[0, 1] = q[0, 1, :1]
+    w.q = q
+    ref = run_oracle(w, 0, key="unit65536")
+    assert ref["sizes"][0, 1, 0] == 65536
+    try:
+        for path in (2, 4, 5):
+            ca.set_kmeans_path(path)
+            got = run_gpu(w, 0)
+            print("driver %d" % path)
+            assert np.array_equal(got["codes"], ref["codes"])
+            assert np.array_equal(got["assign"], ref["assign"]), "driver %d" % path
+            assert np.array_equal(got["sizes"], ref["sizes"]), "driver %d" % path
+            np.testing.assert_allclose(got["centroids"], ref["qc"], rtol=0, atol=2e-6)
+    finally:
+        ca.set_kmeans_path(0)
+
+
 @pytest.mark.parametrize("variant", ["clustered", "iclustered"])
 def test_full_width_codes_every_driver(variant):
     """64-bit hash codes (every bit of the word a plane) on every K-means
