@@ -730,13 +730,16 @@ __global__ __launch_bounds__(kTileThreads) void attn_tile_kernel(AttnArgs a) {
 // in LDS (log-sum-exp), which gives V^c_j and the softmax statistics; then
 // every member row receives V^c_j (Eq. 6).
 //
-// PARTIAL: the same pass over one chunk of kFlashChunk keys per workgroup
+// PARTIAL: the same pass over one chunk of a.pchunk keys per workgroup
 // (several chunks of a long sequence), writing the chunk's (m, z,
 // unnormalised values) for attn_merge_kernel instead of the member rows.
 // ---------------------------------------------------------------------------
 constexpr int kFlashWaves = 8;
 constexpr int kFlashThreads = 64 * kFlashWaves;
-constexpr int kFlashChunk = 2048;  // keys per workgroup of the partial pass
+// keys per workgroup of the partial pass: kFlashChunk, or twice that when
+// the grid still fills most of the chip (flash_chunk)
+constexpr int kFlashChunk = 2048;
+static_assert(kFlashChunk % kChunk == 0, "partial states at the stride of kChunk chunks");
 
 template <int D, typename T, bool PARTIAL>
 __global__ __launch_bounds__(kFlashThreads) void attn_flash_kernel(AttnArgs a) {
@@ -755,9 +758,9 @@ __global__ __launch_bounds__(kFlashThreads) void attn_flash_kernel(AttnArgs a) {
   if (wi >= nfc * a.ntile * a.units) return;
   const int tile = wi % a.ntile, chunk = (wi / a.ntile) % nfc, u = wi / (nfc * a.ntile);
   const int nu = unit_length(a.lengths, u / a.heads, a.N);
-  const int k0 = PARTIAL ? chunk * kFlashChunk : 0;
+  const int k0 = PARTIAL ? chunk * a.pchunk : 0;
   if (PARTIAL && k0 >= nu) return;  // a chunk past the sequence: the merge does not read it
-  const int n = PARTIAL ? min(kFlashChunk, nu - k0) : nu;  // keys of this workgroup
+  const int n = PARTIAL ? min(a.pchunk, nu - k0) : nu;  // keys of this workgroup
   const int C = a.C;
   const int j0 = tile * 16;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -1440,8 +1443,32 @@ static int sparse_tiles(int topk) { return topk <= 16 ? 1 : topk <= 32 ? 2 : top
 
 // part 0: the tile kernel (single chunk: the whole stage); part 1: the merge
 // of several chunks (nothing for a single chunk).  The clustered variant
-// takes every chunk in the single-pass kernel, kFlashChunk keys per
+// takes every chunk in the single-pass kernel, flash_chunk keys per
 // workgroup.
+// Keys per workgroup of the clustered partial pass over several chunks:
+// 2 kFlashChunk when that grid still covers 80 % of two workgroups per
+// compute unit (fewer, longer workgroups: the length-sweep point's clustered
+// stage 100.7 -> 96.7 us in fp32, 60.1 -> 57.0 us in bf16), else
+// kFlashChunk (a grid of a quarter of the chip at 2 kFlashChunk ran 50 %
+// slower).  A multiple of kChunk, so the partial states keep their stride.
+static int flash_chunk(const Problem& p, int ntile) {
+  constexpr int kMaxDev = 64;
+  static int cus[kMaxDev] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDev) return kFlashChunk;
+  if (cus[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
+      (void)hipGetLastError();
+      return kFlashChunk;
+    }
+    cus[dev] = n > 0 ? n : -1;
+  }
+  constexpr int big = 2 * kFlashChunk;
+  const long long wgs = static_cast<long long>((p.n + big - 1) / big) * ntile * p.units();
+  return cus[dev] > 0 && 5 * wgs >= 8LL * cus[dev] ? big : kFlashChunk;
+}
+
 template <int D, typename T>
 static hipError_t launch_attn_t(const Problem& p, const Workspace& ws, const int32_t* topk_in,
                                 int part, hipStream_t s) {
@@ -1458,8 +1485,8 @@ static hipError_t launch_attn_t(const Problem& p, const Workspace& ws, const int
     return hipGetLastError();
   }
   if (!improved) {
-    a.pchunk = kFlashChunk;  // the states keep the stride ws.nchunk
-    a.npc = (p.n + kFlashChunk - 1) / kFlashChunk;
+    a.pchunk = flash_chunk(p, a.ntile);  // the states keep the stride ws.nchunk
+    a.npc = (p.n + a.pchunk - 1) / a.pchunk;
     if (part == 0) {
       const dim3 g1(xcd_grid(static_cast<long long>(a.npc) * a.ntile * a.units));
       hipLaunchKernelGGL((attn_flash_kernel<D, T, true>), g1, dim3(kFlashThreads), 0, s, a);
