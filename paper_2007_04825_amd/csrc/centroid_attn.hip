@@ -81,22 +81,26 @@ __global__ __launch_bounds__(256) void centroid_kernel(const T* __restrict__ q,
 
 // Eq. (3) after the cooperative K-means, in two steps.  Step 1 (unless the
 // K-means kernel formed these sums itself): for every (unit, block of coop_q
-// queries, cluster) D lanes add the block's members of the cluster
-// (consecutive in the member list, ascending query order) in fp64, 32 rows in
-// flight.  Step 2: the blocks' sums are added in block order and divided by
-// the cluster size.  The
-// association is fixed, so the result is deterministic.
-template <int D, typename T>
+// queries, cluster) D / VL lanes add the block's members of the cluster
+// (consecutive in the member list, ascending query order) in fp64, VL
+// dimensions per lane: with VL = 4 a wave takes 256 / D such items at once,
+// 16 rows in flight (for grids of many items); with VL = 1, 64 / D items,
+// 32 rows in flight.  Step 2: the blocks' sums are added in block order and
+// divided by the cluster size.  The association is fixed, so the result is
+// deterministic.
+template <int D, typename T, int VL>
 __global__ __launch_bounds__(256) void centroid_part_kernel(const T* __restrict__ q,
                                                             const int32_t* __restrict__ members,
                                                             const int32_t* __restrict__ bases,
                                                             const int32_t* __restrict__ lsizes,
                                                             int N, int C, int nwg, long long nitems,
                                                             double* __restrict__ qc_part) {
-  constexpr int GPW = 64 / D;  // items per wave
+  static_assert(VL == 1 || VL == 4, "dimensions per lane");
+  constexpr int LPI = D / VL;     // lanes per item
+  constexpr int GPW = 64 / LPI;   // items per wave
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const long long item = (static_cast<long long>(blockIdx.x) * 4 + wave) * GPW + lane / D;
-  const int t = lane % D;
+  const long long item = (static_cast<long long>(blockIdx.x) * 4 + wave) * GPW + lane / LPI;
+  const int t0 = VL * (lane % LPI);
   if (item >= nitems) return;  // item = (u nwg + b) C + j, the layout of bases and lsizes
   const int j = static_cast<int>(item % C);
   const long long ub = item / C;
@@ -104,21 +108,33 @@ __global__ __launch_bounds__(256) void centroid_part_kernel(const T* __restrict_
   const int u = static_cast<int>(ub / nwg);
   const int cnt = lsizes[item];
   const int32_t* mem = members + static_cast<size_t>(u) * N + bases[item];
-  const T* qu = q + static_cast<size_t>(u) * N * D;
-  double acc = 0.0;
-  constexpr int RB = 32;
+  const T* qu = q + static_cast<size_t>(u) * N * D + t0;
+  double acc[VL];
+#pragma unroll
+  for (int v = 0; v < VL; ++v) acc[v] = 0.0;
+  constexpr int RB = VL == 4 ? 16 : 32;
   for (int m = 0; m < cnt; m += RB) {
     int mi[RB];
 #pragma unroll
     for (int e = 0; e < RB; ++e) mi[e] = mem[min(m + e, cnt - 1)];
-    float x[RB];
+    float x[RB][VL];
 #pragma unroll
-    for (int e = 0; e < RB; ++e) x[e] = to_f32(qu[static_cast<size_t>(mi[e]) * D + t]);
+    for (int e = 0; e < RB; ++e) {
+      if constexpr (VL == 4)
+        load4(qu + static_cast<size_t>(mi[e]) * D, x[e]);
+      else
+        x[e][0] = to_f32(qu[static_cast<size_t>(mi[e]) * D]);
+    }
 #pragma unroll
     for (int e = 0; e < RB; ++e)
-      if (m + e < cnt) acc += static_cast<double>(x[e]);
+      if (m + e < cnt) {
+#pragma unroll
+        for (int v = 0; v < VL; ++v) acc[v] += static_cast<double>(x[e][v]);
+      }
   }
-  qc_part[((static_cast<size_t>(u) * C + j) * nwg + b) * D + t] = acc;
+  double* dst = qc_part + ((static_cast<size_t>(u) * C + j) * nwg + b) * D + t0;
+#pragma unroll
+  for (int v = 0; v < VL; ++v) dst[v] = acc[v];
 }
 
 template <int D>
@@ -1371,15 +1387,42 @@ static hipError_t launch_centroids_t(const Problem& p, const Workspace& ws, hipS
   return hipGetLastError();
 }
 
+// Compute units of the current device (cached per device; 0 if unknown).
+static int device_cus() {
+  constexpr int kMaxDev = 64;
+  static int cus[kMaxDev] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDev) return 0;
+  if (cus[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
+      (void)hipGetLastError();
+      return 0;
+    }
+    cus[dev] = n > 0 ? n : -1;
+  }
+  return cus[dev] > 0 ? cus[dev] : 0;
+}
+
 template <int D, typename T>
 static hipError_t launch_coop_centroids_t(const Problem& p, const Workspace& ws, hipStream_t s) {
-  constexpr int per_block = 4 * (64 / D);  // items per workgroup
+  constexpr int per_block = 4 * (64 / D);  // items per workgroup of the final sums (and of VL = 1)
+  constexpr int per_block4 = 4 * (256 / D);  // items per workgroup of the block sums with VL = 4
   const int nwg = (p.n + ws.coop_q - 1) / ws.coop_q;
   if (!ws.coop_sums) {
     const long long n1 = static_cast<long long>(p.units()) * nwg * p.C;
-    hipLaunchKernelGGL((centroid_part_kernel<D, T>), dim3(static_cast<unsigned>((n1 + per_block - 1) / per_block)),
-                       dim3(256), 0, s, static_cast<const T*>(p.q), ws.members, ws.cbases, ws.clsizes,
-                       p.n, p.C, nwg, n1, ws.qc_part);
+    // four dimensions per lane once that still leaves eight waves per compute
+    // unit (sweep point 23.7 -> 22.1 us in fp32, 23.9 -> 19.5 us in bf16; at
+    // N = 8192 its 800 waves took 15.1 us against 12.6 us with one)
+    const int cus = device_cus();
+    if (cus > 0 && n1 / (per_block4 / 4) >= 8LL * cus)
+      hipLaunchKernelGGL((centroid_part_kernel<D, T, 4>), dim3(static_cast<unsigned>((n1 + per_block4 - 1) / per_block4)),
+                         dim3(256), 0, s, static_cast<const T*>(p.q), ws.members, ws.cbases, ws.clsizes,
+                         p.n, p.C, nwg, n1, ws.qc_part);
+    else
+      hipLaunchKernelGGL((centroid_part_kernel<D, T, 1>), dim3(static_cast<unsigned>((n1 + per_block - 1) / per_block)),
+                         dim3(256), 0, s, static_cast<const T*>(p.q), ws.members, ws.cbases, ws.clsizes,
+                         p.n, p.C, nwg, n1, ws.qc_part);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -1452,21 +1495,10 @@ static int sparse_tiles(int topk) { return topk <= 16 ? 1 : topk <= 32 ? 2 : top
 // kFlashChunk (a grid of a quarter of the chip at 2 kFlashChunk ran 50 %
 // slower).  A multiple of kChunk, so the partial states keep their stride.
 static int flash_chunk(const Problem& p, int ntile) {
-  constexpr int kMaxDev = 64;
-  static int cus[kMaxDev] = {0};
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDev) return kFlashChunk;
-  if (cus[dev] == 0) {
-    int n = 0;
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
-      (void)hipGetLastError();
-      return kFlashChunk;
-    }
-    cus[dev] = n > 0 ? n : -1;
-  }
+  const int cus = device_cus();
   constexpr int big = 2 * kFlashChunk;
   const long long wgs = static_cast<long long>((p.n + big - 1) / big) * ntile * p.units();
-  return cus[dev] > 0 && 5 * wgs >= 8LL * cus[dev] ? big : kFlashChunk;
+  return cus > 0 && 5 * wgs >= 8LL * cus ? big : kFlashChunk;
 }
 
 template <int D, typename T>

@@ -347,6 +347,22 @@ inline unsigned xcd_grid(long long nwork) {
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, static_cast<int>(bytes), 0x00020000);
 }
+// Four consecutive elements (fp32 or bf16, 16- or 8-byte aligned) as fp32.
+__device__ __forceinline__ void load4(const float* p, float* d) {
+  const float4 v = *reinterpret_cast<const float4*>(p);
+  d[0] = v.x;
+  d[1] = v.y;
+  d[2] = v.z;
+  d[3] = v.w;
+}
+__device__ __forceinline__ void load4(const bf16_t* p, float* d) {
+  const uint2 v = *reinterpret_cast<const uint2*>(p);
+  d[0] = __uint_as_float(v.x << 16);
+  d[1] = __uint_as_float(v.x & 0xffff0000u);
+  d[2] = __uint_as_float(v.y << 16);
+  d[3] = __uint_as_float(v.y & 0xffff0000u);
+}
+
 // CNT consecutive elements (fp32 or bf16) at byte offset voff + soff, as fp32.
 template <int CNT>
 __device__ __forceinline__ void buf_load(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff, float* d, float) {
