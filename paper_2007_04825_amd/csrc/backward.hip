@@ -166,7 +166,24 @@ __global__ __launch_bounds__(64) void bwd_sparse_kernel(BwdArgs a) {
   const int lane = threadIdx.x, c = lane & 15, g = lane >> 4;
   const int C = a.C;
   const size_t uj = static_cast<size_t>(u) * C + j;
+  // everything that depends on the cluster alone is requested at once: its
+  // size, offset and mass, its T entries with their partial-row slots (the
+  // slots of entries past T are read and ignored) and V^b_j
   const int sz = a.sizes[uj];
+  const int off = a.offsets[static_cast<size_t>(u) * (C + 1) + j];
+  const float mh = a.mass[uj];
+  constexpr int TR = (KP + 63) / 64;
+  int keyv[TR], epv[TR];
+#pragma unroll
+  for (int r = 0; r < TR; ++r) {
+    const int x = 64 * r + lane;
+    const size_t at = uj * a.topk + min(x, a.topk - 1);
+    keyv[r] = x < a.topk ? a.tsets[at] : -1;
+    epv[r] = a.epos[at];
+  }
+  float vcbl[KS];
+#pragma unroll
+  for (int s2 = 0; s2 < KS; ++s2) vcbl[s2] = a.vcb[uj * D + g * KS + s2];
   if (sz == 0) {
     for (int x = lane; x < D; x += 64) a.G[uj * D + x] = 0.0f;
     if (lane == 0) {
@@ -175,18 +192,16 @@ __global__ __launch_bounds__(64) void bwd_sparse_kernel(BwdArgs a) {
     }
     return;
   }
-  const int off = a.offsets[static_cast<size_t>(u) * (C + 1) + j];
-  const float mh = a.mass[uj];
   // T: the leading non-negative entries
   int kk = 0;
-  for (int x0 = 0; x0 < KP; x0 += 64) {
-    const int x = x0 + lane;
-    const int key = x < a.topk ? a.tsets[uj * a.topk + x] : -1;
+#pragma unroll
+  for (int r = 0; r < TR; ++r) {
+    const int x = 64 * r + lane;
     if (x < KP) {
-      sh.tp[x] = key;
-      sh.ep[x] = key >= 0 ? a.epos[uj * a.topk + x] : 0;
+      sh.tp[x] = keyv[r];
+      sh.ep[x] = keyv[r] >= 0 ? epv[r] : 0;
     }
-    kk += __popcll(__ballot(key >= 0));
+    kk += __popcll(__ballot(keyv[r] >= 0));
   }
   const int nkt = (kk + 15) >> 4;
   const size_t base = static_cast<size_t>(u) * a.N * D;
@@ -215,6 +230,9 @@ __global__ __launch_bounds__(64) void bwd_sparse_kernel(BwdArgs a) {
     sh.accv[x / D][x % D] = 0.0f;
   }
   const int32_t* mem = a.members + static_cast<size_t>(u) * a.N + off;
+  // member index of row lane / 4 of the next member tile, requested one tile
+  // ahead (positions past the cluster read its last member and are ignored)
+  int qnext = mem[min(lane >> 2, sz - 1)];
   float gsum[KS];  // per lane: sum over its query column of g, dims g * KS ..
 #pragma unroll
   for (int s = 0; s < KS; ++s) gsum[s] = 0.0f;
@@ -222,13 +240,16 @@ __global__ __launch_bounds__(64) void bwd_sparse_kernel(BwdArgs a) {
   const uint32_t orow = static_cast<uint32_t>(D) * ESZ;
   for (int mt = 0; mt < sz; mt += 16) {
     // member rows of Q and of the output gradient into LDS
+    int qrow;  // member index of row lane / 4 of this tile, -1 past the cluster
     {
       const int r = lane >> 2, part = lane & 3;
-      const int qi = mt + r < sz ? mem[mt + r] : -1;
+      const int qi = mt + r < sz ? qnext : -1;
+      qrow = qi;
       const uint32_t vo = qi >= 0 ? static_cast<uint32_t>(qi) * orow + part * RL * ESZ : kNone;
       float qx[RL], gx[RL];
       buf_load<RL>(rq, vo, 0, qx, T{});
       buf_load<RL>(rg, vo, 0, gx, T{});
+      qnext = mem[min(mt + 16 + r, sz - 1)];
 #pragma unroll
       for (int e = 0; e < RL; ++e) {
         sh.q[r][part * RL + e] = qx[e];
@@ -315,7 +336,8 @@ __global__ __launch_bounds__(64) void bwd_sparse_kernel(BwdArgs a) {
       for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) o[i * DT + dt] = oq[dt][i] * a.scale;
-      const int qi = qvalid ? mem[mt + c] : -1;
+      const int qs = __shfl(qrow, 4 * c);  // row c's index, from lane 4 c (every lane active)
+      const int qi = qvalid ? qs : -1;
       if (qi >= 0) {
         float* dst = a.dq + base + static_cast<size_t>(qi) * D + DT * 4 * g;
 #pragma unroll
@@ -363,7 +385,7 @@ __global__ __launch_bounds__(64) void bwd_sparse_kernel(BwdArgs a) {
 #pragma unroll
   for (int s = 0; s < KS; ++s) {
     gsum[s] = row16_sum(gsum[s]);
-    gvb += gsum[s] * a.vcb[uj * D + g * KS + s];
+    gvb += gsum[s] * vcbl[s];
   }
   gvb = cross_rows_sum(gvb);
   const float dmj = wave_sum(dmacc);
@@ -449,38 +471,87 @@ __global__ __launch_bounds__(64 * kBwdWaves) void bwd_tile_kernel(BwdArgs a) {
   for (int i = 0; i < 4; ++i) buf_load<DT>(rk, ((wave * 16 + 4 * g + i) * D + DT * c) * ESZ, 0, kT[i], T{});
 
   const int ntile = (C + 15) / 16;
-  auto stage = [&](int jt) {
-    const int b = jt & 1, j0 = jt * 16;
-    for (int x = tid; x < 16 * D; x += 64 * kBwdWaves) {
-      const int cc = x / D, dim = x % D, j = j0 + cc;
-      const size_t uj = static_cast<size_t>(u) * C + (j < C ? j : 0);
-      const bool ok = j < C && a.sizes[uj] > 0;
-      sh.qc[b][cc][dim] = ok ? a.qc[uj * D + dim] : 0.0f;
-      sh.g[b][cc][dim] = ok ? a.G[uj * D + dim] : 0.0f;
+  // a centroid tile's rows of Q^c and G, and its statistics, go through
+  // registers: requested (stage_load) before the previous tile goes through
+  // the products, written to LDS buffer jt & 1 (stage_store) after it, so
+  // that their latency overlaps the products
+  constexpr int NTH = 64 * kBwdWaves;
+  constexpr int EPT = (16 * D + NTH - 1) / NTH;  // row elements per thread
+  struct Stage {
+    float qc[EPT], g[EPT];
+    int sz[EPT];
+    float st[4];
+    int szs;
+  };
+  auto stage_load = [&](int jt, Stage& r) {
+    const int j0 = jt * 16;
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      const int x = tid + e * NTH;
+      const int cc = min(x / D, 15), dim = x % D, j = min(j0 + cc, C - 1);
+      const size_t uj = static_cast<size_t>(u) * C + j;
+      r.sz[e] = a.sizes[uj];
+      r.qc[e] = a.qc[uj * D + dim];
+      r.g[e] = a.G[uj * D + dim];
     }
     if (tid < 16) {
-      const int j = j0 + tid;
-      const size_t uj = static_cast<size_t>(u) * C + (j < C ? j : 0);
-      const bool ok = j < C && a.sizes[uj] > 0;
-      sh.valid[b][tid] = ok;
-      sh.st[b][tid][0] = ok ? a.stats[uj * 2] : 0.0f;
-      sh.st[b][tid][1] = ok ? 1.0f / a.stats[uj * 2 + 1] : 0.0f;
-      sh.st[b][tid][2] = ok ? a.delta[uj] : 0.0f;
-      sh.st[b][tid][3] = (ok && IMPROVED) ? a.dm[uj] : 0.0f;
+      const size_t uj = static_cast<size_t>(u) * C + min(j0 + tid, C - 1);
+      r.szs = a.sizes[uj];
+      r.st[0] = a.stats[uj * 2];
+      r.st[1] = a.stats[uj * 2 + 1];
+      r.st[2] = a.delta[uj];
+      r.st[3] = IMPROVED ? a.dm[uj] : 0.0f;
     }
   };
+  auto stage_store = [&](int jt, const Stage& r) {
+    const int b = jt & 1, j0 = jt * 16;
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      const int x = tid + e * NTH;
+      if (EPT * NTH == 16 * D || x < 16 * D) {
+        const int cc = x / D, dim = x % D;
+        const bool ok = j0 + cc < C && r.sz[e] > 0;
+        sh.qc[b][cc][dim] = ok ? r.qc[e] : 0.0f;
+        sh.g[b][cc][dim] = ok ? r.g[e] : 0.0f;
+      }
+    }
+    if (tid < 16) {
+      const bool ok = j0 + tid < C && r.szs > 0;
+      sh.valid[b][tid] = ok;
+      sh.st[b][tid][0] = ok ? r.st[0] : 0.0f;
+      sh.st[b][tid][1] = ok ? 1.0f / r.st[1] : 0.0f;
+      sh.st[b][tid][2] = ok ? r.st[2] : 0.0f;
+      sh.st[b][tid][3] = (ok && IMPROVED) ? r.st[3] : 0.0f;
+    }
+  };
+  Stage pre;
+  stage_load(0, pre);
   if constexpr (IMPROVED) {
-    for (int x = tid; x < ntile * 16 * (kBwdKeys / 32); x += 64 * kBwdWaves) sh.tmask[x / (kBwdKeys / 32)][x % (kBwdKeys / 32)] = 0u;
+    for (int x = tid; x < ntile * 16 * (kBwdKeys / 32); x += NTH) sh.tmask[x / (kBwdKeys / 32)][x % (kBwdKeys / 32)] = 0u;
     __syncthreads();
-    // (the top-k lists of empty clusters are not defined)
-    for (int x = tid; x < C * a.topk; x += 64 * kBwdWaves) {
-      const int j = x / a.topk;
-      if (a.sizes[static_cast<size_t>(u) * C + j] == 0) continue;
-      const int key = a.tsets[static_cast<size_t>(u) * C * a.topk + x];
-      if (key >= k0 && key < k0 + kBwdKeys) atomicOr(&sh.tmask[j][(key - k0) >> 5], 1u << ((key - k0) & 31));
+    // (the top-k lists of empty clusters are not defined); eight entries per
+    // thread requested together with their cluster sizes
+    const int tot = C * a.topk;
+    const int32_t* ts = a.tsets + static_cast<size_t>(u) * C * a.topk;
+    const int32_t* szu = a.sizes + static_cast<size_t>(u) * C;
+    for (int x0 = 0; x0 < tot; x0 += 8 * NTH) {
+      int key[8], sz[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int x = min(x0 + tid + e * NTH, tot - 1);
+        key[e] = ts[x];
+        sz[e] = szu[x / a.topk];
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int x = x0 + tid + e * NTH;
+        const int j = x / a.topk;
+        if (x < tot && sz[e] > 0 && key[e] >= k0 && key[e] < k0 + kBwdKeys)
+          atomicOr(&sh.tmask[j][(key[e] - k0) >> 5], 1u << ((key[e] - k0) & 31));
+      }
     }
   }
-  stage(0);
+  stage_store(0, pre);
   __syncthreads();
 
   v4f dkacc[DT], dvacc[DT];
@@ -488,6 +559,7 @@ __global__ __launch_bounds__(64 * kBwdWaves) void bwd_tile_kernel(BwdArgs a) {
   for (int dt = 0; dt < DT; ++dt) dkacc[dt] = dvacc[dt] = v4f{0.f, 0.f, 0.f, 0.f};
   for (int jt = 0; jt < ntile; ++jt) {
     const int b = jt & 1, j0 = jt * 16;
+    if (jt + 1 < ntile) stage_load(jt + 1, pre);  // in flight during the products
     {
       float bq[KS], bg[KS];
 #pragma unroll
@@ -555,7 +627,7 @@ __global__ __launch_bounds__(64 * kBwdWaves) void bwd_tile_kernel(BwdArgs a) {
       for (int w = 0; w < kBwdWaves; ++w) sacc += sh.red[w][cc][dim];
       if (j0 + cc < C) a.dqc_part[((static_cast<size_t>(u) * a.nkb + kb) * C + j0 + cc) * D + dim] = sacc * a.scale;
     }
-    if (jt + 1 < ntile) stage(jt + 1);
+    if (jt + 1 < ntile) stage_store(jt + 1, pre);
     __syncthreads();
   }
   // dK and dV of the wave's keys (rows past the length get 0)
