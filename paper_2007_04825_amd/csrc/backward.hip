@@ -211,18 +211,27 @@ __global__ __launch_bounds__(64) void bwd_sparse_kernel(BwdArgs a) {
   const __amdgpu_buffer_rsrc_t rv = make_rsrc(static_cast<const T*>(a.v) + base, ubytes);
   const __amdgpu_buffer_rsrc_t rg = make_rsrc(static_cast<const T*>(a.dout) + base, ubytes);
   wave_lds_sync();
-  // T rows of K and V into LDS (rows past kk are zero); 4 lanes per row
+  // T rows of K and V into LDS (rows past kk are zero); 4 lanes per row, up
+  // to four 16-row groups requested before any is stored
   constexpr int RL = D / 4;  // values per lane
-  for (int r0 = 0; r0 < KP; r0 += 16) {
-    const int r = r0 + (lane >> 2), part = lane & 3;
-    const uint32_t vo = r < kk ? static_cast<uint32_t>(sh.tp[r]) * D * ESZ + part * RL * ESZ : kNone;
-    float kx[RL], vx[RL];
-    buf_load<RL>(rk, vo, 0, kx, T{});
-    buf_load<RL>(rv, vo, 0, vx, T{});
+  constexpr int RG = KP / 16 < 4 ? KP / 16 : 4;  // row groups in flight
+  for (int r0 = 0; r0 < KP; r0 += 16 * RG) {
+    float kx[RG][RL], vx[RG][RL];
 #pragma unroll
-    for (int e = 0; e < RL; ++e) {
-      sh.k[r][part * RL + e] = kx[e];
-      sh.v[r][part * RL + e] = vx[e];
+    for (int q = 0; q < RG; ++q) {
+      const int r = r0 + 16 * q + (lane >> 2), part = lane & 3;
+      const uint32_t vo = r < kk ? static_cast<uint32_t>(sh.tp[r]) * D * ESZ + part * RL * ESZ : kNone;
+      buf_load<RL>(rk, vo, 0, kx[q], T{});
+      buf_load<RL>(rv, vo, 0, vx[q], T{});
+    }
+#pragma unroll
+    for (int q = 0; q < RG; ++q) {
+      const int r = r0 + 16 * q + (lane >> 2), part = lane & 3;
+#pragma unroll
+      for (int e = 0; e < RL; ++e) {
+        sh.k[r][part * RL + e] = kx[q][e];
+        sh.v[r][part * RL + e] = vx[q][e];
+      }
     }
   }
   for (int x = lane; x < KP * D; x += 64) {
