@@ -656,39 +656,56 @@ __global__ __launch_bounds__(64 * kBwdWaves) void bwd_tile_kernel(BwdArgs a) {
 // dQ^c_j = (sum over the key blocks, in order, of the partials) / |S_j|.
 template <int D>
 __global__ __launch_bounds__(256) void bwd_dqc_reduce_kernel(BwdArgs a) {
+  constexpr int Q4 = D / 4;  // four consecutive dimensions per thread
   const size_t x = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x;
-  const size_t total = static_cast<size_t>(a.units) * a.C * D;
+  const size_t total = static_cast<size_t>(a.units) * a.C * Q4;
   if (x >= total) return;
-  const int dim = static_cast<int>(x % D);
-  const size_t uj = x / D;
+  const int d4 = static_cast<int>(x % Q4);
+  const size_t uj = x / Q4;
   const int u = static_cast<int>(uj / a.C), j = static_cast<int>(uj % a.C);
   const int sz = a.sizes[uj];
   const int n = unit_length(a.lengths, u / a.heads, a.N);
   const int nkbv = (n + kBwdKeys - 1) / kBwdKeys;
-  float s = 0.0f;
+  float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
   if (sz > 0)
-    for (int kb = 0; kb < nkbv; ++kb) s += a.dqc_part[((static_cast<size_t>(u) * a.nkb + kb) * a.C + j) * D + dim];
-  a.dqc[uj * D + dim] = sz > 0 ? s / static_cast<float>(sz) : 0.0f;
+    for (int kb = 0; kb < nkbv; ++kb) {
+      const float4 t =
+          reinterpret_cast<const float4*>(a.dqc_part)[((static_cast<size_t>(u) * a.nkb + kb) * a.C + j) * Q4 + d4];
+      s.x += t.x;
+      s.y += t.y;
+      s.z += t.z;
+      s.w += t.w;
+    }
+  const float fsz = static_cast<float>(sz);
+  reinterpret_cast<float4*>(a.dqc)[uj * Q4 + d4] =
+      sz > 0 ? make_float4(s.x / fsz, s.y / fsz, s.z / fsz, s.w / fsz) : make_float4(0.f, 0.f, 0.f, 0.f);
 }
 
 // dQ_i = dQ^c_{a_i} (+ the top-k part already in dq for the improved variant);
-// rows past the length get 0.
+// rows past the length get 0.  Four consecutive dimensions per thread.
 template <int D, bool IMPROVED>
 __global__ __launch_bounds__(256) void bwd_dq_kernel(BwdArgs a) {
-  const size_t x = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x;
-  const size_t total = static_cast<size_t>(a.units) * a.N * D;
+  constexpr int Q4 = D / 4;
+  const size_t x = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x;  // float4 index
+  const size_t total = static_cast<size_t>(a.units) * a.N * Q4;
   if (x >= total) return;
-  const int dim = static_cast<int>(x % D);
-  const size_t ui = x / D;
+  const int d4 = static_cast<int>(x % Q4);
+  const size_t ui = x / Q4;
   const int u = static_cast<int>(ui / a.N), i = static_cast<int>(ui % a.N);
   const int n = unit_length(a.lengths, u / a.heads, a.N);
+  float4* dq4 = reinterpret_cast<float4*>(a.dq) + x;
   if (i >= n) {
-    a.dq[x] = 0.0f;
+    *dq4 = make_float4(0.f, 0.f, 0.f, 0.f);
     return;
   }
   const int j = min(max(a.assign[ui], 0), a.C - 1);
-  const float cp = a.dqc[(static_cast<size_t>(u) * a.C + j) * D + dim];
-  a.dq[x] = IMPROVED ? a.dq[x] + cp : cp;
+  const float4 cp = reinterpret_cast<const float4*>(a.dqc)[(static_cast<size_t>(u) * a.C + j) * Q4 + d4];
+  if constexpr (IMPROVED) {
+    const float4 t = *dq4;
+    *dq4 = make_float4(t.x + cp.x, t.y + cp.y, t.z + cp.z, t.w + cp.w);
+  } else {
+    *dq4 = cp;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -903,12 +920,12 @@ static hipError_t launch_backward_t(const BwdProblem& p, hipStream_t s, hipEvent
     hipLaunchKernelGGL((bwd_tile_kernel<D, T, false>), gt, dim3(64 * kBwdWaves), 0, s, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (ev1 && (e = hipEventRecord(ev1, s)) != hipSuccess) return e;
-  hipLaunchKernelGGL((bwd_dqc_reduce_kernel<D>), blocks(U * p.C * D), dim3(256), 0, s, a);
+  hipLaunchKernelGGL((bwd_dqc_reduce_kernel<D>), blocks(U * p.C * (D / 4)), dim3(256), 0, s, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (improved)
-    hipLaunchKernelGGL((bwd_dq_kernel<D, true>), blocks(U * p.n * D), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((bwd_dq_kernel<D, true>), blocks(U * p.n * (D / 4)), dim3(256), 0, s, a);
   else
-    hipLaunchKernelGGL((bwd_dq_kernel<D, false>), blocks(U * p.n * D), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((bwd_dq_kernel<D, false>), blocks(U * p.n * (D / 4)), dim3(256), 0, s, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (improved) {
     hipLaunchKernelGGL((bwd_index_gather_kernel<D>), blocks(U * p.n * (D / 4)), dim3(256), 0, s, a);
