@@ -110,17 +110,19 @@ __global__ __launch_bounds__(256) void bwd_cluster_sums_kernel(BwdArgs a) {
   const int sz = ok ? a.sizes[uj] : 0;
   const int32_t* mem = a.members + static_cast<size_t>(u) * a.N + (ok ? a.offsets[static_cast<size_t>(u) * (C + 1) + j] : 0);
   const T* gu = static_cast<const T*>(a.dout) + static_cast<size_t>(u) * a.N * D;
+  const float vb = a.vcb[uj * D + t];
+  // members in batches of eight, every load issued (positions past the
+  // cluster read its last member again and are not added), added in order
   float acc = 0.0f;
-  int m = 0;
-  for (; m + 8 <= sz; m += 8) {
+  for (int m = 0; m < sz; m += 8) {
     float x[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) x[e] = to_f32(gu[static_cast<size_t>(mem[m + e]) * D + t]);
+    for (int e = 0; e < 8; ++e) x[e] = to_f32(gu[static_cast<size_t>(mem[min(m + e, sz - 1)]) * D + t]);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) acc += x[e];
+    for (int e = 0; e < 8; ++e)
+      if (m + e < sz) acc += x[e];
   }
-  for (; m < sz; ++m) acc += to_f32(gu[static_cast<size_t>(mem[m]) * D + t]);
-  const float del = dgroup_sum<D>(sz > 0 ? acc * a.vcb[uj * D + t] : 0.0f);
+  const float del = dgroup_sum<D>(sz > 0 ? acc * vb : 0.0f);
   if (ok) {
     a.G[uj * D + t] = acc;
     if (t == 0) a.delta[uj] = del;
