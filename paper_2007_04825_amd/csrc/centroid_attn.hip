@@ -75,7 +75,14 @@ __global__ __launch_bounds__(256) void centroid_kernel(const T* __restrict__ q,
 #pragma unroll
     for (int e = 0; e < RB; ++e) acc += static_cast<double>(x[e]);
   }
-  for (; m < sz; ++m) acc += static_cast<double>(to_f32(qu[static_cast<size_t>(mem[m]) * D + t]));
+  if (m < sz) {  // the rest, whose indices are in mi already: every row requested, then added in order
+    float x[RB];
+#pragma unroll
+    for (int e = 0; e < RB; ++e) x[e] = to_f32(qu[static_cast<size_t>(mi[e]) * D + t]);
+#pragma unroll
+    for (int e = 0; e < RB; ++e)
+      if (m + e < sz) acc += static_cast<double>(x[e]);
+  }
   dst[t] = static_cast<float>(acc / static_cast<double>(sz));
 }
 
