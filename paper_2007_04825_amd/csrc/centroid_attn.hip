@@ -1190,11 +1190,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kSparseMinW
   if (t >= C) {
     const int32_t* su = a.sizes + static_cast<size_t>(u) * C;
     const int want = t - C;
+    // every cluster size requested at once (the interface admits C <= 256:
+    // four per lane)
+    constexpr int SPL = 256 / 64;
+    int sv[SPL];
+#pragma unroll
+    for (int e = 0; e < SPL; ++e) sv[e] = su[min(64 * e + lane, C - 1)];
     int run = 0;
     j = -1;
-    for (int x0 = 0; x0 < C; x0 += 64) {
+#pragma unroll
+    for (int e = 0; e < SPL; ++e) {
+      const int x0 = 64 * e;
+      if (x0 >= C) break;
       const int x = x0 + lane;
-      const int s = x < C ? su[x] : 0;
+      const int s = x < C ? sv[e] : 0;
       const int extra = s > kSparseChunk ? (s - 1) / kSparseChunk : 0;
       const int incl = wave_incl_scan(extra);
       const uint64_t hit = __ballot(want >= run + incl - extra && want < run + incl);
